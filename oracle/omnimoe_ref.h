@@ -1,0 +1,93 @@
+/*
+ * Oracle for the OmniMoE atomic-expert layer forward pass: TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, host-only implementation in double precision, written from the
+ * paper (arXiv 2602.05711, "OmniMoE"). It exists to check the GPU library and is
+ * used only by the tests, the smoke check and the CPU-baseline leg of the
+ * benchmark. It shares no source with the GPU library.
+ *
+ * Inputs are float32 host arrays (bf16 inputs are passed as their exact float32
+ * widening). Layouts:
+ *   x          [T, d]
+ *   keys_row   [H, n_rows, d_key]      sub-keys scoring grid rows
+ *   keys_col   [H, n_cols, d_key]      sub-keys scoring grid columns
+ *   u, v       [N, d], N = n_rows * n_cols   down (w_in) and up (w_out) vectors
+ *   idx/gates  [T, H, K]               pair p = (t * H + h) * K + k
+ * Expert id of grid cell (i, j) is n = i * n_cols + j.
+ *
+ * Every function returns 0 on success and a negative value on bad arguments.
+ */
+#ifndef OMNIMOE_REF_H
+#define OMNIMOE_REF_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct {
+  int64_t T;
+  int32_t d;
+  int32_t n_rows;
+  int32_t n_cols;
+  int32_t d_key;
+  int32_t H;
+  int32_t K;
+  int32_t act;        /* 0: GELU (erf form), 1: SiLU */
+  int32_t query_mode; /* 0: split (rows read x[0:d_key], columns x[d_key:2 d_key]); 1: shared (both x[0:d_key]) */
+  int32_t group_size; /* B >= 1: active experts per execution group */
+} omnimoe_ref_desc;
+
+/* Row and column logits s_r = x W_r, s_c = x W_c per head (Eq. 9), fp64, summed
+ * over the key dimension in ascending order. sr [T, H, n_rows], sc [T, H, n_cols]. */
+int omnimoe_ref_half_scores(const omnimoe_ref_desc* desc, const float* x, const float* keys_row,
+                            const float* keys_col, double* sr, double* sc, int n_threads);
+
+/* Top-K over the implicit score grid S_ij = sr[i] + sc[j] (Eq. 11), order
+ * (S descending, n ascending), and softmax gates over the K selected scores
+ * (Eq. 2). method 0: brute force over all N cells (the definition, Eq. 1);
+ * method 1: per-half top-K then the Cartesian candidates (a+1)(b+1) <= K;
+ * method 2: brute force on the literal LogSoftmax log-probabilities of Eq. 10.
+ * sel_scores receives the selected S values (may be NULL). Returns the number of
+ * candidate sums that were not exact in double (see omnimoe_ref.cpp) in
+ * *inexact_sums when that pointer is not NULL. */
+int omnimoe_ref_select(const omnimoe_ref_desc* desc, const double* sr, const double* sc,
+                       int method, int32_t* idx, double* sel_scores, double* gates,
+                       int64_t* inexact_sums, int n_threads);
+
+/* Same selection starting from float32 half-scores laid out [T, H, n_rows + n_cols]
+ * (row logits first), as produced by the GPU scoring stage. */
+int omnimoe_ref_select_f32(const omnimoe_ref_desc* desc, const float* half_scores, int method,
+                           int32_t* idx, double* sel_scores, double* gates,
+                           int64_t* inexact_sums, int n_threads);
+
+/* Expert-Centric Scheduling (Eq. 12-13): pairs sorted by (group of the active
+ * expert, pair id). perm [M]; active [<= min(M, N)] ascending expert ids;
+ * active_offsets [n_active + 1] first sorted position of each active expert,
+ * last entry M; dense_offsets [N + 1] (may be NULL) first sorted position of
+ * expert e. M = T * H * K, N = n_rows * n_cols. */
+int omnimoe_ref_schedule(const omnimoe_ref_desc* desc, const int32_t* idx, int32_t* perm,
+                         int32_t* active, int32_t* active_offsets, int32_t* n_active,
+                         int32_t* dense_offsets);
+
+/* Routed output y[t] = sum over (h, k) of g * act(x_t . u_e) * v_e (Eq. 4, 7),
+ * fp64. scheduled = 0 walks tokens in order; scheduled = 1 walks the expert-major
+ * schedule to form a[p] = g_p * act(x_t . u_e) and then sums a[p] * v_e per
+ * token in slot order. The two give bit-identical y. gates are fp64 [T, H, K]. */
+int omnimoe_ref_expert_forward(const omnimoe_ref_desc* desc, const float* x, const float* u,
+                               const float* v, const int32_t* idx, const double* gates,
+                               int scheduled, double* y, int n_threads);
+
+/* Whole layer: half-scores, selection (method as above), schedule, scheduled
+ * forward. idx, gates may be NULL. */
+int omnimoe_ref_layer_forward(const omnimoe_ref_desc* desc, const float* x, const float* keys_row,
+                              const float* keys_col, const float* u, const float* v, int method,
+                              double* y, int32_t* idx, double* gates, int n_threads);
+
+/* The activation on one value: 0 GELU-erf, 1 SiLU. */
+double omnimoe_ref_act(int act, double z);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
