@@ -1,0 +1,189 @@
+/*
+ * omnimoe.h - C ABI of the MI355X (gfx950) atomic-expert layer library (libomnimoe.so).
+ *
+ * The library computes the routed branch of the OmniMoE layer forward pass
+ * (arXiv 2602.05711, "OmniMoE: An Efficient MoE by Orchestrating Atomic Experts at Scale"):
+ *
+ *   router    Cartesian Product Router, Sec. 2.2: row/column logits s_r = x W_r,
+ *             s_c = x W_c per head (Eq. 9); the implicit grid S_ij = s_r[i] + s_c[j]
+ *             (Eq. 11, with the LogSoftmax of Eq. 10 dropped: it shifts each half by a
+ *             constant and changes neither the selection nor the gates); the top-K cells
+ *             (Eq. 1) and softmax gates over their scores (Eq. 2).
+ *   schedule  Expert-Centric Scheduling, Sec. 2.3: the T*H*K (token, expert) tasks
+ *             (Eq. 12) sorted by (expert, task id), i.e. by (group, token) of Eq. 13 with
+ *             groups of one active expert.
+ *   experts   atomic experts E_e(x) = act(x . u_e) v_e (Eq. 4) with u = W[e], v = V[e]
+ *             (Eq. 5-6), combined as y_t = sum over the token's (head, k) slots of
+ *             g * act(x_t . u_e) * v_e (Eq. 7 without its shared MLP term; Eq. 14 per
+ *             expert).
+ *
+ * Conventions
+ *   - Tensor arguments are DEVICE pointers owned by the caller, row-major, contiguous.
+ *     The library allocates no device memory: callers pass a workspace of at least
+ *     omnimoe_workspace_size() bytes. The workspace and all outputs must not overlap
+ *     the inputs or each other.
+ *   - Every call is asynchronous on `stream` (a hipStream_t passed as void*; NULL is the
+ *     default stream). The return value covers argument checks and launch errors; a
+ *     fault inside a kernel surfaces at the caller's next synchronisation.
+ *   - Pointers must be 16-byte aligned. Inputs must be finite.
+ *   - Calls on different streams with different workspaces may run concurrently.
+ *   - Indices: pair (task) p = (t * H + h) * K + k; expert id of grid cell (i, j) is
+ *     n = i * n_cols + j; idx/gates are [T, H, K] with each (t, h) list ordered by
+ *     score descending, ties to the lower expert id.
+ */
+#ifndef OMNIMOE_H
+#define OMNIMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  OMNIMOE_OK = 0,
+  OMNIMOE_ERR_INVALID_ARG = 1, /* a size is out of range or a required pointer is NULL */
+  OMNIMOE_ERR_UNSUPPORTED = 2, /* valid layer, but outside what this build implements */
+  OMNIMOE_ERR_ALIGNMENT = 3,   /* a pointer is not 16-byte aligned */
+  OMNIMOE_ERR_WORKSPACE = 4,   /* workspace smaller than omnimoe_workspace_size() */
+  OMNIMOE_ERR_HIP = 5          /* the HIP runtime reported an error at launch */
+} omnimoe_status;
+
+typedef enum { OMNIMOE_F32 = 0, OMNIMOE_BF16 = 1 } omnimoe_dtype;
+typedef enum { OMNIMOE_ACT_GELU = 0, OMNIMOE_ACT_SILU = 1 } omnimoe_act;
+typedef enum { OMNIMOE_QUERY_SPLIT = 0, OMNIMOE_QUERY_SHARED = 1 } omnimoe_query_mode;
+
+/* Layer shape. All sizes in elements.
+ *   T           tokens; x is [T, d]. T = 0 is a valid no-op.
+ *   d           hidden size; 8 <= d <= 8192, d % 8 == 0.
+ *   n_rows      N_r, rows of the expert grid; 1 <= n_rows <= 4096.
+ *   n_cols      N_c, columns; 1 <= n_cols <= 4096. N = n_rows * n_cols experts.
+ *   d_key       sub-key dimension; d_key % 8 == 0. SPLIT: rows score x[:, 0:d_key] and
+ *               columns x[:, d_key:2 d_key] (2 d_key <= d). SHARED: both score
+ *               x[:, 0:d_key] (d_key <= d).
+ *   H           heads, each with its own sub-key tables, top-K and softmax; H >= 1.
+ *   K           experts per (token, head); 1 <= K <= 64 and K <= N.
+ *   dtype       storage type of x, sub-keys, u and v (OMNIMOE_F32 or OMNIMOE_BF16);
+ *               arithmetic is fp32 in every case.
+ *   act         activation of Eq. 4: GELU (erf form) or SiLU.
+ *   query_mode  OMNIMOE_QUERY_SPLIT or OMNIMOE_QUERY_SHARED.
+ *   group_size  B of Sec. 2.3 (active experts per execution group); this build
+ *               implements B = 1 and returns OMNIMOE_ERR_UNSUPPORTED otherwise.
+ * T * H * K and T * H * (n_rows + n_cols) must each be below 2^31. */
+typedef struct {
+  int64_t T;
+  int32_t d;
+  int32_t n_rows;
+  int32_t n_cols;
+  int32_t d_key;
+  int32_t H;
+  int32_t K;
+  int32_t dtype;
+  int32_t act;
+  int32_t query_mode;
+  int32_t group_size;
+} omnimoe_layer_desc;
+
+/* Stages, for workspace sizing and timing. */
+typedef enum {
+  OMNIMOE_STAGE_ROUTE = 0,
+  OMNIMOE_STAGE_SELECT = 1,
+  OMNIMOE_STAGE_SCHEDULE = 2,
+  OMNIMOE_STAGE_EXPERT = 3,
+  OMNIMOE_STAGE_LAYER = 4
+} omnimoe_stage;
+
+/* Bytes of workspace the given stage's entry point needs for this shape. */
+omnimoe_status omnimoe_workspace_size(const omnimoe_layer_desc* desc, int32_t stage,
+                                      size_t* bytes);
+
+/* Router (Sec. 2.2; Eq. 9, 11, 1, 2).
+ *   x            [T, d]                  dtype
+ *   keys_row     [H, n_rows, d_key]      dtype   sub-keys of the grid rows (W_r^T per head)
+ *   keys_col     [H, n_cols, d_key]      dtype   sub-keys of the grid columns
+ *   idx          [T, H, K]  int32  out   selected expert ids, best first
+ *   gates        [T, H, K]  fp32   out   softmax of the selected scores
+ *   half_scores  [T, H, n_rows + n_cols] fp32 out, may be NULL: the row logits then the
+ *                column logits of every (token, head), as computed on the way.
+ * Logits accumulate in fp32 (MFMA for bf16). Selection compares those fp32 logits
+ * exactly; a cell's score is their sum in double, which is exact. */
+omnimoe_status omnimoe_route(const omnimoe_layer_desc* desc, const void* x, const void* keys_row,
+                             const void* keys_col, int32_t* idx, float* gates, float* half_scores,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/* Selection only: top-K over the implicit grid and gates, from given fp32 logits
+ *   half_scores [T, H, n_rows + n_cols] (as written by omnimoe_route). */
+omnimoe_status omnimoe_select(const omnimoe_layer_desc* desc, const float* half_scores,
+                              int32_t* idx, float* gates, void* workspace,
+                              size_t workspace_bytes, void* stream);
+
+/* Expert-Centric Scheduling (Sec. 2.3; Eq. 12-13).
+ *   idx             [T, H, K] int32   expert ids in [0, N) (as from omnimoe_route)
+ *   perm            [M] int32 out     task ids sorted by (expert, task id), M = T*H*K
+ *   active          [min(M, N)] int32 out   distinct expert ids, ascending (first n_active used)
+ *   active_offsets  [min(M, N) + 1] int32 out  active_offsets[a] = first position in perm of
+ *                   expert active[a]; active_offsets[n_active] = M
+ *   n_active        [1] int32 out (device)
+ *   dense_offsets   [N + 1] int32 out, may be NULL: first position of every expert id
+ *                   (the exclusive prefix sum of the per-expert task counts)
+ * The result is unique, so it is the same on every run. */
+omnimoe_status omnimoe_schedule(const omnimoe_layer_desc* desc, const int32_t* idx,
+                                int32_t* perm, int32_t* active, int32_t* active_offsets,
+                                int32_t* n_active, int32_t* dense_offsets, void* workspace,
+                                size_t workspace_bytes, void* stream);
+
+/* Expert compute (Eq. 4, 7, 14) on a schedule.
+ *   x      [T, d] dtype;  u, v  [N, d] dtype (down / up vectors of every expert)
+ *   idx    [T, H, K] int32;  gates  [T, H, K] fp32;  perm  [M] int32 (from omnimoe_schedule)
+ *   y      [T, d] fp32 out
+ * Walks perm expert by expert: each expert's u row is read once per run of its tasks and
+ * a[p] = g_p * act(x_t . u_e) is formed for each of them; then every token sums
+ * a[p] * v_e over its slots in (head, k) order. No atomics: y is the same on every run. */
+omnimoe_status omnimoe_expert_forward(const omnimoe_layer_desc* desc, const void* x,
+                                      const void* u, const void* v, const int32_t* idx,
+                                      const float* gates, const int32_t* perm, float* y,
+                                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* The whole routed layer: route, schedule and expert compute on one stream, no host
+ * synchronisation. y [T, d] fp32 out; idx_out and gates_out ([T, H, K]) may be NULL. */
+omnimoe_status omnimoe_layer_forward(const omnimoe_layer_desc* desc, const void* x,
+                                     const void* keys_row, const void* keys_col, const void* u,
+                                     const void* v, float* y, int32_t* idx_out, float* gates_out,
+                                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* Per-kernel timing of omnimoe_layer_forward with HIP events on the call's stream.
+ * A timer holds host-side state and HIP events only (no device memory). Kernel groups: */
+typedef enum {
+  OMNIMOE_KERNEL_SCORE = 0,      /* logit GEMM */
+  OMNIMOE_KERNEL_SELECT = 1,     /* per-half top-K, Cartesian merge, gates */
+  OMNIMOE_KERNEL_SCHEDULE = 2,   /* sort and segment kernels */
+  OMNIMOE_KERNEL_EXPERT_DOT = 3, /* expert-major a = g * act(x . u) */
+  OMNIMOE_KERNEL_ACCUMULATE = 4, /* token-major y = sum a * v */
+  OMNIMOE_KERNEL_COUNT = 5
+} omnimoe_kernel;
+
+typedef struct omnimoe_timer omnimoe_timer;
+
+/* capacity: how many timed calls may be recorded before omnimoe_timer_read. */
+omnimoe_status omnimoe_timer_create(int32_t capacity, omnimoe_timer** timer);
+omnimoe_status omnimoe_timer_destroy(omnimoe_timer* timer);
+/* Waits for the recorded events, writes the summed milliseconds per kernel group
+ * (ms[OMNIMOE_KERNEL_COUNT]) and the number of calls, and clears the timer. */
+omnimoe_status omnimoe_timer_read(omnimoe_timer* timer, float* ms, int32_t* n_calls);
+/* omnimoe_layer_forward with an event recorded around each kernel group. Returns
+ * OMNIMOE_ERR_INVALID_ARG when the timer is full. */
+omnimoe_status omnimoe_layer_forward_timed(const omnimoe_layer_desc* desc, const void* x,
+                                           const void* keys_row, const void* keys_col,
+                                           const void* u, const void* v, float* y,
+                                           int32_t* idx_out, float* gates_out, void* workspace,
+                                           size_t workspace_bytes, void* stream,
+                                           omnimoe_timer* timer);
+
+/* A static, human-readable name of a status code. */
+const char* omnimoe_status_string(int32_t status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* OMNIMOE_H */

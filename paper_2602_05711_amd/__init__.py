@@ -1,0 +1,10 @@
+"""MI355X (gfx950) implementation of the OmniMoE atomic-expert layer forward pass.
+
+The computation lives in libomnimoe.so (HIP kernels behind the C ABI of include/omnimoe.h);
+``binding`` exposes the same entry points to Python for torch tensors.
+"""
+from .binding import (  # noqa: F401
+    EXPORTED, KERNEL_NAMES, OmnimoeError, OmnimoeLayerDesc, Timer, load_library, make_desc,
+    omnimoe_expert_forward, omnimoe_layer_forward, omnimoe_route, omnimoe_schedule,
+    omnimoe_select, omnimoe_workspace_size, workspace,
+)

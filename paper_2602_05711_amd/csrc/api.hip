@@ -1,0 +1,325 @@
+// Host side of the C ABI declared in include/omnimoe.h: argument checks, workspace carving and
+// kernel launches on the caller's stream. No device memory is allocated here and there is no
+// host synchronisation inside a call.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <new>
+#include <vector>
+
+#include "../../include/omnimoe.h"
+#include "internal.hpp"
+
+using omnimoe::Shape;
+
+namespace {
+
+constexpr int64_t kIntMax = 2147483647LL;
+
+size_t align_up(size_t v) { return (v + 255) & ~(size_t)255; }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+omnimoe_status check_desc(const omnimoe_layer_desc* d, Shape* s) {
+  if (!d) return OMNIMOE_ERR_INVALID_ARG;
+  if (d->T < 0 || d->T > (1LL << 23)) return OMNIMOE_ERR_INVALID_ARG;
+  if (d->d < 8 || d->d > 8192 || d->d % 8) return OMNIMOE_ERR_INVALID_ARG;
+  if (d->n_rows < 1 || d->n_rows > 4096 || d->n_cols < 1 || d->n_cols > 4096)
+    return OMNIMOE_ERR_INVALID_ARG;
+  if (d->d_key < 8 || d->d_key % 8) return OMNIMOE_ERR_INVALID_ARG;
+  if (d->query_mode == OMNIMOE_QUERY_SPLIT) {
+    if (2LL * d->d_key > d->d) return OMNIMOE_ERR_INVALID_ARG;
+  } else if (d->query_mode == OMNIMOE_QUERY_SHARED) {
+    if (d->d_key > d->d) return OMNIMOE_ERR_INVALID_ARG;
+  } else {
+    return OMNIMOE_ERR_INVALID_ARG;
+  }
+  if (d->H < 1 || d->K < 1) return OMNIMOE_ERR_INVALID_ARG;
+  const int64_t N = (int64_t)d->n_rows * d->n_cols;
+  if (d->K > N) return OMNIMOE_ERR_INVALID_ARG;
+  if (d->K > 64) return OMNIMOE_ERR_UNSUPPORTED;
+  if (d->dtype != OMNIMOE_F32 && d->dtype != OMNIMOE_BF16) return OMNIMOE_ERR_INVALID_ARG;
+  if (d->act != OMNIMOE_ACT_GELU && d->act != OMNIMOE_ACT_SILU) return OMNIMOE_ERR_INVALID_ARG;
+  if (d->group_size < 1) return OMNIMOE_ERR_INVALID_ARG;
+  if (d->group_size != 1) return OMNIMOE_ERR_UNSUPPORTED;
+  const int64_t rows = d->T * d->H;
+  if (rows * d->K >= kIntMax || rows * (d->n_rows + d->n_cols) >= kIntMax)
+    return OMNIMOE_ERR_INVALID_ARG;
+  s->T = d->T;
+  s->d = d->d;
+  s->nr = d->n_rows;
+  s->nc = d->n_cols;
+  s->dk = d->d_key;
+  s->H = d->H;
+  s->K = d->K;
+  s->bf16 = d->dtype == OMNIMOE_BF16;
+  s->act = d->act;
+  s->col0 = d->query_mode == OMNIMOE_QUERY_SPLIT ? d->d_key : 0;
+  s->N = N;
+  s->rows = rows;
+  s->M = rows * d->K;
+  s->hk = d->H * d->K;
+  return OMNIMOE_OK;
+}
+
+omnimoe_status check_ptrs(std::initializer_list<const void*> ps) {
+  for (const void* p : ps) {
+    if (!p) return OMNIMOE_ERR_INVALID_ARG;
+    if (!aligned16(p)) return OMNIMOE_ERR_ALIGNMENT;
+  }
+  return OMNIMOE_OK;
+}
+
+omnimoe_status check_opt(const void* p) {
+  return (p && !aligned16(p)) ? OMNIMOE_ERR_ALIGNMENT : OMNIMOE_OK;
+}
+
+omnimoe_status hip_status(hipError_t e) { return e == hipSuccess ? OMNIMOE_OK : OMNIMOE_ERR_HIP; }
+
+size_t hs_bytes(const Shape& s) { return align_up((size_t)s.rows * (s.nr + s.nc) * 4); }
+size_t m_bytes(const Shape& s) { return align_up((size_t)s.M * 4); }
+size_t active_bytes(const Shape& s) { return align_up((size_t)(std::min(s.M, s.N) + 1) * 4); }
+
+size_t stage_bytes(const Shape& s, int stage) {
+  switch (stage) {
+    case OMNIMOE_STAGE_ROUTE: return hs_bytes(s);
+    case OMNIMOE_STAGE_SELECT: return 0;
+    case OMNIMOE_STAGE_SCHEDULE: return omnimoe::schedule_ws_bytes(s.M, s.N);
+    case OMNIMOE_STAGE_EXPERT: return m_bytes(s);
+    default: {
+      // idx, gates, perm, active, active_offsets, n_active, then the logits (dead after
+      // selection) overlapped with the sort buffers and the a[] buffer.
+      size_t fixed = 3 * m_bytes(s) + 2 * active_bytes(s) + 256;
+      size_t late = omnimoe::schedule_ws_bytes(s.M, s.N) + m_bytes(s);
+      return fixed + std::max(hs_bytes(s), late);
+    }
+  }
+}
+
+}  // namespace
+
+struct omnimoe_timer {
+  int capacity = 0;
+  int used = 0;
+  std::vector<hipEvent_t> ev;  // capacity * (OMNIMOE_KERNEL_COUNT + 1)
+};
+
+namespace {
+
+constexpr int kEv = OMNIMOE_KERNEL_COUNT + 1;
+
+omnimoe_status layer_impl(const omnimoe_layer_desc* desc, const void* x, const void* keys_row,
+                          const void* keys_col, const void* u, const void* v, float* y,
+                          int32_t* idx_out, float* gates_out, void* ws, size_t ws_bytes,
+                          void* stream, omnimoe_timer* timer) {
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  if (s.T == 0) return OMNIMOE_OK;
+  if ((st = check_ptrs({x, keys_row, keys_col, u, v, y, ws}))) return st;
+  if ((st = check_opt(idx_out)) || (st = check_opt(gates_out))) return st;
+  if (ws_bytes < stage_bytes(s, OMNIMOE_STAGE_LAYER)) return OMNIMOE_ERR_WORKSPACE;
+  if (timer && timer->used >= timer->capacity) return OMNIMOE_ERR_INVALID_ARG;
+  hipStream_t strm = (hipStream_t)stream;
+  char* w = (char*)ws;
+  int32_t* idx = (int32_t*)w; w += m_bytes(s);
+  float* gates = (float*)w; w += m_bytes(s);
+  int32_t* perm = (int32_t*)w; w += m_bytes(s);
+  int32_t* active = (int32_t*)w; w += active_bytes(s);
+  int32_t* offsets = (int32_t*)w; w += active_bytes(s);
+  int32_t* n_active = (int32_t*)w; w += 256;
+  char* late = w;
+  float* hs = (float*)late;
+  void* sched_ws = late;
+  float* abuf = (float*)(late + omnimoe::schedule_ws_bytes(s.M, s.N));
+  if (idx_out) idx = idx_out;
+  if (gates_out) gates = gates_out;
+
+  hipEvent_t* ev = timer ? &timer->ev[(size_t)timer->used * kEv] : nullptr;
+  auto mark = [&](int k) {
+    if (ev) (void)hipEventRecord(ev[k], strm);
+  };
+  hipError_t e;
+  mark(0);
+  if ((e = omnimoe::launch_score(s, x, keys_row, keys_col, hs, strm))) return hip_status(e);
+  mark(1);
+  if ((e = omnimoe::launch_select(s, hs, idx, gates, strm))) return hip_status(e);
+  mark(2);
+  const int32_t* sk = nullptr;
+  if ((e = omnimoe::launch_schedule(s, idx, perm, active, offsets, n_active, nullptr, sched_ws,
+                                    &sk, strm)))
+    return hip_status(e);
+  mark(3);
+  if ((e = omnimoe::launch_expert_dot(s, x, u, idx, gates, perm, sk, abuf, strm)))
+    return hip_status(e);
+  mark(4);
+  if ((e = omnimoe::launch_accumulate(s, v, idx, abuf, y, strm))) return hip_status(e);
+  mark(5);
+  if (timer) ++timer->used;
+  return OMNIMOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* omnimoe_status_string(int32_t status) {
+  switch (status) {
+    case OMNIMOE_OK: return "ok";
+    case OMNIMOE_ERR_INVALID_ARG: return "invalid argument";
+    case OMNIMOE_ERR_UNSUPPORTED: return "unsupported by this build";
+    case OMNIMOE_ERR_ALIGNMENT: return "pointer not 16-byte aligned";
+    case OMNIMOE_ERR_WORKSPACE: return "workspace too small";
+    case OMNIMOE_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+omnimoe_status omnimoe_workspace_size(const omnimoe_layer_desc* desc, int32_t stage,
+                                      size_t* bytes) {
+  if (!bytes) return OMNIMOE_ERR_INVALID_ARG;
+  if (stage < OMNIMOE_STAGE_ROUTE || stage > OMNIMOE_STAGE_LAYER) return OMNIMOE_ERR_INVALID_ARG;
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  *bytes = stage_bytes(s, stage);
+  return OMNIMOE_OK;
+}
+
+omnimoe_status omnimoe_route(const omnimoe_layer_desc* desc, const void* x, const void* keys_row,
+                             const void* keys_col, int32_t* idx, float* gates, float* half_scores,
+                             void* ws, size_t ws_bytes, void* stream) {
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  if (s.T == 0) return OMNIMOE_OK;
+  if ((st = check_ptrs({x, keys_row, keys_col, idx, gates}))) return st;
+  if ((st = check_opt(half_scores))) return st;
+  float* hs = half_scores;
+  if (!hs) {
+    if ((st = check_ptrs({ws}))) return st;
+    if (ws_bytes < stage_bytes(s, OMNIMOE_STAGE_ROUTE)) return OMNIMOE_ERR_WORKSPACE;
+    hs = (float*)ws;
+  }
+  hipStream_t strm = (hipStream_t)stream;
+  hipError_t e = omnimoe::launch_score(s, x, keys_row, keys_col, hs, strm);
+  if (e == hipSuccess) e = omnimoe::launch_select(s, hs, idx, gates, strm);
+  return hip_status(e);
+}
+
+omnimoe_status omnimoe_select(const omnimoe_layer_desc* desc, const float* half_scores,
+                              int32_t* idx, float* gates, void* ws, size_t ws_bytes,
+                              void* stream) {
+  (void)ws;
+  (void)ws_bytes;
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  if (s.T == 0) return OMNIMOE_OK;
+  if ((st = check_ptrs({half_scores, idx, gates}))) return st;
+  return hip_status(omnimoe::launch_select(s, half_scores, idx, gates, (hipStream_t)stream));
+}
+
+omnimoe_status omnimoe_schedule(const omnimoe_layer_desc* desc, const int32_t* idx,
+                                int32_t* perm, int32_t* active, int32_t* active_offsets,
+                                int32_t* n_active, int32_t* dense_offsets, void* ws,
+                                size_t ws_bytes, void* stream) {
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  if ((st = check_ptrs({active_offsets, n_active}))) return st;
+  if ((st = check_opt(dense_offsets))) return st;
+  hipStream_t strm = (hipStream_t)stream;
+  if (s.T == 0) {
+    // No tasks: an empty schedule.
+    hipError_t e = omnimoe::launch_fill_i32(n_active, 1, 0, strm);
+    if (e == hipSuccess) e = omnimoe::launch_fill_i32(active_offsets, 1, 0, strm);
+    if (e == hipSuccess && dense_offsets)
+      e = omnimoe::launch_fill_i32(dense_offsets, s.N + 1, 0, strm);
+    return hip_status(e);
+  }
+  if ((st = check_ptrs({idx, perm, active, ws}))) return st;
+  if (ws_bytes < stage_bytes(s, OMNIMOE_STAGE_SCHEDULE)) return OMNIMOE_ERR_WORKSPACE;
+  const int32_t* sk = nullptr;
+  return hip_status(omnimoe::launch_schedule(s, idx, perm, active, active_offsets, n_active,
+                                             dense_offsets, ws, &sk, strm));
+}
+
+omnimoe_status omnimoe_expert_forward(const omnimoe_layer_desc* desc, const void* x,
+                                      const void* u, const void* v, const int32_t* idx,
+                                      const float* gates, const int32_t* perm, float* y,
+                                      void* ws, size_t ws_bytes, void* stream) {
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  if (s.T == 0) return OMNIMOE_OK;
+  if ((st = check_ptrs({x, u, v, idx, gates, perm, y, ws}))) return st;
+  if (ws_bytes < stage_bytes(s, OMNIMOE_STAGE_EXPERT)) return OMNIMOE_ERR_WORKSPACE;
+  hipStream_t strm = (hipStream_t)stream;
+  float* abuf = (float*)ws;
+  hipError_t e = omnimoe::launch_expert_dot(s, x, u, idx, gates, perm, nullptr, abuf, strm);
+  if (e == hipSuccess) e = omnimoe::launch_accumulate(s, v, idx, abuf, y, strm);
+  return hip_status(e);
+}
+
+omnimoe_status omnimoe_layer_forward(const omnimoe_layer_desc* desc, const void* x,
+                                     const void* keys_row, const void* keys_col, const void* u,
+                                     const void* v, float* y, int32_t* idx_out, float* gates_out,
+                                     void* ws, size_t ws_bytes, void* stream) {
+  return layer_impl(desc, x, keys_row, keys_col, u, v, y, idx_out, gates_out, ws, ws_bytes,
+                    stream, nullptr);
+}
+
+omnimoe_status omnimoe_layer_forward_timed(const omnimoe_layer_desc* desc, const void* x,
+                                           const void* keys_row, const void* keys_col,
+                                           const void* u, const void* v, float* y,
+                                           int32_t* idx_out, float* gates_out, void* ws,
+                                           size_t ws_bytes, void* stream, omnimoe_timer* timer) {
+  if (!timer) return OMNIMOE_ERR_INVALID_ARG;
+  return layer_impl(desc, x, keys_row, keys_col, u, v, y, idx_out, gates_out, ws, ws_bytes,
+                    stream, timer);
+}
+
+omnimoe_status omnimoe_timer_create(int32_t capacity, omnimoe_timer** out) {
+  if (!out || capacity < 1 || capacity > 100000) return OMNIMOE_ERR_INVALID_ARG;
+  omnimoe_timer* t = new (std::nothrow) omnimoe_timer();
+  if (!t) return OMNIMOE_ERR_INVALID_ARG;
+  t->capacity = capacity;
+  t->ev.resize((size_t)capacity * kEv, nullptr);
+  for (auto& e : t->ev) {
+    if (hipEventCreate(&e) != hipSuccess) {
+      e = nullptr;
+      omnimoe_timer_destroy(t);
+      return OMNIMOE_ERR_HIP;
+    }
+  }
+  *out = t;
+  return OMNIMOE_OK;
+}
+
+omnimoe_status omnimoe_timer_destroy(omnimoe_timer* t) {
+  if (!t) return OMNIMOE_ERR_INVALID_ARG;
+  for (auto e : t->ev)
+    if (e) (void)hipEventDestroy(e);
+  delete t;
+  return OMNIMOE_OK;
+}
+
+omnimoe_status omnimoe_timer_read(omnimoe_timer* t, float* ms, int32_t* n_calls) {
+  if (!t || !ms) return OMNIMOE_ERR_INVALID_ARG;
+  for (int k = 0; k < OMNIMOE_KERNEL_COUNT; ++k) ms[k] = 0.0f;
+  for (int c = 0; c < t->used; ++c) {
+    hipEvent_t* ev = &t->ev[(size_t)c * kEv];
+    if (hipEventSynchronize(ev[kEv - 1]) != hipSuccess) return OMNIMOE_ERR_HIP;
+    for (int k = 0; k < OMNIMOE_KERNEL_COUNT; ++k) {
+      float dt = 0.0f;
+      if (hipEventElapsedTime(&dt, ev[k], ev[k + 1]) != hipSuccess) return OMNIMOE_ERR_HIP;
+      ms[k] += dt;
+    }
+  }
+  if (n_calls) *n_calls = t->used;
+  t->used = 0;
+  return OMNIMOE_OK;
+}
+
+}  // extern "C"

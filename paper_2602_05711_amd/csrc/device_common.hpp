@@ -1,0 +1,92 @@
+// Wave-level helpers for gfx950 (64-lane wavefronts).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace omnimoe {
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (kWave - 1)); }
+
+__device__ __forceinline__ uint64_t lanemask_lt() {
+  return (1ull << lane_id()) - 1ull;
+}
+
+// Orders a wave's own LDS traffic: every lane's earlier LDS writes are visible to the
+// wave's later LDS reads.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Order-preserving maps of floats onto unsigned integers (larger value -> larger key);
+// -0 maps like +0.
+__device__ __forceinline__ uint32_t ord_f32(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u << 1) == 0u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float f32_from_ord(uint32_t o) {
+  uint32_t u = (o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o;
+  return __uint_as_float(u);
+}
+__device__ __forceinline__ uint64_t ord_f64(double f) {
+  uint64_t u = (uint64_t)__double_as_longlong(f);
+  if ((u << 1) == 0ull) u = 0ull;
+  return (u & 0x8000000000000000ull) ? ~u : (u | 0x8000000000000000ull);
+}
+__device__ __forceinline__ double f64_from_ord(uint64_t o) {
+  uint64_t u = (o & 0x8000000000000000ull) ? (o & 0x7FFFFFFFFFFFFFFFull) : ~o;
+  return __longlong_as_double((long long)u);
+}
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
+  uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+  lo = (uint32_t)__shfl_xor((int)lo, m, kWave);
+  hi = (uint32_t)__shfl_xor((int)hi, m, kWave);
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
+  uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+  lo = (uint32_t)__shfl((int)lo, src, kWave);
+  hi = (uint32_t)__shfl((int)hi, src, kWave);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Sum over the wave; every lane receives the same value (each butterfly level adds the
+// same two partial sums on both partners, and fp addition commutes).
+__device__ __forceinline__ float wave_sum_f32(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+  return v;
+}
+__device__ __forceinline__ int wave_sum_i32(int v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+  return v;
+}
+// Exclusive prefix sum over lanes.
+__device__ __forceinline__ int wave_excl_scan_i32(int v) {
+  int x = v;
+  const int l = lane_id();
+#pragma unroll
+  for (int m = 1; m < kWave; m <<= 1) {
+    int y = __shfl_up(x, m, kWave);
+    if (l >= m) x += y;
+  }
+  return x - v;
+}
+
+// Activation of Eq. 4 in fp32.
+__device__ __forceinline__ float activation(int act, float z) {
+  if (act == 1) return z / (1.0f + expf(-z));
+  return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f));
+}
+
+}  // namespace omnimoe

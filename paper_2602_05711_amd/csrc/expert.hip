@@ -1,0 +1,317 @@
+// Per-expert vector compute (Eq. 4, 7, 14).
+//
+// expert_dot: expert-major. The schedule's sorted positions are cut into ranges of about 64
+// tasks, each starting at an expert boundary (a range only starts inside an expert's run when
+// the run is longer than 64, so very hot experts are shared out). One wavefront walks its
+// range run by run: it loads the expert's u row once (16-byte loads, every lane a slice),
+// then for up to four of the run's tasks at a time loads the token rows, forms the dot
+// products in fp32, and writes a[p] = g_p * act(x_t . u_e) into the token-major slot p.
+//
+// accumulate: token-major, one wavefront per token. The token's H*K slots are read in
+// (head, k) order, their v rows are fetched eight at a time and y_t += a[p] * v_e is summed in
+// slot order in fp32. The order is fixed, so y is the same on every run; no atomics are used.
+#include "device_common.hpp"
+#include "internal.hpp"
+
+namespace omnimoe {
+namespace {
+
+struct DotArgs {
+  const void* x;
+  const void* u;
+  const int32_t* idx;
+  const float* gates;
+  const int32_t* perm;
+  const int32_t* sk;  // expert of each sorted position, or NULL
+  float* a;
+  int64_t M;
+  int64_t N;
+  int d;
+  int hk;
+  int act;
+  int nchunks;  // 16-byte chunks per row
+};
+
+struct AccArgs {
+  const void* v;
+  const int32_t* idx;
+  const float* a;
+  float* y;
+  int64_t T;
+  int64_t N;
+  int d;
+  int hk;
+  int nchunks;
+};
+
+// fp32 dot of one 16-byte chunk pair.
+template <bool BF16>
+__device__ __forceinline__ float chunk_dot(const uint4& p, const uint4& q, float acc) {
+  if (BF16) {
+    acc = fmaf(bf16_lo(p.x), bf16_lo(q.x), acc);
+    acc = fmaf(bf16_hi(p.x), bf16_hi(q.x), acc);
+    acc = fmaf(bf16_lo(p.y), bf16_lo(q.y), acc);
+    acc = fmaf(bf16_hi(p.y), bf16_hi(q.y), acc);
+    acc = fmaf(bf16_lo(p.z), bf16_lo(q.z), acc);
+    acc = fmaf(bf16_hi(p.z), bf16_hi(q.z), acc);
+    acc = fmaf(bf16_lo(p.w), bf16_lo(q.w), acc);
+    acc = fmaf(bf16_hi(p.w), bf16_hi(q.w), acc);
+  } else {
+    acc = fmaf(__uint_as_float(p.x), __uint_as_float(q.x), acc);
+    acc = fmaf(__uint_as_float(p.y), __uint_as_float(q.y), acc);
+    acc = fmaf(__uint_as_float(p.z), __uint_as_float(q.z), acc);
+    acc = fmaf(__uint_as_float(p.w), __uint_as_float(q.w), acc);
+  }
+  return acc;
+}
+
+// Ids and task numbers are clamped into range, so malformed inputs cannot address memory
+// outside the tables (their results are then meaningless).
+__device__ __forceinline__ int clamp_i(int v, int64_t n) {
+  return v < 0 ? 0 : (v >= n ? (int)(n - 1) : v);
+}
+
+__device__ __forceinline__ int task_at(const DotArgs& a, int64_t pos) {
+  return clamp_i(a.perm[pos], a.M);
+}
+
+__device__ __forceinline__ int key_at(const DotArgs& a, int64_t pos) {
+  return clamp_i(a.sk ? a.sk[pos] : a.idx[task_at(a, pos)], a.N);
+}
+
+// First position of wave range `lo / 64`: the first expert boundary in [lo, lo + 64), or
+// lo + 64 when the window lies inside one expert's run.
+__device__ int64_t range_start(const DotArgs& a, int64_t lo) {
+  if (lo >= a.M) return a.M;
+  const int l = lane_id();
+  const int64_t pos = lo + l;
+  const int key = pos < a.M ? key_at(a, pos) : -1;
+  const int before = lo > 0 ? key_at(a, lo - 1) : -1;
+  int prev = __shfl_up(key, 1, kWave);
+  if (l == 0) prev = before;
+  const uint64_t heads = __ballot(pos < a.M && key != prev);
+  if (heads) return lo + (__ffsll((unsigned long long)heads) - 1);
+  const int64_t nx = lo + kWave;
+  return nx < a.M ? nx : a.M;
+}
+
+template <int CPL, bool BF16>
+__global__ __launch_bounds__(256) void expert_dot_kernel(DotArgs a) {
+  const int l = lane_id();
+  const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t s = range_start(a, wave * kWave);
+  const int64_t e = range_start(a, (wave + 1) * kWave);
+  if (s >= e) return;
+  const uint4* X = (const uint4*)a.x;
+  const uint4* U = (const uint4*)a.u;
+  const int64_t row_chunks = a.nchunks;
+  bool cvalid[CPL];
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) cvalid[q] = (l + kWave * q) < a.nchunks;
+
+  int cur = -1;
+  uint4 ur[CPL];
+  for (int64_t b = s; b < e; b += kWave) {
+    const int64_t pos = b + l;
+    const bool v = pos < e;
+    const int key = v ? key_at(a, pos) : -1;
+    const int p = v ? task_at(a, pos) : 0;
+    const float g = v ? a.gates[p] : 0.0f;
+    const int cnt = (int)((e - b) < kWave ? (e - b) : kWave);
+    int j = 0;
+    while (j < cnt) {
+      const int ej = __builtin_amdgcn_readfirstlane(__shfl(key, j, kWave));
+      const uint64_t same = __ballot(key == ej) >> j;
+      int run = __builtin_ctzll(~same);
+      if (run > cnt - j) run = cnt - j;
+      if (ej != cur) {
+        const uint4* ub = U + (int64_t)ej * row_chunks;
+#pragma unroll
+        for (int q = 0; q < CPL; ++q)
+          ur[q] = cvalid[q] ? ub[l + kWave * q] : make_uint4(0, 0, 0, 0);
+        cur = ej;
+      }
+      for (int q0 = 0; q0 < run; q0 += 4) {
+        const int G = run - q0 < 4 ? run - q0 : 4;
+        uint4 xr[4][CPL];
+        int pj[4];
+        float gj[4];
+#pragma unroll
+        for (int gi = 0; gi < 4; ++gi) {
+          if (gi < G) {
+            pj[gi] = __shfl(p, j + q0 + gi, kWave);
+            gj[gi] = __shfl(g, j + q0 + gi, kWave);
+            const uint4* xb = X + (int64_t)(pj[gi] / a.hk) * row_chunks;
+#pragma unroll
+            for (int q = 0; q < CPL; ++q)
+              xr[gi][q] = cvalid[q] ? xb[l + kWave * q] : make_uint4(0, 0, 0, 0);
+          }
+        }
+#pragma unroll
+        for (int gi = 0; gi < 4; ++gi) {
+          if (gi < G) {
+            float acc = 0.0f;
+#pragma unroll
+            for (int q = 0; q < CPL; ++q) acc = chunk_dot<BF16>(ur[q], xr[gi][q], acc);
+            const float h = wave_sum_f32(acc);
+            if (l == 0) a.a[pj[gi]] = gj[gi] * activation(a.act, h);
+          }
+        }
+      }
+      j += run;
+    }
+  }
+}
+
+template <int CPL, bool BF16>
+__global__ __launch_bounds__(256) void accumulate_kernel(AccArgs a) {
+  constexpr int EPC = BF16 ? 8 : 4;
+  constexpr int UNROLL = CPL >= 16 ? 2 : (CPL >= 8 ? 4 : 8);
+  const int l = lane_id();
+  const uint4* V = (const uint4*)a.v;
+  const int64_t row_chunks = a.nchunks;
+  bool cvalid[CPL];
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) cvalid[q] = (l + kWave * q) < a.nchunks;
+  const int64_t stride = (int64_t)gridDim.x * 4;
+  for (int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < a.T; t += stride) {
+    float acc[CPL][EPC];
+#pragma unroll
+    for (int q = 0; q < CPL; ++q)
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) acc[q][k] = 0.0f;
+    for (int sb = 0; sb < a.hk; sb += kWave) {
+      const int sl = sb + l;
+      const bool valid = sl < a.hk;
+      const int ev = valid ? clamp_i(a.idx[t * a.hk + sl], a.N) : 0;
+      const float av = valid ? a.a[t * a.hk + sl] : 0.0f;
+      const int n = a.hk - sb < kWave ? a.hk - sb : kWave;
+      for (int j = 0; j < n; j += UNROLL) {
+        uint4 vr[UNROLL][CPL];
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u) {
+          if (j + u < n) {
+            const int e = __builtin_amdgcn_readfirstlane(__shfl(ev, j + u, kWave));
+            const uint4* vb = V + (int64_t)e * row_chunks;
+#pragma unroll
+            for (int q = 0; q < CPL; ++q)
+              vr[u][q] = cvalid[q] ? vb[l + kWave * q] : make_uint4(0, 0, 0, 0);
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u) {
+          if (j + u < n) {
+            const float w = __shfl(av, j + u, kWave);
+#pragma unroll
+            for (int q = 0; q < CPL; ++q) {
+              const uint4 c = vr[u][q];
+              if (BF16) {
+                acc[q][0] = fmaf(w, bf16_lo(c.x), acc[q][0]);
+                acc[q][1] = fmaf(w, bf16_hi(c.x), acc[q][1]);
+                acc[q][2] = fmaf(w, bf16_lo(c.y), acc[q][2]);
+                acc[q][3] = fmaf(w, bf16_hi(c.y), acc[q][3]);
+                acc[q][4] = fmaf(w, bf16_lo(c.z), acc[q][4]);
+                acc[q][5] = fmaf(w, bf16_hi(c.z), acc[q][5]);
+                acc[q][6] = fmaf(w, bf16_lo(c.w), acc[q][6]);
+                acc[q][7] = fmaf(w, bf16_hi(c.w), acc[q][7]);
+              } else {
+                acc[q][0] = fmaf(w, __uint_as_float(c.x), acc[q][0]);
+                acc[q][1] = fmaf(w, __uint_as_float(c.y), acc[q][1]);
+                acc[q][2] = fmaf(w, __uint_as_float(c.z), acc[q][2]);
+                acc[q][3] = fmaf(w, __uint_as_float(c.w), acc[q][3]);
+              }
+            }
+          }
+        }
+      }
+    }
+    float4* yt = (float4*)(a.y + t * a.d);
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      if (!cvalid[q]) continue;
+      const int c = l + kWave * q;
+#pragma unroll
+      for (int k = 0; k < EPC; k += 4)
+        yt[(c * EPC + k) / 4] = make_float4(acc[q][k], acc[q][k + 1], acc[q][k + 2], acc[q][k + 3]);
+    }
+  }
+}
+
+template <bool BF16>
+hipError_t dispatch_dot(int cpl, dim3 grid, hipStream_t st, const DotArgs& a) {
+  switch (cpl) {
+    case 1: hipLaunchKernelGGL((expert_dot_kernel<1, BF16>), grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((expert_dot_kernel<2, BF16>), grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((expert_dot_kernel<4, BF16>), grid, dim3(256), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((expert_dot_kernel<8, BF16>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((expert_dot_kernel<16, BF16>), grid, dim3(256), 0, st, a); break;
+  }
+  return hipGetLastError();
+}
+
+template <bool BF16>
+hipError_t dispatch_acc(int cpl, dim3 grid, hipStream_t st, const AccArgs& a) {
+  switch (cpl) {
+    case 1: hipLaunchKernelGGL((accumulate_kernel<1, BF16>), grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((accumulate_kernel<2, BF16>), grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((accumulate_kernel<4, BF16>), grid, dim3(256), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((accumulate_kernel<8, BF16>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((accumulate_kernel<16, BF16>), grid, dim3(256), 0, st, a); break;
+  }
+  return hipGetLastError();
+}
+
+// Chunks per lane, rounded up to a power of two.
+int chunks_per_lane(int nchunks) {
+  int c = 1;
+  while (c * kWave < nchunks) c <<= 1;
+  return c;
+}
+
+}  // namespace
+
+hipError_t launch_expert_dot(const Shape& s, const void* x, const void* u, const int32_t* idx,
+                             const float* gates, const int32_t* perm, const int32_t* sorted_keys,
+                             float* abuf, hipStream_t st) {
+  if (s.M == 0) return hipSuccess;
+  DotArgs a;
+  a.x = x;
+  a.u = u;
+  a.idx = idx;
+  a.gates = gates;
+  a.perm = perm;
+  a.sk = sorted_keys;
+  a.a = abuf;
+  a.M = s.M;
+  a.N = s.N;
+  a.d = s.d;
+  a.hk = s.hk;
+  a.act = s.act;
+  a.nchunks = s.bf16 ? s.d / 8 : s.d / 4;
+  const int64_t waves = (s.M + kWave - 1) / kWave;
+  dim3 grid((unsigned)((waves + 3) / 4));
+  const int cpl = chunks_per_lane(a.nchunks);
+  return s.bf16 ? dispatch_dot<true>(cpl, grid, st, a) : dispatch_dot<false>(cpl, grid, st, a);
+}
+
+hipError_t launch_accumulate(const Shape& s, const void* v, const int32_t* idx, const float* abuf,
+                             float* y, hipStream_t st) {
+  if (s.T == 0) return hipSuccess;
+  AccArgs a;
+  a.v = v;
+  a.idx = idx;
+  a.a = abuf;
+  a.y = y;
+  a.T = s.T;
+  a.N = s.N;
+  a.d = s.d;
+  a.hk = s.hk;
+  a.nchunks = s.bf16 ? s.d / 8 : s.d / 4;
+  int64_t blocks = (s.T + 3) / 4;
+  if (blocks > 16384) blocks = 16384;
+  const int cpl = chunks_per_lane(a.nchunks);
+  return s.bf16 ? dispatch_acc<true>(cpl, dim3((unsigned)blocks), st, a)
+                : dispatch_acc<false>(cpl, dim3((unsigned)blocks), st, a);
+}
+
+}  // namespace omnimoe

@@ -1,0 +1,54 @@
+// Internal declarations shared by the host API and the kernel translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace omnimoe {
+
+// Derived sizes of one layer call (validated by the host API before any launch).
+struct Shape {
+  int64_t T;
+  int d;
+  int nr, nc;    // grid rows / columns
+  int dk;        // sub-key dimension
+  int H, K;
+  bool bf16;     // storage type of x, keys, u, v
+  int act;       // 0 GELU-erf, 1 SiLU
+  int col0;      // first x column scored by the column half (d_key or 0)
+  int64_t N;     // nr * nc
+  int64_t M;     // T * H * K
+  int64_t rows;  // T * H
+  int hk;        // H * K
+};
+
+// Logit GEMM: half_scores[t, h, 0:nr] = x[t, 0:dk] . keys_row[h, i, :],
+// half_scores[t, h, nr:nr+nc] = x[t, col0:col0+dk] . keys_col[h, j, :].
+hipError_t launch_score(const Shape& s, const void* x, const void* keys_row,
+                        const void* keys_col, float* half_scores, hipStream_t st);
+
+// Per-half top-K, Cartesian merge and gates from fp32 half-scores.
+hipError_t launch_select(const Shape& s, const float* half_scores, int32_t* idx, float* gates,
+                         hipStream_t st);
+
+// Radix-sort schedule. Workspace needs schedule_ws_bytes(M) bytes. On return sorted_keys
+// points into the workspace (expert id of each sorted position).
+size_t schedule_ws_bytes(int64_t M, int64_t N);
+hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, int32_t* active,
+                           int32_t* active_offsets, int32_t* n_active, int32_t* dense_offsets,
+                           void* ws, const int32_t** sorted_keys, hipStream_t st);
+
+// a[p] = g_p * act(x_t . u_e) over the expert-major order given by perm (sorted_keys may be
+// NULL: the kernel then reads idx[perm[pos]]).
+hipError_t launch_expert_dot(const Shape& s, const void* x, const void* u, const int32_t* idx,
+                             const float* gates, const int32_t* perm,
+                             const int32_t* sorted_keys, float* a, hipStream_t st);
+
+// dst[0:n] = value (a kernel, so the call can sit inside a captured graph).
+hipError_t launch_fill_i32(int32_t* dst, int64_t n, int32_t value, hipStream_t st);
+
+// y[t] = sum over slots (h, k) in order of a[p] * v[idx[p]].
+hipError_t launch_accumulate(const Shape& s, const void* v, const int32_t* idx, const float* a,
+                             float* y, hipStream_t st);
+
+}  // namespace omnimoe

@@ -1,0 +1,359 @@
+// Expert-Centric Scheduling (Sec. 2.3, Eq. 12-13) as a stable least-significant-digit radix
+// sort of the task ids p = 0 .. M-1 by expert id idx[p], followed by segment extraction.
+//
+// Each pass (digit of up to 10 bits) is three steps:
+//   upsweep   per-tile digit histogram (tile = 4096 tasks), stored digit-major;
+//   scan      exclusive scan of the histogram: the first output slot of (digit, tile);
+//   downsweep each wave ranks its tasks stably (ballot-matched peers in lane order plus a
+//             per-wave running count), then tasks scatter to scan + wave offset + rank.
+// Stability of every pass makes the final order (expert, task id), which is unique.
+// Segment extraction marks positions whose expert differs from the previous one and
+// compacts them with another scan into active / active_offsets / n_active.
+// Everything is integer arithmetic; the LDS atomics only count.
+#include <algorithm>
+
+#include "device_common.hpp"
+#include "internal.hpp"
+
+namespace omnimoe {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kItems = 16;
+constexpr int kTile = kThreads * kItems;   // tasks per tile, 1024 per wave
+constexpr int kMaxDigitBits = 10;
+constexpr int kMaxRadix = 1 << kMaxDigitBits;
+
+// ------------------------------------------------------------------ generic scan
+// Exclusive scan over a virtual int array given by a functor, in chunks of kTile.
+
+struct ArrayVal {
+  const int32_t* a;
+  int64_t n;
+  __device__ int operator()(int64_t i) const { return i < n ? a[i] : 0; }
+};
+
+struct HeadFlag {  // 1 where a new expert segment starts in the sorted keys
+  const int32_t* k;
+  int64_t n;
+  __device__ int operator()(int64_t i) const {
+    if (i >= n) return 0;
+    return (i == 0 || k[i] != k[i - 1]) ? 1 : 0;
+  }
+};
+
+// Block-wide exclusive scan of per-thread values; returns the block total in *total.
+__device__ int block_excl_scan(int v, int* total) {
+  __shared__ int wsum[kThreads / kWave];
+  const int l = lane_id(), w = threadIdx.x >> 6;
+  int incl = v;
+#pragma unroll
+  for (int m = 1; m < kWave; m <<= 1) {
+    int y = __shfl_up(incl, m, kWave);
+    if (l >= m) incl += y;
+  }
+  if (l == kWave - 1) wsum[w] = incl;
+  __syncthreads();
+  int off = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < kThreads / kWave; ++i) {
+    int s = wsum[i];
+    if (i < w) off += s;
+    tot += s;
+  }
+  __syncthreads();
+  *total = tot;
+  return off + incl - v;
+}
+
+template <class F>
+__global__ __launch_bounds__(kThreads) void scan_reduce_kernel(F f, int64_t n, int32_t* partial) {
+  const int64_t base = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kItems;
+  int s = 0;
+#pragma unroll
+  for (int j = 0; j < kItems; ++j) s += f(base + j);
+  int total;
+  block_excl_scan(s, &total);
+  if (threadIdx.x == 0) partial[blockIdx.x] = total;
+}
+
+// Exclusive scan of the partials in place (one block); the grand total goes to *total_out.
+__global__ __launch_bounds__(kThreads) void scan_partials_kernel(int32_t* partial, int nb,
+                                                                 int32_t* total_out) {
+  int carry = 0;
+  for (int base = 0; base < nb; base += kThreads) {
+    int i = base + (int)threadIdx.x;
+    int v = i < nb ? partial[i] : 0;
+    int total;
+    int ex = block_excl_scan(v, &total);
+    if (i < nb) partial[i] = carry + ex;
+    carry += total;
+  }
+  if (threadIdx.x == 0 && total_out) *total_out = carry;
+}
+
+// Writes the exclusive scan of f to out (ArrayVal) ...
+struct EmitScan {
+  int32_t* out;
+  int64_t n;
+  __device__ void operator()(int64_t i, int val, int pos) const {
+    (void)val;
+    if (i < n) out[i] = pos;
+  }
+};
+
+// ... or compacts segment heads into active / active_offsets (HeadFlag). `cap` bounds the
+// output arrays, which only matters if some id lies outside [0, N).
+struct EmitSegments {
+  const int32_t* keys;
+  int32_t* active;
+  int32_t* offsets;
+  int32_t cap;
+  __device__ void operator()(int64_t i, int val, int pos) const {
+    if (val && pos < cap) {
+      active[pos] = keys[i];
+      offsets[pos] = (int32_t)i;
+    }
+  }
+};
+
+template <class F, class E>
+__global__ __launch_bounds__(kThreads) void scan_down_kernel(F f, E emit, const int32_t* partial) {
+  const int64_t base = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kItems;
+  int v[kItems];
+  int s = 0;
+#pragma unroll
+  for (int j = 0; j < kItems; ++j) {
+    v[j] = f(base + j);
+    s += v[j];
+  }
+  int total;
+  int pos = block_excl_scan(s, &total) + partial[blockIdx.x];
+#pragma unroll
+  for (int j = 0; j < kItems; ++j) {
+    emit(base + j, v[j], pos);
+    pos += v[j];
+  }
+}
+
+template <class F, class E>
+hipError_t device_scan(F f, E emit, int64_t n, int32_t* partial, int32_t* total_out,
+                       hipStream_t st) {
+  const int nb = (int)((n + kTile - 1) / kTile);
+  if (nb == 0) return hipSuccess;
+  hipLaunchKernelGGL(scan_reduce_kernel<F>, dim3(nb), dim3(kThreads), 0, st, f, n, partial);
+  hipLaunchKernelGGL(scan_partials_kernel, dim3(1), dim3(kThreads), 0, st, partial, nb, total_out);
+  hipLaunchKernelGGL((scan_down_kernel<F, E>), dim3(nb), dim3(kThreads), 0, st, f, emit,
+                     (const int32_t*)partial);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ radix pass
+
+struct RadixPass {
+  const int32_t* keys_in;
+  const int32_t* vals_in;  // NULL: values are the positions (task ids)
+  int32_t* keys_out;
+  int32_t* vals_out;
+  int32_t* hist;           // [radix][num_tiles]
+  int64_t n;
+  int shift, bits, num_tiles;
+};
+
+__global__ __launch_bounds__(kThreads) void radix_upsweep_kernel(RadixPass p) {
+  __shared__ int cnt[kMaxRadix];
+  const int radix = 1 << p.bits;
+  for (int d = threadIdx.x; d < radix; d += kThreads) cnt[d] = 0;
+  __syncthreads();
+  const int64_t base = (int64_t)blockIdx.x * kTile;
+  const uint32_t mask = (uint32_t)radix - 1u;
+#pragma unroll 4
+  for (int j = 0; j < kItems; ++j) {
+    int64_t i = base + threadIdx.x + (int64_t)kThreads * j;
+    if (i < p.n) atomicAdd(&cnt[((uint32_t)p.keys_in[i] >> p.shift) & mask], 1);
+  }
+  __syncthreads();
+  for (int d = threadIdx.x; d < radix; d += kThreads)
+    p.hist[(int64_t)d * p.num_tiles + blockIdx.x] = cnt[d];
+}
+
+__global__ __launch_bounds__(kThreads) void radix_downsweep_kernel(RadixPass p) {
+  __shared__ int wcnt[kThreads / kWave][kMaxRadix];
+  __shared__ int gofs[kMaxRadix];
+  const int radix = 1 << p.bits;
+  const uint32_t mask = (uint32_t)radix - 1u;
+  for (int d = threadIdx.x; d < radix; d += kThreads) {
+    gofs[d] = p.hist[(int64_t)d * p.num_tiles + blockIdx.x];
+#pragma unroll
+    for (int w = 0; w < kThreads / kWave; ++w) wcnt[w][d] = 0;
+  }
+  __syncthreads();
+  const int l = lane_id(), w = threadIdx.x >> 6;
+  const int64_t wbase = (int64_t)blockIdx.x * kTile + (int64_t)w * (kTile / 4);
+  const uint64_t lt = lanemask_lt();
+  int key[kItems], val[kItems], rank[kItems];
+#pragma unroll
+  for (int r = 0; r < kItems; ++r) {
+    const int64_t i = wbase + (int64_t)r * kWave + l;
+    const bool valid = i < p.n;
+    key[r] = valid ? p.keys_in[i] : 0;
+    val[r] = valid ? (p.vals_in ? p.vals_in[i] : (int)i) : 0;
+    const uint32_t d = ((uint32_t)key[r] >> p.shift) & mask;
+    uint64_t peers = __ballot(valid);
+    for (int b = 0; b < p.bits; ++b) {
+      const bool bit = (d >> b) & 1u;
+      const uint64_t bal = __ballot(bit);
+      peers &= bit ? bal : ~bal;
+    }
+    const int before = __popcll(peers & lt);
+    const int count = __popcll(peers);
+    int run = valid ? wcnt[w][d] : 0;
+    wave_lds_sync();
+    if (valid && before == 0) wcnt[w][d] = run + count;
+    wave_lds_sync();
+    rank[r] = run + before;
+  }
+  __syncthreads();
+  for (int d = threadIdx.x; d < radix; d += kThreads) {
+    int run = gofs[d];
+#pragma unroll
+    for (int ww = 0; ww < kThreads / kWave; ++ww) {
+      int c = wcnt[ww][d];
+      wcnt[ww][d] = run;
+      run += c;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < kItems; ++r) {
+    const int64_t i = wbase + (int64_t)r * kWave + l;
+    if (i < p.n) {
+      const uint32_t d = ((uint32_t)key[r] >> p.shift) & mask;
+      const int pos = wcnt[w][d] + rank[r];
+      p.keys_out[pos] = key[r];
+      p.vals_out[pos] = val[r];
+    }
+  }
+}
+
+__global__ void close_offsets_kernel(int32_t* offsets, int32_t* n_active, int32_t m,
+                                     int32_t cap) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    int n = *n_active;
+    if (n > cap) {
+      n = cap;
+      *n_active = cap;
+    }
+    offsets[n] = m;
+  }
+}
+
+// dense[e] = first sorted position of expert e = active_offsets[lower_bound(active, e)].
+__global__ __launch_bounds__(kThreads) void dense_offsets_kernel(const int32_t* active,
+                                                                 const int32_t* offsets,
+                                                                 const int32_t* n_active,
+                                                                 int32_t* dense, int64_t n_experts) {
+  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (e > n_experts) return;
+  int lo = 0, hi = *n_active;
+  while (lo < hi) {
+    int mid = (lo + hi) >> 1;
+    if ((int64_t)active[mid] < e) lo = mid + 1; else hi = mid;
+  }
+  dense[e] = offsets[lo];
+}
+
+__global__ __launch_bounds__(kThreads) void fill_i32_kernel(int32_t* dst, int64_t n, int32_t v) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i < n) dst[i] = v;
+}
+
+size_t align_up(size_t v) { return (v + 255) & ~(size_t)255; }
+
+int digit_bits_total(int64_t n_experts) {
+  int b = 0;
+  while ((int64_t)1 << b < n_experts) ++b;
+  return b;
+}
+
+}  // namespace
+
+hipError_t launch_fill_i32(int32_t* dst, int64_t n, int32_t value, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_i32_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)),
+                     dim3(kThreads), 0, st, dst, n, value);
+  return hipGetLastError();
+}
+
+size_t schedule_ws_bytes(int64_t M, int64_t N) {
+  const int64_t tiles = (M + kTile - 1) / kTile;
+  const int64_t hist = (int64_t)kMaxRadix * (tiles > 0 ? tiles : 1);
+  const int64_t part = (std::max<int64_t>(hist, M) + kTile - 1) / kTile + 1;
+  size_t b = 0;
+  b += 4 * align_up((size_t)M * 4);      // keys/values ping-pong
+  b += align_up((size_t)hist * 4);       // histogram
+  b += align_up((size_t)part * 4);       // scan partials
+  (void)N;
+  return b;
+}
+
+hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, int32_t* active,
+                           int32_t* active_offsets, int32_t* n_active, int32_t* dense_offsets,
+                           void* ws, const int32_t** sorted_keys, hipStream_t st) {
+  const int64_t M = s.M;
+  char* w = (char*)ws;
+  int32_t* K0 = (int32_t*)w; w += align_up((size_t)M * 4);
+  int32_t* V0 = (int32_t*)w; w += align_up((size_t)M * 4);
+  int32_t* K1 = (int32_t*)w; w += align_up((size_t)M * 4);
+  int32_t* V1 = (int32_t*)w; w += align_up((size_t)M * 4);
+  const int num_tiles = (int)((M + kTile - 1) / kTile);
+  int32_t* hist = (int32_t*)w; w += align_up((size_t)kMaxRadix * num_tiles * 4);
+  int32_t* partial = (int32_t*)w;
+
+  // Digit widths: the fewest passes of at most 10 bits, spread evenly.
+  const int total_bits = digit_bits_total(s.N);
+  const int passes = total_bits == 0 ? 1 : (total_bits + kMaxDigitBits - 1) / kMaxDigitBits;
+  const int per = total_bits == 0 ? 1 : (total_bits + passes - 1) / passes;
+  const int32_t* kin = idx;
+  const int32_t* vin = nullptr;
+  int shift = 0;
+  for (int ps = 0; ps < passes; ++ps) {
+    const bool last = ps == passes - 1;
+    const int bits = std::min(per, std::max(1, total_bits - shift));
+    RadixPass p;
+    p.keys_in = kin;
+    p.vals_in = vin;
+    p.keys_out = (ps & 1) ? K1 : K0;
+    p.vals_out = last ? perm : ((ps & 1) ? V1 : V0);
+    p.hist = hist;
+    p.n = M;
+    p.shift = shift;
+    p.bits = bits;
+    p.num_tiles = num_tiles;
+    hipLaunchKernelGGL(radix_upsweep_kernel, dim3(num_tiles), dim3(kThreads), 0, st, p);
+    const int64_t hn = (int64_t)(1 << bits) * num_tiles;
+    hipError_t e = device_scan(ArrayVal{hist, hn}, EmitScan{hist, hn}, hn, partial, nullptr, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(radix_downsweep_kernel, dim3(num_tiles), dim3(kThreads), 0, st, p);
+    kin = p.keys_out;
+    vin = p.vals_out;
+    shift += bits;
+  }
+  *sorted_keys = kin;
+  const int32_t cap = (int32_t)std::min<int64_t>(M, s.N);
+  hipError_t e = device_scan(HeadFlag{kin, M}, EmitSegments{kin, active, active_offsets, cap}, M,
+                             partial, n_active, st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(close_offsets_kernel, dim3(1), dim3(64), 0, st, active_offsets, n_active,
+                     (int32_t)M, cap);
+  if (dense_offsets) {
+    const int64_t n = s.N + 1;
+    hipLaunchKernelGGL(dense_offsets_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, st, (const int32_t*)active,
+                       (const int32_t*)active_offsets, (const int32_t*)n_active, dense_offsets,
+                       s.N);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace omnimoe

@@ -1,0 +1,232 @@
+// Router logits (Eq. 9): one NT GEMM per grid half, C = Xq * Keys^T, where Xq is the
+// token's query slice x[:, c0:c0+d_key] and Keys stacks the H heads' sub-key tables
+// ([H * n_half, d_key]). Both operands are contiguous along d_key, so MFMA fragments load
+// straight from row-major memory.
+//
+// bf16: 128x128 macro tile, 4 waves of 64x64, v_mfma_f32_16x16x32_bf16, k-step 64,
+// LDS double buffer fed through registers, fp32 accumulation.
+// fp32: a VALU FMA tile kernel (the fp32 layer is small; fp32 MFMA would change rounding).
+#include "device_common.hpp"
+#include "internal.hpp"
+
+namespace omnimoe {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+struct ScoreArgs {
+  const void* x;
+  const void* keys[2];
+  float* out;
+  int64_t T;
+  int d;
+  int dk;
+  int H;
+  int nh[2];        // rows per head of each half's key table
+  int col0[2];      // first x column of each half's query
+  int out_off[2];   // column offset of each half inside one (t, h) output row
+  int per_head;     // nr + nc
+  int64_t ldo;      // H * (nr + nc)
+};
+
+// Output column of GEMM column n (head n / nh, key n % nh) within a token's row.
+__device__ __forceinline__ int64_t out_col(const ScoreArgs& a, int half, int n) {
+  int h = n / a.nh[half];
+  int i = n - h * a.nh[half];
+  return (int64_t)h * a.per_head + a.out_off[half] + i;
+}
+
+constexpr int BM = 128, BN = 128, BK = 64;
+constexpr int LDS_ROW = BK + 8;  // bf16 per LDS row: 144 B keeps 16-lane b128 reads conflict-free
+
+__global__ __launch_bounds__(256) void score_bf16_kernel(ScoreArgs a) {
+  const int half = blockIdx.z;
+  const int ncols = a.H * a.nh[half];
+  const int n0 = blockIdx.x * BN;
+  if (n0 >= ncols) return;
+  const int64_t m0 = (int64_t)blockIdx.y * BM;
+  const uint16_t* X = (const uint16_t*)a.x;
+  const uint16_t* Kt = (const uint16_t*)a.keys[half];
+  const int c0 = a.col0[half];
+
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LDS_ROW];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * LDS_ROW];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wid = tid >> 6;
+  const int wm = wid >> 1, wn = wid & 1;
+
+  // Global-load assignment: chunk c = tid + 256 j (j < 4) is row c / 8, 16-byte column c % 8.
+  uint4 ra[4], rb[4];
+  auto load_tile = [&](int k0) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      int c = tid + 256 * j;
+      int r = c >> 3, kc = (c & 7) * 8;
+      int64_t gm = m0 + r;
+      int gn = n0 + r;
+      bool kin = (k0 + kc) < a.dk;
+      ra[j] = make_uint4(0, 0, 0, 0);
+      rb[j] = make_uint4(0, 0, 0, 0);
+      if (kin && gm < a.T) ra[j] = *(const uint4*)(X + gm * a.d + c0 + k0 + kc);
+      if (kin && gn < ncols) rb[j] = *(const uint4*)(Kt + (int64_t)gn * a.dk + k0 + kc);
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      int c = tid + 256 * j;
+      int r = c >> 3, kc = (c & 7) * 8;
+      *(uint4*)(&As[buf][r * LDS_ROW + kc]) = ra[j];
+      *(uint4*)(&Bs[buf][r * LDS_ROW + kc]) = rb[j];
+    }
+  };
+
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int KT = (a.dk + BK - 1) / BK;
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+
+  // MFMA 16x16x32 operand layout: lane l holds row (l % 16) of A (column of B) and the
+  // eight k values 8 * (l / 16) .. 8 * (l / 16) + 7.
+  const int frag_row = lane & 15;
+  const int frag_k = (lane >> 4) * 8;
+
+  for (int kt = 0; kt < KT; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < KT) load_tile((kt + 1) * BK);
+#pragma unroll
+    for (int ks = 0; ks < BK; ks += 32) {
+      bf16x8 fa[4], fb[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        int r = wm * 64 + i * 16 + frag_row;
+        fa[i] = *(const bf16x8*)(&As[cur][r * LDS_ROW + ks + frag_k]);
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        int r = wn * 64 + j * 16 + frag_row;
+        fb[j] = *(const bf16x8*)(&Bs[cur][r * LDS_ROW + ks + frag_k]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < KT) store_tile(cur ^ 1);
+    __syncthreads();
+  }
+
+  // Accumulator layout: acc[i][j][r] is row 4 * (l / 16) + r, column l % 16 of the
+  // 16x16 tile (i, j).
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    int n = n0 + wn * 64 + j * 16 + (lane & 15);
+    if (n >= ncols) continue;
+    int64_t oc = out_col(a, half, n);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        int64_t m = m0 + wm * 64 + i * 16 + (lane >> 4) * 4 + r;
+        if (m < a.T) a.out[m * a.ldo + oc] = acc[i][j][r];
+      }
+    }
+  }
+}
+
+constexpr int FT = 64, FK = 16;
+
+__global__ __launch_bounds__(256) void score_f32_kernel(ScoreArgs a) {
+  const int half = blockIdx.z;
+  const int ncols = a.H * a.nh[half];
+  const int n0 = blockIdx.x * FT;
+  if (n0 >= ncols) return;
+  const int64_t m0 = (int64_t)blockIdx.y * FT;
+  const float* X = (const float*)a.x;
+  const float* Kt = (const float*)a.keys[half];
+  const int c0 = a.col0[half];
+  __shared__ float As[FK][FT + 4], Bs[FK][FT + 4];
+  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < a.dk; k0 += FK) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      int c = tid + 256 * j;
+      int r = c >> 4, kk = c & 15;
+      int64_t gm = m0 + r;
+      int gn = n0 + r;
+      bool kin = (k0 + kk) < a.dk;
+      As[kk][r] = (kin && gm < a.T) ? X[gm * a.d + c0 + k0 + kk] : 0.f;
+      Bs[kk][r] = (kin && gn < ncols) ? Kt[(int64_t)gn * a.dk + k0 + kk] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < FK; ++kk) {
+      float av[4], bv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) av[i] = As[kk][ty * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bv[j] = Bs[kk][tx * 4 + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    int n = n0 + tx * 4 + j;
+    if (n >= ncols) continue;
+    int64_t oc = out_col(a, half, n);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      int64_t m = m0 + ty * 4 + i;
+      if (m < a.T) a.out[m * a.ldo + oc] = acc[i][j];
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_score(const Shape& s, const void* x, const void* keys_row,
+                        const void* keys_col, float* half_scores, hipStream_t st) {
+  ScoreArgs a;
+  a.x = x;
+  a.keys[0] = keys_row;
+  a.keys[1] = keys_col;
+  a.out = half_scores;
+  a.T = s.T;
+  a.d = s.d;
+  a.dk = s.dk;
+  a.H = s.H;
+  a.nh[0] = s.nr;
+  a.nh[1] = s.nc;
+  a.col0[0] = 0;
+  a.col0[1] = s.col0;
+  a.out_off[0] = 0;
+  a.out_off[1] = s.nr;
+  a.per_head = s.nr + s.nc;
+  a.ldo = (int64_t)s.H * (s.nr + s.nc);
+  const int ncols = s.H * (s.nr > s.nc ? s.nr : s.nc);
+  if (s.bf16) {
+    dim3 grid((ncols + BN - 1) / BN, (unsigned)((s.T + BM - 1) / BM), 2);
+    hipLaunchKernelGGL(score_bf16_kernel, grid, dim3(256), 0, st, a);
+  } else {
+    dim3 grid((ncols + FT - 1) / FT, (unsigned)((s.T + FT - 1) / FT), 2);
+    hipLaunchKernelGGL(score_f32_kernel, grid, dim3(256), 0, st, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace omnimoe

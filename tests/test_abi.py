@@ -1,0 +1,125 @@
+"""The C ABI library loads, exports what include/omnimoe.h declares, and rejects bad arguments
+before touching the GPU (these calls return from the host-side checks, so they run without one)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2602_05711_amd as P
+from paper_2602_05711_amd import binding as B
+import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+OK, INVALID, UNSUPPORTED, ALIGN, WORKSPACE = 0, 1, 2, 3, 4
+
+
+def _declared_functions():
+    with open(os.path.join(ROOT, "include", "omnimoe.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^(?:omnimoe_status|const char\*)\s+(omnimoe_\w+)\(", text,
+                                 flags=re.M)))
+
+
+def test_header_matches_exports():
+    lib = P.load_library()
+    names = _declared_functions()
+    assert len(names) == 11
+    assert sorted(P.EXPORTED) == names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_descriptor_layout_matches_header():
+    # int64 T followed by ten int32 fields: 8 + 40 bytes.
+    assert ctypes.sizeof(B.OmnimoeLayerDesc) == 48
+    assert B.OmnimoeLayerDesc.d.offset == 8
+
+
+def _ws(desc, stage=B.STAGE_LAYER):
+    n = ctypes.c_size_t(0)
+    st = P.load_library().omnimoe_workspace_size(ctypes.byref(desc), stage, ctypes.byref(n))
+    return st, n.value
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("K", 65, UNSUPPORTED), ("K", 0, INVALID), ("d", 100, INVALID), ("d", 0, INVALID),
+    ("d_key", 300, INVALID), ("d_key", 12, INVALID), ("n_rows", 0, INVALID),
+    ("n_rows", 4097, INVALID), ("H", 0, INVALID), ("dtype", 7, INVALID), ("act", 3, INVALID),
+    ("query_mode", 2, INVALID), ("group_size", 2, UNSUPPORTED), ("group_size", 0, INVALID),
+    ("T", -1, INVALID),
+])
+def test_workspace_size_rejects(field, value, status):
+    d = B.make_desc(synth.WORKLOADS["small_bf16"])
+    setattr(d, field, value)
+    assert _ws(d)[0] == status
+
+
+def test_k_above_grid_is_invalid():
+    d = B.make_desc(synth.WORKLOADS["tiny_f32"])
+    d.n_rows, d.n_cols, d.K = 2, 3, 7
+    assert _ws(d)[0] == INVALID
+
+
+def test_shared_query_allows_full_width_keys():
+    d = B.make_desc(synth.WORKLOADS["small_bf16"])
+    d.d_key = 512
+    assert _ws(d)[0] == INVALID
+    d.query_mode = B.OMNIMOE_QUERY_SHARED
+    assert _ws(d)[0] == OK
+
+
+def test_workspace_sizes_cover_buffers():
+    w = synth.WORKLOADS["train_bf16"]
+    d = B.make_desc(w)
+    st, route = _ws(d, B.STAGE_ROUTE)
+    assert st == OK and route >= w.T * w.H * (w.n_rows + w.n_cols) * 4
+    st, layer = _ws(d, B.STAGE_LAYER)
+    assert st == OK and layer >= route + 3 * w.M * 4
+    assert _ws(d, 9)[0] == INVALID
+
+
+def test_entry_points_check_pointers_before_launch():
+    lib = P.load_library()
+    d = B.make_desc(synth.WORKLOADS["tiny_f32"])
+    a = ctypes.c_void_p(0x10000)   # aligned, never dereferenced: the checks fail first
+    bad = ctypes.c_void_p(0x10004)
+    n = ctypes.c_size_t
+    D = ctypes.byref(d)
+    assert lib.omnimoe_route(D, None, a, a, a, a, None, a, n(1 << 30), None) == INVALID
+    assert lib.omnimoe_route(D, bad, a, a, a, a, None, a, n(1 << 30), None) == ALIGN
+    assert lib.omnimoe_route(D, a, a, a, a, a, None, a, n(16), None) == WORKSPACE
+    assert lib.omnimoe_select(D, a, a, None, None, n(0), None) == INVALID
+    assert lib.omnimoe_schedule(D, a, a, a, a, a, bad, a, n(1 << 30), None) == ALIGN
+    assert lib.omnimoe_schedule(D, a, a, a, a, a, None, a, n(8), None) == WORKSPACE
+    assert lib.omnimoe_expert_forward(D, a, a, a, a, a, None, a, a, n(1 << 30), None) == INVALID
+    assert lib.omnimoe_layer_forward(D, a, a, a, a, a, a, None, None, a, n(8), None) == WORKSPACE
+    assert lib.omnimoe_layer_forward(D, a, a, a, a, a, a, bad, None, a, n(1 << 40), None) == ALIGN
+    assert lib.omnimoe_layer_forward_timed(D, a, a, a, a, a, a, None, None, a, n(1 << 40), None,
+                                           None) == INVALID
+
+
+def test_zero_tokens_is_a_noop():
+    lib = P.load_library()
+    d = B.make_desc(synth.WORKLOADS["small_bf16"], T=0)
+    D = ctypes.byref(d)
+    n = ctypes.c_size_t
+    assert lib.omnimoe_route(D, None, None, None, None, None, None, None, n(0), None) == OK
+    assert lib.omnimoe_expert_forward(D, None, None, None, None, None, None, None, None, n(0),
+                                      None) == OK
+    assert lib.omnimoe_layer_forward(D, None, None, None, None, None, None, None, None, None,
+                                     n(0), None) == OK
+
+
+def test_status_strings():
+    lib = P.load_library()
+    assert lib.omnimoe_status_string(0) == b"ok"
+    assert lib.omnimoe_status_string(4) == b"workspace too small"
+    assert lib.omnimoe_status_string(99) == b"unknown status"
+
+
+def test_binding_raises_on_error():
+    d = B.make_desc(synth.WORKLOADS["small_bf16"])
+    d.K = 100
+    with pytest.raises(B.OmnimoeError):
+        B.omnimoe_workspace_size(d, B.STAGE_LAYER)

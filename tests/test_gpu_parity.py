@@ -1,0 +1,339 @@
+"""GPU parity: the HIP library, called through its C ABI, against the oracle on the same seeded inputs.
+
+Tiers: half-scores within Higham's fp32 dot bound; selection bit-exact on identical fp32 logits;
+schedule bit-exact; expert compute and whole layer within the stated relative tolerance
+(1e-5 fp32, 2e-2 bf16), with routing bit-exact on every (token, head) row whose top-(K+1)
+score gaps are certified larger than the logit error.
+"""
+import gc
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_support import (GATE_TOL, compare_routing, higham_bound, row_rel_err, to_dev, tol,
+                         upload)
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+import paper_2602_05711_amd as P  # noqa: E402
+from paper_2602_05711_amd import binding as B  # noqa: E402
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+W = synth.WORKLOADS
+RAGGED = synth.Workload("ragged_bf16", T=300, d=208, n_rows=40, n_cols=72, d_key=96, H=3, K=13)
+SHAPES = {
+    "tiny_f32": W["tiny_f32"],
+    "small_bf16": W["small_bf16"],
+    "ragged_bf16": RAGGED,
+    "ragged_f32": RAGGED.with_(name="ragged_f32", dtype="f32"),
+    "shared_bf16": W["small_bf16"].with_(name="shared_bf16", T=500, d_key=512,
+                                         query_mode="shared"),
+    "silu_k1_bf16": RAGGED.with_(name="silu_k1_bf16", act="silu", K=1),
+    "k64_bf16": synth.Workload("k64_bf16", T=200, d=256, n_rows=64, n_cols=64, d_key=64, H=2,
+                               K=64),
+    "one_row_f32": synth.Workload("one_row_f32", T=100, d=64, n_rows=1, n_cols=96, d_key=32,
+                                  H=2, K=9, dtype="f32"),
+    "all_experts_bf16": synth.Workload("all_experts_bf16", T=64, d=128, n_rows=4, n_cols=4,
+                                       d_key=64, H=2, K=16),
+}
+
+
+def host_inputs(w):
+    inp = synth.make_inputs(w)
+    f32 = {k: synth.as_f32(v) for k, v in inp.items()}
+    return inp, f32
+
+
+def gpu_layer(w, dev):
+    d = B.make_desc(w)
+    y = torch.empty((w.T, w.d), dtype=torch.float32, device="cuda")
+    idx = torch.empty((w.T, w.H, w.K), dtype=torch.int32, device="cuda")
+    g = torch.empty((w.T, w.H, w.K), dtype=torch.float32, device="cuda")
+    P.omnimoe_layer_forward(d, dev["x"], dev["keys_row"], dev["keys_col"], dev["u"], dev["v"], y,
+                            idx, g)
+    torch.cuda.synchronize()
+    return y.cpu().numpy(), idx.cpu().numpy(), g.cpu().numpy()
+
+
+def gpu_half_scores(w, dev):
+    d = B.make_desc(w)
+    hs = torch.empty((w.T, w.H, w.n_rows + w.n_cols), dtype=torch.float32, device="cuda")
+    idx = torch.empty((w.T, w.H, w.K), dtype=torch.int32, device="cuda")
+    g = torch.empty((w.T, w.H, w.K), dtype=torch.float32, device="cuda")
+    P.omnimoe_route(d, dev["x"], dev["keys_row"], dev["keys_col"], idx, g, half_scores=hs)
+    torch.cuda.synchronize()
+    return hs.cpu().numpy(), idx.cpu().numpy(), g.cpu().numpy()
+
+
+# ------------------------------------------------------------------ logits and routing
+
+@pytest.mark.parametrize("name", list(SHAPES))
+def test_route_half_scores_and_selection(name):
+    w = SHAPES[name]
+    say(f"[route] {name} T={w.T} d={w.d} grid={w.n_rows}x{w.n_cols} dk={w.d_key} H={w.H} K={w.K}")
+    inp, f = host_inputs(w)
+    dev = upload(inp)
+    hs, idx, g = gpu_half_scores(w, dev)
+    dsc = oracle.desc(w)
+    sr, sc = oracle.half_scores(dsc, f["x"], f["keys_row"], f["keys_col"])
+    c0 = w.d_key if w.query_mode == "split" else 0
+    bound_r = higham_bound(f["x"][:, :w.d_key], f["keys_row"])
+    bound_c = higham_bound(f["x"][:, c0:c0 + w.d_key], f["keys_col"])
+    err_r = np.abs(hs[..., :w.n_rows] - sr)
+    err_c = np.abs(hs[..., w.n_rows:] - sc)
+    assert np.all(err_r <= bound_r + 1e-30) and np.all(err_c <= bound_c + 1e-30)
+    # selection on the GPU's own logits is exact
+    ri, _, rg, inexact = oracle.select_f32(dsc, hs, oracle.CARTESIAN)
+    assert inexact == 0
+    assert np.array_equal(idx, ri)
+    np.testing.assert_allclose(g, rg, rtol=GATE_TOL, atol=1e-7)
+    # against the fp64 router, exact outside certified near-ties
+    ref_idx, _, _, _ = oracle.select(dsc, sr, sc, oracle.CARTESIAN)
+    delta = max(float(err_r.max()), float(err_c.max()), 1e-300)
+    ties = compare_routing(w, idx, ref_idx, sr, sc, delta)
+    say(f"  max logit err {delta:.3e}, uncertified rows {ties} of {w.T * w.H}")
+
+
+SELECT_CASES = [
+    # (n_rows, n_cols, K, H, T, tie_heavy)
+    (64, 64, 8, 1, 256, False), (256, 256, 16, 4, 300, False), (1024, 1024, 16, 8, 40, False),
+    (40, 72, 13, 3, 100, False), (64, 64, 64, 2, 50, False), (1, 50, 7, 2, 40, False),
+    (50, 1, 7, 2, 40, False), (8, 8, 64, 1, 30, False), (4096, 4096, 16, 1, 6, False),
+    (3000, 17, 20, 2, 9, False), (64, 64, 8, 1, 64, True), (256, 256, 16, 2, 64, True),
+    (1024, 1024, 64, 1, 16, True), (16, 16, 33, 3, 20, True),
+]
+
+
+@pytest.mark.parametrize("case", SELECT_CASES, ids=[str(c) for c in SELECT_CASES])
+def test_select_bitexact(case):
+    nr, nc, K, H, T, ties = case
+    say(f"[select] grid={nr}x{nc} K={K} H={H} T={T} ties={ties}")
+    rng = np.random.default_rng(nr * 7919 + nc * 31 + K)
+    if ties:
+        hs = rng.integers(-3, 4, size=(T, H, nr + nc)).astype(np.float32)
+        hs[hs == 0] = -0.0 if rng.random() < 0.5 else 0.0
+    else:
+        hs = rng.standard_normal((T, H, nr + nc)).astype(np.float32)
+    w = synth.Workload("sel", T=T, d=16, n_rows=nr, n_cols=nc, d_key=8, H=H, K=K, dtype="f32")
+    d = B.make_desc(w)
+    idx = torch.empty((T, H, K), dtype=torch.int32, device="cuda")
+    g = torch.empty((T, H, K), dtype=torch.float32, device="cuda")
+    P.omnimoe_select(d, to_dev(hs), idx, g)
+    torch.cuda.synchronize()
+    ri, _, rg, inexact = oracle.select_f32(oracle.desc(w), hs, oracle.CARTESIAN)
+    bi, _, _, _ = oracle.select_f32(oracle.desc(w), hs, oracle.BRUTE)
+    assert inexact == 0 and np.array_equal(ri, bi)
+    assert np.array_equal(idx.cpu().numpy(), ri)
+    np.testing.assert_allclose(g.cpu().numpy(), rg, rtol=GATE_TOL, atol=1e-7)
+
+
+# ------------------------------------------------------------------ schedule
+
+def _zipf_ids(rng, M, N, s=1.1):
+    ranks = np.arange(1, N + 1, dtype=np.float64)
+    p = ranks ** -s
+    p /= p.sum()
+    ids = rng.choice(N, size=M, p=p)
+    return rng.permutation(N)[ids].astype(np.int32)
+
+
+SCHEDULE_CASES = [
+    # (T, H, K, n_rows, n_cols, kind)
+    (256, 1, 8, 64, 64, "uniform"), (4096, 4, 16, 256, 256, "uniform"), (3, 1, 1, 1, 7, "uniform"),
+    (999, 3, 1, 1, 1, "uniform"), (1000, 2, 7, 200, 250, "uniform"),
+    (16384, 8, 16, 1024, 1024, "uniform"), (16384, 8, 16, 1024, 1024, "zipf"),
+    (64, 8, 16, 1024, 1024, "uniform"), (1, 8, 16, 1024, 1024, "zipf"),
+    (5000, 2, 3, 4096, 4096, "uniform"),
+]
+
+
+@pytest.mark.parametrize("case", SCHEDULE_CASES, ids=[str(c) for c in SCHEDULE_CASES])
+def test_schedule_bitexact(case):
+    T, H, K, nr, nc, kind = case
+    N = nr * nc
+    say(f"[schedule] T={T} H={H} K={K} N={N} {kind}")
+    rng = np.random.default_rng(T + 17 * K + N % 1009)
+    M = T * H * K
+    ids = (_zipf_ids(rng, M, N) if kind == "zipf" else rng.integers(0, N, size=M)).astype(
+        np.int32)
+    w = synth.Workload("sch", T=T, d=16, n_rows=nr, n_cols=nc, d_key=8, H=H, K=K, dtype="f32")
+    d = B.make_desc(w)
+    A = min(M, N)
+    perm = torch.empty(M, dtype=torch.int32, device="cuda")
+    active = torch.full((A,), -7, dtype=torch.int32, device="cuda")
+    off = torch.full((A + 1,), -7, dtype=torch.int32, device="cuda")
+    na = torch.zeros(1, dtype=torch.int32, device="cuda")
+    dense = torch.empty(N + 1, dtype=torch.int32, device="cuda")
+    P.omnimoe_schedule(d, to_dev(ids), perm, active, off, na, dense)
+    torch.cuda.synchronize()
+    rperm, ract, roff, rdense = oracle.schedule(oracle.desc(w), ids)
+    n = int(na.item())
+    assert n == len(ract)
+    assert np.array_equal(perm.cpu().numpy(), rperm)
+    assert np.array_equal(active.cpu().numpy()[:n], ract)
+    assert np.array_equal(off.cpu().numpy()[:n + 1], roff)
+    assert np.array_equal(dense.cpu().numpy(), rdense)
+
+
+# ------------------------------------------------------------------ expert compute
+
+@pytest.mark.parametrize("name", ["tiny_f32", "small_bf16", "ragged_bf16", "ragged_f32",
+                                  "silu_k1_bf16", "k64_bf16", "all_experts_bf16"])
+def test_expert_forward(name):
+    w = SHAPES[name]
+    say(f"[expert] {name}")
+    inp, f = host_inputs(w)
+    dsc = oracle.desc(w)
+    sr, sc = oracle.half_scores(dsc, f["x"], f["keys_row"], f["keys_col"])
+    idx, _, g64, _ = oracle.select(dsc, sr, sc, oracle.CARTESIAN)
+    g32 = g64.astype(np.float32)
+    perm, _, _, _ = oracle.schedule(dsc, idx)
+    y_ref = oracle.expert_forward(dsc, f["x"], f["u"], f["v"], idx, g32.astype(np.float64))
+    dev = upload(inp)
+    y = torch.empty((w.T, w.d), dtype=torch.float32, device="cuda")
+    P.omnimoe_expert_forward(B.make_desc(w), dev["x"], dev["u"], dev["v"], to_dev(idx),
+                             to_dev(g32), to_dev(perm), y)
+    torch.cuda.synchronize()
+    err = row_rel_err(y.cpu().numpy(), y_ref)
+    say(f"  max row rel err {err.max():.3e}")
+    assert err.max() <= tol(w)
+
+
+# ------------------------------------------------------------------ whole layer
+
+@pytest.mark.parametrize("name", list(SHAPES))
+def test_layer_forward(name):
+    w = SHAPES[name]
+    say(f"[layer] {name}")
+    inp, f = host_inputs(w)
+    dev = upload(inp)
+    y, idx, g = gpu_layer(w, dev)
+    hs, _, _ = gpu_half_scores(w, dev)
+    dsc = oracle.desc(w)
+    sr, sc = oracle.half_scores(dsc, f["x"], f["keys_row"], f["keys_col"])
+    ref_idx, _, ref_g, _ = oracle.select(dsc, sr, sc, oracle.CARTESIAN)
+    delta = max(float(np.abs(hs[..., :w.n_rows] - sr).max()),
+                float(np.abs(hs[..., w.n_rows:] - sc).max()), 1e-300)
+    ties = compare_routing(w, idx, ref_idx, sr, sc, delta)
+    same = np.all(idx == ref_idx, axis=(1, 2))
+    np.testing.assert_allclose(g[same], ref_g[same], rtol=GATE_TOL, atol=1e-7)
+    y_ref = oracle.expert_forward(dsc, f["x"], f["u"], f["v"], ref_idx, ref_g)
+    err = row_rel_err(y, y_ref)[same]
+    say(f"  uncertified rows {ties}; tokens compared {int(same.sum())}/{w.T}; "
+        f"max row rel err {err.max():.3e}")
+    assert err.max() <= tol(w)
+    # tokens whose routing differed (near-ties) still match the oracle on the GPU's own routing
+    if (~same).any():
+        y_own = oracle.expert_forward(dsc, f["x"], f["u"], f["v"], idx, g.astype(np.float64))
+        assert row_rel_err(y, y_own).max() <= tol(w)
+
+
+def test_layer_is_deterministic():
+    w = W["small_bf16"]
+    inp, _ = host_inputs(w)
+    dev = upload(inp)
+    a = gpu_layer(w, dev)
+    b = gpu_layer(w, dev)
+    for x, z in zip(a, b):
+        assert np.array_equal(x.view(np.uint8), z.view(np.uint8))
+
+
+def test_zero_input_closed_form():
+    w = SHAPES["ragged_bf16"]
+    inp, _ = host_inputs(w)
+    inp["x"] = np.zeros_like(inp["x"])
+    y, idx, g = gpu_layer(w, upload(inp))
+    assert np.array_equal(idx, np.broadcast_to(np.arange(w.K, dtype=np.int32), idx.shape))
+    np.testing.assert_allclose(g, 1.0 / w.K, rtol=1e-6)
+    assert np.all(y == 0.0)
+
+
+def test_timed_layer_matches_and_reports():
+    w = W["small_bf16"]
+    inp, _ = host_inputs(w)
+    dev = upload(inp)
+    y0, _, _ = gpu_layer(w, dev)
+    d = B.make_desc(w)
+    ws = B.workspace(d, B.STAGE_LAYER)
+    y = torch.empty((w.T, w.d), dtype=torch.float32, device="cuda")
+    t = B.Timer(4)
+    for _ in range(3):
+        t.layer_forward(d, dev["x"], dev["keys_row"], dev["keys_col"], dev["u"], dev["v"], y, ws)
+    ms, n = t.read()
+    t.close()
+    assert n == 3 and all(v > 0 for v in ms.values())
+    assert np.array_equal(y.cpu().numpy(), y0)
+
+
+# ------------------------------------------------------------------ full-size shapes
+
+@pytest.fixture(scope="module")
+def train_tables():
+    """Sub-keys and expert tables of the 1024^2-expert, d=2048 layer, on the GPU (8 GiB)."""
+    w = W["train_bf16"]
+    kr, kc = synth.make_keys(w)
+    dev = {"keys_row": to_dev(kr), "keys_col": to_dev(kc)}
+    for name in ("u", "v"):
+        dev[name] = to_dev(synth.make_expert_rows(w, name))
+        gc.collect()
+    yield dev, synth.as_f32(kr), synth.as_f32(kc)
+    dev.clear()
+    torch.cuda.empty_cache()
+
+
+def _sampled_parity(w, dev, kr, kc, tokens):
+    """Full-size GPU layer; oracle on the sampled tokens (expert rows drawn by id)."""
+    x = synth.make_x(w)
+    y, idx, g = gpu_layer(w, dict(dev, x=to_dev(x)))
+    hs, _, _ = gpu_half_scores(w, dict(dev, x=to_dev(x)))
+    xs = synth.as_f32(x[tokens])
+    dsc = oracle.desc(w, T=len(tokens))
+    sr, sc = oracle.half_scores(dsc, xs, kr, kc)
+    ref_idx, _, ref_g, _ = oracle.select(dsc, sr, sc, oracle.CARTESIAN)
+    hs = hs[tokens]
+    delta = max(float(np.abs(hs[..., :w.n_rows] - sr).max()),
+                float(np.abs(hs[..., w.n_rows:] - sc).max()), 1e-300)
+    ws = w.with_(T=len(tokens))
+    ties = compare_routing(ws, idx[tokens], ref_idx, sr, sc, delta)
+    same = np.all(idx[tokens] == ref_idx, axis=(1, 2))
+    ids = np.unique(ref_idx)
+    remap = np.searchsorted(ids, ref_idx).astype(np.int32)
+    u = synth.as_f32(synth.make_expert_rows(w, "u", rows=ids))
+    v = synth.as_f32(synth.make_expert_rows(w, "v", rows=ids))
+    y_ref = oracle.expert_forward(dsc, xs, u, v, remap, ref_g)
+    err = row_rel_err(y[tokens], y_ref)[same]
+    say(f"  {w.name}: uncertified rows {ties}; tokens compared {int(same.sum())}/{len(tokens)}; "
+        f"max row rel err {err.max():.3e}; logit err {delta:.2e}")
+    assert err.max() <= tol(w)
+    np.testing.assert_allclose(g[tokens][same], ref_g[same], rtol=GATE_TOL, atol=1e-7)
+    return y, idx
+
+
+def test_train_shape_sampled(train_tables):
+    dev, kr, kc = train_tables
+    w = W["train_bf16"]
+    say("[full] train_bf16 T=16384")
+    rng = np.random.default_rng(0)
+    tokens = np.unique(np.concatenate([[0, w.T - 1], rng.choice(w.T, 46, replace=False)]))
+    y, idx = _sampled_parity(w, dev, kr, kc, tokens)
+    # properties at full size: every row holds K distinct ids in range, y is finite
+    assert idx.min() >= 0 and idx.max() < w.N
+    srt = np.sort(idx.reshape(-1, w.K), axis=1)
+    assert np.all(np.diff(srt, axis=1) > 0)
+    assert np.isfinite(y).all()
+
+
+@pytest.mark.parametrize("name", ["decode64_bf16", "decode1_bf16"])
+def test_decode_shapes(train_tables, name):
+    dev, kr, kc = train_tables
+    w = W[name]
+    say(f"[full] {name}")
+    _sampled_parity(w, dev, kr, kc, np.arange(w.T))
