@@ -1,0 +1,244 @@
+#!/usr/bin/env python3
+"""Throughput of the atomic-expert layer forward on one MI355X.
+
+One step = one omnimoe_layer_forward call (router GEMM, selection, schedule, expert compute)
+over the whole batch of seeded synthetic tokens, inputs resident in HBM. Prints one JSON line:
+tokens/s, the roofline fraction of the dominant kernel (timed with HIP events on the call's
+stream) and the oracle's throughput on a bounded token sample on the host cores.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "atomic-expert layer fwd tokens/sec on 1 MI355X; achieved HBM GB/s & MFMA util"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # dense bf16 MFMA
+FP32_PEAK_TFLOPS = 157.3       # fp32 vector
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def kernel_sources_hash(files):
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2602_05711_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+# Source files each kernel group is built from (a counter file stays valid while they match).
+KERNEL_FILES = {
+    "score": ["score_gemm.hip", "device_common.hpp"],
+    "select": ["select.hip", "device_common.hpp"],
+    "schedule": ["schedule.hip", "device_common.hpp"],
+    "expert_dot": ["expert.hip", "device_common.hpp"],
+    "accumulate": ["expert.hip", "device_common.hpp"],
+}
+
+
+def algorithmic_work(w, n_active):
+    """Per-launch algorithmic bytes (or FLOP) of each kernel group, from the layer's own sizes."""
+    s_in = 2 if w.bf16 else 4
+    M, T, d = w.M, w.T, w.d
+    return {
+        # 2 T H (n_rows + n_cols) d_key FLOP (App. A, Eq. ii per head)
+        "score": ("mfma" if w.bf16 else "alu",
+                  2.0 * T * w.H * (w.n_rows + w.n_cols) * w.d_key),
+        # read the fp32 logits once, write idx and gates
+        "select": ("hbm", 4.0 * T * w.H * (w.n_rows + w.n_cols) + 8.0 * M),
+        # read idx, write perm, active list and offsets
+        "schedule": ("hbm", 4.0 * M + 4.0 * M + 8.0 * n_active),
+        # each active u row once, each token row once, perm/idx/gate in and a out per task
+        "expert_dot": ("hbm", float(n_active) * d * s_in + T * d * s_in + 16.0 * M),
+        # each active v row once, y written once, a and idx read per task
+        "accumulate": ("hbm", float(n_active) * d * s_in + T * d * 4.0 + 8.0 * M),
+    }
+
+
+def load_traffic(kernel, workload):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or None when the
+    kernel's sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("sources_sha256_16") != kernel_sources_hash(KERNEL_FILES[kernel]):
+        return None
+    return t.get("bytes_per_launch")
+
+
+def cpu_baseline(w, inp, sample_tokens, threads):
+    """Oracle (route + schedule + scheduled forward) on the first `sample_tokens` tokens."""
+    import numpy as np
+    import oracle
+    import synth
+
+    T = min(sample_tokens, w.T)
+    x = synth.as_f32(inp["x"][:T])
+    kr = synth.as_f32(inp["keys_row"])
+    kc = synth.as_f32(inp["keys_col"])
+    dsc = oracle.desc(w, T=T)
+    # Expert rows the sample reaches, drawn by id and stored compactly (float32 copies of the
+    # full tables would not fit twice in host memory); the monotone id remap keeps the order.
+    sr, sc = oracle.half_scores(dsc, x, kr, kc, n_threads=threads)
+    idx, _, _, _ = oracle.select(dsc, sr, sc, oracle.CARTESIAN, n_threads=threads)
+    ids = np.unique(idx)
+    u = synth.as_f32(synth.make_expert_rows(w, "u", rows=ids))
+    v = synth.as_f32(synth.make_expert_rows(w, "v", rows=ids))
+    # Timed: logits, Cartesian selection and gates, then the scheduled (expert-major) forward.
+    t0 = time.perf_counter()
+    sr, sc = oracle.half_scores(dsc, x, kr, kc, n_threads=threads)
+    idx, _, g, _ = oracle.select(dsc, sr, sc, oracle.CARTESIAN, n_threads=threads)
+    remap = np.searchsorted(ids, idx).astype(np.int32)
+    oracle.expert_forward(dsc, x, u, v, remap, g, scheduled=True, n_threads=threads)
+    dt = time.perf_counter() - t0
+    return {"value": T / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {T} of {w.T} tokens of {w.name} (full router over all "
+                      f"{w.n_rows}x{w.n_cols} sub-keys, Cartesian selection, schedule, "
+                      f"expert-major forward), fp64, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="train_bf16")
+    ap.add_argument("--cpu-sample", type=int, default=2048, help="tokens for the oracle leg")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle leg")
+    ap.add_argument("--out", default=None, help="also write the JSON line here")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this layer runs on a single MI355X and has no "
+              f"multi-GPU path (asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_2602_05711_amd as P
+
+    w = synth.WORKLOADS[args.workload]
+    log(f"workload {w.name}: T={w.T} d={w.d} grid={w.n_rows}x{w.n_cols} d_key={w.d_key} "
+        f"H={w.H} K={w.K} {w.dtype}")
+    t0 = time.time()
+    inp = synth.make_inputs(w)
+    log(f"generated inputs in {time.time() - t0:.1f} s")
+
+    def dev(a):
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+        return torch.from_numpy(a).cuda()
+
+    d_in = {k: dev(v) for k, v in inp.items()}
+    torch.cuda.synchronize()
+    log("inputs resident on the GPU")
+    desc = P.make_desc(w)
+    ws = P.workspace(desc, 4)
+    y = torch.empty((w.T, w.d), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def step():
+        P.omnimoe_layer_forward(desc, d_in["x"], d_in["keys_row"], d_in["keys_col"], d_in["u"],
+                                d_in["v"], y, ws=ws, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} done")
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_step = ev0.elapsed_time(ev1) / args.steps
+    log(f"timed {args.steps} steps: {ms_step:.3f} ms/step (wall {1e3 * wall / args.steps:.3f})")
+
+    # Per-kernel durations: the same calls with HIP events around each kernel group.
+    timer = P.Timer(args.steps)
+    for _ in range(args.steps):
+        timer.layer_forward(desc, d_in["x"], d_in["keys_row"], d_in["keys_col"], d_in["u"],
+                            d_in["v"], y, ws, stream=stream)
+    ms, n = timer.read()
+    timer.close()
+    per = {k: v / n for k, v in ms.items()}
+
+    # Active experts of this batch, for the algorithmic byte counts.
+    idx = torch.empty((w.T, w.H, w.K), dtype=torch.int32, device="cuda")
+    g = torch.empty((w.T, w.H, w.K), dtype=torch.float32, device="cuda")
+    P.omnimoe_route(desc, d_in["x"], d_in["keys_row"], d_in["keys_col"], idx, g)
+    A = min(w.M, w.N)
+    perm = torch.empty(w.M, dtype=torch.int32, device="cuda")
+    act = torch.empty(A, dtype=torch.int32, device="cuda")
+    off = torch.empty(A + 1, dtype=torch.int32, device="cuda")
+    na = torch.zeros(1, dtype=torch.int32, device="cuda")
+    P.omnimoe_schedule(desc, idx, perm, act, off, na)
+    torch.cuda.synchronize()
+    n_active = int(na.item())
+
+    work = algorithmic_work(w, n_active)
+    kernels = {}
+    for k, (bound, amount) in work.items():
+        t_s = per[k] * 1e-3
+        if bound == "hbm":
+            ach = amount / t_s / 1e9
+            kernels[k] = {"bound": "hbm", "ms": per[k], "achieved": ach, "unit": "GB/s",
+                          "frac": ach / HBM_PEAK_GBS, "algorithmic_bytes": amount}
+        else:
+            peak = BF16_PEAK_TFLOPS if bound == "mfma" else FP32_PEAK_TFLOPS
+            ach = amount / t_s / 1e12
+            kernels[k] = {"bound": bound, "ms": per[k], "achieved": ach, "unit": "TFLOP/s",
+                          "frac": ach / peak, "flop": amount}
+    dom = max(per, key=per.get)
+    kd = kernels[dom]
+    traffic = load_traffic(dom, w.name)
+    roofline = {"kernel": dom, "bound": kd["bound"], "achieved": kd["achieved"],
+                "peak": HBM_PEAK_GBS if kd["bound"] == "hbm" else (
+                    BF16_PEAK_TFLOPS if kd["bound"] == "mfma" else FP32_PEAK_TFLOPS),
+                "unit": kd["unit"], "frac": kd["frac"], "traffic": traffic,
+                "ms_per_launch": per[dom]}
+    log("per kernel: " + ", ".join(f"{k} {v:.3f} ms" for k, v in per.items()))
+
+    cpu = None
+    if not args.no_cpu:
+        threads = max(1, min(16, len(os.sched_getaffinity(0))))
+        log(f"oracle leg: {args.cpu_sample} tokens on {threads} host threads")
+        cpu = cpu_baseline(w, inp, args.cpu_sample, threads)
+        log(f"oracle {cpu['value']:.1f} tokens/s")
+
+    line = {
+        "metric": METRIC, "value": w.T / (ms_step * 1e-3), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "T": w.T, "d": w.d, "n_rows": w.n_rows,
+                   "n_cols": w.n_cols, "N": w.N, "d_key": w.d_key, "H": w.H, "K": w.K,
+                   "act": w.act, "query": w.query_mode},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "n_active": n_active, "eta": w.M / max(1, n_active),
+        "kernels": kernels,
+    }
+    s = json.dumps(line)
+    print(s, flush=True)
+    if args.out:
+        with open(args.out, "w") as f:
+            f.write(s + "\n")
+
+
+if __name__ == "__main__":
+    main()

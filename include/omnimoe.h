@@ -56,7 +56,8 @@ typedef enum { OMNIMOE_QUERY_SPLIT = 0, OMNIMOE_QUERY_SHARED = 1 } omnimoe_query
 
 /* Layer shape. All sizes in elements.
  *   T           tokens; x is [T, d]. T = 0 is a valid no-op.
- *   d           hidden size; 8 <= d <= 8192, d % 8 == 0.
+ *   d           hidden size; 8 <= d <= 8192, d % 8 == 0 (fp32 storage: d <= 4096, larger
+ *               returns OMNIMOE_ERR_UNSUPPORTED).
  *   n_rows      N_r, rows of the expert grid; 1 <= n_rows <= 4096.
  *   n_cols      N_c, columns; 1 <= n_cols <= 4096. N = n_rows * n_cols experts.
  *   d_key       sub-key dimension; d_key % 8 == 0. SPLIT: rows score x[:, 0:d_key] and

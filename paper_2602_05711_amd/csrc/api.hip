@@ -39,6 +39,7 @@ omnimoe_status check_desc(const omnimoe_layer_desc* d, Shape* s) {
   if (d->K > N) return OMNIMOE_ERR_INVALID_ARG;
   if (d->K > 64) return OMNIMOE_ERR_UNSUPPORTED;
   if (d->dtype != OMNIMOE_F32 && d->dtype != OMNIMOE_BF16) return OMNIMOE_ERR_INVALID_ARG;
+  if (d->dtype == OMNIMOE_F32 && d->d > 4096) return OMNIMOE_ERR_UNSUPPORTED;
   if (d->act != OMNIMOE_ACT_GELU && d->act != OMNIMOE_ACT_SILU) return OMNIMOE_ERR_INVALID_ARG;
   if (d->group_size < 1) return OMNIMOE_ERR_INVALID_ARG;
   if (d->group_size != 1) return OMNIMOE_ERR_UNSUPPORTED;

@@ -44,18 +44,21 @@ struct AccArgs {
   int nchunks;
 };
 
-// fp32 dot of one 16-byte chunk pair.
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float dot2_bf16(uint32_t p, uint32_t q, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p),
+                                         __builtin_bit_cast(bf16x2, q), acc, false);
+}
+
+// fp32 dot of one 16-byte chunk pair (bf16 pairs through v_dot2_f32_bf16).
 template <bool BF16>
 __device__ __forceinline__ float chunk_dot(const uint4& p, const uint4& q, float acc) {
   if (BF16) {
-    acc = fmaf(bf16_lo(p.x), bf16_lo(q.x), acc);
-    acc = fmaf(bf16_hi(p.x), bf16_hi(q.x), acc);
-    acc = fmaf(bf16_lo(p.y), bf16_lo(q.y), acc);
-    acc = fmaf(bf16_hi(p.y), bf16_hi(q.y), acc);
-    acc = fmaf(bf16_lo(p.z), bf16_lo(q.z), acc);
-    acc = fmaf(bf16_hi(p.z), bf16_hi(q.z), acc);
-    acc = fmaf(bf16_lo(p.w), bf16_lo(q.w), acc);
-    acc = fmaf(bf16_hi(p.w), bf16_hi(q.w), acc);
+    acc = dot2_bf16(p.x, q.x, acc);
+    acc = dot2_bf16(p.y, q.y, acc);
+    acc = dot2_bf16(p.z, q.z, acc);
+    acc = dot2_bf16(p.w, q.w, acc);
   } else {
     acc = fmaf(__uint_as_float(p.x), __uint_as_float(q.x), acc);
     acc = fmaf(__uint_as_float(p.y), __uint_as_float(q.y), acc);
@@ -95,8 +98,19 @@ __device__ int64_t range_start(const DotArgs& a, int64_t lo) {
   return nx < a.M ? nx : a.M;
 }
 
+template <int CPL>
+__device__ __forceinline__ void load_row(uint4 (&r)[CPL], const uint4* base, const bool (&cv)[CPL]) {
+  const int l = lane_id();
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) r[q] = cv[q] ? base[l + kWave * q] : make_uint4(0, 0, 0, 0);
+}
+
+// Positions are taken G at a time (four for rows up to 4096 bf16 values). Slot i holds position j0 + i: its token row is loaded,
+// and its expert's u row is loaded only when that expert differs from the previous position's
+// (otherwise the previous slot's registers are copied), so each run of an expert reads u once.
 template <int CPL, bool BF16>
 __global__ __launch_bounds__(256) void expert_dot_kernel(DotArgs a) {
+  constexpr int G = CPL >= 16 ? 1 : (CPL >= 8 ? 2 : 4);
   const int l = lane_id();
   const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int64_t s = range_start(a, wave * kWave);
@@ -105,12 +119,17 @@ __global__ __launch_bounds__(256) void expert_dot_kernel(DotArgs a) {
   const uint4* X = (const uint4*)a.x;
   const uint4* U = (const uint4*)a.u;
   const int64_t row_chunks = a.nchunks;
-  bool cvalid[CPL];
+  bool cv[CPL];
 #pragma unroll
-  for (int q = 0; q < CPL; ++q) cvalid[q] = (l + kWave * q) < a.nchunks;
+  for (int q = 0; q < CPL; ++q) cv[q] = (l + kWave * q) < a.nchunks;
 
-  int cur = -1;
-  uint4 ur[CPL];
+  int prev = -1;    // expert whose u row sits in ur[G - 1]
+  uint4 ur[G][CPL];
+  uint4 xr[G][CPL];
+#pragma unroll
+  for (int i = 0; i < G; ++i)
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) ur[i][q] = make_uint4(0, 0, 0, 0);
   for (int64_t b = s; b < e; b += kWave) {
     const int64_t pos = b + l;
     const bool v = pos < e;
@@ -118,47 +137,53 @@ __global__ __launch_bounds__(256) void expert_dot_kernel(DotArgs a) {
     const int p = v ? task_at(a, pos) : 0;
     const float g = v ? a.gates[p] : 0.0f;
     const int cnt = (int)((e - b) < kWave ? (e - b) : kWave);
-    int j = 0;
-    while (j < cnt) {
-      const int ej = __builtin_amdgcn_readfirstlane(__shfl(key, j, kWave));
-      const uint64_t same = __ballot(key == ej) >> j;
-      int run = __builtin_ctzll(~same);
-      if (run > cnt - j) run = cnt - j;
-      if (ej != cur) {
-        const uint4* ub = U + (int64_t)ej * row_chunks;
+    for (int j0 = 0; j0 < cnt; j0 += G) {
+      int ej[G], pj[G];
+      float gj[G];
 #pragma unroll
-        for (int q = 0; q < CPL; ++q)
-          ur[q] = cvalid[q] ? ub[l + kWave * q] : make_uint4(0, 0, 0, 0);
-        cur = ej;
+      for (int i = 0; i < G; ++i) {
+        const int jj = (j0 + i < cnt) ? j0 + i : cnt - 1;
+        ej[i] = readlane_i32(key, jj);
+        pj[i] = readlane_i32(p, jj);
+        gj[i] = readlane_f32(g, jj);
       }
-      for (int q0 = 0; q0 < run; q0 += 4) {
-        const int G = run - q0 < 4 ? run - q0 : 4;
-        uint4 xr[4][CPL];
-        int pj[4];
-        float gj[4];
 #pragma unroll
-        for (int gi = 0; gi < 4; ++gi) {
-          if (gi < G) {
-            pj[gi] = __shfl(p, j + q0 + gi, kWave);
-            gj[gi] = __shfl(g, j + q0 + gi, kWave);
-            const uint4* xb = X + (int64_t)(pj[gi] / a.hk) * row_chunks;
+      for (int i = 0; i < G; ++i) {
+        if (j0 + i < cnt) {
+          const int before = (i == 0) ? prev : ej[i - 1];
+          if (ej[i] == before) {
 #pragma unroll
-            for (int q = 0; q < CPL; ++q)
-              xr[gi][q] = cvalid[q] ? xb[l + kWave * q] : make_uint4(0, 0, 0, 0);
+            for (int q = 0; q < CPL; ++q) ur[i][q] = ur[(i + G - 1) % G][q];
+          } else {
+            load_row<CPL>(ur[i], U + (int64_t)ej[i] * row_chunks, cv);
           }
-        }
-#pragma unroll
-        for (int gi = 0; gi < 4; ++gi) {
-          if (gi < G) {
-            float acc = 0.0f;
-#pragma unroll
-            for (int q = 0; q < CPL; ++q) acc = chunk_dot<BF16>(ur[q], xr[gi][q], acc);
-            const float h = wave_sum_f32(acc);
-            if (l == 0) a.a[pj[gi]] = gj[gi] * activation(a.act, h);
-          }
+          load_row<CPL>(xr[i], X + (int64_t)(pj[i] / a.hk) * row_chunks, cv);
         }
       }
-      j += run;
+      float h[G];
+#pragma unroll
+      for (int i = 0; i < G; ++i) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int q = 0; q < CPL; ++q) acc = chunk_dot<BF16>(ur[i][q], xr[i][q], acc);
+        h[i] = acc;
+      }
+#pragma unroll
+      for (int i = 0; i < G; ++i) {
+        if (j0 + i < cnt) {
+          const float hs = wave_sum_uniform(h[i]);
+          if (l == i) a.a[pj[i]] = gj[i] * activation(a.act, hs);
+        }
+      }
+      // The last filled slot's expert carries into the next group.
+      const int last = (cnt - j0 < G ? cnt - j0 : G) - 1;
+#pragma unroll
+      for (int i = 0; i < G - 1; ++i)
+        if (i == last) {
+#pragma unroll
+          for (int q = 0; q < CPL; ++q) ur[G - 1][q] = ur[i][q];
+        }
+      prev = ej[last];
     }
   }
 }
@@ -191,7 +216,7 @@ __global__ __launch_bounds__(256) void accumulate_kernel(AccArgs a) {
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u) {
           if (j + u < n) {
-            const int e = __builtin_amdgcn_readfirstlane(__shfl(ev, j + u, kWave));
+            const int e = readlane_i32(ev, j + u);
             const uint4* vb = V + (int64_t)e * row_chunks;
 #pragma unroll
             for (int q = 0; q < CPL; ++q)
@@ -201,7 +226,7 @@ __global__ __launch_bounds__(256) void accumulate_kernel(AccArgs a) {
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u) {
           if (j + u < n) {
-            const float w = __shfl(av, j + u, kWave);
+            const float w = readlane_f32(av, j + u);
 #pragma unroll
             for (int q = 0; q < CPL; ++q) {
               const uint4 c = vr[u][q];

@@ -8,11 +8,13 @@
 // One wavefront per row. Keys are compared as integers (order-preserving bit maps), so the
 // result is exact and independent of evaluation order.
 //
-// Per-half top-K: each lane holds ceil(n / 64) logits. The K-th largest of the 64 lane
-// maxima, theta, is at most the K-th largest logit (K distinct lanes hold a value >= theta),
-// so the logits >= theta contain the answer. Usually a few more than K of them exist; they are
-// compacted into one per lane and bitonic-sorted. When more than 64 qualify (heavy ties), the
-// row falls back to sorting them in batches of 64 and merging.
+// Per-half top-K: each lane holds ceil(n / 64) logits. theta, the Kh-th largest of the 64
+// lane maxima, is found by a bitwise search with ballots (Kh distinct lanes hold a value
+// >= theta, so theta is at most the Kh-th largest logit and the logits >= theta contain the
+// answer). Usually only a few more than Kh logits qualify: the two halves' survivors are
+// compacted into lanes 0-31 (rows) and 32-63 (columns) and bitonic-sorted together. When more
+// than 32 qualify (heavy ties, or K > 32) that half is instead sorted in batches of 64 from
+// memory and merged.
 #include "device_common.hpp"
 #include "internal.hpp"
 
@@ -29,6 +31,33 @@ struct SelectArgs {
   int nr, nc, K;
 };
 
+// ---------------------------------------------------------------- cross-lane exchange
+// x[l ^ J] for one 32-bit word: DPP for J < 16, ds_swizzle for 16, ds_bpermute for 32.
+template <int J>
+__device__ __forceinline__ uint32_t xor_lane(uint32_t v) {
+  const int x = (int)v;
+  if constexpr (J == 1) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(x, x, 0xB1, 0xF, 0xF, false);  // quad [1,0,3,2]
+  } else if constexpr (J == 2) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(x, x, 0x4E, 0xF, 0xF, false);  // quad [2,3,0,1]
+  } else if constexpr (J == 4) {
+    const int lo = __builtin_amdgcn_update_dpp(x, x, 0x12C, 0xF, 0xF, false);  // row_ror:12
+    const int hi = __builtin_amdgcn_update_dpp(x, x, 0x124, 0xF, 0xF, false);  // row_ror:4
+    return (uint32_t)((lane_id() & 4) ? hi : lo);
+  } else if constexpr (J == 8) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(x, x, 0x128, 0xF, 0xF, false);  // row_ror:8
+  } else if constexpr (J == 16) {
+    return (uint32_t)__builtin_amdgcn_ds_swizzle(x, (16 << 10) | 0x1F);  // bitmask xor 16
+  } else {
+    return (uint32_t)__shfl_xor(x, J, kWave);
+  }
+}
+
+template <int J>
+__device__ __forceinline__ uint64_t xor_lane64(uint64_t v) {
+  return ((uint64_t)xor_lane<J>((uint32_t)(v >> 32)) << 32) | xor_lane<J>((uint32_t)v);
+}
+
 // 96-bit key of a grid cell: score (order map of the double) then lower id first.
 struct CellKey {
   uint64_t s;
@@ -39,122 +68,154 @@ __device__ __forceinline__ bool cell_gt(const CellKey& a, const CellKey& b) {
   return a.s > b.s || (a.s == b.s && a.nn > b.nn);
 }
 
-__device__ __forceinline__ CellKey shfl_xor_cell(const CellKey& k, int m) {
-  CellKey o;
-  o.s = shfl_xor_u64(k.s, m);
-  o.nn = (uint32_t)__shfl_xor((int)k.nn, m, kWave);
-  return o;
+template <int J>
+__device__ __forceinline__ CellKey xor_cell(const CellKey& k) {
+  return CellKey{xor_lane64<J>(k.s), xor_lane<J>(k.nn)};
 }
 
-// Bitonic sort of one key per lane into descending lane order.
-__device__ __forceinline__ uint32_t sort_desc_u32(uint32_t v) {
+// One compare-exchange stage of a descending bitonic sort of segments of S lanes.
+template <int S, int K2, int J>
+__device__ __forceinline__ uint64_t stage64(uint64_t v) {
   const int l = lane_id();
-#pragma unroll
-  for (int k = 2; k <= kWave; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      uint32_t o = (uint32_t)__shfl_xor((int)v, j, kWave);
-      bool keep_max = (((l & j) == 0) == ((l & k) == 0));
-      v = keep_max ? (v > o ? v : o) : (v < o ? v : o);
-    }
+  const uint64_t o = xor_lane64<J>(v);
+  const bool up = (K2 >= S) ? true : ((l & K2) == 0);
+  const bool keep_max = ((l & J) == 0) == up;
+  const uint64_t mx = v > o ? v : o, mn = v > o ? o : v;
+  return keep_max ? mx : mn;
+}
+
+template <int S, int K2, int J>
+__device__ __forceinline__ CellKey stage_cell(CellKey v) {
+  const int l = lane_id();
+  const CellKey o = xor_cell<J>(v);
+  const bool up = (K2 >= S) ? true : ((l & K2) == 0);
+  const bool keep_max = ((l & J) == 0) == up;
+  return (cell_gt(v, o) == keep_max) ? v : o;
+}
+
+// Descending bitonic sort within segments of S lanes (S = 32 or 64).
+template <int S>
+__device__ __forceinline__ uint64_t sort64(uint64_t v) {
+  v = stage64<S, 2, 1>(v);
+  v = stage64<S, 4, 2>(v); v = stage64<S, 4, 1>(v);
+  v = stage64<S, 8, 4>(v); v = stage64<S, 8, 2>(v); v = stage64<S, 8, 1>(v);
+  v = stage64<S, 16, 8>(v); v = stage64<S, 16, 4>(v); v = stage64<S, 16, 2>(v);
+  v = stage64<S, 16, 1>(v);
+  v = stage64<S, 32, 16>(v); v = stage64<S, 32, 8>(v); v = stage64<S, 32, 4>(v);
+  v = stage64<S, 32, 2>(v); v = stage64<S, 32, 1>(v);
+  if constexpr (S == 64) {
+    v = stage64<S, 64, 32>(v); v = stage64<S, 64, 16>(v); v = stage64<S, 64, 8>(v);
+    v = stage64<S, 64, 4>(v); v = stage64<S, 64, 2>(v); v = stage64<S, 64, 1>(v);
   }
   return v;
 }
 
-__device__ __forceinline__ uint64_t sort_desc_u64(uint64_t v) {
-  const int l = lane_id();
-#pragma unroll
-  for (int k = 2; k <= kWave; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      uint64_t o = shfl_xor_u64(v, j);
-      bool keep_max = (((l & j) == 0) == ((l & k) == 0));
-      v = keep_max ? (v > o ? v : o) : (v < o ? v : o);
-    }
-  }
+__device__ __forceinline__ CellKey sort_cells(CellKey v) {
+  v = stage_cell<64, 2, 1>(v);
+  v = stage_cell<64, 4, 2>(v); v = stage_cell<64, 4, 1>(v);
+  v = stage_cell<64, 8, 4>(v); v = stage_cell<64, 8, 2>(v); v = stage_cell<64, 8, 1>(v);
+  v = stage_cell<64, 16, 8>(v); v = stage_cell<64, 16, 4>(v); v = stage_cell<64, 16, 2>(v);
+  v = stage_cell<64, 16, 1>(v);
+  v = stage_cell<64, 32, 16>(v); v = stage_cell<64, 32, 8>(v); v = stage_cell<64, 32, 4>(v);
+  v = stage_cell<64, 32, 2>(v); v = stage_cell<64, 32, 1>(v);
+  v = stage_cell<64, 64, 32>(v); v = stage_cell<64, 64, 16>(v); v = stage_cell<64, 64, 8>(v);
+  v = stage_cell<64, 64, 4>(v); v = stage_cell<64, 64, 2>(v); v = stage_cell<64, 64, 1>(v);
   return v;
 }
 
-// Top 64 of two descending lane-sorted lists, descending.
-__device__ __forceinline__ uint64_t merge_desc_u64(uint64_t a, uint64_t b) {
-  const int l = lane_id();
-  uint64_t rb = shfl_u64(b, (kWave - 1) - l);
-  uint64_t v = a > rb ? a : rb;
-#pragma unroll
-  for (int j = kWave >> 1; j > 0; j >>= 1) {
-    uint64_t o = shfl_xor_u64(v, j);
-    v = ((l & j) == 0) ? (v > o ? v : o) : (v < o ? v : o);
-  }
+// The final merge levels (segments of 64, already bitonic) of a descending sort.
+__device__ __forceinline__ uint64_t bitonic_merge64(uint64_t v) {
+  v = stage64<64, 64, 32>(v); v = stage64<64, 64, 16>(v); v = stage64<64, 64, 8>(v);
+  v = stage64<64, 64, 4>(v); v = stage64<64, 64, 2>(v); v = stage64<64, 64, 1>(v);
+  return v;
+}
+__device__ __forceinline__ CellKey bitonic_merge_cells(CellKey v) {
+  v = stage_cell<64, 64, 32>(v); v = stage_cell<64, 64, 16>(v); v = stage_cell<64, 64, 8>(v);
+  v = stage_cell<64, 64, 4>(v); v = stage_cell<64, 64, 2>(v); v = stage_cell<64, 64, 1>(v);
   return v;
 }
 
-__device__ __forceinline__ CellKey sort_desc_cell(CellKey v) {
-  const int l = lane_id();
-#pragma unroll
-  for (int k = 2; k <= kWave; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      CellKey o = shfl_xor_cell(v, j);
-      bool keep_max = (((l & j) == 0) == ((l & k) == 0));
-      bool gt = cell_gt(v, o);
-      v = (keep_max == gt) ? v : o;
-    }
-  }
-  return v;
+// Top 64 of two descending lane-sorted lists, descending: lane l compares a[l] with
+// b[63 - l] (the larger of each pair forms a bitonic sequence holding the top 64), then merges.
+__device__ __forceinline__ uint64_t merge_top64(uint64_t a, uint64_t b) {
+  const uint64_t rb = ((uint64_t)(uint32_t)__shfl((int)(b >> 32), (kWave - 1) - lane_id(), kWave) << 32) |
+                      (uint32_t)__shfl((int)(uint32_t)b, (kWave - 1) - lane_id(), kWave);
+  return bitonic_merge64(a > rb ? a : rb);
 }
-
-__device__ __forceinline__ CellKey merge_desc_cell(CellKey a, CellKey b) {
-  const int l = lane_id();
+__device__ __forceinline__ CellKey merge_top64_cells(CellKey a, CellKey b) {
+  const int src = (kWave - 1) - lane_id();
   CellKey rb;
-  rb.s = shfl_u64(b.s, (kWave - 1) - l);
-  rb.nn = (uint32_t)__shfl((int)b.nn, (kWave - 1) - l, kWave);
-  CellKey v = cell_gt(a, rb) ? a : rb;
-#pragma unroll
-  for (int j = kWave >> 1; j > 0; j >>= 1) {
-    CellKey o = shfl_xor_cell(v, j);
-    bool gt = cell_gt(v, o);
-    v = (((l & j) == 0) == gt) ? v : o;
-  }
-  return v;
+  rb.s = ((uint64_t)(uint32_t)__shfl((int)(b.s >> 32), src, kWave) << 32) |
+         (uint32_t)__shfl((int)(uint32_t)b.s, src, kWave);
+  rb.nn = (uint32_t)__shfl((int)b.nn, src, kWave);
+  return bitonic_merge_cells(cell_gt(a, rb) ? a : rb);
 }
+
+// ---------------------------------------------------------------- per-half top-K
 
 // Key of logit j: value order in the high word, ~j in the low word (ties to lower j).
 __device__ __forceinline__ uint64_t logit_key(uint32_t ord, int j) {
   return ((uint64_t)ord << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)j);
 }
 
-// Top kh of the n logits at p; lane l < kh receives the l-th best as a logit key.
+// Largest x with at least k lanes holding a value >= x (the k-th largest lane value).
+__device__ __forceinline__ uint32_t kth_largest_lane(uint32_t v, int k) {
+  uint32_t th = 0u;
+#pragma unroll
+  for (int b = 31; b >= 0; --b) {
+    const uint32_t c = th | (1u << b);
+    if (__popcll(__ballot(v >= c)) >= k) th = c;
+  }
+  return th;
+}
+
+// Loads one half, finds its threshold and writes the survivors' keys to buf[0, 32).
+// Returns the number of survivors (those beyond 32 are not written).
 template <int R>
-__device__ uint64_t half_topk(const float* __restrict__ p, int n, int kh, uint64_t* wbuf) {
+__device__ __forceinline__ int half_survivors(const float* __restrict__ p, int n, int kh,
+                                              uint64_t* buf, uint32_t* theta_out) {
   const int l = lane_id();
   uint32_t o[R];
   uint32_t mx = 0u;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    int j = l + kWave * r;
+    const int j = l + kWave * r;
     o[r] = (j < n) ? ord_f32(p[j]) : 0u;  // 0 sits below every finite value
     mx = o[r] > mx ? o[r] : mx;
   }
-  const uint32_t theta = (uint32_t)__shfl((int)sort_desc_u32(mx), kh - 1, kWave);
-  int cnt = 0;
-#pragma unroll
-  for (int r = 0; r < R; ++r) cnt += (o[r] >= theta) ? 1 : 0;
-  const int total = wave_sum_i32(cnt);
-  if (total <= kWave) {
-    int pos = wave_excl_scan_i32(cnt);
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-      if (o[r] >= theta) wbuf[pos++] = logit_key(o[r], l + kWave * r);
-    wave_lds_sync();
-    uint64_t key = (l < total) ? wbuf[l] : 0ull;
-    wave_lds_sync();
-    return sort_desc_u64(key);
-  }
-  uint64_t best = 0ull;
+  const uint32_t theta = kth_largest_lane(mx, kh);
+  *theta_out = theta;
+  const uint64_t lt = lanemask_lt();
+  int base = 0;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    uint64_t key = (o[r] >= theta) ? logit_key(o[r], l + kWave * r) : 0ull;
-    best = merge_desc_u64(best, sort_desc_u64(key));
+    const bool f = o[r] >= theta;
+    const uint64_t bal = __ballot(f);
+    const int pos = base + __popcll(bal & lt);
+    if (f && pos < 32) buf[pos] = logit_key(o[r], l + kWave * r);
+    base += __popcll(bal);
+  }
+  return base;
+}
+
+// Slow path for one half: the logits >= theta, sorted in batches of 64 read from memory and
+// merged; lane l < 64 ends with the l-th best key.
+__device__ __noinline__ uint64_t half_topk_batched(const float* __restrict__ p, int n,
+                                                   uint32_t theta) {
+  const int l = lane_id();
+  uint64_t best = 0ull;
+  bool first = true;
+  for (int base = 0; base < n; base += kWave) {
+    const int j = base + l;
+    uint64_t key = 0ull;
+    if (j < n) {
+      const uint32_t o = ord_f32(p[j]);
+      if (o >= theta) key = logit_key(o, j);
+    }
+    if (__ballot(key != 0ull) == 0ull) continue;
+    key = sort64<64>(key);
+    best = first ? key : merge_top64(best, key);
+    first = false;
   }
   return best;
 }
@@ -163,57 +224,71 @@ template <int R>
 __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
   __shared__ uint16_t cand[kMaxCand];  // (a << 8) | b
   __shared__ int n_cand;
-  __shared__ uint64_t wbuf_all[4][kWave];
+  __shared__ uint64_t lists[4][2][kWave];  // per wave: sorted row keys, sorted column keys
+  __shared__ uint64_t stage[4][kWave];     // per wave: survivors, rows at 0, columns at 32
   const int K = a.K;
   const int kr = K < a.nr ? K : a.nr;
   const int kc = K < a.nc ? K : a.nc;
   if (threadIdx.x == 0) {
     int c = 0;
     for (int ra = 0; ra < kr; ++ra)
-      for (int rb = 0; rb < kc && (ra + 1) * (rb + 1) <= K; ++rb) cand[c++] = (uint16_t)((ra << 8) | rb);
+      for (int rb = 0; rb < kc && (ra + 1) * (rb + 1) <= K; ++rb)
+        cand[c++] = (uint16_t)((ra << 8) | rb);
     n_cand = c;
   }
   __syncthreads();
   const int P = n_cand;
   const int l = lane_id();
   const int w = threadIdx.x >> 6;
-  uint64_t* wbuf = wbuf_all[w];
+  uint64_t* rowk = lists[w][0];
+  uint64_t* colk = lists[w][1];
+  uint64_t* st = stage[w];
   const int64_t stride = (int64_t)gridDim.x * 4;
   for (int64_t row = (int64_t)blockIdx.x * 4 + w; row < a.rows; row += stride) {
     const float* hr = a.hs + row * (int64_t)(a.nr + a.nc);
-    const uint64_t rk = half_topk<R>(hr, a.nr, kr, wbuf);
-    const uint64_t ck = half_topk<R>(hr + a.nr, a.nc, kc, wbuf);
+    uint32_t th_r, th_c;
+    const int cr = half_survivors<R>(hr, a.nr, kr, st, &th_r);
+    const int cc = half_survivors<R>(hr + a.nr, a.nc, kc, st + 32, &th_c);
+    wave_lds_sync();
+    if (cr <= 32 && cc <= 32) {
+      // Both halves in one pass: rows sort in lanes 0-31, columns in lanes 32-63.
+      const int cnt = l < 32 ? cr : cc;
+      uint64_t key = ((l & 31) < cnt) ? st[l] : 0ull;
+      key = sort64<32>(key);
+      if (l < 32) rowk[l] = key; else colk[l - 32] = key;
+    } else {
+      const uint64_t rk = cr <= 32 ? 0ull : half_topk_batched(hr, a.nr, th_r);
+      const uint64_t ck = cc <= 32 ? 0ull : half_topk_batched(hr + a.nr, a.nc, th_c);
+      uint64_t rs = 0ull, cs = 0ull;
+      if (cr <= 32) rs = sort64<32>((l < 32 && l < cr) ? st[l] : 0ull);
+      if (cc <= 32) cs = sort64<32>((l < 32 && l < cc) ? st[32 + l] : 0ull);
+      rowk[l] = cr <= 32 ? rs : rk;
+      colk[l] = cc <= 32 ? cs : ck;
+    }
+    wave_lds_sync();
     // Cartesian candidates, 64 per batch.
-    CellKey best;
-    best.s = 0ull;
-    best.nn = 0u;
+    CellKey best{0ull, 0u};
     for (int base = 0; base < P; base += kWave) {
-      int c = base + l;
-      int ca = 0, cb = 0;
+      const int c = base + l;
+      CellKey key{0ull, 0u};
       if (c < P) {
-        ca = cand[c] >> 8;
-        cb = cand[c] & 0xFF;
-      }
-      uint64_t kr_c = shfl_u64(rk, ca);
-      uint64_t kc_c = shfl_u64(ck, cb);
-      CellKey key;
-      key.s = 0ull;
-      key.nn = 0u;
-      if (c < P) {
-        float vr = f32_from_ord((uint32_t)(kr_c >> 32));
-        float vc = f32_from_ord((uint32_t)(kc_c >> 32));
-        uint32_t i = 0xFFFFFFFFu - (uint32_t)kr_c;
-        uint32_t j = 0xFFFFFFFFu - (uint32_t)kc_c;
+        const uint64_t kr_c = rowk[cand[c] >> 8];
+        const uint64_t kc_c = colk[cand[c] & 0xFF];
+        const float vr = f32_from_ord((uint32_t)(kr_c >> 32));
+        const float vc = f32_from_ord((uint32_t)(kc_c >> 32));
+        const uint32_t i = 0xFFFFFFFFu - (uint32_t)kr_c;
+        const uint32_t j = 0xFFFFFFFFu - (uint32_t)kc_c;
         key.s = ord_f64((double)vr + (double)vc);
         key.nn = 0xFFFFFFFFu - (i * (uint32_t)a.nc + j);
       }
-      key = sort_desc_cell(key);
-      best = (base == 0) ? key : merge_desc_cell(best, key);
+      key = sort_cells(key);
+      best = (base == 0) ? key : merge_top64_cells(best, key);
     }
+    wave_lds_sync();
     // Gates: softmax over the K selected scores, best first.
     const double s = f64_from_ord(best.s);
     const double s0 = __shfl(s, 0, kWave);
-    float e = (l < K) ? expf((float)(s - s0)) : 0.0f;
+    const float e = (l < K) ? expf((float)(s - s0)) : 0.0f;
     const float z = wave_sum_f32(e);
     if (l < K) {
       a.idx[row * K + l] = (int32_t)(0xFFFFFFFFu - best.nn);
@@ -237,7 +312,7 @@ hipError_t launch_select(const Shape& s, const float* half_scores, int32_t* idx,
   a.K = s.K;
   const int nmax = s.nr > s.nc ? s.nr : s.nc;
   int64_t blocks = (s.rows + 3) / 4;
-  if (blocks > 4096) blocks = 4096;
+  if (blocks > 8192) blocks = 8192;
   dim3 grid((unsigned)blocks), block(256);
   if (nmax <= 64)
     hipLaunchKernelGGL(select_kernel<1>, grid, block, 0, st, a);

@@ -55,6 +55,14 @@ def test_workspace_size_rejects(field, value, status):
     assert _ws(d)[0] == status
 
 
+def test_wide_fp32_is_unsupported():
+    d = B.make_desc(synth.WORKLOADS["tiny_f32"])
+    d.d = 8192
+    assert _ws(d)[0] == UNSUPPORTED
+    d.dtype = B.OMNIMOE_BF16
+    assert _ws(d)[0] == OK
+
+
 def test_k_above_grid_is_invalid():
     d = B.make_desc(synth.WORKLOADS["tiny_f32"])
     d.n_rows, d.n_cols, d.K = 2, 3, 7

@@ -43,6 +43,10 @@ SHAPES = {
                                   H=2, K=9, dtype="f32"),
     "all_experts_bf16": synth.Workload("all_experts_bf16", T=64, d=128, n_rows=4, n_cols=4,
                                        d_key=64, H=2, K=16),
+    "wide_bf16": synth.Workload("wide_bf16", T=70, d=8192, n_rows=16, n_cols=32, d_key=64, H=2,
+                                K=8),
+    "wide_f32": synth.Workload("wide_f32", T=70, d=4096, n_rows=32, n_cols=16, d_key=2048, H=1,
+                               K=5, dtype="f32"),
 }
 
 
@@ -186,7 +190,8 @@ def test_schedule_bitexact(case):
 # ------------------------------------------------------------------ expert compute
 
 @pytest.mark.parametrize("name", ["tiny_f32", "small_bf16", "ragged_bf16", "ragged_f32",
-                                  "silu_k1_bf16", "k64_bf16", "all_experts_bf16"])
+                                  "silu_k1_bf16", "k64_bf16", "all_experts_bf16", "wide_bf16",
+                                  "wide_f32"])
 def test_expert_forward(name):
     w = SHAPES[name]
     say(f"[expert] {name}")
