@@ -116,6 +116,9 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=2048, help="tokens for the oracle leg")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle leg")
     ap.add_argument("--out", default=None, help="also write the JSON line here")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="after timing, run a plain device copy of this many bytes twice "
+                         "(a known-size reference for rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this layer runs on a single MI355X and has no "
@@ -212,6 +215,16 @@ def main():
                 "unit": kd["unit"], "frac": kd["frac"], "traffic": traffic,
                 "ms_per_launch": per[dom]}
     log("per kernel: " + ", ".join(f"{k} {v:.3f} ms" for k, v in per.items()))
+
+    if args.copy_bytes > 0:
+        n = args.copy_bytes // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copied {n * 4} bytes twice")
+        del src, dst
 
     cpu = None
     if not args.no_cpu:

@@ -27,7 +27,7 @@ def build(verbose: bool = False) -> str:
                         if "packed-fp32-ops' is not a recognized feature" not in l)
         if r.returncode != 0:
             raise RuntimeError(f"hipcc failed on {src}:\n{err}")
-        if err.strip() and verbose:
+        if verbose and err.strip():
             print(err)
         return obj
 

@@ -54,7 +54,7 @@ __device__ __forceinline__ float dot2_bf16(uint32_t p, uint32_t q, float acc) {
 // fp32 dot of one 16-byte chunk pair (bf16 pairs through v_dot2_f32_bf16).
 template <bool BF16>
 __device__ __forceinline__ float chunk_dot(const uint4& p, const uint4& q, float acc) {
-  if (BF16) {
+  if constexpr (BF16) {
     acc = dot2_bf16(p.x, q.x, acc);
     acc = dot2_bf16(p.y, q.y, acc);
     acc = dot2_bf16(p.z, q.z, acc);
@@ -230,7 +230,7 @@ __global__ __launch_bounds__(256) void accumulate_kernel(AccArgs a) {
 #pragma unroll
             for (int q = 0; q < CPL; ++q) {
               const uint4 c = vr[u][q];
-              if (BF16) {
+              if constexpr (BF16) {
                 acc[q][0] = fmaf(w, bf16_lo(c.x), acc[q][0]);
                 acc[q][1] = fmaf(w, bf16_hi(c.x), acc[q][1]);
                 acc[q][2] = fmaf(w, bf16_lo(c.y), acc[q][2]);

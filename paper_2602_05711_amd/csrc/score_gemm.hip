@@ -14,6 +14,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 struct ScoreArgs {
   const void* x;
@@ -144,6 +145,140 @@ __global__ __launch_bounds__(256) void score_bf16_kernel(ScoreArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- large-tile bf16 kernel
+// 256 x 256 macro tile, four waves of 128 x 128 (8 x 8 MFMA tiles, accumulators in AGPRs),
+// k-step 64, two LDS stages filled straight from global memory (global_load_lds_dwordx4, no
+// register staging). LDS rows are 128 B (64 bf16); the 16-byte chunk j of row r is stored at
+// position j ^ ((r >> 1) & 7), so the 16 rows read by one MFMA operand load fall in distinct
+// banks. Requires d_key % 64 == 0; tails in T and in the key count are handled by clamping the
+// row that is loaded (those rows are never stored).
+
+constexpr int LM = 256, LN = 256, LK = 64;
+constexpr int LROW = LK * 2;                 // bytes per LDS row
+constexpr int LSTAGE = (LM + LN) * LROW;      // bytes per stage: 64 KiB
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
+
+__device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+
+__global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
+  const int half = blockIdx.z;
+  const int ncols = a.H * a.nh[half];
+  const int n0 = blockIdx.x * LN;
+  if (n0 >= ncols) return;
+  const int64_t m0 = (int64_t)blockIdx.y * LM;
+  const uint16_t* X = (const uint16_t*)a.x;
+  const uint16_t* Kt = (const uint16_t*)a.keys[half];
+  const int c0 = a.col0[half];
+
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wid = tid >> 6;
+  const int wm = wid >> 1, wn = wid & 1;
+
+  // Loader: instruction i (0..7) of wave w covers rows 8 (8 w + i) .. +8 of A and of B; lane l
+  // fills LDS position l % 8 of row l / 8, i.e. global chunk (l % 8) ^ swz(row).
+  const uint16_t* ga[8];
+  const uint16_t* gb[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int r = (wid * 8 + i) * 8 + (lane >> 3);
+    const int j = (lane & 7) ^ swz(r);
+    int64_t gm = m0 + r;
+    if (gm >= a.T) gm = a.T - 1;
+    int gn = n0 + r;
+    if (gn >= ncols) gn = ncols - 1;
+    ga[i] = X + gm * a.d + c0 + j * 8;
+    gb[i] = Kt + (int64_t)gn * a.dk + j * 8;
+  }
+  auto issue = [&](int stage, int k0) {
+    unsigned char* base = smem + stage * LSTAGE;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      unsigned char* la = base + (wid * 8 + i) * 8 * LROW;
+      unsigned char* lb = base + LM * LROW + (wid * 8 + i) * 8 * LROW;
+      __builtin_amdgcn_global_load_lds((const void*)(ga[i] + k0), (lds_ptr_t)la, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const void*)(gb[i] + k0), (lds_ptr_t)lb, 16, 0, 0);
+    }
+  };
+
+  // v_mfma_f32_32x32x16_bf16: lane l holds row (l % 32) of the A operand (column of B) and k
+  // values 8 (l / 32) .. +7 of a 16-wide k step; accumulator register q of a 32 x 32 tile is
+  // row 8 (q / 4) + 4 (l / 32) + q % 4, column l % 32.
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
+
+  const int KT = a.dk / LK;
+  issue(0, 0);
+  wait_vm0();
+  __syncthreads();
+
+  const int frow = lane & 31;
+  const int fk = lane >> 5;  // 16-byte chunk within a 16-wide k step
+  int a_off[4], b_off[4];    // LDS row offsets of this lane's operand rows
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    a_off[i] = (wm * 128 + i * 32 + frow) * LROW;
+    b_off[i] = LM * LROW + (wn * 128 + i * 32 + frow) * LROW;
+  }
+  const int sw = swz(frow);  // rows i * 32 + frow share (r >> 1) & 7 with frow
+  auto frag = [&](const unsigned char* st, int off, int ks) -> bf16x8 {
+    return *(const bf16x8*)(st + off + (((ks * 2 + fk) ^ sw) << 4));
+  };
+  for (int kt = 0; kt < KT; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < KT) issue(cur ^ 1, (kt + 1) * LK);
+    const unsigned char* st = smem + cur * LSTAGE;
+    bf16x8 fa[2][4], fb[2][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      fa[0][i] = frag(st, a_off[i], 0);
+      fb[0][i] = frag(st, b_off[i], 0);
+    }
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int c = ks & 1;
+      if (ks + 1 < 4) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          fa[c ^ 1][i] = frag(st, a_off[i], ks + 1);
+          fb[c ^ 1][i] = frag(st, b_off[i], ks + 1);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[c][i], fb[c][j], acc[i][j], 0, 0, 0);
+    }
+    wait_vm0();
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int n = n0 + wn * 128 + j * 32 + (lane & 31);
+    if (n >= ncols) continue;
+    const int64_t oc = out_col(a, half, n);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int64_t m = m0 + wm * 128 + i * 32 + (q >> 2) * 8 + (lane >> 5) * 4 + (q & 3);
+        if (m < a.T) a.out[m * a.ldo + oc] = acc[i][j][q];
+      }
+    }
+  }
+}
+
 constexpr int FT = 64, FK = 16;
 
 __global__ __launch_bounds__(256) void score_f32_kernel(ScoreArgs a) {
@@ -219,7 +354,10 @@ hipError_t launch_score(const Shape& s, const void* x, const void* keys_row,
   a.per_head = s.nr + s.nc;
   a.ldo = (int64_t)s.H * (s.nr + s.nc);
   const int ncols = s.H * (s.nr > s.nc ? s.nr : s.nc);
-  if (s.bf16) {
+  if (s.bf16 && s.dk % LK == 0) {
+    dim3 grid((ncols + LN - 1) / LN, (unsigned)((s.T + LM - 1) / LM), 2);
+    hipLaunchKernelGGL(score_bf16_large_kernel, grid, dim3(256), 2 * LSTAGE, st, a);
+  } else if (s.bf16) {
     dim3 grid((ncols + BN - 1) / BN, (unsigned)((s.T + BM - 1) / BM), 2);
     hipLaunchKernelGGL(score_bf16_kernel, grid, dim3(256), 0, st, a);
   } else {
