@@ -142,9 +142,10 @@ WORKLOADS: Dict[str, Workload] = {
     "train_bf16": Workload("train_bf16", T=16384, d=2048, n_rows=1024, n_cols=1024, d_key=1024,
                            H=8, K=16),
     # As train_bf16, with sub-key rows scaled so that about 10% of the experts take about half
-    # of the (token, expert) pairs. The exponent was set by tests/golden/calibrate_skew.py.
+    # of the (token, expert) pairs: alpha = 0.080078125 routes 50.3% of the pairs to the top 10%
+    # (tests/golden/calibrate_skew.py, result in tests/golden/skew_calibration.json).
     "skew_bf16": Workload("skew_bf16", T=16384, d=2048, n_rows=1024, n_cols=1024, d_key=1024,
-                          H=8, K=16, skew_alpha=0.0),
+                          H=8, K=16, skew_alpha=0.080078125),
     # One decode step of a batch of 64, and a single token.
     "decode64_bf16": Workload("decode64_bf16", T=64, d=2048, n_rows=1024, n_cols=1024,
                               d_key=1024, H=8, K=16),

@@ -336,6 +336,22 @@ def test_train_shape_sampled(train_tables):
     assert np.isfinite(y).all()
 
 
+def test_skewed_shape_sampled(train_tables):
+    # Same expert tables as the training shape (same seed and streams), skewed sub-keys.
+    dev, _, _ = train_tables
+    w = W["skew_bf16"]
+    say("[full] skew_bf16 T=16384")
+    kr, kc = synth.make_keys(w)
+    dev = dict(dev, keys_row=to_dev(kr), keys_col=to_dev(kc))
+    rng = np.random.default_rng(1)
+    tokens = np.unique(np.concatenate([[0, w.T - 1], rng.choice(w.T, 46, replace=False)]))
+    y, idx = _sampled_parity(w, dev, synth.as_f32(kr), synth.as_f32(kc), tokens)
+    counts = np.bincount(idx.ravel(), minlength=w.N)
+    share = np.sort(counts)[::-1][: w.N // 10].sum() / idx.size
+    say(f"  top-10% share {share:.4f}, active {int((counts > 0).sum())}, max {counts.max()}")
+    assert abs(share - 0.50) < 0.02
+
+
 @pytest.mark.parametrize("name", ["decode64_bf16", "decode1_bf16"])
 def test_decode_shapes(train_tables, name):
     dev, kr, kc = train_tables

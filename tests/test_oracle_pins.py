@@ -52,6 +52,24 @@ def test_synth_is_counter_based_and_normalish():
     assert np.array_equal(x1[[3, 7]], x2)
 
 
+def test_skew_scale_recipe(golden_dir):
+    # Row scales: a power law in the seeded rank, normalised to mean square 1, same for every
+    # head; the calibrated exponent is the one the workload table carries.
+    w = synth.WORKLOADS["skew_bf16"]
+    c = synth.skew_row_scale(w, w.n_rows, synth.STREAM_PERM_ROW)
+    assert c.shape == (w.H * w.n_rows,)
+    one = c[: w.n_rows]
+    np.testing.assert_allclose(np.mean(one ** 2), 1.0, rtol=1e-12)
+    assert np.array_equal(np.tile(one, w.H), c)
+    pi = synth.seeded_permutation(w.seed, synth.STREAM_PERM_ROW, w.n_rows)
+    assert np.array_equal(np.sort(pi), np.arange(w.n_rows))
+    assert np.all(np.diff(one[np.argsort(pi)]) < 0)  # rank 0 is the hottest row
+    cal = _load(golden_dir, "skew_calibration.json")
+    assert cal["chosen"]["alpha"] == w.skew_alpha
+    assert abs(cal["chosen"]["top10_share"] - 0.5) <= cal["tolerance"]
+    assert synth.skew_row_scale(synth.WORKLOADS["train_bf16"], 1024, 6) is None
+
+
 # ---------------------------------------------------------------- activation (Eq. 4)
 
 def test_activation_values(golden_dir):
