@@ -169,30 +169,58 @@ __device__ __forceinline__ uint32_t kth_largest_lane(uint32_t v, int k) {
   return th;
 }
 
-// Loads one half, finds its threshold and writes the survivors' keys to buf[0, 32).
-// Returns the number of survivors (those beyond 32 are not written).
-template <int R>
-__device__ __forceinline__ int half_survivors(const float* __restrict__ p, int n, int kh,
-                                              uint64_t* buf, uint32_t* theta_out) {
-  const int l = lane_id();
+// Logits of one half held in registers. VEC: lane l holds 16-byte chunks, element
+// j = 256 (k / 4) + 4 l + k % 4 (needs n % 4 == 0 and 16-byte aligned rows); otherwise element
+// j = l + 64 k. Positions past n hold garbage and are masked by index.
+template <int R, bool VEC>
+__device__ __forceinline__ int elem_index(int k) {
+  return VEC ? 256 * (k >> 2) + 4 * lane_id() + (k & 3) : lane_id() + kWave * k;
+}
+
+template <int R, bool VEC>
+__device__ __forceinline__ void load_half(const float* __restrict__ p, int n, float (&v)[R]) {
+  if constexpr (VEC) {
+#pragma unroll
+    for (int c = 0; c < R / 4; ++c) {
+      const int j0 = 256 * c + 4 * lane_id();
+      float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (j0 < n) t = *(const float4*)(p + j0);
+      v[4 * c] = t.x;
+      v[4 * c + 1] = t.y;
+      v[4 * c + 2] = t.z;
+      v[4 * c + 3] = t.w;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+      const int j = elem_index<R, VEC>(k);
+      v[k] = j < n ? p[j] : 0.f;
+    }
+  }
+}
+
+// Finds one half's threshold and writes the survivors' keys to buf[0, 32). Returns the number
+// of survivors (those beyond 32 are not written).
+template <int R, bool VEC>
+__device__ __forceinline__ int half_survivors(const float (&v)[R], int n, int kh, uint64_t* buf,
+                                              uint32_t* theta_out) {
   uint32_t o[R];
   uint32_t mx = 0u;
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int j = l + kWave * r;
-    o[r] = (j < n) ? ord_f32(p[j]) : 0u;  // 0 sits below every finite value
-    mx = o[r] > mx ? o[r] : mx;
+  for (int k = 0; k < R; ++k) {
+    o[k] = (elem_index<R, VEC>(k) < n) ? ord_f32(v[k]) : 0u;  // 0 sits below every finite value
+    mx = o[k] > mx ? o[k] : mx;
   }
   const uint32_t theta = kth_largest_lane(mx, kh);
   *theta_out = theta;
   const uint64_t lt = lanemask_lt();
   int base = 0;
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const bool f = o[r] >= theta;
+  for (int k = 0; k < R; ++k) {
+    const bool f = o[k] >= theta;
     const uint64_t bal = __ballot(f);
     const int pos = base + __popcll(bal & lt);
-    if (f && pos < 32) buf[pos] = logit_key(o[r], l + kWave * r);
+    if (f && pos < 32) buf[pos] = logit_key(o[k], elem_index<R, VEC>(k));
     base += __popcll(bal);
   }
   return base;
@@ -220,7 +248,7 @@ __device__ __noinline__ uint64_t half_topk_batched(const float* __restrict__ p, 
   return best;
 }
 
-template <int R>
+template <int R, bool VEC>
 __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
   __shared__ uint16_t cand[kMaxCand];  // (a << 8) | b
   __shared__ int n_cand;
@@ -244,11 +272,24 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
   uint64_t* colk = lists[w][1];
   uint64_t* st = stage[w];
   const int64_t stride = (int64_t)gridDim.x * 4;
-  for (int64_t row = (int64_t)blockIdx.x * 4 + w; row < a.rows; row += stride) {
+  int64_t row = (int64_t)blockIdx.x * 4 + w;
+  // The next row's logits are loaded while the current row is processed.
+  float vr[R], vc[R];
+  if (row < a.rows) {
+    load_half<R, VEC>(a.hs + row * (int64_t)(a.nr + a.nc), a.nr, vr);
+    load_half<R, VEC>(a.hs + row * (int64_t)(a.nr + a.nc) + a.nr, a.nc, vc);
+  }
+  for (; row < a.rows; row += stride) {
     const float* hr = a.hs + row * (int64_t)(a.nr + a.nc);
+    float nr_[R], nc_[R];
+    const int64_t nxt = row + stride;
+    if (nxt < a.rows) {
+      load_half<R, VEC>(a.hs + nxt * (int64_t)(a.nr + a.nc), a.nr, nr_);
+      load_half<R, VEC>(a.hs + nxt * (int64_t)(a.nr + a.nc) + a.nr, a.nc, nc_);
+    }
     uint32_t th_r, th_c;
-    const int cr = half_survivors<R>(hr, a.nr, kr, st, &th_r);
-    const int cc = half_survivors<R>(hr + a.nr, a.nc, kc, st + 32, &th_c);
+    const int cr = half_survivors<R, VEC>(vr, a.nr, kr, st, &th_r);
+    const int cc = half_survivors<R, VEC>(vc, a.nc, kc, st + 32, &th_c);
     wave_lds_sync();
     if (cr <= 32 && cc <= 32) {
       // Both halves in one pass: rows sort in lanes 0-31, columns in lanes 32-63.
@@ -294,6 +335,11 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
       a.idx[row * K + l] = (int32_t)(0xFFFFFFFFu - best.nn);
       a.gates[row * K + l] = e / z;
     }
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+      vr[k] = nr_[k];
+      vc[k] = nc_[k];
+    }
   }
 }
 
@@ -314,20 +360,22 @@ hipError_t launch_select(const Shape& s, const float* half_scores, int32_t* idx,
   int64_t blocks = (s.rows + 3) / 4;
   if (blocks > 8192) blocks = 8192;
   dim3 grid((unsigned)blocks), block(256);
-  if (nmax <= 64)
-    hipLaunchKernelGGL(select_kernel<1>, grid, block, 0, st, a);
-  else if (nmax <= 128)
-    hipLaunchKernelGGL(select_kernel<2>, grid, block, 0, st, a);
-  else if (nmax <= 256)
-    hipLaunchKernelGGL(select_kernel<4>, grid, block, 0, st, a);
-  else if (nmax <= 512)
-    hipLaunchKernelGGL(select_kernel<8>, grid, block, 0, st, a);
-  else if (nmax <= 1024)
-    hipLaunchKernelGGL(select_kernel<16>, grid, block, 0, st, a);
-  else if (nmax <= 2048)
-    hipLaunchKernelGGL(select_kernel<32>, grid, block, 0, st, a);
-  else
-    hipLaunchKernelGGL(select_kernel<64>, grid, block, 0, st, a);
+  const bool vec = s.nr % 4 == 0 && s.nc % 4 == 0;
+#define OMNIMOE_SELECT(R)                                                              \
+  do {                                                                                 \
+    if (vec && (R) >= 4)                                                               \
+      hipLaunchKernelGGL((select_kernel<(R), true>), grid, block, 0, st, a);           \
+    else                                                                               \
+      hipLaunchKernelGGL((select_kernel<(R), false>), grid, block, 0, st, a);          \
+  } while (0)
+  if (nmax <= 64) OMNIMOE_SELECT(1);
+  else if (nmax <= 128) OMNIMOE_SELECT(2);
+  else if (nmax <= 256) OMNIMOE_SELECT(4);
+  else if (nmax <= 512) OMNIMOE_SELECT(8);
+  else if (nmax <= 1024) OMNIMOE_SELECT(16);
+  else if (nmax <= 2048) OMNIMOE_SELECT(32);
+  else OMNIMOE_SELECT(64);
+#undef OMNIMOE_SELECT
   return hipGetLastError();
 }
 
