@@ -116,6 +116,8 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=2048, help="tokens for the oracle leg")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle leg")
     ap.add_argument("--out", default=None, help="also write the JSON line here")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of one layer call captured in a HIP graph")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="after timing, run a plain device copy of this many bytes twice "
                          "(a known-size reference for rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -159,6 +161,23 @@ def main():
         step()
     torch.cuda.synchronize()
     log(f"warmup {args.warmup} done")
+    if args.graph:
+        # One layer call captured once (the library allocates nothing and never synchronises
+        # inside a call), then replayed as the timed step.
+        graph = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(stream)
+        with torch.cuda.stream(cap):
+            with torch.cuda.graph(graph, stream=cap):
+                P.omnimoe_layer_forward(desc, d_in["x"], d_in["keys_row"], d_in["keys_col"],
+                                        d_in["u"], d_in["v"], y, ws=ws, stream=cap)
+        stream.wait_stream(cap)
+        torch.cuda.synchronize()
+        step = graph.replay  # noqa: F811
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        log("captured the layer call in a graph")
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
@@ -240,7 +259,7 @@ def main():
         "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": w.name, "T": w.T, "d": w.d, "n_rows": w.n_rows,
                    "n_cols": w.n_cols, "N": w.N, "d_key": w.d_key, "H": w.H, "K": w.K,
-                   "act": w.act, "query": w.query_mode},
+                   "act": w.act, "query": w.query_mode, "graph": bool(args.graph)},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "n_active": n_active, "eta": w.M / max(1, n_active),

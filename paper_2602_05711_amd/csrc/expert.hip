@@ -30,6 +30,7 @@ struct DotArgs {
   int hk;
   int act;
   int nchunks;  // 16-byte chunks per row
+  int range;    // nominal tasks per wave (power of two <= 64)
 };
 
 struct AccArgs {
@@ -42,6 +43,7 @@ struct AccArgs {
   int d;
   int hk;
   int nchunks;
+  int splits;  // waves per token; wave c of a token owns chunk rows [c CPL, (c + 1) CPL)
 };
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -82,19 +84,20 @@ __device__ __forceinline__ int key_at(const DotArgs& a, int64_t pos) {
   return clamp_i(a.sk ? a.sk[pos] : a.idx[task_at(a, pos)], a.N);
 }
 
-// First position of wave range `lo / 64`: the first expert boundary in [lo, lo + 64), or
-// lo + 64 when the window lies inside one expert's run.
+// First position of the wave range starting near lo: the first expert boundary in
+// [lo, lo + range), or lo + range when that window lies inside one expert's run.
 __device__ int64_t range_start(const DotArgs& a, int64_t lo) {
   if (lo >= a.M) return a.M;
   const int l = lane_id();
   const int64_t pos = lo + l;
-  const int key = pos < a.M ? key_at(a, pos) : -1;
+  const bool in = l < a.range && pos < a.M;
+  const int key = in ? key_at(a, pos) : -1;
   const int before = lo > 0 ? key_at(a, lo - 1) : -1;
   int prev = __shfl_up(key, 1, kWave);
   if (l == 0) prev = before;
-  const uint64_t heads = __ballot(pos < a.M && key != prev);
+  const uint64_t heads = __ballot(in && key != prev);
   if (heads) return lo + (__ffsll((unsigned long long)heads) - 1);
-  const int64_t nx = lo + kWave;
+  const int64_t nx = lo + a.range;
   return nx < a.M ? nx : a.M;
 }
 
@@ -113,8 +116,8 @@ __global__ __launch_bounds__(256) void expert_dot_kernel(DotArgs a) {
   constexpr int G = CPL >= 16 ? 1 : (CPL >= 8 ? 2 : 4);
   const int l = lane_id();
   const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int64_t s = range_start(a, wave * kWave);
-  const int64_t e = range_start(a, (wave + 1) * kWave);
+  const int64_t s = range_start(a, wave * a.range);
+  const int64_t e = range_start(a, (wave + 1) * a.range);
   if (s >= e) return;
   const uint4* X = (const uint4*)a.x;
   const uint4* U = (const uint4*)a.u;
@@ -195,11 +198,14 @@ __global__ __launch_bounds__(256) void accumulate_kernel(AccArgs a) {
   const int l = lane_id();
   const uint4* V = (const uint4*)a.v;
   const int64_t row_chunks = a.nchunks;
-  bool cvalid[CPL];
-#pragma unroll
-  for (int q = 0; q < CPL; ++q) cvalid[q] = (l + kWave * q) < a.nchunks;
   const int64_t stride = (int64_t)gridDim.x * 4;
-  for (int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < a.T; t += stride) {
+  for (int64_t wt = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); wt < a.T * a.splits;
+       wt += stride) {
+    const int64_t t = wt / a.splits;
+    const int cbase = (int)(wt % a.splits) * CPL * kWave;  // first chunk of this wave
+    bool cvalid[CPL];
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) cvalid[q] = (cbase + l + kWave * q) < a.nchunks;
     float acc[CPL][EPC];
 #pragma unroll
     for (int q = 0; q < CPL; ++q)
@@ -217,7 +223,7 @@ __global__ __launch_bounds__(256) void accumulate_kernel(AccArgs a) {
         for (int u = 0; u < UNROLL; ++u) {
           if (j + u < n) {
             const int e = readlane_i32(ev, j + u);
-            const uint4* vb = V + (int64_t)e * row_chunks;
+            const uint4* vb = V + (int64_t)e * row_chunks + cbase;
 #pragma unroll
             for (int q = 0; q < CPL; ++q)
               vr[u][q] = cvalid[q] ? vb[l + kWave * q] : make_uint4(0, 0, 0, 0);
@@ -254,11 +260,107 @@ __global__ __launch_bounds__(256) void accumulate_kernel(AccArgs a) {
 #pragma unroll
     for (int q = 0; q < CPL; ++q) {
       if (!cvalid[q]) continue;
-      const int c = l + kWave * q;
+      const int c = cbase + l + kWave * q;
 #pragma unroll
       for (int k = 0; k < EPC; k += 4)
         yt[(c * EPC + k) / 4] = make_float4(acc[q][k], acc[q][k + 1], acc[q][k + 2], acc[q][k + 3]);
     }
+  }
+}
+
+// Few tokens: a workgroup owns one (token, column split) and its four waves take a quarter of
+// the token's slots each; the three later quarters' partial sums go through LDS and wave 0 adds
+// them in wave order, so the per-element order is fixed.
+template <int CPL, bool BF16>
+__global__ __launch_bounds__(256) void accumulate_slots_kernel(AccArgs a) {
+  constexpr int EPC = BF16 ? 8 : 4;
+  constexpr int UNROLL = CPL >= 16 ? 2 : (CPL >= 8 ? 4 : 8);
+  __shared__ float part[3][CPL * EPC * kWave];
+  const int l = lane_id(), w = threadIdx.x >> 6;
+  const uint4* V = (const uint4*)a.v;
+  const int64_t row_chunks = a.nchunks;
+  const int quarter = (a.hk + 3) / 4;
+  const int s_lo = w * quarter;
+  const int s_hi = s_lo + quarter < a.hk ? s_lo + quarter : a.hk;
+  for (int64_t u = blockIdx.x; u < a.T * a.splits; u += gridDim.x) {
+    const int64_t t = u / a.splits;
+    const int cbase = (int)(u % a.splits) * CPL * kWave;
+    bool cvalid[CPL];
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) cvalid[q] = (cbase + l + kWave * q) < a.nchunks;
+    float acc[CPL][EPC];
+#pragma unroll
+    for (int q = 0; q < CPL; ++q)
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) acc[q][k] = 0.0f;
+    for (int sb = s_lo; sb < s_hi; sb += kWave) {
+      const int sl = sb + l;
+      const bool valid = sl < s_hi;
+      const int ev = valid ? clamp_i(a.idx[t * a.hk + sl], a.N) : 0;
+      const float av = valid ? a.a[t * a.hk + sl] : 0.0f;
+      const int n = s_hi - sb < kWave ? s_hi - sb : kWave;
+      for (int j = 0; j < n; j += UNROLL) {
+        uint4 vr[UNROLL][CPL];
+#pragma unroll
+        for (int uu = 0; uu < UNROLL; ++uu) {
+          if (j + uu < n) {
+            const uint4* vb = V + (int64_t)readlane_i32(ev, j + uu) * row_chunks + cbase;
+#pragma unroll
+            for (int q = 0; q < CPL; ++q)
+              vr[uu][q] = cvalid[q] ? vb[l + kWave * q] : make_uint4(0, 0, 0, 0);
+          }
+        }
+#pragma unroll
+        for (int uu = 0; uu < UNROLL; ++uu) {
+          if (j + uu < n) {
+            const float wgt = readlane_f32(av, j + uu);
+#pragma unroll
+            for (int q = 0; q < CPL; ++q) {
+              const uint4 c = vr[uu][q];
+              if constexpr (BF16) {
+                acc[q][0] = fmaf(wgt, bf16_lo(c.x), acc[q][0]);
+                acc[q][1] = fmaf(wgt, bf16_hi(c.x), acc[q][1]);
+                acc[q][2] = fmaf(wgt, bf16_lo(c.y), acc[q][2]);
+                acc[q][3] = fmaf(wgt, bf16_hi(c.y), acc[q][3]);
+                acc[q][4] = fmaf(wgt, bf16_lo(c.z), acc[q][4]);
+                acc[q][5] = fmaf(wgt, bf16_hi(c.z), acc[q][5]);
+                acc[q][6] = fmaf(wgt, bf16_lo(c.w), acc[q][6]);
+                acc[q][7] = fmaf(wgt, bf16_hi(c.w), acc[q][7]);
+              } else {
+                acc[q][0] = fmaf(wgt, __uint_as_float(c.x), acc[q][0]);
+                acc[q][1] = fmaf(wgt, __uint_as_float(c.y), acc[q][1]);
+                acc[q][2] = fmaf(wgt, __uint_as_float(c.z), acc[q][2]);
+                acc[q][3] = fmaf(wgt, __uint_as_float(c.w), acc[q][3]);
+              }
+            }
+          }
+        }
+      }
+    }
+    if (w > 0) {
+#pragma unroll
+      for (int q = 0; q < CPL; ++q)
+#pragma unroll
+        for (int k = 0; k < EPC; ++k) part[w - 1][(q * EPC + k) * kWave + l] = acc[q][k];
+    }
+    __syncthreads();
+    if (w == 0) {
+      float4* yt = (float4*)(a.y + t * a.d);
+#pragma unroll
+      for (int q = 0; q < CPL; ++q) {
+        if (!cvalid[q]) continue;
+        float r[EPC];
+#pragma unroll
+        for (int k = 0; k < EPC; ++k) {
+          const int o = (q * EPC + k) * kWave + l;
+          r[k] = ((acc[q][k] + part[0][o]) + part[1][o]) + part[2][o];
+        }
+        const int c = cbase + l + kWave * q;
+#pragma unroll
+        for (int k = 0; k < EPC; k += 4) yt[(c * EPC + k) / 4] = make_float4(r[k], r[k + 1], r[k + 2], r[k + 3]);
+      }
+    }
+    __syncthreads();
   }
 }
 
@@ -270,6 +372,18 @@ hipError_t dispatch_dot(int cpl, dim3 grid, hipStream_t st, const DotArgs& a) {
     case 4: hipLaunchKernelGGL((expert_dot_kernel<4, BF16>), grid, dim3(256), 0, st, a); break;
     case 8: hipLaunchKernelGGL((expert_dot_kernel<8, BF16>), grid, dim3(256), 0, st, a); break;
     default: hipLaunchKernelGGL((expert_dot_kernel<16, BF16>), grid, dim3(256), 0, st, a); break;
+  }
+  return hipGetLastError();
+}
+
+template <bool BF16>
+hipError_t dispatch_acc_slots(int cpl, dim3 grid, hipStream_t st, const AccArgs& a) {
+  switch (cpl) {
+    case 1: hipLaunchKernelGGL((accumulate_slots_kernel<1, BF16>), grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((accumulate_slots_kernel<2, BF16>), grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((accumulate_slots_kernel<4, BF16>), grid, dim3(256), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((accumulate_slots_kernel<8, BF16>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((accumulate_slots_kernel<16, BF16>), grid, dim3(256), 0, st, a); break;
   }
   return hipGetLastError();
 }
@@ -313,7 +427,10 @@ hipError_t launch_expert_dot(const Shape& s, const void* x, const void* u, const
   a.hk = s.hk;
   a.act = s.act;
   a.nchunks = s.bf16 ? s.d / 8 : s.d / 4;
-  const int64_t waves = (s.M + kWave - 1) / kWave;
+  // About 64 tasks per wave when there are plenty; fewer (down to 16) so that small batches
+  // still spread over the GPU.
+  a.range = s.M >= 131072 ? 64 : (s.M >= 65536 ? 32 : 16);
+  const int64_t waves = (s.M + a.range - 1) / a.range;
   dim3 grid((unsigned)((waves + 3) / 4));
   const int cpl = chunks_per_lane(a.nchunks);
   return s.bf16 ? dispatch_dot<true>(cpl, grid, st, a) : dispatch_dot<false>(cpl, grid, st, a);
@@ -332,9 +449,21 @@ hipError_t launch_accumulate(const Shape& s, const void* v, const int32_t* idx, 
   a.d = s.d;
   a.hk = s.hk;
   a.nchunks = s.bf16 ? s.d / 8 : s.d / 4;
-  int64_t blocks = (s.T + 3) / 4;
+  // Few tokens: split each token's row over several waves (whole 64-chunk rows each).
+  const int rows64 = (a.nchunks + kWave - 1) / kWave;
+  int splits = 1;
+  while (splits < rows64 && s.T * splits < 1024 && rows64 % (splits * 2) == 0) splits *= 2;
+  a.splits = splits;
+  const int cpl = chunks_per_lane((a.nchunks + splits - 1) / splits);
+  if (s.T * splits < 1024 && s.hk >= 16) {
+    // still few waves: a workgroup per (token, column split), slots shared by its four waves
+    const int64_t units = s.T * splits;
+    const dim3 grid((unsigned)(units < 16384 ? units : 16384));
+    return s.bf16 ? dispatch_acc_slots<true>(cpl, grid, st, a)
+                  : dispatch_acc_slots<false>(cpl, grid, st, a);
+  }
+  int64_t blocks = (s.T * splits + 3) / 4;
   if (blocks > 16384) blocks = 16384;
-  const int cpl = chunks_per_lane(a.nchunks);
   return s.bf16 ? dispatch_acc<true>(cpl, dim3((unsigned)blocks), st, a)
                 : dispatch_acc<false>(cpl, dim3((unsigned)blocks), st, a);
 }

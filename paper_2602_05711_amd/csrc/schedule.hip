@@ -192,12 +192,19 @@ __global__ __launch_bounds__(kThreads) void radix_downsweep_kernel(RadixPass p) 
   const int64_t wbase = (int64_t)blockIdx.x * kTile + (int64_t)w * (kTile / 4);
   const uint64_t lt = lanemask_lt();
   int key[kItems], val[kItems], rank[kItems];
+  // All loads first: the LDS fences of the ranking rounds would otherwise hold each round's
+  // loads back until the previous round finished.
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
     const int64_t i = wbase + (int64_t)r * kWave + l;
     const bool valid = i < p.n;
     key[r] = valid ? p.keys_in[i] : 0;
     val[r] = valid ? (p.vals_in ? p.vals_in[i] : (int)i) : 0;
+  }
+#pragma unroll
+  for (int r = 0; r < kItems; ++r) {
+    const int64_t i = wbase + (int64_t)r * kWave + l;
+    const bool valid = i < p.n;
     const uint32_t d = ((uint32_t)key[r] >> p.shift) & mask;
     uint64_t peers = __ballot(valid);
     for (int b = 0; b < p.bits; ++b) {
@@ -278,6 +285,155 @@ int digit_bits_total(int64_t n_experts) {
 
 }  // namespace
 
+// ---------------------------------------------------------------- small task counts
+// One workgroup of 16 waves sorts up to 8192 tasks and extracts the segments in a single
+// launch (decode shapes). Same algorithm as the multi-kernel path: per pass, wave w ranks its
+// contiguous slice of tasks stably with ballot-matched peers and per-wave digit counters, the
+// (digit, wave) counts are scanned digit-major, and tasks scatter; then segment heads are
+// counted and compacted with a block scan.
+
+constexpr int kSmallWaves = 16;
+constexpr int kSmallThreads = kSmallWaves * kWave;
+constexpr int kSmallRounds = 8;
+constexpr int kSmallMax = kSmallThreads * kSmallRounds;  // 8192
+
+struct SmallSched {
+  const int32_t* idx;
+  int32_t* tmp_k[2];
+  int32_t* tmp_v[2];
+  int32_t* perm;
+  int32_t* sorted;  // final keys (one of tmp_k)
+  int32_t* active;
+  int32_t* offsets;
+  int32_t* n_active;
+  int M;
+  int cap;
+  int passes, per, total_bits;
+};
+
+__global__ __launch_bounds__(kSmallThreads) void schedule_small_kernel(SmallSched a) {
+  __shared__ int cnt[kSmallWaves][kMaxRadix];
+  __shared__ int dsum[kMaxRadix];
+  __shared__ int wsum[kSmallWaves];
+  const int tid = threadIdx.x, l = lane_id(), w = tid >> 6;
+  const int slice = (a.M + kSmallWaves - 1) / kSmallWaves;
+  const int wbeg = w * slice;
+  const int wend = wbeg + slice < a.M ? wbeg + slice : a.M;
+  const uint64_t lt = lanemask_lt();
+  const int32_t* kin = a.idx;
+  const int32_t* vin = nullptr;
+  int shift = 0;
+  for (int ps = 0; ps < a.passes; ++ps) {
+    const bool last = ps == a.passes - 1;
+    int bits = a.total_bits - shift;
+    if (bits > a.per) bits = a.per;
+    if (bits < 1) bits = 1;
+    const int radix = 1 << bits;
+    const uint32_t mask = (uint32_t)radix - 1u;
+    int32_t* kout = a.tmp_k[ps & 1];
+    int32_t* vout = last ? a.perm : a.tmp_v[ps & 1];
+    for (int i = tid; i < kSmallWaves * kMaxRadix; i += kSmallThreads) (&cnt[0][0])[i] = 0;
+    __syncthreads();
+    int key[kSmallRounds], val[kSmallRounds], rank[kSmallRounds];
+#pragma unroll
+    for (int r = 0; r < kSmallRounds; ++r) {
+      const int i = wbeg + r * kWave + l;
+      const bool valid = i < wend;
+      key[r] = valid ? kin[i] : 0;
+      val[r] = valid ? (vin ? vin[i] : i) : 0;
+    }
+#pragma unroll
+    for (int r = 0; r < kSmallRounds; ++r) {
+      const int i = wbeg + r * kWave + l;
+      const bool valid = i < wend;
+      const uint32_t d = ((uint32_t)key[r] >> shift) & mask;
+      uint64_t peers = __ballot(valid);
+      for (int b = 0; b < bits; ++b) {
+        const bool bit = (d >> b) & 1u;
+        const uint64_t bal = __ballot(bit);
+        peers &= bit ? bal : ~bal;
+      }
+      const int before = __popcll(peers & lt);
+      const int run = valid ? cnt[w][d] : 0;
+      wave_lds_sync();
+      if (valid && before == 0) cnt[w][d] = run + __popcll(peers);
+      wave_lds_sync();
+      rank[r] = run + before;
+    }
+    __syncthreads();
+    // digit totals, their exclusive scan, then (digit, wave) offsets
+    for (int d = tid; d < radix; d += kSmallThreads) {
+      int t = 0;
+      for (int ww = 0; ww < kSmallWaves; ++ww) t += cnt[ww][d];
+      dsum[d] = t;
+    }
+    __syncthreads();
+    {
+      // exclusive scan of the digit totals: one digit per thread (radix <= 1024 threads)
+      const int v = tid < radix ? dsum[tid] : 0;
+      const int ex = wave_excl_scan_i32(v);
+      if (l == kWave - 1) wsum[w] = ex + v;
+      __syncthreads();
+      int off = 0;
+      for (int ww = 0; ww < w; ++ww) off += wsum[ww];
+      if (tid < radix) dsum[tid] = off + ex;
+    }
+    __syncthreads();
+    for (int d = tid; d < radix; d += kSmallThreads) {
+      int run = dsum[d];
+      for (int ww = 0; ww < kSmallWaves; ++ww) {
+        const int c = cnt[ww][d];
+        cnt[ww][d] = run;
+        run += c;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kSmallRounds; ++r) {
+      const int i = wbeg + r * kWave + l;
+      if (i < wend) {
+        const uint32_t d = ((uint32_t)key[r] >> shift) & mask;
+        const int pos = cnt[w][d] + rank[r];
+        kout[pos] = key[r];
+        vout[pos] = val[r];
+      }
+    }
+    __syncthreads();
+    kin = kout;
+    vin = vout;
+    shift += bits;
+  }
+  // segment heads: each thread owns 8 consecutive sorted positions
+  const int per_t = (a.M + kSmallThreads - 1) / kSmallThreads;
+  const int b0 = tid * per_t;
+  int heads = 0;
+  for (int i = b0; i < b0 + per_t && i < a.M; ++i) heads += (i == 0 || kin[i] != kin[i - 1]);
+  const int ex = wave_excl_scan_i32(heads);
+  if (l == kWave - 1) wsum[w] = ex + heads;
+  __syncthreads();
+  int off = 0, tot = 0;
+  for (int ww = 0; ww < kSmallWaves; ++ww) {
+    const int v = wsum[ww];
+    if (ww < w) off += v;
+    tot += v;
+  }
+  int pos = off + ex;
+  for (int i = b0; i < b0 + per_t && i < a.M; ++i) {
+    if (i == 0 || kin[i] != kin[i - 1]) {
+      if (pos < a.cap) {
+        a.active[pos] = kin[i];
+        a.offsets[pos] = i;
+      }
+      ++pos;
+    }
+  }
+  if (tid == 0) {
+    const int n = tot < a.cap ? tot : a.cap;
+    *a.n_active = n;
+    a.offsets[n] = a.M;
+  }
+}
+
 hipError_t launch_fill_i32(int32_t* dst, int64_t n, int32_t value, hipStream_t st) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(fill_i32_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)),
@@ -314,6 +470,33 @@ hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, in
   const int total_bits = digit_bits_total(s.N);
   const int passes = total_bits == 0 ? 1 : (total_bits + kMaxDigitBits - 1) / kMaxDigitBits;
   const int per = total_bits == 0 ? 1 : (total_bits + passes - 1) / passes;
+  if (M <= kSmallMax) {
+    SmallSched a;
+    a.idx = idx;
+    a.tmp_k[0] = K0;
+    a.tmp_k[1] = K1;
+    a.tmp_v[0] = V0;
+    a.tmp_v[1] = V1;
+    a.perm = perm;
+    a.active = active;
+    a.offsets = active_offsets;
+    a.n_active = n_active;
+    a.M = (int)M;
+    a.cap = (int)std::min<int64_t>(M, s.N);
+    a.passes = passes;
+    a.per = per;
+    a.total_bits = total_bits;
+    hipLaunchKernelGGL(schedule_small_kernel, dim3(1), dim3(kSmallThreads), 0, st, a);
+    *sorted_keys = (passes & 1) ? K0 : K1;
+    if (dense_offsets) {
+      const int64_t n = s.N + 1;
+      hipLaunchKernelGGL(dense_offsets_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)),
+                         dim3(kThreads), 0, st, (const int32_t*)active,
+                         (const int32_t*)active_offsets, (const int32_t*)n_active, dense_offsets,
+                         s.N);
+    }
+    return hipGetLastError();
+  }
   const int32_t* kin = idx;
   const int32_t* vin = nullptr;
   int shift = 0;

@@ -47,6 +47,11 @@ SHAPES = {
                                 K=8),
     "wide_f32": synth.Workload("wide_f32", T=70, d=4096, n_rows=32, n_cols=16, d_key=2048, H=1,
                                K=5, dtype="f32"),
+    # T <= 64 with d_key % 256 == 0: the decode-shaped logit kernel, ragged key tiles
+    "skinny_bf16": synth.Workload("skinny_bf16", T=40, d=1024, n_rows=48, n_cols=80, d_key=256,
+                                  H=3, K=7),
+    "skinny1_bf16": synth.Workload("skinny1_bf16", T=1, d=1024, n_rows=48, n_cols=80, d_key=512,
+                                   H=2, K=12),
 }
 
 
