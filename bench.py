@@ -104,7 +104,19 @@ def cpu_baseline(w, inp, sample_tokens, threads):
     return {"value": T / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"first {T} of {w.T} tokens of {w.name} (full router over all "
                       f"{w.n_rows}x{w.n_cols} sub-keys, Cartesian selection, schedule, "
-                      f"expert-major forward), fp64, {dt:.1f} s"}
+                      f"expert-major forward), fp64, {dt:.1f} s on {threads} threads of "
+                      f"{cpu_model()}"}
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown CPU"
 
 
 def main():
@@ -113,11 +125,14 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="train_bf16")
-    ap.add_argument("--cpu-sample", type=int, default=2048, help="tokens for the oracle leg")
+    ap.add_argument("--cpu-sample", type=int, default=16384,
+                    help="tokens for the oracle leg (16384: about 10 s on 16 host threads)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle leg")
     ap.add_argument("--out", default=None, help="also write the JSON line here")
     ap.add_argument("--graph", action="store_true",
                     help="time replays of one layer call captured in a HIP graph")
+    ap.add_argument("--no-cold", action="store_true",
+                    help="skip the second timing with the caches flushed before each step")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="after timing, run a plain device copy of this many bytes twice "
                          "(a known-size reference for rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -189,6 +204,26 @@ def main():
     wall = time.perf_counter() - wall0
     ms_step = ev0.elapsed_time(ev1) / args.steps
     log(f"timed {args.steps} steps: {ms_step:.3f} ms/step (wall {1e3 * wall / args.steps:.3f})")
+
+    # Cold steps: before each one a 512 MiB fill evicts the L2 and the MALL, so the step reads
+    # its inputs (x, sub-keys, expert rows) from HBM; only the layer call sits between events.
+    cold = None
+    if not args.no_cold:
+        flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        for e0, e1 in evs:
+            flush.fill_(1)
+            e0.record(stream)
+            step()
+            e1.record(stream)
+        torch.cuda.synchronize()
+        cold_ms = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
+        med = cold_ms[len(cold_ms) // 2]
+        cold = {"ms_per_step_median": med, "tokens_per_s": w.T / (med * 1e-3),
+                "flush_bytes": 512 << 20}
+        del flush
+        log(f"cold steps (512 MiB flush before each): median {med:.3f} ms")
 
     # Per-kernel durations: the same calls with HIP events around each kernel group.
     timer = P.Timer(args.steps)
@@ -262,6 +297,7 @@ def main():
                    "act": w.act, "query": w.query_mode, "graph": bool(args.graph)},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "cold": cold,
         "n_active": n_active, "eta": w.M / max(1, n_active),
         "kernels": kernels,
     }
