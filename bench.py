@@ -76,6 +76,35 @@ def load_traffic(kernel, workload):
     return t.get("bytes_per_launch")
 
 
+def routing_stats(idx, N):
+    """Expert usage of one batch: active experts, usage, KL(z || uniform), top-10% share."""
+    import numpy as np
+    counts = np.bincount(idx.ravel(), minlength=N)
+    z = counts[counts > 0] / idx.size
+    top = np.sort(counts)[::-1]
+    return {"n_active": int((counts > 0).sum()), "usage": float((counts > 0).mean()),
+            "kl_to_uniform": float(np.sum(z * np.log(z * N))),
+            "top10pct_share": float(top[: max(1, N // 10)].sum() / idx.size),
+            "max_segment": int(top[0])}
+
+
+def cpu_bruteforce(w, inp, sample_tokens, threads):
+    """Oracle selection by the plain definition (all n_rows x n_cols cells per token and head)
+    on the first `sample_tokens` tokens; the logits are computed outside the timed region."""
+    import oracle
+    import synth
+
+    T = min(sample_tokens, w.T)
+    dsc = oracle.desc(w, T=T)
+    sr, sc = oracle.half_scores(dsc, synth.as_f32(inp["x"][:T]), synth.as_f32(inp["keys_row"]),
+                                synth.as_f32(inp["keys_col"]), n_threads=threads)
+    t0 = time.perf_counter()
+    oracle.select(dsc, sr, sc, oracle.BRUTE, n_threads=threads)
+    dt = time.perf_counter() - t0
+    return {"value": T / dt, "unit": "tokens/s", "cores": threads,
+            "sample": f"brute-force top-{w.K} over all {w.N} cells, first {T} tokens, {dt:.1f} s"}
+
+
 def cpu_baseline(w, inp, sample_tokens, threads):
     """Oracle (route + schedule + scheduled forward) on the first `sample_tokens` tokens."""
     import numpy as np
@@ -128,6 +157,8 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=16384,
                     help="tokens for the oracle leg (16384: about 10 s on 16 host threads)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle leg")
+    ap.add_argument("--brute-sample", type=int, default=256,
+                    help="tokens for the oracle's brute-force selection timing (0: skip)")
     ap.add_argument("--out", default=None, help="also write the JSON line here")
     ap.add_argument("--graph", action="store_true",
                     help="time replays of one layer call captured in a HIP graph")
@@ -246,6 +277,8 @@ def main():
     P.omnimoe_schedule(desc, idx, perm, act, off, na)
     torch.cuda.synchronize()
     n_active = int(na.item())
+    routing = routing_stats(idx.cpu().numpy(), w.N)
+    assert routing["n_active"] == n_active
 
     work = algorithmic_work(w, n_active)
     kernels = {}
@@ -260,6 +293,12 @@ def main():
             ach = amount / t_s / 1e12
             kernels[k] = {"bound": bound, "ms": per[k], "achieved": ach, "unit": "TFLOP/s",
                           "frac": ach / peak, "flop": amount}
+    for k, kd in kernels.items():
+        tb = load_traffic(k, w.name)
+        if tb is not None:
+            # rocprofv3 bytes (L2 misses, MALL hits included) over the event-timed duration
+            kd["counter_bytes"] = tb
+            kd["counter_GBps"] = tb / (per[k] * 1e-3) / 1e9
     dom = max(per, key=per.get)
     kd = kernels[dom]
     traffic = load_traffic(dom, w.name)
@@ -286,6 +325,9 @@ def main():
         log(f"oracle leg: {args.cpu_sample} tokens on {threads} host threads")
         cpu = cpu_baseline(w, inp, args.cpu_sample, threads)
         log(f"oracle {cpu['value']:.1f} tokens/s")
+        if args.brute_sample > 0:
+            cpu["bruteforce_select"] = cpu_bruteforce(w, inp, args.brute_sample, threads)
+            log(f"oracle brute-force selection {cpu['bruteforce_select']['value']:.1f} tokens/s")
 
     line = {
         "metric": METRIC, "value": w.T / (ms_step * 1e-3), "unit": "tokens/s", "n_gpus": 1,
@@ -298,7 +340,8 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "cold": cold,
-        "n_active": n_active, "eta": w.M / max(1, n_active),
+        "n_active": n_active, "eta": w.M / max(1, n_active), "routing": routing,
+        "schedule_share": per["schedule"] / sum(per.values()),
         "kernels": kernels,
     }
     s = json.dumps(line)

@@ -130,7 +130,7 @@ class Workload:
         return replace(self, **kw)
 
 
-# The five layer shapes the implementation is checked and measured on.
+# The layer shapes the implementation is checked and measured on.
 WORKLOADS: Dict[str, Workload] = {
     # T=256, d=64, N=64^2, sub-keys 2 x 64 of dim 32, H=1, K=8, fp32.
     "tiny_f32": Workload("tiny_f32", T=256, d=64, n_rows=64, n_cols=64, d_key=32, H=1, K=8,
@@ -146,6 +146,10 @@ WORKLOADS: Dict[str, Workload] = {
     # (tests/golden/calibrate_skew.py, result in tests/golden/skew_calibration.json).
     "skew_bf16": Workload("skew_bf16", T=16384, d=2048, n_rows=1024, n_cols=1024, d_key=1024,
                           H=8, K=16, skew_alpha=0.080078125),
+    # One GPU's share of the training batch when tokens are split over eight GPUs with the
+    # tables replicated (data-parallel): 2048 tokens against all 1024^2 experts.
+    "dp8share_bf16": Workload("dp8share_bf16", T=2048, d=2048, n_rows=1024, n_cols=1024,
+                              d_key=1024, H=8, K=16),
     # One decode step of a batch of 64, and a single token.
     "decode64_bf16": Workload("decode64_bf16", T=64, d=2048, n_rows=1024, n_cols=1024,
                               d_key=1024, H=8, K=16),

@@ -357,6 +357,17 @@ def test_skewed_shape_sampled(train_tables):
     assert abs(share - 0.50) < 0.02
 
 
+def test_dp_share_shape_sampled(train_tables):
+    # 2048 tokens against the full tables: one GPU's share of a data-parallel split.
+    dev, kr, kc = train_tables
+    w = W["dp8share_bf16"]
+    say("[full] dp8share_bf16 T=2048")
+    rng = np.random.default_rng(2)
+    tokens = np.unique(np.concatenate([[0, w.T - 1], rng.choice(w.T, 62, replace=False)]))
+    y, idx = _sampled_parity(w, dev, kr, kc, tokens)
+    assert np.isfinite(y).all()
+
+
 @pytest.mark.parametrize("name", ["decode64_bf16", "decode1_bf16"])
 def test_decode_shapes(train_tables, name):
     dev, kr, kc = train_tables
