@@ -10,6 +10,16 @@ constexpr int kWave = 64;
 
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (kWave - 1)); }
 
+// Workgroups are dispatched to the eight XCDs round robin (workgroup b runs on XCD b % 8).
+// xcd_contiguous(b, n) is a bijection on [0, n) under which each XCD works through one
+// contiguous block of items, so neighbouring items share an L2 (and its partial lines).
+__device__ __forceinline__ int64_t xcd_contiguous(int64_t b, int64_t n) {
+  constexpr int kXcds = 8;
+  const int64_t full = n - n % kXcds;
+  if (b >= full) return b;
+  return (b % kXcds) * (full / kXcds) + b / kXcds;
+}
+
 __device__ __forceinline__ uint64_t lanemask_lt() {
   return (1ull << lane_id()) - 1ull;
 }

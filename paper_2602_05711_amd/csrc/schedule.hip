@@ -77,21 +77,6 @@ __global__ __launch_bounds__(kThreads) void scan_reduce_kernel(F f, int64_t n, i
   if (threadIdx.x == 0) partial[blockIdx.x] = total;
 }
 
-// Exclusive scan of the partials in place (one block); the grand total goes to *total_out.
-__global__ __launch_bounds__(kThreads) void scan_partials_kernel(int32_t* partial, int nb,
-                                                                 int32_t* total_out) {
-  int carry = 0;
-  for (int base = 0; base < nb; base += kThreads) {
-    int i = base + (int)threadIdx.x;
-    int v = i < nb ? partial[i] : 0;
-    int total;
-    int ex = block_excl_scan(v, &total);
-    if (i < nb) partial[i] = carry + ex;
-    carry += total;
-  }
-  if (threadIdx.x == 0 && total_out) *total_out = carry;
-}
-
 // Writes the exclusive scan of f to out (ArrayVal) ...
 struct EmitScan {
   int32_t* out;
@@ -100,25 +85,41 @@ struct EmitScan {
     (void)val;
     if (i < n) out[i] = pos;
   }
+  __device__ void finish(int total) const { (void)total; }
 };
 
-// ... or compacts segment heads into active / active_offsets (HeadFlag). `cap` bounds the
-// output arrays, which only matters if some id lies outside [0, N).
+// ... or compacts segment heads into active / active_offsets (HeadFlag) and closes the list:
+// n_active and the end offset M. `cap` bounds the output arrays, which only matters if some id
+// lies outside [0, N).
 struct EmitSegments {
   const int32_t* keys;
   int32_t* active;
   int32_t* offsets;
+  int32_t* n_active;
   int32_t cap;
+  int32_t m;
   __device__ void operator()(int64_t i, int val, int pos) const {
     if (val && pos < cap) {
       active[pos] = keys[i];
       offsets[pos] = (int32_t)i;
     }
   }
+  __device__ void finish(int total) const {
+    const int n = total < cap ? total : cap;
+    *n_active = n;
+    offsets[n] = m;
+  }
 };
 
+// Second step of the scan: each block first adds up the chunk totals of the blocks before it
+// (at most a few hundred values), so no separate pass over the totals is needed. The last
+// block hands the grand total to emit.finish.
 template <class F, class E>
 __global__ __launch_bounds__(kThreads) void scan_down_kernel(F f, E emit, const int32_t* partial) {
+  int pre = 0;
+  for (int i = threadIdx.x; i < (int)blockIdx.x; i += kThreads) pre += partial[i];
+  int before;
+  block_excl_scan(pre, &before);
   const int64_t base = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kItems;
   int v[kItems];
   int s = 0;
@@ -128,21 +129,20 @@ __global__ __launch_bounds__(kThreads) void scan_down_kernel(F f, E emit, const 
     s += v[j];
   }
   int total;
-  int pos = block_excl_scan(s, &total) + partial[blockIdx.x];
+  int pos = block_excl_scan(s, &total) + before;
 #pragma unroll
   for (int j = 0; j < kItems; ++j) {
     emit(base + j, v[j], pos);
     pos += v[j];
   }
+  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) emit.finish(before + total);
 }
 
 template <class F, class E>
-hipError_t device_scan(F f, E emit, int64_t n, int32_t* partial, int32_t* total_out,
-                       hipStream_t st) {
+hipError_t device_scan(F f, E emit, int64_t n, int32_t* partial, hipStream_t st) {
   const int nb = (int)((n + kTile - 1) / kTile);
   if (nb == 0) return hipSuccess;
   hipLaunchKernelGGL(scan_reduce_kernel<F>, dim3(nb), dim3(kThreads), 0, st, f, n, partial);
-  hipLaunchKernelGGL(scan_partials_kernel, dim3(1), dim3(kThreads), 0, st, partial, nb, total_out);
   hipLaunchKernelGGL((scan_down_kernel<F, E>), dim3(nb), dim3(kThreads), 0, st, f, emit,
                      (const int32_t*)partial);
   return hipGetLastError();
@@ -165,7 +165,8 @@ __global__ __launch_bounds__(kThreads) void radix_upsweep_kernel(RadixPass p) {
   const int radix = 1 << p.bits;
   for (int d = threadIdx.x; d < radix; d += kThreads) cnt[d] = 0;
   __syncthreads();
-  const int64_t base = (int64_t)blockIdx.x * kTile;
+  const int64_t tile = xcd_contiguous(blockIdx.x, p.num_tiles);
+  const int64_t base = tile * kTile;
   const uint32_t mask = (uint32_t)radix - 1u;
 #pragma unroll 4
   for (int j = 0; j < kItems; ++j) {
@@ -174,7 +175,7 @@ __global__ __launch_bounds__(kThreads) void radix_upsweep_kernel(RadixPass p) {
   }
   __syncthreads();
   for (int d = threadIdx.x; d < radix; d += kThreads)
-    p.hist[(int64_t)d * p.num_tiles + blockIdx.x] = cnt[d];
+    p.hist[(int64_t)d * p.num_tiles + tile] = cnt[d];
 }
 
 __global__ __launch_bounds__(kThreads) void radix_downsweep_kernel(RadixPass p) {
@@ -182,14 +183,17 @@ __global__ __launch_bounds__(kThreads) void radix_downsweep_kernel(RadixPass p) 
   __shared__ int gofs[kMaxRadix];
   const int radix = 1 << p.bits;
   const uint32_t mask = (uint32_t)radix - 1u;
+  // Tiles in XCD-contiguous order: a digit's runs from neighbouring tiles are adjacent in the
+  // output, and written from one L2 they merge into whole lines.
+  const int64_t tile = xcd_contiguous(blockIdx.x, p.num_tiles);
   for (int d = threadIdx.x; d < radix; d += kThreads) {
-    gofs[d] = p.hist[(int64_t)d * p.num_tiles + blockIdx.x];
+    gofs[d] = p.hist[(int64_t)d * p.num_tiles + tile];
 #pragma unroll
     for (int w = 0; w < kThreads / kWave; ++w) wcnt[w][d] = 0;
   }
   __syncthreads();
   const int l = lane_id(), w = threadIdx.x >> 6;
-  const int64_t wbase = (int64_t)blockIdx.x * kTile + (int64_t)w * (kTile / 4);
+  const int64_t wbase = tile * kTile + (int64_t)w * (kTile / 4);
   const uint64_t lt = lanemask_lt();
   int key[kItems], val[kItems], rank[kItems];
   // All loads first: the LDS fences of the ranking rounds would otherwise hold each round's
@@ -240,18 +244,6 @@ __global__ __launch_bounds__(kThreads) void radix_downsweep_kernel(RadixPass p) 
       p.keys_out[pos] = key[r];
       p.vals_out[pos] = val[r];
     }
-  }
-}
-
-__global__ void close_offsets_kernel(int32_t* offsets, int32_t* n_active, int32_t m,
-                                     int32_t cap) {
-  if (threadIdx.x == 0 && blockIdx.x == 0) {
-    int n = *n_active;
-    if (n > cap) {
-      n = cap;
-      *n_active = cap;
-    }
-    offsets[n] = m;
   }
 }
 
@@ -515,7 +507,7 @@ hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, in
     p.num_tiles = num_tiles;
     hipLaunchKernelGGL(radix_upsweep_kernel, dim3(num_tiles), dim3(kThreads), 0, st, p);
     const int64_t hn = (int64_t)(1 << bits) * num_tiles;
-    hipError_t e = device_scan(ArrayVal{hist, hn}, EmitScan{hist, hn}, hn, partial, nullptr, st);
+    hipError_t e = device_scan(ArrayVal{hist, hn}, EmitScan{hist, hn}, hn, partial, st);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(radix_downsweep_kernel, dim3(num_tiles), dim3(kThreads), 0, st, p);
     kin = p.keys_out;
@@ -524,11 +516,10 @@ hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, in
   }
   *sorted_keys = kin;
   const int32_t cap = (int32_t)std::min<int64_t>(M, s.N);
-  hipError_t e = device_scan(HeadFlag{kin, M}, EmitSegments{kin, active, active_offsets, cap}, M,
-                             partial, n_active, st);
+  hipError_t e = device_scan(HeadFlag{kin, M},
+                             EmitSegments{kin, active, active_offsets, n_active, cap, (int32_t)M},
+                             M, partial, st);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(close_offsets_kernel, dim3(1), dim3(64), 0, st, active_offsets, n_active,
-                     (int32_t)M, cap);
   if (dense_offsets) {
     const int64_t n = s.N + 1;
     hipLaunchKernelGGL(dense_offsets_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)),
