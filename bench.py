@@ -280,6 +280,26 @@ def main():
     routing = routing_stats(idx.cpu().numpy(), w.N)
     assert routing["n_active"] == n_active
 
+    # Ablation of the schedule (Table 3, "w/o Expert-Centric Scheduling"): the same expert
+    # compute token by token, each task gathering its own u and v rows.
+    y_tc = torch.empty_like(y)
+    tc = lambda: P.omnimoe_expert_forward_token_centric(  # noqa: E731
+        desc, d_in["x"], d_in["u"], d_in["v"], idx, g, y_tc, stream=stream)
+    for _ in range(2):
+        tc()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        tc()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    tc_ms = ev0.elapsed_time(ev1) / args.steps
+    ec_ms = per["schedule"] + per["expert_dot"] + per["accumulate"]
+    ablation = {"token_centric_expert_ms": tc_ms, "expert_centric_expert_ms": ec_ms,
+                "token_over_expert_centric": tc_ms / ec_ms,
+                "same_y": bool(torch.equal(y_tc, y))}
+    log(f"expert stage: expert-centric (schedule + dot + accumulate) {ec_ms:.3f} ms, "
+        f"token-centric {tc_ms:.3f} ms")
+
     work = algorithmic_work(w, n_active)
     kernels = {}
     for k, (bound, amount) in work.items():
@@ -340,6 +360,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "cold": cold,
+        "ablation_no_schedule": ablation,
         "n_active": n_active, "eta": w.M / max(1, n_active), "routing": routing,
         "schedule_share": per["schedule"] / sum(per.values()),
         "kernels": kernels,

@@ -146,6 +146,18 @@ omnimoe_status omnimoe_expert_forward(const omnimoe_layer_desc* desc, const void
                                       const float* gates, const int32_t* perm, float* y,
                                       void* workspace, size_t workspace_bytes, void* stream);
 
+/* Expert compute without the schedule, token by token: the ablation of Expert-Centric
+ * Scheduling (Sec. 3.3, Table 3, "w/o Expert-Centric Scheduling"), for measuring what the
+ * schedule buys. Same arguments and result as omnimoe_expert_forward (bit for bit from 1024
+ * tokens up; below that omnimoe_expert_forward adds each token's slots in four partial sums,
+ * which can change the last bits), but every task gathers its own u and v rows: u is read once
+ * per task, not once per expert run. Needs no workspace. Pointers 16-byte aligned; T = 0 is a
+ * no-op. */
+omnimoe_status omnimoe_expert_forward_token_centric(const omnimoe_layer_desc* desc,
+                                                   const void* x, const void* u, const void* v,
+                                                   const int32_t* idx, const float* gates,
+                                                   float* y, void* stream);
+
 /* The whole routed layer: route, schedule and expert compute on one stream, no host
  * synchronisation. y [T, d] fp32 out; idx_out and gates_out ([T, H, K]) may be NULL. */
 omnimoe_status omnimoe_layer_forward(const omnimoe_layer_desc* desc, const void* x,

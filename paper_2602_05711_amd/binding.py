@@ -22,7 +22,8 @@ KERNEL_NAMES = ("score", "select", "schedule", "expert_dot", "accumulate")
 
 EXPORTED = (
     "omnimoe_workspace_size", "omnimoe_route", "omnimoe_select", "omnimoe_schedule",
-    "omnimoe_expert_forward", "omnimoe_layer_forward", "omnimoe_timer_create",
+    "omnimoe_expert_forward", "omnimoe_expert_forward_token_centric",
+    "omnimoe_layer_forward", "omnimoe_timer_create",
     "omnimoe_timer_destroy", "omnimoe_timer_read", "omnimoe_layer_forward_timed",
     "omnimoe_status_string",
 )
@@ -60,6 +61,7 @@ def load_library():
         "omnimoe_select": [D, P, P, P, P, SZ, P],
         "omnimoe_schedule": [D, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_expert_forward": [D, P, P, P, P, P, P, P, P, SZ, P],
+        "omnimoe_expert_forward_token_centric": [D, P, P, P, P, P, P, P],
         "omnimoe_layer_forward": [D, P, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_layer_forward_timed": [D, P, P, P, P, P, P, P, P, P, SZ, P, P],
         "omnimoe_timer_create": [I32, ctypes.POINTER(P)],
@@ -147,6 +149,13 @@ def omnimoe_expert_forward(desc, x, u, v, idx, gates, perm, y, ws=None, stream=N
     _check("omnimoe_expert_forward", load_library().omnimoe_expert_forward(
         ctypes.byref(desc), _ptr(x), _ptr(u), _ptr(v), _ptr(idx), _ptr(gates), _ptr(perm),
         _ptr(y), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def omnimoe_expert_forward_token_centric(desc, x, u, v, idx, gates, y, stream=None):
+    _check("omnimoe_expert_forward_token_centric",
+           load_library().omnimoe_expert_forward_token_centric(
+               ctypes.byref(desc), _ptr(x), _ptr(u), _ptr(v), _ptr(idx), _ptr(gates), _ptr(y),
+               _stream(stream)))
 
 
 def omnimoe_layer_forward(desc, x, keys_row, keys_col, u, v, y, idx_out=None, gates_out=None,

@@ -263,6 +263,19 @@ omnimoe_status omnimoe_expert_forward(const omnimoe_layer_desc* desc, const void
   return hip_status(e);
 }
 
+omnimoe_status omnimoe_expert_forward_token_centric(const omnimoe_layer_desc* desc,
+                                                   const void* x, const void* u, const void* v,
+                                                   const int32_t* idx, const float* gates,
+                                                   float* y, void* stream) {
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  if (s.T == 0) return OMNIMOE_OK;
+  if ((st = check_ptrs({x, u, v, idx, gates, y}))) return st;
+  return hip_status(omnimoe::launch_token_centric(s, x, u, v, idx, gates, y,
+                                                  (hipStream_t)stream));
+}
+
 omnimoe_status omnimoe_layer_forward(const omnimoe_layer_desc* desc, const void* x,
                                      const void* keys_row, const void* keys_col, const void* u,
                                      const void* v, float* y, int32_t* idx_out, float* gates_out,

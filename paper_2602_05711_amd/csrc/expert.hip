@@ -364,6 +364,118 @@ __global__ __launch_bounds__(256) void accumulate_slots_kernel(AccArgs a) {
   }
 }
 
+// Token-centric execution (the scheduling ablation): one wavefront per token keeps x_t in
+// registers and, G slots at a time in (head, k) order, gathers each slot's u and v rows
+// together, forms a = g * act(x_t . u_e) exactly as expert_dot_kernel does and adds a * v_e
+// into the fp32 row as accumulate_kernel does. Same operations in the same order, so y equals
+// the scheduled path's bit for bit; every u row is read once per task instead of once per run.
+struct TokenArgs {
+  const void* x;
+  const void* u;
+  const void* v;
+  const int32_t* idx;
+  const float* gates;
+  float* y;
+  int64_t T;
+  int64_t N;
+  int d;
+  int hk;
+  int act;
+  int nchunks;
+};
+
+template <int CPL, bool BF16>
+__global__ __launch_bounds__(256) void token_centric_kernel(TokenArgs a) {
+  constexpr int EPC = BF16 ? 8 : 4;
+  constexpr int G = CPL >= 16 ? 1 : (CPL >= 8 ? 2 : 4);
+  const int l = lane_id();
+  const uint4* X = (const uint4*)a.x;
+  const uint4* U = (const uint4*)a.u;
+  const uint4* V = (const uint4*)a.v;
+  const int64_t row_chunks = a.nchunks;
+  bool cv[CPL];
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) cv[q] = (l + kWave * q) < a.nchunks;
+  const int64_t stride = (int64_t)gridDim.x * 4;
+  for (int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < a.T; t += stride) {
+    uint4 xr[CPL];
+    load_row<CPL>(xr, X + t * row_chunks, cv);
+    float acc[CPL][EPC];
+#pragma unroll
+    for (int q = 0; q < CPL; ++q)
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) acc[q][k] = 0.0f;
+    for (int sb = 0; sb < a.hk; sb += kWave) {
+      const int sl = sb + l;
+      const bool valid = sl < a.hk;
+      const int ev = valid ? clamp_i(a.idx[t * a.hk + sl], a.N) : 0;
+      const float gv = valid ? a.gates[t * a.hk + sl] : 0.0f;
+      const int n = a.hk - sb < kWave ? a.hk - sb : kWave;
+      for (int j = 0; j < n; j += G) {
+        uint4 ur[G][CPL], vr[G][CPL];
+        float gj[G];
+#pragma unroll
+        for (int i = 0; i < G; ++i) {
+          const int jj = j + i < n ? j + i : n - 1;
+          const int e = readlane_i32(ev, jj);
+          gj[i] = readlane_f32(gv, jj);
+          load_row<CPL>(ur[i], U + (int64_t)e * row_chunks, cv);
+          load_row<CPL>(vr[i], V + (int64_t)e * row_chunks, cv);
+        }
+#pragma unroll
+        for (int i = 0; i < G; ++i) {
+          if (j + i < n) {
+            float h = 0.0f;
+#pragma unroll
+            for (int q = 0; q < CPL; ++q) h = chunk_dot<BF16>(ur[i][q], xr[q], h);
+            const float w = gj[i] * activation(a.act, wave_sum_uniform(h));
+#pragma unroll
+            for (int q = 0; q < CPL; ++q) {
+              const uint4 c = vr[i][q];
+              if constexpr (BF16) {
+                acc[q][0] = fmaf(w, bf16_lo(c.x), acc[q][0]);
+                acc[q][1] = fmaf(w, bf16_hi(c.x), acc[q][1]);
+                acc[q][2] = fmaf(w, bf16_lo(c.y), acc[q][2]);
+                acc[q][3] = fmaf(w, bf16_hi(c.y), acc[q][3]);
+                acc[q][4] = fmaf(w, bf16_lo(c.z), acc[q][4]);
+                acc[q][5] = fmaf(w, bf16_hi(c.z), acc[q][5]);
+                acc[q][6] = fmaf(w, bf16_lo(c.w), acc[q][6]);
+                acc[q][7] = fmaf(w, bf16_hi(c.w), acc[q][7]);
+              } else {
+                acc[q][0] = fmaf(w, __uint_as_float(c.x), acc[q][0]);
+                acc[q][1] = fmaf(w, __uint_as_float(c.y), acc[q][1]);
+                acc[q][2] = fmaf(w, __uint_as_float(c.z), acc[q][2]);
+                acc[q][3] = fmaf(w, __uint_as_float(c.w), acc[q][3]);
+              }
+            }
+          }
+        }
+      }
+    }
+    float4* yt = (float4*)(a.y + t * a.d);
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      if (!cv[q]) continue;
+      const int c = l + kWave * q;
+#pragma unroll
+      for (int k = 0; k < EPC; k += 4)
+        yt[(c * EPC + k) / 4] = make_float4(acc[q][k], acc[q][k + 1], acc[q][k + 2], acc[q][k + 3]);
+    }
+  }
+}
+
+template <bool BF16>
+hipError_t dispatch_token(int cpl, dim3 grid, hipStream_t st, const TokenArgs& a) {
+  switch (cpl) {
+    case 1: hipLaunchKernelGGL((token_centric_kernel<1, BF16>), grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((token_centric_kernel<2, BF16>), grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((token_centric_kernel<4, BF16>), grid, dim3(256), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((token_centric_kernel<8, BF16>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((token_centric_kernel<16, BF16>), grid, dim3(256), 0, st, a); break;
+  }
+  return hipGetLastError();
+}
+
 template <bool BF16>
 hipError_t dispatch_dot(int cpl, dim3 grid, hipStream_t st, const DotArgs& a) {
   switch (cpl) {
@@ -466,6 +578,30 @@ hipError_t launch_accumulate(const Shape& s, const void* v, const int32_t* idx, 
   if (blocks > 16384) blocks = 16384;
   return s.bf16 ? dispatch_acc<true>(cpl, dim3((unsigned)blocks), st, a)
                 : dispatch_acc<false>(cpl, dim3((unsigned)blocks), st, a);
+}
+
+hipError_t launch_token_centric(const Shape& s, const void* x, const void* u, const void* v,
+                                const int32_t* idx, const float* gates, float* y,
+                                hipStream_t st) {
+  if (s.T == 0) return hipSuccess;
+  TokenArgs a;
+  a.x = x;
+  a.u = u;
+  a.v = v;
+  a.idx = idx;
+  a.gates = gates;
+  a.y = y;
+  a.T = s.T;
+  a.N = s.N;
+  a.d = s.d;
+  a.hk = s.hk;
+  a.act = s.act;
+  a.nchunks = s.bf16 ? s.d / 8 : s.d / 4;
+  int64_t blocks = (s.T + 3) / 4;
+  if (blocks > 16384) blocks = 16384;
+  const int cpl = chunks_per_lane(a.nchunks);
+  return s.bf16 ? dispatch_token<true>(cpl, dim3((unsigned)blocks), st, a)
+                : dispatch_token<false>(cpl, dim3((unsigned)blocks), st, a);
 }
 
 }  // namespace omnimoe

@@ -48,6 +48,9 @@ hipError_t launch_expert_dot(const Shape& s, const void* x, const void* u, const
 hipError_t launch_fill_i32(int32_t* dst, int64_t n, int32_t value, hipStream_t st);
 
 // y[t] = sum over slots (h, k) in order of a[p] * v[idx[p]].
+hipError_t launch_token_centric(const Shape& s, const void* x, const void* u, const void* v,
+                                const int32_t* idx, const float* gates, float* y,
+                                hipStream_t st);
 hipError_t launch_accumulate(const Shape& s, const void* v, const int32_t* idx, const float* a,
                              float* y, hipStream_t st);
 

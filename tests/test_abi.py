@@ -24,7 +24,7 @@ def _declared_functions():
 def test_header_matches_exports():
     lib = P.load_library()
     names = _declared_functions()
-    assert len(names) == 11
+    assert len(names) == 12
     assert sorted(P.EXPORTED) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -101,6 +101,8 @@ def test_entry_points_check_pointers_before_launch():
     assert lib.omnimoe_schedule(D, a, a, a, a, a, bad, a, n(1 << 30), None) == ALIGN
     assert lib.omnimoe_schedule(D, a, a, a, a, a, None, a, n(8), None) == WORKSPACE
     assert lib.omnimoe_expert_forward(D, a, a, a, a, a, None, a, a, n(1 << 30), None) == INVALID
+    assert lib.omnimoe_expert_forward_token_centric(D, a, a, None, a, a, a, None) == INVALID
+    assert lib.omnimoe_expert_forward_token_centric(D, a, a, a, a, a, bad, None) == ALIGN
     assert lib.omnimoe_layer_forward(D, a, a, a, a, a, a, None, None, a, n(8), None) == WORKSPACE
     assert lib.omnimoe_layer_forward(D, a, a, a, a, a, a, bad, None, a, n(1 << 40), None) == ALIGN
     assert lib.omnimoe_layer_forward_timed(D, a, a, a, a, a, a, None, None, a, n(1 << 40), None,
@@ -115,6 +117,8 @@ def test_zero_tokens_is_a_noop():
     assert lib.omnimoe_route(D, None, None, None, None, None, None, None, n(0), None) == OK
     assert lib.omnimoe_expert_forward(D, None, None, None, None, None, None, None, None, n(0),
                                       None) == OK
+    assert lib.omnimoe_expert_forward_token_centric(D, None, None, None, None, None, None,
+                                                    None) == OK
     assert lib.omnimoe_layer_forward(D, None, None, None, None, None, None, None, None, None,
                                      n(0), None) == OK
 

@@ -194,12 +194,13 @@ def test_schedule_bitexact(case):
 
 # ------------------------------------------------------------------ expert compute
 
-@pytest.mark.parametrize("name", ["tiny_f32", "small_bf16", "ragged_bf16", "ragged_f32",
-                                  "silu_k1_bf16", "k64_bf16", "all_experts_bf16", "wide_bf16",
-                                  "wide_f32"])
-def test_expert_forward(name):
+EXPERT_SHAPES = ["tiny_f32", "small_bf16", "ragged_bf16", "ragged_f32", "silu_k1_bf16",
+                 "k64_bf16", "all_experts_bf16", "wide_bf16", "wide_f32"]
+
+
+def _expert_case(name):
+    """Oracle routing and schedule of one shape, the oracle's y, and the inputs on the GPU."""
     w = SHAPES[name]
-    say(f"[expert] {name}")
     inp, f = host_inputs(w)
     dsc = oracle.desc(w)
     sr, sc = oracle.half_scores(dsc, f["x"], f["keys_row"], f["keys_col"])
@@ -207,7 +208,13 @@ def test_expert_forward(name):
     g32 = g64.astype(np.float32)
     perm, _, _, _ = oracle.schedule(dsc, idx)
     y_ref = oracle.expert_forward(dsc, f["x"], f["u"], f["v"], idx, g32.astype(np.float64))
-    dev = upload(inp)
+    return w, upload(inp), idx, g32, perm, y_ref
+
+
+@pytest.mark.parametrize("name", EXPERT_SHAPES)
+def test_expert_forward(name):
+    say(f"[expert] {name}")
+    w, dev, idx, g32, perm, y_ref = _expert_case(name)
     y = torch.empty((w.T, w.d), dtype=torch.float32, device="cuda")
     P.omnimoe_expert_forward(B.make_desc(w), dev["x"], dev["u"], dev["v"], to_dev(idx),
                              to_dev(g32), to_dev(perm), y)
@@ -215,6 +222,31 @@ def test_expert_forward(name):
     err = row_rel_err(y.cpu().numpy(), y_ref)
     say(f"  max row rel err {err.max():.3e}")
     assert err.max() <= tol(w)
+
+
+@pytest.mark.parametrize("name", EXPERT_SHAPES)
+def test_token_centric_ablation(name):
+    # Without the schedule: within tolerance of the oracle, and equal to the scheduled path (same
+    # dot, activation and slot-order sum). Below 1024 tokens the scheduled path adds each
+    # token's slots in four partial sums, so there the two agree to rounding only.
+    say(f"[token-centric] {name}")
+    w, dev, idx, g32, perm, y_ref = _expert_case(name)
+    d = B.make_desc(w)
+    y = torch.empty((w.T, w.d), dtype=torch.float32, device="cuda")
+    y_tc = torch.full((w.T, w.d), float("nan"), dtype=torch.float32, device="cuda")
+    gi, gg = to_dev(idx), to_dev(g32)
+    P.omnimoe_expert_forward(d, dev["x"], dev["u"], dev["v"], gi, gg, to_dev(perm), y)
+    P.omnimoe_expert_forward_token_centric(d, dev["x"], dev["u"], dev["v"], gi, gg, y_tc)
+    torch.cuda.synchronize()
+    y_tc = y_tc.cpu().numpy()
+    err = row_rel_err(y_tc, y_ref)
+    say(f"  max row rel err {err.max():.3e}")
+    assert err.max() <= tol(w)
+    y = y.cpu().numpy()
+    if w.T >= 1024:
+        assert np.array_equal(y_tc, y)
+    else:
+        assert row_rel_err(y_tc, y.astype(np.float64)).max() <= 1e-6
 
 
 # ------------------------------------------------------------------ whole layer
