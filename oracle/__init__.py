@@ -52,10 +52,12 @@ def _load():
                                                    ctypes.c_int]
         lib.omnimoe_ref_layer_forward.argtypes = [D, P, P, P, P, P, ctypes.c_int, P, P, P,
                                                   ctypes.c_int]
+        lib.omnimoe_ref_route_dense.argtypes = [D, P, P, P, P, P, ctypes.c_int]
+        lib.omnimoe_ref_select_dense_f32.argtypes = [D, P, P, P, ctypes.c_int]
         lib.omnimoe_ref_act.argtypes = [ctypes.c_int, ctypes.c_double]
         lib.omnimoe_ref_act.restype = ctypes.c_double
         for f in ("half_scores", "select", "select_f32", "schedule", "expert_forward",
-                  "layer_forward"):
+                  "layer_forward", "route_dense", "select_dense_f32"):
             getattr(lib, "omnimoe_ref_" + f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -182,6 +184,34 @@ def layer_forward(dsc: RefDesc, x, keys_row, keys_col, u, v, method=CARTESIAN, n
                                          y.ctypes.data, idx.ctypes.data, g.ctypes.data,
                                          n_threads or default_threads()), "layer_forward")
     return y, idx, g
+
+
+def route_dense(dsc: RefDesc, x, w_gate, with_logits=False, n_threads=None):
+    """Dense router (the router ablation): (idx [T,H,K], gates fp64, logits [T,H,N] fp64 or
+    None). w_gate is [H, N, d]."""
+    lib = _load()
+    x, px = _f32(x)
+    wg, pwg = _f32(w_gate)
+    N = dsc.n_rows * dsc.n_cols
+    idx = np.empty((dsc.T, dsc.H, dsc.K), np.int32)
+    g = np.empty((dsc.T, dsc.H, dsc.K), np.float64)
+    L = np.empty((dsc.T, dsc.H, N), np.float64) if with_logits else None
+    _check(lib.omnimoe_ref_route_dense(ctypes.byref(dsc), px, pwg, idx.ctypes.data, g.ctypes.data,
+                                       None if L is None else L.ctypes.data,
+                                       n_threads or default_threads()), "route_dense")
+    return idx, g, L
+
+
+def select_dense_f32(dsc: RefDesc, logits, n_threads=None):
+    """The dense router's top-K and gates from float32 logits [T, H, N]."""
+    lib = _load()
+    L, pl = _f32(logits)
+    idx = np.empty((dsc.T, dsc.H, dsc.K), np.int32)
+    g = np.empty((dsc.T, dsc.H, dsc.K), np.float64)
+    _check(lib.omnimoe_ref_select_dense_f32(ctypes.byref(dsc), pl, idx.ctypes.data,
+                                            g.ctypes.data, n_threads or default_threads()),
+           "select_dense_f32")
+    return idx, g
 
 
 def act(kind: int, z: float) -> float:

@@ -7,6 +7,7 @@
 //             grid S_ij = p_r[i] + p_c[j] (Eq. 11), top-K (Eq. 1) and softmax gates (Eq. 2)
 //   Sec. 2.3  Expert-Centric Scheduling: task flatten (Eq. 12), active-expert groups of
 //             size B, sort by (group, token) (Eq. 13), per-group compute (Eq. 14)
+//   Sec. 3.3  the router ablation: a dense router scoring all N experts (Table 3)
 // It is used only by tests, the smoke check and the benchmark's CPU-baseline leg, and it
 // shares no code with the GPU library. Nothing here is blocked, fused or reordered
 // beyond what those passages state; library sorts serve as steps where a sort is what
@@ -153,6 +154,19 @@ int64_t select_row(const omnimoe_ref_desc* d, const double* sr, const double* sc
   }
   softmax_gates(s.data(), K, gates);
   return inexact;
+}
+
+// Dense selection for one (token, head) row of N logits: the plain definition of Eq. 1.
+void select_dense_row(const double* L, int64_t N, int K, int32_t* idx, double* gates) {
+  std::vector<Cand> cand((size_t)N);
+  for (int64_t n = 0; n < N; ++n) cand[(size_t)n] = Cand{L[n], n};
+  top_k(cand, K);
+  std::vector<double> s(K);
+  for (int k = 0; k < K; ++k) {
+    idx[k] = (int32_t)cand[k].n;
+    s[k] = cand[k].s;
+  }
+  softmax_gates(s.data(), K, gates);
 }
 
 double gelu_erf(double z) { return 0.5 * z * (1.0 + std::erf(z / std::sqrt(2.0))); }
@@ -349,6 +363,40 @@ int omnimoe_ref_layer_forward(const omnimoe_ref_desc* d, const float* x, const f
   rc = omnimoe_ref_select(d, sr.data(), sc.data(), method, I, nullptr, G, nullptr, n_threads);
   if (rc) return rc;
   return omnimoe_ref_expert_forward(d, x, u, v, I, G, 1, y, n_threads);
+}
+
+int omnimoe_ref_route_dense(const omnimoe_ref_desc* d, const float* x, const float* w_gate,
+                            int32_t* idx, double* gates, double* logits, int n_threads) {
+  if (!valid(d)) return -1;
+  const int H = d->H, K = d->K, D = d->d;
+  const int64_t N = (int64_t)d->n_rows * d->n_cols;
+  parallel_for(d->T * H, n_threads, [&](int64_t b, int64_t e) {
+    std::vector<double> L((size_t)N);
+    for (int64_t th = b; th < e; ++th) {
+      const int64_t t = th / H;
+      const int h = (int)(th % H);
+      for (int64_t n = 0; n < N; ++n)
+        L[(size_t)n] = dot_row(x + t * D, w_gate + ((int64_t)h * N + n) * D, D);
+      if (logits) std::copy(L.begin(), L.end(), logits + th * N);
+      select_dense_row(L.data(), N, K, idx + th * K, gates + th * K);
+    }
+  });
+  return 0;
+}
+
+int omnimoe_ref_select_dense_f32(const omnimoe_ref_desc* d, const float* logits, int32_t* idx,
+                                 double* gates, int n_threads) {
+  if (!valid(d)) return -1;
+  const int K = d->K;
+  const int64_t N = (int64_t)d->n_rows * d->n_cols;
+  parallel_for(d->T * d->H, n_threads, [&](int64_t b, int64_t e) {
+    std::vector<double> L((size_t)N);
+    for (int64_t th = b; th < e; ++th) {
+      for (int64_t n = 0; n < N; ++n) L[(size_t)n] = (double)logits[th * N + n];
+      select_dense_row(L.data(), N, K, idx + th * K, gates + th * K);
+    }
+  });
+  return 0;
 }
 
 }  // extern "C"

@@ -84,6 +84,18 @@ int omnimoe_ref_layer_forward(const omnimoe_ref_desc* desc, const float* x, cons
                               const float* keys_col, const float* u, const float* v, int method,
                               double* y, int32_t* idx, double* gates, int n_threads);
 
+/* Dense router, the router ablation (Sec. 3.3, Table 3, "w/o Cartesian Product Router"):
+ * logits L[t, h, n] = x_t . w_gate[h, n] over all N = n_rows * n_cols experts (fp64,
+ * summed over d in ascending order), top-K by (L descending, n ascending) (Eq. 1) and
+ * softmax gates over the K selected logits (Eq. 2). w_gate [H, N, d]; idx, gates [T, H, K];
+ * logits [T, H, N] may be NULL. d_key and query_mode are not used. */
+int omnimoe_ref_route_dense(const omnimoe_ref_desc* desc, const float* x, const float* w_gate,
+                            int32_t* idx, double* gates, double* logits, int n_threads);
+
+/* The dense router's selection from given float32 logits [T, H, N]. */
+int omnimoe_ref_select_dense_f32(const omnimoe_ref_desc* desc, const float* logits,
+                                 int32_t* idx, double* gates, int n_threads);
+
 /* The activation on one value: 0 GELU-erf, 1 SiLU. */
 double omnimoe_ref_act(int act, double z);
 

@@ -21,6 +21,7 @@ _lib = None
 # Tensor streams under one seed.
 STREAM_X, STREAM_KEYS_ROW, STREAM_KEYS_COL, STREAM_U, STREAM_V = 1, 2, 3, 4, 5
 STREAM_PERM_ROW, STREAM_PERM_COL = 6, 7
+STREAM_GATE = 8
 
 
 def build(verbose: bool = False) -> str:
@@ -204,6 +205,13 @@ def make_expert_rows(w: Workload, which: str, rows: Optional[Sequence[int]] = No
     r = np.asarray(rows, dtype=np.int64)
     return fill_rows(w.seed, stream, len(r), w.d, w.weight_scale, w.bf16, rows=r,
                      n_threads=n_threads)
+
+
+def make_gate_table(w: Workload, n_threads=None) -> np.ndarray:
+    """Gating vectors of a dense router over all N experts, [H, N, d] ~ N(0, 1/d)."""
+    g = fill_rows(w.seed, STREAM_GATE, w.H * w.N, w.d, w.weight_scale, w.bf16,
+                  n_threads=n_threads)
+    return g.reshape(w.H, w.N, w.d)
 
 
 def make_inputs(w: Workload, n_threads=None) -> Dict[str, np.ndarray]:

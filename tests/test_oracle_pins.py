@@ -371,3 +371,72 @@ def test_rejects_bad_shapes():
     s = Shape(T=4, d=8, n_rows=2, n_cols=2, d_key=4, H=1, K=5)  # K > N
     with pytest.raises(ValueError):
         oracle.select(oracle.desc(s), np.zeros((4, 1, 2)), np.zeros((4, 1, 2)))
+
+
+# ------------------------------------------------------------------ dense router (ablation)
+
+def _product_key_gates(kr, kc, d, query_mode):
+    """Gate table [H, N, d] whose dense logits equal the Cartesian scores: row n = i * n_cols + j
+    holds keys_row[h, i] on the row query's columns and keys_col[h, j] on the column query's."""
+    H, nr, dk = kr.shape
+    nc = kc.shape[1]
+    c0 = dk if query_mode == "split" else 0
+    wg = np.zeros((H, nr * nc, d), np.float32)
+    for i in range(nr):
+        for j in range(nc):
+            wg[:, i * nc + j, 0:dk] += kr[:, i]
+            wg[:, i * nc + j, c0:c0 + dk] += kc[:, j]
+    return wg
+
+
+@pytest.mark.parametrize("mode", ["split", "shared"])
+def test_dense_router_on_product_keys_equals_cartesian(mode):
+    # With small-integer inputs every dot product is exact, so scoring all N cells densely
+    # with w_gate[n] = (keys_row[i], keys_col[j]) must select exactly what the Cartesian router
+    # selects, ties and order included.
+    rng = np.random.default_rng(11)
+    for (nr, nc, K) in [(6, 5, 4), (7, 9, 13), (4, 4, 16), (1, 8, 3), (10, 3, 1)]:
+        dk = 3
+        d = 2 * dk if mode == "split" else dk
+        s = Shape(T=9, d=d, n_rows=nr, n_cols=nc, d_key=dk, H=2, K=K, query_mode=mode)
+        dsc = oracle.desc(s)
+        x = rng.integers(-2, 3, size=(s.T, d)).astype(np.float32)
+        kr = rng.integers(-2, 3, size=(2, nr, dk)).astype(np.float32)
+        kc = rng.integers(-2, 3, size=(2, nc, dk)).astype(np.float32)
+        sr, sc = oracle.half_scores(dsc, x, kr, kc)
+        i_c, _, g_c, _ = oracle.select(dsc, sr, sc, oracle.CARTESIAN, n_threads=1)
+        i_d, g_d, L = oracle.route_dense(dsc, x, _product_key_gates(kr, kc, d, mode),
+                                         with_logits=True, n_threads=1)
+        assert np.array_equal(i_d, i_c), (nr, nc, K)
+        np.testing.assert_array_equal(g_d, g_c)
+        assert np.array_equal(L, (sr[..., :, None] + sc[..., None, :]).reshape(L.shape))
+
+
+def test_dense_router_matches_numpy_definition():
+    rng = np.random.default_rng(12)
+    s = Shape(T=30, d=24, n_rows=9, n_cols=11, d_key=4, H=3, K=7)
+    dsc = oracle.desc(s)
+    x = rng.standard_normal((s.T, s.d)).astype(np.float32)
+    wg = rng.standard_normal((s.H, 99, s.d)).astype(np.float32)
+    idx, g, L = oracle.route_dense(dsc, x, wg, with_logits=True)
+    want_L = np.einsum("td,hnd->thn", x.astype(np.float64), wg.astype(np.float64))
+    np.testing.assert_allclose(L, want_L, rtol=1e-12, atol=1e-12)
+    for t in range(s.T):
+        for h in range(s.H):
+            top = _brute_topk_lexsort(want_L[t, h], s.K)
+            assert np.array_equal(idx[t, h], top)
+            e = np.exp(want_L[t, h, top] - want_L[t, h, top[0]])
+            np.testing.assert_allclose(g[t, h], e / e.sum(), rtol=1e-12)
+
+
+def test_dense_select_ties_and_full_k():
+    # Integer logits with heavy ties: ids ascending among equals; K = N returns every expert.
+    rng = np.random.default_rng(13)
+    s = Shape(T=20, d=2, n_rows=5, n_cols=6, d_key=1, H=2, K=30)
+    L = rng.integers(-3, 4, size=(s.T, s.H, 30)).astype(np.float32)
+    for K in (1, 4, 30):
+        idx, g = oracle.select_dense_f32(oracle.desc(s, K=K), L)
+        for t in range(s.T):
+            for h in range(s.H):
+                assert np.array_equal(idx[t, h], _brute_topk_lexsort(L[t, h].astype(np.float64), K))
+        np.testing.assert_allclose(g.sum(axis=2), 1.0, rtol=1e-14)
