@@ -299,6 +299,34 @@ def main():
                 "same_y": bool(torch.equal(y_tc, y))}
     log(f"expert stage: expert-centric (schedule + dot + accumulate) {ec_ms:.3f} ms, "
         f"token-centric {tc_ms:.3f} ms")
+    del y_tc
+
+    # Ablation of the router (Table 3, "w/o Cartesian Product Router"): a dense router with a
+    # gating vector per expert, all N logits per (token, head) materialised.
+    dense_bytes = w.T * w.H * w.N * 4
+    if dense_bytes <= (8 << 30):
+        import synth as _synth
+        wg = dev(_synth.make_gate_table(w))
+        wsd = P.workspace(desc, 5)
+        idx_d, g_d = torch.empty_like(idx), torch.empty_like(g)
+        rd = lambda: P.omnimoe_route_dense(  # noqa: E731
+            desc, d_in["x"], wg, idx_d, g_d, ws=wsd, stream=stream)
+        for _ in range(2):
+            rd()
+        ev0.record(stream)
+        for _ in range(args.steps):
+            rd()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        dr_ms = ev0.elapsed_time(ev1) / args.steps
+        cr_ms = per["score"] + per["select"]
+        no_cpr = {"dense_route_ms": dr_ms, "cartesian_route_ms": cr_ms,
+                  "route_ratio": dr_ms / cr_ms, "logit_bytes": dense_bytes,
+                  "layer_ratio": (dr_ms + ec_ms) / (cr_ms + ec_ms)}
+        log(f"router: Cartesian {cr_ms:.3f} ms, dense over all {w.N} experts {dr_ms:.3f} ms")
+        del wg, wsd
+    else:
+        no_cpr = {"skipped": f"the dense logits would take {dense_bytes / 2**30:.0f} GiB"}
 
     work = algorithmic_work(w, n_active)
     kernels = {}
@@ -361,6 +389,7 @@ def main():
         "cpu_baseline": cpu,
         "cold": cold,
         "ablation_no_schedule": ablation,
+        "ablation_no_cartesian_router": no_cpr,
         "n_active": n_active, "eta": w.M / max(1, n_active), "routing": routing,
         "schedule_share": per["schedule"] / sum(per.values()),
         "kernels": kernels,

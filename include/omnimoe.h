@@ -92,7 +92,8 @@ typedef enum {
   OMNIMOE_STAGE_SELECT = 1,
   OMNIMOE_STAGE_SCHEDULE = 2,
   OMNIMOE_STAGE_EXPERT = 3,
-  OMNIMOE_STAGE_LAYER = 4
+  OMNIMOE_STAGE_LAYER = 4,
+  OMNIMOE_STAGE_ROUTE_DENSE = 5  /* omnimoe_route_dense without a logits buffer */
 } omnimoe_stage;
 
 /* Bytes of workspace the given stage's entry point needs for this shape. */
@@ -112,6 +113,23 @@ omnimoe_status omnimoe_workspace_size(const omnimoe_layer_desc* desc, int32_t st
 omnimoe_status omnimoe_route(const omnimoe_layer_desc* desc, const void* x, const void* keys_row,
                              const void* keys_col, int32_t* idx, float* gates, float* half_scores,
                              void* workspace, size_t workspace_bytes, void* stream);
+
+/* Dense router, the router ablation (Sec. 3.3, Table 3, "w/o Cartesian Product Router"):
+ * every expert has its own gating vector and all N = n_rows * n_cols logits are computed.
+ *   x        [T, d]      dtype
+ *   w_gate   [H, N, d]   dtype   gating vector of every expert, per head
+ *   idx      [T, H, K]   int32 out  top K by (logit descending, id ascending) (Eq. 1)
+ *   gates    [T, H, K]   fp32  out  softmax of the K selected logits (Eq. 2)
+ *   logits   [T, H, N]   fp32  out, may be NULL (then the workspace holds them:
+ *            OMNIMOE_STAGE_ROUTE_DENSE bytes, T * H * N * 4 rounded up).
+ * d_key and query_mode are not used. The logit GEMM accumulates in fp32 (MFMA for bf16). */
+omnimoe_status omnimoe_route_dense(const omnimoe_layer_desc* desc, const void* x,
+                                   const void* w_gate, int32_t* idx, float* gates, float* logits,
+                                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* The dense router's selection alone, from given fp32 logits [T, H, N]. */
+omnimoe_status omnimoe_select_dense(const omnimoe_layer_desc* desc, const float* logits,
+                                    int32_t* idx, float* gates, void* stream);
 
 /* Selection only: top-K over the implicit grid and gates, from given fp32 logits
  *   half_scores [T, H, n_rows + n_cols] (as written by omnimoe_route). */

@@ -6,5 +6,6 @@ The computation lives in libomnimoe.so (HIP kernels behind the C ABI of include/
 from .binding import (  # noqa: F401
     EXPORTED, KERNEL_NAMES, OmnimoeError, OmnimoeLayerDesc, Timer, load_library, make_desc,
     omnimoe_expert_forward, omnimoe_expert_forward_token_centric, omnimoe_layer_forward,
-    omnimoe_route, omnimoe_schedule, omnimoe_select, omnimoe_workspace_size, workspace,
+    omnimoe_route, omnimoe_route_dense, omnimoe_schedule, omnimoe_select, omnimoe_select_dense,
+    omnimoe_workspace_size, workspace,
 )

@@ -17,11 +17,12 @@ LIB_PATH = os.path.join(HERE, "libomnimoe.so")
 OMNIMOE_F32, OMNIMOE_BF16 = 0, 1
 OMNIMOE_ACT_GELU, OMNIMOE_ACT_SILU = 0, 1
 OMNIMOE_QUERY_SPLIT, OMNIMOE_QUERY_SHARED = 0, 1
-STAGE_ROUTE, STAGE_SELECT, STAGE_SCHEDULE, STAGE_EXPERT, STAGE_LAYER = range(5)
+STAGE_ROUTE, STAGE_SELECT, STAGE_SCHEDULE, STAGE_EXPERT, STAGE_LAYER, STAGE_ROUTE_DENSE = range(6)
 KERNEL_NAMES = ("score", "select", "schedule", "expert_dot", "accumulate")
 
 EXPORTED = (
-    "omnimoe_workspace_size", "omnimoe_route", "omnimoe_select", "omnimoe_schedule",
+    "omnimoe_workspace_size", "omnimoe_route", "omnimoe_select", "omnimoe_route_dense",
+    "omnimoe_select_dense", "omnimoe_schedule",
     "omnimoe_expert_forward", "omnimoe_expert_forward_token_centric",
     "omnimoe_layer_forward", "omnimoe_timer_create",
     "omnimoe_timer_destroy", "omnimoe_timer_read", "omnimoe_layer_forward_timed",
@@ -59,6 +60,8 @@ def load_library():
         "omnimoe_workspace_size": [D, I32, ctypes.POINTER(SZ)],
         "omnimoe_route": [D, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_select": [D, P, P, P, P, SZ, P],
+        "omnimoe_route_dense": [D, P, P, P, P, P, P, SZ, P],
+        "omnimoe_select_dense": [D, P, P, P, P],
         "omnimoe_schedule": [D, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_expert_forward": [D, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_expert_forward_token_centric": [D, P, P, P, P, P, P, P],
@@ -132,6 +135,19 @@ def omnimoe_route(desc, x, keys_row, keys_col, idx, gates, half_scores=None, ws=
 def omnimoe_select(desc, half_scores, idx, gates, stream=None):
     _check("omnimoe_select", load_library().omnimoe_select(
         ctypes.byref(desc), _ptr(half_scores), _ptr(idx), _ptr(gates), None, 0, _stream(stream)))
+
+
+def omnimoe_route_dense(desc, x, w_gate, idx, gates, logits=None, ws=None, stream=None):
+    if ws is None and logits is None:
+        ws = workspace(desc, STAGE_ROUTE_DENSE, x.device)
+    _check("omnimoe_route_dense", load_library().omnimoe_route_dense(
+        ctypes.byref(desc), _ptr(x), _ptr(w_gate), _ptr(idx), _ptr(gates), _ptr(logits),
+        _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))
+
+
+def omnimoe_select_dense(desc, logits, idx, gates, stream=None):
+    _check("omnimoe_select_dense", load_library().omnimoe_select_dense(
+        ctypes.byref(desc), _ptr(logits), _ptr(idx), _ptr(gates), _stream(stream)))
 
 
 def omnimoe_schedule(desc, idx, perm, active, active_offsets, n_active, dense_offsets=None,

@@ -79,6 +79,7 @@ omnimoe_status hip_status(hipError_t e) { return e == hipSuccess ? OMNIMOE_OK : 
 
 size_t hs_bytes(const Shape& s) { return align_up((size_t)s.rows * (s.nr + s.nc) * 4); }
 size_t m_bytes(const Shape& s) { return align_up((size_t)s.M * 4); }
+size_t dense_bytes(const Shape& s) { return align_up((size_t)s.rows * (size_t)s.N * 4); }
 size_t active_bytes(const Shape& s) { return align_up((size_t)(std::min(s.M, s.N) + 1) * 4); }
 
 size_t stage_bytes(const Shape& s, int stage) {
@@ -87,6 +88,7 @@ size_t stage_bytes(const Shape& s, int stage) {
     case OMNIMOE_STAGE_SELECT: return 0;
     case OMNIMOE_STAGE_SCHEDULE: return omnimoe::schedule_ws_bytes(s.M, s.N);
     case OMNIMOE_STAGE_EXPERT: return m_bytes(s);
+    case OMNIMOE_STAGE_ROUTE_DENSE: return dense_bytes(s);
     default: {
       // idx, gates, perm, active, active_offsets, n_active, then the logits (dead after
       // selection) overlapped with the sort buffers and the a[] buffer.
@@ -179,7 +181,8 @@ const char* omnimoe_status_string(int32_t status) {
 omnimoe_status omnimoe_workspace_size(const omnimoe_layer_desc* desc, int32_t stage,
                                       size_t* bytes) {
   if (!bytes) return OMNIMOE_ERR_INVALID_ARG;
-  if (stage < OMNIMOE_STAGE_ROUTE || stage > OMNIMOE_STAGE_LAYER) return OMNIMOE_ERR_INVALID_ARG;
+  if (stage < OMNIMOE_STAGE_ROUTE || stage > OMNIMOE_STAGE_ROUTE_DENSE)
+    return OMNIMOE_ERR_INVALID_ARG;
   Shape s;
   omnimoe_status st = check_desc(desc, &s);
   if (st) return st;
@@ -206,6 +209,46 @@ omnimoe_status omnimoe_route(const omnimoe_layer_desc* desc, const void* x, cons
   hipError_t e = omnimoe::launch_score(s, x, keys_row, keys_col, hs, strm);
   if (e == hipSuccess) e = omnimoe::launch_select(s, hs, idx, gates, strm);
   return hip_status(e);
+}
+
+omnimoe_status omnimoe_route_dense(const omnimoe_layer_desc* desc, const void* x,
+                                   const void* w_gate, int32_t* idx, float* gates, float* logits,
+                                   void* ws, size_t ws_bytes, void* stream) {
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  if (s.T == 0) return OMNIMOE_OK;
+  if ((st = check_ptrs({x, w_gate, idx, gates}))) return st;
+  if ((st = check_opt(logits))) return st;
+  if ((int64_t)s.H * s.N >= kIntMax) return OMNIMOE_ERR_UNSUPPORTED;
+  float* L = logits;
+  if (!L) {
+    if ((st = check_ptrs({ws}))) return st;
+    if (ws_bytes < stage_bytes(s, OMNIMOE_STAGE_ROUTE_DENSE)) return OMNIMOE_ERR_WORKSPACE;
+    L = (float*)ws;
+  }
+  // The logit GEMM with one "half" holding all N gating vectors of each head over the full
+  // width of x, and an empty second half.
+  Shape g = s;
+  g.nr = (int)s.N;
+  g.nc = 0;
+  g.dk = s.d;
+  g.col0 = 0;
+  hipStream_t strm = (hipStream_t)stream;
+  hipError_t e = omnimoe::launch_score(g, x, w_gate, w_gate, L, strm);
+  if (e == hipSuccess) e = omnimoe::launch_select_dense(s.rows, s.N, s.K, L, idx, gates, strm);
+  return hip_status(e);
+}
+
+omnimoe_status omnimoe_select_dense(const omnimoe_layer_desc* desc, const float* logits,
+                                    int32_t* idx, float* gates, void* stream) {
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  if (s.T == 0) return OMNIMOE_OK;
+  if ((st = check_ptrs({logits, idx, gates}))) return st;
+  return hip_status(omnimoe::launch_select_dense(s.rows, s.N, s.K, logits, idx, gates,
+                                                 (hipStream_t)stream));
 }
 
 omnimoe_status omnimoe_select(const omnimoe_layer_desc* desc, const float* half_scores,

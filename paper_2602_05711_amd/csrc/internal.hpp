@@ -31,6 +31,11 @@ hipError_t launch_score(const Shape& s, const void* x, const void* keys_row,
 hipError_t launch_select(const Shape& s, const float* half_scores, int32_t* idx, float* gates,
                          hipStream_t st);
 
+// Dense-router selection (the router ablation): top K of each row of logits [rows, n] by
+// (logit desc, id asc) and softmax gates.
+hipError_t launch_select_dense(int64_t rows, int64_t n, int K, const float* logits, int32_t* idx,
+                               float* gates, hipStream_t st);
+
 // Radix-sort schedule. Workspace needs schedule_ws_bytes(M) bytes. On return sorted_keys
 // points into the workspace (expert id of each sorted position).
 size_t schedule_ws_bytes(int64_t M, int64_t N);
@@ -47,10 +52,13 @@ hipError_t launch_expert_dot(const Shape& s, const void* x, const void* u, const
 // dst[0:n] = value (a kernel, so the call can sit inside a captured graph).
 hipError_t launch_fill_i32(int32_t* dst, int64_t n, int32_t value, hipStream_t st);
 
-// y[t] = sum over slots (h, k) in order of a[p] * v[idx[p]].
+// The expert compute token by token (the scheduling ablation): same y as expert_dot followed
+// by accumulate, with each task gathering its own u and v rows.
 hipError_t launch_token_centric(const Shape& s, const void* x, const void* u, const void* v,
                                 const int32_t* idx, const float* gates, float* y,
                                 hipStream_t st);
+
+// y[t] = sum over slots (h, k) in order of a[p] * v[idx[p]].
 hipError_t launch_accumulate(const Shape& s, const void* v, const int32_t* idx, const float* a,
                              float* y, hipStream_t st);
 

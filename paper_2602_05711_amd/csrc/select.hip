@@ -343,6 +343,92 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- dense router (ablation)
+// Top K of all N logits of one (token, head) row by (logit desc, id asc), then softmax gates:
+// the router without the Cartesian product (Table 3). One workgroup of four waves per row.
+//   1. every thread keeps the largest of its logits (16-byte loads when N % 4 == 0);
+//   2. theta = the K-th largest of the 256 thread maxima (bitwise search with ballots), so at
+//      least K logits are >= theta and the top K are among them;
+//   3. each wave scans a quarter of the row 64 logits at a time; a batch holding logits >= theta
+//      is bitonic-sorted and merged into the wave's running top 64;
+//   4. wave 0 merges the four lists and writes ids and gates.
+struct DenseArgs {
+  const float* logits;
+  int32_t* idx;
+  float* gates;
+  int64_t rows;
+  int64_t N;
+  int K;
+};
+
+__global__ __launch_bounds__(256) void select_dense_kernel(DenseArgs a) {
+  __shared__ uint32_t tmax[256];
+  __shared__ uint64_t lists[3][kWave];
+  const int tid = threadIdx.x, l = lane_id(), w = tid >> 6;
+  const int64_t N = a.N;
+  const int K = a.K;
+  const bool vec = (N & 3) == 0;
+  const int64_t quarter = (N + 3) / 4;
+  for (int64_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
+    const float* p = a.logits + row * N;
+    uint32_t mx = 0u;
+    if (vec) {
+      for (int64_t j = 4 * (int64_t)tid; j < N; j += 4 * 256) {
+        const float4 f = *(const float4*)(p + j);
+        const uint32_t m0 = max(ord_f32(f.x), ord_f32(f.y));
+        const uint32_t m1 = max(ord_f32(f.z), ord_f32(f.w));
+        mx = max(mx, max(m0, m1));
+      }
+    } else {
+      for (int64_t j = tid; j < N; j += 256) mx = max(mx, ord_f32(p[j]));
+    }
+    tmax[tid] = mx;
+    __syncthreads();
+    uint32_t m4[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) m4[i] = tmax[l + kWave * i];
+    uint32_t th = 0u;
+    for (int b = 31; b >= 0; --b) {
+      const uint32_t c = th | (1u << b);
+      int cnt = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) cnt += __popcll(__ballot(m4[i] >= c));
+      if (cnt >= K) th = c;
+    }
+    const int64_t q0 = w * quarter;
+    const int64_t q1 = q0 + quarter < N ? q0 + quarter : N;
+    uint64_t best = 0ull;
+    bool first = true;
+    for (int64_t base = q0; base < q1; base += kWave) {
+      const int64_t j = base + l;
+      uint64_t key = 0ull;
+      if (j < q1) {
+        const uint32_t o = ord_f32(p[j]);
+        if (o >= th) key = logit_key(o, (int)j);
+      }
+      if (__ballot(key != 0ull) == 0ull) continue;
+      key = sort64<64>(key);
+      best = first ? key : merge_top64(best, key);
+      first = false;
+    }
+    if (w > 0) lists[w - 1][l] = best;
+    __syncthreads();
+    if (w == 0) {
+#pragma unroll
+      for (int i = 0; i < 3; ++i) best = merge_top64(best, lists[i][l]);
+      const float v = f32_from_ord((uint32_t)(best >> 32));
+      const float v0 = __shfl(v, 0, kWave);
+      const float e = (l < K) ? expf(v - v0) : 0.0f;
+      const float z = wave_sum_f32(e);
+      if (l < K) {
+        a.idx[row * K + l] = (int32_t)(0xFFFFFFFFu - (uint32_t)best);
+        a.gates[row * K + l] = e / z;
+      }
+    }
+    __syncthreads();
+  }
+}
+
 }  // namespace
 
 hipError_t launch_select(const Shape& s, const float* half_scores, int32_t* idx, float* gates,
@@ -376,6 +462,21 @@ hipError_t launch_select(const Shape& s, const float* half_scores, int32_t* idx,
   else if (nmax <= 2048) OMNIMOE_SELECT(32);
   else OMNIMOE_SELECT(64);
 #undef OMNIMOE_SELECT
+  return hipGetLastError();
+}
+
+hipError_t launch_select_dense(int64_t rows, int64_t n, int K, const float* logits, int32_t* idx,
+                               float* gates, hipStream_t st) {
+  if (rows == 0) return hipSuccess;
+  DenseArgs a;
+  a.logits = logits;
+  a.idx = idx;
+  a.gates = gates;
+  a.rows = rows;
+  a.N = n;
+  a.K = K;
+  const dim3 grid((unsigned)(rows < 16384 ? rows : 16384));
+  hipLaunchKernelGGL(select_dense_kernel, grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

@@ -40,7 +40,7 @@ def higham_bound(xq: np.ndarray, keys: np.ndarray, u: float = 2.0 ** -23) -> np.
     n = xq.shape[-1]
     gamma = n * u / (1 - n * u)
     return 2 * gamma * np.einsum("tm,hjm->thj", np.abs(xq).astype(np.float64),
-                                 np.abs(keys).astype(np.float64))
+                                 np.abs(keys).astype(np.float64), optimize=True)
 
 
 def grid_scores(sr_row, sc_row, ids, n_cols):

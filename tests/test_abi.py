@@ -24,7 +24,7 @@ def _declared_functions():
 def test_header_matches_exports():
     lib = P.load_library()
     names = _declared_functions()
-    assert len(names) == 12
+    assert len(names) == 14
     assert sorted(P.EXPORTED) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -85,6 +85,8 @@ def test_workspace_sizes_cover_buffers():
     st, layer = _ws(d, B.STAGE_LAYER)
     assert st == OK and layer >= route + 3 * w.M * 4
     assert _ws(d, 9)[0] == INVALID
+    st, dense = _ws(d, B.STAGE_ROUTE_DENSE)
+    assert st == OK and dense >= w.T * w.H * w.N * 4
 
 
 def test_entry_points_check_pointers_before_launch():
@@ -102,6 +104,10 @@ def test_entry_points_check_pointers_before_launch():
     assert lib.omnimoe_schedule(D, a, a, a, a, a, None, a, n(8), None) == WORKSPACE
     assert lib.omnimoe_expert_forward(D, a, a, a, a, a, None, a, a, n(1 << 30), None) == INVALID
     assert lib.omnimoe_expert_forward_token_centric(D, a, a, None, a, a, a, None) == INVALID
+    assert lib.omnimoe_route_dense(D, a, None, a, a, None, a, n(1 << 40), None) == INVALID
+    assert lib.omnimoe_route_dense(D, a, a, a, a, None, a, n(16), None) == WORKSPACE
+    assert lib.omnimoe_route_dense(D, a, a, a, a, bad, a, n(16), None) == ALIGN
+    assert lib.omnimoe_select_dense(D, a, bad, a, None) == ALIGN
     assert lib.omnimoe_expert_forward_token_centric(D, a, a, a, a, a, bad, None) == ALIGN
     assert lib.omnimoe_layer_forward(D, a, a, a, a, a, a, None, None, a, n(8), None) == WORKSPACE
     assert lib.omnimoe_layer_forward(D, a, a, a, a, a, a, bad, None, a, n(1 << 40), None) == ALIGN

@@ -406,3 +406,81 @@ def test_decode_shapes(train_tables, name):
     w = W[name]
     say(f"[full] {name}")
     _sampled_parity(w, dev, kr, kc, np.arange(w.T))
+
+
+# ------------------------------------------------------------------ dense router (ablation)
+
+DENSE_SHAPES = {
+    "tiny_f32": W["tiny_f32"],
+    "ragged_bf16": RAGGED,
+    "odd_n_bf16": synth.Workload("odd_n_bf16", T=100, d=128, n_rows=7, n_cols=9, d_key=64, H=2,
+                                 K=5),
+    "k64_bf16": SHAPES["k64_bf16"],
+    "wide_rows_bf16": synth.Workload("wide_rows_bf16", T=512, d=128, n_rows=128, n_cols=128,
+                                     d_key=64, H=1, K=16),
+    # 64 tokens: the skinny logit kernel, 65536-wide rows
+    "small64_bf16": W["small_bf16"].with_(name="small64_bf16", T=64),
+}
+
+
+@pytest.mark.parametrize("name", list(DENSE_SHAPES))
+def test_route_dense(name):
+    w = DENSE_SHAPES[name]
+    say(f"[dense route] {name} T={w.T} d={w.d} N={w.N} H={w.H} K={w.K}")
+    x = synth.make_x(w)
+    wg = synth.make_gate_table(w)
+    xf, wgf = synth.as_f32(x), synth.as_f32(wg)
+    d = B.make_desc(w)
+    L = torch.empty((w.T, w.H, w.N), dtype=torch.float32, device="cuda")
+    idx = torch.empty((w.T, w.H, w.K), dtype=torch.int32, device="cuda")
+    g = torch.empty((w.T, w.H, w.K), dtype=torch.float32, device="cuda")
+    P.omnimoe_route_dense(d, to_dev(x), to_dev(wg), idx, g, logits=L)
+    # the same call through the workspace (no logits buffer) gives the same selection
+    idx2 = torch.empty_like(idx)
+    g2 = torch.empty_like(g)
+    P.omnimoe_route_dense(d, to_dev(x), to_dev(wg), idx2, g2)
+    torch.cuda.synchronize()
+    L, idx, g = L.cpu().numpy(), idx.cpu().numpy(), g.cpu().numpy()
+    assert np.array_equal(idx, idx2.cpu().numpy())
+    assert np.array_equal(g, g2.cpu().numpy())
+    dsc = oracle.desc(w)
+    ref_idx, ref_g, ref_L = oracle.route_dense(dsc, xf, wgf, with_logits=True)
+    bound = higham_bound(xf, wgf)
+    err = np.abs(L - ref_L)
+    assert np.all(err <= bound + 1e-30)
+    # selection on the GPU's own logits is exact
+    si, sg = oracle.select_dense_f32(dsc, L)
+    assert np.array_equal(idx, si)
+    np.testing.assert_allclose(g, sg, rtol=GATE_TOL, atol=1e-7)
+    # against the fp64 router: exact wherever the top-(K+1) gaps exceed twice the logit error
+    delta = max(float(err.max()), 1e-300)
+    srt = -np.sort(-ref_L, axis=-1)[..., : w.K + 1]
+    cert = (-np.diff(srt, axis=-1)).min(axis=-1) > 2 * delta if w.K < w.N else \
+        np.ones(srt.shape[:-1], bool)
+    assert np.array_equal(idx[cert], ref_idx[cert])
+    say(f"  max logit err {delta:.3e}, uncertified rows {int((~cert).sum())} of {w.T * w.H}")
+
+
+@pytest.mark.parametrize("n,K,tie", [(4096, 16, False), (65536, 64, False), (63, 5, False),
+                                     (4096, 64, True), (65536, 16, True), (1000, 1000 // 16, True)])
+def test_select_dense_bitexact(n, K, tie):
+    rng = np.random.default_rng(n + K)
+    T, H = 24, 2
+    if tie:
+        L = rng.integers(-3, 4, size=(T, H, n)).astype(np.float32)
+        L[0, 0, :] = 0.0
+        L[1, 0, ::2] = -0.0
+    else:
+        L = rng.standard_normal((T, H, n)).astype(np.float32)
+    nr = 1
+    while n % (nr * 2) == 0 and nr * 2 <= 4096 and n // (nr * 2) >= 1 and nr < 64:
+        nr *= 2
+    w = synth.Workload("sel", T=T, d=16, n_rows=nr, n_cols=n // nr, d_key=8, H=H, K=K)
+    say(f"[dense select] n={n} K={K} tie={tie}")
+    idx = torch.empty((T, H, K), dtype=torch.int32, device="cuda")
+    g = torch.empty((T, H, K), dtype=torch.float32, device="cuda")
+    P.omnimoe_select_dense(B.make_desc(w), to_dev(L), idx, g)
+    torch.cuda.synchronize()
+    ri, rg = oracle.select_dense_f32(oracle.desc(w), L)
+    assert np.array_equal(idx.cpu().numpy(), ri)
+    np.testing.assert_allclose(g.cpu().numpy(), rg, rtol=GATE_TOL, atol=1e-7)
