@@ -54,10 +54,11 @@ def _load():
                                                   ctypes.c_int]
         lib.omnimoe_ref_route_dense.argtypes = [D, P, P, P, P, P, ctypes.c_int]
         lib.omnimoe_ref_select_dense_f32.argtypes = [D, P, P, P, ctypes.c_int]
+        lib.omnimoe_ref_shared_mlp.argtypes = [D, ctypes.c_int32, P, P, P, P, ctypes.c_int]
         lib.omnimoe_ref_act.argtypes = [ctypes.c_int, ctypes.c_double]
         lib.omnimoe_ref_act.restype = ctypes.c_double
         for f in ("half_scores", "select", "select_f32", "schedule", "expert_forward",
-                  "layer_forward", "route_dense", "select_dense_f32"):
+                  "layer_forward", "route_dense", "select_dense_f32", "shared_mlp"):
             getattr(lib, "omnimoe_ref_" + f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -212,6 +213,21 @@ def select_dense_f32(dsc: RefDesc, logits, n_threads=None):
                                             g.ctypes.data, n_threads or default_threads()),
            "select_dense_f32")
     return idx, g
+
+
+def shared_mlp(dsc: RefDesc, x, w_gu, w_down, y=None, n_threads=None):
+    """y + MLP(x) in fp64 (y = 0 when not given): the shared SwiGLU branch, w_gu [2 d_ff, d]
+    (gate rows then up rows), w_down [d, d_ff]."""
+    lib = _load()
+    x, px = _f32(x)
+    wgu, pgu = _f32(w_gu)
+    wd, pwd = _f32(w_down)
+    d_ff = wd.shape[1]
+    assert wgu.shape == (2 * d_ff, dsc.d) and wd.shape == (dsc.d, d_ff)
+    out = np.zeros((dsc.T, dsc.d), np.float64) if y is None else np.array(y, np.float64)
+    _check(lib.omnimoe_ref_shared_mlp(ctypes.byref(dsc), d_ff, px, pgu, pwd, out.ctypes.data,
+                                      n_threads or default_threads()), "shared_mlp")
+    return out
 
 
 def act(kind: int, z: float) -> float:

@@ -7,6 +7,8 @@
 //             grid S_ij = p_r[i] + p_c[j] (Eq. 11), top-K (Eq. 1) and softmax gates (Eq. 2)
 //   Sec. 2.3  Expert-Centric Scheduling: task flatten (Eq. 12), active-expert groups of
 //             size B, sort by (group, token) (Eq. 13), per-group compute (Eq. 14)
+//   Sec. 2.1  the shared dense branch MLP(x) added to the routed output (Eq. 3, 7), a
+//             SwiGLU feed-forward block
 //   Sec. 3.3  the router ablation: a dense router scoring all N experts (Table 3)
 // It is used only by tests, the smoke check and the benchmark's CPU-baseline leg, and it
 // shares no code with the GPU library. Nothing here is blocked, fused or reordered
@@ -394,6 +396,29 @@ int omnimoe_ref_select_dense_f32(const omnimoe_ref_desc* d, const float* logits,
     for (int64_t th = b; th < e; ++th) {
       for (int64_t n = 0; n < N; ++n) L[(size_t)n] = (double)logits[th * N + n];
       select_dense_row(L.data(), N, K, idx + th * K, gates + th * K);
+    }
+  });
+  return 0;
+}
+
+int omnimoe_ref_shared_mlp(const omnimoe_ref_desc* d, int32_t d_ff, const float* x,
+                           const float* w_gu, const float* w_down, double* y, int n_threads) {
+  if (!valid(d) || d_ff < 1) return -1;
+  const int D = d->d;
+  parallel_for(d->T, n_threads, [&](int64_t b, int64_t e) {
+    std::vector<double> a((size_t)d_ff);
+    for (int64_t t = b; t < e; ++t) {
+      const float* xt = x + t * D;
+      for (int f = 0; f < d_ff; ++f) {
+        const double g = dot_row(xt, w_gu + (int64_t)f * D, D);
+        const double u = dot_row(xt, w_gu + ((int64_t)d_ff + f) * D, D);
+        a[(size_t)f] = silu(g) * u;
+      }
+      for (int c = 0; c < D; ++c) {
+        double s = 0.0;
+        for (int f = 0; f < d_ff; ++f) s += (double)w_down[(int64_t)c * d_ff + f] * a[(size_t)f];
+        y[t * D + c] += s;
+      }
     }
   });
   return 0;

@@ -96,6 +96,13 @@ int omnimoe_ref_route_dense(const omnimoe_ref_desc* desc, const float* x, const 
 int omnimoe_ref_select_dense_f32(const omnimoe_ref_desc* desc, const float* logits,
                                  int32_t* idx, double* gates, int n_threads);
 
+/* The shared dense branch MLP(x) of Eq. 3 / Eq. 7, as a SwiGLU feed-forward block:
+ *   g_f = x . w_gu[f],  u_f = x . w_gu[d_ff + f]  (f < d_ff),  a_f = silu(g_f) * u_f,
+ *   y[t, c] += sum_f w_down[c, f] * a_f            (fp64, sums in ascending index order).
+ * w_gu [2 d_ff, d] (gate rows, then up rows); w_down [d, d_ff]; y [T, d] is added to. */
+int omnimoe_ref_shared_mlp(const omnimoe_ref_desc* desc, int32_t d_ff, const float* x,
+                           const float* w_gu, const float* w_down, double* y, int n_threads);
+
 /* The activation on one value: 0 GELU-erf, 1 SiLU. */
 double omnimoe_ref_act(int act, double z);
 

@@ -440,3 +440,38 @@ def test_dense_select_ties_and_full_k():
             for h in range(s.H):
                 assert np.array_equal(idx[t, h], _brute_topk_lexsort(L[t, h].astype(np.float64), K))
         np.testing.assert_allclose(g.sum(axis=2), 1.0, rtol=1e-14)
+
+
+# ------------------------------------------------------------------ shared dense MLP (Eq. 7)
+
+def test_shared_mlp_hand_example(golden_dir):
+    # d = 2, d_ff = 2: gate rows e0, e1; up rows 2 e0 and (e0 + e1); w_down swaps the features.
+    # For x = (1, -2): g = (1, -2), u = (2, -1), a = (silu(1) * 2, silu(-2) * -1) with
+    # silu(z) = z * logistic(z) from the table; y = (a_1, a_0) added to y0.
+    lg = _load(golden_dir, "activation_values.json")["logistic"]
+    s = Shape(T=1, d=2, n_rows=1, n_cols=1, d_key=1, H=1, K=1)
+    x = np.array([[1.0, -2.0]], np.float32)
+    w_gu = np.array([[1, 0], [0, 1], [2, 0], [1, 1]], np.float32)
+    w_down = np.array([[0, 1], [1, 0]], np.float32)
+    a0 = 1.0 * lg["1"] * 2.0
+    a1 = -2.0 * lg["-2"] * -1.0
+    y = oracle.shared_mlp(oracle.desc(s), x, w_gu, w_down, y=np.array([[0.5, -0.25]]))
+    np.testing.assert_allclose(y, [[0.5 + a1, -0.25 + a0]], rtol=1e-15)
+
+
+def test_shared_mlp_matches_numpy_and_is_linear_in_w_down():
+    rng = np.random.default_rng(21)
+    s = Shape(T=17, d=12, n_rows=2, n_cols=2, d_key=2, H=1, K=1)
+    dsc = oracle.desc(s)
+    x = rng.standard_normal((s.T, s.d)).astype(np.float32)
+    w_gu = rng.standard_normal((2 * 9, s.d)).astype(np.float32)
+    w_down = rng.standard_normal((s.d, 9)).astype(np.float32)
+    y = oracle.shared_mlp(dsc, x, w_gu, w_down)
+    h = x.astype(np.float64) @ w_gu.astype(np.float64).T
+    g, u = h[:, :9], h[:, 9:]
+    want = (g / (1.0 + np.exp(-g)) * u) @ w_down.astype(np.float64).T
+    np.testing.assert_allclose(y, want, rtol=1e-12, atol=1e-12)
+    # scaling w_down by a power of two scales every product and sum exactly
+    y2 = oracle.shared_mlp(dsc, x, w_gu, 2.0 * w_down)
+    np.testing.assert_array_equal(y2, 2.0 * y)
+    assert np.all(oracle.shared_mlp(dsc, np.zeros_like(x), w_gu, w_down) == 0.0)
