@@ -301,11 +301,35 @@ def main():
         f"token-centric {tc_ms:.3f} ms")
     del y_tc
 
+    # The full OmniMoE FFN adds the shared dense SwiGLU branch (Eq. 7) to the routed output;
+    # its width here is d_ff = d, the ratio of the paper's benchmark configuration.
+    import synth as _synth
+    d_ff = w.d
+    gu, dn = _synth.make_mlp_weights(w, d_ff)
+    gu, dn = dev(gu), dev(dn)
+    ws_mlp = torch.empty(P.omnimoe_shared_mlp_workspace_size(desc, d_ff), dtype=torch.uint8,
+                         device="cuda")
+    mlp = lambda: P.omnimoe_shared_mlp(  # noqa: E731
+        desc, d_ff, d_in["x"], gu, dn, y, ws=ws_mlp, stream=stream)
+    for _ in range(2):
+        mlp()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        mlp()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    mlp_ms = ev0.elapsed_time(ev1) / args.steps
+    mlp_flop = 2.0 * w.T * w.d * 3 * d_ff
+    shared_mlp = {"d_ff": d_ff, "ms": mlp_ms, "TFLOPs": mlp_flop / (mlp_ms * 1e-3) / 1e12,
+                  "ffn_ms": ms_step + mlp_ms, "routed_share": ms_step / (ms_step + mlp_ms)}
+    log(f"shared SwiGLU branch (d_ff={d_ff}): {mlp_ms:.3f} ms; routed layer + branch "
+        f"{ms_step + mlp_ms:.3f} ms")
+    del gu, dn, ws_mlp
+
     # Ablation of the router (Table 3, "w/o Cartesian Product Router"): a dense router with a
     # gating vector per expert, all N logits per (token, head) materialised.
     dense_bytes = w.T * w.H * w.N * 4
     if dense_bytes <= (8 << 30):
-        import synth as _synth
         wg = dev(_synth.make_gate_table(w))
         wsd = P.workspace(desc, 5)
         idx_d, g_d = torch.empty_like(idx), torch.empty_like(g)
@@ -388,6 +412,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "cold": cold,
+        "shared_mlp": shared_mlp,
         "ablation_no_schedule": ablation,
         "ablation_no_cartesian_router": no_cpr,
         "n_active": n_active, "eta": w.M / max(1, n_active), "routing": routing,

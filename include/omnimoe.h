@@ -183,6 +183,22 @@ omnimoe_status omnimoe_layer_forward(const omnimoe_layer_desc* desc, const void*
                                      const void* v, float* y, int32_t* idx_out, float* gates_out,
                                      void* workspace, size_t workspace_bytes, void* stream);
 
+/* The shared dense branch MLP(x) that the full layer adds to the routed output (Eq. 3, 7),
+ * as a SwiGLU feed-forward block of width d_ff:
+ *   y[t] += w_down (silu(w_gu[0:d_ff] x_t) * (w_gu[d_ff:2 d_ff] x_t))
+ *   x       [T, d]          dtype
+ *   w_gu    [2 d_ff, d]     dtype   gate rows, then up rows
+ *   w_down  [d, d_ff]       dtype
+ *   y       [T, d]          fp32 in/out (e.g. the output of omnimoe_layer_forward)
+ * d_ff % 8 == 0 and d_ff <= 65536 (else OMNIMOE_ERR_INVALID_ARG). Both projections accumulate
+ * in fp32 on the logit GEMM kernels; silu(g) * u is rounded to the layer's dtype before the
+ * down projection. Workspace: omnimoe_shared_mlp_workspace_size bytes. */
+omnimoe_status omnimoe_shared_mlp_workspace_size(const omnimoe_layer_desc* desc, int32_t d_ff,
+                                                 size_t* bytes);
+omnimoe_status omnimoe_shared_mlp(const omnimoe_layer_desc* desc, int32_t d_ff, const void* x,
+                                  const void* w_gu, const void* w_down, float* y,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
 /* Per-kernel timing of omnimoe_layer_forward with HIP events on the call's stream.
  * A timer holds host-side state and HIP events only (no device memory). Kernel groups: */
 typedef enum {

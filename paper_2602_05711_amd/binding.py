@@ -22,7 +22,8 @@ KERNEL_NAMES = ("score", "select", "schedule", "expert_dot", "accumulate")
 
 EXPORTED = (
     "omnimoe_workspace_size", "omnimoe_route", "omnimoe_select", "omnimoe_route_dense",
-    "omnimoe_select_dense", "omnimoe_schedule",
+    "omnimoe_select_dense", "omnimoe_shared_mlp", "omnimoe_shared_mlp_workspace_size",
+    "omnimoe_schedule",
     "omnimoe_expert_forward", "omnimoe_expert_forward_token_centric",
     "omnimoe_layer_forward", "omnimoe_timer_create",
     "omnimoe_timer_destroy", "omnimoe_timer_read", "omnimoe_layer_forward_timed",
@@ -62,6 +63,8 @@ def load_library():
         "omnimoe_select": [D, P, P, P, P, SZ, P],
         "omnimoe_route_dense": [D, P, P, P, P, P, P, SZ, P],
         "omnimoe_select_dense": [D, P, P, P, P],
+        "omnimoe_shared_mlp_workspace_size": [D, I32, ctypes.POINTER(SZ)],
+        "omnimoe_shared_mlp": [D, I32, P, P, P, P, P, SZ, P],
         "omnimoe_schedule": [D, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_expert_forward": [D, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_expert_forward_token_centric": [D, P, P, P, P, P, P, P],
@@ -148,6 +151,24 @@ def omnimoe_route_dense(desc, x, w_gate, idx, gates, logits=None, ws=None, strea
 def omnimoe_select_dense(desc, logits, idx, gates, stream=None):
     _check("omnimoe_select_dense", load_library().omnimoe_select_dense(
         ctypes.byref(desc), _ptr(logits), _ptr(idx), _ptr(gates), _stream(stream)))
+
+
+def omnimoe_shared_mlp_workspace_size(desc, d_ff: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check("omnimoe_shared_mlp_workspace_size", load_library().omnimoe_shared_mlp_workspace_size(
+        ctypes.byref(desc), d_ff, ctypes.byref(n)))
+    return n.value
+
+
+def omnimoe_shared_mlp(desc, d_ff, x, w_gu, w_down, y, ws=None, stream=None):
+    """y += MLP(x), the shared SwiGLU branch."""
+    import torch
+    if ws is None:
+        ws = torch.empty(max(256, omnimoe_shared_mlp_workspace_size(desc, d_ff)),
+                         dtype=torch.uint8, device=x.device)
+    _check("omnimoe_shared_mlp", load_library().omnimoe_shared_mlp(
+        ctypes.byref(desc), d_ff, _ptr(x), _ptr(w_gu), _ptr(w_down), _ptr(y), _ptr(ws),
+        ws.numel(), _stream(stream)))
 
 
 def omnimoe_schedule(desc, idx, perm, active, active_offsets, n_active, dense_offsets=None,

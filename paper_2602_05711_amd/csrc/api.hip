@@ -251,6 +251,60 @@ omnimoe_status omnimoe_select_dense(const omnimoe_layer_desc* desc, const float*
                                                  (hipStream_t)stream));
 }
 
+namespace {
+
+size_t mlp_ws_bytes(const Shape& s, int d_ff) {
+  return align_up((size_t)s.T * 2 * d_ff * 4) + align_up((size_t)s.T * d_ff * (s.bf16 ? 2 : 4));
+}
+
+bool valid_d_ff(int32_t d_ff) { return d_ff >= 8 && d_ff <= 65536 && d_ff % 8 == 0; }
+
+}  // namespace
+
+omnimoe_status omnimoe_shared_mlp_workspace_size(const omnimoe_layer_desc* desc, int32_t d_ff,
+                                                 size_t* bytes) {
+  if (!bytes || !valid_d_ff(d_ff)) return OMNIMOE_ERR_INVALID_ARG;
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  *bytes = mlp_ws_bytes(s, d_ff);
+  return OMNIMOE_OK;
+}
+
+omnimoe_status omnimoe_shared_mlp(const omnimoe_layer_desc* desc, int32_t d_ff, const void* x,
+                                  const void* w_gu, const void* w_down, float* y, void* ws,
+                                  size_t ws_bytes, void* stream) {
+  if (!valid_d_ff(d_ff)) return OMNIMOE_ERR_INVALID_ARG;
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  if (s.T == 0) return OMNIMOE_OK;
+  if ((st = check_ptrs({x, w_gu, w_down, y, ws}))) return st;
+  if (ws_bytes < mlp_ws_bytes(s, d_ff)) return OMNIMOE_ERR_WORKSPACE;
+  float* h = (float*)ws;
+  void* act = (char*)ws + align_up((size_t)s.T * 2 * d_ff * 4);
+  hipStream_t strm = (hipStream_t)stream;
+  // gate and up projections: h [T, 2 d_ff] = x w_gu^T
+  Shape g = s;
+  g.H = 1;
+  g.nr = 2 * d_ff;
+  g.nc = 0;
+  g.dk = s.d;
+  g.col0 = 0;
+  hipError_t e = omnimoe::launch_score(g, x, w_gu, w_gu, h, strm);
+  if (e == hipSuccess) e = omnimoe::launch_swiglu(s.T, d_ff, s.bf16, h, act, strm);
+  // down projection added into y: y [T, d] += act w_down^T
+  Shape dn = s;
+  dn.H = 1;
+  dn.d = d_ff;
+  dn.dk = d_ff;
+  dn.nr = s.d;
+  dn.nc = 0;
+  dn.col0 = 0;
+  if (e == hipSuccess) e = omnimoe::launch_score(dn, act, w_down, w_down, y, strm, true);
+  return hip_status(e);
+}
+
 omnimoe_status omnimoe_select(const omnimoe_layer_desc* desc, const float* half_scores,
                               int32_t* idx, float* gates, void* ws, size_t ws_bytes,
                               void* stream) {

@@ -24,8 +24,15 @@ struct Shape {
 
 // Logit GEMM: half_scores[t, h, 0:nr] = x[t, 0:dk] . keys_row[h, i, :],
 // half_scores[t, h, nr:nr+nc] = x[t, col0:col0+dk] . keys_col[h, j, :].
+// With accumulate, the products are added to half_scores instead of stored.
 hipError_t launch_score(const Shape& s, const void* x, const void* keys_row,
-                        const void* keys_col, float* half_scores, hipStream_t st);
+                        const void* keys_col, float* half_scores, hipStream_t st,
+                        bool accumulate = false);
+
+// a[t, f] = silu(h[t, f]) * h[t, d_ff + f] for h [T, 2 d_ff] fp32; a [T, d_ff] in the layer's
+// dtype (bf16 by round-to-nearest-even).
+hipError_t launch_swiglu(int64_t T, int d_ff, bool bf16, const float* h, void* a,
+                         hipStream_t st);
 
 // Per-half top-K, Cartesian merge and gates from fp32 half-scores.
 hipError_t launch_select(const Shape& s, const float* half_scores, int32_t* idx, float* gates,

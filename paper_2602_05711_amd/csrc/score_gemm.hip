@@ -1,11 +1,16 @@
 // Router logits (Eq. 9): one NT GEMM per grid half, C = Xq * Keys^T, where Xq is the
 // token's query slice x[:, c0:c0+d_key] and Keys stacks the H heads' sub-key tables
 // ([H * n_half, d_key]). Both operands are contiguous along d_key, so MFMA fragments load
-// straight from row-major memory.
+// straight from row-major memory. The same kernels serve the dense router of the ablation
+// (one half of N gating vectors) and the shared MLP's projections (accumulating into y).
 //
-// bf16: 128x128 macro tile, 4 waves of 64x64, v_mfma_f32_16x16x32_bf16, k-step 64,
-// LDS double buffer fed through registers, fp32 accumulation.
+// bf16, d_key % 64 == 0: 256 x 256 tile, four waves of 128 x 128 on v_mfma_f32_32x32x16_bf16,
+//   operands copied global -> LDS without registers (two 64 KiB stages, XOR-swizzled rows);
+// bf16, at most 64 tokens and d_key % 256 == 0: a split-K skinny kernel (decode);
+// bf16 otherwise: 128 x 128 tile, four waves of 64 x 64 on v_mfma_f32_16x16x32_bf16, LDS
+//   double buffer fed through registers;
 // fp32: a VALU FMA tile kernel (the fp32 layer is small; fp32 MFMA would change rounding).
+// All accumulate in fp32.
 #include "device_common.hpp"
 #include "internal.hpp"
 
@@ -31,6 +36,16 @@ struct ScoreArgs {
   int64_t ldo;      // H * (nr + nc)
 };
 
+// One output element (ACC: added to what is there). Each element is written by exactly one
+// lane, so the sum is deterministic. ACC is a template parameter rather than a flag: with a
+// runtime flag the compiler may hoist the read of out above the branch (the store makes the
+// address safe to read), which would read every logit back.
+template <bool ACC>
+__device__ __forceinline__ void store_out(const ScoreArgs& a, int64_t off, float v) {
+  if constexpr (ACC) a.out[off] += v;
+  else a.out[off] = v;
+}
+
 // Output column of GEMM column n (head n / nh, key n % nh) within a token's row.
 __device__ __forceinline__ int64_t out_col(const ScoreArgs& a, int half, int n) {
   int h = n / a.nh[half];
@@ -41,6 +56,7 @@ __device__ __forceinline__ int64_t out_col(const ScoreArgs& a, int half, int n) 
 constexpr int BM = 128, BN = 128, BK = 64;
 constexpr int LDS_ROW = BK + 8;  // bf16 per LDS row: 144 B keeps 16-lane b128 reads conflict-free
 
+template <bool ACC>
 __global__ __launch_bounds__(256) void score_bf16_kernel(ScoreArgs a) {
   const int half = blockIdx.z;
   const int ncols = a.H * a.nh[half];
@@ -139,7 +155,7 @@ __global__ __launch_bounds__(256) void score_bf16_kernel(ScoreArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         int64_t m = m0 + wm * 64 + i * 16 + (lane >> 4) * 4 + r;
-        if (m < a.T) a.out[m * a.ldo + oc] = acc[i][j][r];
+        if (m < a.T) store_out<ACC>(a, m * a.ldo + oc, acc[i][j][r]);
       }
     }
   }
@@ -163,6 +179,7 @@ __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 
 __device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
+template <bool ACC>
 __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
   const int half = blockIdx.z;
   const int ncols = a.H * a.nh[half];
@@ -273,7 +290,7 @@ __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const int64_t m = m0 + wm * 128 + i * 32 + (q >> 2) * 8 + (lane >> 5) * 4 + (q & 3);
-        if (m < a.T) a.out[m * a.ldo + oc] = acc[i][j][q];
+        if (m < a.T) store_out<ACC>(a, m * a.ldo + oc, acc[i][j][q]);
       }
     }
   }
@@ -288,6 +305,7 @@ __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
 
 constexpr int SK_N = 32;
 
+template <bool ACC>
 __global__ __launch_bounds__(256) void score_bf16_skinny_kernel(ScoreArgs a) {
   const int half = blockIdx.y;
   const int ncols = a.H * a.nh[half];
@@ -352,13 +370,14 @@ __global__ __launch_bounds__(256) void score_bf16_skinny_kernel(ScoreArgs a) {
         const int r = i * 32 + (q >> 2) * 8 + (lane >> 5) * 4 + (q & 3);
         const float v = ((acc[i][q] + part[0][r * SK_N + c]) + part[1][r * SK_N + c]) +
                         part[2][r * SK_N + c];
-        if (r < a.T) a.out[(int64_t)r * a.ldo + oc] = v;
+        if (r < a.T) store_out<ACC>(a, (int64_t)r * a.ldo + oc, v);
       }
   }
 }
 
 constexpr int FT = 64, FK = 16;
 
+template <bool ACC>
 __global__ __launch_bounds__(256) void score_f32_kernel(ScoreArgs a) {
   const int half = blockIdx.z;
   const int ncols = a.H * a.nh[half];
@@ -405,7 +424,7 @@ __global__ __launch_bounds__(256) void score_f32_kernel(ScoreArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       int64_t m = m0 + ty * 4 + i;
-      if (m < a.T) a.out[m * a.ldo + oc] = acc[i][j];
+      if (m < a.T) store_out<ACC>(a, m * a.ldo + oc, acc[i][j]);
     }
   }
 }
@@ -413,7 +432,8 @@ __global__ __launch_bounds__(256) void score_f32_kernel(ScoreArgs a) {
 }  // namespace
 
 hipError_t launch_score(const Shape& s, const void* x, const void* keys_row,
-                        const void* keys_col, float* half_scores, hipStream_t st) {
+                        const void* keys_col, float* half_scores, hipStream_t st,
+                        bool accumulate) {
   ScoreArgs a;
   a.x = x;
   a.keys[0] = keys_row;
@@ -434,16 +454,28 @@ hipError_t launch_score(const Shape& s, const void* x, const void* keys_row,
   const int ncols = s.H * (s.nr > s.nc ? s.nr : s.nc);
   if (s.bf16 && s.T <= 64 && s.dk % 256 == 0) {
     dim3 grid((ncols + SK_N - 1) / SK_N, 2);
-    hipLaunchKernelGGL(score_bf16_skinny_kernel, grid, dim3(256), 0, st, a);
+    if (accumulate)
+      hipLaunchKernelGGL(score_bf16_skinny_kernel<true>, grid, dim3(256), 0, st, a);
+    else
+      hipLaunchKernelGGL(score_bf16_skinny_kernel<false>, grid, dim3(256), 0, st, a);
   } else if (s.bf16 && s.dk % LK == 0) {
     dim3 grid((ncols + LN - 1) / LN, (unsigned)((s.T + LM - 1) / LM), 2);
-    hipLaunchKernelGGL(score_bf16_large_kernel, grid, dim3(256), 2 * LSTAGE, st, a);
+    if (accumulate)
+      hipLaunchKernelGGL(score_bf16_large_kernel<true>, grid, dim3(256), 2 * LSTAGE, st, a);
+    else
+      hipLaunchKernelGGL(score_bf16_large_kernel<false>, grid, dim3(256), 2 * LSTAGE, st, a);
   } else if (s.bf16) {
     dim3 grid((ncols + BN - 1) / BN, (unsigned)((s.T + BM - 1) / BM), 2);
-    hipLaunchKernelGGL(score_bf16_kernel, grid, dim3(256), 0, st, a);
+    if (accumulate)
+      hipLaunchKernelGGL(score_bf16_kernel<true>, grid, dim3(256), 0, st, a);
+    else
+      hipLaunchKernelGGL(score_bf16_kernel<false>, grid, dim3(256), 0, st, a);
   } else {
     dim3 grid((ncols + FT - 1) / FT, (unsigned)((s.T + FT - 1) / FT), 2);
-    hipLaunchKernelGGL(score_f32_kernel, grid, dim3(256), 0, st, a);
+    if (accumulate)
+      hipLaunchKernelGGL(score_f32_kernel<true>, grid, dim3(256), 0, st, a);
+    else
+      hipLaunchKernelGGL(score_f32_kernel<false>, grid, dim3(256), 0, st, a);
   }
   return hipGetLastError();
 }

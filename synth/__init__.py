@@ -22,6 +22,7 @@ _lib = None
 STREAM_X, STREAM_KEYS_ROW, STREAM_KEYS_COL, STREAM_U, STREAM_V = 1, 2, 3, 4, 5
 STREAM_PERM_ROW, STREAM_PERM_COL = 6, 7
 STREAM_GATE = 8
+STREAM_MLP_GU, STREAM_MLP_DOWN = 9, 10
 
 
 def build(verbose: bool = False) -> str:
@@ -212,6 +213,15 @@ def make_gate_table(w: Workload, n_threads=None) -> np.ndarray:
     g = fill_rows(w.seed, STREAM_GATE, w.H * w.N, w.d, w.weight_scale, w.bf16,
                   n_threads=n_threads)
     return g.reshape(w.H, w.N, w.d)
+
+
+def make_mlp_weights(w: Workload, d_ff: int, n_threads=None):
+    """Shared SwiGLU branch: (w_gu [2 d_ff, d] ~ N(0, 1/d), w_down [d, d_ff] ~ N(0, 1/d_ff))."""
+    gu = fill_rows(w.seed, STREAM_MLP_GU, 2 * d_ff, w.d, w.weight_scale, w.bf16,
+                   n_threads=n_threads)
+    down = fill_rows(w.seed, STREAM_MLP_DOWN, w.d, d_ff, 1.0 / float(np.sqrt(d_ff)), w.bf16,
+                     n_threads=n_threads)
+    return gu, down
 
 
 def make_inputs(w: Workload, n_threads=None) -> Dict[str, np.ndarray]:

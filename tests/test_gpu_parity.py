@@ -484,3 +484,48 @@ def test_select_dense_bitexact(n, K, tie):
     ri, rg = oracle.select_dense_f32(oracle.desc(w), L)
     assert np.array_equal(idx.cpu().numpy(), ri)
     np.testing.assert_allclose(g.cpu().numpy(), rg, rtol=GATE_TOL, atol=1e-7)
+
+
+# ------------------------------------------------------------------ shared dense MLP (Eq. 7)
+
+MLP_CASES = {
+    "tiny_f32": (W["tiny_f32"], 64),
+    "ragged_bf16": (RAGGED, 104),
+    "small_bf16": (W["small_bf16"], 512),
+    "skinny_bf16": (SHAPES["skinny_bf16"], 512),
+    "wide_f32": (SHAPES["wide_f32"], 1024),
+}
+
+
+def _mlp_parity(w, d_ff, tokens=None):
+    x = synth.make_x(w)
+    w_gu, w_down = synth.make_mlp_weights(w, d_ff)
+    rng = np.random.default_rng(w.T + d_ff)
+    y0 = rng.standard_normal((w.T, w.d)).astype(np.float32)
+    y = to_dev(y0.copy())
+    P.omnimoe_shared_mlp(B.make_desc(w), d_ff, to_dev(x), to_dev(w_gu), to_dev(w_down), y)
+    torch.cuda.synchronize()
+    y = y.cpu().numpy()
+    tok = np.arange(w.T) if tokens is None else tokens
+    dsc = oracle.desc(w, T=len(tok))
+    ref = oracle.shared_mlp(dsc, synth.as_f32(x[tok]), synth.as_f32(w_gu),
+                            synth.as_f32(w_down), y=y0[tok])
+    # error relative to the MLP term itself (y0 only shifts both sides)
+    err = row_rel_err(y[tok] - y0[tok], ref - y0[tok])
+    say(f"  max row rel err {err.max():.3e}")
+    assert err.max() <= tol(w)
+
+
+@pytest.mark.parametrize("name", list(MLP_CASES))
+def test_shared_mlp(name):
+    w, d_ff = MLP_CASES[name]
+    say(f"[mlp] {name} T={w.T} d={w.d} d_ff={d_ff}")
+    _mlp_parity(w, d_ff)
+
+
+def test_shared_mlp_train_shape_sampled():
+    w = W["train_bf16"]
+    say("[mlp] train_bf16 T=16384 d=2048 d_ff=2048, sampled tokens")
+    rng = np.random.default_rng(5)
+    tokens = np.unique(np.concatenate([[0, w.T - 1], rng.choice(w.T, 30, replace=False)]))
+    _mlp_parity(w, 2048, tokens)
