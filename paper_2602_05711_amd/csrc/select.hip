@@ -8,10 +8,10 @@
 // One wavefront per row. Keys are compared as integers (order-preserving bit maps), so the
 // result is exact and independent of evaluation order.
 //
-// Per-half top-K: each lane holds ceil(n / 64) logits. theta, the Kh-th largest of the 64
-// lane maxima, is found by a bitwise search with ballots (Kh distinct lanes hold a value
-// >= theta, so theta is at most the Kh-th largest logit and the logits >= theta contain the
-// answer). Usually only a few more than Kh logits qualify: the two halves' survivors are
+// Per-half top-K: each lane holds ceil(n / 64) logits. theta, at most the Kh-th largest of
+// the 64 lane maxima, is found by a bitwise search with ballots (Kh distinct lanes hold a
+// value >= theta, so theta is at most the Kh-th largest logit and the logits >= theta contain
+// the answer). Usually only a few more than Kh logits qualify: the two halves' survivors are
 // compacted into lanes 0-31 (rows) and 32-63 (columns) and bitonic-sorted together. When more
 // than 32 qualify (heavy ties, or K > 32) that half is instead sorted in batches of 64 from
 // memory and merged.
@@ -158,11 +158,15 @@ __device__ __forceinline__ uint64_t logit_key(uint32_t ord, int j) {
   return ((uint64_t)ord << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)j);
 }
 
-// Largest x with at least k lanes holding a value >= x (the k-th largest lane value).
+// A threshold th with at least k lanes holding a value >= th, at most the k-th largest lane
+// value: a bitwise search with ballots for the k-th largest value that leaves the lowest
+// kLowBits bits at zero. Those bits only move th by less than 2^kLowBits ordered steps, so at
+// most a few extra logits survive; the selection stays exact.
+constexpr int kLowBits = 8;
 __device__ __forceinline__ uint32_t kth_largest_lane(uint32_t v, int k) {
   uint32_t th = 0u;
 #pragma unroll
-  for (int b = 31; b >= 0; --b) {
+  for (int b = 31; b >= kLowBits; --b) {
     const uint32_t c = th | (1u << b);
     if (__popcll(__ballot(v >= c)) >= k) th = c;
   }
