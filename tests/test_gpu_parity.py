@@ -288,6 +288,42 @@ def test_layer_is_deterministic():
         assert np.array_equal(x.view(np.uint8), z.view(np.uint8))
 
 
+@pytest.mark.parametrize("name", ["small_bf16", "decode64_like_bf16"])
+def test_layer_graph_replays_match_eager(name):
+    # The layer call allocates nothing and clears with kernels only, so it can be captured in a
+    # HIP graph; every replay (with other eager work and synchronisations in between) must
+    # reproduce the eager result bit for bit, idx and gates included.
+    w = W["small_bf16"] if name == "small_bf16" else SHAPES["skinny_bf16"].with_(T=64)
+    inp, _ = host_inputs(w)
+    dev = upload(inp)
+    y_ref, idx_ref, g_ref = gpu_layer(w, dev)
+    d = B.make_desc(w)
+    ws = B.workspace(d, B.STAGE_LAYER)
+    y = torch.empty((w.T, w.d), dtype=torch.float32, device="cuda")
+    idx = torch.empty((w.T, w.H, w.K), dtype=torch.int32, device="cuda")
+    g = torch.empty((w.T, w.H, w.K), dtype=torch.float32, device="cuda")
+    graph = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(graph, stream=cap):
+            P.omnimoe_layer_forward(d, dev["x"], dev["keys_row"], dev["keys_col"], dev["u"],
+                                    dev["v"], y, idx, g, ws=ws, stream=cap)
+    torch.cuda.current_stream().wait_stream(cap)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        y.fill_(float("nan"))
+        idx.fill_(-1)
+        ws.fill_(0xAB)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(y.cpu().numpy().view(np.uint8), y_ref.view(np.uint8)), rep
+        assert np.array_equal(idx.cpu().numpy(), idx_ref), rep
+        assert np.array_equal(g.cpu().numpy().view(np.uint8), g_ref.view(np.uint8)), rep
+        _ = gpu_layer(w, dev)  # eager work between replays
+
+
 def test_zero_input_closed_form():
     w = SHAPES["ragged_bf16"]
     inp, _ = host_inputs(w)
