@@ -64,7 +64,9 @@ typedef enum { OMNIMOE_QUERY_SPLIT = 0, OMNIMOE_QUERY_SHARED = 1 } omnimoe_query
  *               columns x[:, d_key:2 d_key] (2 d_key <= d). SHARED: both score
  *               x[:, 0:d_key] (d_key <= d).
  *   H           heads, each with its own sub-key tables, top-K and softmax; H >= 1.
- *   K           experts per (token, head); 1 <= K <= 64 and K <= N.
+ *   K           experts per (token, head); 1 <= K <= 4096 and K <= N (K > 64 selects
+ *               with one workgroup per (token, head) instead of one wavefront; the dense
+ *               router of the ablation takes K <= 64).
  *   dtype       storage type of x, sub-keys, u and v (OMNIMOE_F32 or OMNIMOE_BF16);
  *               arithmetic is fp32 in every case.
  *   act         activation of Eq. 4: GELU (erf form) or SiLU.

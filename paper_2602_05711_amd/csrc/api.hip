@@ -37,7 +37,7 @@ omnimoe_status check_desc(const omnimoe_layer_desc* d, Shape* s) {
   if (d->H < 1 || d->K < 1) return OMNIMOE_ERR_INVALID_ARG;
   const int64_t N = (int64_t)d->n_rows * d->n_cols;
   if (d->K > N) return OMNIMOE_ERR_INVALID_ARG;
-  if (d->K > 64) return OMNIMOE_ERR_UNSUPPORTED;
+  if (d->K > 4096) return OMNIMOE_ERR_UNSUPPORTED;
   if (d->dtype != OMNIMOE_F32 && d->dtype != OMNIMOE_BF16) return OMNIMOE_ERR_INVALID_ARG;
   if (d->dtype == OMNIMOE_F32 && d->d > 4096) return OMNIMOE_ERR_UNSUPPORTED;
   if (d->act != OMNIMOE_ACT_GELU && d->act != OMNIMOE_ACT_SILU) return OMNIMOE_ERR_INVALID_ARG;
@@ -220,7 +220,7 @@ omnimoe_status omnimoe_route_dense(const omnimoe_layer_desc* desc, const void* x
   if (s.T == 0) return OMNIMOE_OK;
   if ((st = check_ptrs({x, w_gate, idx, gates}))) return st;
   if ((st = check_opt(logits))) return st;
-  if ((int64_t)s.H * s.N >= kIntMax) return OMNIMOE_ERR_UNSUPPORTED;
+  if ((int64_t)s.H * s.N >= kIntMax || s.K > 64) return OMNIMOE_ERR_UNSUPPORTED;
   float* L = logits;
   if (!L) {
     if ((st = check_ptrs({ws}))) return st;
@@ -247,6 +247,7 @@ omnimoe_status omnimoe_select_dense(const omnimoe_layer_desc* desc, const float*
   if (st) return st;
   if (s.T == 0) return OMNIMOE_OK;
   if ((st = check_ptrs({logits, idx, gates}))) return st;
+  if (s.K > 64) return OMNIMOE_ERR_UNSUPPORTED;
   return hip_status(omnimoe::launch_select_dense(s.rows, s.N, s.K, logits, idx, gates,
                                                  (hipStream_t)stream));
 }

@@ -347,6 +347,287 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- large K (65 .. 4096)
+// One workgroup of four waves per (token, head) row, for K beyond one wavefront:
+//   1. both halves are bitonic-sorted in LDS by (logit desc, index asc);
+//   2. the Cartesian candidates (a, b) with (a+1)(b+1) <= K are enumerated as a flat list
+//      (row rank a holds min(Kc, floor(K / (a+1))) of them; the offsets depend only on
+//      (K, Kr, Kc) and are computed once per workgroup), each thread walking a contiguous
+//      chunk; a candidate's key is (S as an order-preserving 64-bit integer, ~id);
+//   3. an 8-bit-digit radix select over the 96-bit keys finds the K-th largest key exactly
+//      (twelve passes with an LDS histogram), the K keys at or above it are gathered and
+//      bitonic-sorted descending;
+//   4. gates: softmax over the K scores, summed in a fixed order.
+// Integer comparisons throughout, so the result is exact and independent of thread timing.
+
+constexpr int kLargeThreads = 256;
+
+struct LargeArgs {
+  const float* hs;
+  int32_t* idx;
+  float* gates;
+  int64_t rows;
+  int nr, nc, K;
+  int n2;   // power of two >= max(nr, nc)
+  int k2;   // power of two >= K
+};
+
+// Bytes of dynamic LDS the kernel needs.
+size_t large_lds_bytes(int n2, int k2, int kr) {
+  return (size_t)2 * n2 * 8 + (size_t)k2 * 12 + (size_t)(kr + 1) * 4;
+}
+
+struct LargeShared {
+  uint32_t hist[256];
+  uint64_t ts, ms;   // decided high bits of the threshold key and their mask (score part)
+  uint32_t tn, mn;   // the same for the ~id part
+  int krem;          // keys still to select at and below the current digit
+  int count;         // gathered keys
+  int wint[4];
+  float wsum[4];
+};
+
+// Key of candidate (a, b) from the sorted half keys.
+__device__ __forceinline__ void cand_key(const uint64_t* rk, const uint64_t* ck, int a, int b, int nc,
+                                         uint64_t* ks, uint32_t* kn) {
+  const uint64_t r = rk[a], c = ck[b];
+  const float vr = f32_from_ord((uint32_t)(r >> 32));
+  const float vc = f32_from_ord((uint32_t)(c >> 32));
+  const uint32_t i = 0xFFFFFFFFu - (uint32_t)r;
+  const uint32_t j = 0xFFFFFFFFu - (uint32_t)c;
+  *ks = ord_f64((double)vr + (double)vc);
+  *kn = 0xFFFFFFFFu - (i * (uint32_t)nc + j);
+}
+
+__global__ __launch_bounds__(kLargeThreads) void select_large_kernel(LargeArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  __shared__ LargeShared sh;
+  const int n2 = a.n2, k2 = a.k2, K = a.K;
+  const int kr = K < a.nr ? K : a.nr;
+  const int kc = K < a.nc ? K : a.nc;
+  uint64_t* hk = (uint64_t*)smem;                 // [2][n2]: rows, then columns
+  uint64_t* sel_s = hk + 2 * n2;                  // [k2]
+  uint32_t* sel_n = (uint32_t*)(sel_s + k2);      // [k2]
+  uint32_t* cum = sel_n + k2;                     // [kr + 1]
+  const int tid = threadIdx.x, l = lane_id(), w = tid >> 6;
+
+  // candidate offsets: cum[a] = sum over a' < a of min(kc, K / (a' + 1)), by a block scan
+  {
+    const int per = (kr + kLargeThreads - 1) / kLargeThreads;
+    const int a0 = tid * per;
+    int loc = 0;
+    for (int q = a0; q < a0 + per && q < kr; ++q) {
+      const int c = K / (q + 1);
+      loc += c < kc ? c : kc;
+    }
+    const int ex = wave_excl_scan_i32(loc);
+    if (l == kWave - 1) sh.wint[w] = ex + loc;
+    __syncthreads();
+    int off = 0;
+    for (int ww = 0; ww < w; ++ww) off += sh.wint[ww];
+    int run = off + ex;
+    for (int q = a0; q < a0 + per && q < kr; ++q) {
+      cum[q] = (uint32_t)run;
+      const int c = K / (q + 1);
+      run += c < kc ? c : kc;
+    }
+    if (a0 < kr && a0 + per >= kr) cum[kr] = (uint32_t)run;
+    __syncthreads();
+  }
+  const int P = (int)cum[kr];
+  const int chunk = (P + kLargeThreads - 1) / kLargeThreads;
+  const int c0 = tid * chunk;
+  const int c1 = c0 + chunk < P ? c0 + chunk : P;
+  // first row rank of this thread's chunk (binary search in cum)
+  int a_first = 0;
+  if (c0 < P) {
+    int lo = 0, hi = kr - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if ((int)cum[mid] <= c0) lo = mid; else hi = mid - 1;
+    }
+    a_first = lo;
+  }
+
+  for (int64_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
+    const float* hr = a.hs + row * (int64_t)(a.nr + a.nc);
+    // 1. half keys, padded with 0 (below every finite logit), both halves sorted descending
+    for (int i = tid; i < 2 * n2; i += kLargeThreads) {
+      const int h = i >= n2, j = i - h * n2;
+      const int n = h ? a.nc : a.nr;
+      hk[i] = j < n ? logit_key(ord_f32(hr[h * a.nr + j]), j) : 0ull;
+    }
+    __syncthreads();
+    for (int lk = 1; (1 << lk) <= n2; ++lk) {
+      const int k = 1 << lk;
+      for (int lj = lk - 1; lj >= 0; --lj) {
+        const int j = 1 << lj;
+        for (int t = tid; t < n2; t += kLargeThreads) {
+          const int i = ((t >> lj) << (lj + 1)) | (t & (j - 1));
+          const uint64_t x = hk[i], y = hk[i + j];
+          const bool up = (i & k & (n2 - 1)) == 0;
+          if ((x < y) == up) {
+            hk[i] = y;
+            hk[i + j] = x;
+          }
+        }
+        __syncthreads();
+      }
+    }
+    const uint64_t* rk = hk;
+    const uint64_t* ck = hk + n2;
+    // 3. radix select of the K-th largest candidate key, eight bits at a time from the top
+    if (tid == 0) {
+      sh.ts = 0ull;
+      sh.ms = 0ull;
+      sh.tn = 0u;
+      sh.mn = 0u;
+      sh.krem = K;
+      sh.count = 0;
+    }
+    for (int pass = 0; pass < 12; ++pass) {
+      for (int i = tid; i < 256; i += kLargeThreads) sh.hist[i] = 0u;
+      __syncthreads();
+      const uint64_t ts = sh.ts, ms = sh.ms;
+      const uint32_t tn = sh.tn, mn = sh.mn;
+      const int sh_s = 56 - 8 * pass;            // digit position in the score word (pass < 8)
+      const int sh_n = 24 - 8 * (pass - 8);      // digit position in the id word (pass >= 8)
+      int ra = a_first, rb = c0 - (c0 < P ? (int)cum[a_first] : 0);
+      int rend = c0 < P ? (int)cum[ra + 1] : 0;
+      for (int c = c0; c < c1; ++c) {
+        while (c >= rend && ra < kr - 1) {  // each row rank holds at least one candidate
+          ++ra;
+          rb = 0;
+          rend = (int)cum[ra + 1];
+        }
+        uint64_t ks;
+        uint32_t kn;
+        cand_key(rk, ck, ra, rb, a.nc, &ks, &kn);
+        ++rb;
+        if ((ks & ms) == ts && (kn & mn) == tn) {
+          const uint32_t dg = pass < 8 ? (uint32_t)(ks >> sh_s) & 0xFFu : (kn >> sh_n) & 0xFFu;
+          atomicAdd(&sh.hist[dg], 1u);
+        }
+      }
+      __syncthreads();
+      if (w == 0) {
+        // largest digit whose suffix count reaches krem: lane l holds bins 4l .. 4l + 3
+        const int krem = sh.krem;
+        const uint32_t h0 = sh.hist[4 * l], h1 = sh.hist[4 * l + 1];
+        const uint32_t h2 = sh.hist[4 * l + 2], h3 = sh.hist[4 * l + 3];
+        const int mine = (int)(h0 + h1 + h2 + h3);
+        // suffix sum over lanes >= l
+        int suf = mine;
+#pragma unroll
+        for (int m = 1; m < kWave; m <<= 1) {
+          const int y = __shfl_down(suf, m, kWave);
+          if (l + m < kWave) suf += y;
+        }
+        const int above = suf - mine;  // keys in bins of higher lanes
+        const uint64_t hit = __ballot(suf >= krem && above < krem);
+        const int L = __ffsll((unsigned long long)hit) - 1;
+        if (l == L) {
+          // within the lane, from bin 4l + 3 down
+          int acc = above, dg;
+          if (acc + (int)h3 >= krem) {
+            dg = 4 * l + 3;
+          } else {
+            acc += (int)h3;
+            if (acc + (int)h2 >= krem) {
+              dg = 4 * l + 2;
+            } else {
+              acc += (int)h2;
+              if (acc + (int)h1 >= krem) {
+                dg = 4 * l + 1;
+              } else {
+                acc += (int)h1;
+                dg = 4 * l;
+              }
+            }
+          }
+          sh.krem = krem - acc;
+          if (pass < 8) {
+            sh.ts |= (uint64_t)dg << sh_s;
+            sh.ms |= (uint64_t)0xFF << sh_s;
+          } else {
+            sh.tn |= (uint32_t)dg << sh_n;
+            sh.mn |= 0xFFu << sh_n;
+          }
+        }
+      }
+      __syncthreads();
+    }
+    // the threshold key is exact now; gather the K keys at or above it
+    {
+      const uint64_t ts = sh.ts;
+      const uint32_t tn = sh.tn;
+      int ra = a_first, rb = c0 - (c0 < P ? (int)cum[a_first] : 0);
+      int rend = c0 < P ? (int)cum[ra + 1] : 0;
+      for (int c = c0; c < c1; ++c) {
+        while (c >= rend && ra < kr - 1) {  // each row rank holds at least one candidate
+          ++ra;
+          rb = 0;
+          rend = (int)cum[ra + 1];
+        }
+        uint64_t ks;
+        uint32_t kn;
+        cand_key(rk, ck, ra, rb, a.nc, &ks, &kn);
+        ++rb;
+        if (ks > ts || (ks == ts && kn >= tn)) {
+          const int pos = atomicAdd(&sh.count, 1);
+          if (pos < k2) {
+            sel_s[pos] = ks;
+            sel_n[pos] = kn;
+          }
+        }
+      }
+      for (int i = K + tid; i < k2; i += kLargeThreads) {
+        sel_s[i] = 0ull;
+        sel_n[i] = 0u;
+      }
+    }
+    __syncthreads();
+    // bitonic sort of the K selected keys, descending by (score, ~id)
+    for (int lk = 1; (1 << lk) <= k2; ++lk) {
+      const int k = 1 << lk;
+      for (int lj = lk - 1; lj >= 0; --lj) {
+        const int j = 1 << lj;
+        for (int t = tid; t < (k2 >> 1); t += kLargeThreads) {
+          const int i = ((t >> lj) << (lj + 1)) | (t & (j - 1));
+          const uint64_t xs = sel_s[i], ys = sel_s[i + j];
+          const uint32_t xn = sel_n[i], yn = sel_n[i + j];
+          const bool up = (i & k) == 0;
+          const bool lt = xs < ys || (xs == ys && xn < yn);
+          if (lt == up) {
+            sel_s[i] = ys;
+            sel_s[i + j] = xs;
+            sel_n[i] = yn;
+            sel_n[i + j] = xn;
+          }
+        }
+        __syncthreads();
+      }
+    }
+    // 4. gates: e_k = exp(S_k - S_0), summed per thread over a contiguous range, then across
+    // lanes and waves in a fixed order
+    const double s0 = f64_from_ord(sel_s[0]);
+    const int per = (K + kLargeThreads - 1) / kLargeThreads;
+    const int g0 = tid * per;
+    float part = 0.0f;
+    for (int q = g0; q < g0 + per && q < K; ++q)
+      part += expf((float)(f64_from_ord(sel_s[q]) - s0));
+    part = wave_sum_f32(part);
+    if (l == 0) sh.wsum[w] = part;
+    __syncthreads();
+    const float z = (sh.wsum[0] + sh.wsum[1]) + (sh.wsum[2] + sh.wsum[3]);
+    for (int q = tid; q < K; q += kLargeThreads) {
+      a.idx[row * K + q] = (int32_t)(0xFFFFFFFFu - sel_n[q]);
+      a.gates[row * K + q] = expf((float)(f64_from_ord(sel_s[q]) - s0)) / z;
+    }
+    __syncthreads();
+  }
+}
+
 // ---------------------------------------------------------------- dense router (ablation)
 // Top K of all N logits of one (token, head) row by (logit desc, id asc), then softmax gates:
 // the router without the Cartesian product (Table 3). One workgroup of four waves per row.
@@ -438,6 +719,27 @@ __global__ __launch_bounds__(256) void select_dense_kernel(DenseArgs a) {
 hipError_t launch_select(const Shape& s, const float* half_scores, int32_t* idx, float* gates,
                          hipStream_t st) {
   if (s.rows == 0) return hipSuccess;
+  if (s.K > kWave) {
+    LargeArgs a;
+    a.hs = half_scores;
+    a.idx = idx;
+    a.gates = gates;
+    a.rows = s.rows;
+    a.nr = s.nr;
+    a.nc = s.nc;
+    a.K = s.K;
+    int n2 = 2;
+    while (n2 < s.nr || n2 < s.nc) n2 <<= 1;
+    int k2 = 2;
+    while (k2 < s.K) k2 <<= 1;
+    a.n2 = n2;
+    a.k2 = k2;
+    const int kr = s.K < s.nr ? s.K : s.nr;
+    const size_t lds = large_lds_bytes(n2, k2, kr);
+    const dim3 grid((unsigned)(s.rows < 4096 ? s.rows : 4096));
+    hipLaunchKernelGGL(select_large_kernel, grid, dim3(kLargeThreads), lds, st, a);
+    return hipGetLastError();
+  }
   SelectArgs a;
   a.hs = half_scores;
   a.idx = idx;

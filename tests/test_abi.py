@@ -43,7 +43,7 @@ def _ws(desc, stage=B.STAGE_LAYER):
 
 
 @pytest.mark.parametrize("field,value,status", [
-    ("K", 65, UNSUPPORTED), ("K", 0, INVALID), ("d", 100, INVALID), ("d", 0, INVALID),
+    ("K", 4097, UNSUPPORTED), ("K", 0, INVALID), ("d", 100, INVALID), ("d", 0, INVALID),
     ("d_key", 300, INVALID), ("d_key", 12, INVALID), ("n_rows", 0, INVALID),
     ("n_rows", 4097, INVALID), ("H", 0, INVALID), ("dtype", 7, INVALID), ("act", 3, INVALID),
     ("query_mode", 2, INVALID), ("group_size", 2, UNSUPPORTED), ("group_size", 0, INVALID),
@@ -144,6 +144,6 @@ def test_status_strings():
 
 def test_binding_raises_on_error():
     d = B.make_desc(synth.WORKLOADS["small_bf16"])
-    d.K = 100
+    d.K = 5000
     with pytest.raises(B.OmnimoeError):
         B.omnimoe_workspace_size(d, B.STAGE_LAYER)

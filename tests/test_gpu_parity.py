@@ -52,6 +52,11 @@ SHAPES = {
                                   H=3, K=7),
     "skinny1_bf16": synth.Workload("skinny1_bf16", T=1, d=1024, n_rows=48, n_cols=80, d_key=512,
                                    H=2, K=12),
+    # K > 64 (workgroup-per-row selection), incl. the paper's benchmark grid 320 x 320, K = 512
+    "k256_bf16": synth.Workload("k256_bf16", T=100, d=256, n_rows=64, n_cols=64, d_key=64, H=2,
+                                K=256),
+    "paper_k512_bf16": synth.Workload("paper_k512_bf16", T=256, d=1024, n_rows=320, n_cols=320,
+                                      d_key=512, H=1, K=512),
 }
 
 
@@ -118,6 +123,10 @@ SELECT_CASES = [
     (50, 1, 7, 2, 40, False), (8, 8, 64, 1, 30, False), (4096, 4096, 16, 1, 6, False),
     (3000, 17, 20, 2, 9, False), (64, 64, 8, 1, 64, True), (256, 256, 16, 2, 64, True),
     (1024, 1024, 64, 1, 16, True), (16, 16, 33, 3, 20, True),
+    # K > 64: one workgroup per row (full half sorts, Cartesian radix select)
+    (320, 320, 512, 1, 12, False), (320, 320, 4096, 1, 6, False), (64, 64, 65, 2, 20, False),
+    (1024, 1024, 128, 8, 8, False), (4096, 4096, 4096, 1, 3, False), (50, 7, 300, 2, 10, False),
+    (16, 16, 256, 1, 8, False), (256, 256, 1000, 1, 10, True), (64, 64, 200, 2, 12, True),
 ]
 
 
