@@ -329,7 +329,9 @@ def main():
     # Ablation of the router (Table 3, "w/o Cartesian Product Router"): a dense router with a
     # gating vector per expert, all N logits per (token, head) materialised.
     dense_bytes = w.T * w.H * w.N * 4
-    if dense_bytes <= (8 << 30):
+    if w.K > 64:
+        no_cpr = {"skipped": "the dense router's selection takes K <= 64"}
+    elif dense_bytes <= (8 << 30):
         wg = dev(_synth.make_gate_table(w))
         wsd = P.workspace(desc, 5)
         idx_d, g_d = torch.empty_like(idx), torch.empty_like(g)

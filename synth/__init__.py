@@ -152,6 +152,12 @@ WORKLOADS: Dict[str, Workload] = {
     # tables replicated (data-parallel): 2048 tokens against all 1024^2 experts.
     "dp8share_bf16": Workload("dp8share_bf16", T=2048, d=2048, n_rows=1024, n_cols=1024,
                               d_key=1024, H=8, K=16),
+    # The paper's speed-benchmark configuration (Table A): d = 1024, N = 102,400 = 320^2, one
+    # head, 4096 tokens, K = 512 and K = 4096 (reuse per active expert eta ~ 20 and ~ 160).
+    "paper_k512_bf16": Workload("paper_k512_bf16", T=4096, d=1024, n_rows=320, n_cols=320,
+                                d_key=512, H=1, K=512),
+    "paper_k4096_bf16": Workload("paper_k4096_bf16", T=4096, d=1024, n_rows=320, n_cols=320,
+                                 d_key=512, H=1, K=4096),
     # One decode step of a batch of 64, and a single token.
     "decode64_bf16": Workload("decode64_bf16", T=64, d=2048, n_rows=1024, n_cols=1024,
                               d_key=1024, H=8, K=16),

@@ -445,6 +445,23 @@ def test_dp_share_shape_sampled(train_tables):
     assert np.isfinite(y).all()
 
 
+@pytest.mark.parametrize("name", ["paper_k512_bf16", "paper_k4096_bf16"])
+def test_paper_benchmark_shapes_sampled(name):
+    # The paper's speed-benchmark shape: 4096 tokens, 320 x 320 experts of d = 1024, one head,
+    # K = 512 and 4096 (about 16.8 M tasks at K = 4096), checked on sampled tokens.
+    w = W[name]
+    say(f"[full] {name} T={w.T} K={w.K}")
+    kr, kc = synth.make_keys(w)
+    dev = {"keys_row": to_dev(kr), "keys_col": to_dev(kc),
+           "u": to_dev(synth.make_expert_rows(w, "u")), "v": to_dev(synth.make_expert_rows(w, "v"))}
+    rng = np.random.default_rng(3)
+    tokens = np.unique(np.concatenate([[0, w.T - 1], rng.choice(w.T, 14, replace=False)]))
+    y, idx = _sampled_parity(w, dev, synth.as_f32(kr), synth.as_f32(kc), tokens)
+    srt = np.sort(idx.reshape(-1, w.K), axis=1)
+    assert np.all(np.diff(srt, axis=1) > 0) and idx.min() >= 0 and idx.max() < w.N
+    assert np.isfinite(y).all()
+
+
 @pytest.mark.parametrize("name", ["decode64_bf16", "decode1_bf16"])
 def test_decode_shapes(train_tables, name):
     dev, kr, kc = train_tables
