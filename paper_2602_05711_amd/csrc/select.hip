@@ -181,14 +181,15 @@ __device__ __forceinline__ int elem_index(int k) {
   return VEC ? 256 * (k >> 2) + 4 * lane_id() + (k & 3) : lane_id() + kWave * k;
 }
 
-template <int R, bool VEC>
+// FULL: n == 64 R, every register position holds a logit (no masks by index).
+template <int R, bool VEC, bool FULL>
 __device__ __forceinline__ void load_half(const float* __restrict__ p, int n, float (&v)[R]) {
   if constexpr (VEC) {
 #pragma unroll
     for (int c = 0; c < R / 4; ++c) {
       const int j0 = 256 * c + 4 * lane_id();
       float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (j0 < n) t = *(const float4*)(p + j0);
+      if (FULL || j0 < n) t = *(const float4*)(p + j0);
       v[4 * c] = t.x;
       v[4 * c + 1] = t.y;
       v[4 * c + 2] = t.z;
@@ -198,36 +199,42 @@ __device__ __forceinline__ void load_half(const float* __restrict__ p, int n, fl
 #pragma unroll
     for (int k = 0; k < R; ++k) {
       const int j = elem_index<R, VEC>(k);
-      v[k] = j < n ? p[j] : 0.f;
+      v[k] = (FULL || j < n) ? p[j] : 0.f;
     }
   }
 }
 
 // Finds one half's threshold and writes the survivors' keys to buf[0, 32). Returns the number
 // of survivors (those beyond 32 are not written).
-template <int R, bool VEC>
+template <int R, bool VEC, bool FULL>
 __device__ __forceinline__ int half_survivors(const float (&v)[R], int n, int kh, uint64_t* buf,
                                               uint32_t* theta_out) {
   uint32_t o[R];
   uint32_t mx = 0u;
 #pragma unroll
   for (int k = 0; k < R; ++k) {
-    o[k] = (elem_index<R, VEC>(k) < n) ? ord_f32(v[k]) : 0u;  // 0 sits below every finite value
+    // 0 sits below every finite value
+    o[k] = (FULL || elem_index<R, VEC>(k) < n) ? ord_f32(v[k]) : 0u;
     mx = o[k] > mx ? o[k] : mx;
   }
   const uint32_t theta = kth_largest_lane(mx, kh);
   *theta_out = theta;
-  const uint64_t lt = lanemask_lt();
-  int base = 0;
+  // Compaction: every lane counts its survivors, an exclusive scan over lanes gives each lane
+  // its first slot, and the lane writes its survivors in order (the sort that follows makes
+  // the slot order irrelevant).
+  int mine = 0;
+#pragma unroll
+  for (int k = 0; k < R; ++k) mine += o[k] >= theta ? 1 : 0;
+  int pos = wave_excl_scan_i32(mine);
+  const int total = __shfl(pos + mine, kWave - 1, kWave);
 #pragma unroll
   for (int k = 0; k < R; ++k) {
-    const bool f = o[k] >= theta;
-    const uint64_t bal = __ballot(f);
-    const int pos = base + __popcll(bal & lt);
-    if (f && pos < 32) buf[pos] = logit_key(o[k], elem_index<R, VEC>(k));
-    base += __popcll(bal);
+    if (o[k] >= theta) {
+      if (pos < 32) buf[pos] = logit_key(o[k], elem_index<R, VEC>(k));
+      ++pos;
+    }
   }
-  return base;
+  return total;
 }
 
 // Slow path for one half: the logits >= theta, sorted in batches of 64 read from memory and
@@ -252,7 +259,7 @@ __device__ __noinline__ uint64_t half_topk_batched(const float* __restrict__ p, 
   return best;
 }
 
-template <int R, bool VEC>
+template <int R, bool VEC, bool FULL>
 __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
   __shared__ uint16_t cand[kMaxCand];  // (a << 8) | b
   __shared__ int n_cand;
@@ -280,20 +287,20 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
   // The next row's logits are loaded while the current row is processed.
   float vr[R], vc[R];
   if (row < a.rows) {
-    load_half<R, VEC>(a.hs + row * (int64_t)(a.nr + a.nc), a.nr, vr);
-    load_half<R, VEC>(a.hs + row * (int64_t)(a.nr + a.nc) + a.nr, a.nc, vc);
+    load_half<R, VEC, FULL>(a.hs + row * (int64_t)(a.nr + a.nc), a.nr, vr);
+    load_half<R, VEC, FULL>(a.hs + row * (int64_t)(a.nr + a.nc) + a.nr, a.nc, vc);
   }
   for (; row < a.rows; row += stride) {
     const float* hr = a.hs + row * (int64_t)(a.nr + a.nc);
     float nr_[R], nc_[R];
     const int64_t nxt = row + stride;
     if (nxt < a.rows) {
-      load_half<R, VEC>(a.hs + nxt * (int64_t)(a.nr + a.nc), a.nr, nr_);
-      load_half<R, VEC>(a.hs + nxt * (int64_t)(a.nr + a.nc) + a.nr, a.nc, nc_);
+      load_half<R, VEC, FULL>(a.hs + nxt * (int64_t)(a.nr + a.nc), a.nr, nr_);
+      load_half<R, VEC, FULL>(a.hs + nxt * (int64_t)(a.nr + a.nc) + a.nr, a.nc, nc_);
     }
     uint32_t th_r, th_c;
-    const int cr = half_survivors<R, VEC>(vr, a.nr, kr, st, &th_r);
-    const int cc = half_survivors<R, VEC>(vc, a.nc, kc, st + 32, &th_c);
+    const int cr = half_survivors<R, VEC, FULL>(vr, a.nr, kr, st, &th_r);
+    const int cc = half_survivors<R, VEC, FULL>(vc, a.nc, kc, st + 32, &th_c);
     wave_lds_sync();
     if (cr <= 32 && cc <= 32) {
       // Both halves in one pass: rows sort in lanes 0-31, columns in lanes 32-63.
@@ -755,10 +762,12 @@ hipError_t launch_select(const Shape& s, const float* half_scores, int32_t* idx,
   const bool vec = s.nr % 4 == 0 && s.nc % 4 == 0;
 #define OMNIMOE_SELECT(R)                                                              \
   do {                                                                                 \
-    if (vec && (R) >= 4)                                                               \
-      hipLaunchKernelGGL((select_kernel<(R), true>), grid, block, 0, st, a);           \
+    if (vec && (R) >= 4 && s.nr == 64 * (R) && s.nc == 64 * (R))                       \
+      hipLaunchKernelGGL((select_kernel<(R), true, true>), grid, block, 0, st, a);     \
+    else if (vec && (R) >= 4)                                                          \
+      hipLaunchKernelGGL((select_kernel<(R), true, false>), grid, block, 0, st, a);    \
     else                                                                               \
-      hipLaunchKernelGGL((select_kernel<(R), false>), grid, block, 0, st, a);          \
+      hipLaunchKernelGGL((select_kernel<(R), false, false>), grid, block, 0, st, a);   \
   } while (0)
   if (nmax <= 64) OMNIMOE_SELECT(1);
   else if (nmax <= 128) OMNIMOE_SELECT(2);
