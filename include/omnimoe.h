@@ -71,8 +71,9 @@ typedef enum { OMNIMOE_QUERY_SPLIT = 0, OMNIMOE_QUERY_SHARED = 1 } omnimoe_query
  *               arithmetic is fp32 in every case.
  *   act         activation of Eq. 4: GELU (erf form) or SiLU.
  *   query_mode  OMNIMOE_QUERY_SPLIT or OMNIMOE_QUERY_SHARED.
- *   group_size  B of Sec. 2.3 (active experts per execution group); this build
- *               implements B = 1 and returns OMNIMOE_ERR_UNSUPPORTED otherwise.
+ *   group_size  B of Sec. 2.3, B >= 1: active experts per execution group. The schedule
+ *               orders tasks by (group, task id) (Eq. 13); B = 1 gives (expert, task id).
+ *               The layer's output does not depend on B.
  * T * H * K and T * H * (n_rows + n_cols) must each be below 2^31. */
 typedef struct {
   int64_t T;

@@ -42,7 +42,6 @@ omnimoe_status check_desc(const omnimoe_layer_desc* d, Shape* s) {
   if (d->dtype == OMNIMOE_F32 && d->d > 4096) return OMNIMOE_ERR_UNSUPPORTED;
   if (d->act != OMNIMOE_ACT_GELU && d->act != OMNIMOE_ACT_SILU) return OMNIMOE_ERR_INVALID_ARG;
   if (d->group_size < 1) return OMNIMOE_ERR_INVALID_ARG;
-  if (d->group_size != 1) return OMNIMOE_ERR_UNSUPPORTED;
   const int64_t rows = d->T * d->H;
   if (rows * d->K >= kIntMax || rows * (d->n_rows + d->n_cols) >= kIntMax)
     return OMNIMOE_ERR_INVALID_ARG;
@@ -60,6 +59,7 @@ omnimoe_status check_desc(const omnimoe_layer_desc* d, Shape* s) {
   s->rows = rows;
   s->M = rows * d->K;
   s->hk = d->H * d->K;
+  s->B = d->group_size;
   return OMNIMOE_OK;
 }
 

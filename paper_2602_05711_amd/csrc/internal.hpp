@@ -20,6 +20,7 @@ struct Shape {
   int64_t M;     // T * H * K
   int64_t rows;  // T * H
   int hk;        // H * K
+  int B;         // execution-group size of the schedule (Sec. 2.3)
 };
 
 // Logit GEMM: half_scores[t, h, 0:nr] = x[t, 0:dk] . keys_row[h, i, :],
@@ -43,8 +44,9 @@ hipError_t launch_select(const Shape& s, const float* half_scores, int32_t* idx,
 hipError_t launch_select_dense(int64_t rows, int64_t n, int K, const float* logits, int32_t* idx,
                                float* gates, hipStream_t st);
 
-// Radix-sort schedule. Workspace needs schedule_ws_bytes(M) bytes. On return sorted_keys
-// points into the workspace (expert id of each sorted position).
+// Radix-sort schedule. Workspace needs schedule_ws_bytes(M, N) bytes. On return sorted_keys
+// points into the workspace (expert id of each sorted position), or is NULL when the groups
+// hold more than one expert (then the expert of position i is idx[perm[i]]).
 size_t schedule_ws_bytes(int64_t M, int64_t N);
 hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, int32_t* active,
                            int32_t* active_offsets, int32_t* n_active, int32_t* dense_offsets,

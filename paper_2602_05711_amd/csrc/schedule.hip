@@ -9,6 +9,10 @@
 // Stability of every pass makes the final order (expert, task id), which is unique.
 // Segment extraction marks positions whose expert differs from the previous one and
 // compacts them with another scan into active / active_offsets / n_active.
+// Groups of B > 1 active experts (Eq. 13): each task gets the key q = rank(expert) / B, rank
+// being the expert's place in the active list, and a second stable radix sort of the task ids
+// by q gives the order (group, task id). Groups are unions of consecutive experts, so
+// active_offsets[q B] still marks where group q starts.
 // Everything is integer arithmetic; the LDS atomics only count.
 #include <algorithm>
 
@@ -267,6 +271,27 @@ __global__ __launch_bounds__(kThreads) void fill_i32_kernel(int32_t* dst, int64_
   if (i < n) dst[i] = v;
 }
 
+// rank[active[a]] = a for the n_active active experts.
+__global__ __launch_bounds__(kThreads) void rank_fill_kernel(const int32_t* active,
+                                                            const int32_t* n_active, int32_t* rank,
+                                                            int64_t cap, int64_t n_experts) {
+  const int64_t a = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (a >= cap || a >= *n_active) return;
+  const int32_t e = active[a];
+  if (e >= 0 && e < n_experts) rank[e] = (int32_t)a;
+}
+
+// Group key of every task: q[p] = rank[idx[p]] / B.
+__global__ __launch_bounds__(kThreads) void group_key_kernel(const int32_t* idx,
+                                                            const int32_t* rank, int32_t* q,
+                                                            int64_t m, int64_t n_experts, int b) {
+  const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (p >= m) return;
+  int32_t e = idx[p];
+  e = e < 0 ? 0 : (e >= n_experts ? (int32_t)(n_experts - 1) : e);
+  q[p] = rank[e] / b;
+}
+
 size_t align_up(size_t v) { return (v + 255) & ~(size_t)255; }
 
 int digit_bits_total(int64_t n_experts) {
@@ -433,63 +458,27 @@ hipError_t launch_fill_i32(int32_t* dst, int64_t n, int32_t value, hipStream_t s
   return hipGetLastError();
 }
 
-size_t schedule_ws_bytes(int64_t M, int64_t N) {
+namespace {
+
+int64_t partial_count(int64_t M) {
   const int64_t tiles = (M + kTile - 1) / kTile;
   const int64_t hist = (int64_t)kMaxRadix * (tiles > 0 ? tiles : 1);
-  const int64_t part = (std::max<int64_t>(hist, M) + kTile - 1) / kTile + 1;
-  size_t b = 0;
-  b += 4 * align_up((size_t)M * 4);      // keys/values ping-pong
-  b += align_up((size_t)hist * 4);       // histogram
-  b += align_up((size_t)part * 4);       // scan partials
-  (void)N;
-  return b;
+  return (std::max<int64_t>(hist, M) + kTile - 1) / kTile + 1;
 }
 
-hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, int32_t* active,
-                           int32_t* active_offsets, int32_t* n_active, int32_t* dense_offsets,
-                           void* ws, const int32_t** sorted_keys, hipStream_t st) {
-  const int64_t M = s.M;
-  char* w = (char*)ws;
-  int32_t* K0 = (int32_t*)w; w += align_up((size_t)M * 4);
-  int32_t* V0 = (int32_t*)w; w += align_up((size_t)M * 4);
-  int32_t* K1 = (int32_t*)w; w += align_up((size_t)M * 4);
-  int32_t* V1 = (int32_t*)w; w += align_up((size_t)M * 4);
-  const int num_tiles = (int)((M + kTile - 1) / kTile);
-  int32_t* hist = (int32_t*)w; w += align_up((size_t)kMaxRadix * num_tiles * 4);
-  int32_t* partial = (int32_t*)w;
+struct SortBuffers {
+  int32_t *k0, *v0, *k1, *v1, *hist, *partial;
+};
 
-  // Digit widths: the fewest passes of at most 10 bits, spread evenly.
-  const int total_bits = digit_bits_total(s.N);
+// Stable LSD radix sort of the task ids 0 .. M-1 by keys[] (all below 2^total_bits), in the
+// fewest passes of at most 10 bits. The sorted task ids go to ids_out; *keys_out points to the
+// sorted keys (one of the ping-pong buffers).
+hipError_t radix_sort_tasks(const int32_t* keys, int64_t M, int total_bits, int32_t* ids_out,
+                            const SortBuffers& b, const int32_t** keys_out, hipStream_t st) {
   const int passes = total_bits == 0 ? 1 : (total_bits + kMaxDigitBits - 1) / kMaxDigitBits;
   const int per = total_bits == 0 ? 1 : (total_bits + passes - 1) / passes;
-  if (M <= kSmallMax) {
-    SmallSched a;
-    a.idx = idx;
-    a.tmp_k[0] = K0;
-    a.tmp_k[1] = K1;
-    a.tmp_v[0] = V0;
-    a.tmp_v[1] = V1;
-    a.perm = perm;
-    a.active = active;
-    a.offsets = active_offsets;
-    a.n_active = n_active;
-    a.M = (int)M;
-    a.cap = (int)std::min<int64_t>(M, s.N);
-    a.passes = passes;
-    a.per = per;
-    a.total_bits = total_bits;
-    hipLaunchKernelGGL(schedule_small_kernel, dim3(1), dim3(kSmallThreads), 0, st, a);
-    *sorted_keys = (passes & 1) ? K0 : K1;
-    if (dense_offsets) {
-      const int64_t n = s.N + 1;
-      hipLaunchKernelGGL(dense_offsets_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)),
-                         dim3(kThreads), 0, st, (const int32_t*)active,
-                         (const int32_t*)active_offsets, (const int32_t*)n_active, dense_offsets,
-                         s.N);
-    }
-    return hipGetLastError();
-  }
-  const int32_t* kin = idx;
+  const int num_tiles = (int)((M + kTile - 1) / kTile);
+  const int32_t* kin = keys;
   const int32_t* vin = nullptr;
   int shift = 0;
   for (int ps = 0; ps < passes; ++ps) {
@@ -498,34 +487,109 @@ hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, in
     RadixPass p;
     p.keys_in = kin;
     p.vals_in = vin;
-    p.keys_out = (ps & 1) ? K1 : K0;
-    p.vals_out = last ? perm : ((ps & 1) ? V1 : V0);
-    p.hist = hist;
+    p.keys_out = (ps & 1) ? b.k1 : b.k0;
+    p.vals_out = last ? ids_out : ((ps & 1) ? b.v1 : b.v0);
+    p.hist = b.hist;
     p.n = M;
     p.shift = shift;
     p.bits = bits;
     p.num_tiles = num_tiles;
     hipLaunchKernelGGL(radix_upsweep_kernel, dim3(num_tiles), dim3(kThreads), 0, st, p);
     const int64_t hn = (int64_t)(1 << bits) * num_tiles;
-    hipError_t e = device_scan(ArrayVal{hist, hn}, EmitScan{hist, hn}, hn, partial, st);
+    hipError_t e = device_scan(ArrayVal{b.hist, hn}, EmitScan{b.hist, hn}, hn, b.partial, st);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(radix_downsweep_kernel, dim3(num_tiles), dim3(kThreads), 0, st, p);
     kin = p.keys_out;
     vin = p.vals_out;
     shift += bits;
   }
-  *sorted_keys = kin;
-  const int32_t cap = (int32_t)std::min<int64_t>(M, s.N);
-  hipError_t e = device_scan(HeadFlag{kin, M},
-                             EmitSegments{kin, active, active_offsets, n_active, cap, (int32_t)M},
-                             M, partial, st);
-  if (e != hipSuccess) return e;
+  *keys_out = kin;
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t schedule_ws_bytes(int64_t M, int64_t N) {
+  const int64_t tiles = (M + kTile - 1) / kTile;
+  const int64_t hist = (int64_t)kMaxRadix * (tiles > 0 ? tiles : 1);
+  size_t b = 0;
+  b += 4 * align_up((size_t)M * 4);               // keys/values ping-pong
+  b += align_up((size_t)hist * 4);                // histogram
+  b += align_up((size_t)partial_count(M) * 4);    // scan partials
+  b += align_up((size_t)N * 4);                   // expert -> rank in the active list (B > 1)
+  b += align_up((size_t)M * 4);                   // group key of every task (B > 1)
+  return b;
+}
+
+hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, int32_t* active,
+                           int32_t* active_offsets, int32_t* n_active, int32_t* dense_offsets,
+                           void* ws, const int32_t** sorted_keys, hipStream_t st) {
+  const int64_t M = s.M;
+  const int64_t tiles = (M + kTile - 1) / kTile;
+  char* w = (char*)ws;
+  SortBuffers b;
+  b.k0 = (int32_t*)w; w += align_up((size_t)M * 4);
+  b.v0 = (int32_t*)w; w += align_up((size_t)M * 4);
+  b.k1 = (int32_t*)w; w += align_up((size_t)M * 4);
+  b.v1 = (int32_t*)w; w += align_up((size_t)M * 4);
+  b.hist = (int32_t*)w; w += align_up((size_t)kMaxRadix * (tiles > 0 ? tiles : 1) * 4);
+  b.partial = (int32_t*)w; w += align_up((size_t)partial_count(M) * 4);
+  int32_t* rank = (int32_t*)w; w += align_up((size_t)s.N * 4);
+  int32_t* gkey = (int32_t*)w;
+  const int64_t cap64 = std::min<int64_t>(M, s.N);
+  const int32_t cap = (int32_t)cap64;
+
+  // Digit widths: the fewest passes of at most 10 bits, spread evenly.
+  const int total_bits = digit_bits_total(s.N);
+  if (M <= kSmallMax) {
+    const int passes = total_bits == 0 ? 1 : (total_bits + kMaxDigitBits - 1) / kMaxDigitBits;
+    const int per = total_bits == 0 ? 1 : (total_bits + passes - 1) / passes;
+    SmallSched a;
+    a.idx = idx;
+    a.tmp_k[0] = b.k0;
+    a.tmp_k[1] = b.k1;
+    a.tmp_v[0] = b.v0;
+    a.tmp_v[1] = b.v1;
+    a.perm = perm;
+    a.active = active;
+    a.offsets = active_offsets;
+    a.n_active = n_active;
+    a.M = (int)M;
+    a.cap = cap;
+    a.passes = passes;
+    a.per = per;
+    a.total_bits = total_bits;
+    hipLaunchKernelGGL(schedule_small_kernel, dim3(1), dim3(kSmallThreads), 0, st, a);
+    *sorted_keys = (passes & 1) ? b.k0 : b.k1;
+  } else {
+    const int32_t* sk = nullptr;
+    hipError_t e = radix_sort_tasks(idx, M, total_bits, perm, b, &sk, st);
+    if (e != hipSuccess) return e;
+    *sorted_keys = sk;
+    e = device_scan(HeadFlag{sk, M},
+                    EmitSegments{sk, active, active_offsets, n_active, cap, (int32_t)M}, M,
+                    b.partial, st);
+    if (e != hipSuccess) return e;
+  }
   if (dense_offsets) {
     const int64_t n = s.N + 1;
     hipLaunchKernelGGL(dense_offsets_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)),
                        dim3(kThreads), 0, st, (const int32_t*)active,
                        (const int32_t*)active_offsets, (const int32_t*)n_active, dense_offsets,
                        s.N);
+  }
+  if (s.B > 1) {
+    // Groups of B active experts: order the tasks by (rank / B, task id).
+    hipLaunchKernelGGL(rank_fill_kernel, dim3((unsigned)((cap64 + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, st, (const int32_t*)active, (const int32_t*)n_active,
+                       rank, cap64, s.N);
+    hipLaunchKernelGGL(group_key_kernel, dim3((unsigned)((M + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, st, idx, (const int32_t*)rank, gkey, M, s.N, s.B);
+    const int group_bits = digit_bits_total((cap64 + s.B - 1) / s.B);
+    const int32_t* gk = nullptr;
+    hipError_t e = radix_sort_tasks(gkey, M, group_bits, perm, b, &gk, st);
+    if (e != hipSuccess) return e;
+    *sorted_keys = nullptr;
   }
   return hipGetLastError();
 }

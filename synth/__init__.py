@@ -111,6 +111,7 @@ class Workload:
     query_mode: str = "split"    # "split" or "shared"
     seed: int = 0
     skew_alpha: float = 0.0
+    group_size: int = 1          # B of the schedule (active experts per execution group)
 
     @property
     def N(self) -> int:

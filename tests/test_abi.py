@@ -46,13 +46,20 @@ def _ws(desc, stage=B.STAGE_LAYER):
     ("K", 4097, UNSUPPORTED), ("K", 0, INVALID), ("d", 100, INVALID), ("d", 0, INVALID),
     ("d_key", 300, INVALID), ("d_key", 12, INVALID), ("n_rows", 0, INVALID),
     ("n_rows", 4097, INVALID), ("H", 0, INVALID), ("dtype", 7, INVALID), ("act", 3, INVALID),
-    ("query_mode", 2, INVALID), ("group_size", 2, UNSUPPORTED), ("group_size", 0, INVALID),
+    ("query_mode", 2, INVALID), ("group_size", 0, INVALID),
     ("T", -1, INVALID),
 ])
 def test_workspace_size_rejects(field, value, status):
     d = B.make_desc(synth.WORKLOADS["small_bf16"])
     setattr(d, field, value)
     assert _ws(d)[0] == status
+
+
+def test_group_sizes_are_accepted():
+    d = B.make_desc(synth.WORKLOADS["small_bf16"])
+    for b in (2, 7, 1 << 20):
+        d.group_size = b
+        assert _ws(d)[0] == OK
 
 
 def test_wide_fp32_is_unsupported():

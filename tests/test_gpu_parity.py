@@ -201,6 +201,61 @@ def test_schedule_bitexact(case):
     assert np.array_equal(dense.cpu().numpy(), rdense)
 
 
+GROUP_CASES = [
+    # (T, H, K, n_rows, n_cols, kind, B)
+    (256, 1, 8, 64, 64, "uniform", 2), (4096, 4, 16, 256, 256, "uniform", 7),
+    (16384, 8, 16, 1024, 1024, "zipf", 64), (64, 8, 16, 1024, 1024, "uniform", 3),
+    (3, 1, 1, 1, 7, "uniform", 5), (5000, 2, 3, 4096, 4096, "uniform", 1000),
+    (4096, 1, 512, 320, 320, "uniform", 16),
+]
+
+
+@pytest.mark.parametrize("case", GROUP_CASES, ids=[str(c) for c in GROUP_CASES])
+def test_schedule_groups_bitexact(case):
+    # Groups of B active experts (Eq. 13): tasks ordered by (group, task id).
+    T, H, K, nr, nc, kind, Bg = case
+    N = nr * nc
+    say(f"[schedule B={Bg}] T={T} H={H} K={K} N={N} {kind}")
+    rng = np.random.default_rng(T + 17 * K + N % 1009 + Bg)
+    M = T * H * K
+    if K > 16:
+        ids = np.stack([rng.choice(N, K, replace=False) for _ in range(T * H)]).astype(np.int32)
+    else:
+        ids = (_zipf_ids(rng, M, N) if kind == "zipf" else rng.integers(0, N, size=M)).astype(
+            np.int32)
+    w = synth.Workload("sch", T=T, d=16, n_rows=nr, n_cols=nc, d_key=8, H=H, K=K, dtype="f32")
+    d = B.make_desc(w)
+    d.group_size = Bg
+    A = min(M, N)
+    perm = torch.empty(M, dtype=torch.int32, device="cuda")
+    active = torch.full((A,), -7, dtype=torch.int32, device="cuda")
+    off = torch.full((A + 1,), -7, dtype=torch.int32, device="cuda")
+    na = torch.zeros(1, dtype=torch.int32, device="cuda")
+    dense = torch.empty(N + 1, dtype=torch.int32, device="cuda")
+    P.omnimoe_schedule(d, to_dev(ids.ravel()), perm, active, off, na, dense)
+    torch.cuda.synchronize()
+    rperm, ract, roff, rdense = oracle.schedule(oracle.desc(w, group_size=Bg), ids.ravel())
+    n = int(na.item())
+    assert n == len(ract)
+    assert np.array_equal(perm.cpu().numpy(), rperm)
+    assert np.array_equal(active.cpu().numpy()[:n], ract)
+    assert np.array_equal(off.cpu().numpy()[:n + 1], roff)
+    assert np.array_equal(dense.cpu().numpy(), rdense)
+
+
+@pytest.mark.parametrize("name", ["small_bf16", "skinny_bf16", "k256_bf16"])
+def test_layer_output_does_not_depend_on_group_size(name):
+    w = SHAPES[name]
+    inp, _ = host_inputs(w)
+    dev = upload(inp)
+    y1, i1, g1 = gpu_layer(w, dev)
+    for Bg in (4, 33):
+        say(f"[layer B={Bg}] {name}")
+        yb, ib, gb = gpu_layer(w.with_(group_size=Bg), dev)
+        assert np.array_equal(yb.view(np.uint8), y1.view(np.uint8))
+        assert np.array_equal(ib, i1) and np.array_equal(gb.view(np.uint8), g1.view(np.uint8))
+
+
 # ------------------------------------------------------------------ expert compute
 
 EXPERT_SHAPES = ["tiny_f32", "small_bf16", "ragged_bf16", "ragged_f32", "silu_k1_bf16",
