@@ -148,6 +148,88 @@ def cpu_model():
     return "unknown CPU"
 
 
+def extras(args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1):
+    """The shared SwiGLU branch and the two ablations of Table 3, timed like the layer."""
+    import torch
+    import paper_2602_05711_amd as P
+    import synth as _synth
+
+    # Ablation of the schedule (Table 3, "w/o Expert-Centric Scheduling"): the same expert
+    # compute token by token, each task gathering its own u and v rows.
+    y_tc = torch.empty_like(y)
+    tc = lambda: P.omnimoe_expert_forward_token_centric(  # noqa: E731
+        desc, d_in["x"], d_in["u"], d_in["v"], idx, g, y_tc, stream=stream)
+    for _ in range(2):
+        tc()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        tc()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    tc_ms = ev0.elapsed_time(ev1) / args.steps
+    ec_ms = per["schedule"] + per["expert_dot"] + per["accumulate"]
+    ablation = {"token_centric_expert_ms": tc_ms, "expert_centric_expert_ms": ec_ms,
+                "token_over_expert_centric": tc_ms / ec_ms,
+                "same_y": bool(torch.equal(y_tc, y))}
+    log(f"expert stage: expert-centric (schedule + dot + accumulate) {ec_ms:.3f} ms, "
+        f"token-centric {tc_ms:.3f} ms")
+    del y_tc
+
+    # The full OmniMoE FFN adds the shared dense SwiGLU branch (Eq. 7) to the routed output;
+    # its width here is d_ff = d, the ratio of the paper's benchmark configuration.
+    d_ff = w.d
+    gu, dn = _synth.make_mlp_weights(w, d_ff)
+    gu, dn = dev(gu), dev(dn)
+    ws_mlp = torch.empty(P.omnimoe_shared_mlp_workspace_size(desc, d_ff), dtype=torch.uint8,
+                         device="cuda")
+    mlp = lambda: P.omnimoe_shared_mlp(  # noqa: E731
+        desc, d_ff, d_in["x"], gu, dn, y, ws=ws_mlp, stream=stream)
+    for _ in range(2):
+        mlp()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        mlp()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    mlp_ms = ev0.elapsed_time(ev1) / args.steps
+    mlp_flop = 2.0 * w.T * w.d * 3 * d_ff
+    shared_mlp = {"d_ff": d_ff, "ms": mlp_ms, "TFLOPs": mlp_flop / (mlp_ms * 1e-3) / 1e12,
+                  "ffn_ms": ms_step + mlp_ms, "routed_share": ms_step / (ms_step + mlp_ms)}
+    log(f"shared SwiGLU branch (d_ff={d_ff}): {mlp_ms:.3f} ms; routed layer + branch "
+        f"{ms_step + mlp_ms:.3f} ms")
+    del gu, dn, ws_mlp
+
+    # Ablation of the router (Table 3, "w/o Cartesian Product Router"): a dense router with a
+    # gating vector per expert, all N logits per (token, head) materialised.
+    dense_bytes = w.T * w.H * w.N * 4
+    if w.K > 64:
+        no_cpr = {"skipped": "the dense router's selection takes K <= 64"}
+    elif dense_bytes <= (8 << 30):
+        wg = dev(_synth.make_gate_table(w))
+        wsd = P.workspace(desc, 5)
+        idx_d, g_d = torch.empty_like(idx), torch.empty_like(g)
+        rd = lambda: P.omnimoe_route_dense(  # noqa: E731
+            desc, d_in["x"], wg, idx_d, g_d, ws=wsd, stream=stream)
+        for _ in range(2):
+            rd()
+        ev0.record(stream)
+        for _ in range(args.steps):
+            rd()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        dr_ms = ev0.elapsed_time(ev1) / args.steps
+        cr_ms = per["score"] + per["select"]
+        no_cpr = {"dense_route_ms": dr_ms, "cartesian_route_ms": cr_ms,
+                  "route_ratio": dr_ms / cr_ms, "logit_bytes": dense_bytes,
+                  "layer_ratio": (dr_ms + ec_ms) / (cr_ms + ec_ms)}
+        log(f"router: Cartesian {cr_ms:.3f} ms, dense over all {w.N} experts {dr_ms:.3f} ms")
+        del wg, wsd
+    else:
+        no_cpr = {"skipped": f"the dense logits would take {dense_bytes / 2**30:.0f} GiB"}
+
+    return ablation, shared_mlp, no_cpr
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -164,6 +246,9 @@ def main():
                     help="time replays of one layer call captured in a HIP graph")
     ap.add_argument("--no-cold", action="store_true",
                     help="skip the second timing with the caches flushed before each step")
+    ap.add_argument("--layer-only", action="store_true",
+                    help="time the layer alone: no cold timing, shared branch or ablations (for "
+                         "kernel traces and counters that should hold the layer's kernels only)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="after timing, run a plain device copy of this many bytes twice "
                          "(a known-size reference for rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -239,7 +324,7 @@ def main():
     # Cold steps: before each one a 512 MiB fill evicts the L2 and the MALL, so the step reads
     # its inputs (x, sub-keys, expert rows) from HBM; only the layer call sits between events.
     cold = None
-    if not args.no_cold:
+    if not (args.no_cold or args.layer_only):
         flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                for _ in range(args.steps)]
@@ -280,79 +365,10 @@ def main():
     routing = routing_stats(idx.cpu().numpy(), w.N)
     assert routing["n_active"] == n_active
 
-    # Ablation of the schedule (Table 3, "w/o Expert-Centric Scheduling"): the same expert
-    # compute token by token, each task gathering its own u and v rows.
-    y_tc = torch.empty_like(y)
-    tc = lambda: P.omnimoe_expert_forward_token_centric(  # noqa: E731
-        desc, d_in["x"], d_in["u"], d_in["v"], idx, g, y_tc, stream=stream)
-    for _ in range(2):
-        tc()
-    ev0.record(stream)
-    for _ in range(args.steps):
-        tc()
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    tc_ms = ev0.elapsed_time(ev1) / args.steps
-    ec_ms = per["schedule"] + per["expert_dot"] + per["accumulate"]
-    ablation = {"token_centric_expert_ms": tc_ms, "expert_centric_expert_ms": ec_ms,
-                "token_over_expert_centric": tc_ms / ec_ms,
-                "same_y": bool(torch.equal(y_tc, y))}
-    log(f"expert stage: expert-centric (schedule + dot + accumulate) {ec_ms:.3f} ms, "
-        f"token-centric {tc_ms:.3f} ms")
-    del y_tc
-
-    # The full OmniMoE FFN adds the shared dense SwiGLU branch (Eq. 7) to the routed output;
-    # its width here is d_ff = d, the ratio of the paper's benchmark configuration.
-    import synth as _synth
-    d_ff = w.d
-    gu, dn = _synth.make_mlp_weights(w, d_ff)
-    gu, dn = dev(gu), dev(dn)
-    ws_mlp = torch.empty(P.omnimoe_shared_mlp_workspace_size(desc, d_ff), dtype=torch.uint8,
-                         device="cuda")
-    mlp = lambda: P.omnimoe_shared_mlp(  # noqa: E731
-        desc, d_ff, d_in["x"], gu, dn, y, ws=ws_mlp, stream=stream)
-    for _ in range(2):
-        mlp()
-    ev0.record(stream)
-    for _ in range(args.steps):
-        mlp()
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    mlp_ms = ev0.elapsed_time(ev1) / args.steps
-    mlp_flop = 2.0 * w.T * w.d * 3 * d_ff
-    shared_mlp = {"d_ff": d_ff, "ms": mlp_ms, "TFLOPs": mlp_flop / (mlp_ms * 1e-3) / 1e12,
-                  "ffn_ms": ms_step + mlp_ms, "routed_share": ms_step / (ms_step + mlp_ms)}
-    log(f"shared SwiGLU branch (d_ff={d_ff}): {mlp_ms:.3f} ms; routed layer + branch "
-        f"{ms_step + mlp_ms:.3f} ms")
-    del gu, dn, ws_mlp
-
-    # Ablation of the router (Table 3, "w/o Cartesian Product Router"): a dense router with a
-    # gating vector per expert, all N logits per (token, head) materialised.
-    dense_bytes = w.T * w.H * w.N * 4
-    if w.K > 64:
-        no_cpr = {"skipped": "the dense router's selection takes K <= 64"}
-    elif dense_bytes <= (8 << 30):
-        wg = dev(_synth.make_gate_table(w))
-        wsd = P.workspace(desc, 5)
-        idx_d, g_d = torch.empty_like(idx), torch.empty_like(g)
-        rd = lambda: P.omnimoe_route_dense(  # noqa: E731
-            desc, d_in["x"], wg, idx_d, g_d, ws=wsd, stream=stream)
-        for _ in range(2):
-            rd()
-        ev0.record(stream)
-        for _ in range(args.steps):
-            rd()
-        ev1.record(stream)
-        torch.cuda.synchronize()
-        dr_ms = ev0.elapsed_time(ev1) / args.steps
-        cr_ms = per["score"] + per["select"]
-        no_cpr = {"dense_route_ms": dr_ms, "cartesian_route_ms": cr_ms,
-                  "route_ratio": dr_ms / cr_ms, "logit_bytes": dense_bytes,
-                  "layer_ratio": (dr_ms + ec_ms) / (cr_ms + ec_ms)}
-        log(f"router: Cartesian {cr_ms:.3f} ms, dense over all {w.N} experts {dr_ms:.3f} ms")
-        del wg, wsd
-    else:
-        no_cpr = {"skipped": f"the dense logits would take {dense_bytes / 2**30:.0f} GiB"}
+    ablation = shared_mlp = no_cpr = None
+    if not args.layer_only:
+        ablation, shared_mlp, no_cpr = extras(args, w, desc, d_in, dev, idx, g, y, stream, per,
+                                              ms_step, ev0, ev1)
 
     work = algorithmic_work(w, n_active)
     kernels = {}
