@@ -306,8 +306,9 @@ int digit_bits_total(int64_t n_experts) {
 // One workgroup of 16 waves sorts up to 8192 tasks and extracts the segments in a single
 // launch (decode shapes). Same algorithm as the multi-kernel path: per pass, wave w ranks its
 // contiguous slice of tasks stably with ballot-matched peers and per-wave digit counters, the
-// (digit, wave) counts are scanned digit-major, and tasks scatter; then segment heads are
-// counted and compacted with a block scan.
+// (digit, wave) counts are scanned digit-major, and tasks scatter. Keys and task ids stay in
+// LDS between passes (only the last pass writes perm and the sorted keys out); then segment
+// heads are counted from LDS and compacted with a block scan.
 
 constexpr int kSmallWaves = 16;
 constexpr int kSmallThreads = kSmallWaves * kWave;
@@ -316,10 +317,8 @@ constexpr int kSmallMax = kSmallThreads * kSmallRounds;  // 8192
 
 struct SmallSched {
   const int32_t* idx;
-  int32_t* tmp_k[2];
-  int32_t* tmp_v[2];
+  int32_t* sorted;  // expert id of each sorted position
   int32_t* perm;
-  int32_t* sorted;  // final keys (one of tmp_k)
   int32_t* active;
   int32_t* offsets;
   int32_t* n_active;
@@ -332,13 +331,13 @@ __global__ __launch_bounds__(kSmallThreads) void schedule_small_kernel(SmallSche
   __shared__ int cnt[kSmallWaves][kMaxRadix];
   __shared__ int dsum[kMaxRadix];
   __shared__ int wsum[kSmallWaves];
+  __shared__ int skey[kSmallMax];  // keys and task ids between passes, then the sorted keys
+  __shared__ int sval[kSmallMax];
   const int tid = threadIdx.x, l = lane_id(), w = tid >> 6;
   const int slice = (a.M + kSmallWaves - 1) / kSmallWaves;
   const int wbeg = w * slice;
   const int wend = wbeg + slice < a.M ? wbeg + slice : a.M;
   const uint64_t lt = lanemask_lt();
-  const int32_t* kin = a.idx;
-  const int32_t* vin = nullptr;
   int shift = 0;
   for (int ps = 0; ps < a.passes; ++ps) {
     const bool last = ps == a.passes - 1;
@@ -347,18 +346,16 @@ __global__ __launch_bounds__(kSmallThreads) void schedule_small_kernel(SmallSche
     if (bits < 1) bits = 1;
     const int radix = 1 << bits;
     const uint32_t mask = (uint32_t)radix - 1u;
-    int32_t* kout = a.tmp_k[ps & 1];
-    int32_t* vout = last ? a.perm : a.tmp_v[ps & 1];
     for (int i = tid; i < kSmallWaves * kMaxRadix; i += kSmallThreads) (&cnt[0][0])[i] = 0;
-    __syncthreads();
     int key[kSmallRounds], val[kSmallRounds], rank[kSmallRounds];
 #pragma unroll
     for (int r = 0; r < kSmallRounds; ++r) {
       const int i = wbeg + r * kWave + l;
       const bool valid = i < wend;
-      key[r] = valid ? kin[i] : 0;
-      val[r] = valid ? (vin ? vin[i] : i) : 0;
+      key[r] = valid ? (ps == 0 ? a.idx[i] : skey[i]) : 0;
+      val[r] = valid ? (ps == 0 ? i : sval[i]) : 0;
     }
+    __syncthreads();
 #pragma unroll
     for (int r = 0; r < kSmallRounds; ++r) {
       const int i = wbeg + r * kWave + l;
@@ -411,20 +408,22 @@ __global__ __launch_bounds__(kSmallThreads) void schedule_small_kernel(SmallSche
       if (i < wend) {
         const uint32_t d = ((uint32_t)key[r] >> shift) & mask;
         const int pos = cnt[w][d] + rank[r];
-        kout[pos] = key[r];
-        vout[pos] = val[r];
+        skey[pos] = key[r];
+        sval[pos] = val[r];
+        if (last) {
+          a.sorted[pos] = key[r];
+          a.perm[pos] = val[r];
+        }
       }
     }
     __syncthreads();
-    kin = kout;
-    vin = vout;
     shift += bits;
   }
-  // segment heads: each thread owns 8 consecutive sorted positions
+  // segment heads: each thread owns up to 8 consecutive sorted positions (keys in LDS)
   const int per_t = (a.M + kSmallThreads - 1) / kSmallThreads;
   const int b0 = tid * per_t;
   int heads = 0;
-  for (int i = b0; i < b0 + per_t && i < a.M; ++i) heads += (i == 0 || kin[i] != kin[i - 1]);
+  for (int i = b0; i < b0 + per_t && i < a.M; ++i) heads += (i == 0 || skey[i] != skey[i - 1]);
   const int ex = wave_excl_scan_i32(heads);
   if (l == kWave - 1) wsum[w] = ex + heads;
   __syncthreads();
@@ -436,9 +435,9 @@ __global__ __launch_bounds__(kSmallThreads) void schedule_small_kernel(SmallSche
   }
   int pos = off + ex;
   for (int i = b0; i < b0 + per_t && i < a.M; ++i) {
-    if (i == 0 || kin[i] != kin[i - 1]) {
+    if (i == 0 || skey[i] != skey[i - 1]) {
       if (pos < a.cap) {
-        a.active[pos] = kin[i];
+        a.active[pos] = skey[i];
         a.offsets[pos] = i;
       }
       ++pos;
@@ -546,10 +545,7 @@ hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, in
     const int per = total_bits == 0 ? 1 : (total_bits + passes - 1) / passes;
     SmallSched a;
     a.idx = idx;
-    a.tmp_k[0] = b.k0;
-    a.tmp_k[1] = b.k1;
-    a.tmp_v[0] = b.v0;
-    a.tmp_v[1] = b.v1;
+    a.sorted = b.k0;
     a.perm = perm;
     a.active = active;
     a.offsets = active_offsets;
@@ -560,7 +556,7 @@ hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, in
     a.per = per;
     a.total_bits = total_bits;
     hipLaunchKernelGGL(schedule_small_kernel, dim3(1), dim3(kSmallThreads), 0, st, a);
-    *sorted_keys = (passes & 1) ? b.k0 : b.k1;
+    *sorted_keys = b.k0;
   } else {
     const int32_t* sk = nullptr;
     hipError_t e = radix_sort_tasks(idx, M, total_bits, perm, b, &sk, st);
