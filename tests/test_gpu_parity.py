@@ -646,3 +646,43 @@ def test_shared_mlp_train_shape_sampled():
     rng = np.random.default_rng(5)
     tokens = np.unique(np.concatenate([[0, w.T - 1], rng.choice(w.T, 30, replace=False)]))
     _mlp_parity(w, 2048, tokens)
+
+
+# ------------------------------------------------------------------ plain-C caller of the ABI
+
+@pytest.mark.parametrize("name", ["tiny_f32", "small_bf16"])
+def test_c_abi_caller(name, tmp_path):
+    # tests/abi_c/layer_main calls omnimoe_workspace_size and omnimoe_layer_forward from C with
+    # hipMalloc'd buffers (no Python in the loop); its output must equal the binding's bit for
+    # bit and the oracle's within tolerance.
+    import os
+    import subprocess
+    w = W[name]
+    exe = os.path.join(os.path.dirname(os.path.abspath(__file__)), "abi_c", "layer_main")
+    assert os.path.exists(exe), "build() compiles tests/abi_c/layer_main"
+    inp, f = host_inputs(w)
+    d = B.make_desc(w)
+    src, dst = tmp_path / "in.bin", tmp_path / "out.bin"
+    with open(src, "wb") as fh:
+        fh.write(bytes(d))
+        for k in ("x", "keys_row", "keys_col", "u", "v"):
+            fh.write(np.ascontiguousarray(inp[k]).tobytes())
+    say(f"[c abi] {name}")
+    r = subprocess.run([exe, str(src), str(dst)], capture_output=True, text=True, timeout=120)
+    say(r.stdout.strip(), r.stderr.strip())
+    assert r.returncode == 0
+    raw = np.fromfile(dst, dtype=np.uint8)
+    ny, nm = w.T * w.d * 4, w.M * 4
+    assert raw.size == ny + 2 * nm
+    y = raw[:ny].view(np.float32).reshape(w.T, w.d)
+    idx = raw[ny:ny + nm].view(np.int32).reshape(w.T, w.H, w.K)
+    g = raw[ny + nm:].view(np.float32).reshape(w.T, w.H, w.K)
+    y_b, idx_b, g_b = gpu_layer(w, upload(inp))
+    assert np.array_equal(y.view(np.uint8), y_b.view(np.uint8))
+    assert np.array_equal(idx, idx_b) and np.array_equal(g.view(np.uint8), g_b.view(np.uint8))
+    dsc = oracle.desc(w)
+    sr, sc = oracle.half_scores(dsc, f["x"], f["keys_row"], f["keys_col"])
+    ref_idx, _, ref_g, _ = oracle.select(dsc, sr, sc, oracle.CARTESIAN)
+    same = np.all(idx == ref_idx, axis=(1, 2))
+    y_ref = oracle.expert_forward(dsc, f["x"], f["u"], f["v"], ref_idx, ref_g)
+    assert row_rel_err(y, y_ref)[same].max() <= tol(w)
