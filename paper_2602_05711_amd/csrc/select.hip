@@ -390,6 +390,8 @@ struct LargeShared {
   uint32_t tn, mn;   // the same for the ~id part
   int krem;          // keys still to select at and below the current digit
   int count;         // gathered keys
+  int first_pass;    // first radix pass that needs a histogram
+  uint64_t wlo[4], whi[4];
   int wint[4];
   float wsum[4];
 };
@@ -483,22 +485,11 @@ __global__ __launch_bounds__(kLargeThreads) void select_large_kernel(LargeArgs a
     }
     const uint64_t* rk = hk;
     const uint64_t* ck = hk + n2;
-    // 3. radix select of the K-th largest candidate key, eight bits at a time from the top
-    if (tid == 0) {
-      sh.ts = 0ull;
-      sh.ms = 0ull;
-      sh.tn = 0u;
-      sh.mn = 0u;
-      sh.krem = K;
-      sh.count = 0;
-    }
-    for (int pass = 0; pass < 12; ++pass) {
-      for (int i = tid; i < 256; i += kLargeThreads) sh.hist[i] = 0u;
-      __syncthreads();
-      const uint64_t ts = sh.ts, ms = sh.ms;
-      const uint32_t tn = sh.tn, mn = sh.mn;
-      const int sh_s = 56 - 8 * pass;            // digit position in the score word (pass < 8)
-      const int sh_n = 24 - 8 * (pass - 8);      // digit position in the id word (pass >= 8)
+    // 3. radix select of the K-th largest candidate key, eight bits at a time from the top.
+    // The leading bytes that every candidate's score shares are taken as decided without a
+    // histogram pass: the minimum and maximum score keys bound them.
+    {
+      uint64_t lo = ~0ull, hi = 0ull;
       int ra = a_first, rb = c0 - (c0 < P ? (int)cum[a_first] : 0);
       int rend = c0 < P ? (int)cum[ra + 1] : 0;
       for (int c = c0; c < c1; ++c) {
@@ -511,11 +502,72 @@ __global__ __launch_bounds__(kLargeThreads) void select_large_kernel(LargeArgs a
         uint32_t kn;
         cand_key(rk, ck, ra, rb, a.nc, &ks, &kn);
         ++rb;
+        lo = ks < lo ? ks : lo;
+        hi = ks > hi ? ks : hi;
+      }
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) {
+        const uint64_t olo = shfl_xor_u64(lo, m), ohi = shfl_xor_u64(hi, m);
+        lo = olo < lo ? olo : lo;
+        hi = ohi > hi ? ohi : hi;
+      }
+      if (l == 0) {
+        sh.wlo[w] = lo;
+        sh.whi[w] = hi;
+      }
+      __syncthreads();
+      if (tid == 0) {
+        uint64_t mn = sh.wlo[0], mx = sh.whi[0];
+        for (int ww = 1; ww < 4; ++ww) {
+          mn = sh.wlo[ww] < mn ? sh.wlo[ww] : mn;
+          mx = sh.whi[ww] > mx ? sh.whi[ww] : mx;
+        }
+        int common = 0;  // leading bytes shared by every score key
+        while (common < 8 && ((mn ^ mx) >> (56 - 8 * common)) == 0) ++common;
+        const uint64_t mask = common == 0 ? 0ull : (~0ull << (64 - 8 * common));
+        sh.ts = mx & mask;
+        sh.ms = mask;
+        sh.tn = 0u;
+        sh.mn = 0u;
+        sh.krem = K;
+        sh.count = 0;
+        sh.first_pass = common;
+      }
+      __syncthreads();
+    }
+    for (int pass = sh.first_pass; pass < 12; ++pass) {
+      for (int i = tid; i < 256; i += kLargeThreads) sh.hist[i] = 0u;
+      __syncthreads();
+      const uint64_t ts = sh.ts, ms = sh.ms;
+      const uint32_t tn = sh.tn, mn = sh.mn;
+      const int sh_s = 56 - 8 * pass;            // digit position in the score word (pass < 8)
+      const int sh_n = 24 - 8 * (pass - 8);      // digit position in the id word (pass >= 8)
+      int ra = a_first, rb = c0 - (c0 < P ? (int)cum[a_first] : 0);
+      int rend = c0 < P ? (int)cum[ra + 1] : 0;
+      // runs of equal digits along the thread's chunk are counted before one LDS atomic, so
+      // bins that nearly every candidate hits are not serialised over all of them
+      uint32_t run_dg = 0u, run_n = 0u;
+      for (int c = c0; c < c1; ++c) {
+        while (c >= rend && ra < kr - 1) {  // each row rank holds at least one candidate
+          ++ra;
+          rb = 0;
+          rend = (int)cum[ra + 1];
+        }
+        uint64_t ks;
+        uint32_t kn;
+        cand_key(rk, ck, ra, rb, a.nc, &ks, &kn);
+        ++rb;
         if ((ks & ms) == ts && (kn & mn) == tn) {
           const uint32_t dg = pass < 8 ? (uint32_t)(ks >> sh_s) & 0xFFu : (kn >> sh_n) & 0xFFu;
-          atomicAdd(&sh.hist[dg], 1u);
+          if (run_n != 0u && dg != run_dg) {
+            atomicAdd(&sh.hist[run_dg], run_n);
+            run_n = 0u;
+          }
+          run_dg = dg;
+          ++run_n;
         }
       }
+      if (run_n != 0u) atomicAdd(&sh.hist[run_dg], run_n);
       __syncthreads();
       if (w == 0) {
         // largest digit whose suffix count reaches krem: lane l holds bins 4l .. 4l + 3
