@@ -55,10 +55,15 @@ def _load():
         lib.omnimoe_ref_route_dense.argtypes = [D, P, P, P, P, P, ctypes.c_int]
         lib.omnimoe_ref_select_dense_f32.argtypes = [D, P, P, P, ctypes.c_int]
         lib.omnimoe_ref_shared_mlp.argtypes = [D, ctypes.c_int32, P, P, P, P, ctypes.c_int]
+        lib.omnimoe_ref_expert_backward.argtypes = [D, P, P, P, P, P, P, P, P, P, P, P, P, P,
+                                                    ctypes.c_int]
+        lib.omnimoe_ref_act_grad.argtypes = [ctypes.c_int, ctypes.c_double]
+        lib.omnimoe_ref_act_grad.restype = ctypes.c_double
         lib.omnimoe_ref_act.argtypes = [ctypes.c_int, ctypes.c_double]
         lib.omnimoe_ref_act.restype = ctypes.c_double
         for f in ("half_scores", "select", "select_f32", "schedule", "expert_forward",
-                  "layer_forward", "route_dense", "select_dense_f32", "shared_mlp"):
+                  "layer_forward", "route_dense", "select_dense_f32", "shared_mlp",
+                  "expert_backward"):
             getattr(lib, "omnimoe_ref_" + f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -228,6 +233,40 @@ def shared_mlp(dsc: RefDesc, x, w_gu, w_down, y=None, n_threads=None):
     _check(lib.omnimoe_ref_shared_mlp(ctypes.byref(dsc), d_ff, px, pgu, pwd, out.ctypes.data,
                                       n_threads or default_threads()), "shared_mlp")
     return out
+
+
+def expert_backward(dsc: RefDesc, x, u, v, idx, gates, dy, n_threads=None):
+    """Gradients of L = sum_t dy_t . y_t through the expert compute, fp64: a dict with dx [T, d],
+    active [A], du_rows / dv_rows [A, d] (rows of the active experts, ascending id), dgates and
+    dscores [T, H, K]."""
+    lib = _load()
+    x, px = _f32(x)
+    u, pu = _f32(u)
+    v, pv = _f32(v)
+    idx = np.ascontiguousarray(idx, np.int32)
+    gates = np.ascontiguousarray(gates, np.float64)
+    dy = np.ascontiguousarray(dy, np.float64)
+    T, D = dsc.T, dsc.d
+    M = T * dsc.H * dsc.K
+    cap = min(M, dsc.n_rows * dsc.n_cols)
+    dx = np.empty((T, D), np.float64)
+    du = np.empty((cap, D), np.float64)
+    dv = np.empty((cap, D), np.float64)
+    active = np.empty(cap, np.int32)
+    na = np.zeros(1, np.int32)
+    dg = np.empty((T, dsc.H, dsc.K), np.float64)
+    ds = np.empty((T, dsc.H, dsc.K), np.float64)
+    _check(lib.omnimoe_ref_expert_backward(
+        ctypes.byref(dsc), px, pu, pv, idx.ctypes.data, gates.ctypes.data, dy.ctypes.data,
+        dx.ctypes.data, du.ctypes.data, dv.ctypes.data, active.ctypes.data, na.ctypes.data,
+        dg.ctypes.data, ds.ctypes.data, n_threads or default_threads()), "expert_backward")
+    A = int(na[0])
+    return {"dx": dx, "active": active[:A], "du_rows": du[:A], "dv_rows": dv[:A],
+            "dgates": dg, "dscores": ds}
+
+
+def act_grad(kind: int, z: float) -> float:
+    return _load().omnimoe_ref_act_grad(kind, float(z))
 
 
 def act(kind: int, z: float) -> float:

@@ -173,6 +173,15 @@ void select_dense_row(const double* L, int64_t N, int K, int32_t* idx, double* g
 
 double gelu_erf(double z) { return 0.5 * z * (1.0 + std::erf(z / std::sqrt(2.0))); }
 double silu(double z) { return z / (1.0 + std::exp(-z)); }
+// d/dz of z Phi(z) = Phi(z) + z phi(z); d/dz of z s(z) = s(z) (1 + z (1 - s(z))).
+double gelu_erf_grad(double z) {
+  const double pi = 3.14159265358979323846;
+  return 0.5 * (1.0 + std::erf(z / std::sqrt(2.0))) + z * std::exp(-0.5 * z * z) / std::sqrt(2.0 * pi);
+}
+double silu_grad(double z) {
+  const double sg = 1.0 / (1.0 + std::exp(-z));
+  return sg * (1.0 + z * (1.0 - sg));
+}
 
 double dot_row(const float* a, const float* b, int n) {
   double s = 0.0;
@@ -185,6 +194,7 @@ double dot_row(const float* a, const float* b, int n) {
 extern "C" {
 
 double omnimoe_ref_act(int act, double z) { return act == 1 ? silu(z) : gelu_erf(z); }
+double omnimoe_ref_act_grad(int act, double z) { return act == 1 ? silu_grad(z) : gelu_erf_grad(z); }
 
 int omnimoe_ref_half_scores(const omnimoe_ref_desc* d, const float* x, const float* keys_row,
                             const float* keys_col, double* sr, double* sc, int n_threads) {
@@ -418,6 +428,80 @@ int omnimoe_ref_shared_mlp(const omnimoe_ref_desc* d, int32_t d_ff, const float*
         double s = 0.0;
         for (int f = 0; f < d_ff; ++f) s += (double)w_down[(int64_t)c * d_ff + f] * a[(size_t)f];
         y[t * D + c] += s;
+      }
+    }
+  });
+  return 0;
+}
+
+int omnimoe_ref_expert_backward(const omnimoe_ref_desc* d, const float* x, const float* u,
+                                const float* v, const int32_t* idx, const double* gates,
+                                const double* dy, double* dx, double* du_rows, double* dv_rows,
+                                int32_t* active, int32_t* n_active, double* dgates,
+                                double* dscores, int n_threads) {
+  if (!valid(d)) return -1;
+  const int D = d->d, K = d->K;
+  const int64_t HK = (int64_t)d->H * K;
+  const int64_t M = d->T * HK;
+  const int64_t N = (int64_t)d->n_rows * d->n_cols;
+  for (int64_t p = 0; p < M; ++p)
+    if (idx[p] < 0 || idx[p] >= N) return -2;
+  // per task: a_p and dh_p = da_p g_p act'(h_p); gate and score gradients per (t, h) row
+  std::vector<double> a(M), dh(M);
+  parallel_for(d->T * d->H, n_threads, [&](int64_t b, int64_t e) {
+    for (int64_t th = b; th < e; ++th) {
+      const int64_t t = th / d->H;
+      double sgd = 0.0;
+      for (int k = 0; k < K; ++k) {
+        const int64_t p = th * K + k;
+        const int64_t ex = idx[p];
+        const double h = dot_row(x + t * D, u + ex * D, D);
+        double da = 0.0;
+        for (int m = 0; m < D; ++m) da += dy[t * D + m] * (double)v[ex * D + m];
+        a[p] = gates[p] * omnimoe_ref_act(d->act, h);
+        dh[p] = da * gates[p] * omnimoe_ref_act_grad(d->act, h);
+        dgates[p] = da * omnimoe_ref_act(d->act, h);
+        sgd += gates[p] * dgates[p];
+      }
+      for (int k = 0; k < K; ++k) {
+        const int64_t p = th * K + k;
+        dscores[p] = gates[p] * (dgates[p] - sgd);
+      }
+    }
+  });
+  // dx: token by token over the slots
+  parallel_for(d->T, n_threads, [&](int64_t b, int64_t e) {
+    for (int64_t t = b; t < e; ++t) {
+      double* dxt = dx + t * D;
+      for (int m = 0; m < D; ++m) dxt[m] = 0.0;
+      for (int64_t s = 0; s < HK; ++s) {
+        const int64_t p = t * HK + s;
+        const int64_t ex = idx[p];
+        for (int m = 0; m < D; ++m) dxt[m] += dh[p] * (double)u[ex * D + m];
+      }
+    }
+  });
+  // du, dv: expert by expert over the schedule's segments (tasks in id order)
+  const int64_t cap = std::min(M, N);
+  std::vector<int32_t> perm(M), off(cap + 2);
+  int32_t A = 0;
+  omnimoe_ref_desc d1 = *d;
+  d1.group_size = 1;
+  int rc = omnimoe_ref_schedule(&d1, idx, perm.data(), active, off.data(), &A, nullptr);
+  if (rc) return rc;
+  *n_active = A;
+  parallel_for(A, n_threads, [&](int64_t b, int64_t e) {
+    for (int64_t r = b; r < e; ++r) {
+      double* du = du_rows + r * D;
+      double* dv = dv_rows + r * D;
+      for (int m = 0; m < D; ++m) du[m] = dv[m] = 0.0;
+      for (int64_t tau = off[r]; tau < off[r + 1]; ++tau) {
+        const int64_t p = perm[tau];
+        const int64_t t = p / HK;
+        for (int m = 0; m < D; ++m) {
+          du[m] += dh[p] * (double)x[t * D + m];
+          dv[m] += a[p] * dy[t * D + m];
+        }
       }
     }
   });

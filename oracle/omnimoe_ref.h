@@ -103,6 +103,25 @@ int omnimoe_ref_select_dense_f32(const omnimoe_ref_desc* desc, const float* logi
 int omnimoe_ref_shared_mlp(const omnimoe_ref_desc* desc, int32_t d_ff, const float* x,
                            const float* w_gu, const float* w_down, double* y, int n_threads);
 
+/* Backward of the expert compute (the gradients of Eq. 4 / 7 for L = sum_t dy_t . y_t), fp64:
+ *   h_p = x_t . u_e, a_p = g_p act(h_p), da_p = dy_t . v_e,
+ *   dgates[p]  = da_p act(h_p)
+ *   dscores[p] = g_p (dgates[p] - sum over the K slots q of (t, h) of g_q dgates[q])
+ *                (the gradient with respect to the selected scores through the softmax, Eq. 2)
+ *   dx[t]      = sum over t's slots of da_p g_p act'(h_p) u_e
+ *   du_rows[a] = sum over the tasks of expert active[a] of da_p g_p act'(h_p) x_t
+ *   dv_rows[a] = sum over the tasks of expert active[a] of a_p dy_t
+ * Rows of du / dv are those of the active experts in ascending id order (active[a], a <
+ * *n_active); x, u, v fp32 as stored, gates and dy fp64. */
+int omnimoe_ref_expert_backward(const omnimoe_ref_desc* desc, const float* x, const float* u,
+                                const float* v, const int32_t* idx, const double* gates,
+                                const double* dy, double* dx, double* du_rows, double* dv_rows,
+                                int32_t* active, int32_t* n_active, double* dgates,
+                                double* dscores, int n_threads);
+
+/* Derivative of the activation on one value: 0 GELU-erf, 1 SiLU. */
+double omnimoe_ref_act_grad(int act, double z);
+
 /* The activation on one value: 0 GELU-erf, 1 SiLU. */
 double omnimoe_ref_act(int act, double z);
 

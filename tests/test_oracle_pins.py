@@ -475,3 +475,94 @@ def test_shared_mlp_matches_numpy_and_is_linear_in_w_down():
     y2 = oracle.shared_mlp(dsc, x, w_gu, 2.0 * w_down)
     np.testing.assert_array_equal(y2, 2.0 * y)
     assert np.all(oracle.shared_mlp(dsc, np.zeros_like(x), w_gu, w_down) == 0.0)
+
+
+# ------------------------------------------------------------------ expert backward
+
+@pytest.mark.parametrize("act", ["gelu", "silu"])
+def test_activation_derivative_matches_central_differences(act):
+    kind = {"gelu": 0, "silu": 1}[act]
+    for z in (-3.0, -1.3, -0.2, 0.0, 0.4, 1.0, 2.7):
+        h = 1e-5
+        fd = (oracle.act(kind, z + h) - oracle.act(kind, z - h)) / (2 * h)
+        assert abs(oracle.act_grad(kind, z) - fd) < 1e-9
+    # closed forms at 0: GELU' = Phi(0) = 1/2, SiLU' = s(0) = 1/2
+    assert oracle.act_grad(kind, 0.0) == 0.5
+
+
+def _backward_case(seed, act):
+    rng = np.random.default_rng(seed)
+    s = Shape(T=5, d=6, n_rows=3, n_cols=4, d_key=2, H=2, K=3, act=act)
+    N = s.n_rows * s.n_cols
+    # dyadic values, so a perturbation of 2^-12 is exact in float32
+    x = (rng.integers(-8, 9, size=(s.T, s.d)) / 8).astype(np.float32)
+    u = (rng.integers(-8, 9, size=(N, s.d)) / 16).astype(np.float32)
+    v = (rng.integers(-8, 9, size=(N, s.d)) / 16).astype(np.float32)
+    idx = np.stack([rng.choice(N, s.K, replace=False) for _ in range(s.T * s.H)]).reshape(
+        s.T, s.H, s.K).astype(np.int32)
+    idx[0, 1] = idx[0, 0]   # one expert picked by both heads of a token
+    scores = np.sort(rng.standard_normal((s.T, s.H, s.K)), axis=-1)[..., ::-1].copy()
+    dy = rng.standard_normal((s.T, s.d))
+    return s, x, u, v, idx, scores, dy
+
+
+def _softmax(scores):
+    e = np.exp(scores - scores[..., :1])
+    return e / e.sum(axis=-1, keepdims=True)
+
+
+@pytest.mark.parametrize("act", ["gelu", "silu"])
+def test_expert_backward_matches_finite_differences(act):
+    s, x, u, v, idx, scores, dy = _backward_case(31, act)
+    dsc = oracle.desc(s)
+    gates = _softmax(scores)
+
+    def loss(x=x, u=u, v=v, gates=gates):
+        y = oracle.expert_forward(dsc, x, u, v, idx, gates, scheduled=False, n_threads=1)
+        return float(np.sum(dy * y))
+
+    g = oracle.expert_backward(dsc, x, u, v, idx, gates, dy, n_threads=1)
+    h = 2.0 ** -12
+    for (t, m) in [(0, 0), (1, 3), (4, 5), (2, 2)]:
+        xp, xm = x.copy(), x.copy()
+        xp[t, m] += h
+        xm[t, m] -= h
+        fd = (loss(x=xp) - loss(x=xm)) / (2 * h)
+        assert abs(g["dx"][t, m] - fd) <= 1e-6 * max(1.0, abs(fd))
+    rows = {int(e): r for r, e in enumerate(g["active"])}
+    assert sorted(rows) == sorted(set(idx.ravel().tolist()))
+    for e in sorted(rows)[:4]:
+        for m in (0, 5):
+            for name, tab in (("du_rows", u), ("dv_rows", v)):
+                tp, tm = tab.copy(), tab.copy()
+                tp[e, m] += h
+                tm[e, m] -= h
+                kw = {"u": tp} if name == "du_rows" else {"v": tp}
+                kw2 = {"u": tm} if name == "du_rows" else {"v": tm}
+                fd = (loss(**kw) - loss(**kw2)) / (2 * h)
+                assert abs(g[name][rows[e], m] - fd) <= 1e-6 * max(1.0, abs(fd)), (name, e, m)
+    hg = 1e-6
+    for p in [(0, 0, 0), (0, 1, 2), (3, 1, 1)]:
+        gp, gm = gates.copy(), gates.copy()
+        gp[p] += hg
+        gm[p] -= hg
+        fd = (loss(gates=gp) - loss(gates=gm)) / (2 * hg)
+        assert abs(g["dgates"][p] - fd) <= 1e-7 * max(1.0, abs(fd))
+    for p in [(0, 0, 0), (2, 1, 2), (4, 0, 1)]:
+        sp, sm = scores.copy(), scores.copy()
+        sp[p] += hg
+        sm[p] -= hg
+        fd = (loss(gates=_softmax(sp)) - loss(gates=_softmax(sm))) / (2 * hg)
+        assert abs(g["dscores"][p] - fd) <= 1e-7 * max(1.0, abs(fd))
+    # the softmax gradient sums to zero over each (token, head) row
+    np.testing.assert_allclose(g["dscores"].sum(axis=-1), 0.0, atol=1e-12)
+
+
+def test_expert_backward_linearity_in_dy():
+    s, x, u, v, idx, scores, dy = _backward_case(32, "gelu")
+    dsc = oracle.desc(s)
+    gates = _softmax(scores)
+    g1 = oracle.expert_backward(dsc, x, u, v, idx, gates, dy)
+    g2 = oracle.expert_backward(dsc, x, u, v, idx, gates, 2.0 * dy)
+    for k in ("dx", "du_rows", "dv_rows", "dgates", "dscores"):
+        np.testing.assert_array_equal(g2[k], 2.0 * g1[k])
