@@ -96,7 +96,8 @@ typedef enum {
   OMNIMOE_STAGE_SCHEDULE = 2,
   OMNIMOE_STAGE_EXPERT = 3,
   OMNIMOE_STAGE_LAYER = 4,
-  OMNIMOE_STAGE_ROUTE_DENSE = 5  /* omnimoe_route_dense without a logits buffer */
+  OMNIMOE_STAGE_ROUTE_DENSE = 5,    /* omnimoe_route_dense without a logits buffer */
+  OMNIMOE_STAGE_EXPERT_BACKWARD = 6 /* omnimoe_expert_backward */
 } omnimoe_stage;
 
 /* Bytes of workspace the given stage's entry point needs for this shape. */
@@ -178,6 +179,29 @@ omnimoe_status omnimoe_expert_forward_token_centric(const omnimoe_layer_desc* de
                                                    const void* x, const void* u, const void* v,
                                                    const int32_t* idx, const float* gates,
                                                    float* y, void* stream);
+
+/* Backward of the expert compute (gradients of Eq. 4 and 7) for a loss L with dL/dy = dy:
+ *   h_p = x_t . u_e, a_p = g_p act(h_p), da_p = dy_t . v_e, dh_p = da_p g_p act'(h_p);
+ *   dx       [T, d]  fp32 out   sum over t's slots of dh_p u_e (the expert branch's share of
+ *                               dL/dx; the router's share is not included)
+ *   du_rows  [min(M, N), d] fp32 out   row a < n_active: sum over the tasks of expert active[a]
+ *                               of dh_p x_t (the gradient of u's row active[a])
+ *   dv_rows  [min(M, N), d] fp32 out   row a: sum over those tasks of a_p dy_t
+ *   dgates   [T, H, K] fp32 out   da_p act(h_p)
+ *   dscores  [T, H, K] fp32 out   g_p (dgates_p - sum over the (t, h) row of g dgates): the
+ *                               gradient of the K selected scores through the softmax (Eq. 2)
+ * x, u, v, idx, gates as in omnimoe_expert_forward; dy [T, d] fp32; perm, active_offsets and
+ * n_active from omnimoe_schedule with group_size 1 (each expert's tasks contiguous). The
+ * per-expert sums run over the schedule's segments in task order, so the result is the same
+ * on every run. d <= 4096 (bf16) or 2048 (fp32), else OMNIMOE_ERR_UNSUPPORTED. Workspace:
+ * OMNIMOE_STAGE_EXPERT_BACKWARD bytes. */
+omnimoe_status omnimoe_expert_backward(const omnimoe_layer_desc* desc, const void* x,
+                                       const void* u, const void* v, const int32_t* idx,
+                                       const float* gates, const int32_t* perm,
+                                       const int32_t* active_offsets, const int32_t* n_active,
+                                       const float* dy, float* dx, float* du_rows,
+                                       float* dv_rows, float* dgates, float* dscores,
+                                       void* workspace, size_t workspace_bytes, void* stream);
 
 /* The whole routed layer: route, schedule and expert compute on one stream, no host
  * synchronisation. y [T, d] fp32 out; idx_out and gates_out ([T, H, K]) may be NULL. */

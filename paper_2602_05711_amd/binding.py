@@ -17,14 +17,15 @@ LIB_PATH = os.path.join(HERE, "libomnimoe.so")
 OMNIMOE_F32, OMNIMOE_BF16 = 0, 1
 OMNIMOE_ACT_GELU, OMNIMOE_ACT_SILU = 0, 1
 OMNIMOE_QUERY_SPLIT, OMNIMOE_QUERY_SHARED = 0, 1
-STAGE_ROUTE, STAGE_SELECT, STAGE_SCHEDULE, STAGE_EXPERT, STAGE_LAYER, STAGE_ROUTE_DENSE = range(6)
+(STAGE_ROUTE, STAGE_SELECT, STAGE_SCHEDULE, STAGE_EXPERT, STAGE_LAYER, STAGE_ROUTE_DENSE,
+ STAGE_EXPERT_BACKWARD) = range(7)
 KERNEL_NAMES = ("score", "select", "schedule", "expert_dot", "accumulate")
 
 EXPORTED = (
     "omnimoe_workspace_size", "omnimoe_route", "omnimoe_select", "omnimoe_route_dense",
     "omnimoe_select_dense", "omnimoe_shared_mlp", "omnimoe_shared_mlp_workspace_size",
     "omnimoe_schedule",
-    "omnimoe_expert_forward", "omnimoe_expert_forward_token_centric",
+    "omnimoe_expert_forward", "omnimoe_expert_forward_token_centric", "omnimoe_expert_backward",
     "omnimoe_layer_forward", "omnimoe_timer_create",
     "omnimoe_timer_destroy", "omnimoe_timer_read", "omnimoe_layer_forward_timed",
     "omnimoe_status_string",
@@ -68,6 +69,7 @@ def load_library():
         "omnimoe_schedule": [D, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_expert_forward": [D, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_expert_forward_token_centric": [D, P, P, P, P, P, P, P],
+        "omnimoe_expert_backward": [D, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_layer_forward": [D, P, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_layer_forward_timed": [D, P, P, P, P, P, P, P, P, P, SZ, P, P],
         "omnimoe_timer_create": [I32, ctypes.POINTER(P)],
@@ -193,6 +195,16 @@ def omnimoe_expert_forward_token_centric(desc, x, u, v, idx, gates, y, stream=No
            load_library().omnimoe_expert_forward_token_centric(
                ctypes.byref(desc), _ptr(x), _ptr(u), _ptr(v), _ptr(idx), _ptr(gates), _ptr(y),
                _stream(stream)))
+
+
+def omnimoe_expert_backward(desc, x, u, v, idx, gates, perm, active_offsets, n_active, dy, dx,
+                            du_rows, dv_rows, dgates, dscores, ws=None, stream=None):
+    if ws is None:
+        ws = workspace(desc, STAGE_EXPERT_BACKWARD, x.device)
+    _check("omnimoe_expert_backward", load_library().omnimoe_expert_backward(
+        ctypes.byref(desc), _ptr(x), _ptr(u), _ptr(v), _ptr(idx), _ptr(gates), _ptr(perm),
+        _ptr(active_offsets), _ptr(n_active), _ptr(dy), _ptr(dx), _ptr(du_rows), _ptr(dv_rows),
+        _ptr(dgates), _ptr(dscores), _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def omnimoe_layer_forward(desc, x, keys_row, keys_col, u, v, y, idx_out=None, gates_out=None,

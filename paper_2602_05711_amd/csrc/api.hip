@@ -89,6 +89,7 @@ size_t stage_bytes(const Shape& s, int stage) {
     case OMNIMOE_STAGE_SCHEDULE: return omnimoe::schedule_ws_bytes(s.M, s.N);
     case OMNIMOE_STAGE_EXPERT: return m_bytes(s);
     case OMNIMOE_STAGE_ROUTE_DENSE: return dense_bytes(s);
+    case OMNIMOE_STAGE_EXPERT_BACKWARD: return omnimoe::backward_ws_bytes(s.M);
     default: {
       // idx, gates, perm, active, active_offsets, n_active, then the logits (dead after
       // selection) overlapped with the sort buffers and the a[] buffer.
@@ -181,7 +182,7 @@ const char* omnimoe_status_string(int32_t status) {
 omnimoe_status omnimoe_workspace_size(const omnimoe_layer_desc* desc, int32_t stage,
                                       size_t* bytes) {
   if (!bytes) return OMNIMOE_ERR_INVALID_ARG;
-  if (stage < OMNIMOE_STAGE_ROUTE || stage > OMNIMOE_STAGE_ROUTE_DENSE)
+  if (stage < OMNIMOE_STAGE_ROUTE || stage > OMNIMOE_STAGE_EXPERT_BACKWARD)
     return OMNIMOE_ERR_INVALID_ARG;
   Shape s;
   omnimoe_status st = check_desc(desc, &s);
@@ -372,6 +373,27 @@ omnimoe_status omnimoe_expert_forward_token_centric(const omnimoe_layer_desc* de
   if ((st = check_ptrs({x, u, v, idx, gates, y}))) return st;
   return hip_status(omnimoe::launch_token_centric(s, x, u, v, idx, gates, y,
                                                   (hipStream_t)stream));
+}
+
+omnimoe_status omnimoe_expert_backward(const omnimoe_layer_desc* desc, const void* x,
+                                       const void* u, const void* v, const int32_t* idx,
+                                       const float* gates, const int32_t* perm,
+                                       const int32_t* active_offsets, const int32_t* n_active,
+                                       const float* dy, float* dx, float* du_rows,
+                                       float* dv_rows, float* dgates, float* dscores, void* ws,
+                                       size_t ws_bytes, void* stream) {
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  if (s.T == 0) return OMNIMOE_OK;
+  if (s.d > (s.bf16 ? 4096 : 2048)) return OMNIMOE_ERR_UNSUPPORTED;
+  if ((st = check_ptrs({x, u, v, idx, gates, perm, active_offsets, n_active, dy, dx, du_rows,
+                        dv_rows, dgates, dscores, ws})))
+    return st;
+  if (ws_bytes < stage_bytes(s, OMNIMOE_STAGE_EXPERT_BACKWARD)) return OMNIMOE_ERR_WORKSPACE;
+  return hip_status(omnimoe::launch_expert_backward(s, x, u, v, idx, gates, perm, active_offsets,
+                                                    n_active, dy, dx, du_rows, dv_rows, dgates,
+                                                    dscores, ws, (hipStream_t)stream));
 }
 
 omnimoe_status omnimoe_layer_forward(const omnimoe_layer_desc* desc, const void* x,

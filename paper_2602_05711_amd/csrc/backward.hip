@@ -1,0 +1,284 @@
+// Backward of the expert compute (Eq. 4, 7) for L = sum_t dy_t . y_t, the gradients a training
+// step needs from this layer's experts and gates:
+//   h_p = x_t . u_e,  a_p = g_p act(h_p),  da_p = dy_t . v_e,
+//   dgates_p = da_p act(h_p),  dh_p = da_p g_p act'(h_p),
+//   dx_t = sum over t's slots of dh_p u_e,
+//   du_e = sum over e's tasks of dh_p x_t,  dv_e = sum over e's tasks of a_p dy_t,
+//   dscores_p = g_p (dgates_p - sum over the (t, h) row of g dgates)   (softmax, Eq. 2).
+// token pass: one wavefront per token gathers each slot's u and v rows (as the token-centric
+//   forward does), forms h, da, a, dh, dgates and sums dx in slot order;
+// expert pass: one wavefront per active expert walks its segment of the schedule (task ids
+//   ascending) and sums du and dv in that order: the expert-major order makes the per-expert
+//   gradients plain sequential sums, with no atomics, so every run gives the same bits;
+// score pass: one wavefront per (token, head) row.
+#include "device_common.hpp"
+#include "internal.hpp"
+
+namespace omnimoe {
+namespace {
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+struct BwdArgs {
+  const void* x;
+  const void* u;
+  const void* v;
+  const int32_t* idx;
+  const float* gates;
+  const float* dy;
+  const int32_t* perm;
+  const int32_t* offsets;
+  const int32_t* n_active;
+  float* dx;
+  float* du;
+  float* dv;
+  float* dgates;
+  float* dscores;
+  float* a;    // a_p per task (workspace)
+  float* dh;   // dh_p per task (workspace)
+  int64_t T;
+  int64_t N;
+  int64_t M;
+  int64_t cap;  // min(M, N): rows of du / dv
+  int d;
+  int hk;
+  int K;
+  int act;
+  int nchunks;  // 16-byte chunks of a stored row
+};
+
+__device__ __forceinline__ int clamp_id(int v, int64_t n) {
+  return v < 0 ? 0 : (v >= n ? (int)(n - 1) : v);
+}
+
+// Element k (0 .. EPC-1) of a stored 16-byte chunk, as fp32.
+template <bool BF16>
+__device__ __forceinline__ float chunk_elem(const uint4& c, int k) {
+  if constexpr (BF16) {
+    const uint32_t w = k < 2 ? c.x : (k < 4 ? c.y : (k < 6 ? c.z : c.w));
+    return (k & 1) ? bf16_hi(w) : bf16_lo(w);
+  } else {
+    const uint32_t w = k == 0 ? c.x : (k == 1 ? c.y : (k == 2 ? c.z : c.w));
+    return __uint_as_float(w);
+  }
+}
+
+template <int CPL, bool BF16>
+__global__ __launch_bounds__(256) void bwd_token_kernel(BwdArgs a) {
+  constexpr int EPC = BF16 ? 8 : 4;
+  const int l = lane_id();
+  const uint4* X = (const uint4*)a.x;
+  const uint4* U = (const uint4*)a.u;
+  const uint4* V = (const uint4*)a.v;
+  const int64_t rc = a.nchunks;
+  bool cv[CPL];
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) cv[q] = (l + kWave * q) < a.nchunks;
+  const int64_t stride = (int64_t)gridDim.x * 4;
+  for (int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < a.T; t += stride) {
+    uint4 xr[CPL];
+    float dyr[CPL][EPC];
+    float acc[CPL][EPC];
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      const int c = l + kWave * q;
+      xr[q] = cv[q] ? X[t * rc + c] : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) {
+        dyr[q][k] = cv[q] ? a.dy[t * a.d + (int64_t)c * EPC + k] : 0.0f;
+        acc[q][k] = 0.0f;
+      }
+    }
+    for (int s = 0; s < a.hk; ++s) {
+      const int64_t p = t * a.hk + s;
+      const int e = clamp_id(a.idx[p], a.N);
+      const float g = a.gates[p];
+      uint4 ur[CPL], vr[CPL];
+#pragma unroll
+      for (int q = 0; q < CPL; ++q) {
+        ur[q] = cv[q] ? U[(int64_t)e * rc + l + kWave * q] : make_uint4(0, 0, 0, 0);
+        vr[q] = cv[q] ? V[(int64_t)e * rc + l + kWave * q] : make_uint4(0, 0, 0, 0);
+      }
+      float hs = 0.0f, ds = 0.0f;
+#pragma unroll
+      for (int q = 0; q < CPL; ++q)
+#pragma unroll
+        for (int k = 0; k < EPC; ++k) {
+          hs = fmaf(chunk_elem<BF16>(xr[q], k), chunk_elem<BF16>(ur[q], k), hs);
+          ds = fmaf(dyr[q][k], chunk_elem<BF16>(vr[q], k), ds);
+        }
+      const float h = wave_sum_uniform(hs);
+      const float da = wave_sum_uniform(ds);
+      const float act = activation(a.act, h);
+      const float dh = da * g * activation_grad(a.act, h);
+      if (l == 0) {
+        a.a[p] = g * act;
+        a.dh[p] = dh;
+        a.dgates[p] = da * act;
+      }
+#pragma unroll
+      for (int q = 0; q < CPL; ++q)
+#pragma unroll
+        for (int k = 0; k < EPC; ++k) acc[q][k] = fmaf(dh, chunk_elem<BF16>(ur[q], k), acc[q][k]);
+    }
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      if (!cv[q]) continue;
+      const int c = l + kWave * q;
+      float4* o = (float4*)(a.dx + t * a.d + (int64_t)c * EPC);
+#pragma unroll
+      for (int k = 0; k < EPC; k += 4) o[k / 4] = make_float4(acc[q][k], acc[q][k + 1], acc[q][k + 2], acc[q][k + 3]);
+    }
+  }
+}
+
+template <int CPL, bool BF16>
+__global__ __launch_bounds__(256) void bwd_expert_kernel(BwdArgs a) {
+  constexpr int EPC = BF16 ? 8 : 4;
+  const int l = lane_id();
+  const uint4* X = (const uint4*)a.x;
+  const int64_t rc = a.nchunks;
+  bool cv[CPL];
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) cv[q] = (l + kWave * q) < a.nchunks;
+  const int64_t na = *a.n_active < a.cap ? *a.n_active : a.cap;
+  const int64_t stride = (int64_t)gridDim.x * 4;
+  for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < na; r += stride) {
+    float du[CPL][EPC], dv[CPL][EPC];
+#pragma unroll
+    for (int q = 0; q < CPL; ++q)
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) du[q][k] = dv[q][k] = 0.0f;
+    int64_t b = a.offsets[r], e = a.offsets[r + 1];
+    b = b < 0 ? 0 : (b > a.M ? a.M : b);
+    e = e < b ? b : (e > a.M ? a.M : e);
+    for (int64_t tau = b; tau < e; ++tau) {
+      const int p = clamp_id(a.perm[tau], a.M);
+      const int64_t t = p / a.hk;
+      const float ap = a.a[p], dhp = a.dh[p];
+#pragma unroll
+      for (int q = 0; q < CPL; ++q) {
+        if (!cv[q]) continue;
+        const int c = l + kWave * q;
+        const uint4 xc = X[t * rc + c];
+        const float4* dyc = (const float4*)(a.dy + t * a.d + (int64_t)c * EPC);
+#pragma unroll
+        for (int k = 0; k < EPC; k += 4) {
+          const float4 yv = dyc[k / 4];
+          dv[q][k] = fmaf(ap, yv.x, dv[q][k]);
+          dv[q][k + 1] = fmaf(ap, yv.y, dv[q][k + 1]);
+          dv[q][k + 2] = fmaf(ap, yv.z, dv[q][k + 2]);
+          dv[q][k + 3] = fmaf(ap, yv.w, dv[q][k + 3]);
+        }
+#pragma unroll
+        for (int k = 0; k < EPC; ++k) du[q][k] = fmaf(dhp, chunk_elem<BF16>(xc, k), du[q][k]);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      if (!cv[q]) continue;
+      const int c = l + kWave * q;
+      float4* ou = (float4*)(a.du + r * a.d + (int64_t)c * EPC);
+      float4* ov = (float4*)(a.dv + r * a.d + (int64_t)c * EPC);
+#pragma unroll
+      for (int k = 0; k < EPC; k += 4) {
+        ou[k / 4] = make_float4(du[q][k], du[q][k + 1], du[q][k + 2], du[q][k + 3]);
+        ov[k / 4] = make_float4(dv[q][k], dv[q][k + 1], dv[q][k + 2], dv[q][k + 3]);
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void bwd_score_kernel(BwdArgs a) {
+  const int l = lane_id();
+  const int64_t rows = a.T * (a.hk / a.K);
+  const int64_t stride = (int64_t)gridDim.x * 4;
+  for (int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); row < rows; row += stride) {
+    const int64_t base = row * a.K;
+    float part = 0.0f;
+    for (int k = l; k < a.K; k += kWave) part = fmaf(a.gates[base + k], a.dgates[base + k], part);
+    const float sgd = wave_sum_f32(part);
+    for (int k = l; k < a.K; k += kWave)
+      a.dscores[base + k] = a.gates[base + k] * (a.dgates[base + k] - sgd);
+  }
+}
+
+int cpl_of(int nchunks) {
+  int c = 1;
+  while (c * kWave < nchunks) c <<= 1;
+  return c;
+}
+
+template <bool BF16>
+hipError_t dispatch_bwd(int cpl, int64_t t_blocks, int64_t e_blocks, hipStream_t st,
+                        const BwdArgs& a) {
+#define OMNIMOE_BWD(C)                                                                    \
+  case C:                                                                                 \
+    hipLaunchKernelGGL((bwd_token_kernel<C, BF16>), dim3((unsigned)t_blocks), dim3(256), 0,  \
+                       st, a);                                                            \
+    hipLaunchKernelGGL((bwd_expert_kernel<C, BF16>), dim3((unsigned)e_blocks), dim3(256), 0, \
+                       st, a);                                                            \
+    break;
+  switch (cpl) {
+    OMNIMOE_BWD(1)
+    OMNIMOE_BWD(2)
+    OMNIMOE_BWD(4)
+    OMNIMOE_BWD(8)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef OMNIMOE_BWD
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t backward_ws_bytes(int64_t M) { return 2 * (((size_t)M * 4 + 255) & ~(size_t)255); }
+
+hipError_t launch_expert_backward(const Shape& s, const void* x, const void* u, const void* v,
+                                  const int32_t* idx, const float* gates, const int32_t* perm,
+                                  const int32_t* offsets, const int32_t* n_active,
+                                  const float* dy, float* dx, float* du, float* dv,
+                                  float* dgates, float* dscores, void* ws, hipStream_t st) {
+  if (s.T == 0) return hipSuccess;
+  BwdArgs a;
+  a.x = x;
+  a.u = u;
+  a.v = v;
+  a.idx = idx;
+  a.gates = gates;
+  a.dy = dy;
+  a.perm = perm;
+  a.offsets = offsets;
+  a.n_active = n_active;
+  a.dx = dx;
+  a.du = du;
+  a.dv = dv;
+  a.dgates = dgates;
+  a.dscores = dscores;
+  a.a = (float*)ws;
+  a.dh = (float*)((char*)ws + (((size_t)s.M * 4 + 255) & ~(size_t)255));
+  a.T = s.T;
+  a.N = s.N;
+  a.M = s.M;
+  a.cap = s.M < s.N ? s.M : s.N;
+  a.d = s.d;
+  a.hk = s.hk;
+  a.K = s.K;
+  a.act = s.act;
+  a.nchunks = s.bf16 ? s.d / 8 : s.d / 4;
+  const int cpl = cpl_of(a.nchunks);
+  int64_t tb = (s.T + 3) / 4;
+  if (tb > 16384) tb = 16384;
+  int64_t eb = (a.cap + 3) / 4;
+  if (eb > 65536) eb = 65536;
+  hipError_t e = s.bf16 ? dispatch_bwd<true>(cpl, tb, eb, st, a)
+                        : dispatch_bwd<false>(cpl, tb, eb, st, a);
+  if (e != hipSuccess) return e;
+  int64_t sb = (s.rows + 3) / 4;
+  if (sb > 16384) sb = 16384;
+  hipLaunchKernelGGL(bwd_score_kernel, dim3((unsigned)sb), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace omnimoe

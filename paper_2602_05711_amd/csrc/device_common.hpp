@@ -119,10 +119,21 @@ __device__ __forceinline__ float readlane_f32(float v, int lane) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
 
-// Activation of Eq. 4 in fp32.
+// Activation of Eq. 4 in fp32. GELU uses Phi(z) = erfc(-z / sqrt 2) / 2, which keeps full
+// relative precision for negative z, where 1 + erf(z / sqrt 2) would cancel.
 __device__ __forceinline__ float activation(int act, float z) {
   if (act == 1) return z / (1.0f + expf(-z));
-  return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f));
+  return 0.5f * z * erfcf(-z * 0.70710678118654752f);
+}
+
+// Its derivative: GELU (erf form) z Phi(z) -> Phi(z) + z phi(z); SiLU z s(z) ->
+// s(z) (1 + z (1 - s(z))).
+__device__ __forceinline__ float activation_grad(int act, float z) {
+  if (act == 1) {
+    const float sg = 1.0f / (1.0f + expf(-z));
+    return sg * (1.0f + z * (1.0f - sg));
+  }
+  return 0.5f * erfcf(-z * 0.70710678118654752f) + z * expf(-0.5f * z * z) * 0.39894228040143268f;
 }
 
 }  // namespace omnimoe

@@ -67,6 +67,15 @@ hipError_t launch_token_centric(const Shape& s, const void* x, const void* u, co
                                 const int32_t* idx, const float* gates, float* y,
                                 hipStream_t st);
 
+// Backward of the expert compute: dx, per-active-expert du / dv rows (expert-major, from a
+// group-size-1 schedule), dgates and dscores. Workspace: backward_ws_bytes(M).
+size_t backward_ws_bytes(int64_t M);
+hipError_t launch_expert_backward(const Shape& s, const void* x, const void* u, const void* v,
+                                  const int32_t* idx, const float* gates, const int32_t* perm,
+                                  const int32_t* offsets, const int32_t* n_active,
+                                  const float* dy, float* dx, float* du, float* dv,
+                                  float* dgates, float* dscores, void* ws, hipStream_t st);
+
 // y[t] = sum over slots (h, k) in order of a[p] * v[idx[p]].
 hipError_t launch_accumulate(const Shape& s, const void* v, const int32_t* idx, const float* a,
                              float* y, hipStream_t st);

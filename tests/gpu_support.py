@@ -75,3 +75,63 @@ def compare_routing(w, gpu_idx, ref_idx, sr, sc, delta):
         assert np.all(s >= kth[t, h] - 4 * delta), (t, h)
         assert len(set(g[t, h].tolist())) == w.K
     return int((~cert).sum())
+
+
+def backward_error_bounds(x, u, v, idx, g, dy, f_act, f_dact, dd_act_max=0.8,
+                          unit=2.0 ** -23):
+    """First-order bounds on the fp32 errors of the expert backward, element by element.
+
+    h_p = x_t . u_e and da_p = dy_t . v_e are fp32 dot products of length d, each within
+    2 gamma_d sum |.||.| (Higham, Thm 3.1); the errors propagate through a = g act(h),
+    dh = da g act'(h) and dgates = da act(h) (|act''| <= dd_act_max), and the fp32 sums of dx,
+    du, dv and of the softmax term each add gamma_n of their absolute terms. A small multiple
+    of the unit roundoff covers each rounded product and activation. Returns arrays shaped like
+    the outputs: dx [T, d], du / dv [A, d] over the active experts in ascending id order,
+    dgates and dscores [T, H, K]. f_act and f_dact evaluate act and act' in fp64.
+    """
+    T, D = x.shape
+    H, K = idx.shape[1], idx.shape[2]
+    hk = H * K
+    M = T * hk
+
+    def gam(n):
+        return n * unit / (1 - n * unit)
+
+    ii = idx.reshape(-1).astype(np.int64)
+    t = np.arange(M) // hk
+    x64, u64, v64, dy64 = (np.asarray(a, np.float64) for a in (x, u, v, dy))
+    gg = np.asarray(g, np.float64).reshape(-1)
+    h = np.einsum("pd,pd->p", x64[t], u64[ii])
+    da = np.einsum("pd,pd->p", dy64[t], v64[ii])
+    bh = 2 * gam(D) * np.einsum("pd,pd->p", np.abs(x64[t]), np.abs(u64[ii]))
+    bda = 2 * gam(D) * np.einsum("pd,pd->p", np.abs(dy64[t]), np.abs(v64[ii]))
+    act, dact = f_act(h), f_dact(h)
+    a, dh, dg = gg * act, da * gg * dact, da * act
+    ba = np.abs(gg) * (np.abs(dact) + dd_act_max * bh) * bh + 8 * unit * np.abs(a)
+    bdh = (np.abs(gg) * (np.abs(dact) * bda + np.abs(da) * dd_act_max * bh)
+           + 8 * unit * np.abs(dh))
+    bdg = (np.abs(act) * bda + np.abs(da) * (np.abs(dact) + dd_act_max * bh) * bh
+           + 8 * unit * np.abs(dg))
+    out = {}
+    dx = np.zeros((T, D))
+    for s_ in range(hk):
+        p = np.arange(T) * hk + s_
+        dx += bdh[p, None] * np.abs(u64[ii[p]]) + gam(hk) * np.abs(dh[p, None] * u64[ii[p]])
+    out["dx"] = dx
+    active = np.unique(ii)
+    rows = np.searchsorted(active, ii)
+    cnt = np.bincount(rows, minlength=active.size)
+    ge = gam(np.maximum(cnt, 1))[:, None]
+    for name, bterm, val, other in (("du", bdh, dh, x64[t]), ("dv", ba, a, dy64[t])):
+        b = np.zeros((active.size, D))
+        ab = np.zeros((active.size, D))
+        np.add.at(b, rows, bterm[:, None] * np.abs(other))
+        np.add.at(ab, rows, np.abs(val[:, None] * other))
+        out[name] = b + ge * ab
+    out["dgates"] = bdg.reshape(T, H, K)
+    g3, dg3, bdg3 = gg.reshape(T, H, K), dg.reshape(T, H, K), bdg.reshape(T, H, K)
+    srow = (np.abs(g3) * bdg3).sum(axis=-1, keepdims=True) + gam(K) * np.abs(g3 * dg3).sum(
+        axis=-1, keepdims=True)
+    ds = g3 * (dg3 - (g3 * dg3).sum(axis=-1, keepdims=True))
+    out["dscores"] = np.abs(g3) * (bdg3 + srow) + 8 * unit * np.abs(ds)
+    return out

@@ -13,8 +13,8 @@ import pytest
 
 import oracle
 import synth
-from gpu_support import (GATE_TOL, compare_routing, higham_bound, row_rel_err, to_dev, tol,
-                         upload)
+from gpu_support import (GATE_TOL, backward_error_bounds, compare_routing, higham_bound,
+                         row_rel_err, to_dev, tol, upload)
 
 pytestmark = pytest.mark.gpu
 
@@ -686,3 +686,60 @@ def test_c_abi_caller(name, tmp_path):
     same = np.all(idx == ref_idx, axis=(1, 2))
     y_ref = oracle.expert_forward(dsc, f["x"], f["u"], f["v"], ref_idx, ref_g)
     assert row_rel_err(y, y_ref)[same].max() <= tol(w)
+
+
+# ------------------------------------------------------------------ expert backward
+
+@pytest.mark.parametrize("name", ["tiny_f32", "small_bf16", "ragged_bf16", "ragged_f32",
+                                  "silu_k1_bf16", "k64_bf16", "all_experts_bf16", "k256_bf16"])
+def test_expert_backward(name):
+    w, dev, idx, g32, perm, _ = _expert_case(name)
+    say(f"[backward] {name}")
+    dsc = oracle.desc(w)
+    _, act_ref, off_ref, _ = oracle.schedule(dsc, idx)
+    rng = np.random.default_rng(len(name))
+    dy = rng.standard_normal((w.T, w.d)).astype(np.float32)
+    A = min(w.M, w.N)
+    out = {k: torch.full(shape, float("nan"), dtype=torch.float32, device="cuda") for k, shape in
+           [("dx", (w.T, w.d)), ("du", (A, w.d)), ("dv", (A, w.d)), ("dg", (w.T, w.H, w.K)),
+            ("ds", (w.T, w.H, w.K))]}
+    off = torch.full((A + 1,), -1, dtype=torch.int32, device="cuda")
+    off[: len(off_ref)] = to_dev(off_ref)
+    na = torch.tensor([len(act_ref)], dtype=torch.int32, device="cuda")
+    d = B.make_desc(w)
+    args = (d, dev["x"], dev["u"], dev["v"], to_dev(idx), to_dev(g32), to_dev(perm), off, na,
+            to_dev(dy), out["dx"], out["du"], out["dv"], out["dg"], out["ds"])
+    P.omnimoe_expert_backward(*args)
+    torch.cuda.synchronize()
+    got = {k: v.cpu().numpy() for k, v in out.items()}
+    ref = oracle.expert_backward(dsc, synth.as_f32(synth.make_x(w)),
+                                 synth.as_f32(synth.make_expert_rows(w, "u")),
+                                 synth.as_f32(synth.make_expert_rows(w, "v")), idx,
+                                 g32.astype(np.float64), dy.astype(np.float64))
+    n = len(ref["active"])
+    assert np.array_equal(ref["active"], act_ref)
+    # Element-wise bounds: a token whose h = x . u nearly cancels has an fp32 dot error that is
+    # large relative to h itself, so a relative tolerance per row would not hold; the bound
+    # follows the dot products' error (Higham) through the backward formulas.
+    kind = 1 if w.act == "silu" else 0
+    bnd = backward_error_bounds(
+        synth.as_f32(synth.make_x(w)), synth.as_f32(synth.make_expert_rows(w, "u")),
+        synth.as_f32(synth.make_expert_rows(w, "v")), idx, g32, dy,
+        np.vectorize(lambda z: oracle.act(kind, z)), np.vectorize(lambda z: oracle.act_grad(kind, z)))
+    pairs = {"dx": (got["dx"], ref["dx"], bnd["dx"]),
+             "du": (got["du"][:n], ref["du_rows"], bnd["du"]),
+             "dv": (got["dv"][:n], ref["dv_rows"], bnd["dv"]),
+             "dgates": (got["dg"], ref["dgates"], bnd["dgates"]),
+             "dscores": (got["ds"], ref["dscores"], bnd["dscores"])}
+    for k, (gv, rv, bv) in pairs.items():
+        err = np.abs(gv.astype(np.float64) - rv)
+        ratio = (err / (2 * bv + 1e-30)).max()
+        say(f"  {k}: max row rel err {row_rel_err(gv.reshape(rv.shape[0], -1), rv.reshape(rv.shape[0], -1)).max():.2e}, "
+            f"max err / bound {ratio:.2f}")
+        assert np.all(err <= 2 * bv + 1e-30), k
+    # same bits on a second run
+    P.omnimoe_expert_backward(*args)
+    torch.cuda.synchronize()
+    for k, v in out.items():
+        rows = n if k in ("du", "dv") else None
+        assert np.array_equal(v.cpu().numpy()[:rows].view(np.uint8), got[k][:rows].view(np.uint8))
