@@ -148,7 +148,7 @@ def cpu_model():
     return "unknown CPU"
 
 
-def extras(args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1):
+def extras(args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1, sched):
     """The shared SwiGLU branch and the two ablations of Table 3, timed like the layer."""
     import torch
     import paper_2602_05711_amd as P
@@ -227,7 +227,35 @@ def extras(args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1):
     else:
         no_cpr = {"skipped": f"the dense logits would take {dense_bytes / 2**30:.0f} GiB"}
 
-    return ablation, shared_mlp, no_cpr
+    # Backward of the expert compute (training): token pass, per-expert pass over the
+    # schedule's segments, softmax pass; dy is a seeded standard normal.
+    perm, off, na, n_active = sched
+    backward = None
+    if w.d <= (4096 if w.bf16 else 2048):
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(0)
+        dy = torch.randn((w.T, w.d), generator=gen, device="cuda", dtype=torch.float32)
+        dx = torch.empty_like(dy)
+        du = torch.empty((max(1, n_active), w.d), dtype=torch.float32, device="cuda")
+        dv = torch.empty_like(du)
+        dgt = torch.empty_like(g)
+        dsc = torch.empty_like(g)
+        wsb = P.workspace(desc, 6)
+        bw = lambda: P.omnimoe_expert_backward(  # noqa: E731
+            desc, d_in["x"], d_in["u"], d_in["v"], idx, g, perm, off, na, dy, dx, du, dv, dgt,
+            dsc, ws=wsb, stream=stream)
+        bw()
+        ev0.record(stream)
+        for _ in range(args.steps):
+            bw()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        bw_ms = ev0.elapsed_time(ev1) / args.steps
+        backward = {"expert_backward_ms": bw_ms, "active_rows": n_active,
+                    "tokens_per_s": w.T / (bw_ms * 1e-3)}
+        log(f"expert backward: {bw_ms:.3f} ms")
+        del dy, dx, du, dv, wsb
+    return ablation, shared_mlp, no_cpr, backward
 
 
 def main():
@@ -365,10 +393,11 @@ def main():
     routing = routing_stats(idx.cpu().numpy(), w.N)
     assert routing["n_active"] == n_active
 
-    ablation = shared_mlp = no_cpr = None
+    ablation = shared_mlp = no_cpr = backward = None
     if not args.layer_only:
-        ablation, shared_mlp, no_cpr = extras(args, w, desc, d_in, dev, idx, g, y, stream, per,
-                                              ms_step, ev0, ev1)
+        ablation, shared_mlp, no_cpr, backward = extras(args, w, desc, d_in, dev, idx, g, y,
+                                                        stream, per, ms_step, ev0, ev1,
+                                                        (perm, off, na, n_active))
 
     work = algorithmic_work(w, n_active)
     kernels = {}
@@ -431,6 +460,7 @@ def main():
         "cpu_baseline": cpu,
         "cold": cold,
         "shared_mlp": shared_mlp,
+        "expert_backward": backward,
         "ablation_no_schedule": ablation,
         "ablation_no_cartesian_router": no_cpr,
         "n_active": n_active, "eta": w.M / max(1, n_active), "routing": routing,

@@ -184,9 +184,10 @@ omnimoe_status omnimoe_expert_forward_token_centric(const omnimoe_layer_desc* de
  *   h_p = x_t . u_e, a_p = g_p act(h_p), da_p = dy_t . v_e, dh_p = da_p g_p act'(h_p);
  *   dx       [T, d]  fp32 out   sum over t's slots of dh_p u_e (the expert branch's share of
  *                               dL/dx; the router's share is not included)
- *   du_rows  [min(M, N), d] fp32 out   row a < n_active: sum over the tasks of expert active[a]
- *                               of dh_p x_t (the gradient of u's row active[a])
- *   dv_rows  [min(M, N), d] fp32 out   row a: sum over those tasks of a_p dy_t
+ *   du_rows  [n_active, d] fp32 out   row a: sum over the tasks of expert active[a] of
+ *                               dh_p x_t (the gradient of u's row active[a]); min(M, N) rows
+ *                               always suffice
+ *   dv_rows  [n_active, d] fp32 out   row a: sum over those tasks of a_p dy_t
  *   dgates   [T, H, K] fp32 out   da_p act(h_p)
  *   dscores  [T, H, K] fp32 out   g_p (dgates_p - sum over the (t, h) row of g dgates): the
  *                               gradient of the K selected scores through the softmax (Eq. 2)
