@@ -57,13 +57,14 @@ def _load():
         lib.omnimoe_ref_shared_mlp.argtypes = [D, ctypes.c_int32, P, P, P, P, ctypes.c_int]
         lib.omnimoe_ref_expert_backward.argtypes = [D, P, P, P, P, P, P, P, P, P, P, P, P, P,
                                                     ctypes.c_int]
+        lib.omnimoe_ref_route_backward.argtypes = [D, P, P, P, P, P, P, P, P, ctypes.c_int]
         lib.omnimoe_ref_act_grad.argtypes = [ctypes.c_int, ctypes.c_double]
         lib.omnimoe_ref_act_grad.restype = ctypes.c_double
         lib.omnimoe_ref_act.argtypes = [ctypes.c_int, ctypes.c_double]
         lib.omnimoe_ref_act.restype = ctypes.c_double
         for f in ("half_scores", "select", "select_f32", "schedule", "expert_forward",
                   "layer_forward", "route_dense", "select_dense_f32", "shared_mlp",
-                  "expert_backward"):
+                  "expert_backward", "route_backward"):
             getattr(lib, "omnimoe_ref_" + f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -263,6 +264,24 @@ def expert_backward(dsc: RefDesc, x, u, v, idx, gates, dy, n_threads=None):
     A = int(na[0])
     return {"dx": dx, "active": active[:A], "du_rows": du[:A], "dv_rows": dv[:A],
             "dgates": dg, "dscores": ds}
+
+
+def route_backward(dsc: RefDesc, x, keys_row, keys_col, idx, dscores, dx=None, n_threads=None):
+    """Router backward for fixed selections, fp64: (dx + router share, dkeys_row, dkeys_col)."""
+    lib = _load()
+    x, px = _f32(x)
+    kr, pkr = _f32(keys_row)
+    kc, pkc = _f32(keys_col)
+    idx = np.ascontiguousarray(idx, np.int32)
+    ds = np.ascontiguousarray(dscores, np.float64)
+    out = np.zeros((dsc.T, dsc.d), np.float64) if dx is None else np.array(dx, np.float64)
+    dkr = np.empty((dsc.H, dsc.n_rows, dsc.d_key), np.float64)
+    dkc = np.empty((dsc.H, dsc.n_cols, dsc.d_key), np.float64)
+    _check(lib.omnimoe_ref_route_backward(ctypes.byref(dsc), px, pkr, pkc, idx.ctypes.data,
+                                          ds.ctypes.data, out.ctypes.data, dkr.ctypes.data,
+                                          dkc.ctypes.data, n_threads or default_threads()),
+           "route_backward")
+    return out, dkr, dkc
 
 
 def act_grad(kind: int, z: float) -> float:

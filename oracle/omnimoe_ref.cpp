@@ -508,4 +508,48 @@ int omnimoe_ref_expert_backward(const omnimoe_ref_desc* d, const float* x, const
   return 0;
 }
 
+int omnimoe_ref_route_backward(const omnimoe_ref_desc* d, const float* x, const float* keys_row,
+                               const float* keys_col, const int32_t* idx, const double* dscores,
+                               double* dx, double* dkeys_row, double* dkeys_col, int n_threads) {
+  if (!valid(d)) return -1;
+  const int H = d->H, K = d->K, D = d->d, dk = d->d_key, nr = d->n_rows, nc = d->n_cols;
+  const int c0 = d->query_mode == 0 ? dk : 0;
+  const int64_t rows = d->T * H;
+  const int64_t N = (int64_t)nr * nc;
+  for (int64_t p = 0; p < rows * K; ++p)
+    if (idx[p] < 0 || idx[p] >= N) return -2;
+  // sub-key gradients: one head at a time (each head's tables are independent)
+  parallel_for(H, n_threads, [&](int64_t hb, int64_t he) {
+    for (int64_t h = hb; h < he; ++h) {
+      double* dr = dkeys_row + h * nr * dk;
+      double* dc = dkeys_col + h * nc * dk;
+      std::fill(dr, dr + (int64_t)nr * dk, 0.0);
+      std::fill(dc, dc + (int64_t)nc * dk, 0.0);
+      for (int64_t t = 0; t < d->T; ++t)
+        for (int k = 0; k < K; ++k) {
+          const int64_t p = (t * H + h) * K + k;
+          const int64_t i = idx[p] / nc, j = idx[p] % nc;
+          for (int m = 0; m < dk; ++m) {
+            dr[i * dk + m] += dscores[p] * (double)x[t * D + m];
+            dc[j * dk + m] += dscores[p] * (double)x[t * D + c0 + m];
+          }
+        }
+    }
+  });
+  // input gradient, token by token
+  parallel_for(d->T, n_threads, [&](int64_t b, int64_t e) {
+    for (int64_t t = b; t < e; ++t)
+      for (int h = 0; h < H; ++h)
+        for (int k = 0; k < K; ++k) {
+          const int64_t p = (t * H + h) * K + k;
+          const int64_t i = idx[p] / nc, j = idx[p] % nc;
+          for (int m = 0; m < dk; ++m) {
+            dx[t * D + m] += dscores[p] * (double)keys_row[((int64_t)h * nr + i) * dk + m];
+            dx[t * D + c0 + m] += dscores[p] * (double)keys_col[((int64_t)h * nc + j) * dk + m];
+          }
+        }
+  });
+  return 0;
+}
+
 }  // extern "C"

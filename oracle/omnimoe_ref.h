@@ -119,6 +119,18 @@ int omnimoe_ref_expert_backward(const omnimoe_ref_desc* desc, const float* x, co
                                 int32_t* active, int32_t* n_active, double* dgates,
                                 double* dscores, int n_threads);
 
+/* Backward of the router's scores for fixed selections (the selection itself is piecewise
+ * constant): with S_p = s_r[t, h, i_p] + s_c[t, h, j_p] (Eq. 9, 11) and dL/dS_p = dscores[p],
+ *   dkeys_row[h, i] = sum over tasks p of (t, h) with row i_p = i of dscores[p] x_t[0 : d_key]
+ *   dkeys_col[h, j] = sum over tasks with column j_p = j of dscores[p] x_t[c0 : c0 + d_key]
+ *   dx[t]          += sum over t's tasks of dscores[p] (keys_row[h, i_p] on x[0 : d_key] and
+ *                     keys_col[h, j_p] on x[c0 : c0 + d_key])
+ * (c0 = d_key for split queries, 0 for shared). dkeys_row [H, n_rows, d_key] and dkeys_col
+ * [H, n_cols, d_key] are written in full; dx [T, d] is added to. fp64. */
+int omnimoe_ref_route_backward(const omnimoe_ref_desc* desc, const float* x, const float* keys_row,
+                               const float* keys_col, const int32_t* idx, const double* dscores,
+                               double* dx, double* dkeys_row, double* dkeys_col, int n_threads);
+
 /* Derivative of the activation on one value: 0 GELU-erf, 1 SiLU. */
 double omnimoe_ref_act_grad(int act, double z);
 

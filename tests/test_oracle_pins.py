@@ -566,3 +566,43 @@ def test_expert_backward_linearity_in_dy():
     g2 = oracle.expert_backward(dsc, x, u, v, idx, gates, 2.0 * dy)
     for k in ("dx", "du_rows", "dv_rows", "dgates", "dscores"):
         np.testing.assert_array_equal(g2[k], 2.0 * g1[k])
+
+
+@pytest.mark.parametrize("mode", ["split", "shared"])
+def test_route_backward_matches_finite_differences(mode):
+    # With the selections held fixed, L = sum_p dscores_p S_p is linear in x and the sub-keys,
+    # so central differences of the oracle's own half-scores give the gradient up to rounding.
+    rng = np.random.default_rng(41)
+    dk = 3
+    d = 2 * dk if mode == "split" else dk + 2
+    s = Shape(T=5, d=d, n_rows=4, n_cols=3, d_key=dk, H=2, K=3, query_mode=mode)
+    dsc = oracle.desc(s)
+    x = (rng.integers(-8, 9, size=(s.T, d)) / 8).astype(np.float32)
+    kr = (rng.integers(-8, 9, size=(s.H, s.n_rows, dk)) / 8).astype(np.float32)
+    kc = (rng.integers(-8, 9, size=(s.H, s.n_cols, dk)) / 8).astype(np.float32)
+    N = s.n_rows * s.n_cols
+    idx = np.stack([rng.choice(N, s.K, replace=False) for _ in range(s.T * s.H)]).reshape(
+        s.T, s.H, s.K).astype(np.int32)
+    ds = rng.standard_normal((s.T, s.H, s.K))
+
+    def loss(x=x, kr=kr, kc=kc):
+        sr, sc = oracle.half_scores(dsc, x, kr, kc, n_threads=1)
+        i, j = idx // s.n_cols, idx % s.n_cols
+        S = np.take_along_axis(sr, i, axis=2) + np.take_along_axis(sc, j, axis=2)
+        return float(np.sum(ds * S))
+
+    dx, dkr, dkc = oracle.route_backward(dsc, x, kr, kc, idx, ds, n_threads=1)
+    h = 2.0 ** -10
+    for arr, grad, key in ((x, dx, "x"), (kr, dkr, "kr"), (kc, dkc, "kc")):
+        for pos in [tuple(rng.integers(0, n) for n in arr.shape) for _ in range(6)]:
+            ap, am = arr.copy(), arr.copy()
+            ap[pos] += h
+            am[pos] -= h
+            fd = (loss(**{key: ap}) - loss(**{key: am})) / (2 * h)
+            assert abs(grad[pos] - fd) <= 1e-9 * max(1.0, abs(fd)), (key, pos)
+    # rows no task selected have zero gradient
+    used_r = {(h_, int(i)) for h_ in range(s.H) for i in (idx[:, h_] // s.n_cols).ravel()}
+    for h_ in range(s.H):
+        for i in range(s.n_rows):
+            if (h_, i) not in used_r:
+                assert np.all(dkr[h_, i] == 0.0)
