@@ -251,10 +251,25 @@ def extras(args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1, 
         ev1.record(stream)
         torch.cuda.synchronize()
         bw_ms = ev0.elapsed_time(ev1) / args.steps
-        backward = {"expert_backward_ms": bw_ms, "active_rows": n_active,
-                    "tokens_per_s": w.T / (bw_ms * 1e-3)}
-        log(f"expert backward: {bw_ms:.3f} ms")
-        del dy, dx, du, dv, wsb
+        # router backward from the score gradients just computed (selections fixed)
+        dkr = torch.empty((w.H, w.n_rows, w.d_key), dtype=torch.float32, device="cuda")
+        dkc = torch.empty((w.H, w.n_cols, w.d_key), dtype=torch.float32, device="cuda")
+        wsr = P.workspace(desc, 7)
+        rb = lambda: P.omnimoe_route_backward(  # noqa: E731
+            desc, d_in["x"], d_in["keys_row"], d_in["keys_col"], idx, dsc, dx, dkr, dkc,
+            ws=wsr, stream=stream)
+        rb()
+        ev0.record(stream)
+        for _ in range(args.steps):
+            rb()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        rb_ms = ev0.elapsed_time(ev1) / args.steps
+        backward = {"expert_backward_ms": bw_ms, "route_backward_ms": rb_ms,
+                    "active_rows": n_active,
+                    "tokens_per_s": w.T / ((bw_ms + rb_ms) * 1e-3)}
+        log(f"expert backward: {bw_ms:.3f} ms, router backward: {rb_ms:.3f} ms")
+        del dy, dx, du, dv, wsb, dkr, dkc, wsr
     return ablation, shared_mlp, no_cpr, backward
 
 

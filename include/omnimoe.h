@@ -97,7 +97,8 @@ typedef enum {
   OMNIMOE_STAGE_EXPERT = 3,
   OMNIMOE_STAGE_LAYER = 4,
   OMNIMOE_STAGE_ROUTE_DENSE = 5,    /* omnimoe_route_dense without a logits buffer */
-  OMNIMOE_STAGE_EXPERT_BACKWARD = 6 /* omnimoe_expert_backward */
+  OMNIMOE_STAGE_EXPERT_BACKWARD = 6, /* omnimoe_expert_backward */
+  OMNIMOE_STAGE_ROUTE_BACKWARD = 7   /* omnimoe_route_backward */
 } omnimoe_stage;
 
 /* Bytes of workspace the given stage's entry point needs for this shape. */
@@ -203,6 +204,25 @@ omnimoe_status omnimoe_expert_backward(const omnimoe_layer_desc* desc, const voi
                                        const float* dy, float* dx, float* du_rows,
                                        float* dv_rows, float* dgates, float* dscores,
                                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* Backward of the router's scores for fixed selections (the top-K choice is piecewise
+ * constant, so gradients flow only through the selected scores S_p = s_r[i_p] + s_c[j_p],
+ * Eq. 9 and 11), given dscores (as from omnimoe_expert_backward):
+ *   dkeys_row [H, n_rows, d_key] fp32 out   row (h, i): sum over the tasks of head h whose
+ *                                          expert lies in grid row i of dscores_p x_t[0:d_key]
+ *   dkeys_col [H, n_cols, d_key] fp32 out   the same for grid columns, with x_t[c0:c0+d_key]
+ *   dx        [T, d] fp32 in/out           adds sum over t's tasks of dscores_p keys_row[h, i_p]
+ *                                          (columns 0:d_key) and dscores_p keys_col[h, j_p]
+ *                                          (columns c0:c0+d_key); c0 = d_key (split) or 0
+ * Tasks are sorted by sub-key with the schedule's radix sort and each sub-key's gradient is
+ * summed over its tasks in task order, so the result is the same on every run. d_key <= 4096
+ * (bf16) or 2048 (fp32), else OMNIMOE_ERR_UNSUPPORTED. Workspace: OMNIMOE_STAGE_ROUTE_BACKWARD
+ * bytes. */
+omnimoe_status omnimoe_route_backward(const omnimoe_layer_desc* desc, const void* x,
+                                      const void* keys_row, const void* keys_col,
+                                      const int32_t* idx, const float* dscores, float* dx,
+                                      float* dkeys_row, float* dkeys_col, void* workspace,
+                                      size_t workspace_bytes, void* stream);
 
 /* The whole routed layer: route, schedule and expert compute on one stream, no host
  * synchronisation. y [T, d] fp32 out; idx_out and gates_out ([T, H, K]) may be NULL. */

@@ -18,7 +18,7 @@ OMNIMOE_F32, OMNIMOE_BF16 = 0, 1
 OMNIMOE_ACT_GELU, OMNIMOE_ACT_SILU = 0, 1
 OMNIMOE_QUERY_SPLIT, OMNIMOE_QUERY_SHARED = 0, 1
 (STAGE_ROUTE, STAGE_SELECT, STAGE_SCHEDULE, STAGE_EXPERT, STAGE_LAYER, STAGE_ROUTE_DENSE,
- STAGE_EXPERT_BACKWARD) = range(7)
+ STAGE_EXPERT_BACKWARD, STAGE_ROUTE_BACKWARD) = range(8)
 KERNEL_NAMES = ("score", "select", "schedule", "expert_dot", "accumulate")
 
 EXPORTED = (
@@ -26,6 +26,7 @@ EXPORTED = (
     "omnimoe_select_dense", "omnimoe_shared_mlp", "omnimoe_shared_mlp_workspace_size",
     "omnimoe_schedule",
     "omnimoe_expert_forward", "omnimoe_expert_forward_token_centric", "omnimoe_expert_backward",
+    "omnimoe_route_backward",
     "omnimoe_layer_forward", "omnimoe_timer_create",
     "omnimoe_timer_destroy", "omnimoe_timer_read", "omnimoe_layer_forward_timed",
     "omnimoe_status_string",
@@ -70,6 +71,7 @@ def load_library():
         "omnimoe_expert_forward": [D, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_expert_forward_token_centric": [D, P, P, P, P, P, P, P],
         "omnimoe_expert_backward": [D, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
+        "omnimoe_route_backward": [D, P, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_layer_forward": [D, P, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_layer_forward_timed": [D, P, P, P, P, P, P, P, P, P, SZ, P, P],
         "omnimoe_timer_create": [I32, ctypes.POINTER(P)],
@@ -205,6 +207,15 @@ def omnimoe_expert_backward(desc, x, u, v, idx, gates, perm, active_offsets, n_a
         ctypes.byref(desc), _ptr(x), _ptr(u), _ptr(v), _ptr(idx), _ptr(gates), _ptr(perm),
         _ptr(active_offsets), _ptr(n_active), _ptr(dy), _ptr(dx), _ptr(du_rows), _ptr(dv_rows),
         _ptr(dgates), _ptr(dscores), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def omnimoe_route_backward(desc, x, keys_row, keys_col, idx, dscores, dx, dkeys_row, dkeys_col,
+                           ws=None, stream=None):
+    if ws is None:
+        ws = workspace(desc, STAGE_ROUTE_BACKWARD, x.device)
+    _check("omnimoe_route_backward", load_library().omnimoe_route_backward(
+        ctypes.byref(desc), _ptr(x), _ptr(keys_row), _ptr(keys_col), _ptr(idx), _ptr(dscores),
+        _ptr(dx), _ptr(dkeys_row), _ptr(dkeys_col), _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def omnimoe_layer_forward(desc, x, keys_row, keys_col, u, v, y, idx_out=None, gates_out=None,

@@ -90,6 +90,7 @@ size_t stage_bytes(const Shape& s, int stage) {
     case OMNIMOE_STAGE_EXPERT: return m_bytes(s);
     case OMNIMOE_STAGE_ROUTE_DENSE: return dense_bytes(s);
     case OMNIMOE_STAGE_EXPERT_BACKWARD: return omnimoe::backward_ws_bytes(s.M);
+    case OMNIMOE_STAGE_ROUTE_BACKWARD: return omnimoe::route_backward_ws_bytes(s);
     default: {
       // idx, gates, perm, active, active_offsets, n_active, then the logits (dead after
       // selection) overlapped with the sort buffers and the a[] buffer.
@@ -182,7 +183,7 @@ const char* omnimoe_status_string(int32_t status) {
 omnimoe_status omnimoe_workspace_size(const omnimoe_layer_desc* desc, int32_t stage,
                                       size_t* bytes) {
   if (!bytes) return OMNIMOE_ERR_INVALID_ARG;
-  if (stage < OMNIMOE_STAGE_ROUTE || stage > OMNIMOE_STAGE_EXPERT_BACKWARD)
+  if (stage < OMNIMOE_STAGE_ROUTE || stage > OMNIMOE_STAGE_ROUTE_BACKWARD)
     return OMNIMOE_ERR_INVALID_ARG;
   Shape s;
   omnimoe_status st = check_desc(desc, &s);
@@ -394,6 +395,24 @@ omnimoe_status omnimoe_expert_backward(const omnimoe_layer_desc* desc, const voi
   return hip_status(omnimoe::launch_expert_backward(s, x, u, v, idx, gates, perm, active_offsets,
                                                     n_active, dy, dx, du_rows, dv_rows, dgates,
                                                     dscores, ws, (hipStream_t)stream));
+}
+
+omnimoe_status omnimoe_route_backward(const omnimoe_layer_desc* desc, const void* x,
+                                      const void* keys_row, const void* keys_col,
+                                      const int32_t* idx, const float* dscores, float* dx,
+                                      float* dkeys_row, float* dkeys_col, void* ws,
+                                      size_t ws_bytes, void* stream) {
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  if (s.T == 0) return OMNIMOE_OK;
+  if (s.dk > (s.bf16 ? 4096 : 2048)) return OMNIMOE_ERR_UNSUPPORTED;
+  if ((st = check_ptrs({x, keys_row, keys_col, idx, dscores, dx, dkeys_row, dkeys_col, ws})))
+    return st;
+  if (ws_bytes < stage_bytes(s, OMNIMOE_STAGE_ROUTE_BACKWARD)) return OMNIMOE_ERR_WORKSPACE;
+  return hip_status(omnimoe::launch_route_backward(s, x, keys_row, keys_col, idx, dscores, dx,
+                                                   dkeys_row, dkeys_col, ws,
+                                                   (hipStream_t)stream));
 }
 
 omnimoe_status omnimoe_layer_forward(const omnimoe_layer_desc* desc, const void* x,

@@ -11,6 +11,10 @@
 //   ascending) and sums du and dv in that order: the expert-major order makes the per-expert
 //   gradients plain sequential sums, with no atomics, so every run gives the same bits;
 // score pass: one wavefront per (token, head) row.
+// Router backward (selections fixed; S_p = s_r[i_p] + s_c[j_p]): tasks are sorted by sub-key
+// row (h, i) with the schedule's radix sort, and one wavefront per selected sub-key sums
+// dscores_p x_t over its segment in task order (the same expert-major pattern, applied to the
+// sub-key tables); the input gradient adds dscores_p times the two sub-keys, token by token.
 #include "device_common.hpp"
 #include "internal.hpp"
 
@@ -203,6 +207,182 @@ __global__ __launch_bounds__(256) void bwd_score_kernel(BwdArgs a) {
   }
 }
 
+// Sub-key of every task for one half: key = h * n_half + (row or column of the expert id).
+__global__ __launch_bounds__(256) void subkey_kernel(const int32_t* idx, int32_t* key, int64_t m,
+                                                     int hk, int K, int nc, int n_half, int col,
+                                                     int64_t n_experts) {
+  const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (p >= m) return;
+  const int e = clamp_id(idx[p], n_experts);
+  const int h = (int)((p % hk) / K);
+  key[p] = h * n_half + (col ? e % nc : e / nc);
+}
+
+struct KeySumArgs {
+  const void* x;
+  const float* ds;
+  const int32_t* perm;
+  const int32_t* active;
+  const int32_t* offsets;
+  const int32_t* n_active;
+  float* dk;         // [H * n_half, d_key]
+  int64_t M;
+  int64_t cap;
+  int64_t n_keys;
+  int d;             // row length of x
+  int dkey;
+  int c0;            // first x column of this half's query
+  int hk;
+  int nchunks;       // 16-byte chunks of a d_key slice
+};
+
+// One wavefront per selected sub-key: dk[key] = sum over its tasks (task order) of ds_p x_t.
+template <int CPL, bool BF16>
+__global__ __launch_bounds__(256) void keysum_kernel(KeySumArgs a) {
+  constexpr int EPC = BF16 ? 8 : 4;
+  const int l = lane_id();
+  const int64_t xrc = a.d / EPC;   // chunks per x row
+  const int64_t c0 = a.c0 / EPC;
+  const uint4* X = (const uint4*)a.x;
+  bool cv[CPL];
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) cv[q] = (l + kWave * q) < a.nchunks;
+  const int64_t na = *a.n_active < a.cap ? *a.n_active : a.cap;
+  const int64_t stride = (int64_t)gridDim.x * 4;
+  for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < na; r += stride) {
+    float acc[CPL][EPC];
+#pragma unroll
+    for (int q = 0; q < CPL; ++q)
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) acc[q][k] = 0.0f;
+    int64_t b = a.offsets[r], e = a.offsets[r + 1];
+    b = b < 0 ? 0 : (b > a.M ? a.M : b);
+    e = e < b ? b : (e > a.M ? a.M : e);
+    for (int64_t tau = b; tau < e; ++tau) {
+      const int p = clamp_id(a.perm[tau], a.M);
+      const int64_t t = p / a.hk;
+      const float w = a.ds[p];
+#pragma unroll
+      for (int q = 0; q < CPL; ++q) {
+        if (!cv[q]) continue;
+        const uint4 xc = X[t * xrc + c0 + l + kWave * q];
+#pragma unroll
+        for (int k = 0; k < EPC; ++k) acc[q][k] = fmaf(w, chunk_elem<BF16>(xc, k), acc[q][k]);
+      }
+    }
+    const int key = clamp_id(a.active[r], a.n_keys);
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      if (!cv[q]) continue;
+      float4* o = (float4*)(a.dk + (int64_t)key * a.dkey + (int64_t)(l + kWave * q) * EPC);
+#pragma unroll
+      for (int k = 0; k < EPC; k += 4) o[k / 4] = make_float4(acc[q][k], acc[q][k + 1], acc[q][k + 2], acc[q][k + 3]);
+    }
+  }
+}
+
+struct RouteDxArgs {
+  const void* kr;
+  const void* kc;
+  const int32_t* idx;
+  const float* ds;
+  float* dx;
+  int64_t T;
+  int64_t N;
+  int d;
+  int dkey;
+  int c0;
+  int hk;
+  int K;
+  int nr, nc;
+  int nchunks;   // 16-byte chunks of a d_key row
+};
+
+// dx_t[0 : d_key] += sum of ds_p keys_row[h, i_p]; dx_t[c0 : c0 + d_key] += sum of ds_p
+// keys_col[h, j_p]; one wavefront per token, slots in order.
+template <int CPL, bool BF16>
+__global__ __launch_bounds__(256) void route_dx_kernel(RouteDxArgs a) {
+  constexpr int EPC = BF16 ? 8 : 4;
+  const int l = lane_id();
+  const uint4* KR = (const uint4*)a.kr;
+  const uint4* KC = (const uint4*)a.kc;
+  const int64_t rc = a.nchunks;
+  bool cv[CPL];
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) cv[q] = (l + kWave * q) < a.nchunks;
+  const int64_t stride = (int64_t)gridDim.x * 4;
+  for (int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < a.T; t += stride) {
+    float ar[CPL][EPC], ac[CPL][EPC];
+#pragma unroll
+    for (int q = 0; q < CPL; ++q)
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) ar[q][k] = ac[q][k] = 0.0f;
+    for (int s = 0; s < a.hk; ++s) {
+      const int64_t p = t * a.hk + s;
+      const int e = clamp_id(a.idx[p], a.N);
+      const int h = s / a.K;
+      const float w = a.ds[p];
+      const int64_t ri = (int64_t)h * a.nr + e / a.nc;
+      const int64_t cj = (int64_t)h * a.nc + e % a.nc;
+#pragma unroll
+      for (int q = 0; q < CPL; ++q) {
+        if (!cv[q]) continue;
+        const uint4 r = KR[ri * rc + l + kWave * q];
+        const uint4 c = KC[cj * rc + l + kWave * q];
+#pragma unroll
+        for (int k = 0; k < EPC; ++k) {
+          ar[q][k] = fmaf(w, chunk_elem<BF16>(r, k), ar[q][k]);
+          ac[q][k] = fmaf(w, chunk_elem<BF16>(c, k), ac[q][k]);
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      if (!cv[q]) continue;
+      float* o1 = a.dx + t * a.d + (int64_t)(l + kWave * q) * EPC;
+      float* o2 = a.dx + t * a.d + a.c0 + (int64_t)(l + kWave * q) * EPC;
+      if (a.c0 == 0) {
+#pragma unroll
+        for (int k = 0; k < EPC; ++k) o1[k] += ar[q][k] + ac[q][k];
+      } else {
+#pragma unroll
+        for (int k = 0; k < EPC; ++k) {
+          o1[k] += ar[q][k];
+          o2[k] += ac[q][k];
+        }
+      }
+    }
+  }
+}
+
+template <int CPL, bool BF16>
+void launch_router_bwd_kernels(const KeySumArgs& kr, const KeySumArgs& kc, const RouteDxArgs& rd,
+                               int pass, hipStream_t st) {
+  if (pass < 2) {
+    const KeySumArgs& a = pass == 0 ? kr : kc;
+    int64_t blocks = (a.cap + 3) / 4;
+    if (blocks > 65536) blocks = 65536;
+    hipLaunchKernelGGL((keysum_kernel<CPL, BF16>), dim3((unsigned)blocks), dim3(256), 0, st, a);
+  } else {
+    int64_t blocks = (rd.T + 3) / 4;
+    if (blocks > 16384) blocks = 16384;
+    hipLaunchKernelGGL((route_dx_kernel<CPL, BF16>), dim3((unsigned)blocks), dim3(256), 0, st, rd);
+  }
+}
+
+template <bool BF16>
+hipError_t dispatch_router_bwd(int cpl, const KeySumArgs& kr, const KeySumArgs& kc,
+                               const RouteDxArgs& rd, int pass, hipStream_t st) {
+  switch (cpl) {
+    case 1: launch_router_bwd_kernels<1, BF16>(kr, kc, rd, pass, st); break;
+    case 2: launch_router_bwd_kernels<2, BF16>(kr, kc, rd, pass, st); break;
+    case 4: launch_router_bwd_kernels<4, BF16>(kr, kc, rd, pass, st); break;
+    case 8: launch_router_bwd_kernels<8, BF16>(kr, kc, rd, pass, st); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 int cpl_of(int nchunks) {
   int c = 1;
   while (c * kWave < nchunks) c <<= 1;
@@ -279,6 +459,90 @@ hipError_t launch_expert_backward(const Shape& s, const void* x, const void* u, 
   if (sb > 16384) sb = 16384;
   hipLaunchKernelGGL(bwd_score_kernel, dim3((unsigned)sb), dim3(256), 0, st, a);
   return hipGetLastError();
+}
+
+size_t route_backward_ws_bytes(const Shape& s) {
+  const int64_t nkeys = (int64_t)s.H * (s.nr > s.nc ? s.nr : s.nc);
+  const int64_t cap = s.M < nkeys ? s.M : nkeys;
+  auto al = [](size_t v) { return (v + 255) & ~(size_t)255; };
+  return 2 * al((size_t)s.M * 4) + al((size_t)s.M * 4) + 2 * al((size_t)(cap + 1) * 4) + 256 +
+         schedule_ws_bytes(s.M, nkeys);
+}
+
+hipError_t launch_route_backward(const Shape& s, const void* x, const void* keys_row,
+                                 const void* keys_col, const int32_t* idx, const float* dscores,
+                                 float* dx, float* dkeys_row, float* dkeys_col, void* ws,
+                                 hipStream_t st) {
+  if (s.T == 0) return hipSuccess;
+  auto al = [](size_t v) { return (v + 255) & ~(size_t)255; };
+  const int64_t nkeys = (int64_t)s.H * (s.nr > s.nc ? s.nr : s.nc);
+  const int64_t cap = s.M < nkeys ? s.M : nkeys;
+  char* w = (char*)ws;
+  int32_t* rkey = (int32_t*)w; w += al((size_t)s.M * 4);
+  int32_t* ckey = (int32_t*)w; w += al((size_t)s.M * 4);
+  int32_t* perm = (int32_t*)w; w += al((size_t)s.M * 4);
+  int32_t* active = (int32_t*)w; w += al((size_t)(cap + 1) * 4);
+  int32_t* offsets = (int32_t*)w; w += al((size_t)(cap + 1) * 4);
+  int32_t* n_active = (int32_t*)w; w += 256;
+  void* sws = w;
+  const int64_t mb = (s.M + 255) / 256;
+  hipLaunchKernelGGL(subkey_kernel, dim3((unsigned)mb), dim3(256), 0, st, idx, rkey, s.M, s.hk,
+                     s.K, s.nc, s.nr, 0, s.N);
+  hipLaunchKernelGGL(subkey_kernel, dim3((unsigned)mb), dim3(256), 0, st, idx, ckey, s.M, s.hk,
+                     s.K, s.nc, s.nc, 1, s.N);
+  hipError_t e = launch_fill_i32((int32_t*)dkeys_row, (int64_t)s.H * s.nr * s.dk, 0, st);
+  if (e == hipSuccess) e = launch_fill_i32((int32_t*)dkeys_col, (int64_t)s.H * s.nc * s.dk, 0, st);
+  if (e != hipSuccess) return e;
+  const int epc = s.bf16 ? 8 : 4;
+  const int nchunks = s.dk / epc;
+  const int cpl = cpl_of(nchunks);
+  KeySumArgs ka;
+  ka.x = x;
+  ka.ds = dscores;
+  ka.perm = perm;
+  ka.active = active;
+  ka.offsets = offsets;
+  ka.n_active = n_active;
+  ka.M = s.M;
+  ka.d = s.d;
+  ka.dkey = s.dk;
+  ka.hk = s.hk;
+  ka.nchunks = nchunks;
+  RouteDxArgs rd;
+  rd.kr = keys_row;
+  rd.kc = keys_col;
+  rd.idx = idx;
+  rd.ds = dscores;
+  rd.dx = dx;
+  rd.T = s.T;
+  rd.N = s.N;
+  rd.d = s.d;
+  rd.dkey = s.dk;
+  rd.c0 = s.col0;
+  rd.hk = s.hk;
+  rd.K = s.K;
+  rd.nr = s.nr;
+  rd.nc = s.nc;
+  rd.nchunks = nchunks;
+  for (int half = 0; half < 2; ++half) {
+    // the tasks sorted by this half's sub-key, then one wavefront per selected sub-key
+    Shape ss = s;
+    ss.N = (int64_t)s.H * (half ? s.nc : s.nr);
+    ss.B = 1;
+    const int32_t* sk = nullptr;
+    e = launch_schedule(ss, half ? ckey : rkey, perm, active, offsets, n_active, nullptr, sws, &sk,
+                        st);
+    if (e != hipSuccess) return e;
+    ka.cap = s.M < ss.N ? s.M : ss.N;
+    ka.n_keys = ss.N;
+    ka.c0 = half ? s.col0 : 0;
+    ka.dk = half ? dkeys_col : dkeys_row;
+    e = s.bf16 ? dispatch_router_bwd<true>(cpl, ka, ka, rd, 0, st)
+               : dispatch_router_bwd<false>(cpl, ka, ka, rd, 0, st);
+    if (e != hipSuccess) return e;
+  }
+  return s.bf16 ? dispatch_router_bwd<true>(cpl, ka, ka, rd, 2, st)
+                : dispatch_router_bwd<false>(cpl, ka, ka, rd, 2, st);
 }
 
 }  // namespace omnimoe

@@ -76,6 +76,13 @@ hipError_t launch_expert_backward(const Shape& s, const void* x, const void* u, 
                                   const float* dy, float* dx, float* du, float* dv,
                                   float* dgates, float* dscores, void* ws, hipStream_t st);
 
+// Router backward for fixed selections: dkeys_row / dkeys_col written in full, dx added to.
+size_t route_backward_ws_bytes(const Shape& s);
+hipError_t launch_route_backward(const Shape& s, const void* x, const void* keys_row,
+                                 const void* keys_col, const int32_t* idx, const float* dscores,
+                                 float* dx, float* dkeys_row, float* dkeys_col, void* ws,
+                                 hipStream_t st);
+
 // y[t] = sum over slots (h, k) in order of a[p] * v[idx[p]].
 hipError_t launch_accumulate(const Shape& s, const void* v, const int32_t* idx, const float* a,
                              float* y, hipStream_t st);

@@ -24,7 +24,7 @@ def _declared_functions():
 def test_header_matches_exports():
     lib = P.load_library()
     names = _declared_functions()
-    assert len(names) == 17
+    assert len(names) == 18
     assert sorted(P.EXPORTED) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -119,6 +119,9 @@ def test_entry_points_check_pointers_before_launch():
                                        n(1 << 40), None) == INVALID
     assert lib.omnimoe_expert_backward(D, a, a, a, a, a, a, a, a, a, a, a, a, a, a, a, n(4),
                                        None) == WORKSPACE
+    assert lib.omnimoe_route_backward(D, a, a, a, a, a, a, a, a, a, n(4), None) == WORKSPACE
+    assert lib.omnimoe_route_backward(D, a, a, a, a, None, a, a, a, a, n(1 << 40),
+                                      None) == INVALID
     assert lib.omnimoe_shared_mlp(D, 12, a, a, a, a, a, n(1 << 40), None) == INVALID
     assert lib.omnimoe_shared_mlp(D, 64, a, a, a, a, a, n(16), None) == WORKSPACE
     assert lib.omnimoe_shared_mlp(D, 64, a, a, bad, a, a, n(1 << 40), None) == ALIGN

@@ -743,3 +743,43 @@ def test_expert_backward(name):
     for k, v in out.items():
         rows = n if k in ("du", "dv") else None
         assert np.array_equal(v.cpu().numpy()[:rows].view(np.uint8), got[k][:rows].view(np.uint8))
+
+
+@pytest.mark.parametrize("name", ["tiny_f32", "small_bf16", "ragged_bf16", "ragged_f32",
+                                  "shared_bf16", "k256_bf16", "skinny_bf16"])
+def test_route_backward(name):
+    w = SHAPES[name]
+    say(f"[route backward] {name}")
+    inp, f = host_inputs(w)
+    dsc = oracle.desc(w)
+    sr, sc = oracle.half_scores(dsc, f["x"], f["keys_row"], f["keys_col"])
+    idx, _, _, _ = oracle.select(dsc, sr, sc, oracle.CARTESIAN)
+    rng = np.random.default_rng(7 + len(name))
+    ds = rng.standard_normal((w.T, w.H, w.K)).astype(np.float32)
+    dx0 = rng.standard_normal((w.T, w.d)).astype(np.float32)
+    dev = upload(inp)
+    dx = to_dev(dx0.copy())
+    dkr = torch.full((w.H, w.n_rows, w.d_key), float("nan"), dtype=torch.float32, device="cuda")
+    dkc = torch.full((w.H, w.n_cols, w.d_key), float("nan"), dtype=torch.float32, device="cuda")
+    P.omnimoe_route_backward(B.make_desc(w), dev["x"], dev["keys_row"], dev["keys_col"],
+                             to_dev(idx), to_dev(ds), dx, dkr, dkc)
+    torch.cuda.synchronize()
+    got = (dx.cpu().numpy(), dkr.cpu().numpy(), dkc.cpu().numpy())
+    ref = oracle.route_backward(dsc, f["x"], f["keys_row"], f["keys_col"], idx, ds, dx=dx0)
+    # the same sums over absolute values bound the fp32 summation error (Higham): gamma_n times
+    # the sum of |terms|, n the number of terms of the element
+    absb = oracle.route_backward(dsc, np.abs(f["x"]), np.abs(f["keys_row"]),
+                                 np.abs(f["keys_col"]), idx, np.abs(ds), dx=np.abs(dx0))
+    u = 2.0 ** -23
+    hk = w.H * w.K
+    i_r = (np.arange(w.H)[None, :, None] * w.n_rows + idx // w.n_cols).ravel()
+    i_c = (np.arange(w.H)[None, :, None] * w.n_cols + idx % w.n_cols).ravel()
+    n_r = np.bincount(i_r, minlength=w.H * w.n_rows).reshape(w.H, w.n_rows, 1) + 1
+    n_c = np.bincount(i_c, minlength=w.H * w.n_cols).reshape(w.H, w.n_cols, 1) + 1
+    for k, gv, rv, ab, n in (("dx", got[0], ref[0], absb[0], 2 * hk + 2),
+                             ("dkeys_row", got[1], ref[1], absb[1], n_r),
+                             ("dkeys_col", got[2], ref[2], absb[2], n_c)):
+        bound = 2 * (n * u / (1 - n * u)) * ab + 1e-30
+        err = np.abs(gv.astype(np.float64) - rv)
+        say(f"  {k}: max err / bound {(err / bound).max():.3f}")
+        assert np.all(err <= bound), k
