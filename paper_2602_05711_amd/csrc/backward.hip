@@ -70,6 +70,7 @@ __device__ __forceinline__ float chunk_elem(const uint4& c, int k) {
 template <int CPL, bool BF16>
 __global__ __launch_bounds__(256) void bwd_token_kernel(BwdArgs a) {
   constexpr int EPC = BF16 ? 8 : 4;
+  constexpr int G = CPL >= 8 ? 1 : (CPL >= 4 ? 2 : 4);
   const int l = lane_id();
   const uint4* X = (const uint4*)a.x;
   const uint4* U = (const uint4*)a.u;
@@ -93,37 +94,49 @@ __global__ __launch_bounds__(256) void bwd_token_kernel(BwdArgs a) {
         acc[q][k] = 0.0f;
       }
     }
-    for (int s = 0; s < a.hk; ++s) {
-      const int64_t p = t * a.hk + s;
-      const int e = clamp_id(a.idx[p], a.N);
-      const float g = a.gates[p];
-      uint4 ur[CPL], vr[CPL];
+    // G slots at a time: their u and v rows are all in flight before the first reduction
+    for (int s0 = 0; s0 < a.hk; s0 += G) {
+      uint4 ur[G][CPL], vr[G][CPL];
+      float gj[G];
+      int64_t pj[G];
 #pragma unroll
-      for (int q = 0; q < CPL; ++q) {
-        ur[q] = cv[q] ? U[(int64_t)e * rc + l + kWave * q] : make_uint4(0, 0, 0, 0);
-        vr[q] = cv[q] ? V[(int64_t)e * rc + l + kWave * q] : make_uint4(0, 0, 0, 0);
-      }
-      float hs = 0.0f, ds = 0.0f;
+      for (int i = 0; i < G; ++i) {
+        const int s = s0 + i < a.hk ? s0 + i : a.hk - 1;
+        pj[i] = t * a.hk + s;
+        const int e = clamp_id(a.idx[pj[i]], a.N);
+        gj[i] = a.gates[pj[i]];
 #pragma unroll
-      for (int q = 0; q < CPL; ++q)
-#pragma unroll
-        for (int k = 0; k < EPC; ++k) {
-          hs = fmaf(chunk_elem<BF16>(xr[q], k), chunk_elem<BF16>(ur[q], k), hs);
-          ds = fmaf(dyr[q][k], chunk_elem<BF16>(vr[q], k), ds);
+        for (int q = 0; q < CPL; ++q) {
+          ur[i][q] = cv[q] ? U[(int64_t)e * rc + l + kWave * q] : make_uint4(0, 0, 0, 0);
+          vr[i][q] = cv[q] ? V[(int64_t)e * rc + l + kWave * q] : make_uint4(0, 0, 0, 0);
         }
-      const float h = wave_sum_uniform(hs);
-      const float da = wave_sum_uniform(ds);
-      const float act = activation(a.act, h);
-      const float dh = da * g * activation_grad(a.act, h);
-      if (l == 0) {
-        a.a[p] = g * act;
-        a.dh[p] = dh;
-        a.dgates[p] = da * act;
       }
 #pragma unroll
-      for (int q = 0; q < CPL; ++q)
+      for (int i = 0; i < G; ++i) {
+        if (s0 + i >= a.hk) break;
+        float hs = 0.0f, ds = 0.0f;
 #pragma unroll
-        for (int k = 0; k < EPC; ++k) acc[q][k] = fmaf(dh, chunk_elem<BF16>(ur[q], k), acc[q][k]);
+        for (int q = 0; q < CPL; ++q)
+#pragma unroll
+          for (int k = 0; k < EPC; ++k) {
+            hs = fmaf(chunk_elem<BF16>(xr[q], k), chunk_elem<BF16>(ur[i][q], k), hs);
+            ds = fmaf(dyr[q][k], chunk_elem<BF16>(vr[i][q], k), ds);
+          }
+        const float h = wave_sum_uniform(hs);
+        const float da = wave_sum_uniform(ds);
+        const float act = activation(a.act, h);
+        const float dh = da * gj[i] * activation_grad(a.act, h);
+        if (l == 0) {
+          a.a[pj[i]] = gj[i] * act;
+          a.dh[pj[i]] = dh;
+          a.dgates[pj[i]] = da * act;
+        }
+#pragma unroll
+        for (int q = 0; q < CPL; ++q)
+#pragma unroll
+          for (int k = 0; k < EPC; ++k)
+            acc[q][k] = fmaf(dh, chunk_elem<BF16>(ur[i][q], k), acc[q][k]);
+      }
     }
 #pragma unroll
     for (int q = 0; q < CPL; ++q) {
