@@ -355,19 +355,27 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
 }
 
 // ---------------------------------------------------------------- large K (65 .. 4096)
-// One workgroup of four waves per (token, head) row, for K beyond one wavefront:
-//   1. both halves are bitonic-sorted in LDS by (logit desc, index asc);
-//   2. the Cartesian candidates (a, b) with (a+1)(b+1) <= K are enumerated as a flat list
-//      (row rank a holds min(Kc, floor(K / (a+1))) of them; the offsets depend only on
-//      (K, Kr, Kc) and are computed once per workgroup), each thread walking a contiguous
-//      chunk; a candidate's key is (S as an order-preserving 64-bit integer, ~id);
-//   3. an 8-bit-digit radix select over the 96-bit keys finds the K-th largest key exactly
-//      (twelve passes with an LDS histogram), the K keys at or above it are gathered and
-//      bitonic-sorted descending;
-//   4. gates: softmax over the K scores, summed in a fixed order.
+// One workgroup per (token, head) row, for K beyond one wavefront (eight waves when the final
+// sort holds 2048 keys or more, four below, where more rows share a compute unit):
+//   1. each half is put in (logit desc, index asc) order. A half of at most 512 logits is
+//      ordered by counting, for each key, the larger keys of its half (keys are distinct, so
+//      that count is the key's rank); a longer half by a bitonic sort in LDS;
+//   2. the Cartesian candidates (a, b) with (a+1)(b+1) <= K form a flat list (row rank a
+//      holds min(Kc, floor(K / (a+1))) of them; the offsets depend only on (K, Kr, Kc) and are
+//      computed once per workgroup), and each thread walks a contiguous chunk of it. A
+//      candidate's key is (S as an order-preserving 64-bit integer, ~id);
+//   3. a radix select over the 96-bit keys, eight bits at a time from the top (twelve passes
+//      with an LDS histogram), finds the K-th largest key exactly. Passes walk every candidate
+//      until the keys that share the decided prefix fit in LDS; the next pass also copies
+//      those keys out, and the remaining passes read only the copy (one wave alone takes them
+//      when the copy is short, with no workgroup barriers);
+//   4. the K keys at or above the threshold are gathered and bitonic-sorted descending;
+//   5. gates: softmax over the K scores, summed in a fixed order.
 // Integer comparisons throughout, so the result is exact and independent of thread timing.
 
-constexpr int kLargeThreads = 256;
+constexpr int kLargeMaxWaves = 8;  // workgroups of 256 or 512 threads
+constexpr int kRankSortMax = 512;  // halves up to this padded length are ordered by counting
+constexpr int kWaveFinish = 1024;  // radix survivors up to this many are finished by one wave
 
 struct LargeArgs {
   const float* hs;
@@ -379,9 +387,23 @@ struct LargeArgs {
   int k2;   // power of two >= K
 };
 
+// LDS after the sorted halves: the selected keys (k2 of 12 bytes). Before the gather the
+// same bytes hold the radix survivors and, when counting orders the halves, the unsorted
+// half keys.
+size_t large_region_bytes(int n2, int k2) {
+  const size_t sel = (size_t)k2 * 12;
+  const size_t stage = n2 <= kRankSortMax ? (size_t)2 * n2 * 8 : 0;
+  return sel > stage ? sel : stage;
+}
+__device__ __forceinline__ int large_region_bytes_dev(int n2, int k2) {
+  const int sel = k2 * 12;
+  const int stage = n2 <= kRankSortMax ? 2 * n2 * 8 : 0;
+  return sel > stage ? sel : stage;
+}
+
 // Bytes of dynamic LDS the kernel needs.
 size_t large_lds_bytes(int n2, int k2, int kr) {
-  return (size_t)2 * n2 * 8 + (size_t)k2 * 12 + (size_t)(kr + 1) * 4;
+  return (size_t)2 * n2 * 8 + large_region_bytes(n2, k2) + (size_t)(kr + 1) * 4;
 }
 
 struct LargeShared {
@@ -389,26 +411,197 @@ struct LargeShared {
   uint64_t ts, ms;   // decided high bits of the threshold key and their mask (score part)
   uint32_t tn, mn;   // the same for the ~id part
   int krem;          // keys still to select at and below the current digit
+  int mode;          // 0: walk every candidate; 1: walk and copy the prefix matches; 2: read the copy
+  int nsurv;         // keys copied
   int count;         // gathered keys
-  int first_pass;    // first radix pass that needs a histogram
-  uint64_t wlo[4], whi[4];
-  int wint[4];
-  float wsum[4];
+  int wint[kLargeMaxWaves];
+  float wsum[kLargeMaxWaves];
 };
 
-// Key of candidate (a, b) from the sorted half keys.
-__device__ __forceinline__ void cand_key(const uint64_t* rk, const uint64_t* ck, int a, int b, int nc,
-                                         uint64_t* ks, uint32_t* kn) {
-  const uint64_t r = rk[a], c = ck[b];
-  const float vr = f32_from_ord((uint32_t)(r >> 32));
-  const float vc = f32_from_ord((uint32_t)(c >> 32));
-  const uint32_t i = 0xFFFFFFFFu - (uint32_t)r;
-  const uint32_t j = 0xFFFFFFFFu - (uint32_t)c;
-  *ks = ord_f64((double)vr + (double)vc);
-  *kn = 0xFFFFFFFFu - (i * (uint32_t)nc + j);
+// Walks one thread's chunk of the flat candidate list, one candidate after the other. The
+// current row rank's logit (as a double) and id offset stay in registers; the next column key
+// and the next row rank's key and end offset are read one step ahead, so LDS latency overlaps
+// the work on the current candidate. Every row rank below kr holds at least one candidate,
+// so a step moves at most one row rank on.
+struct CandWalk {
+  const uint64_t* rk;
+  const uint64_t* ck;
+  const uint32_t* cum;
+  int kr, nc;
+  int ra, rb, rend;
+  double vr;
+  uint32_t rid;
+  uint64_t cv;     // column key of the current candidate
+  uint64_t rnext;  // key of row rank ra + 1
+  int rend_next;   // end offset of row rank ra + 1
+
+  __device__ __forceinline__ void set_row(uint64_t r) {
+    vr = (double)f32_from_ord((uint32_t)(r >> 32));
+    rid = (0xFFFFFFFFu - (uint32_t)r) * (uint32_t)nc;
+  }
+  __device__ __forceinline__ void prefetch_row() {
+    if (ra + 1 < kr) {
+      rnext = rk[ra + 1];
+      rend_next = (int)cum[ra + 2];
+    }
+  }
+  // Positions the walk at candidate c0 of row rank a_first (c0 < P).
+  __device__ __forceinline__ void start(int a_first, int c0) {
+    ra = a_first;
+    rb = c0 - (int)cum[ra];
+    rend = (int)cum[ra + 1];
+    set_row(rk[ra]);
+    cv = ck[rb];
+    prefetch_row();
+  }
+  // Key of candidate c, then a step to c + 1 (c < P; called for consecutive c).
+  __device__ __forceinline__ void next(int c, uint64_t* ks, uint32_t* kn) {
+    *ks = ord_f64(vr + (double)f32_from_ord((uint32_t)(cv >> 32)));
+    *kn = 0xFFFFFFFFu - (rid + (0xFFFFFFFFu - (uint32_t)cv));
+    if (c + 1 >= rend) {
+      if (ra + 1 < kr) {
+        ++ra;
+        rb = 0;
+        rend = rend_next;
+        set_row(rnext);
+        prefetch_row();
+      }
+    } else {
+      ++rb;
+    }
+    cv = ck[rb];  // in bounds also past the last candidate (rb stays below kc)
+  }
+};
+
+// Wave-aggregated append: lanes with take set store (ks, kn) at consecutive slots of
+// (dst_s, dst_n) reserved with one LDS atomic on *counter. Every lane of the wave calls it.
+__device__ __forceinline__ void wave_append(bool take, uint64_t ks, uint32_t kn, int* counter,
+                                            uint64_t* dst_s, uint32_t* dst_n, int cap) {
+  const uint64_t bal = __ballot(take);
+  if (bal == 0ull) return;
+  int base = 0;
+  if (lane_id() == 0) base = atomicAdd(counter, (int)__popcll(bal));
+  base = __builtin_amdgcn_readfirstlane(base);  // lane 0 is active: every lane calls this
+  if (take) {
+    const int pos = base + (int)__popcll(bal & lanemask_lt());
+    if (pos < cap) {
+      dst_s[pos] = ks;
+      dst_n[pos] = kn;
+    }
+  }
 }
 
-__global__ __launch_bounds__(kLargeThreads) void select_large_kernel(LargeArgs a) {
+// One radix step, run by all lanes of one wave once the histogram of the current digit is
+// complete: the largest digit whose count of keys at or above it reaches krem becomes part of
+// the threshold. Lane l reads bins 4l .. 4l + 3. Also advances the survivor-copy mode.
+__device__ __forceinline__ void pick_digit(LargeShared& sh, int pass, int mode, int k2) {
+  const int l = lane_id();
+  const int sh_s = 56 - 8 * pass;
+  const int sh_n = 24 - 8 * (pass - 8);
+  const int krem = sh.krem;
+  const uint32_t h0 = sh.hist[4 * l], h1 = sh.hist[4 * l + 1];
+  const uint32_t h2 = sh.hist[4 * l + 2], h3 = sh.hist[4 * l + 3];
+  const int mine = (int)(h0 + h1 + h2 + h3);
+  // suffix sum over lanes >= l
+  int suf = mine;
+#pragma unroll
+  for (int m = 1; m < kWave; m <<= 1) {
+    const int y = __shfl_down(suf, m, kWave);
+    if (l + m < kWave) suf += y;
+  }
+  const int above = suf - mine;  // keys in bins of higher lanes
+  const uint64_t hit = __ballot(suf >= krem && above < krem);
+  const int L = __ffsll((unsigned long long)hit) - 1;
+  if (l == L) {
+    // within the lane, from bin 4l + 3 down
+    int acc = above, dg;
+    uint32_t in_bin;
+    if (acc + (int)h3 >= krem) {
+      dg = 4 * l + 3;
+      in_bin = h3;
+    } else {
+      acc += (int)h3;
+      if (acc + (int)h2 >= krem) {
+        dg = 4 * l + 2;
+        in_bin = h2;
+      } else {
+        acc += (int)h2;
+        if (acc + (int)h1 >= krem) {
+          dg = 4 * l + 1;
+          in_bin = h1;
+        } else {
+          acc += (int)h1;
+          dg = 4 * l;
+          in_bin = h0;
+        }
+      }
+    }
+    sh.krem = krem - acc;
+    if (pass < 8) {
+      sh.ts |= (uint64_t)dg << sh_s;
+      sh.ms |= (uint64_t)0xFF << sh_s;
+    } else {
+      sh.tn |= (uint32_t)dg << sh_n;
+      sh.mn |= 0xFFu << sh_n;
+    }
+    // the copy is taken by the pass after the one whose chosen bin first fits
+    sh.mode = mode == 1 ? 2 : ((mode == 0 && (int)in_bin <= k2) ? 1 : mode);
+  }
+}
+
+// Histogram of the current digit over the survivor copy, threads tid, tid + stride, ...
+__device__ __forceinline__ void survivor_hist(LargeShared& sh, const uint64_t* sel_s,
+                                              const uint32_t* sel_n, int n, int pass, int tid,
+                                              int stride) {
+  const uint64_t ts = sh.ts, ms = sh.ms;
+  const uint32_t tn = sh.tn, mn = sh.mn;
+  const int sh_s = 56 - 8 * pass;
+  const int sh_n = 24 - 8 * (pass - 8);
+  for (int i = tid; i < n; i += stride) {
+    const uint64_t ks = sel_s[i];
+    const uint32_t kn = sel_n[i];
+    if ((ks & ms) == ts && (kn & mn) == tn) {
+      const uint32_t dg = pass < 8 ? (uint32_t)(ks >> sh_s) & 0xFFu : (kn >> sh_n) & 0xFFu;
+      atomicAdd(&sh.hist[dg], 1u);
+    }
+  }
+}
+
+// Writes the keep largest of the n distinct keys src[0, n) to dst in descending order: the
+// rank of a key is the number of larger keys. src is padded with 0 to an even length and
+// 16-byte aligned; thread t of NT ranks keys t, t + NT, ...
+template <int NT>
+__device__ __forceinline__ void rank_half(const uint64_t* src, int n, int keep, int t,
+                                          uint64_t* dst) {
+  constexpr int kStride = NT;
+  constexpr int S = kRankSortMax / kStride;
+  uint64_t key[S];
+  int rank[S];
+#pragma unroll
+  for (int s = 0; s < S; ++s) {
+    const int j = t + kStride * s;
+    key[s] = j < n ? src[j] : ~0ull;
+    rank[s] = 0;
+  }
+  const int n_even = (n + 1) & ~1;
+#pragma unroll 4
+  for (int q = 0; q < n_even; q += 2) {
+    const ulonglong2 p = *reinterpret_cast<const ulonglong2*>(src + q);
+#pragma unroll
+    for (int s = 0; s < S; ++s) rank[s] += (p.x > key[s] ? 1 : 0) + (p.y > key[s] ? 1 : 0);
+  }
+#pragma unroll
+  for (int s = 0; s < S; ++s) {
+    const int j = t + kStride * s;
+    if (j < n && rank[s] < keep) dst[rank[s]] = key[s];
+  }
+}
+
+template <int NT>
+__global__ __launch_bounds__(NT, NT == 256 ? 5 : 4) void select_large_kernel(LargeArgs a) {
+  constexpr int kLargeThreads = NT;
+  constexpr int kLargeWaves = NT / kWave;
+  static_assert(kLargeWaves <= kLargeMaxWaves, "workgroup size");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   __shared__ LargeShared sh;
   const int n2 = a.n2, k2 = a.k2, K = a.K;
@@ -417,7 +610,7 @@ __global__ __launch_bounds__(kLargeThreads) void select_large_kernel(LargeArgs a
   uint64_t* hk = (uint64_t*)smem;                 // [2][n2]: rows, then columns
   uint64_t* sel_s = hk + 2 * n2;                  // [k2]
   uint32_t* sel_n = (uint32_t*)(sel_s + k2);      // [k2]
-  uint32_t* cum = sel_n + k2;                     // [kr + 1]
+  uint32_t* cum = (uint32_t*)((unsigned char*)sel_s + large_region_bytes_dev(n2, k2));  // [kr + 1]
   const int tid = threadIdx.x, l = lane_id(), w = tid >> 6;
 
   // candidate offsets: cum[a] = sum over a' < a of min(kc, K / (a' + 1)), by a block scan
@@ -444,7 +637,7 @@ __global__ __launch_bounds__(kLargeThreads) void select_large_kernel(LargeArgs a
     __syncthreads();
   }
   const int P = (int)cum[kr];
-  const int chunk = (P + kLargeThreads - 1) / kLargeThreads;
+  const int chunk = (P + kLargeThreads - 1) / kLargeThreads;  // same on every thread
   const int c0 = tid * chunk;
   const int c1 = c0 + chunk < P ? c0 + chunk : P;
   // first row rank of this thread's chunk (binary search in cum)
@@ -460,185 +653,131 @@ __global__ __launch_bounds__(kLargeThreads) void select_large_kernel(LargeArgs a
 
   for (int64_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
     const float* hr = a.hs + row * (int64_t)(a.nr + a.nc);
-    // 1. half keys, padded with 0 (below every finite logit), both halves sorted descending
-    for (int i = tid; i < 2 * n2; i += kLargeThreads) {
-      const int h = i >= n2, j = i - h * n2;
-      const int n = h ? a.nc : a.nr;
-      hk[i] = j < n ? logit_key(ord_f32(hr[h * a.nr + j]), j) : 0ull;
-    }
-    __syncthreads();
-    for (int lk = 1; (1 << lk) <= n2; ++lk) {
-      const int k = 1 << lk;
-      for (int lj = lk - 1; lj >= 0; --lj) {
-        const int j = 1 << lj;
-        for (int t = tid; t < n2; t += kLargeThreads) {
-          const int i = ((t >> lj) << (lj + 1)) | (t & (j - 1));
-          const uint64_t x = hk[i], y = hk[i + j];
-          const bool up = (i & k & (n2 - 1)) == 0;
-          if ((x < y) == up) {
-            hk[i] = y;
-            hk[i + j] = x;
+    // 1. the top kr row keys and top kc column keys, descending
+    if (n2 <= kRankSortMax) {
+      uint64_t* stage = sel_s;  // [2][n2], unsorted, padded with 0 (below every finite logit)
+      for (int i = tid; i < 2 * n2; i += kLargeThreads) {
+        const int h = i >= n2, j = i - h * n2;
+        const int n = h ? a.nc : a.nr;
+        stage[i] = j < n ? logit_key(ord_f32(hr[h * a.nr + j]), j) : 0ull;
+      }
+      __syncthreads();
+      rank_half<NT>(stage, a.nr, kr, tid, hk);
+      rank_half<NT>(stage + n2, a.nc, kc, tid, hk + n2);
+      __syncthreads();
+    } else {
+      // keys padded with 0 (below every finite logit), both halves sorted descending
+      for (int i = tid; i < 2 * n2; i += kLargeThreads) {
+        const int h = i >= n2, j = i - h * n2;
+        const int n = h ? a.nc : a.nr;
+        hk[i] = j < n ? logit_key(ord_f32(hr[h * a.nr + j]), j) : 0ull;
+      }
+      __syncthreads();
+      for (int lk = 1; (1 << lk) <= n2; ++lk) {
+        const int k = 1 << lk;
+        for (int lj = lk - 1; lj >= 0; --lj) {
+          const int j = 1 << lj;
+          for (int t = tid; t < n2; t += kLargeThreads) {
+            const int i = ((t >> lj) << (lj + 1)) | (t & (j - 1));
+            const uint64_t x = hk[i], y = hk[i + j];
+            const bool up = (i & k & (n2 - 1)) == 0;
+            if ((x < y) == up) {
+              hk[i] = y;
+              hk[i + j] = x;
+            }
           }
+          __syncthreads();
         }
-        __syncthreads();
       }
     }
-    const uint64_t* rk = hk;
-    const uint64_t* ck = hk + n2;
-    // 3. radix select of the K-th largest candidate key, eight bits at a time from the top.
-    // The leading bytes that every candidate's score shares are taken as decided without a
-    // histogram pass: the minimum and maximum score keys bound them.
-    {
-      uint64_t lo = ~0ull, hi = 0ull;
-      int ra = a_first, rb = c0 - (c0 < P ? (int)cum[a_first] : 0);
-      int rend = c0 < P ? (int)cum[ra + 1] : 0;
-      for (int c = c0; c < c1; ++c) {
-        while (c >= rend && ra < kr - 1) {  // each row rank holds at least one candidate
-          ++ra;
-          rb = 0;
-          rend = (int)cum[ra + 1];
-        }
-        uint64_t ks;
-        uint32_t kn;
-        cand_key(rk, ck, ra, rb, a.nc, &ks, &kn);
-        ++rb;
-        lo = ks < lo ? ks : lo;
-        hi = ks > hi ? ks : hi;
-      }
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) {
-        const uint64_t olo = shfl_xor_u64(lo, m), ohi = shfl_xor_u64(hi, m);
-        lo = olo < lo ? olo : lo;
-        hi = ohi > hi ? ohi : hi;
-      }
-      if (l == 0) {
-        sh.wlo[w] = lo;
-        sh.whi[w] = hi;
-      }
-      __syncthreads();
-      if (tid == 0) {
-        uint64_t mn = sh.wlo[0], mx = sh.whi[0];
-        for (int ww = 1; ww < 4; ++ww) {
-          mn = sh.wlo[ww] < mn ? sh.wlo[ww] : mn;
-          mx = sh.whi[ww] > mx ? sh.whi[ww] : mx;
-        }
-        int common = 0;  // leading bytes shared by every score key
-        while (common < 8 && ((mn ^ mx) >> (56 - 8 * common)) == 0) ++common;
-        const uint64_t mask = common == 0 ? 0ull : (~0ull << (64 - 8 * common));
-        sh.ts = mx & mask;
-        sh.ms = mask;
-        sh.tn = 0u;
-        sh.mn = 0u;
-        sh.krem = K;
-        sh.count = 0;
-        sh.first_pass = common;
-      }
-      __syncthreads();
+    CandWalk walk;
+    walk.rk = hk;
+    walk.ck = hk + n2;
+    walk.cum = cum;
+    walk.kr = kr;
+    walk.nc = a.nc;
+    // 3. radix select of the K-th largest candidate key, eight bits at a time from the top
+    if (tid == 0) {
+      sh.ts = 0ull;
+      sh.ms = 0ull;
+      sh.tn = 0u;
+      sh.mn = 0u;
+      sh.krem = K;
+      sh.mode = 0;
+      sh.nsurv = 0;
+      sh.count = 0;
     }
-    for (int pass = sh.first_pass; pass < 12; ++pass) {
+    int pass = 0;
+    for (; pass < 12; ++pass) {
       for (int i = tid; i < 256; i += kLargeThreads) sh.hist[i] = 0u;
       __syncthreads();
       const uint64_t ts = sh.ts, ms = sh.ms;
       const uint32_t tn = sh.tn, mn = sh.mn;
+      const int mode = sh.mode;
+      const int nsurv = sh.nsurv < k2 ? sh.nsurv : k2;
+      if (mode == 2 && nsurv <= kWaveFinish) break;  // the same on every thread
       const int sh_s = 56 - 8 * pass;            // digit position in the score word (pass < 8)
       const int sh_n = 24 - 8 * (pass - 8);      // digit position in the id word (pass >= 8)
-      int ra = a_first, rb = c0 - (c0 < P ? (int)cum[a_first] : 0);
-      int rend = c0 < P ? (int)cum[ra + 1] : 0;
-      // runs of equal digits along the thread's chunk are counted before one LDS atomic, so
-      // bins that nearly every candidate hits are not serialised over all of them
-      uint32_t run_dg = 0u, run_n = 0u;
-      for (int c = c0; c < c1; ++c) {
-        while (c >= rend && ra < kr - 1) {  // each row rank holds at least one candidate
-          ++ra;
-          rb = 0;
-          rend = (int)cum[ra + 1];
-        }
-        uint64_t ks;
-        uint32_t kn;
-        cand_key(rk, ck, ra, rb, a.nc, &ks, &kn);
-        ++rb;
-        if ((ks & ms) == ts && (kn & mn) == tn) {
-          const uint32_t dg = pass < 8 ? (uint32_t)(ks >> sh_s) & 0xFFu : (kn >> sh_n) & 0xFFu;
-          if (run_n != 0u && dg != run_dg) {
-            atomicAdd(&sh.hist[run_dg], run_n);
-            run_n = 0u;
-          }
-          run_dg = dg;
-          ++run_n;
-        }
-      }
-      if (run_n != 0u) atomicAdd(&sh.hist[run_dg], run_n);
-      __syncthreads();
-      if (w == 0) {
-        // largest digit whose suffix count reaches krem: lane l holds bins 4l .. 4l + 3
-        const int krem = sh.krem;
-        const uint32_t h0 = sh.hist[4 * l], h1 = sh.hist[4 * l + 1];
-        const uint32_t h2 = sh.hist[4 * l + 2], h3 = sh.hist[4 * l + 3];
-        const int mine = (int)(h0 + h1 + h2 + h3);
-        // suffix sum over lanes >= l
-        int suf = mine;
-#pragma unroll
-        for (int m = 1; m < kWave; m <<= 1) {
-          const int y = __shfl_down(suf, m, kWave);
-          if (l + m < kWave) suf += y;
-        }
-        const int above = suf - mine;  // keys in bins of higher lanes
-        const uint64_t hit = __ballot(suf >= krem && above < krem);
-        const int L = __ffsll((unsigned long long)hit) - 1;
-        if (l == L) {
-          // within the lane, from bin 4l + 3 down
-          int acc = above, dg;
-          if (acc + (int)h3 >= krem) {
-            dg = 4 * l + 3;
-          } else {
-            acc += (int)h3;
-            if (acc + (int)h2 >= krem) {
-              dg = 4 * l + 2;
-            } else {
-              acc += (int)h2;
-              if (acc + (int)h1 >= krem) {
-                dg = 4 * l + 1;
-              } else {
-                acc += (int)h1;
-                dg = 4 * l;
-              }
+      if (mode == 2) {
+        survivor_hist(sh, sel_s, sel_n, nsurv, pass, tid, kLargeThreads);
+      } else {
+        // runs of equal digits along the chunk are counted before one LDS atomic, so bins that
+        // nearly every candidate hits are not serialised over all of them
+        uint32_t run_dg = 0u, run_n = 0u;
+        if (c0 < P) walk.start(a_first, c0);
+        for (int it = 0; it < chunk; ++it) {
+          const int c = c0 + it;
+          const bool live = c < c1;
+          uint64_t ks = 0ull;
+          uint32_t kn = 0u;
+          if (live) walk.next(c, &ks, &kn);
+          const bool match = live && (ks & ms) == ts && (kn & mn) == tn;
+          if (match) {
+            const uint32_t dg = pass < 8 ? (uint32_t)(ks >> sh_s) & 0xFFu : (kn >> sh_n) & 0xFFu;
+            if (run_n != 0u && dg != run_dg) {
+              atomicAdd(&sh.hist[run_dg], run_n);
+              run_n = 0u;
             }
+            run_dg = dg;
+            ++run_n;
           }
-          sh.krem = krem - acc;
-          if (pass < 8) {
-            sh.ts |= (uint64_t)dg << sh_s;
-            sh.ms |= (uint64_t)0xFF << sh_s;
-          } else {
-            sh.tn |= (uint32_t)dg << sh_n;
-            sh.mn |= 0xFFu << sh_n;
-          }
+          if (mode == 1) wave_append(match, ks, kn, &sh.nsurv, sel_s, sel_n, k2);
+        }
+        if (run_n != 0u) atomicAdd(&sh.hist[run_dg], run_n);
+      }
+      __syncthreads();
+      if (w == 0) pick_digit(sh, pass, mode, k2);
+      __syncthreads();
+    }
+    if (pass < 12) {
+      // a short survivor copy: wave 0 alone takes the remaining digits, with no workgroup
+      // barriers between them
+      if (w == 0) {
+        const int nsurv = sh.nsurv < k2 ? sh.nsurv : k2;
+        for (; pass < 12; ++pass) {
+          for (int i = l; i < 256; i += kWave) sh.hist[i] = 0u;
+          wave_lds_sync();
+          survivor_hist(sh, sel_s, sel_n, nsurv, pass, l, kWave);
+          wave_lds_sync();
+          pick_digit(sh, pass, 2, k2);
+          wave_lds_sync();
         }
       }
       __syncthreads();
     }
-    // the threshold key is exact now; gather the K keys at or above it
+    // 4. the threshold key is exact now; gather the K keys at or above it
     {
       const uint64_t ts = sh.ts;
       const uint32_t tn = sh.tn;
-      int ra = a_first, rb = c0 - (c0 < P ? (int)cum[a_first] : 0);
-      int rend = c0 < P ? (int)cum[ra + 1] : 0;
-      for (int c = c0; c < c1; ++c) {
-        while (c >= rend && ra < kr - 1) {  // each row rank holds at least one candidate
-          ++ra;
-          rb = 0;
-          rend = (int)cum[ra + 1];
-        }
-        uint64_t ks;
-        uint32_t kn;
-        cand_key(rk, ck, ra, rb, a.nc, &ks, &kn);
-        ++rb;
-        if (ks > ts || (ks == ts && kn >= tn)) {
-          const int pos = atomicAdd(&sh.count, 1);
-          if (pos < k2) {
-            sel_s[pos] = ks;
-            sel_n[pos] = kn;
-          }
-        }
+      if (c0 < P) walk.start(a_first, c0);
+      for (int it = 0; it < chunk; ++it) {
+        const int c = c0 + it;
+        const bool live = c < c1;
+        uint64_t ks = 0ull;
+        uint32_t kn = 0u;
+        if (live) walk.next(c, &ks, &kn);
+        const bool take = live && (ks > ts || (ks == ts && kn >= tn));
+        wave_append(take, ks, kn, &sh.count, sel_s, sel_n, k2);
       }
       for (int i = K + tid; i < k2; i += kLargeThreads) {
         sel_s[i] = 0ull;
@@ -667,7 +806,7 @@ __global__ __launch_bounds__(kLargeThreads) void select_large_kernel(LargeArgs a
         __syncthreads();
       }
     }
-    // 4. gates: e_k = exp(S_k - S_0), summed per thread over a contiguous range, then across
+    // 5. gates: e_k = exp(S_k - S_0), summed per thread over a contiguous range, then across
     // lanes and waves in a fixed order
     const double s0 = f64_from_ord(sel_s[0]);
     const int per = (K + kLargeThreads - 1) / kLargeThreads;
@@ -678,7 +817,9 @@ __global__ __launch_bounds__(kLargeThreads) void select_large_kernel(LargeArgs a
     part = wave_sum_f32(part);
     if (l == 0) sh.wsum[w] = part;
     __syncthreads();
-    const float z = (sh.wsum[0] + sh.wsum[1]) + (sh.wsum[2] + sh.wsum[3]);
+    float z = sh.wsum[0];
+#pragma unroll
+    for (int ww = 1; ww < kLargeWaves; ++ww) z += sh.wsum[ww];
     for (int q = tid; q < K; q += kLargeThreads) {
       a.idx[row * K + q] = (int32_t)(0xFFFFFFFFu - sel_n[q]);
       a.gates[row * K + q] = expf((float)(f64_from_ord(sel_s[q]) - s0)) / z;
@@ -796,7 +937,12 @@ hipError_t launch_select(const Shape& s, const float* half_scores, int32_t* idx,
     const int kr = s.K < s.nr ? s.K : s.nr;
     const size_t lds = large_lds_bytes(n2, k2, kr);
     const dim3 grid((unsigned)(s.rows < 4096 ? s.rows : 4096));
-    hipLaunchKernelGGL(select_large_kernel, grid, dim3(kLargeThreads), lds, st, a);
+    // eight waves per row once the final sort has 2048 keys or more; four below, where more
+    // rows share a compute unit
+    if (k2 >= 2048)
+      hipLaunchKernelGGL(select_large_kernel<512>, grid, dim3(512), lds, st, a);
+    else
+      hipLaunchKernelGGL(select_large_kernel<256>, grid, dim3(256), lds, st, a);
     return hipGetLastError();
   }
   SelectArgs a;
