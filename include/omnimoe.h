@@ -73,7 +73,10 @@ typedef enum { OMNIMOE_QUERY_SPLIT = 0, OMNIMOE_QUERY_SHARED = 1 } omnimoe_query
  *   query_mode  OMNIMOE_QUERY_SPLIT or OMNIMOE_QUERY_SHARED.
  *   group_size  B of Sec. 2.3, B >= 1: active experts per execution group. The schedule
  *               orders tasks by (group, task id) (Eq. 13); B = 1 gives (expert, task id).
- *               The layer's output does not depend on B.
+ *               With B > 1 the layer computes the expert activations group by group as
+ *               dense tiles on the matrix cores (Eq. 14, omnimoe_expert_forward_grouped)
+ *               when dtype is bf16 and d % 64 == 0; its output then matches B = 1 to fp32
+ *               rounding. Otherwise the output does not depend on B.
  * T * H * K and T * H * (n_rows + n_cols) must each be below 2^31. */
 typedef struct {
   int64_t T;
@@ -98,7 +101,8 @@ typedef enum {
   OMNIMOE_STAGE_LAYER = 4,
   OMNIMOE_STAGE_ROUTE_DENSE = 5,    /* omnimoe_route_dense without a logits buffer */
   OMNIMOE_STAGE_EXPERT_BACKWARD = 6, /* omnimoe_expert_backward */
-  OMNIMOE_STAGE_ROUTE_BACKWARD = 7   /* omnimoe_route_backward */
+  OMNIMOE_STAGE_ROUTE_BACKWARD = 7,  /* omnimoe_route_backward */
+  OMNIMOE_STAGE_EXPERT_GROUPED = 8   /* omnimoe_expert_forward_grouped */
 } omnimoe_stage;
 
 /* Bytes of workspace the given stage's entry point needs for this shape. */
@@ -169,6 +173,27 @@ omnimoe_status omnimoe_expert_forward(const omnimoe_layer_desc* desc, const void
                                       const float* gates, const int32_t* perm, float* y,
                                       void* workspace, size_t workspace_bytes, void* stream);
 
+/* Expert compute by groups of B active experts (Sec. 2.3, Eq. 13-14), desc->group_size = B:
+ * for each group q, the activations G_q (.) act(X_q W_q^T) are computed as dense tiles on the
+ * matrix cores, X_q being the distinct tokens of the group's tasks and W_q the u rows of its
+ * experts, and only the entries that are tasks are kept, a[p] = g_p act(x_t . u_e); then
+ * every token sums a[p] v_e over its slots in (head, k) order, as in omnimoe_expert_forward.
+ * No atomics: y is the same on every run. It pays where the experts of a group share
+ * tokens (many tasks per expert), and B = 1 is allowed but wastes the matrix cores.
+ *   perm [M], active [min(M, N)], n_active [1] (device): omnimoe_schedule's outputs for the
+ *   same desc (so the same group_size); group q holds the experts active[q B .. q B + B - 1],
+ *   and perm lists its tasks in task order.
+ * bf16 with d % 64 == 0, else OMNIMOE_ERR_UNSUPPORTED. omnimoe_layer_forward takes this path
+ * whenever group_size > 1 and these hold. Results agree with omnimoe_expert_forward to fp32
+ * rounding (the dot products are summed in another order). Workspace:
+ * OMNIMOE_STAGE_EXPERT_GROUPED bytes. Pointers 16-byte aligned; T = 0 is a no-op. */
+omnimoe_status omnimoe_expert_forward_grouped(const omnimoe_layer_desc* desc, const void* x,
+                                              const void* u, const void* v, const int32_t* idx,
+                                              const float* gates, const int32_t* perm,
+                                              const int32_t* active, const int32_t* n_active,
+                                              float* y, void* workspace, size_t workspace_bytes,
+                                              void* stream);
+
 /* Expert compute without the schedule, token by token: the ablation of Expert-Centric
  * Scheduling (Sec. 3.3, Table 3, "w/o Expert-Centric Scheduling"), for measuring what the
  * schedule buys. Same arguments and result as omnimoe_expert_forward (bit for bit from 1024
@@ -225,7 +250,9 @@ omnimoe_status omnimoe_route_backward(const omnimoe_layer_desc* desc, const void
                                       size_t workspace_bytes, void* stream);
 
 /* The whole routed layer: route, schedule and expert compute on one stream, no host
- * synchronisation. y [T, d] fp32 out; idx_out and gates_out ([T, H, K]) may be NULL. */
+ * synchronisation. y [T, d] fp32 out; idx_out and gates_out ([T, H, K]) may be NULL. The
+ * expert compute is omnimoe_expert_forward's, or omnimoe_expert_forward_grouped's when
+ * group_size > 1, dtype is bf16 and d % 64 == 0. */
 omnimoe_status omnimoe_layer_forward(const omnimoe_layer_desc* desc, const void* x,
                                      const void* keys_row, const void* keys_col, const void* u,
                                      const void* v, float* y, int32_t* idx_out, float* gates_out,

@@ -82,6 +82,17 @@ size_t m_bytes(const Shape& s) { return align_up((size_t)s.M * 4); }
 size_t dense_bytes(const Shape& s) { return align_up((size_t)s.rows * (size_t)s.N * 4); }
 size_t active_bytes(const Shape& s) { return align_up((size_t)(std::min(s.M, s.N) + 1) * 4); }
 
+// The grouped expert GEMM (Eq. 14) runs for bf16 with d a multiple of 64; the layer takes it
+// when the schedule's groups hold more than one expert.
+bool grouped_supported(const Shape& s) { return s.bf16 && s.d % 64 == 0; }
+bool layer_grouped(const Shape& s) { return s.B > 1 && grouped_supported(s); }
+
+// Schedule workspace, followed by the grouped plan's (which reads the schedule's sorted keys).
+size_t sched_or_plan_bytes(const Shape& s) {
+  const size_t sb = omnimoe::schedule_ws_bytes(s.M, s.N);
+  return layer_grouped(s) ? sb + omnimoe::group_plan_ws_bytes(s) : sb;
+}
+
 size_t stage_bytes(const Shape& s, int stage) {
   switch (stage) {
     case OMNIMOE_STAGE_ROUTE: return hs_bytes(s);
@@ -91,11 +102,12 @@ size_t stage_bytes(const Shape& s, int stage) {
     case OMNIMOE_STAGE_ROUTE_DENSE: return dense_bytes(s);
     case OMNIMOE_STAGE_EXPERT_BACKWARD: return omnimoe::backward_ws_bytes(s.M);
     case OMNIMOE_STAGE_ROUTE_BACKWARD: return omnimoe::route_backward_ws_bytes(s);
+    case OMNIMOE_STAGE_EXPERT_GROUPED: return m_bytes(s) + omnimoe::group_plan_ws_bytes(s);
     default: {
       // idx, gates, perm, active, active_offsets, n_active, then the logits (dead after
       // selection) overlapped with the sort buffers and the a[] buffer.
       size_t fixed = 3 * m_bytes(s) + 2 * active_bytes(s) + 256;
-      size_t late = omnimoe::schedule_ws_bytes(s.M, s.N) + m_bytes(s);
+      size_t late = sched_or_plan_bytes(s) + m_bytes(s);
       return fixed + std::max(hs_bytes(s), late);
     }
   }
@@ -136,7 +148,7 @@ omnimoe_status layer_impl(const omnimoe_layer_desc* desc, const void* x, const v
   char* late = w;
   float* hs = (float*)late;
   void* sched_ws = late;
-  float* abuf = (float*)(late + omnimoe::schedule_ws_bytes(s.M, s.N));
+  float* abuf = (float*)(late + sched_or_plan_bytes(s));
   if (idx_out) idx = idx_out;
   if (gates_out) gates = gates_out;
 
@@ -151,12 +163,23 @@ omnimoe_status layer_impl(const omnimoe_layer_desc* desc, const void* x, const v
   if ((e = omnimoe::launch_select(s, hs, idx, gates, strm))) return hip_status(e);
   mark(2);
   const int32_t* sk = nullptr;
+  const int32_t* gk = nullptr;
   if ((e = omnimoe::launch_schedule(s, idx, perm, active, offsets, n_active, nullptr, sched_ws,
-                                    &sk, strm)))
+                                    &sk, strm, &gk)))
     return hip_status(e);
   mark(3);
-  if ((e = omnimoe::launch_expert_dot(s, x, u, idx, gates, perm, sk, abuf, strm)))
+  if (layer_grouped(s)) {
+    omnimoe::GroupPlan plan;
+    void* plan_ws = (char*)sched_ws + omnimoe::schedule_ws_bytes(s.M, s.N);
+    if ((e = omnimoe::launch_group_plan(s, perm, n_active, gk, idx, active, plan_ws, &plan,
+                                        strm)))
+      return hip_status(e);
+    if ((e = omnimoe::launch_grouped_dot(s, x, u, gates, perm, active, n_active, plan, abuf,
+                                         strm)))
+      return hip_status(e);
+  } else if ((e = omnimoe::launch_expert_dot(s, x, u, idx, gates, perm, sk, abuf, strm))) {
     return hip_status(e);
+  }
   mark(4);
   if ((e = omnimoe::launch_accumulate(s, v, idx, abuf, y, strm))) return hip_status(e);
   mark(5);
@@ -183,7 +206,7 @@ const char* omnimoe_status_string(int32_t status) {
 omnimoe_status omnimoe_workspace_size(const omnimoe_layer_desc* desc, int32_t stage,
                                       size_t* bytes) {
   if (!bytes) return OMNIMOE_ERR_INVALID_ARG;
-  if (stage < OMNIMOE_STAGE_ROUTE || stage > OMNIMOE_STAGE_ROUTE_BACKWARD)
+  if (stage < OMNIMOE_STAGE_ROUTE || stage > OMNIMOE_STAGE_EXPERT_GROUPED)
     return OMNIMOE_ERR_INVALID_ARG;
   Shape s;
   omnimoe_status st = check_desc(desc, &s);
@@ -359,6 +382,30 @@ omnimoe_status omnimoe_expert_forward(const omnimoe_layer_desc* desc, const void
   hipStream_t strm = (hipStream_t)stream;
   float* abuf = (float*)ws;
   hipError_t e = omnimoe::launch_expert_dot(s, x, u, idx, gates, perm, nullptr, abuf, strm);
+  if (e == hipSuccess) e = omnimoe::launch_accumulate(s, v, idx, abuf, y, strm);
+  return hip_status(e);
+}
+
+omnimoe_status omnimoe_expert_forward_grouped(const omnimoe_layer_desc* desc, const void* x,
+                                              const void* u, const void* v, const int32_t* idx,
+                                              const float* gates, const int32_t* perm,
+                                              const int32_t* active, const int32_t* n_active,
+                                              float* y, void* ws, size_t ws_bytes,
+                                              void* stream) {
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  if (s.T == 0) return OMNIMOE_OK;
+  if ((st = check_ptrs({x, u, v, idx, gates, perm, active, n_active, y, ws}))) return st;
+  if (!grouped_supported(s)) return OMNIMOE_ERR_UNSUPPORTED;
+  if (ws_bytes < stage_bytes(s, OMNIMOE_STAGE_EXPERT_GROUPED)) return OMNIMOE_ERR_WORKSPACE;
+  hipStream_t strm = (hipStream_t)stream;
+  float* abuf = (float*)ws;
+  omnimoe::GroupPlan plan;
+  hipError_t e = omnimoe::launch_group_plan(s, perm, n_active, nullptr, idx, active,
+                                            (char*)ws + m_bytes(s), &plan, strm);
+  if (e == hipSuccess)
+    e = omnimoe::launch_grouped_dot(s, x, u, gates, perm, active, n_active, plan, abuf, strm);
   if (e == hipSuccess) e = omnimoe::launch_accumulate(s, v, idx, abuf, y, strm);
   return hip_status(e);
 }

@@ -1,0 +1,254 @@
+// Grouped expert GEMM of Eq. 14 for a schedule with groups of B > 1 active experts: the
+// activations G_q (.) act(X_q W_q^T) of group q are formed as dense tiles on MFMA, X_q being
+// the group's distinct tokens (its slots) and W_q the u rows of its experts. Only the entries
+// that are tasks are kept: a[p] = g_p * act(x_t . u_e) for every task p of the group.
+//
+// Work tile: 256 slots x 64 experts of one group per workgroup of four waves (each wave 64
+// slots x 64 experts, four 32 x 32 accumulators of v_mfma_f32_32x32x16_bf16). k steps of 64
+// go through two LDS stages filled straight from global memory with global_load_lds_dwordx4:
+// every lane supplies its own row address, so the token rows (x at the slots' tokens) and the
+// expert rows (u at the group's experts) are gathered on the way into LDS. LDS rows are 128 B;
+// chunk j of row r sits at position j ^ ((r >> 1) & 7), so the 16 rows read by one operand
+// load fall in distinct banks. bf16 products are exact and accumulate in fp32, as in the
+// per-task kernel.
+//
+// Epilogue: the 256 x 64 fp32 tile goes to LDS (over the stages), and the workgroup walks the
+// tasks of the tile's slots (one contiguous run of sorted positions) 256 at a time; those whose
+// expert lies in the tile (its place in the group, from the schedule's packed key) read their
+// entry (slot row from the plan) and write a[p].
+//
+// Tiles are numbered group by group (slot tiles major, expert tiles fastest), so consecutive
+// tiles share their token rows and the group's u rows stay in the XCD's L2; each XCD takes one
+// contiguous range of tiles and each workgroup a contiguous run inside it, so the group search
+// is done once per workgroup and then advances.
+#include "device_common.hpp"
+#include "internal.hpp"
+
+namespace omnimoe {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+constexpr int kThreads = 256;
+constexpr int kK = 64;                                         // k per stage
+constexpr int kRow = kK * 2;                                   // bytes per LDS row
+constexpr int kStage = (kGroupSlots + kGroupExperts) * kRow;   // 40 KiB
+constexpr int kHStride = kGroupExperts + 1;                    // floats per epilogue row
+static_assert(kGroupSlots == 4 * 64 && kGroupExperts == 64, "four waves of 64 x 64");
+static_assert(kGroupSlots * kHStride * 4 <= 2 * kStage, "the epilogue tile fits the stages");
+
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
+__device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+
+struct GroupedDotArgs {
+  const uint16_t* x;
+  const uint16_t* u;
+  const float* gates;
+  const int32_t* perm;
+  const int32_t* active;
+  const int32_t* n_active;
+  const int32_t* key;
+  const int32_t* slot_token;
+  const int32_t* slot_off;
+  const int32_t* pos_slot;
+  const int32_t* grp_slot;
+  const int32_t* grp_tile;
+  const int32_t* counters;
+  float* a;
+  int64_t M, N, G;
+  int d, B, act, gbits;
+};
+
+__device__ __forceinline__ int32_t clamp_i32(int32_t v, int64_t n) {
+  return v < 0 ? 0 : (v >= n ? (int32_t)(n - 1) : v);
+}
+
+__global__ __launch_bounds__(kThreads, 2) void grouped_dot_kernel(GroupedDotArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
+  const int n_act = *a.n_active;
+  int64_t ng = ((int64_t)n_act + a.B - 1) / a.B;
+  if (ng > a.G) ng = a.G;
+  const int total = a.counters[1];
+  if (ng <= 0 || total <= 0) return;
+  // each XCD a contiguous range of tiles, each workgroup a contiguous run inside it
+  constexpr int kXcds = 8;
+  const int xcd = blockIdx.x % kXcds;
+  const int blocks_per_xcd = gridDim.x / kXcds;
+  const int per_xcd = (total + kXcds - 1) / kXcds;
+  const int x_lo = xcd * per_xcd;
+  const int x_hi = min(total, x_lo + per_xcd);
+  const int per_block = (per_xcd + blocks_per_xcd - 1) / blocks_per_xcd;
+  const int t_lo = x_lo + (blockIdx.x / kXcds) * per_block;
+  const int t_hi = min(x_hi, t_lo + per_block);
+  if (t_lo >= t_hi) return;
+  // group of the first tile: the last q < ng with grp_tile[q] <= t_lo
+  int q;
+  {
+    int lo = 0, hi = (int)ng - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (a.grp_tile[mid] <= t_lo) lo = mid; else hi = mid - 1;
+    }
+    q = lo;
+  }
+  const int frow = l & 31;
+  const int fk = l >> 5;  // 16-byte chunk within a 16-wide k step
+  const int sw = swz(frow);
+  const int KT = a.d / kK;
+  for (int tile = t_lo; tile < t_hi; ++tile) {
+    while (q + 1 < ng && a.grp_tile[q + 1] <= tile) ++q;
+    const int s_q = a.grp_slot[q];
+    const int tq = a.grp_slot[q + 1] - s_q;
+    const int e_q = q * a.B;
+    const int bq = min(a.B, n_act - e_q);
+    const int n_et = (bq + kGroupExperts - 1) / kGroupExperts;
+    const int local = tile - a.grp_tile[q];
+    const int stl = local / n_et, et = local - stl * n_et;
+    const int s0 = s_q + stl * kGroupSlots;
+    const int ns = min(kGroupSlots, tq - stl * kGroupSlots);
+    const int r0 = e_q + et * kGroupExperts;
+    const int ne = min(kGroupExperts, bq - et * kGroupExperts);
+    // Loader: instruction i of wave w fills 8 LDS rows; lane l writes position l % 8 of row
+    // l / 8 of them, i.e. global chunk (l % 8) ^ swz(row). Rows past the tile's slots or
+    // experts load the tile's first row (never read back).
+    const uint16_t* ga[8];
+    const uint16_t* gb[2];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int r = (w * 8 + i) * 8 + (l >> 3);
+      const int j = (l & 7) ^ swz(r);
+      const int32_t tok = a.slot_token[s0 + (r < ns ? r : 0)];
+      ga[i] = a.x + (int64_t)tok * a.d + j * 8;
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int r = (w * 2 + i) * 8 + (l >> 3);
+      const int j = (l & 7) ^ swz(r);
+      const int32_t e = clamp_i32(a.active[r0 + (r < ne ? r : 0)], a.N);
+      gb[i] = a.u + (int64_t)e * a.d + j * 8;
+    }
+    auto issue = [&](int stage, int k0) {
+      unsigned char* base = smem + stage * kStage;
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        __builtin_amdgcn_global_load_lds((const void*)(ga[i] + k0),
+                                         (lds_ptr_t)(base + (w * 8 + i) * 8 * kRow), 16, 0, 0);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        __builtin_amdgcn_global_load_lds(
+            (const void*)(gb[i] + k0),
+            (lds_ptr_t)(base + kGroupSlots * kRow + (w * 2 + i) * 8 * kRow), 16, 0, 0);
+    };
+    int a_off[2], b_off[2];  // LDS row offsets of this lane's operand rows
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      a_off[i] = (w * 64 + i * 32 + frow) * kRow;
+      b_off[i] = kGroupSlots * kRow + (i * 32 + frow) * kRow;
+    }
+    auto frag = [&](const unsigned char* st, int off, int ks) -> bf16x8 {
+      return *(const bf16x8*)(st + off + (((ks * 2 + fk) ^ sw) << 4));
+    };
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    issue(0, 0);
+    wait_vm0();
+    __syncthreads();
+    for (int kt = 0; kt < KT; ++kt) {
+      const int cur = kt & 1;
+      if (kt + 1 < KT) issue(cur ^ 1, (kt + 1) * kK);
+      const unsigned char* st = smem + cur * kStage;
+      bf16x8 fa[2][2], fb[2][2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        fa[0][i] = frag(st, a_off[i], 0);
+        fb[0][i] = frag(st, b_off[i], 0);
+      }
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const int c = ks & 1;
+        if (ks + 1 < 4) {
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            fa[c ^ 1][i] = frag(st, a_off[i], ks + 1);
+            fb[c ^ 1][i] = frag(st, b_off[i], ks + 1);
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[c][i], fb[c][j], acc[i][j],
+                                                                0, 0, 0);
+      }
+      wait_vm0();
+      __syncthreads();
+    }
+    // accumulator element r of block (i, j) of wave w: slot row 64 w + 32 i + 8 (r / 4) +
+    // 4 (l / 32) + r % 4, expert column 32 j + l % 32
+    float* H = (float*)smem;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          H[(w * 64 + i * 32 + (r >> 2) * 8 + (l >> 5) * 4 + (r & 3)) * kHStride + j * 32 +
+            (l & 31)] = acc[i][j][r];
+    __syncthreads();
+    const int p_lo = a.slot_off[s0], p_hi = a.slot_off[s0 + ns];
+    const int c0 = et * kGroupExperts;
+    for (int pos = p_lo + tid; pos < p_hi; pos += kThreads) {
+      const int c = (int)((uint32_t)a.key[pos] >> a.gbits) - c0;
+      const int r = a.pos_slot[pos] - s0;
+      if (c >= 0 && c < ne && r >= 0 && r < ns) {
+        const int32_t p = clamp_i32(a.perm[pos], a.M);
+        a.a[p] = a.gates[p] * activation(a.act, H[r * kHStride + c]);
+      }
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace
+
+hipError_t launch_grouped_dot(const Shape& s, const void* x, const void* u, const float* gates,
+                              const int32_t* perm, const int32_t* active,
+                              const int32_t* n_active, const GroupPlan& plan, float* a,
+                              hipStream_t st) {
+  if (s.M == 0) return hipSuccess;
+  GroupedDotArgs g;
+  g.x = (const uint16_t*)x;
+  g.u = (const uint16_t*)u;
+  g.gates = gates;
+  g.perm = perm;
+  g.active = active;
+  g.n_active = n_active;
+  g.slot_token = plan.slot_token;
+  g.slot_off = plan.slot_off;
+  g.key = plan.key;
+  g.pos_slot = plan.pos_slot;
+  g.gbits = plan.gbits;
+  g.grp_slot = plan.grp_slot;
+  g.grp_tile = plan.grp_tile;
+  g.counters = plan.counters;
+  g.a = a;
+  g.M = s.M;
+  g.N = s.N;
+  g.G = plan.G;
+  g.d = s.d;
+  g.B = s.B;
+  g.act = s.act;
+  // persistent: a multiple of eight workgroups, two per compute unit
+  hipLaunchKernelGGL(grouped_dot_kernel, dim3(512), dim3(kThreads), 2 * kStage, st, g);
+  return hipGetLastError();
+}
+
+}  // namespace omnimoe

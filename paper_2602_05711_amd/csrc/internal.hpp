@@ -46,11 +46,15 @@ hipError_t launch_select_dense(int64_t rows, int64_t n, int K, const float* logi
 
 // Radix-sort schedule. Workspace needs schedule_ws_bytes(M, N) bytes. On return sorted_keys
 // points into the workspace (expert id of each sorted position), or is NULL when the groups
-// hold more than one expert (then the expert of position i is idx[perm[i]]).
+// hold more than one expert (then the expert of position i is idx[perm[i]]); with groups,
+// *group_keys (if asked for) points to each sorted position's packed key
+// (place of the expert in its group) << group_key_bits(s) | group.
 size_t schedule_ws_bytes(int64_t M, int64_t N);
+int group_key_bits(const Shape& s);
 hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, int32_t* active,
                            int32_t* active_offsets, int32_t* n_active, int32_t* dense_offsets,
-                           void* ws, const int32_t** sorted_keys, hipStream_t st);
+                           void* ws, const int32_t** sorted_keys, hipStream_t st,
+                           const int32_t** group_keys = nullptr);
 
 // a[p] = g_p * act(x_t . u_e) over the expert-major order given by perm (sorted_keys may be
 // NULL: the kernel then reads idx[perm[pos]]).
@@ -82,6 +86,37 @@ hipError_t launch_route_backward(const Shape& s, const void* x, const void* keys
                                  const void* keys_col, const int32_t* idx, const float* dscores,
                                  float* dx, float* dkeys_row, float* dkeys_col, void* ws,
                                  hipStream_t st);
+
+// Plan of the grouped expert GEMM (Eq. 14) over a schedule whose groups hold B > 1 active
+// experts (tasks in (group, task id) order). A slot is a (group, token) pair; slots are numbered
+// group by group, tokens ascending. Work tiles are 256 slots x 64 experts of one group.
+constexpr int kGroupSlots = 256;
+constexpr int kGroupExperts = 64;
+struct GroupPlan {
+  const int32_t* key;   // [M]     packed key of sorted position i: place << gbits | group
+  int gbits;
+  int32_t* slot_token;  // [M]     token of slot s
+  int32_t* slot_off;    // [M + 1] first sorted position of slot s (slot_off[slots] = M)
+  int32_t* pos_slot;    // [M]     slot of sorted position i
+  int32_t* grp_slot;    // [G + 1] first slot of group q
+  int32_t* grp_tile;    // [G + 1] first work tile of group q
+  int32_t* counters;    // [0] slots, [1] work tiles
+  int64_t G;            // upper bound on the number of groups: ceil(min(M, N) / B)
+};
+// sorted_group_keys: the schedule's packed keys, or NULL to derive them from perm, idx and
+// active (a caller's schedule).
+size_t group_plan_ws_bytes(const Shape& s);
+hipError_t launch_group_plan(const Shape& s, const int32_t* perm, const int32_t* n_active,
+                             const int32_t* sorted_group_keys, const int32_t* idx,
+                             const int32_t* active, void* ws, GroupPlan* plan, hipStream_t st);
+
+// a[p] = g_p * act(x_t . u_e) by groups: per work tile, the 256 x 64 block of
+// X_q U_q^T over the tile's slots (token rows) and experts on MFMA, then each task of the
+// tile's slots whose expert lies in the tile reads its entry. bf16, d % 64 == 0.
+hipError_t launch_grouped_dot(const Shape& s, const void* x, const void* u, const float* gates,
+                              const int32_t* perm, const int32_t* active,
+                              const int32_t* n_active, const GroupPlan& plan, float* a,
+                              hipStream_t st);
 
 // y[t] = sum over slots (h, k) in order of a[p] * v[idx[p]].
 hipError_t launch_accumulate(const Shape& s, const void* v, const int32_t* idx, const float* a,

@@ -281,16 +281,134 @@ __global__ __launch_bounds__(kThreads) void rank_fill_kernel(const int32_t* acti
   if (e >= 0 && e < n_experts) rank[e] = (int32_t)a;
 }
 
-// Group key of every task: q[p] = rank[idx[p]] / B.
+// Group key of every task, with the expert's place inside its group packed above it:
+// key[p] = (r % B) << gb | r / B for r = rank[idx[p]]. The sort reads only the low gb bits,
+// so the place rides along to the sorted order.
 __global__ __launch_bounds__(kThreads) void group_key_kernel(const int32_t* idx,
-                                                            const int32_t* rank, int32_t* q,
-                                                            int64_t m, int64_t n_experts, int b) {
+                                                            const int32_t* rank, int32_t* key,
+                                                            int64_t m, int64_t n_experts, int b,
+                                                            int gb) {
   const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (p >= m) return;
   int32_t e = idx[p];
   e = e < 0 ? 0 : (e >= n_experts ? (int32_t)(n_experts - 1) : e);
-  q[p] = rank[e] / b;
+  const int32_t r = rank[e];
+  key[p] = ((r % b) << gb) | (r / b);
 }
+
+// The same key for each sorted position of a caller's schedule: key[i] of task perm[i].
+__global__ __launch_bounds__(kThreads) void position_key_kernel(const int32_t* perm,
+                                                               const int32_t* idx,
+                                                               const int32_t* rank, int32_t* key,
+                                                               int64_t m, int64_t n_experts,
+                                                               int b, int gb) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i >= m) return;
+  int32_t p = perm[i];
+  p = p < 0 ? 0 : (p >= m ? (int32_t)(m - 1) : p);
+  int32_t e = idx[p];
+  e = e < 0 ? 0 : (e >= n_experts ? (int32_t)(n_experts - 1) : e);
+  const int32_t r = rank[e];
+  key[i] = ((r % b) << gb) | (r / b);
+}
+
+// ------------------------------------------------------------------ grouped-GEMM plan
+// For a schedule with groups of B > 1 experts (tasks in (group, task id) order), a slot is a
+// (group, token) pair: the tasks of one token inside one group, contiguous in perm since a
+// group's tasks are in task-id (so token) order. Slots are numbered group by group.
+
+__device__ __forceinline__ int32_t clamp_task(int32_t p, int64_t m) {
+  return p < 0 ? 0 : (p >= m ? (int32_t)(m - 1) : p);
+}
+
+// Division by the runtime constant H K without a divide: q = (umulhi(m, n) + n) >> l with
+// l = ceil(log2 d) and m = floor(2^32 (2^l - d) / d) + 1 (Granlund and Montgomery), exact for
+// 0 <= n < 2^31.
+struct DivMagic {
+  uint32_t m;
+  int l;
+};
+DivMagic div_magic(uint32_t d) {
+  int l = 0;
+  while (((uint64_t)1 << l) < d) ++l;
+  const uint64_t m = (((uint64_t)1 << 32) * (((uint64_t)1 << l) - d)) / d + 1;
+  return DivMagic{(uint32_t)m, l};
+}
+__device__ __forceinline__ uint32_t div_by(uint32_t n, DivMagic g) {
+  return (__umulhi(g.m, n) + n) >> g.l;
+}
+
+struct SlotHead {  // 1 where sorted position i starts a new (group, token) slot
+  const int32_t* perm;
+  const int32_t* key;
+  int64_t m;
+  uint32_t gmask;
+  DivMagic hk;
+  __device__ int operator()(int64_t i) const {
+    if (i >= m) return 0;
+    const int64_t j = i > 0 ? i - 1 : 0;
+    const uint32_t p = (uint32_t)clamp_task(perm[i], m);
+    const uint32_t p0 = (uint32_t)clamp_task(perm[j], m);
+    const uint32_t g = (uint32_t)key[i] ^ (uint32_t)key[j];
+    return ((i == 0) | ((g & gmask) != 0u) | (div_by(p, hk) != div_by(p0, hk))) ? 1 : 0;
+  }
+};
+
+struct EmitSlots {
+  SlotHead h;
+  const int32_t* n_active;
+  int64_t groups;
+  int b;
+  int32_t* slot_token;
+  int32_t* slot_off;
+  int32_t* grp_slot;
+  int32_t* pos_slot;
+  int32_t* counters;
+  __device__ void operator()(int64_t i, int val, int pos) const {
+    if (i >= h.m) return;
+    pos_slot[i] = val ? pos : pos - 1;
+    if (!val) return;
+    slot_token[pos] = (int32_t)div_by((uint32_t)clamp_task(h.perm[i], h.m), h.hk);
+    slot_off[pos] = (int32_t)i;
+    const uint32_t g = (uint32_t)h.key[i] & h.gmask;
+    if ((i == 0 || ((((uint32_t)h.key[i - 1]) ^ (uint32_t)h.key[i]) & h.gmask) != 0u) &&
+        g < (uint64_t)groups)
+      grp_slot[g] = pos;
+  }
+  __device__ void finish(int total) const {
+    slot_off[total] = (int32_t)h.m;
+    counters[0] = total;
+    const int64_t ng = ((int64_t)*n_active + b - 1) / b;
+    grp_slot[ng < groups ? ng : groups] = total;
+  }
+};
+
+struct GroupTiles {  // work tiles of group q: ceil(slots / 256) * ceil(experts / 64)
+  const int32_t* grp_slot;
+  const int32_t* n_active;
+  int64_t groups;
+  int b;
+  __device__ int operator()(int64_t q) const {
+    const int na = *n_active;
+    const int64_t ng = ((int64_t)na + b - 1) / b;
+    if (q >= ng || q >= groups) return 0;
+    const int tq = grp_slot[q + 1] - grp_slot[q];
+    const int64_t bq64 = (int64_t)na - q * b;
+    const int bq = bq64 < b ? (int)bq64 : b;
+    return ((tq + kGroupSlots - 1) / kGroupSlots) * ((bq + kGroupExperts - 1) / kGroupExperts);
+  }
+};
+
+struct EmitTiles {
+  int32_t* grp_tile;
+  int64_t n;
+  int32_t* counters;
+  __device__ void operator()(int64_t i, int val, int pos) const {
+    (void)val;
+    if (i < n) grp_tile[i] = pos;
+  }
+  __device__ void finish(int total) const { counters[1] = total; }
+};
 
 size_t align_up(size_t v) { return (v + 255) & ~(size_t)255; }
 
@@ -520,9 +638,16 @@ size_t schedule_ws_bytes(int64_t M, int64_t N) {
   return b;
 }
 
+int group_key_bits(const Shape& s) {
+  const int64_t cap = std::min<int64_t>(s.M, s.N);
+  const int gb = digit_bits_total((cap + s.B - 1) / s.B);
+  return gb > 0 ? gb : 1;
+}
+
 hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, int32_t* active,
                            int32_t* active_offsets, int32_t* n_active, int32_t* dense_offsets,
-                           void* ws, const int32_t** sorted_keys, hipStream_t st) {
+                           void* ws, const int32_t** sorted_keys, hipStream_t st,
+                           const int32_t** group_keys) {
   const int64_t M = s.M;
   const int64_t tiles = (M + kTile - 1) / kTile;
   char* w = (char*)ws;
@@ -579,15 +704,76 @@ hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, in
     hipLaunchKernelGGL(rank_fill_kernel, dim3((unsigned)((cap64 + kThreads - 1) / kThreads)),
                        dim3(kThreads), 0, st, (const int32_t*)active, (const int32_t*)n_active,
                        rank, cap64, s.N);
+    const int gb = group_key_bits(s);
     hipLaunchKernelGGL(group_key_kernel, dim3((unsigned)((M + kThreads - 1) / kThreads)),
-                       dim3(kThreads), 0, st, idx, (const int32_t*)rank, gkey, M, s.N, s.B);
-    const int group_bits = digit_bits_total((cap64 + s.B - 1) / s.B);
+                       dim3(kThreads), 0, st, idx, (const int32_t*)rank, gkey, M, s.N, s.B, gb);
     const int32_t* gk = nullptr;
-    hipError_t e = radix_sort_tasks(gkey, M, group_bits, perm, b, &gk, st);
+    hipError_t e = radix_sort_tasks(gkey, M, gb, perm, b, &gk, st);
     if (e != hipSuccess) return e;
     *sorted_keys = nullptr;
+    if (group_keys) *group_keys = gk;
   }
   return hipGetLastError();
+}
+
+
+int64_t group_count_bound(const Shape& s) {
+  const int64_t cap = std::min<int64_t>(s.M, s.N);
+  return (cap + s.B - 1) / s.B;
+}
+
+size_t group_plan_ws_bytes(const Shape& s) {
+  const int64_t G = group_count_bound(s);
+  size_t b = 0;
+  b += align_up((size_t)s.N * 4);                  // rank (caller's schedule only)
+  b += align_up((size_t)s.M * 4);                  // packed keys (caller's schedule only)
+  b += align_up((size_t)s.M * 4);                  // slot_token
+  b += align_up((size_t)(s.M + 1) * 4);            // slot_off
+  b += align_up((size_t)s.M * 4);                  // pos_slot
+  b += 2 * align_up((size_t)(G + 1) * 4);          // grp_slot, grp_tile
+  b += align_up((size_t)partial_count(s.M) * 4);   // scan partials
+  b += 256;                                        // counters
+  return b;
+}
+
+hipError_t launch_group_plan(const Shape& s, const int32_t* perm, const int32_t* n_active,
+                             const int32_t* sorted_group_keys, const int32_t* idx,
+                             const int32_t* active, void* ws, GroupPlan* plan,
+                             hipStream_t st) {
+  const int64_t M = s.M;
+  const int64_t G = group_count_bound(s);
+  const int64_t cap = std::min<int64_t>(M, s.N);
+  char* w = (char*)ws;
+  int32_t* rank = (int32_t*)w; w += align_up((size_t)s.N * 4);
+  int32_t* keys = (int32_t*)w; w += align_up((size_t)M * 4);
+  plan->slot_token = (int32_t*)w; w += align_up((size_t)M * 4);
+  plan->slot_off = (int32_t*)w; w += align_up((size_t)(M + 1) * 4);
+  plan->pos_slot = (int32_t*)w; w += align_up((size_t)M * 4);
+  plan->grp_slot = (int32_t*)w; w += align_up((size_t)(G + 1) * 4);
+  plan->grp_tile = (int32_t*)w; w += align_up((size_t)(G + 1) * 4);
+  int32_t* partial = (int32_t*)w; w += align_up((size_t)partial_count(M) * 4);
+  plan->counters = (int32_t*)w;
+  plan->G = G;
+  plan->gbits = group_key_bits(s);
+  if (sorted_group_keys) {
+    plan->key = sorted_group_keys;
+  } else {
+    hipLaunchKernelGGL(rank_fill_kernel, dim3((unsigned)((cap + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, st, active, n_active, rank, cap, s.N);
+    hipLaunchKernelGGL(position_key_kernel, dim3((unsigned)((M + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, st, perm, idx, (const int32_t*)rank, keys, M, s.N, s.B,
+                       plan->gbits);
+    plan->key = keys;
+  }
+  const SlotHead head{perm, plan->key, M, (1u << plan->gbits) - 1u,
+                      div_magic((uint32_t)s.hk)};
+  hipError_t e = device_scan(head,
+                             EmitSlots{head, n_active, G, s.B, plan->slot_token, plan->slot_off,
+                                       plan->grp_slot, plan->pos_slot, plan->counters},
+                             M, partial, st);
+  if (e != hipSuccess) return e;
+  return device_scan(GroupTiles{plan->grp_slot, n_active, G, s.B},
+                     EmitTiles{plan->grp_tile, G + 1, plan->counters}, G + 1, partial, st);
 }
 
 }  // namespace omnimoe

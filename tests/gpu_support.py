@@ -135,3 +135,43 @@ def backward_error_bounds(x, u, v, idx, g, dy, f_act, f_dact, dd_act_max=0.8,
     ds = g3 * (dg3 - (g3 * dg3).sum(axis=-1, keepdims=True))
     out["dscores"] = np.abs(g3) * (bdg3 + srow) + 8 * unit * np.abs(ds)
     return out
+
+
+def _act64(kind: int, h: np.ndarray) -> np.ndarray:
+    from scipy.special import erfc
+    if kind == 1:
+        return h / (1.0 + np.exp(-h))
+    return 0.5 * h * erfc(-h / np.sqrt(2.0))
+
+
+def grouped_gap_bound(f, idx, g, d: int, act_kind: int) -> np.ndarray:
+    """Element-wise bound on |y_a - y_b| for two expert computations that differ only in the
+    order in which each x_t . u_e is summed in fp32 (per task, as in the scheduled kernel, or
+    as dense tiles on the matrix cores): each dot lies within gamma_d sum |x u| of the exact
+    value (Higham, Thm. 3.1), |act'| <= 1.13 for GELU (1.10 for SiLU), the activation and the
+    gate multiply add a few ulp, and both results then go through the same fp32 slot-order sum
+    of a * v, each within gamma_{n+1} sum |a| |v| of its exact value."""
+    x, u, v = f["x"], f["u"], f["v"]
+    T = x.shape[0]
+    e = idx.reshape(T, -1)
+    gg = np.abs(g.reshape(T, -1)).astype(np.float64)
+    n = e.shape[1]
+
+    def gam(k):
+        return k * 2.0 ** -24 / (1 - k * 2.0 ** -24)
+
+    out = np.empty((T, d))
+    chunk = max(1, (1 << 23) // max(1, n * d))
+    for t0 in range(0, T, chunk):
+        xs = np.asarray(x[t0:t0 + chunk], dtype=np.float64)
+        es, gs = e[t0:t0 + chunk], gg[t0:t0 + chunk]
+        U = np.asarray(u[es], dtype=np.float64)
+        h = np.einsum("cd,cnd->cn", xs, U, optimize=True)
+        S = np.einsum("cd,cnd->cn", np.abs(xs), np.abs(U), optimize=True)
+        del U
+        a = gs * np.abs(_act64(act_kind, h))
+        da = gs * 1.13 * 2 * gam(d) * S + 16 * 2.0 ** -24 * a
+        V = np.abs(np.asarray(v[es], dtype=np.float64))
+        out[t0:t0 + chunk] = np.einsum("cn,cnd->cd", da + 2.02 * gam(n + 1) * a, V,
+                                       optimize=True)
+    return out + 1e-30

@@ -24,7 +24,7 @@ def _declared_functions():
 def test_header_matches_exports():
     lib = P.load_library()
     names = _declared_functions()
-    assert len(names) == 18
+    assert len(names) == 19
     assert sorted(P.EXPORTED) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -91,7 +91,9 @@ def test_workspace_sizes_cover_buffers():
     assert st == OK and route >= w.T * w.H * (w.n_rows + w.n_cols) * 4
     st, layer = _ws(d, B.STAGE_LAYER)
     assert st == OK and layer >= route + 3 * w.M * 4
-    assert _ws(d, 9)[0] == INVALID
+    assert _ws(d, 10)[0] == INVALID
+    st, grouped = _ws(d, B.STAGE_EXPERT_GROUPED)
+    assert st == OK and grouped >= w.M * 4 + w.N * 4 + 2 * w.M * 4
     st, dense = _ws(d, B.STAGE_ROUTE_DENSE)
     assert st == OK and dense >= w.T * w.H * w.N * 4
 
@@ -111,6 +113,19 @@ def test_entry_points_check_pointers_before_launch():
     assert lib.omnimoe_schedule(D, a, a, a, a, a, None, a, n(8), None) == WORKSPACE
     assert lib.omnimoe_expert_forward(D, a, a, a, a, a, None, a, a, n(1 << 30), None) == INVALID
     assert lib.omnimoe_expert_forward_token_centric(D, a, a, None, a, a, a, None) == INVALID
+    assert lib.omnimoe_expert_forward_grouped(D, a, a, a, a, a, a, None, a, a, a, n(1 << 40),
+                                              None) == INVALID
+    assert lib.omnimoe_expert_forward_grouped(D, a, a, a, a, a, a, a, bad, a, a, n(1 << 40),
+                                              None) == ALIGN
+    # fp32 tables: the grouped path runs on bf16 matrix cores only
+    assert lib.omnimoe_expert_forward_grouped(D, a, a, a, a, a, a, a, a, a, a, n(1 << 40),
+                                              None) == UNSUPPORTED
+    db = B.make_desc(synth.WORKLOADS["small_bf16"])
+    assert lib.omnimoe_expert_forward_grouped(ctypes.byref(db), a, a, a, a, a, a, a, a, a, a,
+                                              n(16), None) == WORKSPACE
+    db.d = 520  # d % 64 != 0
+    assert lib.omnimoe_expert_forward_grouped(ctypes.byref(db), a, a, a, a, a, a, a, a, a, a,
+                                              n(1 << 40), None) == UNSUPPORTED
     assert lib.omnimoe_route_dense(D, a, None, a, a, None, a, n(1 << 40), None) == INVALID
     assert lib.omnimoe_route_dense(D, a, a, a, a, None, a, n(16), None) == WORKSPACE
     assert lib.omnimoe_route_dense(D, a, a, a, a, bad, a, n(16), None) == ALIGN

@@ -13,8 +13,8 @@ import pytest
 
 import oracle
 import synth
-from gpu_support import (GATE_TOL, backward_error_bounds, compare_routing, higham_bound,
-                         row_rel_err, to_dev, tol, upload)
+from gpu_support import (GATE_TOL, backward_error_bounds, compare_routing, grouped_gap_bound,
+                         higham_bound, row_rel_err, to_dev, tol, upload)
 
 pytestmark = pytest.mark.gpu
 
@@ -243,17 +243,81 @@ def test_schedule_groups_bitexact(case):
     assert np.array_equal(dense.cpu().numpy(), rdense)
 
 
-@pytest.mark.parametrize("name", ["small_bf16", "skinny_bf16", "k256_bf16"])
-def test_layer_output_does_not_depend_on_group_size(name):
+def grouped_path(w):
+    """Whether the layer runs the grouped expert GEMM for group sizes above 1."""
+    return w.bf16 and w.d % 64 == 0
+
+
+@pytest.mark.parametrize("name", ["small_bf16", "skinny_bf16", "k256_bf16", "ragged_bf16"])
+def test_layer_group_size(name):
+    # Routing does not depend on B. With B > 1 the expert activations come from the grouped GEMM
+    # (bf16, d % 64 == 0): equal to the B = 1 result up to the order of the fp32 dot sums, within
+    # the element-wise bound of that reordering; otherwise bit for bit.
     w = SHAPES[name]
-    inp, _ = host_inputs(w)
+    inp, f = host_inputs(w)
     dev = upload(inp)
     y1, i1, g1 = gpu_layer(w, dev)
     for Bg in (4, 33):
         say(f"[layer B={Bg}] {name}")
         yb, ib, gb = gpu_layer(w.with_(group_size=Bg), dev)
-        assert np.array_equal(yb.view(np.uint8), y1.view(np.uint8))
         assert np.array_equal(ib, i1) and np.array_equal(gb.view(np.uint8), g1.view(np.uint8))
+        if grouped_path(w):
+            bound = grouped_gap_bound(f, i1, g1, w.d, oracle.desc(w).act)
+            gap = np.abs(yb.astype(np.float64) - y1)
+            say(f"  max gap / bound {(gap / bound).max():.3e}")
+            assert np.all(gap <= bound)
+        else:
+            assert np.array_equal(yb.view(np.uint8), y1.view(np.uint8))
+
+
+GROUPED_CASES = [
+    # (shape, B): partial expert tiles, groups of 64 and of more than 64 experts, a single group
+    # holding every active expert, B = 1, wide d, few tokens, K > 64 and the paper's grid
+    ("small_bf16", 2), ("small_bf16", 64), ("small_bf16", 100), ("k64_bf16", 33),
+    ("all_experts_bf16", 5), ("all_experts_bf16", 1 << 20), ("k64_bf16", 1),
+    ("wide_bf16", 3), ("skinny_bf16", 16), ("skinny1_bf16", 7), ("k256_bf16", 64),
+    ("shared_bf16", 48), ("paper_k512_bf16", 320),
+]
+
+
+@pytest.mark.parametrize("case", GROUPED_CASES, ids=[f"{n}-B{b}" for n, b in GROUPED_CASES])
+def test_expert_forward_grouped(case):
+    name, Bg = case
+    w1 = SHAPES[name]
+    w = w1.with_(group_size=Bg)
+    say(f"[grouped] {name} B={Bg}")
+    inp, f = host_inputs(w)
+    dev = upload(inp)
+    dsc = oracle.desc(w)
+    sr, sc = oracle.half_scores(dsc, f["x"], f["keys_row"], f["keys_col"])
+    idx, _, g64, _ = oracle.select(dsc, sr, sc, oracle.CARTESIAN)
+    g32 = g64.astype(np.float32)
+    perm, active, _, _ = oracle.schedule(dsc, idx)
+    perm1, _, _, _ = oracle.schedule(oracle.desc(w1), idx)
+    cap = min(w.M, w.N)
+    act_pad = np.zeros(cap, dtype=np.int32)
+    act_pad[:len(active)] = active
+    gi, gg = to_dev(idx), to_dev(g32)
+    y = torch.full((w.T, w.d), float("nan"), dtype=torch.float32, device="cuda")
+    y1 = torch.empty((w.T, w.d), dtype=torch.float32, device="cuda")
+    na = torch.tensor([len(active)], dtype=torch.int32, device="cuda")
+    P.omnimoe_expert_forward_grouped(B.make_desc(w), dev["x"], dev["u"], dev["v"], gi, gg,
+                                     to_dev(perm), to_dev(act_pad), na, y)
+    P.omnimoe_expert_forward(B.make_desc(w1), dev["x"], dev["u"], dev["v"], gi, gg,
+                             to_dev(perm1), y1)
+    y_again = torch.empty_like(y)
+    P.omnimoe_expert_forward_grouped(B.make_desc(w), dev["x"], dev["u"], dev["v"], gi, gg,
+                                     to_dev(perm), to_dev(act_pad), na, y_again)
+    torch.cuda.synchronize()
+    y, y1, y_again = y.cpu().numpy(), y1.cpu().numpy(), y_again.cpu().numpy()
+    assert np.array_equal(y.view(np.uint8), y_again.view(np.uint8))
+    y_ref = oracle.expert_forward(dsc, f["x"], f["u"], f["v"], idx, g32.astype(np.float64))
+    err = row_rel_err(y, y_ref)
+    bound = grouped_gap_bound(f, idx, g32, w.d, dsc.act)
+    gap = np.abs(y.astype(np.float64) - y1)
+    say(f"  max row rel err {err.max():.3e}; max gap / bound {(gap / bound).max():.3e}")
+    assert err.max() <= tol(w)
+    assert np.all(gap <= bound)
 
 
 # ------------------------------------------------------------------ expert compute
@@ -500,12 +564,18 @@ def test_dp_share_shape_sampled(train_tables):
     assert np.isfinite(y).all()
 
 
-@pytest.mark.parametrize("name", ["paper_k512_bf16", "paper_k4096_bf16"])
-def test_paper_benchmark_shapes_sampled(name):
+PAPER_CASES = [("paper_k512_bf16", 1), ("paper_k512_bf16", 320), ("paper_k4096_bf16", 1),
+               ("paper_k4096_bf16", 320)]
+
+
+@pytest.mark.parametrize("case", PAPER_CASES, ids=[f"{n}-B{b}" for n, b in PAPER_CASES])
+def test_paper_benchmark_shapes_sampled(case):
     # The paper's speed-benchmark shape: 4096 tokens, 320 x 320 experts of d = 1024, one head,
-    # K = 512 and 4096 (about 16.8 M tasks at K = 4096), checked on sampled tokens.
-    w = W[name]
-    say(f"[full] {name} T={w.T} K={w.K}")
+    # K = 512 and 4096 (about 16.8 M tasks at K = 4096), checked on sampled tokens; with
+    # groups of one grid row of experts (B = 320) the expert stage is the grouped GEMM.
+    name, Bg = case
+    w = W[name].with_(group_size=Bg)
+    say(f"[full] {name} T={w.T} K={w.K} B={Bg}")
     kr, kc = synth.make_keys(w)
     dev = {"keys_row": to_dev(kr), "keys_col": to_dev(kc),
            "u": to_dev(synth.make_expert_rows(w, "u")), "v": to_dev(synth.make_expert_rows(w, "v"))}
