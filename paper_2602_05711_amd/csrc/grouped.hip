@@ -12,10 +12,11 @@
 // load fall in distinct banks. bf16 products are exact and accumulate in fp32, as in the
 // per-task kernel.
 //
-// Epilogue: the 256 x 64 fp32 tile goes to LDS (over the stages), and the workgroup walks the
-// tasks of the tile's slots (one contiguous run of sorted positions) 256 at a time; those whose
-// expert lies in the tile (its place in the group, from the schedule's packed key) read their
-// entry (slot row from the plan) and write a[p].
+// Epilogue: the 256 x 64 fp32 tile goes to LDS (over the stages) with the tile's slot offsets,
+// and the workgroup walks the tasks of the tile's slots (one contiguous run of sorted positions)
+// 256 at a time; those whose expert lies in the tile (its place in the group, from the
+// schedule's packed key) find their slot row by binary search in the offsets, read their entry
+// and write a[p].
 //
 // Tiles are numbered group by group (slot tiles major, expert tiles fastest), so consecutive
 // tiles share their token rows and the group's u rows stay in the XCD's L2; each XCD takes one
@@ -37,7 +38,8 @@ constexpr int kRow = kK * 2;                                   // bytes per LDS 
 constexpr int kStage = (kGroupSlots + kGroupExperts) * kRow;   // 40 KiB
 constexpr int kHStride = kGroupExperts + 1;                    // floats per epilogue row
 static_assert(kGroupSlots == 4 * 64 && kGroupExperts == 64, "four waves of 64 x 64");
-static_assert(kGroupSlots * kHStride * 4 <= 2 * kStage, "the epilogue tile fits the stages");
+constexpr int kOffBase = kGroupSlots * kHStride * 4;            // slot offsets after the tile
+static_assert(kOffBase + (kGroupSlots + 1) * 4 <= 2 * kStage, "the epilogue fits the stages");
 
 __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 __device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
@@ -52,7 +54,6 @@ struct GroupedDotArgs {
   const int32_t* key;
   const int32_t* slot_token;
   const int32_t* slot_off;
-  const int32_t* pos_slot;
   const int32_t* grp_slot;
   const int32_t* grp_tile;
   const int32_t* counters;
@@ -202,15 +203,21 @@ __global__ __launch_bounds__(kThreads, 2) void grouped_dot_kernel(GroupedDotArgs
         for (int r = 0; r < 16; ++r)
           H[(w * 64 + i * 32 + (r >> 2) * 8 + (l >> 5) * 4 + (r & 3)) * kHStride + j * 32 +
             (l & 31)] = acc[i][j][r];
+    int32_t* offs = (int32_t*)(smem + kOffBase);  // offs[r] = first position of slot s0 + r
+    for (int r = tid; r <= ns; r += kThreads) offs[r] = a.slot_off[s0 + r];
     __syncthreads();
-    const int p_lo = a.slot_off[s0], p_hi = a.slot_off[s0 + ns];
+    const int p_lo = offs[0], p_hi = offs[ns];
     const int c0 = et * kGroupExperts;
     for (int pos = p_lo + tid; pos < p_hi; pos += kThreads) {
       const int c = (int)((uint32_t)a.key[pos] >> a.gbits) - c0;
-      const int r = a.pos_slot[pos] - s0;
-      if (c >= 0 && c < ne && r >= 0 && r < ns) {
+      if (c >= 0 && c < ne) {
+        int lo = 0, hi = ns - 1;  // the last slot r with offs[r] <= pos
+        while (lo < hi) {
+          const int mid = (lo + hi + 1) >> 1;
+          if (offs[mid] <= pos) lo = mid; else hi = mid - 1;
+        }
         const int32_t p = clamp_i32(a.perm[pos], a.M);
-        a.a[p] = a.gates[p] * activation(a.act, H[r * kHStride + c]);
+        a.a[p] = a.gates[p] * activation(a.act, H[lo * kHStride + c]);
       }
     }
     __syncthreads();
@@ -234,7 +241,6 @@ hipError_t launch_grouped_dot(const Shape& s, const void* x, const void* u, cons
   g.slot_token = plan.slot_token;
   g.slot_off = plan.slot_off;
   g.key = plan.key;
-  g.pos_slot = plan.pos_slot;
   g.gbits = plan.gbits;
   g.grp_slot = plan.grp_slot;
   g.grp_tile = plan.grp_tile;

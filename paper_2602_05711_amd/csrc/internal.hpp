@@ -97,7 +97,6 @@ struct GroupPlan {
   int gbits;
   int32_t* slot_token;  // [M]     token of slot s
   int32_t* slot_off;    // [M + 1] first sorted position of slot s (slot_off[slots] = M)
-  int32_t* pos_slot;    // [M]     slot of sorted position i
   int32_t* grp_slot;    // [G + 1] first slot of group q
   int32_t* grp_tile;    // [G + 1] first work tile of group q
   int32_t* counters;    // [0] slots, [1] work tiles

@@ -362,11 +362,8 @@ struct EmitSlots {
   int32_t* slot_token;
   int32_t* slot_off;
   int32_t* grp_slot;
-  int32_t* pos_slot;
   int32_t* counters;
   __device__ void operator()(int64_t i, int val, int pos) const {
-    if (i >= h.m) return;
-    pos_slot[i] = val ? pos : pos - 1;
     if (!val) return;
     slot_token[pos] = (int32_t)div_by((uint32_t)clamp_task(h.perm[i], h.m), h.hk);
     slot_off[pos] = (int32_t)i;
@@ -729,7 +726,6 @@ size_t group_plan_ws_bytes(const Shape& s) {
   b += align_up((size_t)s.M * 4);                  // packed keys (caller's schedule only)
   b += align_up((size_t)s.M * 4);                  // slot_token
   b += align_up((size_t)(s.M + 1) * 4);            // slot_off
-  b += align_up((size_t)s.M * 4);                  // pos_slot
   b += 2 * align_up((size_t)(G + 1) * 4);          // grp_slot, grp_tile
   b += align_up((size_t)partial_count(s.M) * 4);   // scan partials
   b += 256;                                        // counters
@@ -748,7 +744,6 @@ hipError_t launch_group_plan(const Shape& s, const int32_t* perm, const int32_t*
   int32_t* keys = (int32_t*)w; w += align_up((size_t)M * 4);
   plan->slot_token = (int32_t*)w; w += align_up((size_t)M * 4);
   plan->slot_off = (int32_t*)w; w += align_up((size_t)(M + 1) * 4);
-  plan->pos_slot = (int32_t*)w; w += align_up((size_t)M * 4);
   plan->grp_slot = (int32_t*)w; w += align_up((size_t)(G + 1) * 4);
   plan->grp_tile = (int32_t*)w; w += align_up((size_t)(G + 1) * 4);
   int32_t* partial = (int32_t*)w; w += align_up((size_t)partial_count(M) * 4);
@@ -769,7 +764,7 @@ hipError_t launch_group_plan(const Shape& s, const int32_t* perm, const int32_t*
                       div_magic((uint32_t)s.hk)};
   hipError_t e = device_scan(head,
                              EmitSlots{head, n_active, G, s.B, plan->slot_token, plan->slot_off,
-                                       plan->grp_slot, plan->pos_slot, plan->counters},
+                                       plan->grp_slot, plan->counters},
                              M, partial, st);
   if (e != hipSuccess) return e;
   return device_scan(GroupTiles{plan->grp_slot, n_active, G, s.B},
