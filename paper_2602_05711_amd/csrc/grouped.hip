@@ -3,20 +3,21 @@
 // the group's distinct tokens (its slots) and W_q the u rows of its experts. Only the entries
 // that are tasks are kept: a[p] = g_p * act(x_t . u_e) for every task p of the group.
 //
-// Work tile: 256 slots x 64 experts of one group per workgroup of four waves (each wave 64
-// slots x 64 experts, four 32 x 32 accumulators of v_mfma_f32_32x32x16_bf16). k steps of 64
-// go through two LDS stages filled straight from global memory with global_load_lds_dwordx4:
-// every lane supplies its own row address, so the token rows (x at the slots' tokens) and the
-// expert rows (u at the group's experts) are gathered on the way into LDS. LDS rows are 128 B;
-// chunk j of row r sits at position j ^ ((r >> 1) & 7), so the 16 rows read by one operand
-// load fall in distinct banks. bf16 products are exact and accumulate in fp32, as in the
-// per-task kernel.
+// Work tile: 256 slots x 32 NJ experts of one group per workgroup of four waves (each wave 64
+// slots x 32 NJ experts, 2 NJ accumulators of v_mfma_f32_32x32x16_bf16); NJ = 2 (64 experts)
+// for groups of up to 64, else 5 (160 experts), so that one load of a token row serves more
+// experts. k steps of 64 go through two LDS stages filled straight from global memory with
+// global_load_lds_dwordx4: every lane supplies its own row address, so the token rows (x at the
+// slots' tokens) and the expert rows (u at the group's experts) are gathered on the way into
+// LDS. LDS rows are 128 B; chunk j of row r sits at position j ^ ((r >> 1) & 7), so the 16 rows
+// read by one operand load fall in distinct banks. bf16 products are exact and accumulate in
+// fp32, as in the per-task kernel.
 //
-// Epilogue: the 256 x 64 fp32 tile goes to LDS (over the stages) with the tile's slot offsets,
-// and the workgroup walks the tasks of the tile's slots (one contiguous run of sorted positions)
-// 256 at a time; those whose expert lies in the tile (its place in the group, from the
-// schedule's packed key) find their slot row by binary search in the offsets, read their entry
-// and write a[p].
+// Epilogue: the fp32 tile goes to LDS (over the stages; in two halves of 128 slot rows when it
+// does not fit at once) with the tile's slot offsets, and the workgroup walks the tasks of those
+// slots (one contiguous run of sorted positions) 256 at a time; those whose expert lies in the
+// tile (its place in the group, from the schedule's packed key) find their slot row by binary
+// search in the offsets, read their entry and write a[p].
 //
 // Tiles are numbered group by group (slot tiles major, expert tiles fastest), so consecutive
 // tiles share their token rows and the group's u rows stay in the XCD's L2; each XCD takes one
@@ -33,13 +34,22 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 constexpr int kThreads = 256;
-constexpr int kK = 64;                                         // k per stage
-constexpr int kRow = kK * 2;                                   // bytes per LDS row
-constexpr int kStage = (kGroupSlots + kGroupExperts) * kRow;   // 40 KiB
-constexpr int kHStride = kGroupExperts + 1;                    // floats per epilogue row
-static_assert(kGroupSlots == 4 * 64 && kGroupExperts == 64, "four waves of 64 x 64");
-constexpr int kOffBase = kGroupSlots * kHStride * 4;            // slot offsets after the tile
-static_assert(kOffBase + (kGroupSlots + 1) * 4 <= 2 * kStage, "the epilogue fits the stages");
+constexpr int kK = 64;      // k per stage
+constexpr int kRow = kK * 2;  // bytes per LDS row
+static_assert(kGroupSlots == 4 * 64, "four waves of 64 slot rows");
+
+template <int NJ>
+struct TileShape {
+  static constexpr int kExperts = 32 * NJ;
+  static constexpr int kStage = (kGroupSlots + kExperts) * kRow;
+  static constexpr int kHStride = kExperts + 1;  // floats per epilogue row
+  // slot rows per epilogue pass: all 256 if the tile and the offsets fit in the two stages
+  static constexpr int kRowsPerPass =
+      kGroupSlots * kHStride * 4 + (kGroupSlots + 1) * 4 <= 2 * kStage ? kGroupSlots
+                                                                        : kGroupSlots / 2;
+  static constexpr int kOffBase = kRowsPerPass * kHStride * 4;
+  static_assert(kOffBase + (kGroupSlots + 1) * 4 <= 2 * kStage, "the epilogue fits the stages");
+};
 
 __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 __device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
@@ -66,7 +76,10 @@ __device__ __forceinline__ int32_t clamp_i32(int32_t v, int64_t n) {
   return v < 0 ? 0 : (v >= n ? (int32_t)(n - 1) : v);
 }
 
-__global__ __launch_bounds__(kThreads, 2) void grouped_dot_kernel(GroupedDotArgs a) {
+template <int NJ>
+__global__ __launch_bounds__(kThreads, 1) void grouped_dot_kernel(GroupedDotArgs a) {
+  using TS = TileShape<NJ>;
+  constexpr int TE = TS::kExperts;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
   const int n_act = *a.n_active;
@@ -105,18 +118,18 @@ __global__ __launch_bounds__(kThreads, 2) void grouped_dot_kernel(GroupedDotArgs
     const int tq = a.grp_slot[q + 1] - s_q;
     const int e_q = q * a.B;
     const int bq = min(a.B, n_act - e_q);
-    const int n_et = (bq + kGroupExperts - 1) / kGroupExperts;
+    const int n_et = (bq + TE - 1) / TE;
     const int local = tile - a.grp_tile[q];
     const int stl = local / n_et, et = local - stl * n_et;
     const int s0 = s_q + stl * kGroupSlots;
     const int ns = min(kGroupSlots, tq - stl * kGroupSlots);
-    const int r0 = e_q + et * kGroupExperts;
-    const int ne = min(kGroupExperts, bq - et * kGroupExperts);
+    const int r0 = e_q + et * TE;
+    const int ne = min(TE, bq - et * TE);
     // Loader: instruction i of wave w fills 8 LDS rows; lane l writes position l % 8 of row
     // l / 8 of them, i.e. global chunk (l % 8) ^ swz(row). Rows past the tile's slots or
     // experts load the tile's first row (never read back).
     const uint16_t* ga[8];
-    const uint16_t* gb[2];
+    const uint16_t* gb[NJ];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int r = (w * 8 + i) * 8 + (l >> 3);
@@ -125,38 +138,37 @@ __global__ __launch_bounds__(kThreads, 2) void grouped_dot_kernel(GroupedDotArgs
       ga[i] = a.x + (int64_t)tok * a.d + j * 8;
     }
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int r = (w * 2 + i) * 8 + (l >> 3);
+    for (int i = 0; i < NJ; ++i) {
+      const int r = (w * NJ + i) * 8 + (l >> 3);
       const int j = (l & 7) ^ swz(r);
       const int32_t e = clamp_i32(a.active[r0 + (r < ne ? r : 0)], a.N);
       gb[i] = a.u + (int64_t)e * a.d + j * 8;
     }
     auto issue = [&](int stage, int k0) {
-      unsigned char* base = smem + stage * kStage;
+      unsigned char* base = smem + stage * TS::kStage;
 #pragma unroll
       for (int i = 0; i < 8; ++i)
         __builtin_amdgcn_global_load_lds((const void*)(ga[i] + k0),
                                          (lds_ptr_t)(base + (w * 8 + i) * 8 * kRow), 16, 0, 0);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < NJ; ++i)
         __builtin_amdgcn_global_load_lds(
             (const void*)(gb[i] + k0),
-            (lds_ptr_t)(base + kGroupSlots * kRow + (w * 2 + i) * 8 * kRow), 16, 0, 0);
+            (lds_ptr_t)(base + kGroupSlots * kRow + (w * NJ + i) * 8 * kRow), 16, 0, 0);
     };
-    int a_off[2], b_off[2];  // LDS row offsets of this lane's operand rows
+    int a_off[2], b_off[NJ];  // LDS row offsets of this lane's operand rows
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      a_off[i] = (w * 64 + i * 32 + frow) * kRow;
-      b_off[i] = kGroupSlots * kRow + (i * 32 + frow) * kRow;
-    }
+    for (int i = 0; i < 2; ++i) a_off[i] = (w * 64 + i * 32 + frow) * kRow;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) b_off[j] = kGroupSlots * kRow + (j * 32 + frow) * kRow;
     auto frag = [&](const unsigned char* st, int off, int ks) -> bf16x8 {
       return *(const bf16x8*)(st + off + (((ks * 2 + fk) ^ sw) << 4));
     };
-    f32x16 acc[2][2];
+    f32x16 acc[2][NJ];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < NJ; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
     issue(0, 0);
@@ -165,27 +177,25 @@ __global__ __launch_bounds__(kThreads, 2) void grouped_dot_kernel(GroupedDotArgs
     for (int kt = 0; kt < KT; ++kt) {
       const int cur = kt & 1;
       if (kt + 1 < KT) issue(cur ^ 1, (kt + 1) * kK);
-      const unsigned char* st = smem + cur * kStage;
-      bf16x8 fa[2][2], fb[2][2];
+      const unsigned char* st = smem + cur * TS::kStage;
+      bf16x8 fa[2][2], fb[2][NJ];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        fa[0][i] = frag(st, a_off[i], 0);
-        fb[0][i] = frag(st, b_off[i], 0);
-      }
+      for (int i = 0; i < 2; ++i) fa[0][i] = frag(st, a_off[i], 0);
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) fb[0][j] = frag(st, b_off[j], 0);
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const int c = ks & 1;
         if (ks + 1 < 4) {
 #pragma unroll
-          for (int i = 0; i < 2; ++i) {
-            fa[c ^ 1][i] = frag(st, a_off[i], ks + 1);
-            fb[c ^ 1][i] = frag(st, b_off[i], ks + 1);
-          }
+          for (int i = 0; i < 2; ++i) fa[c ^ 1][i] = frag(st, a_off[i], ks + 1);
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) fb[c ^ 1][j] = frag(st, b_off[j], ks + 1);
         }
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
+          for (int j = 0; j < NJ; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[c][i], fb[c][j], acc[i][j],
                                                                 0, 0, 0);
       }
@@ -195,36 +205,47 @@ __global__ __launch_bounds__(kThreads, 2) void grouped_dot_kernel(GroupedDotArgs
     // accumulator element r of block (i, j) of wave w: slot row 64 w + 32 i + 8 (r / 4) +
     // 4 (l / 32) + r % 4, expert column 32 j + l % 32
     float* H = (float*)smem;
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          H[(w * 64 + i * 32 + (r >> 2) * 8 + (l >> 5) * 4 + (r & 3)) * kHStride + j * 32 +
-            (l & 31)] = acc[i][j][r];
-    int32_t* offs = (int32_t*)(smem + kOffBase);  // offs[r] = first position of slot s0 + r
+    int32_t* offs = (int32_t*)(smem + TS::kOffBase);  // offs[r] = first position of slot s0 + r
     for (int r = tid; r <= ns; r += kThreads) offs[r] = a.slot_off[s0 + r];
-    __syncthreads();
-    const int p_lo = offs[0], p_hi = offs[ns];
-    const int c0 = et * kGroupExperts;
-    for (int pos = p_lo + tid; pos < p_hi; pos += kThreads) {
-      const int c = (int)((uint32_t)a.key[pos] >> a.gbits) - c0;
-      if (c >= 0 && c < ne) {
-        int lo = 0, hi = ns - 1;  // the last slot r with offs[r] <= pos
-        while (lo < hi) {
-          const int mid = (lo + hi + 1) >> 1;
-          if (offs[mid] <= pos) lo = mid; else hi = mid - 1;
-        }
-        const int32_t p = clamp_i32(a.perm[pos], a.M);
-        a.a[p] = a.gates[p] * activation(a.act, H[lo * kHStride + c]);
+    const int c0 = et * TE;
+#pragma unroll
+    for (int pass = 0; pass < kGroupSlots / TS::kRowsPerPass; ++pass) {
+      const int row0 = pass * TS::kRowsPerPass;  // first slot row held in H this pass
+      if (w * 64 >= row0 && w * 64 < row0 + TS::kRowsPerPass) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < NJ; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              H[(w * 64 - row0 + i * 32 + (r >> 2) * 8 + (l >> 5) * 4 + (r & 3)) * TS::kHStride +
+                j * 32 + (l & 31)] = acc[i][j][r];
       }
+      __syncthreads();
+      const int r_hi = min(ns, row0 + TS::kRowsPerPass);
+      if (row0 < r_hi) {
+        const int p_lo = offs[row0], p_hi = offs[r_hi];
+        for (int pos = p_lo + tid; pos < p_hi; pos += kThreads) {
+          const int c = (int)((uint32_t)a.key[pos] >> a.gbits) - c0;
+          if (c >= 0 && c < ne) {
+            int lo = row0, hi = r_hi - 1;  // the last slot r with offs[r] <= pos
+            while (lo < hi) {
+              const int mid = (lo + hi + 1) >> 1;
+              if (offs[mid] <= pos) lo = mid; else hi = mid - 1;
+            }
+            const int32_t p = clamp_i32(a.perm[pos], a.M);
+            a.a[p] = a.gates[p] * activation(a.act, H[(lo - row0) * TS::kHStride + c]);
+          }
+        }
+      }
+      __syncthreads();
     }
-    __syncthreads();
   }
 }
 
 }  // namespace
+
+int grouped_tile_experts(int B) { return B <= 64 ? 64 : 160; }
 
 hipError_t launch_grouped_dot(const Shape& s, const void* x, const void* u, const float* gates,
                               const int32_t* perm, const int32_t* active,
@@ -252,8 +273,13 @@ hipError_t launch_grouped_dot(const Shape& s, const void* x, const void* u, cons
   g.d = s.d;
   g.B = s.B;
   g.act = s.act;
-  // persistent: a multiple of eight workgroups, two per compute unit
-  hipLaunchKernelGGL(grouped_dot_kernel, dim3(512), dim3(kThreads), 2 * kStage, st, g);
+  // persistent: a multiple of eight workgroups, one or two per compute unit
+  if (grouped_tile_experts(s.B) == 64)
+    hipLaunchKernelGGL(grouped_dot_kernel<2>, dim3(512), dim3(kThreads),
+                       2 * TileShape<2>::kStage, st, g);
+  else
+    hipLaunchKernelGGL(grouped_dot_kernel<5>, dim3(256), dim3(kThreads),
+                       2 * TileShape<5>::kStage, st, g);
   return hipGetLastError();
 }
 

@@ -89,9 +89,10 @@ hipError_t launch_route_backward(const Shape& s, const void* x, const void* keys
 
 // Plan of the grouped expert GEMM (Eq. 14) over a schedule whose groups hold B > 1 active
 // experts (tasks in (group, task id) order). A slot is a (group, token) pair; slots are numbered
-// group by group, tokens ascending. Work tiles are 256 slots x 64 experts of one group.
+// group by group, tokens ascending. Work tiles are 256 slots x grouped_tile_experts(B) experts
+// of one group.
 constexpr int kGroupSlots = 256;
-constexpr int kGroupExperts = 64;
+int grouped_tile_experts(int B);
 struct GroupPlan {
   const int32_t* key;   // [M]     packed key of sorted position i: place << gbits | group
   int gbits;

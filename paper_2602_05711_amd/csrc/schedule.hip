@@ -380,11 +380,11 @@ struct EmitSlots {
   }
 };
 
-struct GroupTiles {  // work tiles of group q: ceil(slots / 256) * ceil(experts / 64)
+struct GroupTiles {  // work tiles of group q: ceil(slots / 256) * ceil(experts / te)
   const int32_t* grp_slot;
   const int32_t* n_active;
   int64_t groups;
-  int b;
+  int b, te;
   __device__ int operator()(int64_t q) const {
     const int na = *n_active;
     const int64_t ng = ((int64_t)na + b - 1) / b;
@@ -392,7 +392,7 @@ struct GroupTiles {  // work tiles of group q: ceil(slots / 256) * ceil(experts 
     const int tq = grp_slot[q + 1] - grp_slot[q];
     const int64_t bq64 = (int64_t)na - q * b;
     const int bq = bq64 < b ? (int)bq64 : b;
-    return ((tq + kGroupSlots - 1) / kGroupSlots) * ((bq + kGroupExperts - 1) / kGroupExperts);
+    return ((tq + kGroupSlots - 1) / kGroupSlots) * ((bq + te - 1) / te);
   }
 };
 
@@ -767,7 +767,7 @@ hipError_t launch_group_plan(const Shape& s, const int32_t* perm, const int32_t*
                                        plan->grp_slot, plan->counters},
                              M, partial, st);
   if (e != hipSuccess) return e;
-  return device_scan(GroupTiles{plan->grp_slot, n_active, G, s.B},
+  return device_scan(GroupTiles{plan->grp_slot, n_active, G, s.B, grouped_tile_experts(s.B)},
                      EmitTiles{plan->grp_tile, G + 1, plan->counters}, G + 1, partial, st);
 }
 
