@@ -227,6 +227,39 @@ def extras(args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1, 
     else:
         no_cpr = {"skipped": f"the dense logits would take {dense_bytes / 2**30:.0f} GiB"}
 
+    # The grouped expert GEMM (Eq. 14): the same layer with groups of B active experts, per kernel
+    # group (the schedule then adds the group sort, the expert stage the group plan).
+    grouped = None
+    gb = args.grouped_b
+    if gb > 1 and w.group_size == 1 and w.bf16 and w.d % 64 == 0:
+        wg = w.with_(group_size=gb)
+        dg = P.make_desc(wg)
+        wsg = P.workspace(dg, 4)
+        yg = torch.empty_like(y)
+        for _ in range(2):
+            P.omnimoe_layer_forward(dg, d_in["x"], d_in["keys_row"], d_in["keys_col"], d_in["u"],
+                                    d_in["v"], yg, ws=wsg, stream=stream)
+        tg = P.Timer(args.steps)
+        for _ in range(args.steps):
+            tg.layer_forward(dg, d_in["x"], d_in["keys_row"], d_in["keys_col"], d_in["u"],
+                             d_in["v"], yg, wsg, stream=stream)
+        msg, ng = tg.read()
+        tg.close()
+        perg = {k: v / ng for k, v in msg.items()}
+        y1 = torch.empty_like(y)  # the per-task layer again (y itself now holds the MLP too)
+        P.omnimoe_layer_forward(desc, d_in["x"], d_in["keys_row"], d_in["keys_col"], d_in["u"],
+                                d_in["v"], y1, stream=stream)
+        torch.cuda.synchronize()
+        rel = float(((yg - y1).abs().amax(dim=1) / y1.abs().amax(dim=1).clamp_min(1e-30)).max())
+        grouped = {"group_size": gb, "per_kernel_ms": perg, "layer_ms": sum(perg.values()),
+                   "expert_stage_ms": perg["expert_dot"] + perg["accumulate"],
+                   "per_task_expert_stage_ms": per["expert_dot"] + per["accumulate"],
+                   "max_row_rel_diff_vs_per_task": rel}
+        del y1
+        log(f"grouped GEMM, B={gb}: layer {grouped['layer_ms']:.3f} ms (dot "
+            f"{perg['expert_dot']:.3f} ms vs per-task {per['expert_dot']:.3f} ms)")
+        del wsg, yg
+
     # Backward of the expert compute (training): token pass, per-expert pass over the
     # schedule's segments, softmax pass; dy is a seeded standard normal.
     perm, off, na, n_active = sched
@@ -270,7 +303,7 @@ def extras(args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1, 
                     "tokens_per_s": w.T / ((bw_ms + rb_ms) * 1e-3)}
         log(f"expert backward: {bw_ms:.3f} ms, router backward: {rb_ms:.3f} ms")
         del dy, dx, du, dv, wsb, dkr, dkc, wsr
-    return ablation, shared_mlp, no_cpr, backward
+    return ablation, shared_mlp, no_cpr, backward, grouped
 
 
 def main():
@@ -292,6 +325,12 @@ def main():
     ap.add_argument("--layer-only", action="store_true",
                     help="time the layer alone: no cold timing, shared branch or ablations (for "
                          "kernel traces and counters that should hold the layer's kernels only)")
+    ap.add_argument("--group-size", type=int, default=0,
+                    help="execution-group size B of the schedule (0: the workload's own); with "
+                         "B > 1 the layer runs the grouped expert GEMM")
+    ap.add_argument("--grouped-b", type=int, default=64,
+                    help="group size of the grouped-GEMM comparison timed beside the layer "
+                         "(0: skip)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="after timing, run a plain device copy of this many bytes twice "
                          "(a known-size reference for rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -308,8 +347,10 @@ def main():
     import paper_2602_05711_amd as P
 
     w = synth.WORKLOADS[args.workload]
+    if args.group_size > 0:
+        w = w.with_(group_size=args.group_size)
     log(f"workload {w.name}: T={w.T} d={w.d} grid={w.n_rows}x{w.n_cols} d_key={w.d_key} "
-        f"H={w.H} K={w.K} {w.dtype}")
+        f"H={w.H} K={w.K} B={w.group_size} {w.dtype}")
     t0 = time.time()
     inp = synth.make_inputs(w)
     log(f"generated inputs in {time.time() - t0:.1f} s")
@@ -402,17 +443,18 @@ def main():
     act = torch.empty(A, dtype=torch.int32, device="cuda")
     off = torch.empty(A + 1, dtype=torch.int32, device="cuda")
     na = torch.zeros(1, dtype=torch.int32, device="cuda")
-    P.omnimoe_schedule(desc, idx, perm, act, off, na)
+    # expert-major schedule (group size 1): the backward walks its per-expert segments
+    P.omnimoe_schedule(P.make_desc(w.with_(group_size=1)), idx, perm, act, off, na)
     torch.cuda.synchronize()
     n_active = int(na.item())
     routing = routing_stats(idx.cpu().numpy(), w.N)
     assert routing["n_active"] == n_active
 
-    ablation = shared_mlp = no_cpr = backward = None
+    ablation = shared_mlp = no_cpr = backward = grouped = None
     if not args.layer_only:
-        ablation, shared_mlp, no_cpr, backward = extras(args, w, desc, d_in, dev, idx, g, y,
-                                                        stream, per, ms_step, ev0, ev1,
-                                                        (perm, off, na, n_active))
+        ablation, shared_mlp, no_cpr, backward, grouped = extras(
+            args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1,
+            (perm, off, na, n_active))
 
     work = algorithmic_work(w, n_active)
     kernels = {}
@@ -470,7 +512,8 @@ def main():
         "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": w.name, "T": w.T, "d": w.d, "n_rows": w.n_rows,
                    "n_cols": w.n_cols, "N": w.N, "d_key": w.d_key, "H": w.H, "K": w.K,
-                   "act": w.act, "query": w.query_mode, "graph": bool(args.graph)},
+                   "act": w.act, "query": w.query_mode, "group_size": w.group_size,
+                   "graph": bool(args.graph)},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "cold": cold,
@@ -478,6 +521,7 @@ def main():
         "expert_backward": backward,
         "ablation_no_schedule": ablation,
         "ablation_no_cartesian_router": no_cpr,
+        "grouped_expert_gemm": grouped,
         "n_active": n_active, "eta": w.M / max(1, n_active), "routing": routing,
         "schedule_share": per["schedule"] / sum(per.values()),
         "kernels": kernels,
