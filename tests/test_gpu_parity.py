@@ -416,12 +416,17 @@ def test_layer_is_deterministic():
         assert np.array_equal(x.view(np.uint8), z.view(np.uint8))
 
 
-@pytest.mark.parametrize("name", ["small_bf16", "decode64_like_bf16"])
+@pytest.mark.parametrize("name", ["small_bf16", "decode64_like_bf16", "grouped_b64_bf16",
+                                  "grouped_k256_b100_bf16"])
 def test_layer_graph_replays_match_eager(name):
     # The layer call allocates nothing and clears with kernels only, so it can be captured in a
     # HIP graph; every replay (with other eager work and synchronisations in between) must
     # reproduce the eager result bit for bit, idx and gates included.
-    w = W["small_bf16"] if name == "small_bf16" else SHAPES["skinny_bf16"].with_(T=64)
+    w = {"small_bf16": W["small_bf16"],
+         "decode64_like_bf16": SHAPES["skinny_bf16"].with_(T=64),
+         # groups of B > 1: the grouped GEMM, its plan and the group sort inside the graph
+         "grouped_b64_bf16": W["small_bf16"].with_(group_size=64),
+         "grouped_k256_b100_bf16": SHAPES["k256_bf16"].with_(group_size=100)}[name]
     inp, _ = host_inputs(w)
     dev = upload(inp)
     y_ref, idx_ref, g_ref = gpu_layer(w, dev)
