@@ -70,12 +70,40 @@ __device__ int block_excl_scan(int v, int* total) {
   return off + incl - v;
 }
 
+// The values of a thread's kItems consecutive items, one call of f each; functors over
+// arrays that can do better (vector loads) overload this.
+template <class F>
+__device__ __forceinline__ void eval_items(const F& f, int64_t base, int (&v)[kItems]) {
+#pragma unroll
+  for (int j = 0; j < kItems; ++j) v[j] = f(base + j);
+}
+
+// HeadFlag over a full interior run: keys base - 1 .. base + kItems - 1 with 16-byte loads.
+__device__ __forceinline__ void eval_items(const HeadFlag& f, int64_t base, int (&v)[kItems]) {
+  if (base <= 0 || base + kItems > f.n) {
+#pragma unroll
+    for (int j = 0; j < kItems; ++j) v[j] = f(base + j);
+    return;
+  }
+  int32_t k[kItems + 1];
+  k[0] = f.k[base - 1];
+#pragma unroll
+  for (int q = 0; q < kItems / 4; ++q) {
+    const int4 kk = *(const int4*)(f.k + base + 4 * q);
+    k[1 + 4 * q] = kk.x; k[2 + 4 * q] = kk.y; k[3 + 4 * q] = kk.z; k[4 + 4 * q] = kk.w;
+  }
+#pragma unroll
+  for (int j = 0; j < kItems; ++j) v[j] = k[j + 1] != k[j] ? 1 : 0;
+}
+
 template <class F>
 __global__ __launch_bounds__(kThreads) void scan_reduce_kernel(F f, int64_t n, int32_t* partial) {
   const int64_t base = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kItems;
+  int v[kItems];
+  eval_items(f, base, v);
   int s = 0;
 #pragma unroll
-  for (int j = 0; j < kItems; ++j) s += f(base + j);
+  for (int j = 0; j < kItems; ++j) s += v[j];
   int total;
   block_excl_scan(s, &total);
   if (threadIdx.x == 0) partial[blockIdx.x] = total;
@@ -126,12 +154,10 @@ __global__ __launch_bounds__(kThreads) void scan_down_kernel(F f, E emit, const 
   block_excl_scan(pre, &before);
   const int64_t base = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kItems;
   int v[kItems];
+  eval_items(f, base, v);
   int s = 0;
 #pragma unroll
-  for (int j = 0; j < kItems; ++j) {
-    v[j] = f(base + j);
-    s += v[j];
-  }
+  for (int j = 0; j < kItems; ++j) s += v[j];
   int total;
   int pos = block_excl_scan(s, &total) + before;
 #pragma unroll
@@ -353,6 +379,33 @@ struct SlotHead {  // 1 where sorted position i starts a new (group, token) slot
     return ((i == 0) | ((g & gmask) != 0u) | (div_by(p, hk) != div_by(p0, hk))) ? 1 : 0;
   }
 };
+
+// SlotHead over a full interior run of items: perm and the keys of positions base - 1 ..
+// base + kItems - 1 with 16-byte loads (base is a multiple of kItems, the arrays 16-byte
+// aligned), the rest as above.
+__device__ __forceinline__ void eval_items(const SlotHead& h, int64_t base, int (&v)[kItems]) {
+  if (base <= 0 || base + kItems > h.m) {
+#pragma unroll
+    for (int j = 0; j < kItems; ++j) v[j] = h(base + j);
+    return;
+  }
+  int32_t p[kItems + 1], k[kItems + 1];
+  p[0] = h.perm[base - 1];
+  k[0] = h.key[base - 1];
+#pragma unroll
+  for (int q = 0; q < kItems / 4; ++q) {
+    const int4 pp = *(const int4*)(h.perm + base + 4 * q);
+    const int4 kk = *(const int4*)(h.key + base + 4 * q);
+    p[1 + 4 * q] = pp.x; p[2 + 4 * q] = pp.y; p[3 + 4 * q] = pp.z; p[4 + 4 * q] = pp.w;
+    k[1 + 4 * q] = kk.x; k[2 + 4 * q] = kk.y; k[3 + 4 * q] = kk.z; k[4 + 4 * q] = kk.w;
+  }
+  uint32_t t[kItems + 1];
+#pragma unroll
+  for (int j = 0; j <= kItems; ++j) t[j] = div_by((uint32_t)clamp_task(p[j], h.m), h.hk);
+#pragma unroll
+  for (int j = 0; j < kItems; ++j)
+    v[j] = ((((uint32_t)k[j + 1] ^ (uint32_t)k[j]) & h.gmask) != 0u || t[j + 1] != t[j]) ? 1 : 0;
+}
 
 struct EmitSlots {
   SlotHead h;
