@@ -472,11 +472,14 @@ int digit_bits_total(int64_t n_experts) {
 
 // ---------------------------------------------------------------- small task counts
 // One workgroup of 16 waves sorts up to 8192 tasks and extracts the segments in a single
-// launch (decode shapes). Same algorithm as the multi-kernel path: per pass, wave w ranks its
-// contiguous slice of tasks stably with ballot-matched peers and per-wave digit counters, the
-// (digit, wave) counts are scanned digit-major, and tasks scatter. Keys and task ids stay in
-// LDS between passes (only the last pass writes perm and the sorted keys out); then segment
-// heads are counted from LDS and compacted with a block scan.
+// launch (decode shapes). When the keys are spread out (no bucket of the top ten key bits holds
+// more than 128 tasks, the usual case), the tasks are counted into those 1024 buckets, placed
+// into their bucket's range in any order, and each task's final place is its bucket's start
+// plus the number of (expert, task) keys in the bucket below its own: no radix passes. Otherwise
+// the multi-kernel path's algorithm runs in LDS: per pass, wave w ranks its contiguous slice of
+// tasks stably with ballot-matched peers and per-wave digit counters, the (digit, wave) counts
+// are scanned digit-major, and tasks scatter. Either way the segment heads are then counted from
+// the sorted keys in LDS and compacted with a block scan.
 
 constexpr int kSmallWaves = 16;
 constexpr int kSmallThreads = kSmallWaves * kWave;
@@ -495,17 +498,174 @@ struct SmallSched {
   int passes, per, total_bits;
 };
 
+// Segment heads of the sorted keys in LDS (expert of each sorted position): each thread owns up
+// to 8 consecutive positions; the heads are counted, scanned and written to active / offsets.
+__device__ void small_heads(const SmallSched& a, const int* skey, int* wsum) {
+  const int tid = threadIdx.x, l = lane_id(), w = tid >> 6;
+  const int per_t = (a.M + kSmallThreads - 1) / kSmallThreads;
+  const int b0 = tid * per_t;
+  int heads = 0;
+  if (per_t == 8 && b0 + 8 <= a.M) {
+    // eight consecutive keys with two 16-byte reads (b0 is a multiple of 8)
+    const int4 k0 = *(const int4*)(skey + b0);
+    const int4 k1 = *(const int4*)(skey + b0 + 4);
+    const int pv = b0 > 0 ? skey[b0 - 1] : ~k0.x;
+    heads = (k0.x != pv) + (k0.y != k0.x) + (k0.z != k0.y) + (k0.w != k0.z) + (k1.x != k0.w) +
+            (k1.y != k1.x) + (k1.z != k1.y) + (k1.w != k1.z);
+  } else {
+    for (int i = b0; i < b0 + per_t && i < a.M; ++i) heads += (i == 0 || skey[i] != skey[i - 1]);
+  }
+  const int ex = wave_excl_scan_i32(heads);
+  if (l == kWave - 1) wsum[w] = ex + heads;
+  __syncthreads();
+  int off = 0, tot = 0;
+  for (int ww = 0; ww < kSmallWaves; ++ww) {
+    const int v = wsum[ww];
+    if (ww < w) off += v;
+    tot += v;
+  }
+  int pos = off + ex;
+  for (int i = b0; i < b0 + per_t && i < a.M; ++i) {
+    if (i == 0 || skey[i] != skey[i - 1]) {
+      if (pos < a.cap) {
+        a.active[pos] = skey[i];
+        a.offsets[pos] = i;
+      }
+      ++pos;
+    }
+  }
+  if (tid == 0) {
+    const int n = tot < a.cap ? tot : a.cap;
+    *a.n_active = n;
+    a.offsets[n] = a.M;
+  }
+}
+
+// Outputs of the bucket path from the sorted 64-bit keys in LDS: thread t writes positions
+// 8 t .. 8 t + 7 of perm and of the sorted experts with 16-byte stores, keeps the experts in
+// LDS for the segment heads, then compacts the heads.
+__device__ void small_out_sorted(const SmallSched& a, const uint64_t* keys, int* sorted_lds,
+                                 int* wsum) {
+  const int tid = threadIdx.x;
+  const int b0 = tid * 8;
+  if (b0 + 8 <= a.M) {
+    int32_t e[8], t[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const uint64_t k = keys[b0 + q];
+      e[q] = (int32_t)(k >> 32);
+      t[q] = (int32_t)(uint32_t)k;
+    }
+    *(int4*)(a.perm + b0) = make_int4(t[0], t[1], t[2], t[3]);
+    *(int4*)(a.perm + b0 + 4) = make_int4(t[4], t[5], t[6], t[7]);
+    *(int4*)(a.sorted + b0) = make_int4(e[0], e[1], e[2], e[3]);
+    *(int4*)(a.sorted + b0 + 4) = make_int4(e[4], e[5], e[6], e[7]);
+    *(int4*)(sorted_lds + b0) = make_int4(e[0], e[1], e[2], e[3]);
+    *(int4*)(sorted_lds + b0 + 4) = make_int4(e[4], e[5], e[6], e[7]);
+  } else {
+    for (int i = b0; i < b0 + 8 && i < a.M; ++i) {
+      const uint64_t k = keys[i];
+      a.perm[i] = (int32_t)(uint32_t)k;
+      a.sorted[i] = (int32_t)(k >> 32);
+      sorted_lds[i] = (int32_t)(k >> 32);
+    }
+  }
+  __syncthreads();
+  small_heads(a, sorted_lds, wsum);
+}
+
 __global__ __launch_bounds__(kSmallThreads) void schedule_small_kernel(SmallSched a) {
   __shared__ int cnt[kSmallWaves][kMaxRadix];
   __shared__ int dsum[kMaxRadix];
   __shared__ int wsum[kSmallWaves];
-  __shared__ int skey[kSmallMax];  // keys and task ids between passes, then the sorted keys
-  __shared__ int sval[kSmallMax];
+  // keys and task ids between radix passes, then the sorted keys; the bucket path's 64-bit keys
+  __shared__ uint64_t sbuf[kSmallMax];
+  int* skey = (int*)sbuf;
+  int* sval = skey + kSmallMax;
   const int tid = threadIdx.x, l = lane_id(), w = tid >> 6;
   const int slice = (a.M + kSmallWaves - 1) / kSmallWaves;
   const int wbeg = w * slice;
   const int wend = wbeg + slice < a.M ? wbeg + slice : a.M;
   const uint64_t lt = lanemask_lt();
+  // --- bucket path
+  constexpr int kBuckets = 1024;  // = kSmallThreads: one bucket per thread in the scan
+  constexpr int kBucketMax = 128;
+  static_assert(kBuckets == kSmallThreads && kBuckets <= kMaxRadix, "bucket scan layout");
+  int* bcount = cnt[0];
+  int* bfill = cnt[1];
+  int* bstart = cnt[2];
+  int* bsorted = cnt[3];  // [kSmallMax] (rows 3 .. 10): expert of each sorted position
+  uint64_t* bk = sbuf;  // [kSmallMax]
+  static_assert(3 * kMaxRadix + kSmallMax <= kSmallWaves * kMaxRadix, "bucket arrays fit");
+  const int hb = a.total_bits > 10 ? a.total_bits - 10 : 0;
+  bcount[tid] = 0;
+  bfill[tid] = 0;
+  __syncthreads();
+  uint64_t key64[kSmallRounds];
+#pragma unroll
+  for (int r = 0; r < kSmallRounds; ++r) {
+    const int i = r * kSmallThreads + tid;
+    key64[r] = ~0ull;
+    if (i < a.M) {
+      const uint32_t e = (uint32_t)a.idx[i];
+      key64[r] = ((uint64_t)e << 32) | (uint32_t)i;
+      atomicAdd(&bcount[(e >> hb) & (kBuckets - 1)], 1);
+    }
+  }
+  __syncthreads();
+  {
+    const int c = bcount[tid];
+    const int ex = wave_excl_scan_i32(c);
+    int mx = c;
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) mx = max(mx, __shfl_xor(mx, m, kWave));
+    if (l == kWave - 1) wsum[w] = ex + c;
+    if (l == 0) dsum[w] = mx;
+    __syncthreads();
+    int off = 0, big = 0;
+    for (int ww = 0; ww < kSmallWaves; ++ww) {
+      if (ww < w) off += wsum[ww];
+      big = max(big, dsum[ww]);
+    }
+    bstart[tid] = off + ex;
+    __syncthreads();
+    if (big <= kBucketMax) {  // the same on every thread
+#pragma unroll
+      for (int r = 0; r < kSmallRounds; ++r) {
+        const int i = r * kSmallThreads + tid;
+        if (i < a.M) {
+          const int b = (int)((uint32_t)(key64[r] >> 32) >> hb) & (kBuckets - 1);
+          bk[bstart[b] + atomicAdd(&bfill[b], 1)] = key64[r];
+        }
+      }
+      __syncthreads();
+      // taken in bucket order, so the lanes of a wave mostly scan the same bucket (broadcast
+      // reads); the keys then move to their final places in LDS
+      int fpos[kSmallRounds];
+#pragma unroll
+      for (int r = 0; r < kSmallRounds; ++r) {
+        const int i = r * kSmallThreads + tid;
+        fpos[r] = -1;
+        if (i < a.M) {
+          const uint64_t key = bk[i];
+          key64[r] = key;
+          const int b = (int)((uint32_t)(key >> 32) >> hb) & (kBuckets - 1);
+          const int b0 = bstart[b], n = bcount[b];
+          int rank = 0;
+          for (int q = 0; q < n; ++q) rank += bk[b0 + q] < key ? 1 : 0;
+          fpos[r] = b0 + rank;
+        }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int r = 0; r < kSmallRounds; ++r)
+        if (fpos[r] >= 0) bk[fpos[r]] = key64[r];
+      __syncthreads();
+      small_out_sorted(a, bk, bsorted, wsum);
+      return;
+    }
+  }
+  // --- radix path (a crowded bucket)
   int shift = 0;
   for (int ps = 0; ps < a.passes; ++ps) {
     const bool last = ps == a.passes - 1;
@@ -587,35 +747,7 @@ __global__ __launch_bounds__(kSmallThreads) void schedule_small_kernel(SmallSche
     __syncthreads();
     shift += bits;
   }
-  // segment heads: each thread owns up to 8 consecutive sorted positions (keys in LDS)
-  const int per_t = (a.M + kSmallThreads - 1) / kSmallThreads;
-  const int b0 = tid * per_t;
-  int heads = 0;
-  for (int i = b0; i < b0 + per_t && i < a.M; ++i) heads += (i == 0 || skey[i] != skey[i - 1]);
-  const int ex = wave_excl_scan_i32(heads);
-  if (l == kWave - 1) wsum[w] = ex + heads;
-  __syncthreads();
-  int off = 0, tot = 0;
-  for (int ww = 0; ww < kSmallWaves; ++ww) {
-    const int v = wsum[ww];
-    if (ww < w) off += v;
-    tot += v;
-  }
-  int pos = off + ex;
-  for (int i = b0; i < b0 + per_t && i < a.M; ++i) {
-    if (i == 0 || skey[i] != skey[i - 1]) {
-      if (pos < a.cap) {
-        a.active[pos] = skey[i];
-        a.offsets[pos] = i;
-      }
-      ++pos;
-    }
-  }
-  if (tid == 0) {
-    const int n = tot < a.cap ? tot : a.cap;
-    *a.n_active = n;
-    a.offsets[n] = a.M;
-  }
+  small_heads(a, skey, wsum);
 }
 
 hipError_t launch_fill_i32(int32_t* dst, int64_t n, int32_t value, hipStream_t st) {
