@@ -539,9 +539,10 @@ hipError_t launch_expert_dot(const Shape& s, const void* x, const void* u, const
   a.hk = s.hk;
   a.act = s.act;
   a.nchunks = s.bf16 ? s.d / 8 : s.d / 4;
-  // About 64 tasks per wave when there are plenty; fewer (down to 16) so that small batches
-  // still spread over the GPU.
-  a.range = s.M >= 131072 ? 64 : (s.M >= 65536 ? 32 : 16);
+  // About 64 tasks per wave when there are plenty; fewer (down to one) so that small batches
+  // still give at least 2048 waves.
+  a.range = 64;
+  while (a.range > 1 && s.M < (int64_t)a.range * 2048) a.range >>= 1;
   const int64_t waves = (s.M + a.range - 1) / a.range;
   dim3 grid((unsigned)((waves + 3) / 4));
   const int cpl = chunks_per_lane(a.nchunks);
