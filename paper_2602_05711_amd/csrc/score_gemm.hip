@@ -300,12 +300,13 @@ __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
 // For T <= 64 (decode): the work is reading the sub-keys once. A workgroup owns 32 keys of one
 // half for all (<= 64) tokens; its four waves split d_key in four quarters, load MFMA operand
 // fragments straight from global memory (no LDS staging), and run v_mfma_f32_32x32x16_bf16 on
-// a 64 x 32 tile each; the four partial tiles are then added through LDS in wave order, so the
-// sum order is fixed. Requires d_key % 256 == 0 (each wave's quarter is a multiple of 64).
+// a 32·RB x 32 tile each (RB = 1 row block when T <= 32, else 2); the four partial tiles are then
+// added through LDS in wave order, so the sum order is fixed. Requires d_key % 256 == 0 (each
+// wave's quarter is a multiple of 64).
 
 constexpr int SK_N = 32;
 
-template <bool ACC>
+template <bool ACC, int RB>
 __global__ __launch_bounds__(256) void score_bf16_skinny_kernel(ScoreArgs a) {
   const int half = blockIdx.y;
   const int ncols = a.H * a.nh[half];
@@ -318,9 +319,9 @@ __global__ __launch_bounds__(256) void score_bf16_skinny_kernel(ScoreArgs a) {
   const int kq = a.dk / 4;  // this wave's k range: [wid * kq, (wid + 1) * kq)
   const int frow = lane & 31, fk = (lane >> 5) * 8;
   // operand rows: tokens 0..63 (clamped to T - 1) and keys n0 .. n0 + 63 (clamped)
-  const uint16_t* pa[2];
+  const uint16_t* pa[RB];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < RB; ++i) {
     int64_t m = i * 32 + frow;
     if (m >= a.T) m = a.T - 1;
     pa[i] = X + m * a.d + wid * kq + fk;
@@ -328,24 +329,24 @@ __global__ __launch_bounds__(256) void score_bf16_skinny_kernel(ScoreArgs a) {
   int n = n0 + frow;
   if (n >= ncols) n = ncols - 1;
   const uint16_t* pb = Kt + (int64_t)n * a.dk + wid * kq + fk;
-  f32x16 acc[2];
+  f32x16 acc[RB];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < RB; ++i)
 #pragma unroll
     for (int q = 0; q < 16; ++q) acc[i][q] = 0.f;
   // four k steps of 16 in flight per iteration
   for (int k = 0; k < kq; k += 64) {
-    bf16x8 fa[4][2], fb[4];
+    bf16x8 fa[4][RB], fb[4];
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
 #pragma unroll
-      for (int i = 0; i < 2; ++i) fa[s][i] = *(const bf16x8*)(pa[i] + k + 16 * s);
+      for (int i = 0; i < RB; ++i) fa[s][i] = *(const bf16x8*)(pa[i] + k + 16 * s);
       fb[s] = *(const bf16x8*)(pb + k + 16 * s);
     }
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < RB; ++i)
         acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s], acc[i], 0, 0, 0);
   }
   // tile element (row, col) of a 32 x 32 block: register q, lane l with
@@ -353,7 +354,7 @@ __global__ __launch_bounds__(256) void score_bf16_skinny_kernel(ScoreArgs a) {
   const int c = lane & 31;
   if (wid > 0) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < RB; ++i)
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const int r = i * 32 + (q >> 2) * 8 + (lane >> 5) * 4 + (q & 3);
@@ -364,7 +365,7 @@ __global__ __launch_bounds__(256) void score_bf16_skinny_kernel(ScoreArgs a) {
   if (wid == 0 && n0 + c < ncols) {
     const int64_t oc = out_col(a, half, n0 + c);
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < RB; ++i)
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const int r = i * 32 + (q >> 2) * 8 + (lane >> 5) * 4 + (q & 3);
@@ -454,10 +455,14 @@ hipError_t launch_score(const Shape& s, const void* x, const void* keys_row,
   const int ncols = s.H * (s.nr > s.nc ? s.nr : s.nc);
   if (s.bf16 && s.T <= 64 && s.dk % 256 == 0) {
     dim3 grid((ncols + SK_N - 1) / SK_N, 2);
-    if (accumulate)
-      hipLaunchKernelGGL(score_bf16_skinny_kernel<true>, grid, dim3(256), 0, st, a);
+    if (accumulate && s.T > 32)
+      hipLaunchKernelGGL((score_bf16_skinny_kernel<true, 2>), grid, dim3(256), 0, st, a);
+    else if (accumulate)
+      hipLaunchKernelGGL((score_bf16_skinny_kernel<true, 1>), grid, dim3(256), 0, st, a);
+    else if (s.T > 32)
+      hipLaunchKernelGGL((score_bf16_skinny_kernel<false, 2>), grid, dim3(256), 0, st, a);
     else
-      hipLaunchKernelGGL(score_bf16_skinny_kernel<false>, grid, dim3(256), 0, st, a);
+      hipLaunchKernelGGL((score_bf16_skinny_kernel<false, 1>), grid, dim3(256), 0, st, a);
   } else if (s.bf16 && s.dk % LK == 0) {
     dim3 grid((ncols + LN - 1) / LN, (unsigned)((s.T + LM - 1) / LM), 2);
     if (accumulate)
