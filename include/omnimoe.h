@@ -44,7 +44,7 @@ extern "C" {
 typedef enum {
   OMNIMOE_OK = 0,
   OMNIMOE_ERR_INVALID_ARG = 1, /* a size is out of range or a required pointer is NULL */
-  OMNIMOE_ERR_UNSUPPORTED = 2, /* valid layer, but outside what this build implements */
+  OMNIMOE_ERR_UNSUPPORTED = 2, /* valid layer, but outside what the library implements */
   OMNIMOE_ERR_ALIGNMENT = 3,   /* a pointer is not 16-byte aligned */
   OMNIMOE_ERR_WORKSPACE = 4,   /* workspace smaller than omnimoe_workspace_size() */
   OMNIMOE_ERR_HIP = 5          /* the HIP runtime reported an error at launch */

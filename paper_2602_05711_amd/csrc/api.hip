@@ -195,7 +195,7 @@ const char* omnimoe_status_string(int32_t status) {
   switch (status) {
     case OMNIMOE_OK: return "ok";
     case OMNIMOE_ERR_INVALID_ARG: return "invalid argument";
-    case OMNIMOE_ERR_UNSUPPORTED: return "unsupported by this build";
+    case OMNIMOE_ERR_UNSUPPORTED: return "unsupported by the library";
     case OMNIMOE_ERR_ALIGNMENT: return "pointer not 16-byte aligned";
     case OMNIMOE_ERR_WORKSPACE: return "workspace too small";
     case OMNIMOE_ERR_HIP: return "HIP runtime error";
