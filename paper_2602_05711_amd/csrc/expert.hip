@@ -268,20 +268,22 @@ __global__ __launch_bounds__(256) void accumulate_kernel(AccArgs a) {
   }
 }
 
-// Few tokens: a workgroup owns one (token, column split) and its four waves take a quarter of
-// the token's slots each; the three later quarters' partial sums go through LDS and wave 0 adds
-// them in wave order, so the per-element order is fixed.
-template <int CPL, bool BF16>
-__global__ __launch_bounds__(256) void accumulate_slots_kernel(AccArgs a) {
+// Few tokens: a workgroup of W waves owns one (token, column split); wave w takes the w-th
+// of W equal runs of the token's slots, so that all of a wave's v rows are in flight at once.
+// The waves' partial rows go through LDS (in y order) and are added in wave order, so the
+// per-element order is fixed.
+template <int W, int CPL, bool BF16>
+__global__ __launch_bounds__(64 * W) void accumulate_slots_kernel(AccArgs a) {
   constexpr int EPC = BF16 ? 8 : 4;
   constexpr int UNROLL = CPL >= 16 ? 2 : (CPL >= 8 ? 4 : 8);
-  __shared__ float part[3][CPL * EPC * kWave];
+  constexpr int ROW = CPL * EPC * kWave;  // floats of one wave's partial row
+  __shared__ __attribute__((aligned(16))) float part[W][ROW];
   const int l = lane_id(), w = threadIdx.x >> 6;
   const uint4* V = (const uint4*)a.v;
   const int64_t row_chunks = a.nchunks;
-  const int quarter = (a.hk + 3) / 4;
-  const int s_lo = w * quarter;
-  const int s_hi = s_lo + quarter < a.hk ? s_lo + quarter : a.hk;
+  const int per = (a.hk + W - 1) / W;
+  const int s_lo = w * per < a.hk ? w * per : a.hk;
+  const int s_hi = s_lo + per < a.hk ? s_lo + per : a.hk;
   for (int64_t u = blockIdx.x; u < a.T * a.splits; u += gridDim.x) {
     const int64_t t = u / a.splits;
     const int cbase = (int)(u % a.splits) * CPL * kWave;
@@ -337,28 +339,21 @@ __global__ __launch_bounds__(256) void accumulate_slots_kernel(AccArgs a) {
         }
       }
     }
-    if (w > 0) {
+    // Wave w's partial row in y order: chunk l + 64 q of the split at floats (l + 64 q) EPC.
 #pragma unroll
-      for (int q = 0; q < CPL; ++q)
+    for (int q = 0; q < CPL; ++q)
 #pragma unroll
-        for (int k = 0; k < EPC; ++k) part[w - 1][(q * EPC + k) * kWave + l] = acc[q][k];
-    }
+      for (int k = 0; k < EPC; k += 4)
+        *(float4*)&part[w][(l + kWave * q) * EPC + k] =
+            make_float4(acc[q][k], acc[q][k + 1], acc[q][k + 2], acc[q][k + 3]);
     __syncthreads();
-    if (w == 0) {
-      float4* yt = (float4*)(a.y + t * a.d);
+    const int nc = a.nchunks - cbase < CPL * kWave ? a.nchunks - cbase : CPL * kWave;
+    float* yt = a.y + t * a.d + (int64_t)cbase * EPC;
+    for (int j = threadIdx.x; j < nc * EPC; j += 64 * W) {
+      float r = part[0][j];
 #pragma unroll
-      for (int q = 0; q < CPL; ++q) {
-        if (!cvalid[q]) continue;
-        float r[EPC];
-#pragma unroll
-        for (int k = 0; k < EPC; ++k) {
-          const int o = (q * EPC + k) * kWave + l;
-          r[k] = ((acc[q][k] + part[0][o]) + part[1][o]) + part[2][o];
-        }
-        const int c = cbase + l + kWave * q;
-#pragma unroll
-        for (int k = 0; k < EPC; k += 4) yt[(c * EPC + k) / 4] = make_float4(r[k], r[k + 1], r[k + 2], r[k + 3]);
-      }
+      for (int ww = 1; ww < W; ++ww) r += part[ww][j];
+      yt[j] = r;
     }
     __syncthreads();
   }
@@ -488,14 +483,24 @@ hipError_t dispatch_dot(int cpl, dim3 grid, hipStream_t st, const DotArgs& a) {
   return hipGetLastError();
 }
 
+// Sixteen waves per workgroup when a wave holds at most two chunks of a row (registers for
+// eight rows in flight, at most 64 KiB of partial rows in LDS) and each wave still gets a few
+// slots; four otherwise.
 template <bool BF16>
-hipError_t dispatch_acc_slots(int cpl, dim3 grid, hipStream_t st, const AccArgs& a) {
+hipError_t dispatch_acc_slots(int cpl, int hk, dim3 grid, hipStream_t st, const AccArgs& a) {
+  if (cpl <= 2 && hk >= 64) {
+    if (cpl == 1)
+      hipLaunchKernelGGL((accumulate_slots_kernel<16, 1, BF16>), grid, dim3(1024), 0, st, a);
+    else
+      hipLaunchKernelGGL((accumulate_slots_kernel<16, 2, BF16>), grid, dim3(1024), 0, st, a);
+    return hipGetLastError();
+  }
   switch (cpl) {
-    case 1: hipLaunchKernelGGL((accumulate_slots_kernel<1, BF16>), grid, dim3(256), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((accumulate_slots_kernel<2, BF16>), grid, dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((accumulate_slots_kernel<4, BF16>), grid, dim3(256), 0, st, a); break;
-    case 8: hipLaunchKernelGGL((accumulate_slots_kernel<8, BF16>), grid, dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL((accumulate_slots_kernel<16, BF16>), grid, dim3(256), 0, st, a); break;
+    case 1: hipLaunchKernelGGL((accumulate_slots_kernel<4, 1, BF16>), grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((accumulate_slots_kernel<4, 2, BF16>), grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((accumulate_slots_kernel<4, 4, BF16>), grid, dim3(256), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((accumulate_slots_kernel<4, 8, BF16>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((accumulate_slots_kernel<4, 16, BF16>), grid, dim3(256), 0, st, a); break;
   }
   return hipGetLastError();
 }
@@ -569,11 +574,11 @@ hipError_t launch_accumulate(const Shape& s, const void* v, const int32_t* idx, 
   a.splits = splits;
   const int cpl = chunks_per_lane((a.nchunks + splits - 1) / splits);
   if (s.T * splits < 1024 && s.hk >= 16) {
-    // still few waves: a workgroup per (token, column split), slots shared by its four waves
+    // still few waves: a workgroup per (token, column split), slots shared by its waves
     const int64_t units = s.T * splits;
     const dim3 grid((unsigned)(units < 16384 ? units : 16384));
-    return s.bf16 ? dispatch_acc_slots<true>(cpl, grid, st, a)
-                  : dispatch_acc_slots<false>(cpl, grid, st, a);
+    return s.bf16 ? dispatch_acc_slots<true>(cpl, s.hk, grid, st, a)
+                  : dispatch_acc_slots<false>(cpl, s.hk, grid, st, a);
   }
   int64_t blocks = (s.T * splits + 3) / 4;
   if (blocks > 16384) blocks = 16384;

@@ -356,7 +356,7 @@ def test_expert_forward(name):
 def test_token_centric_ablation(name):
     # Without the schedule: within tolerance of the oracle, and equal to the scheduled path (same
     # dot, activation and slot-order sum). Below 1024 tokens the scheduled path adds each
-    # token's slots in four partial sums, so there the two agree to rounding only.
+    # token's slots in several partial sums, so there the two agree to rounding only.
     say(f"[token-centric] {name}")
     w, dev, idx, g32, perm, y_ref = _expert_case(name)
     d = B.make_desc(w)
