@@ -15,6 +15,7 @@
 // active_offsets[q B] still marks where group q starts.
 // Everything is integer arithmetic; the LDS atomics only count.
 #include <algorithm>
+#include <climits>
 
 #include "device_common.hpp"
 #include "internal.hpp"
@@ -496,6 +497,12 @@ struct SmallSched {
   int M;
   int cap;
   int passes, per, total_bits;
+  // after schedule_ranges_kernel (G > 0): its staged heads, placed here unless a range overflowed
+  const int32_t* stage_act;
+  const int32_t* stage_off;
+  const int32_t* range_base;
+  const int32_t* range_heads;
+  int G;
 };
 
 // Segment heads of the sorted keys in LDS (expert of each sorted position): each thread owns up
@@ -574,6 +581,150 @@ __device__ void small_out_sorted(const SmallSched& a, const uint64_t* keys, int*
   small_heads(a, sorted_lds, wsum);
 }
 
+// ---------------------------------------------------------------- range-partitioned small sort
+// Up to 8192 tasks over many compute units (decode with tens of tokens): workgroup r owns the
+// experts [r N / G, (r + 1) N / G). It reads every task id, counts the tasks of lower ranges
+// (its first sorted position) and gathers its own (expert, task) keys into LDS; each key's
+// place is the number of smaller keys (keys are distinct). It writes its stretch of perm and
+// of the sorted experts, and stages its segment heads. schedule_small_kernel then places the
+// staged heads (an exclusive scan over the G head counts) with one workgroup. A range that
+// holds more than kRangeCap tasks (heavy skew, few experts) reports -1, and
+// schedule_small_kernel then sorts everything itself.
+constexpr int kRangeThreads = 1024;
+constexpr int kRangeCap = 1024;
+constexpr int kRangeTasks = 256;  // nominal tasks per range under uniform routing
+constexpr int kRangeMinTasks = 4096;  // up to this many tasks: schedule_small_kernel alone
+constexpr int kRangeLoads = kSmallMax / kRangeThreads;  // task ids per thread
+static_assert(kSmallMax / kRangeTasks <= kWave, "range head counts scanned by one wave");
+
+struct RangeSched {
+  const int32_t* idx;
+  int32_t* sorted;       // [M] expert of each sorted position
+  int32_t* perm;         // [M]
+  int32_t* stage_act;    // [M] heads of range r from range_base[r] on: expert
+  int32_t* stage_off;    // [M] ... and its first sorted position
+  int32_t* range_base;   // [G] tasks in lower ranges
+  int32_t* range_heads;  // [G] heads in the range, -1 when it held more than kRangeCap tasks
+  int64_t N;
+  int M;
+  int G;
+};
+
+// Exclusive scan of one int per thread over a workgroup of kRangeThreads; *total gets the sum.
+__device__ __forceinline__ int range_block_scan(int v, int* wsum, int* total) {
+  const int l = lane_id(), w = threadIdx.x >> 6;
+  const int ex = wave_excl_scan_i32(v);
+  if (l == kWave - 1) wsum[w] = ex + v;
+  __syncthreads();
+  int off = 0, tot = 0;
+#pragma unroll
+  for (int ww = 0; ww < kRangeThreads / kWave; ++ww) {
+    off += ww < w ? wsum[ww] : 0;
+    tot += wsum[ww];
+  }
+  __syncthreads();
+  *total = tot;
+  return off + ex;
+}
+
+__global__ __launch_bounds__(kRangeThreads) void schedule_ranges_kernel(RangeSched a) {
+  // gathered keys in any order (padded with ~0 to a multiple of eight), then in order
+  __shared__ __attribute__((aligned(16))) uint64_t keys[kRangeCap + 8];
+  __shared__ uint64_t sorted[kRangeCap];
+  __shared__ int rk[kRangeCap];
+  __shared__ int wsum[kRangeThreads / kWave];
+  const int tid = threadIdx.x, l = lane_id();
+  const int r = blockIdx.x;
+  const int64_t lo = (int64_t)r * a.N / a.G, hi = (int64_t)(r + 1) * a.N / a.G;
+  int e[kRangeLoads];
+#pragma unroll
+  for (int u = 0; u < kRangeLoads; ++u) {
+    const int i = u * kRangeThreads + tid;
+    e[u] = i < a.M ? a.idx[i] : INT_MAX;
+  }
+  // own keys: counted per wave with ballots, a scan over the waves, then written in place
+  int below = 0, own = 0;
+#pragma unroll
+  for (int u = 0; u < kRangeLoads; ++u) {
+    const int i = u * kRangeThreads + tid;
+    below += (i < a.M && e[u] < lo) ? 1 : 0;
+    own += __popcll(__ballot(i < a.M && e[u] >= lo && e[u] < hi));
+  }
+  // one scan for both counts: the wave's own keys (from lane 0) above bit 16, the thread's
+  // lower-range tasks below it (each total is at most 8192)
+  int tot;
+  const int ex = range_block_scan((l == 0 ? own << 16 : 0) + below, wsum, &tot);
+  const int n = tot >> 16, n_below = tot & 0xFFFF;
+  const int wbase = ex >> 16;
+  if (n > kRangeCap) {
+    if (tid == 0) a.range_heads[r] = -1;
+    return;
+  }
+  for (int j = tid; j < n; j += kRangeThreads) rk[j] = 0;
+  const uint64_t lt = lanemask_lt();
+  int pos = __shfl(wbase, 0, kWave);
+#pragma unroll
+  for (int u = 0; u < kRangeLoads; ++u) {
+    const int i = u * kRangeThreads + tid;
+    const bool mine = i < a.M && e[u] >= lo && e[u] < hi;
+    const uint64_t bal = __ballot(mine);
+    if (mine) keys[pos + __popcll(bal & lt)] = ((uint64_t)(uint32_t)e[u] << 32) | (uint32_t)i;
+    pos += __popcll(bal);
+  }
+  const int n8 = (n + 7) & ~7;
+  if (tid < n8 - n) keys[n + tid] = ~0ull;
+  __syncthreads();
+  // place of key j: the number of smaller keys, counted by four threads over a quarter of the
+  // keys each (eight per step, 16-byte broadcast reads) and added up in LDS
+  constexpr int kParts = 4, kPerPass = kRangeThreads / kParts;
+  const int part = tid / kPerPass;
+  const int qlen = ((n8 / 8 + kParts - 1) / kParts) * 8;
+  const int q0 = part * qlen < n8 ? part * qlen : n8;
+  const int q1 = q0 + qlen < n8 ? q0 + qlen : n8;
+  for (int j0 = 0; j0 < n; j0 += kPerPass) {
+    const int j = j0 + tid % kPerPass;
+    const uint64_t kj = j < n ? keys[j] : 0ull;
+    int rank = 0;
+    for (int q = q0; q < q1; q += 8) {
+      const ulonglong2 k0 = *(const ulonglong2*)&keys[q];
+      const ulonglong2 k1 = *(const ulonglong2*)&keys[q + 2];
+      const ulonglong2 k2 = *(const ulonglong2*)&keys[q + 4];
+      const ulonglong2 k3 = *(const ulonglong2*)&keys[q + 6];
+      rank += (k0.x < kj) + (k0.y < kj) + (k1.x < kj) + (k1.y < kj) + (k2.x < kj) +
+              (k2.y < kj) + (k3.x < kj) + (k3.y < kj);
+    }
+    if (j < n && rank > 0) atomicAdd(&rk[j], rank);
+  }
+  __syncthreads();
+  for (int j = tid; j < n; j += kRangeThreads) sorted[rk[j]] = keys[j];
+  __syncthreads();
+  for (int j = tid; j < n; j += kRangeThreads) {
+    const uint64_t k = sorted[j];
+    a.perm[n_below + j] = (int32_t)(uint32_t)k;
+    a.sorted[n_below + j] = (int32_t)(k >> 32);
+  }
+  // segment heads: thread t owns positions [t per, (t + 1) per)
+  const int per = (n + kRangeThreads - 1) / kRangeThreads;
+  const int j0 = tid * per;
+  const int j1 = j0 + per < n ? j0 + per : n;
+  int heads = 0;
+  for (int j = j0; j < j1; ++j)
+    heads += (j == 0 || (sorted[j] >> 32) != (sorted[j - 1] >> 32)) ? 1 : 0;
+  int n_heads;
+  int h = range_block_scan(heads, wsum, &n_heads);
+  for (int j = j0; j < j1; ++j) {
+    if (j == 0 || (sorted[j] >> 32) != (sorted[j - 1] >> 32)) {
+      a.stage_act[n_below + h] = (int32_t)(sorted[j] >> 32);
+      a.stage_off[n_below + h] = n_below + j;
+      ++h;
+    }
+  }
+  if (tid == 0) {
+    a.range_base[r] = n_below;
+    a.range_heads[r] = n_heads;
+  }
+}
+
 __global__ __launch_bounds__(kSmallThreads) void schedule_small_kernel(SmallSched a) {
   __shared__ int cnt[kSmallWaves][kMaxRadix];
   __shared__ int dsum[kMaxRadix];
@@ -587,6 +738,41 @@ __global__ __launch_bounds__(kSmallThreads) void schedule_small_kernel(SmallSche
   const int wbeg = w * slice;
   const int wend = wbeg + slice < a.M ? wbeg + slice : a.M;
   const uint64_t lt = lanemask_lt();
+  if (a.G > 0) {
+    // place the heads staged by schedule_ranges_kernel, unless a range overflowed
+    const int hv = tid < a.G ? a.range_heads[tid] : 0;
+    const int bv = tid < a.G ? a.range_base[tid] : 0;
+    if (!__syncthreads_or(hv < 0)) {
+      // workgroup r places range r's heads after the heads of ranges 0 .. r-1
+      const int r = blockIdx.x;
+      const int ex = wave_excl_scan_i32(hv);
+      if (l == kWave - 1) wsum[w] = ex + hv;
+      if (tid == r) {
+        cnt[0][0] = hv;
+        cnt[0][1] = bv;
+        cnt[0][2] = ex;  // G <= 64: the scan within wave 0 is the whole scan
+      }
+      __syncthreads();
+      int tot = 0;
+      for (int ww = 0; ww < kSmallWaves; ++ww) tot += wsum[ww];
+      const int nh = cnt[0][0], src = cnt[0][1], dst = cnt[0][2];
+      for (int j = tid; j < nh; j += kSmallThreads) {
+        const int va = a.stage_act[src + j], vo = a.stage_off[src + j];
+        if (dst + j < a.cap) {
+          a.active[dst + j] = va;
+          a.offsets[dst + j] = vo;
+        }
+      }
+      if (r != 0) return;
+      if (tid == 0) {
+        const int n = tot < a.cap ? tot : a.cap;
+        *a.n_active = n;
+        a.offsets[n] = a.M;
+      }
+      return;
+    }
+    if (blockIdx.x != 0) return;
+  }
   // --- bucket path
   constexpr int kBuckets = 1024;  // = kSmallThreads: one bucket per thread in the scan
   constexpr int kBucketMax = 128;
@@ -862,7 +1048,30 @@ hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, in
     a.passes = passes;
     a.per = per;
     a.total_bits = total_bits;
-    hipLaunchKernelGGL(schedule_small_kernel, dim3(1), dim3(kSmallThreads), 0, st, a);
+    a.G = 0;
+    if (M > kRangeMinTasks) {
+      RangeSched r;
+      r.idx = idx;
+      r.sorted = b.k0;
+      r.perm = perm;
+      r.stage_act = b.v0;
+      r.stage_off = b.k1;
+      r.G = (int)((M + kRangeTasks - 1) / kRangeTasks);
+      r.range_base = b.v1;
+      r.range_heads = b.v1 + r.G;
+      r.N = s.N;
+      r.M = (int)M;
+      hipLaunchKernelGGL(schedule_ranges_kernel, dim3(r.G), dim3(kRangeThreads), 0, st, r);
+      a.stage_act = r.stage_act;
+      a.stage_off = r.stage_off;
+      a.range_base = r.range_base;
+      a.range_heads = r.range_heads;
+      a.G = r.G;
+    }
+    // with ranges: one workgroup per range places its heads; only workgroup 0 sorts when a
+    // range overflowed
+    hipLaunchKernelGGL(schedule_small_kernel, dim3(a.G > 0 ? a.G : 1), dim3(kSmallThreads), 0, st,
+                       a);
     *sorted_keys = b.k0;
   } else {
     const int32_t* sk = nullptr;

@@ -170,6 +170,10 @@ SCHEDULE_CASES = [
     (16384, 8, 16, 1024, 1024, "uniform"), (16384, 8, 16, 1024, 1024, "zipf"),
     (64, 8, 16, 1024, 1024, "uniform"), (1, 8, 16, 1024, 1024, "zipf"),
     (5000, 2, 3, 4096, 4096, "uniform"),
+    # 4097 .. 8192 tasks: expert ranges over several workgroups, and the fallback when one
+    # range holds too many tasks (few experts, skew)
+    (64, 8, 16, 1024, 1024, "zipf"), (256, 8, 4, 2, 2, "zipf"), (40, 8, 16, 64, 64, "uniform"),
+    (256, 8, 3, 1, 3, "uniform"), (33, 8, 16, 1024, 1024, "uniform"),
 ]
 
 
