@@ -6,7 +6,9 @@
 //
 // bf16, d_key % 64 == 0: 256 x 256 tile, four waves of 128 x 128 on v_mfma_f32_32x32x16_bf16,
 //   operands copied global -> LDS without registers (two 64 KiB stages, XOR-swizzled rows);
-// bf16, at most 64 tokens and d_key % 256 == 0: a split-K skinny kernel (decode);
+// bf16, at most 64 tokens, d_key % 256 == 0: a split-K decode kernel with the token rows in LDS
+//   (8 or more tokens, d_key <= 1024), else a split-K skinny kernel with operands straight from
+//   memory;
 // bf16 otherwise: 128 x 128 tile, four waves of 64 x 64 on v_mfma_f32_16x16x32_bf16, LDS
 //   double buffer fed through registers;
 // fp32: a VALU FMA tile kernel (the fp32 layer is small; fp32 MFMA would change rounding).
@@ -376,6 +378,106 @@ __global__ __launch_bounds__(256) void score_bf16_skinny_kernel(ScoreArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- decode bf16 kernel
+// For T <= 64 and d_key <= 1024 (decode): a workgroup owns 64 keys of one half and copies the
+// half's token rows (32·RB rows of d_key, RB = 1 when T <= 32, else 2) into LDS with coalesced
+// 16-byte loads straight to LDS. Wave w takes key block w % 2 (32 keys) over quarter w / 2 of
+// d_key: it requests all its key fragments from memory at once, before the token copy is
+// waited for, then runs v_mfma_f32_32x32x16_bf16 with the token fragments read from LDS. The
+// four quarters' partial tiles are added through LDS in quarter order, so the sum order is
+// fixed. LDS row r holds its 16-byte chunk c at c ^ (r % 16) within each group of sixteen, so
+// the sixteen rows read by a quarter-wave fall in distinct banks. Requires d_key % 256 == 0.
+
+constexpr int DC_KEYS = 64;
+constexpr int DC_WAVES = 8;
+
+size_t decode_lds_bytes(int dk, int rb) {
+  const size_t xb = (size_t)rb * 32 * dk * 2;                 // token rows
+  const size_t pb = (size_t)6 * rb * 32 * 32 * sizeof(float);  // partial tiles of quarters 1-3
+  return xb > pb ? xb : pb;
+}
+
+template <bool ACC, int RB>
+__global__ __launch_bounds__(64 * DC_WAVES) void score_bf16_decode_kernel(ScoreArgs a) {
+  const int half = blockIdx.y;
+  const int ncols = a.H * a.nh[half];
+  const int n0 = blockIdx.x * DC_KEYS;
+  if (n0 >= ncols) return;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const uint16_t* X = (const uint16_t*)a.x + a.col0[half];
+  const uint16_t* Kt = (const uint16_t*)a.keys[half];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int kb = wid & 1, qi = wid >> 1;
+  const int kq = a.dk / 4;
+  const int steps = kq / 16;  // 4, 8, 12 or 16
+  const int frow = lane & 31;
+  // this wave's key fragments, all in flight
+  int n = n0 + kb * 32 + frow;
+  if (n >= ncols) n = ncols - 1;
+  const uint16_t* pb = Kt + (int64_t)n * a.dk + qi * kq + (lane >> 5) * 8;
+  bf16x8 fb[16];
+#pragma unroll
+  for (int s = 0; s < 16; ++s)
+    if (s < steps) fb[s] = *(const bf16x8*)(pb + 16 * s);
+  // token rows into LDS: 16-byte position p holds row p / cpr, chunk (p % cpr) ^ (row % 16)
+  const int cpr = a.dk / 8;
+  const int npos = RB * 32 * cpr;
+  for (int q = wid; q * kWave < npos; q += DC_WAVES) {
+    const int p = q * kWave + lane;
+    const int r = p / cpr;
+    const int c = (p - r * cpr) ^ (r & 15);
+    int64_t m = r < a.T ? r : a.T - 1;
+    __builtin_amdgcn_global_load_lds((const void*)(X + m * a.d + c * 8),
+                                     (lds_ptr_t)(smem + (size_t)q * kWave * 16), 16, 0, 0);
+  }
+  wait_vm0();
+  __syncthreads();
+  f32x16 acc[RB];
+#pragma unroll
+  for (int i = 0; i < RB; ++i)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[i][e] = 0.f;
+  const int c0 = qi * kq / 8 + (lane >> 5);  // logical chunk of step 0
+#pragma unroll
+  for (int s = 0; s < 16; ++s) {
+    if (s < steps) {
+#pragma unroll
+      for (int i = 0; i < RB; ++i) {
+        const int r = i * 32 + frow;
+        const int ph = (c0 + 2 * s) ^ (r & 15);
+        const bf16x8 fa = *(const bf16x8*)(smem + ((size_t)r * cpr + ph) * 16);
+        acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb[s], acc[i], 0, 0, 0);
+      }
+    }
+  }
+  __syncthreads();  // the token rows are no longer needed: the space takes the partial tiles
+  float* part = (float*)smem;  // [quarter - 1][key block][32 RB rows][32 keys]
+  const int c = lane & 31;
+  if (qi > 0) {
+#pragma unroll
+    for (int i = 0; i < RB; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int r = i * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
+        part[(((qi - 1) * 2 + kb) * RB * 32 + r) * 32 + c] = acc[i][e];
+      }
+  }
+  __syncthreads();
+  if (qi == 0 && n0 + kb * 32 + c < ncols) {
+    const int64_t oc = out_col(a, half, n0 + kb * 32 + c);
+#pragma unroll
+    for (int i = 0; i < RB; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int r = i * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
+        float v = acc[i][e];
+#pragma unroll
+        for (int qq = 0; qq < 3; ++qq) v += part[((qq * 2 + kb) * RB * 32 + r) * 32 + c];
+        if (r < a.T) store_out<ACC>(a, (int64_t)r * a.ldo + oc, v);
+      }
+  }
+}
+
 constexpr int FT = 64, FK = 16;
 
 template <bool ACC>
@@ -453,7 +555,20 @@ hipError_t launch_score(const Shape& s, const void* x, const void* keys_row,
   a.per_head = s.nr + s.nc;
   a.ldo = (int64_t)s.H * (s.nr + s.nc);
   const int ncols = s.H * (s.nr > s.nc ? s.nr : s.nc);
-  if (s.bf16 && s.T <= 64 && s.dk % 256 == 0) {
+  if (s.bf16 && s.T >= 8 && s.T <= 64 && s.dk % 256 == 0 && s.dk <= 1024) {
+    dim3 grid((ncols + DC_KEYS - 1) / DC_KEYS, 2);
+    const int rb = s.T > 32 ? 2 : 1;
+    const size_t lds = decode_lds_bytes(s.dk, rb);
+    const dim3 block(64 * DC_WAVES);
+    if (accumulate && rb == 2)
+      hipLaunchKernelGGL((score_bf16_decode_kernel<true, 2>), grid, block, lds, st, a);
+    else if (accumulate)
+      hipLaunchKernelGGL((score_bf16_decode_kernel<true, 1>), grid, block, lds, st, a);
+    else if (rb == 2)
+      hipLaunchKernelGGL((score_bf16_decode_kernel<false, 2>), grid, block, lds, st, a);
+    else
+      hipLaunchKernelGGL((score_bf16_decode_kernel<false, 1>), grid, block, lds, st, a);
+  } else if (s.bf16 && s.T <= 64 && s.dk % 256 == 0) {
     dim3 grid((ncols + SK_N - 1) / SK_N, 2);
     if (accumulate && s.T > 32)
       hipLaunchKernelGGL((score_bf16_skinny_kernel<true, 2>), grid, dim3(256), 0, st, a);

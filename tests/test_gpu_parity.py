@@ -52,6 +52,8 @@ SHAPES = {
                                   H=3, K=7),
     "skinny1_bf16": synth.Workload("skinny1_bf16", T=1, d=1024, n_rows=48, n_cols=80, d_key=512,
                                    H=2, K=12),
+    "decode8_bf16": synth.Workload("decode8_bf16", T=8, d=2048, n_rows=100, n_cols=36,
+                                   d_key=1024, H=2, K=9),
     # K > 64 (workgroup-per-row selection), incl. the paper's benchmark grid 320 x 320, K = 512
     "k256_bf16": synth.Workload("k256_bf16", T=100, d=256, n_rows=64, n_cols=64, d_key=64, H=2,
                                 K=256),
