@@ -219,20 +219,18 @@ __device__ __forceinline__ int half_survivors(const float (&v)[R], int n, int kh
   }
   const uint32_t theta = kth_largest_lane(mx, kh);
   *theta_out = theta;
-  // Compaction: every lane counts its survivors, an exclusive scan over lanes gives each lane
-  // its first slot, and the lane writes its survivors in order (the sort that follows makes
-  // the slot order irrelevant).
-  int mine = 0;
-#pragma unroll
-  for (int k = 0; k < R; ++k) mine += o[k] >= theta ? 1 : 0;
-  int pos = wave_excl_scan_i32(mine);
-  const int total = __shfl(pos + mine, kWave - 1, kWave);
+  // Compaction, register position by register position: a ballot gives the position's
+  // survivors, each writes at the running count plus the number of lower lanes that also
+  // survive (the sort that follows makes the slot order irrelevant).
+  int total = 0;  // the same on every lane
 #pragma unroll
   for (int k = 0; k < R; ++k) {
-    if (o[k] >= theta) {
-      if (pos < 32) buf[pos] = logit_key(o[k], elem_index<R, VEC>(k));
-      ++pos;
-    }
+    const bool sv = o[k] >= theta;
+    const uint64_t m = __ballot(sv);
+    const int pos = total + (int)__builtin_amdgcn_mbcnt_hi(
+                                (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+    if (sv && pos < 32) buf[pos] = logit_key(o[k], elem_index<R, VEC>(k));
+    total += __popcll(m);
   }
   return total;
 }
