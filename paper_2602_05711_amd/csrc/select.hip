@@ -32,7 +32,9 @@ struct SelectArgs {
 };
 
 // ---------------------------------------------------------------- cross-lane exchange
-// x[l ^ J] for one 32-bit word: DPP for J < 16, ds_swizzle for 16, ds_bpermute for 32.
+// x[l ^ J] for one 32-bit word: DPP for J < 16; for 16 and 32 the lane-half swaps of gfx950
+// (v_permlane16_swap / v_permlane32_swap of the word with itself leave x[l ^ J] in one of the
+// two results, chosen by lane), so no exchange goes through LDS.
 template <int J>
 __device__ __forceinline__ uint32_t xor_lane(uint32_t v) {
   const int x = (int)v;
@@ -47,10 +49,27 @@ __device__ __forceinline__ uint32_t xor_lane(uint32_t v) {
   } else if constexpr (J == 8) {
     return (uint32_t)__builtin_amdgcn_update_dpp(x, x, 0x128, 0xF, 0xF, false);  // row_ror:8
   } else if constexpr (J == 16) {
-    return (uint32_t)__builtin_amdgcn_ds_swizzle(x, (16 << 10) | 0x1F);  // bitmask xor 16
+    // results: rows (0, 0, 2, 2) and rows (1, 1, 3, 3) of 16 lanes
+    const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+    return (lane_id() & 16) ? r[0] : r[1];
   } else {
-    return (uint32_t)__shfl_xor(x, J, kWave);
+    static_assert(J == 32, "xor_lane: J is a power of two below 64");
+    // results: lanes (0-31, 0-31) and lanes (32-63, 32-63)
+    const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return (lane_id() & 32) ? r[0] : r[1];
   }
+}
+
+// Sum over the wave by a butterfly of xor exchanges (32, 16, ..., 1); every lane receives the
+// same value, as the two partners of each level add the same two partial sums.
+__device__ __forceinline__ float wave_sum_xor(float v) {
+  v += __uint_as_float(xor_lane<32>(__float_as_uint(v)));
+  v += __uint_as_float(xor_lane<16>(__float_as_uint(v)));
+  v += __uint_as_float(xor_lane<8>(__float_as_uint(v)));
+  v += __uint_as_float(xor_lane<4>(__float_as_uint(v)));
+  v += __uint_as_float(xor_lane<2>(__float_as_uint(v)));
+  v += __uint_as_float(xor_lane<1>(__float_as_uint(v)));
+  return v;
 }
 
 template <int J>
@@ -337,9 +356,10 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
     wave_lds_sync();
     // Gates: softmax over the K selected scores, best first.
     const double s = f64_from_ord(best.s);
-    const double s0 = __shfl(s, 0, kWave);
+    const double s0 = f64_from_ord(((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(best.s >> 32), 0) << 32) |
+                                   (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)best.s, 0));
     const float e = (l < K) ? expf((float)(s - s0)) : 0.0f;
-    const float z = wave_sum_f32(e);
+    const float z = wave_sum_xor(e);
     if (l < K) {
       a.idx[row * K + l] = (int32_t)(0xFFFFFFFFu - best.nn);
       a.gates[row * K + l] = e / z;
@@ -812,7 +832,7 @@ __global__ __launch_bounds__(NT, NT == 256 ? 5 : 4) void select_large_kernel(Lar
     float part = 0.0f;
     for (int q = g0; q < g0 + per && q < K; ++q)
       part += expf((float)(f64_from_ord(sel_s[q]) - s0));
-    part = wave_sum_f32(part);
+    part = wave_sum_xor(part);
     if (l == 0) sh.wsum[w] = part;
     __syncthreads();
     float z = sh.wsum[0];
@@ -902,7 +922,7 @@ __global__ __launch_bounds__(256) void select_dense_kernel(DenseArgs a) {
       const float v = f32_from_ord((uint32_t)(best >> 32));
       const float v0 = __shfl(v, 0, kWave);
       const float e = (l < K) ? expf(v - v0) : 0.0f;
-      const float z = wave_sum_f32(e);
+      const float z = wave_sum_xor(e);
       if (l < K) {
         a.idx[row * K + l] = (int32_t)(0xFFFFFFFFu - (uint32_t)best);
         a.gates[row * K + l] = e / z;
