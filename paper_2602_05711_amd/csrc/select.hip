@@ -177,19 +177,25 @@ __device__ __forceinline__ uint64_t logit_key(uint32_t ord, int j) {
   return ((uint64_t)ord << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)j);
 }
 
-// A threshold th with at least k lanes holding a value >= th, at most the k-th largest lane
-// value: a bitwise search with ballots for the k-th largest value that leaves the lowest
-// kLowBits bits at zero. Those bits only move th by less than 2^kLowBits ordered steps, so at
-// most a few extra logits survive; the selection stays exact.
+// For each of two halves, a threshold th with at least k lanes holding a value >= th, at most
+// the k-th largest lane value: a bitwise search with ballots for the k-th largest value that
+// leaves the lowest kLowBits bits at zero. Those bits only move th by less than 2^kLowBits
+// ordered steps, so at most a few extra logits survive; the selection stays exact. Both halves'
+// searches run in one loop (two independent chains, so their latencies overlap).
 constexpr int kLowBits = 8;
-__device__ __forceinline__ uint32_t kth_largest_lane(uint32_t v, int k) {
-  uint32_t th = 0u;
+__device__ __forceinline__ void kth_largest_lane2(uint32_t va, int ka, uint32_t vb, int kb,
+                                                  uint32_t* tha, uint32_t* thb) {
+  uint32_t ta = 0u, tb = 0u;
 #pragma unroll
   for (int b = 31; b >= kLowBits; --b) {
-    const uint32_t c = th | (1u << b);
-    if (__popcll(__ballot(v >= c)) >= k) th = c;
+    const uint32_t ca = ta | (1u << b), cb = tb | (1u << b);
+    const int na = __popcll(__ballot(va >= ca));
+    const int nb = __popcll(__ballot(vb >= cb));
+    if (na >= ka) ta = ca;
+    if (nb >= kb) tb = cb;
   }
-  return th;
+  *tha = ta;
+  *thb = tb;
 }
 
 // Logits of one half held in registers. VEC: lane l holds 16-byte chunks, element
@@ -223,12 +229,9 @@ __device__ __forceinline__ void load_half(const float* __restrict__ p, int n, fl
   }
 }
 
-// Finds one half's threshold and writes the survivors' keys to buf[0, 32). Returns the number
-// of survivors (those beyond 32 are not written).
+// Order keys of one half's logits in registers and their lane maximum.
 template <int R, bool VEC, bool FULL>
-__device__ __forceinline__ int half_survivors(const float (&v)[R], int n, int kh, uint64_t* buf,
-                                              uint32_t* theta_out) {
-  uint32_t o[R];
+__device__ __forceinline__ uint32_t half_keys(const float (&v)[R], int n, uint32_t (&o)[R]) {
   uint32_t mx = 0u;
 #pragma unroll
   for (int k = 0; k < R; ++k) {
@@ -236,11 +239,16 @@ __device__ __forceinline__ int half_survivors(const float (&v)[R], int n, int kh
     o[k] = (FULL || elem_index<R, VEC>(k) < n) ? ord_f32(v[k]) : 0u;
     mx = o[k] > mx ? o[k] : mx;
   }
-  const uint32_t theta = kth_largest_lane(mx, kh);
-  *theta_out = theta;
-  // Compaction, register position by register position: a ballot gives the position's
-  // survivors, each writes at the running count plus the number of lower lanes that also
-  // survive (the sort that follows makes the slot order irrelevant).
+  return mx;
+}
+
+// Writes the keys of one half's logits >= theta to buf[0, 32) and returns their number (those
+// beyond 32 are not written). Register position by register position: a ballot gives the
+// position's survivors, each writes at the running count plus the number of lower lanes that
+// also survive (the sort that follows makes the slot order irrelevant).
+template <int R, bool VEC>
+__device__ __forceinline__ int half_survivors(const uint32_t (&o)[R], uint32_t theta,
+                                              uint64_t* buf) {
   int total = 0;  // the same on every lane
 #pragma unroll
   for (int k = 0; k < R; ++k) {
@@ -315,9 +323,12 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
       load_half<R, VEC, FULL>(a.hs + nxt * (int64_t)(a.nr + a.nc), a.nr, nr_);
       load_half<R, VEC, FULL>(a.hs + nxt * (int64_t)(a.nr + a.nc) + a.nr, a.nc, nc_);
     }
-    uint32_t th_r, th_c;
-    const int cr = half_survivors<R, VEC, FULL>(vr, a.nr, kr, st, &th_r);
-    const int cc = half_survivors<R, VEC, FULL>(vc, a.nc, kc, st + 32, &th_c);
+    uint32_t o_r[R], o_c[R], th_r, th_c;
+    const uint32_t mx_r = half_keys<R, VEC, FULL>(vr, a.nr, o_r);
+    const uint32_t mx_c = half_keys<R, VEC, FULL>(vc, a.nc, o_c);
+    kth_largest_lane2(mx_r, kr, mx_c, kc, &th_r, &th_c);
+    const int cr = half_survivors<R, VEC>(o_r, th_r, st);
+    const int cc = half_survivors<R, VEC>(o_c, th_c, st + 32);
     wave_lds_sync();
     if (cr <= 32 && cc <= 32) {
       // Both halves in one pass: rows sort in lanes 0-31, columns in lanes 32-63.
