@@ -8,7 +8,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libomnimoe.so")
 SOURCES = ["api.hip", "score_gemm.hip", "select.hip", "schedule.hip", "expert.hip", "grouped.hip",
-           "mlp.hip", "backward.hip"]
+           "mlp.hip", "backward.hip", "dense.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

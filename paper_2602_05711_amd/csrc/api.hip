@@ -88,6 +88,16 @@ bool grouped_supported(const Shape& s) { return s.bf16 && s.d % 64 == 0; }
 bool layer_grouped(const Shape& s) { return s.B > 1 && grouped_supported(s); }
 
 // Schedule workspace, followed by the grouped plan's (which reads the schedule's sorted keys).
+// The routed sum y_t = sum of a_p v_e over t's tasks: one dense GEMM over all experts when
+// the pairs are dense enough (Eq. 14 with a single group), else the token-major slot-order
+// kernel. dense_ws holds dense_accumulate_ws_bytes(s) bytes.
+hipError_t routed_sum(const Shape& s, const void* v, const int32_t* idx, const float* abuf,
+                      float* y, void* dense_ws, hipStream_t st) {
+  if (omnimoe::dense_accumulate(s))
+    return omnimoe::launch_dense_accumulate(s, v, idx, abuf, y, dense_ws, st);
+  return omnimoe::launch_accumulate(s, v, idx, abuf, y, st);
+}
+
 size_t sched_or_plan_bytes(const Shape& s) {
   const size_t sb = omnimoe::schedule_ws_bytes(s.M, s.N);
   return layer_grouped(s) ? sb + omnimoe::group_plan_ws_bytes(s) : sb;
@@ -98,16 +108,19 @@ size_t stage_bytes(const Shape& s, int stage) {
     case OMNIMOE_STAGE_ROUTE: return hs_bytes(s);
     case OMNIMOE_STAGE_SELECT: return 0;
     case OMNIMOE_STAGE_SCHEDULE: return omnimoe::schedule_ws_bytes(s.M, s.N);
-    case OMNIMOE_STAGE_EXPERT: return m_bytes(s);
+    case OMNIMOE_STAGE_EXPERT: return m_bytes(s) + omnimoe::dense_accumulate_ws_bytes(s);
     case OMNIMOE_STAGE_ROUTE_DENSE: return dense_bytes(s);
     case OMNIMOE_STAGE_EXPERT_BACKWARD: return omnimoe::backward_ws_bytes(s.M);
     case OMNIMOE_STAGE_ROUTE_BACKWARD: return omnimoe::route_backward_ws_bytes(s);
-    case OMNIMOE_STAGE_EXPERT_GROUPED: return m_bytes(s) + omnimoe::group_plan_ws_bytes(s);
+    case OMNIMOE_STAGE_EXPERT_GROUPED:  // the plan is dead once the grouped dot has run
+      return m_bytes(s) + std::max(omnimoe::group_plan_ws_bytes(s),
+                                   omnimoe::dense_accumulate_ws_bytes(s));
     default: {
       // idx, gates, perm, active, active_offsets, n_active, then the logits (dead after
-      // selection) overlapped with the sort buffers and the a[] buffer.
+      // selection) overlapped with the sort buffers, the a[] buffer and the dense routed sum's
+      // buffers.
       size_t fixed = 3 * m_bytes(s) + 2 * active_bytes(s) + 256;
-      size_t late = sched_or_plan_bytes(s) + m_bytes(s);
+      size_t late = sched_or_plan_bytes(s) + m_bytes(s) + omnimoe::dense_accumulate_ws_bytes(s);
       return fixed + std::max(hs_bytes(s), late);
     }
   }
@@ -181,7 +194,7 @@ omnimoe_status layer_impl(const omnimoe_layer_desc* desc, const void* x, const v
     return hip_status(e);
   }
   mark(4);
-  if ((e = omnimoe::launch_accumulate(s, v, idx, abuf, y, strm))) return hip_status(e);
+  if ((e = routed_sum(s, v, idx, abuf, y, (char*)abuf + m_bytes(s), strm))) return hip_status(e);
   mark(5);
   if (timer) ++timer->used;
   return OMNIMOE_OK;
@@ -382,7 +395,7 @@ omnimoe_status omnimoe_expert_forward(const omnimoe_layer_desc* desc, const void
   hipStream_t strm = (hipStream_t)stream;
   float* abuf = (float*)ws;
   hipError_t e = omnimoe::launch_expert_dot(s, x, u, idx, gates, perm, nullptr, abuf, strm);
-  if (e == hipSuccess) e = omnimoe::launch_accumulate(s, v, idx, abuf, y, strm);
+  if (e == hipSuccess) e = routed_sum(s, v, idx, abuf, y, (char*)ws + m_bytes(s), strm);
   return hip_status(e);
 }
 
@@ -406,7 +419,7 @@ omnimoe_status omnimoe_expert_forward_grouped(const omnimoe_layer_desc* desc, co
                                             (char*)ws + m_bytes(s), &plan, strm);
   if (e == hipSuccess)
     e = omnimoe::launch_grouped_dot(s, x, u, gates, perm, active, n_active, plan, abuf, strm);
-  if (e == hipSuccess) e = omnimoe::launch_accumulate(s, v, idx, abuf, y, strm);
+  if (e == hipSuccess) e = routed_sum(s, v, idx, abuf, y, (char*)ws + m_bytes(s), strm);
   return hip_status(e);
 }
 

@@ -1,0 +1,166 @@
+// The second product of Eq. 14 as one dense GEMM over all experts, for layers whose routed
+// pairs are dense (one head, K a sizeable fraction of N): y = A V with A[t, e] = a_p for the
+// task p of token t routed to expert e and zero elsewhere, i.e. Eq. 14 with all experts in a
+// single group. A is built in bf16 (a_p rounded to nearest even), V is transposed once so that
+// the expert dimension is contiguous, the product runs on the MFMA logit kernel split over the
+// expert dimension, and the split partials are added in split order, so y is deterministic.
+// With one head the K experts of a token are distinct, so each A[t, e] is a single a_p.
+#include "device_common.hpp"
+#include "internal.hpp"
+
+namespace omnimoe {
+namespace {
+
+constexpr int kDenseChunk = 32768;  // columns of A built at a time (64 KiB of LDS)
+constexpr int kDenseSlots = 16;     // a token's slots held per thread (hk <= 4096)
+
+// Row t of A: the token's K (expert, a) pairs are loaded once into registers; then, chunk by
+// chunk of columns, the chunk is zeroed in LDS, the pairs that fall in it are placed, and it
+// is written out with 16-byte stores.
+__global__ __launch_bounds__(256) void densify_kernel(const int32_t* __restrict__ idx,
+                                                      const float* __restrict__ a,
+                                                      uint16_t* __restrict__ A, int hk,
+                                                      int64_t N, int64_t kpad) {
+  __shared__ __attribute__((aligned(16))) uint16_t row[kDenseChunk];
+  const int64_t t = blockIdx.x;
+  const int tid = threadIdx.x;
+  int e[kDenseSlots];
+  uint16_t v[kDenseSlots];
+#pragma unroll
+  for (int q = 0; q < kDenseSlots; ++q) {
+    const int j = q * 256 + tid;
+    e[q] = j < hk ? idx[t * hk + j] : -1;
+    v[q] = j < hk ? bf16_rne(a[t * hk + j]) : (uint16_t)0;
+  }
+  uint4* dst_row = (uint4*)(A + t * kpad);
+  for (int64_t c0 = 0; c0 < kpad; c0 += kDenseChunk) {
+    for (int i = tid; i < kDenseChunk / 8; i += 256) ((uint4*)row)[i] = make_uint4(0, 0, 0, 0);
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kDenseSlots; ++q) {
+      const int64_t c = (int64_t)e[q] - c0;
+      if (e[q] >= 0 && e[q] < N && c >= 0 && c < kDenseChunk) row[c] = v[q];
+    }
+    __syncthreads();
+    const int64_t n = kpad - c0 < kDenseChunk ? kpad - c0 : kDenseChunk;  // a multiple of 64
+    for (int i = tid; i < n / 8; i += 256) dst_row[c0 / 8 + i] = ((const uint4*)row)[i];
+    __syncthreads();
+  }
+}
+
+// Vt[c, e] = V[e, c] for e < N, zero for N <= e < kpad; 64 x 64 tiles through LDS, 16-byte
+// loads (eight d values of one expert) and 16-byte stores (eight experts of one d index).
+__global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __restrict__ V,
+                                                             uint16_t* __restrict__ Vt,
+                                                             int64_t N, int d, int64_t kpad) {
+  __shared__ uint16_t tile[64][72];  // [expert][d index], rows padded to 144 bytes
+  const int64_t e0 = (int64_t)blockIdx.x * 64;
+  const int c0 = blockIdx.y * 64;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int i = q * 256 + tid;  // 512 chunks: expert i / 8, d indices 8 (i % 8) .. + 7
+    const int r = i >> 3, k = (i & 7) * 8;
+    const int64_t e = e0 + r;
+    uint4 x = make_uint4(0, 0, 0, 0);
+    if (e < N) x = *(const uint4*)(V + e * d + c0 + k);
+    *(uint4*)&tile[r][k] = x;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int i = q * 256 + tid;  // 512 chunks: d index i / 8, experts 8 (i % 8) .. + 7
+    const int c = i >> 3, k = (i & 7) * 8;
+    uint16_t w[8];
+#pragma unroll
+    for (int m = 0; m < 8; ++m) w[m] = tile[k + m][c];
+    const uint4 o = make_uint4((uint32_t)w[0] | ((uint32_t)w[1] << 16),
+                               (uint32_t)w[2] | ((uint32_t)w[3] << 16),
+                               (uint32_t)w[4] | ((uint32_t)w[5] << 16),
+                               (uint32_t)w[6] | ((uint32_t)w[7] << 16));
+    if (e0 + k < kpad) *(uint4*)(Vt + (int64_t)(c0 + c) * kpad + e0 + k) = o;
+  }
+}
+
+// y[i] = sum over splits z = 0, 1, ... of part[z][i], four elements per thread.
+__global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restrict__ part,
+                                                            float* __restrict__ y, int64_t n4,
+                                                            int splits, int64_t stride4) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4;
+       i += (int64_t)gridDim.x * 256) {
+    float4 s = ((const float4*)part)[i];
+    for (int z = 1; z < splits; ++z) {
+      const float4 p = ((const float4*)part)[z * stride4 + i];
+      s.x += p.x;
+      s.y += p.y;
+      s.z += p.z;
+      s.w += p.w;
+    }
+    ((float4*)y)[i] = s;
+  }
+}
+
+struct DensePlan {
+  int splits;
+  int kchunk;
+  int64_t kpad;
+};
+
+DensePlan dense_plan(const Shape& s) {
+  const int64_t tiles = ((s.T + 255) / 256) * (((int64_t)s.d + 255) / 256);
+  int64_t splits = (512 + tiles - 1) / tiles;
+  const int64_t max_splits = (s.N + 511) / 512;  // at least eight 64-wide k steps per split
+  if (splits > max_splits) splits = max_splits;
+  if (splits < 1) splits = 1;
+  DensePlan p;
+  p.splits = (int)splits;
+  p.kchunk = (int)(((s.N + splits * 64 - 1) / (splits * 64)) * 64);
+  p.kpad = (int64_t)p.kchunk * splits;
+  return p;
+}
+
+size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+}  // namespace
+
+bool dense_accumulate(const Shape& s) {
+  return s.bf16 && s.H == 1 && s.d % 64 == 0 && s.hk <= 256 * kDenseSlots &&
+         (int64_t)s.K * kDenseRatio >= s.N;
+}
+
+size_t dense_accumulate_ws_bytes(const Shape& s) {
+  if (!dense_accumulate(s)) return 0;
+  const DensePlan p = dense_plan(s);
+  size_t b = align256((size_t)s.T * p.kpad * 2);              // A
+  b += align256((size_t)s.d * p.kpad * 2);                    // V transposed
+  if (p.splits > 1) b += align256((size_t)p.splits * s.T * s.d * 4);  // split partials
+  return b;
+}
+
+hipError_t launch_dense_accumulate(const Shape& s, const void* v, const int32_t* idx,
+                                   const float* abuf, float* y, void* ws, hipStream_t st) {
+  if (s.T == 0) return hipSuccess;
+  const DensePlan p = dense_plan(s);
+  char* w = (char*)ws;
+  uint16_t* A = (uint16_t*)w;
+  w += align256((size_t)s.T * p.kpad * 2);
+  uint16_t* Vt = (uint16_t*)w;
+  w += align256((size_t)s.d * p.kpad * 2);
+  float* part = p.splits > 1 ? (float*)w : y;
+  hipLaunchKernelGGL(densify_kernel, dim3((unsigned)s.T), dim3(256), 0, st, idx, abuf, A, s.hk,
+                     s.N, p.kpad);
+  hipLaunchKernelGGL(transpose_bf16_kernel, dim3((unsigned)(p.kpad / 64), (unsigned)(s.d / 64)),
+                     dim3(256), 0, st, (const uint16_t*)v, Vt, s.N, s.d, p.kpad);
+  hipError_t e = launch_gemm_splitk(s.T, s.d, A, p.kpad, Vt, p.kpad, p.kchunk, p.splits, part, st);
+  if (e != hipSuccess) return e;
+  if (p.splits > 1) {
+    const int64_t n4 = s.T * (int64_t)s.d / 4;
+    int64_t blocks = (n4 + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    hipLaunchKernelGGL(reduce_splits_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
+                       (const float*)part, y, n4, p.splits, n4);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace omnimoe

@@ -35,6 +35,20 @@ hipError_t launch_score(const Shape& s, const void* x, const void* keys_row,
 hipError_t launch_swiglu(int64_t T, int d_ff, bool bf16, const float* h, void* a,
                          hipStream_t st);
 
+// Split-K bf16 product (fp32 out): out[z][m, n] = sum over k in [z kchunk, (z + 1) kchunk) of
+// A[m, k] B[n, k], A [M, lda] and B [N, ldb] row-major, kchunk a multiple of 64, z < splits;
+// partial z at out + z M N.
+hipError_t launch_gemm_splitk(int64_t M, int N, const void* A, int64_t lda, const void* B,
+                              int64_t ldb, int kchunk, int splits, float* out, hipStream_t st);
+
+// The second product of Eq. 14 as one dense GEMM (all experts in one group), taken when
+// dense_accumulate(s): bf16, one head, d % 64 == 0, K <= 4096 and K * kDenseRatio >= N.
+constexpr int64_t kDenseRatio = 64;
+bool dense_accumulate(const Shape& s);
+size_t dense_accumulate_ws_bytes(const Shape& s);  // 0 when not taken
+hipError_t launch_dense_accumulate(const Shape& s, const void* v, const int32_t* idx,
+                                   const float* abuf, float* y, void* ws, hipStream_t st);
+
 // Per-half top-K, Cartesian merge and gates from fp32 half-scores.
 hipError_t launch_select(const Shape& s, const float* half_scores, int32_t* idx, float* gates,
                          hipStream_t st);

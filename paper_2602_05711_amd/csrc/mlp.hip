@@ -8,14 +8,6 @@
 namespace omnimoe {
 namespace {
 
-// fp32 -> bf16 bits, round to nearest even (NaN stays NaN).
-__device__ __forceinline__ uint16_t bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x40u);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
-
 // Four features per thread: h row t holds the d_ff gate values then the d_ff up values.
 template <bool BF16>
 __global__ __launch_bounds__(256) void swiglu_kernel(const float* __restrict__ h, void* a,

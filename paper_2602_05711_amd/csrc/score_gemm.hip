@@ -36,6 +36,10 @@ struct ScoreArgs {
   int out_off[2];   // column offset of each half inside one (t, h) output row
   int per_head;     // nr + nc
   int64_t ldo;      // H * (nr + nc)
+  // split-K (large kernel only): grid z is the split; split z covers k in [z kchunk, (z + 1)
+  // kchunk) of half 0 and writes its partial product at out + z part_stride
+  int kchunk;
+  int64_t part_stride;
 };
 
 // One output element (ACC: added to what is there). Each element is written by exactly one
@@ -181,16 +185,18 @@ __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 
 __device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
-template <bool ACC>
+template <bool ACC, bool SPLIT = false>
 __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
-  const int half = blockIdx.z;
+  const int half = SPLIT ? 0 : blockIdx.z;
   const int ncols = a.H * a.nh[half];
   const int n0 = blockIdx.x * LN;
   if (n0 >= ncols) return;
   const int64_t m0 = (int64_t)blockIdx.y * LM;
-  const uint16_t* X = (const uint16_t*)a.x;
-  const uint16_t* Kt = (const uint16_t*)a.keys[half];
+  const int64_t kbase = SPLIT ? (int64_t)blockIdx.z * a.kchunk : 0;
+  const uint16_t* X = (const uint16_t*)a.x + kbase;
+  const uint16_t* Kt = (const uint16_t*)a.keys[half] + kbase;
   const int c0 = a.col0[half];
+  [[maybe_unused]] float* const out = SPLIT ? a.out + (int64_t)blockIdx.z * a.part_stride : a.out;
 
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int tid = threadIdx.x;
@@ -235,7 +241,7 @@ __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
 
-  const int KT = a.dk / LK;
+  const int KT = (SPLIT ? a.kchunk : a.dk) / LK;
   issue(0, 0);
   wait_vm0();
   __syncthreads();
@@ -292,7 +298,10 @@ __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const int64_t m = m0 + wm * 128 + i * 32 + (q >> 2) * 8 + (lane >> 5) * 4 + (q & 3);
-        if (m < a.T) store_out<ACC>(a, m * a.ldo + oc, acc[i][j][q]);
+        if (m < a.T) {
+          if constexpr (SPLIT) out[m * a.ldo + oc] = acc[i][j][q];
+          else store_out<ACC>(a, m * a.ldo + oc, acc[i][j][q]);
+        }
       }
     }
   }
@@ -554,6 +563,8 @@ hipError_t launch_score(const Shape& s, const void* x, const void* keys_row,
   a.out_off[1] = s.nr;
   a.per_head = s.nr + s.nc;
   a.ldo = (int64_t)s.H * (s.nr + s.nc);
+  a.kchunk = 0;
+  a.part_stride = 0;
   const int ncols = s.H * (s.nr > s.nc ? s.nr : s.nc);
   if (s.bf16 && s.T >= 8 && s.T <= 64 && s.dk % 256 == 0 && s.dk <= 1024) {
     dim3 grid((ncols + DC_KEYS - 1) / DC_KEYS, 2);
@@ -597,6 +608,33 @@ hipError_t launch_score(const Shape& s, const void* x, const void* keys_row,
     else
       hipLaunchKernelGGL(score_f32_kernel<false>, grid, dim3(256), 0, st, a);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_splitk(int64_t M, int N, const void* A, int64_t lda, const void* B,
+                              int64_t ldb, int kchunk, int splits, float* out, hipStream_t st) {
+  if (M == 0 || N == 0) return hipSuccess;
+  ScoreArgs a;
+  a.x = A;
+  a.keys[0] = B;
+  a.keys[1] = B;
+  a.out = out;
+  a.T = M;
+  a.d = (int)lda;
+  a.dk = (int)ldb;
+  a.H = 1;
+  a.nh[0] = N;
+  a.nh[1] = 0;
+  a.col0[0] = 0;
+  a.col0[1] = 0;
+  a.out_off[0] = 0;
+  a.out_off[1] = 0;
+  a.per_head = N;
+  a.ldo = N;
+  a.kchunk = kchunk;
+  a.part_stride = M * (int64_t)N;
+  dim3 grid((N + LN - 1) / LN, (unsigned)((M + LM - 1) / LM), splits);
+  hipLaunchKernelGGL((score_bf16_large_kernel<false, true>), grid, dim3(256), 2 * LSTAGE, st, a);
   return hipGetLastError();
 }
 

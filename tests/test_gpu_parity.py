@@ -59,6 +59,12 @@ SHAPES = {
                                 K=256),
     "paper_k512_bf16": synth.Workload("paper_k512_bf16", T=256, d=1024, n_rows=320, n_cols=320,
                                       d_key=512, H=1, K=512),
+    # one head with K >= N / 64: the routed sum as one dense GEMM over all experts (Eq. 14 with
+    # a single group); split over the expert dimension, N not a multiple of the split width
+    "dense_bf16": synth.Workload("dense_bf16", T=300, d=256, n_rows=32, n_cols=32, d_key=64, H=1,
+                                 K=64),
+    "dense_k100_bf16": synth.Workload("dense_k100_bf16", T=77, d=192, n_rows=40, n_cols=50,
+                                      d_key=64, H=1, K=100),
 }
 
 
@@ -381,6 +387,43 @@ def test_token_centric_ablation(name):
         assert np.array_equal(y_tc, y)
     else:
         assert row_rel_err(y_tc, y.astype(np.float64)).max() <= 1e-6
+
+
+@pytest.mark.parametrize("name", ["dense_bf16", "dense_k100_bf16"])
+def test_dense_routed_sum(name):
+    # y = A V with A[t, e] = a_p rounded to bf16: within tolerance of the oracle, the same on a
+    # second run, and within the bf16 rounding of a (plus fp32 sums) of the slot-order sum of
+    # the token-centric kernel, which keeps a in fp32.
+    say(f"[dense routed sum] {name}")
+    w, dev, idx, g32, perm, y_ref = _expert_case(name)
+    d = B.make_desc(w)
+    gi, gg = to_dev(idx), to_dev(g32)
+    y = torch.empty((w.T, w.d), dtype=torch.float32, device="cuda")
+    y2 = torch.empty_like(y)
+    y_tc = torch.empty_like(y)
+    P.omnimoe_expert_forward(d, dev["x"], dev["u"], dev["v"], gi, gg, to_dev(perm), y)
+    P.omnimoe_expert_forward(d, dev["x"], dev["u"], dev["v"], gi, gg, to_dev(perm), y2)
+    P.omnimoe_expert_forward_token_centric(d, dev["x"], dev["u"], dev["v"], gi, gg, y_tc)
+    torch.cuda.synchronize()
+    y, y2, y_tc = y.cpu().numpy(), y2.cpu().numpy(), y_tc.cpu().numpy()
+    assert np.array_equal(y.view(np.uint8), y2.view(np.uint8))
+    err = row_rel_err(y, y_ref)
+    say(f"  max row rel err {err.max():.3e}")
+    assert err.max() <= tol(w)
+    # |a_p| = g_p |act(x_t . u_e)| <= g_p ||x_t|| ||u_e|| (|GELU(z)|, |SiLU(z)| <= |z|)
+    _, f = host_inputs(w)
+    xn = np.linalg.norm(f["x"].astype(np.float64), axis=1)
+    un = np.linalg.norm(f["u"].astype(np.float64), axis=1)
+    va = np.abs(f["v"].astype(np.float64))
+    flat = idx.reshape(w.T, -1)
+    a = g32.reshape(w.T, -1).astype(np.float64) * xn[:, None] * un[flat]
+    mass = np.zeros((w.T, w.d))
+    for j in range(flat.shape[1]):
+        mass += a[:, j:j + 1] * va[flat[:, j]]
+    bound = mass * (2.0 ** -8 + 2 * (flat.shape[1] + 4) * 2.0 ** -24) + 1e-30
+    gap = np.abs(y.astype(np.float64) - y_tc)
+    say(f"  max gap / bound {(gap / bound).max():.3e}")
+    assert np.all(gap <= bound)
 
 
 # ------------------------------------------------------------------ whole layer
