@@ -596,6 +596,48 @@ __device__ __forceinline__ void survivor_hist(LargeShared& sh, const uint64_t* s
   }
 }
 
+// Bitonic merges k = k_lo, 2 k_lo, ..., k_hi (k_hi <= 8) restricted to partner distances below
+// 8, on blocks of eight consecutive keys (block b of k2 / 8 held by one thread in registers):
+// for each merge, distances min(k / 2, 4), ..., 1; keys are ordered descending by (s, n) where
+// (i & k) == 0, ascending elsewhere, as in the LDS levels.
+__device__ __forceinline__ void sort_block8(uint64_t* ks, uint32_t* kn, int k2, int k_lo,
+                                            int k_hi, int tid, int nthreads) {
+  for (int b = tid; b < (k2 >> 3); b += nthreads) {
+    uint64_t s[8];
+    uint32_t n[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      s[q] = ks[8 * b + q];
+      n[q] = kn[8 * b + q];
+    }
+    for (int k = k_lo; k <= k_hi; k <<= 1) {
+#pragma unroll
+      for (int j = 4; j >= 1; j >>= 1) {
+        if (j >= k) continue;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          if (q & j) continue;
+          const bool up = ((8 * b + q) & k) == 0;
+          const bool lt = s[q] < s[q + j] || (s[q] == s[q + j] && n[q] < n[q + j]);
+          if (lt == up) {
+            const uint64_t ts = s[q];
+            s[q] = s[q + j];
+            s[q + j] = ts;
+            const uint32_t tn = n[q];
+            n[q] = n[q + j];
+            n[q + j] = tn;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      ks[8 * b + q] = s[q];
+      kn[8 * b + q] = n[q];
+    }
+  }
+}
+
 // Writes the keep largest of the n distinct keys src[0, n) to dst in descending order: the
 // rank of a key is the number of larger keys. src is padded with 0 to an even length and
 // 16-byte aligned; thread t of NT ranks keys t, t + NT, ...
@@ -814,10 +856,20 @@ __global__ __launch_bounds__(NT, NT == 256 ? 5 : 4) void select_large_kernel(Lar
       }
     }
     __syncthreads();
-    // bitonic sort of the K selected keys, descending by (score, ~id)
-    for (int lk = 1; (1 << lk) <= k2; ++lk) {
+    // bitonic sort of the K selected keys, descending by (score, ~id). With eight waves (2048 keys
+    // or more) the levels with partner distance 8 or more run over LDS, one compare-exchange
+    // per pair, and the last three levels of each merge (distances 4, 2, 1), and the whole of
+    // the first three merges, run on eight consecutive keys held in one thread's registers: one
+    // LDS pass instead of three. With four waves every level runs over LDS (registers are kept
+    // for occupancy there).
+    constexpr int kRegFrom = NT == 512 ? 4 : 1;  // first merge whose low levels use registers
+    if constexpr (NT == 512) {
+      sort_block8(sel_s, sel_n, k2, 2, 8, tid, kLargeThreads);
+      __syncthreads();
+    }
+    for (int lk = kRegFrom; (1 << lk) <= k2; ++lk) {
       const int k = 1 << lk;
-      for (int lj = lk - 1; lj >= 0; --lj) {
+      for (int lj = lk - 1; lj >= (NT == 512 ? 3 : 0); --lj) {
         const int j = 1 << lj;
         for (int t = tid; t < (k2 >> 1); t += kLargeThreads) {
           const int i = ((t >> lj) << (lj + 1)) | (t & (j - 1));
@@ -832,6 +884,10 @@ __global__ __launch_bounds__(NT, NT == 256 ? 5 : 4) void select_large_kernel(Lar
             sel_n[i + j] = xn;
           }
         }
+        __syncthreads();
+      }
+      if constexpr (NT == 512) {
+        sort_block8(sel_s, sel_n, k2, k, k, tid, kLargeThreads);
         __syncthreads();
       }
     }
