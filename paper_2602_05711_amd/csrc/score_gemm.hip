@@ -278,11 +278,15 @@ __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
           fb[c ^ 1][i] = frag(st, b_off[i], ks + 1);
         }
       }
+      // keep the double buffer: the next step's fragment reads are issued before this step's
+      // MFMAs (left alone, the scheduler sinks each read next to its use)
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[c][i], fb[c][j], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
     wait_vm0();
     __syncthreads();
