@@ -10,6 +10,8 @@
 // accumulate: token-major, one wavefront per token. The token's H*K slots are read in
 // (head, k) order, their v rows are fetched eight at a time and y_t += a[p] * v_e is summed in
 // slot order in fp32. The order is fixed, so y is the same on every run; no atomics are used.
+// With too few tokens to fill the chip, a token's row is split over column ranges and its slots
+// over the waves of a workgroup, whose partial rows are added in wave order.
 #include "device_common.hpp"
 #include "internal.hpp"
 

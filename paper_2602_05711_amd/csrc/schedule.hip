@@ -13,6 +13,9 @@
 // being the expert's place in the active list, and a second stable radix sort of the task ids
 // by q gives the order (group, task id). Groups are unions of consecutive experts, so
 // active_offsets[q B] still marks where group q starts.
+// Up to 8192 tasks (decode) take single-launch paths instead: one 16-wave workgroup sorts up to
+// 4096 tasks in LDS; from 4097 to 8192 the tasks are split over workgroups by ranges of expert
+// ids and a second launch places the segment heads (both further down).
 // Everything is integer arithmetic; the LDS atomics only count.
 #include <algorithm>
 #include <climits>
