@@ -168,9 +168,9 @@ omnimoe_status omnimoe_schedule(const omnimoe_layer_desc* desc, const int32_t* i
  * Walks perm expert by expert: each expert's u row is read once per run of its tasks and
  * a[p] = g_p * act(x_t . u_e) is formed for each of them; then every token sums
  * a[p] * v_e over its slots in (head, k) order. When the routed pairs are dense (bf16, H = 1,
- * d % 64 == 0, K * 64 >= N) the sum is instead one dense product y = A V over all experts
- * (Eq. 14 with a single group; A[t, e] = a[p] rounded to bf16), which the workspace size
- * accounts for. No atomics: y is the same on every run. */
+ * d % 64 == 0, K * 64 >= N, T * N * 2 bytes <= 16 GiB) the sum is instead one dense product
+ * y = A V over all experts (Eq. 14 with a single group; A[t, e] = a[p] rounded to bf16), which
+ * the workspace size accounts for. No atomics: y is the same on every run. */
 omnimoe_status omnimoe_expert_forward(const omnimoe_layer_desc* desc, const void* x,
                                       const void* u, const void* v, const int32_t* idx,
                                       const float* gates, const int32_t* perm, float* y,

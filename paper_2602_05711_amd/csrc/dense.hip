@@ -125,7 +125,7 @@ size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 bool dense_accumulate(const Shape& s) {
   return s.bf16 && s.H == 1 && s.d % 64 == 0 && s.hk <= 256 * kDenseSlots &&
-         (int64_t)s.K * kDenseRatio >= s.N;
+         (int64_t)s.K * kDenseRatio >= s.N && (double)s.T * (double)s.N * 2.0 <= kDenseMaxBytes;
 }
 
 size_t dense_accumulate_ws_bytes(const Shape& s) {

@@ -42,8 +42,10 @@ hipError_t launch_gemm_splitk(int64_t M, int N, const void* A, int64_t lda, cons
                               int64_t ldb, int kchunk, int splits, float* out, hipStream_t st);
 
 // The second product of Eq. 14 as one dense GEMM (all experts in one group), taken when
-// dense_accumulate(s): bf16, one head, d % 64 == 0, K <= 4096 and K * kDenseRatio >= N.
+// dense_accumulate(s): bf16, one head, d % 64 == 0, K <= 4096, K * kDenseRatio >= N and the
+// bf16 matrix A [T, N] within kDenseMaxBytes.
 constexpr int64_t kDenseRatio = 64;
+constexpr double kDenseMaxBytes = 16.0 * (1ull << 30);
 bool dense_accumulate(const Shape& s);
 size_t dense_accumulate_ws_bytes(const Shape& s);  // 0 when not taken
 hipError_t launch_dense_accumulate(const Shape& s, const void* v, const int32_t* idx,
