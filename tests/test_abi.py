@@ -96,6 +96,17 @@ def test_workspace_sizes_cover_buffers():
     assert st == OK and grouped >= w.M * 4 + w.N * 4 + 2 * w.M * 4
     st, dense = _ws(d, B.STAGE_ROUTE_DENSE)
     assert st == OK and dense >= w.T * w.H * w.N * 4
+    # one head with K >= N / 64: the routed sum is one dense product, whose bf16 A [T, N] and
+    # V transposed [d, N] live in the expert and layer workspaces
+    p = synth.WORKLOADS["paper_k4096_bf16"]
+    dp = B.make_desc(p)
+    st, ex = _ws(dp, B.STAGE_EXPERT)
+    assert st == OK and ex >= p.M * 4 + p.T * p.N * 2 + p.d * p.N * 2
+    st, lay = _ws(dp, B.STAGE_LAYER)
+    assert st == OK and lay >= ex
+    dp.K = 1024  # below N / 64: the slot-order sum, no dense buffers
+    st, ex2 = _ws(dp, B.STAGE_EXPERT)
+    assert st == OK and ex2 < p.T * p.N * 2
 
 
 def test_entry_points_check_pointers_before_launch():
