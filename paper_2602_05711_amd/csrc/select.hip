@@ -77,6 +77,8 @@ __device__ __forceinline__ uint64_t xor_lane64(uint64_t v) {
   return ((uint64_t)xor_lane<J>((uint32_t)(v >> 32)) << 32) | xor_lane<J>((uint32_t)v);
 }
 
+__device__ __forceinline__ uint64_t max_u64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+
 // 96-bit key of a grid cell: score (order map of the double) then lower id first.
 struct CellKey {
   uint64_t s;
@@ -445,6 +447,8 @@ struct LargeShared {
   int count;         // gathered keys
   int wint[kLargeMaxWaves];
   float wsum[kLargeMaxWaves];
+  uint64_t wmax[kLargeMaxWaves];
+  int pass0;         // first radix pass (the score bytes before it are shared, see step 3)
 };
 
 // Walks one thread's chunk of the flat candidate list, one candidate after the other. The
@@ -767,18 +771,50 @@ __global__ __launch_bounds__(NT, NT == 256 ? 5 : 4) void select_large_kernel(Lar
     walk.cum = cum;
     walk.kr = kr;
     walk.nc = a.nc;
-    // 3. radix select of the K-th largest candidate key, eight bits at a time from the top
-    if (tid == 0) {
-      sh.ts = 0ull;
-      sh.ms = 0ull;
-      sh.tn = 0u;
-      sh.mn = 0u;
-      sh.krem = K;
-      sh.mode = 0;
-      sh.nsurv = 0;
-      sh.count = 0;
+    // 3. radix select of the K-th largest candidate key, eight bits at a time from the top.
+    // The leading score bytes that every key at or above the threshold shares are skipped: the
+    // largest score is row rank 0 plus column rank 0, and any A x B corner of the sorted grid
+    // with A B >= K holds K cells at or above its last cell, so r[A - 1] + c[B - 1] is at most
+    // the K-th largest score. All keys between the two share their common leading bytes, and no
+    // key lies above the largest, so the search starts below those bytes with krem = K.
+    {
+      const int amin = (K + kc - 1) / kc;
+      uint64_t lo = 0ull;
+      for (int A = amin + tid; A <= kr; A += kLargeThreads) {
+        const int Bn = (K + A - 1) / A;  // <= kc
+        const double v = (double)f32_from_ord((uint32_t)(hk[A - 1] >> 32)) +
+                         (double)f32_from_ord((uint32_t)(hk[n2 + Bn - 1] >> 32));
+        const uint64_t o = ord_f64(v);
+        lo = o > lo ? o : lo;
+      }
+      lo = max_u64(lo, xor_lane64<32>(lo));
+      lo = max_u64(lo, xor_lane64<16>(lo));
+      lo = max_u64(lo, xor_lane64<8>(lo));
+      lo = max_u64(lo, xor_lane64<4>(lo));
+      lo = max_u64(lo, xor_lane64<2>(lo));
+      lo = max_u64(lo, xor_lane64<1>(lo));
+      if (l == 0) sh.wmax[w] = lo;
+      __syncthreads();
+      if (tid == 0) {
+        for (int ww = 1; ww < kLargeWaves; ++ww) lo = sh.wmax[ww] > lo ? sh.wmax[ww] : lo;
+        const uint64_t hi = ord_f64((double)f32_from_ord((uint32_t)(hk[0] >> 32)) +
+                                    (double)f32_from_ord((uint32_t)(hk[n2] >> 32)));
+        const uint64_t diff = hi ^ lo;
+        const int same = diff == 0ull ? 8 : (int)(__clzll((long long)diff) >> 3);
+        const uint64_t mask = same == 0 ? 0ull : (same == 8 ? ~0ull : ~0ull << (64 - 8 * same));
+        sh.ts = hi & mask;
+        sh.ms = mask;
+        sh.pass0 = same;
+        sh.tn = 0u;
+        sh.mn = 0u;
+        sh.krem = K;
+        sh.mode = 0;
+        sh.nsurv = 0;
+        sh.count = 0;
+      }
+      __syncthreads();
     }
-    int pass = 0;
+    int pass = sh.pass0;
     for (; pass < 12; ++pass) {
       for (int i = tid; i < 256; i += kLargeThreads) sh.hist[i] = 0u;
       __syncthreads();
