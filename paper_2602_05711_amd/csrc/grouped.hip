@@ -22,7 +22,8 @@
 // Tiles are numbered group by group (slot tiles major, expert tiles fastest), so consecutive
 // tiles share their token rows and the group's u rows stay in the XCD's L2; each XCD takes one
 // contiguous range of tiles and each workgroup a contiguous run inside it, so the group search
-// is done once per workgroup and then advances.
+// is done once per workgroup and then advances. With groups of up to 64 experts and six or more
+// slot tiles per group on average the XCDs split the tiles by token range instead (below).
 #include "device_common.hpp"
 #include "internal.hpp"
 
@@ -97,10 +98,9 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_dot_kernel(GroupedDotArgs
   const int per_block = (per_xcd + blocks_per_xcd - 1) / blocks_per_xcd;
   const int t_lo = x_lo + (blockIdx.x / kXcds) * per_block;
   const int t_hi = min(x_hi, t_lo + per_block);
-  if (t_lo >= t_hi) return;
-  // group of the first tile: the last q < ng with grp_tile[q] <= t_lo
-  int q;
-  {
+  // group of the first tile (contiguous mapping): the last q < ng with grp_tile[q] <= t_lo
+  int q = 0;
+  if (t_lo < t_hi) {
     int lo = 0, hi = (int)ng - 1;
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
@@ -112,15 +112,12 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_dot_kernel(GroupedDotArgs
   const int fk = l >> 5;  // 16-byte chunk within a 16-wide k step
   const int sw = swz(frow);
   const int KT = a.d / kK;
-  for (int tile = t_lo; tile < t_hi; ++tile) {
-    while (q + 1 < ng && a.grp_tile[q + 1] <= tile) ++q;
+  // One work tile: slot tile stl and expert tile et of group q (the same on every lane).
+  auto run_tile = [&](int q, int stl, int et) {
     const int s_q = a.grp_slot[q];
     const int tq = a.grp_slot[q + 1] - s_q;
     const int e_q = q * a.B;
     const int bq = min(a.B, n_act - e_q);
-    const int n_et = (bq + TE - 1) / TE;
-    const int local = tile - a.grp_tile[q];
-    const int stl = local / n_et, et = local - stl * n_et;
     const int s0 = s_q + stl * kGroupSlots;
     const int ns = min(kGroupSlots, tq - stl * kGroupSlots);
     const int r0 = e_q + et * TE;
@@ -240,6 +237,51 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_dot_kernel(GroupedDotArgs
       }
       __syncthreads();
     }
+  };
+
+  if (NJ == 2 && total >= 6 * ng) {
+    // Groups of up to 64 experts with many slot tiles each: a group's slots are in token order,
+    // so its slot tiles cover successive eighths of the tokens. XCD x takes the slot tiles stl
+    // with (8 stl + 4) / n_st = x of every group (n_st slot tiles), about an eighth of the
+    // tokens, whose rows then stay in its L2 across groups; workgroup r of the XCD takes every
+    // R-th of those tiles in group order. Every wave computes the same tile sequence from the
+    // same data. (Each XCD now reads every group's u rows; with the small groups that costs
+    // less than the token rows saved, with 160-expert tiles it does not, measured.)
+    const int r = blockIdx.x / kXcds, R = blocks_per_xcd;
+    int seen = 0;  // tiles of this XCD in the groups before this batch
+    for (int qb = 0; qb < (int)ng; qb += kWave) {
+      const int qq = qb + l;
+      int cnt = 0, lo_st = 0, n_et = 1;
+      if (qq < ng) {
+        const int n_st = (a.grp_slot[qq + 1] - a.grp_slot[qq] + kGroupSlots - 1) / kGroupSlots;
+        n_et = (min(a.B, n_act - qq * a.B) + TE - 1) / TE;
+        const int lo8 = xcd * n_st - 4, hi8 = (xcd + 1) * n_st - 4;
+        lo_st = lo8 <= 0 ? 0 : (lo8 + 7) / 8;
+        const int hi_st = hi8 <= 0 ? 0 : min(n_st, (hi8 + 7) / 8);
+        cnt = hi_st > lo_st ? (hi_st - lo_st) * n_et : 0;
+      }
+      const int ex = wave_excl_scan_i32(cnt);
+      const int first = seen + ex;  // XCD-stream index of this lane's first tile
+      const int skip = ((r - first) % R + R) % R;
+      uint64_t mine = __ballot(skip < cnt);
+      while (mine) {
+        const int L = __ffsll((unsigned long long)mine) - 1;
+        mine &= mine - 1;
+        const int cL = readlane_i32(cnt, L), lL = readlane_i32(lo_st, L);
+        const int eL = readlane_i32(n_et, L), sL = readlane_i32(skip, L);
+        for (int i = sL; i < cL; i += R) run_tile(qb + L, lL + i / eL, i % eL);
+      }
+      seen += readlane_i32(ex + cnt, kWave - 1);
+    }
+    return;
+  }
+  for (int tile = t_lo; tile < t_hi; ++tile) {
+    while (q + 1 < ng && a.grp_tile[q + 1] <= tile) ++q;
+    const int bq = min(a.B, n_act - q * a.B);
+    const int n_et = (bq + TE - 1) / TE;
+    const int local = tile - a.grp_tile[q];
+    const int stl = local / n_et;
+    run_tile(q, stl, local - stl * n_et);
   }
 }
 

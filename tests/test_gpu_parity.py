@@ -65,6 +65,10 @@ SHAPES = {
                                  K=64),
     "dense_k100_bf16": synth.Workload("dense_k100_bf16", T=77, d=192, n_rows=40, n_cols=50,
                                       d_key=64, H=1, K=100),
+    # groups of 64 experts with about twelve slot tiles each: the grouped GEMM's tiles are
+    # shared out to the XCDs by token range
+    "bucket_bf16": synth.Workload("bucket_bf16", T=3000, d=128, n_rows=64, n_cols=64, d_key=64,
+                                  H=2, K=128),
 }
 
 
@@ -288,7 +292,7 @@ GROUPED_CASES = [
     ("small_bf16", 2), ("small_bf16", 64), ("small_bf16", 100), ("k64_bf16", 33),
     ("all_experts_bf16", 5), ("all_experts_bf16", 1 << 20), ("k64_bf16", 1),
     ("wide_bf16", 3), ("skinny_bf16", 16), ("skinny1_bf16", 7), ("k256_bf16", 64),
-    ("shared_bf16", 48), ("paper_k512_bf16", 320),
+    ("shared_bf16", 48), ("paper_k512_bf16", 320), ("bucket_bf16", 64), ("bucket_bf16", 100),
 ]
 
 
