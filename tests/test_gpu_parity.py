@@ -54,6 +54,8 @@ SHAPES = {
                                    H=2, K=12),
     "decode8_bf16": synth.Workload("decode8_bf16", T=8, d=2048, n_rows=100, n_cols=36,
                                    d_key=1024, H=2, K=9),
+    "decode_dk768_bf16": synth.Workload("decode_dk768_bf16", T=20, d=1536, n_rows=70, n_cols=64,
+                                        d_key=768, H=2, K=5),
     # K > 64 (workgroup-per-row selection), incl. the paper's benchmark grid 320 x 320, K = 512
     "k256_bf16": synth.Workload("k256_bf16", T=100, d=256, n_rows=64, n_cols=64, d_key=64, H=2,
                                 K=256),
