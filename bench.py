@@ -175,6 +175,34 @@ def extras(args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1, 
         f"token-centric {tc_ms:.3f} ms")
     del y_tc
 
+    # The accumulate in expert-major order (v read once per expert run): contribution rows
+    # a_p v_e [M, d] fp32, then a token-major sum in slot order. Same dot kernel in front.
+    contrib = None
+    perm = sched[0]
+    sc_bytes = P.omnimoe_workspace_size(desc, P.binding.STAGE_EXPERT_SCATTER)
+    if sc_bytes <= (64 << 30):
+        ws_sc = torch.empty(sc_bytes, dtype=torch.uint8, device="cuda")
+        y_sc = torch.empty_like(y)
+        sc = lambda: P.omnimoe_expert_forward_scatter(  # noqa: E731
+            desc, d_in["x"], d_in["u"], d_in["v"], idx, g, perm, y_sc, ws=ws_sc, stream=stream)
+        for _ in range(2):
+            sc()
+        ev0.record(stream)
+        for _ in range(args.steps):
+            sc()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        sc_ms = ev0.elapsed_time(ev1) / args.steps
+        slot_ms = per["expert_dot"] + per["accumulate"]
+        den = y.abs().amax(dim=1).clamp_min(1e-30)
+        rel = float(((y_sc - y).abs().amax(dim=1) / den).max())
+        contrib = {"dot_scatter_reduce_ms": sc_ms, "dot_accumulate_ms": slot_ms,
+                   "ratio": sc_ms / slot_ms, "buffer_bytes": sc_bytes,
+                   "max_row_rel_diff": rel}
+        log(f"contribution rows: dot + scatter + reduce {sc_ms:.3f} ms against dot + "
+            f"slot-order accumulate {slot_ms:.3f} ms")
+        del ws_sc, y_sc
+
     # The full OmniMoE FFN adds the shared dense SwiGLU branch (Eq. 7) to the routed output;
     # its width here is d_ff = d, the ratio of the paper's benchmark configuration.
     d_ff = w.d
@@ -303,7 +331,7 @@ def extras(args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1, 
                     "tokens_per_s": w.T / ((bw_ms + rb_ms) * 1e-3)}
         log(f"expert backward: {bw_ms:.3f} ms, router backward: {rb_ms:.3f} ms")
         del dy, dx, du, dv, wsb, dkr, dkc, wsr
-    return ablation, shared_mlp, no_cpr, backward, grouped
+    return ablation, shared_mlp, no_cpr, backward, grouped, contrib
 
 
 def main():
@@ -450,9 +478,9 @@ def main():
     routing = routing_stats(idx.cpu().numpy(), w.N)
     assert routing["n_active"] == n_active
 
-    ablation = shared_mlp = no_cpr = backward = grouped = None
+    ablation = shared_mlp = no_cpr = backward = grouped = contrib = None
     if not args.layer_only:
-        ablation, shared_mlp, no_cpr, backward, grouped = extras(
+        ablation, shared_mlp, no_cpr, backward, grouped, contrib = extras(
             args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1,
             (perm, off, na, n_active))
 
@@ -522,6 +550,7 @@ def main():
         "ablation_no_schedule": ablation,
         "ablation_no_cartesian_router": no_cpr,
         "grouped_expert_gemm": grouped,
+        "accumulate_contribution_rows": contrib,
         "n_active": n_active, "eta": w.M / max(1, n_active), "routing": routing,
         "schedule_share": per["schedule"] / sum(per.values()),
         "kernels": kernels,

@@ -102,7 +102,8 @@ typedef enum {
   OMNIMOE_STAGE_ROUTE_DENSE = 5,    /* omnimoe_route_dense without a logits buffer */
   OMNIMOE_STAGE_EXPERT_BACKWARD = 6, /* omnimoe_expert_backward */
   OMNIMOE_STAGE_ROUTE_BACKWARD = 7,  /* omnimoe_route_backward */
-  OMNIMOE_STAGE_EXPERT_GROUPED = 8   /* omnimoe_expert_forward_grouped */
+  OMNIMOE_STAGE_EXPERT_GROUPED = 8,  /* omnimoe_expert_forward_grouped */
+  OMNIMOE_STAGE_EXPERT_SCATTER = 9   /* omnimoe_expert_forward_scatter */
 } omnimoe_stage;
 
 /* Bytes of workspace the given stage's entry point needs for this shape. */
@@ -195,6 +196,24 @@ omnimoe_status omnimoe_expert_forward_grouped(const omnimoe_layer_desc* desc, co
                                               const float* gates, const int32_t* perm,
                                               const int32_t* active, const int32_t* n_active,
                                               float* y, void* workspace, size_t workspace_bytes,
+                                              void* stream);
+
+/* Expert compute with the output stage in expert-major order, as the scatter-add of Eq. 14
+ * orders it, made deterministic by a token-major reduction (the accumulate variant that reads
+ * each v row once): a[p] = g_p * act(x_t . u_e) as in omnimoe_expert_forward; then, walking
+ * perm expert by expert, each expert's v row is read once per run of its tasks and the fp32
+ * row a[p] * v_e is written to row p of a contribution buffer [M, d] in the workspace; then
+ * every token sums its H*K rows in (head, k) order into y. Same arguments as
+ * omnimoe_expert_forward; workspace OMNIMOE_STAGE_EXPERT_SCATTER bytes (M * d * 4 for the
+ * contribution rows plus M * 4). y agrees with omnimoe_expert_forward to fp32 rounding (each
+ * product is rounded before it is added instead of fused into the sum) and is the same on
+ * every run: no atomics. It exists to measure that trade-off: v is read A times instead of M
+ * times, at the cost of writing and reading back M * d * 4 bytes. Pointers 16-byte aligned;
+ * T = 0 is a no-op. */
+omnimoe_status omnimoe_expert_forward_scatter(const omnimoe_layer_desc* desc, const void* x,
+                                              const void* u, const void* v, const int32_t* idx,
+                                              const float* gates, const int32_t* perm, float* y,
+                                              void* workspace, size_t workspace_bytes,
                                               void* stream);
 
 /* Expert compute without the schedule, token by token: the ablation of Expert-Centric

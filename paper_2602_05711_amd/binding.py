@@ -18,7 +18,8 @@ OMNIMOE_F32, OMNIMOE_BF16 = 0, 1
 OMNIMOE_ACT_GELU, OMNIMOE_ACT_SILU = 0, 1
 OMNIMOE_QUERY_SPLIT, OMNIMOE_QUERY_SHARED = 0, 1
 (STAGE_ROUTE, STAGE_SELECT, STAGE_SCHEDULE, STAGE_EXPERT, STAGE_LAYER, STAGE_ROUTE_DENSE,
- STAGE_EXPERT_BACKWARD, STAGE_ROUTE_BACKWARD, STAGE_EXPERT_GROUPED) = range(9)
+ STAGE_EXPERT_BACKWARD, STAGE_ROUTE_BACKWARD, STAGE_EXPERT_GROUPED,
+ STAGE_EXPERT_SCATTER) = range(10)
 KERNEL_NAMES = ("score", "select", "schedule", "expert_dot", "accumulate")
 
 EXPORTED = (
@@ -26,7 +27,8 @@ EXPORTED = (
     "omnimoe_select_dense", "omnimoe_shared_mlp", "omnimoe_shared_mlp_workspace_size",
     "omnimoe_schedule",
     "omnimoe_expert_forward", "omnimoe_expert_forward_grouped",
-    "omnimoe_expert_forward_token_centric", "omnimoe_expert_backward",
+    "omnimoe_expert_forward_scatter", "omnimoe_expert_forward_token_centric",
+    "omnimoe_expert_backward",
     "omnimoe_route_backward",
     "omnimoe_layer_forward", "omnimoe_timer_create",
     "omnimoe_timer_destroy", "omnimoe_timer_read", "omnimoe_layer_forward_timed",
@@ -71,6 +73,7 @@ def load_library():
         "omnimoe_schedule": [D, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_expert_forward": [D, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_expert_forward_grouped": [D, P, P, P, P, P, P, P, P, P, P, SZ, P],
+        "omnimoe_expert_forward_scatter": [D, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_expert_forward_token_centric": [D, P, P, P, P, P, P, P],
         "omnimoe_expert_backward": [D, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_route_backward": [D, P, P, P, P, P, P, P, P, P, SZ, P],
@@ -201,6 +204,14 @@ def omnimoe_expert_forward_grouped(desc, x, u, v, idx, gates, perm, active, n_ac
     _check("omnimoe_expert_forward_grouped", load_library().omnimoe_expert_forward_grouped(
         ctypes.byref(desc), _ptr(x), _ptr(u), _ptr(v), _ptr(idx), _ptr(gates), _ptr(perm),
         _ptr(active), _ptr(n_active), _ptr(y), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def omnimoe_expert_forward_scatter(desc, x, u, v, idx, gates, perm, y, ws=None, stream=None):
+    if ws is None:
+        ws = workspace(desc, STAGE_EXPERT_SCATTER, x.device)
+    _check("omnimoe_expert_forward_scatter", load_library().omnimoe_expert_forward_scatter(
+        ctypes.byref(desc), _ptr(x), _ptr(u), _ptr(v), _ptr(idx), _ptr(gates), _ptr(perm),
+        _ptr(y), _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def omnimoe_expert_forward_token_centric(desc, x, u, v, idx, gates, y, stream=None):

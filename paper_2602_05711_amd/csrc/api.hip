@@ -112,6 +112,7 @@ size_t stage_bytes(const Shape& s, int stage) {
     case OMNIMOE_STAGE_ROUTE_DENSE: return dense_bytes(s);
     case OMNIMOE_STAGE_EXPERT_BACKWARD: return omnimoe::backward_ws_bytes(s.M);
     case OMNIMOE_STAGE_ROUTE_BACKWARD: return omnimoe::route_backward_ws_bytes(s);
+    case OMNIMOE_STAGE_EXPERT_SCATTER: return m_bytes(s) + align_up((size_t)s.M * s.d * 4);
     case OMNIMOE_STAGE_EXPERT_GROUPED:  // the plan is dead once the grouped dot has run
       return m_bytes(s) + std::max(omnimoe::group_plan_ws_bytes(s),
                                    omnimoe::dense_accumulate_ws_bytes(s));
@@ -219,7 +220,7 @@ const char* omnimoe_status_string(int32_t status) {
 omnimoe_status omnimoe_workspace_size(const omnimoe_layer_desc* desc, int32_t stage,
                                       size_t* bytes) {
   if (!bytes) return OMNIMOE_ERR_INVALID_ARG;
-  if (stage < OMNIMOE_STAGE_ROUTE || stage > OMNIMOE_STAGE_EXPERT_GROUPED)
+  if (stage < OMNIMOE_STAGE_ROUTE || stage > OMNIMOE_STAGE_EXPERT_SCATTER)
     return OMNIMOE_ERR_INVALID_ARG;
   Shape s;
   omnimoe_status st = check_desc(desc, &s);
@@ -421,6 +422,22 @@ omnimoe_status omnimoe_expert_forward_grouped(const omnimoe_layer_desc* desc, co
     e = omnimoe::launch_grouped_dot(s, x, u, gates, perm, active, n_active, plan, abuf, strm);
   if (e == hipSuccess) e = routed_sum(s, v, idx, abuf, y, (char*)ws + m_bytes(s), strm);
   return hip_status(e);
+}
+
+omnimoe_status omnimoe_expert_forward_scatter(const omnimoe_layer_desc* desc, const void* x,
+                                              const void* u, const void* v, const int32_t* idx,
+                                              const float* gates, const int32_t* perm, float* y,
+                                              void* ws, size_t ws_bytes, void* stream) {
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  if (s.T == 0) return OMNIMOE_OK;
+  if ((st = check_ptrs({x, u, v, idx, gates, perm, y, ws}))) return st;
+  if (ws_bytes < stage_bytes(s, OMNIMOE_STAGE_EXPERT_SCATTER)) return OMNIMOE_ERR_WORKSPACE;
+  float* abuf = (float*)ws;
+  float* cbuf = (float*)((char*)ws + m_bytes(s));
+  return hip_status(omnimoe::launch_expert_contrib(s, x, u, v, idx, gates, perm, abuf, cbuf, y,
+                                                   (hipStream_t)stream));
 }
 
 omnimoe_status omnimoe_expert_forward_token_centric(const omnimoe_layer_desc* desc,

@@ -12,6 +12,9 @@
 // slot order in fp32. The order is fixed, so y is the same on every run; no atomics are used.
 // With too few tokens to fill the chip, a token's row is split over column ranges and its slots
 // over the waves of a workgroup, whose partial rows are added in wave order.
+//
+// scatter_contrib / reduce_contrib: the output stage in expert-major order (v read once per
+// expert run) through per-task fp32 contribution rows and a token-major sum of them.
 #include "device_common.hpp"
 #include "internal.hpp"
 
@@ -361,6 +364,155 @@ __global__ __launch_bounds__(64 * W) void accumulate_slots_kernel(AccArgs a) {
   }
 }
 
+// Contribution rows (the accumulate written the way the method's scatter-add reads, but with a
+// deterministic reduction): expert-major, each wave walks its range of the schedule like
+// expert_dot_kernel, loads an expert's v row once per run and writes the fp32 row a[p] * v_e
+// into row p of a [M, d] buffer, p being the token-major slot; reduce_contrib_kernel then sums
+// each token's H*K rows in slot order. v is read once per run instead of once per task, at the
+// price of writing and reading back M * d * 4 bytes.
+struct ContribArgs {
+  DotArgs s;       // schedule walk: perm, idx, sorted keys, M, N, hk, range
+  const void* v;
+  float* c;        // [M, d] fp32 contribution rows
+  float* y;        // [T, d] fp32 out
+  int64_t T;
+  int d;
+  int vchunks;     // 16-byte chunks of a v row
+  int splits;      // reduce: waves per token (column splits of whole 64-chunk rows)
+};
+
+template <int CPL, bool BF16>
+__global__ __launch_bounds__(256) void scatter_contrib_kernel(ContribArgs a) {
+  constexpr int EPC = BF16 ? 8 : 4;
+  constexpr int G = CPL >= 8 ? 2 : 4;
+  const DotArgs& sa = a.s;
+  const int l = lane_id();
+  const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t s = range_start(sa, wave * sa.range);
+  const int64_t e = range_start(sa, (wave + 1) * sa.range);
+  if (s >= e) return;
+  const uint4* V = (const uint4*)a.v;
+  const int64_t row_chunks = a.vchunks;
+  bool cv[CPL];
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) cv[q] = (l + kWave * q) < a.vchunks;
+  int prev = -1;  // expert whose v row sits in vr[G - 1]
+  uint4 vr[G][CPL];
+#pragma unroll
+  for (int i = 0; i < G; ++i)
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) vr[i][q] = make_uint4(0, 0, 0, 0);
+  for (int64_t b = s; b < e; b += kWave) {
+    const int64_t pos = b + l;
+    const bool ok = pos < e;
+    const int key = ok ? key_at(sa, pos) : -1;
+    const int p = ok ? task_at(sa, pos) : 0;
+    const float av = ok ? sa.a[p] : 0.0f;
+    const int cnt = (int)((e - b) < kWave ? (e - b) : kWave);
+    for (int j0 = 0; j0 < cnt; j0 += G) {
+      int ej[G], pj[G];
+      float wj[G];
+#pragma unroll
+      for (int i = 0; i < G; ++i) {
+        const int jj = (j0 + i < cnt) ? j0 + i : cnt - 1;
+        ej[i] = readlane_i32(key, jj);
+        pj[i] = readlane_i32(p, jj);
+        wj[i] = readlane_f32(av, jj);
+      }
+#pragma unroll
+      for (int i = 0; i < G; ++i) {
+        if (j0 + i < cnt) {
+          const int before = (i == 0) ? prev : ej[i - 1];
+          if (ej[i] == before) {
+#pragma unroll
+            for (int q = 0; q < CPL; ++q) vr[i][q] = vr[(i + G - 1) % G][q];
+          } else {
+            load_row<CPL>(vr[i], V + (int64_t)ej[i] * row_chunks, cv);
+          }
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < G; ++i) {
+        if (j0 + i < cnt) {
+          float4* row = (float4*)(a.c + (int64_t)pj[i] * a.d);
+#pragma unroll
+          for (int q = 0; q < CPL; ++q) {
+            if (!cv[q]) continue;
+            const uint4 c = vr[i][q];
+            const int o = (l + kWave * q) * (EPC / 4);
+            const float w = wj[i];
+            if constexpr (BF16) {
+              row[o] = make_float4(w * bf16_lo(c.x), w * bf16_hi(c.x), w * bf16_lo(c.y),
+                                   w * bf16_hi(c.y));
+              row[o + 1] = make_float4(w * bf16_lo(c.z), w * bf16_hi(c.z), w * bf16_lo(c.w),
+                                       w * bf16_hi(c.w));
+            } else {
+              row[o] = make_float4(w * __uint_as_float(c.x), w * __uint_as_float(c.y),
+                                   w * __uint_as_float(c.z), w * __uint_as_float(c.w));
+            }
+          }
+        }
+      }
+      const int last = (cnt - j0 < G ? cnt - j0 : G) - 1;
+#pragma unroll
+      for (int i = 0; i < G - 1; ++i)
+        if (i == last) {
+#pragma unroll
+          for (int q = 0; q < CPL; ++q) vr[G - 1][q] = vr[i][q];
+        }
+      prev = ej[last];
+    }
+  }
+}
+
+// y_t = sum over t's slots s (in order) of row t*H*K + s of the contribution buffer, fp32.
+// One wave per (token, column split); lane l holds float4 columns l + 64 q of the split.
+template <int CPL>
+__global__ __launch_bounds__(256) void reduce_contrib_kernel(ContribArgs a) {
+  constexpr int UNROLL = CPL >= 16 ? 2 : 4;
+  const int l = lane_id();
+  const int f4 = a.d / 4;  // float4 columns per row
+  const int hk = a.s.hk;
+  const int64_t stride = (int64_t)gridDim.x * 4;
+  for (int64_t wt = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); wt < a.T * a.splits;
+       wt += stride) {
+    const int64_t t = wt / a.splits;
+    const int cbase = (int)(wt % a.splits) * CPL * kWave;
+    bool cvalid[CPL];
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) cvalid[q] = (cbase + l + kWave * q) < f4;
+    float4 acc[CPL];
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) acc[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+    const float4* base = (const float4*)(a.c + t * hk * (int64_t)a.d) + cbase + l;
+    for (int s0 = 0; s0 < hk; s0 += UNROLL) {
+      float4 r[UNROLL][CPL];
+#pragma unroll
+      for (int u = 0; u < UNROLL; ++u)
+#pragma unroll
+        for (int q = 0; q < CPL; ++q)
+          r[u][q] = (s0 + u < hk && cvalid[q]) ? base[(int64_t)(s0 + u) * f4 + kWave * q]
+                                               : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int u = 0; u < UNROLL; ++u) {
+        if (s0 + u < hk) {
+#pragma unroll
+          for (int q = 0; q < CPL; ++q) {
+            acc[q].x += r[u][q].x;
+            acc[q].y += r[u][q].y;
+            acc[q].z += r[u][q].z;
+            acc[q].w += r[u][q].w;
+          }
+        }
+      }
+    }
+    float4* yt = (float4*)(a.y + t * a.d) + cbase + l;
+#pragma unroll
+    for (int q = 0; q < CPL; ++q)
+      if (cvalid[q]) yt[kWave * q] = acc[q];
+  }
+}
+
 // Token-centric execution (the scheduling ablation): one wavefront per token keeps x_t in
 // registers and, G slots at a time in (head, k) order, gathers each slot's u and v rows
 // together, forms a = g * act(x_t . u_e) exactly as expert_dot_kernel does and adds a * v_e
@@ -519,6 +671,29 @@ hipError_t dispatch_acc(int cpl, dim3 grid, hipStream_t st, const AccArgs& a) {
   return hipGetLastError();
 }
 
+template <bool BF16>
+hipError_t dispatch_scatter(int cpl, dim3 grid, hipStream_t st, const ContribArgs& a) {
+  switch (cpl) {
+    case 1: hipLaunchKernelGGL((scatter_contrib_kernel<1, BF16>), grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((scatter_contrib_kernel<2, BF16>), grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((scatter_contrib_kernel<4, BF16>), grid, dim3(256), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((scatter_contrib_kernel<8, BF16>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((scatter_contrib_kernel<16, BF16>), grid, dim3(256), 0, st, a); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t dispatch_reduce_contrib(int cpl, dim3 grid, hipStream_t st, const ContribArgs& a) {
+  switch (cpl) {
+    case 1: hipLaunchKernelGGL((reduce_contrib_kernel<1>), grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((reduce_contrib_kernel<2>), grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((reduce_contrib_kernel<4>), grid, dim3(256), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((reduce_contrib_kernel<8>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((reduce_contrib_kernel<16>), grid, dim3(256), 0, st, a); break;
+  }
+  return hipGetLastError();
+}
+
 // Chunks per lane, rounded up to a power of two.
 int chunks_per_lane(int nchunks) {
   int c = 1;
@@ -610,6 +785,52 @@ hipError_t launch_token_centric(const Shape& s, const void* x, const void* u, co
   const int cpl = chunks_per_lane(a.nchunks);
   return s.bf16 ? dispatch_token<true>(cpl, dim3((unsigned)blocks), st, a)
                 : dispatch_token<false>(cpl, dim3((unsigned)blocks), st, a);
+}
+
+hipError_t launch_expert_contrib(const Shape& s, const void* x, const void* u, const void* v,
+                                 const int32_t* idx, const float* gates, const int32_t* perm,
+                                 float* abuf, float* cbuf, float* y, hipStream_t st) {
+  if (s.T == 0) return hipSuccess;
+  hipError_t e = launch_expert_dot(s, x, u, idx, gates, perm, nullptr, abuf, st);
+  if (e != hipSuccess || s.M == 0) return e;
+  ContribArgs a;
+  a.s.x = x;
+  a.s.u = u;
+  a.s.idx = idx;
+  a.s.gates = gates;
+  a.s.perm = perm;
+  a.s.sk = nullptr;
+  a.s.a = abuf;
+  a.s.M = s.M;
+  a.s.N = s.N;
+  a.s.d = s.d;
+  a.s.hk = s.hk;
+  a.s.act = s.act;
+  a.s.nchunks = s.bf16 ? s.d / 8 : s.d / 4;
+  a.s.range = 64;
+  while (a.s.range > 1 && s.M < (int64_t)a.s.range * 2048) a.s.range >>= 1;
+  a.v = v;
+  a.c = cbuf;
+  a.y = y;
+  a.T = s.T;
+  a.d = s.d;
+  a.vchunks = a.s.nchunks;
+  const int64_t waves = (s.M + a.s.range - 1) / a.s.range;
+  const dim3 grid((unsigned)((waves + 3) / 4));
+  const int cpl = chunks_per_lane(a.vchunks);
+  e = s.bf16 ? dispatch_scatter<true>(cpl, grid, st, a) : dispatch_scatter<false>(cpl, grid, st, a);
+  if (e != hipSuccess) return e;
+  // Reduce: float4 columns, split over waves while there are few tokens.
+  const int f4 = s.d / 4;
+  const int rows64 = (f4 + kWave - 1) / kWave;
+  int splits = 1;
+  while ((f4 + splits - 1) / splits > 16 * kWave) splits *= 2;  // at most 16 float4 per lane
+  while (splits < rows64 && s.T * splits < 1024 && rows64 % (splits * 2) == 0) splits *= 2;
+  a.splits = splits;
+  int64_t blocks = (s.T * splits + 3) / 4;
+  if (blocks > 16384) blocks = 16384;
+  return dispatch_reduce_contrib(chunks_per_lane((f4 + splits - 1) / splits),
+                                 dim3((unsigned)blocks), st, a);
 }
 
 }  // namespace omnimoe

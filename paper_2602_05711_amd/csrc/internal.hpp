@@ -83,6 +83,13 @@ hipError_t launch_fill_i32(int32_t* dst, int64_t n, int32_t value, hipStream_t s
 
 // The expert compute token by token (the scheduling ablation): same y as expert_dot followed
 // by accumulate, with each task gathering its own u and v rows.
+// Expert compute with per-task contribution rows: the expert dot into a[], then an
+// expert-major pass writing c[p] = a[p] * v_e ([M, d] fp32) and a token-major sum of each
+// token's rows in slot order into y.
+hipError_t launch_expert_contrib(const Shape& s, const void* x, const void* u, const void* v,
+                                 const int32_t* idx, const float* gates, const int32_t* perm,
+                                 float* a, float* c, float* y, hipStream_t st);
+
 hipError_t launch_token_centric(const Shape& s, const void* x, const void* u, const void* v,
                                 const int32_t* idx, const float* gates, float* y,
                                 hipStream_t st);

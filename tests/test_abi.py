@@ -24,7 +24,7 @@ def _declared_functions():
 def test_header_matches_exports():
     lib = P.load_library()
     names = _declared_functions()
-    assert len(names) == 19
+    assert len(names) == 20
     assert sorted(P.EXPORTED) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -92,6 +92,8 @@ def test_workspace_sizes_cover_buffers():
     st, layer = _ws(d, B.STAGE_LAYER)
     assert st == OK and layer >= route + 3 * w.M * 4
     assert _ws(d, 10)[0] == INVALID
+    st, scatter = _ws(d, B.STAGE_EXPERT_SCATTER)
+    assert st == OK and scatter >= w.M * 4 + w.M * w.d * 4  # a[] and the contribution rows
     st, grouped = _ws(d, B.STAGE_EXPERT_GROUPED)
     assert st == OK and grouped >= w.M * 4 + w.N * 4 + 2 * w.M * 4
     st, dense = _ws(d, B.STAGE_ROUTE_DENSE)
@@ -124,6 +126,12 @@ def test_entry_points_check_pointers_before_launch():
     assert lib.omnimoe_schedule(D, a, a, a, a, a, None, a, n(8), None) == WORKSPACE
     assert lib.omnimoe_expert_forward(D, a, a, a, a, a, None, a, a, n(1 << 30), None) == INVALID
     assert lib.omnimoe_expert_forward_token_centric(D, a, a, None, a, a, a, None) == INVALID
+    assert lib.omnimoe_expert_forward_scatter(D, a, a, a, a, a, None, a, a, n(1 << 40),
+                                              None) == INVALID
+    assert lib.omnimoe_expert_forward_scatter(D, a, a, a, a, a, a, a, bad, n(1 << 40),
+                                              None) == ALIGN
+    assert lib.omnimoe_expert_forward_scatter(D, a, a, a, a, a, a, a, a, n(16),
+                                              None) == WORKSPACE
     assert lib.omnimoe_expert_forward_grouped(D, a, a, a, a, a, a, None, a, a, a, n(1 << 40),
                                               None) == INVALID
     assert lib.omnimoe_expert_forward_grouped(D, a, a, a, a, a, a, a, bad, a, a, n(1 << 40),
@@ -171,6 +179,8 @@ def test_zero_tokens_is_a_noop():
                                       None) == OK
     assert lib.omnimoe_expert_forward_token_centric(D, None, None, None, None, None, None,
                                                     None) == OK
+    assert lib.omnimoe_expert_forward_scatter(D, None, None, None, None, None, None, None, None,
+                                              n(0), None) == OK
     assert lib.omnimoe_layer_forward(D, None, None, None, None, None, None, None, None, None,
                                      n(0), None) == OK
 

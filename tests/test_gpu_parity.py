@@ -395,6 +395,33 @@ def test_token_centric_ablation(name):
         assert row_rel_err(y_tc, y.astype(np.float64)).max() <= 1e-6
 
 
+@pytest.mark.parametrize("name", EXPERT_SHAPES)
+def test_expert_forward_scatter(name):
+    # Contribution rows a_p v_e written expert by expert, then summed per token in slot order:
+    # within tolerance of the oracle, the same bits on a second call (into a workspace full of
+    # the first call's rows), and within fp32 rounding of the slot-order sum (which fuses each
+    # product into the sum; here each product is rounded first).
+    say(f"[scatter] {name}")
+    w, dev, idx, g32, perm, y_ref = _expert_case(name)
+    d = B.make_desc(w)
+    gi, gg, gp = to_dev(idx), to_dev(g32), to_dev(perm)
+    ws = B.workspace(d, B.STAGE_EXPERT_SCATTER)
+    y = torch.empty((w.T, w.d), dtype=torch.float32, device="cuda")
+    y_sc = torch.full((w.T, w.d), float("nan"), dtype=torch.float32, device="cuda")
+    y_sc2 = torch.full_like(y_sc, float("nan"))
+    P.omnimoe_expert_forward(d, dev["x"], dev["u"], dev["v"], gi, gg, gp, y)
+    P.omnimoe_expert_forward_scatter(d, dev["x"], dev["u"], dev["v"], gi, gg, gp, y_sc, ws=ws)
+    P.omnimoe_expert_forward_scatter(d, dev["x"], dev["u"], dev["v"], gi, gg, gp, y_sc2, ws=ws)
+    torch.cuda.synchronize()
+    y_sc, y_sc2 = y_sc.cpu().numpy(), y_sc2.cpu().numpy()
+    assert np.array_equal(y_sc.view(np.uint8), y_sc2.view(np.uint8))
+    err = row_rel_err(y_sc, y_ref)
+    say(f"  max row rel err {err.max():.3e}")
+    assert err.max() <= tol(w)
+    if w.dtype == "f32" or not (w.H == 1 and w.K * 64 >= w.N):  # not the dense routed sum
+        assert row_rel_err(y_sc, y.cpu().numpy().astype(np.float64)).max() <= 1e-5
+
+
 @pytest.mark.parametrize("name", ["dense_bf16", "dense_k100_bf16"])
 def test_dense_routed_sum(name):
     # y = A V with A[t, e] = a_p rounded to bf16: within tolerance of the oracle, the same on a
