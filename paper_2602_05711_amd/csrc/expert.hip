@@ -1,8 +1,9 @@
 // Per-expert vector compute (Eq. 4, 7, 14).
 //
-// expert_dot: expert-major. The schedule's sorted positions are cut into ranges of about 64
-// tasks, each starting at an expert boundary (a range only starts inside an expert's run when
-// the run is longer than 64, so very hot experts are shared out). One wavefront walks its
+// expert_dot: expert-major. The schedule's sorted positions are cut into ranges of about 16 or
+// 64 tasks, each starting at an expert boundary (a range only starts inside an expert's run
+// when the run is longer than the range, so very hot experts are shared out); each XCD takes a
+// contiguous share of the ranges. One wavefront walks its
 // range run by run: it loads the expert's u row once (16-byte loads, every lane a slice),
 // then for up to four of the run's tasks at a time loads the token rows, forms the dot
 // products in fp32, and writes a[p] = g_p * act(x_t . u_e) into the token-major slot p.
@@ -120,7 +121,12 @@ template <int CPL, bool BF16>
 __global__ __launch_bounds__(256) void expert_dot_kernel(DotArgs a) {
   constexpr int G = CPL >= 16 ? 1 : (CPL >= 8 ? 2 : 4);
   const int l = lane_id();
-  const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  // Workgroup b runs on XCD b % 8; each XCD takes a contiguous share of the sorted positions,
+  // so the token rows that recur within a stretch of the expert order (a token's experts in
+  // one grid row are neighbours there) are fetched into that XCD's L2 once.
+  const int64_t nb = gridDim.x, per_xcd = nb / 8, extra = nb % 8, xcd = blockIdx.x % 8;
+  const int64_t blk = xcd * per_xcd + (xcd < extra ? xcd : extra) + blockIdx.x / 8;
+  const int64_t wave = blk * 4 + (threadIdx.x >> 6);
   const int64_t s = range_start(a, wave * a.range);
   const int64_t e = range_start(a, (wave + 1) * a.range);
   if (s >= e) return;
@@ -721,9 +727,11 @@ hipError_t launch_expert_dot(const Shape& s, const void* x, const void* u, const
   a.hk = s.hk;
   a.act = s.act;
   a.nchunks = s.bf16 ? s.d / 8 : s.d / 4;
-  // About 64 tasks per wave when there are plenty; fewer (down to one) so that small batches
-  // still give at least 2048 waves.
-  a.range = 64;
+  // 16 tasks per wave when experts average fewer than 8 tasks (fewer tasks in flight per XCD
+  // keeps its stretch of token rows in L2), 64 otherwise (a range starts inside an expert's run
+  // only when the run is longer than the range, and each such start reads u again); fewer, down
+  // to one, so that small batches still give at least 2048 waves.
+  a.range = s.M < 8 * s.N ? 16 : 64;
   while (a.range > 1 && s.M < (int64_t)a.range * 2048) a.range >>= 1;
   const int64_t waves = (s.M + a.range - 1) / a.range;
   dim3 grid((unsigned)((waves + 3) / 4));
