@@ -3,8 +3,8 @@
 // expert_dot: expert-major. The schedule's sorted positions are cut into ranges of about 16 or
 // 64 tasks, each starting at an expert boundary (a range only starts inside an expert's run
 // when the run is longer than the range, so very hot experts are shared out); each XCD takes a
-// contiguous share of the ranges. One wavefront walks its
-// range run by run: it loads the expert's u row once (16-byte loads, every lane a slice),
+// contiguous share of the ranges. One wavefront walks its range run by run: it loads the
+// expert's u row once (16-byte loads with the non-temporal hint, every lane a slice),
 // then for up to four of the run's tasks at a time loads the token rows, forms the dot
 // products in fp32, and writes a[p] = g_p * act(x_t . u_e) into the token-major slot p.
 //
@@ -114,6 +114,25 @@ __device__ __forceinline__ void load_row(uint4 (&r)[CPL], const uint4* base, con
   for (int q = 0; q < CPL; ++q) r[q] = cv[q] ? base[l + kWave * q] : make_uint4(0, 0, 0, 0);
 }
 
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+// load_row with the non-temporal hint: for rows read once (an expert's u row), so that they
+// do not push out of L2 the token rows that are read again.
+template <int CPL>
+__device__ __forceinline__ void load_row_nt(uint4 (&r)[CPL], const uint4* base,
+                                            const bool (&cv)[CPL]) {
+  const int l = lane_id();
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) {
+    if (cv[q]) {
+      const u32x4_t v = __builtin_nontemporal_load((const u32x4_t*)(base + l + kWave * q));
+      r[q] = make_uint4(v.x, v.y, v.z, v.w);
+    } else {
+      r[q] = make_uint4(0, 0, 0, 0);
+    }
+  }
+}
+
 // Positions are taken G at a time (four for rows up to 4096 bf16 values). Slot i holds position j0 + i: its token row is loaded,
 // and its expert's u row is loaded only when that expert differs from the previous position's
 // (otherwise the previous slot's registers are copied), so each run of an expert reads u once.
@@ -169,7 +188,7 @@ __global__ __launch_bounds__(256) void expert_dot_kernel(DotArgs a) {
 #pragma unroll
             for (int q = 0; q < CPL; ++q) ur[i][q] = ur[(i + G - 1) % G][q];
           } else {
-            load_row<CPL>(ur[i], U + (int64_t)ej[i] * row_chunks, cv);
+            load_row_nt<CPL>(ur[i], U + (int64_t)ej[i] * row_chunks, cv);
           }
           load_row<CPL>(xr[i], X + (int64_t)(pj[i] / a.hk) * row_chunks, cv);
         }
