@@ -286,14 +286,19 @@ __global__ __launch_bounds__(256) void accumulate_kernel(AccArgs a) {
         }
       }
     }
-    float4* yt = (float4*)(a.y + t * a.d);
+    // y is written once and not read back here: non-temporal stores keep it out of the caches
+    // the v gathers use.
+    typedef float f32x4_t __attribute__((ext_vector_type(4)));
+    f32x4_t* yt = (f32x4_t*)(a.y + t * a.d);
 #pragma unroll
     for (int q = 0; q < CPL; ++q) {
       if (!cvalid[q]) continue;
       const int c = cbase + l + kWave * q;
 #pragma unroll
-      for (int k = 0; k < EPC; k += 4)
-        yt[(c * EPC + k) / 4] = make_float4(acc[q][k], acc[q][k + 1], acc[q][k + 2], acc[q][k + 3]);
+      for (int k = 0; k < EPC; k += 4) {
+        const f32x4_t o = {acc[q][k], acc[q][k + 1], acc[q][k + 2], acc[q][k + 3]};
+        __builtin_nontemporal_store(o, &yt[(c * EPC + k) / 4]);
+      }
     }
   }
 }
