@@ -304,7 +304,10 @@ __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
         const int64_t m = m0 + wm * 128 + i * 32 + (q >> 2) * 8 + (lane >> 5) * 4 + (q & 3);
         if (m < a.T) {
           if constexpr (SPLIT) out[m * a.ldo + oc] = acc[i][j][q];
-          else store_out<ACC>(a, m * a.ldo + oc, acc[i][j][q]);
+          else if constexpr (ACC) store_out<ACC>(a, m * a.ldo + oc, acc[i][j][q]);
+          // non-temporal: the next kernel reads these once, and dirty lines left in L2 would
+          // otherwise be written back while it streams them
+          else __builtin_nontemporal_store(acc[i][j][q], &a.out[m * a.ldo + oc]);
         }
       }
     }
