@@ -215,8 +215,10 @@ __device__ __forceinline__ void load_half(const float* __restrict__ p, int n, fl
 #pragma unroll
     for (int c = 0; c < R / 4; ++c) {
       const int j0 = 256 * c + 4 * lane_id();
-      float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (FULL || j0 < n) t = *(const float4*)(p + j0);
+      // The logits are read once: non-temporal loads leave the caches to the later kernels.
+      typedef float f32x4_t __attribute__((ext_vector_type(4)));
+      f32x4_t t = {0.f, 0.f, 0.f, 0.f};
+      if (FULL || j0 < n) t = __builtin_nontemporal_load((const f32x4_t*)(p + j0));
       v[4 * c] = t.x;
       v[4 * c + 1] = t.y;
       v[4 * c + 2] = t.z;
