@@ -5,7 +5,8 @@
 //   upsweep   per-tile digit histogram (tile = 4096 tasks), stored digit-major;
 //   scan      exclusive scan of the histogram: the first output slot of (digit, tile);
 //   downsweep each wave ranks its tasks stably (ballot-matched peers in lane order plus a
-//             per-wave running count), then tasks scatter to scan + wave offset + rank.
+//             per-wave running count); the tile is put in digit order in LDS and each digit's
+//             tasks leave as one run, at scan + wave offset + rank.
 // Stability of every pass makes the final order (expert, task id), which is unique.
 // Segment extraction marks positions whose expert differs from the previous one and
 // compacts them with another scan into active / active_offsets / n_active.
@@ -213,8 +214,13 @@ __global__ __launch_bounds__(kThreads) void radix_upsweep_kernel(RadixPass p) {
 }
 
 __global__ __launch_bounds__(kThreads) void radix_downsweep_kernel(RadixPass p) {
+  static_assert(kMaxRadix <= 4 * kThreads, "each thread scans four digits");
   __shared__ int wcnt[kThreads / kWave][kMaxRadix];
   __shared__ int gofs[kMaxRadix];
+  __shared__ int lofs[kMaxRadix];
+  __shared__ int wsum[kThreads / kWave];
+  __shared__ int skey[kTile];
+  __shared__ int sval[kTile];
   const int radix = 1 << p.bits;
   const uint32_t mask = (uint32_t)radix - 1u;
   // Tiles in XCD-contiguous order: a digit's runs from neighbouring tiles are adjacent in the
@@ -259,13 +265,47 @@ __global__ __launch_bounds__(kThreads) void radix_downsweep_kernel(RadixPass p) 
     rank[r] = run + before;
   }
   __syncthreads();
-  for (int d = threadIdx.x; d < radix; d += kThreads) {
-    int run = gofs[d];
+  // The tile is first put in digit order in LDS, so that its keys leave as one run per digit
+  // (consecutive threads, consecutive addresses) instead of one scattered word per task.
+  // lofs[d]: first local position of digit d; wcnt[ww][d] becomes the local start of wave
+  // ww's keys of digit d. Thread t scans digits 4 t .. 4 t + 3.
+  {
+    int c[4], sum = 0;
 #pragma unroll
-    for (int ww = 0; ww < kThreads / kWave; ++ww) {
-      int c = wcnt[ww][d];
-      wcnt[ww][d] = run;
-      run += c;
+    for (int k = 0; k < 4; ++k) {
+      const int d = 4 * threadIdx.x + k;
+      int t = 0;
+      if (d < radix) {
+#pragma unroll
+        for (int ww = 0; ww < kThreads / kWave; ++ww) t += wcnt[ww][d];
+      }
+      c[k] = t;
+      sum += t;
+    }
+    int incl = sum;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int y = __shfl_up(incl, off, kWave);
+      if (l >= off) incl += y;
+    }
+    if (l == kWave - 1) wsum[w] = incl;
+    __syncthreads();
+    int base = incl - sum;
+    for (int ww = 0; ww < w; ++ww) base += wsum[ww];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int d = 4 * threadIdx.x + k;
+      if (d < radix) {
+        lofs[d] = base;
+        int run = base;
+#pragma unroll
+        for (int ww = 0; ww < kThreads / kWave; ++ww) {
+          const int cc = wcnt[ww][d];
+          wcnt[ww][d] = run;
+          run += cc;
+        }
+      }
+      base += c[k];
     }
   }
   __syncthreads();
@@ -274,10 +314,20 @@ __global__ __launch_bounds__(kThreads) void radix_downsweep_kernel(RadixPass p) 
     const int64_t i = wbase + (int64_t)r * kWave + l;
     if (i < p.n) {
       const uint32_t d = ((uint32_t)key[r] >> p.shift) & mask;
-      const int pos = wcnt[w][d] + rank[r];
-      p.keys_out[pos] = key[r];
-      p.vals_out[pos] = val[r];
+      const int lp = wcnt[w][d] + rank[r];
+      skey[lp] = key[r];
+      sval[lp] = val[r];
     }
+  }
+  __syncthreads();
+  const int64_t t0 = tile * kTile;
+  const int tn = (int)(p.n - t0 < kTile ? p.n - t0 : kTile);
+  for (int j = threadIdx.x; j < tn; j += kThreads) {
+    const int k = skey[j];
+    const uint32_t d = ((uint32_t)k >> p.shift) & mask;
+    const int64_t pos = (int64_t)gofs[d] + (j - lofs[d]);
+    p.keys_out[pos] = k;
+    p.vals_out[pos] = sval[j];
   }
 }
 
