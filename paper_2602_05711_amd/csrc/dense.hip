@@ -43,7 +43,13 @@ __global__ __launch_bounds__(256) void densify_kernel(const int32_t* __restrict_
     }
     __syncthreads();
     const int64_t n = kpad - c0 < kDenseChunk ? kpad - c0 : kDenseChunk;  // a multiple of 64
-    for (int i = tid; i < n / 8; i += 256) dst_row[c0 / 8 + i] = ((const uint4*)row)[i];
+    for (int i = tid; i < n / 8; i += 256) {
+      // non-temporal: A (T x N bf16) is far larger than the caches and read once by the GEMM
+      typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+      const uint4 q = ((const uint4*)row)[i];
+      const u32x4_t o = {q.x, q.y, q.z, q.w};
+      __builtin_nontemporal_store(o, (u32x4_t*)&dst_row[c0 / 8 + i]);
+    }
     __syncthreads();
   }
 }
