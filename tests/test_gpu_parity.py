@@ -188,6 +188,8 @@ SCHEDULE_CASES = [
     # range holds too many tasks (few experts, skew)
     (64, 8, 16, 1024, 1024, "zipf"), (256, 8, 4, 2, 2, "zipf"), (40, 8, 16, 64, 64, "uniform"),
     (256, 8, 3, 1, 3, "uniform"), (33, 8, 16, 1024, 1024, "uniform"),
+    # radix passes with a ragged last tile and a tiny digit range (2 bits; one expert)
+    (3000, 4, 1, 1, 3, "uniform"), (2500, 4, 1, 1, 1, "uniform"), (4099, 3, 1, 2, 3, "zipf"),
 ]
 
 
