@@ -216,8 +216,7 @@ __global__ __launch_bounds__(kThreads) void radix_upsweep_kernel(RadixPass p) {
 __global__ __launch_bounds__(kThreads) void radix_downsweep_kernel(RadixPass p) {
   static_assert(kMaxRadix <= 4 * kThreads, "each thread scans four digits");
   __shared__ int wcnt[kThreads / kWave][kMaxRadix];
-  __shared__ int gofs[kMaxRadix];
-  __shared__ int lofs[kMaxRadix];
+  __shared__ int gofs[kMaxRadix];  // first output slot of each digit, then minus its local start
   __shared__ int wsum[kThreads / kWave];
   __shared__ int skey[kTile];
   __shared__ int sval[kTile];
@@ -267,8 +266,10 @@ __global__ __launch_bounds__(kThreads) void radix_downsweep_kernel(RadixPass p) 
   __syncthreads();
   // The tile is first put in digit order in LDS, so that its keys leave as one run per digit
   // (consecutive threads, consecutive addresses) instead of one scattered word per task.
-  // lofs[d]: first local position of digit d; wcnt[ww][d] becomes the local start of wave
-  // ww's keys of digit d. Thread t scans digits 4 t .. 4 t + 3.
+  // With lofs(d) the first local position of digit d, gofs[d] becomes gofs[d] - lofs(d) (a key at
+  // local position j goes to gofs[d] + j) and wcnt[ww][d] the local start of wave ww's keys of
+  // digit d. Thread t scans digits 4 t .. 4 t + 3. (One array instead of two keeps the LDS at
+  // three workgroups per compute unit.)
   {
     int c[4], sum = 0;
 #pragma unroll
@@ -296,7 +297,7 @@ __global__ __launch_bounds__(kThreads) void radix_downsweep_kernel(RadixPass p) 
     for (int k = 0; k < 4; ++k) {
       const int d = 4 * threadIdx.x + k;
       if (d < radix) {
-        lofs[d] = base;
+        gofs[d] -= base;
         int run = base;
 #pragma unroll
         for (int ww = 0; ww < kThreads / kWave; ++ww) {
@@ -325,7 +326,7 @@ __global__ __launch_bounds__(kThreads) void radix_downsweep_kernel(RadixPass p) 
   for (int j = threadIdx.x; j < tn; j += kThreads) {
     const int k = skey[j];
     const uint32_t d = ((uint32_t)k >> p.shift) & mask;
-    const int64_t pos = (int64_t)gofs[d] + (j - lofs[d]);
+    const int64_t pos = (int64_t)gofs[d] + j;
     p.keys_out[pos] = k;
     p.vals_out[pos] = sval[j];
   }
