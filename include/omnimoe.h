@@ -141,8 +141,14 @@ omnimoe_status omnimoe_route_dense(const omnimoe_layer_desc* desc, const void* x
 omnimoe_status omnimoe_select_dense(const omnimoe_layer_desc* desc, const float* logits,
                                     int32_t* idx, float* gates, void* stream);
 
-/* Selection only: top-K over the implicit grid and gates, from given fp32 logits
- *   half_scores [T, H, n_rows + n_cols] (as written by omnimoe_route). */
+/* Selection only (Sec. 2.2, "Parallel Top-K Selection"; Eq. 11, 1, 2): for every (token, head)
+ * row, the K best cells of the implicit grid S[i, j] = s_r[i] + s_c[j] (Eq. 11) by (S
+ * descending, id ascending), id = i * n_cols + j (Eq. 1), and the softmax of their scores
+ * (Eq. 2), from given fp32 logits
+ *   half_scores [T, H, n_rows + n_cols] fp32   row logits then column logits (omnimoe_route's)
+ *   idx         [T, H, K] int32 out,  gates [T, H, K] fp32 out   (as omnimoe_route's)
+ * Comparisons are exact (S is the double sum of two floats), so the result depends only on
+ * the logits. Needs no workspace (workspace may be NULL). */
 omnimoe_status omnimoe_select(const omnimoe_layer_desc* desc, const float* half_scores,
                               int32_t* idx, float* gates, void* workspace,
                               size_t workspace_bytes, void* stream);
@@ -271,14 +277,21 @@ omnimoe_status omnimoe_route_backward(const omnimoe_layer_desc* desc, const void
                                       float* dkeys_row, float* dkeys_col, void* workspace,
                                       size_t workspace_bytes, void* stream);
 
-/* The whole routed layer: route, schedule and expert compute on one stream, no host
- * synchronisation. y [T, d] fp32 out; idx_out and gates_out ([T, H, K]) may be NULL. The
- * expert compute is omnimoe_expert_forward's, or omnimoe_expert_forward_grouped's when
- * group_size > 1, dtype is bf16 and d % 64 == 0. */
+/* The whole routed layer (Sec. 2.1-2.3): the routed term of Eq. 7, y_t = sum over heads h and
+ * slots k of g_{t,h,k} act(x_t . u_e) v_e with e = idx[t, h, k] (Eq. 4-6), the experts and
+ * gates chosen by the Cartesian Product Router (Eq. 9, 11, 1, 2) and the expert compute
+ * ordered by Expert-Centric Scheduling (Eq. 12-14); on one stream, no host synchronisation.
+ *   x [T, d], keys_row [H, n_rows, d_key], keys_col [H, n_cols, d_key], u, v [N, d]   dtype
+ *   y [T, d] fp32 out; idx_out and gates_out ([T, H, K], as omnimoe_route's) may be NULL.
+ * The expert compute is omnimoe_expert_forward's, or omnimoe_expert_forward_grouped's when
+ * group_size > 1, dtype is bf16 and d % 64 == 0. Workspace: OMNIMOE_STAGE_LAYER bytes
+ * (caller-owned device memory, contents need not be initialised; OMNIMOE_ERR_WORKSPACE when
+ * short). */
 omnimoe_status omnimoe_layer_forward(const omnimoe_layer_desc* desc, const void* x,
                                      const void* keys_row, const void* keys_col, const void* u,
                                      const void* v, float* y, int32_t* idx_out, float* gates_out,
                                      void* workspace, size_t workspace_bytes, void* stream);
+
 
 /* The shared dense branch MLP(x) that the full layer adds to the routed output (Eq. 3, 7),
  * as a SwiGLU feed-forward block of width d_ff:

@@ -4,24 +4,32 @@
 // single group. A is built in bf16 (a_p rounded to nearest even), V is transposed once so that
 // the expert dimension is contiguous, the product runs on the MFMA logit kernel split over the
 // expert dimension, and the split partials are added in split order, so y is deterministic.
-// With one head the K experts of a token are distinct, so each A[t, e] is a single a_p.
+// A token's slots normally name distinct experts (the router picks K distinct cells), so each
+// A[t, e] is a single a_p; when a caller's idx repeats an expert within a token, that entry is
+// the sum of the repeated slots' a_p in slot order, so the result stays deterministic.
 #include "device_common.hpp"
 #include "internal.hpp"
 
 namespace omnimoe {
 namespace {
 
-constexpr int kDenseChunk = 32768;  // columns of A built at a time (64 KiB of LDS)
+constexpr int kDenseChunk = 16384;  // columns of A built at a time (32 KiB of LDS)
 constexpr int kDenseSlots = 16;     // a token's slots held per thread (hk <= 4096)
 
 // Row t of A: the token's K (expert, a) pairs are loaded once into registers; then, chunk by
 // chunk of columns, the chunk is zeroed in LDS, the pairs that fall in it are placed, and it
-// is written out with 16-byte stores.
+// is written out with 16-byte stores. Placement first marks each column with the number of
+// one slot that falls in it (any one: concurrent plain stores); a slot that then reads back
+// another slot's number shares its expert with it. Without such a slot in the chunk (the
+// router's case) every slot stores its own value. Otherwise the slot whose mark survived
+// sums, in slot order, the a of every slot with its expert (read again from memory), so the
+// result does not depend on which store won.
 __global__ __launch_bounds__(256) void densify_kernel(const int32_t* __restrict__ idx,
                                                       const float* __restrict__ a,
                                                       uint16_t* __restrict__ A, int hk,
                                                       int64_t N, int64_t kpad) {
   __shared__ __attribute__((aligned(16))) uint16_t row[kDenseChunk];
+  __shared__ __attribute__((aligned(16))) uint16_t mark[kDenseChunk];  // slot number + 1
   const int64_t t = blockIdx.x;
   const int tid = threadIdx.x;
   int e[kDenseSlots];
@@ -34,12 +42,41 @@ __global__ __launch_bounds__(256) void densify_kernel(const int32_t* __restrict_
   }
   uint4* dst_row = (uint4*)(A + t * kpad);
   for (int64_t c0 = 0; c0 < kpad; c0 += kDenseChunk) {
-    for (int i = tid; i < kDenseChunk / 8; i += 256) ((uint4*)row)[i] = make_uint4(0, 0, 0, 0);
+    for (int i = tid; i < kDenseChunk / 8; i += 256) {
+      ((uint4*)row)[i] = make_uint4(0, 0, 0, 0);
+      ((uint4*)mark)[i] = make_uint4(0, 0, 0, 0);
+    }
     __syncthreads();
 #pragma unroll
     for (int q = 0; q < kDenseSlots; ++q) {
       const int64_t c = (int64_t)e[q] - c0;
-      if (e[q] >= 0 && e[q] < N && c >= 0 && c < kDenseChunk) row[c] = v[q];
+      if (e[q] >= 0 && e[q] < N && c >= 0 && c < kDenseChunk) mark[c] = (uint16_t)(q * 256 + tid + 1);
+    }
+    __syncthreads();
+    int shared_expert = 0;
+#pragma unroll
+    for (int q = 0; q < kDenseSlots; ++q) {
+      const int64_t c = (int64_t)e[q] - c0;
+      if (e[q] >= 0 && e[q] < N && c >= 0 && c < kDenseChunk)
+        shared_expert |= mark[c] != (uint16_t)(q * 256 + tid + 1);
+    }
+    if (!__syncthreads_or(shared_expert)) {
+#pragma unroll
+      for (int q = 0; q < kDenseSlots; ++q) {
+        const int64_t c = (int64_t)e[q] - c0;
+        if (e[q] >= 0 && e[q] < N && c >= 0 && c < kDenseChunk) row[c] = v[q];
+      }
+    } else {
+      for (int q = 0; q < kDenseSlots; ++q) {
+        const int64_t c = (int64_t)e[q] - c0;
+        if (e[q] >= 0 && e[q] < N && c >= 0 && c < kDenseChunk &&
+            mark[c] == (uint16_t)(q * 256 + tid + 1)) {
+          float sum = 0.f;
+          for (int jj = 0; jj < hk; ++jj)
+            if (idx[t * hk + jj] == e[q]) sum += a[t * hk + jj];
+          row[c] = bf16_rne(sum);
+        }
+      }
     }
     __syncthreads();
     const int64_t n = kpad - c0 < kDenseChunk ? kpad - c0 : kDenseChunk;  // a multiple of 64

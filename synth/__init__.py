@@ -82,7 +82,9 @@ def fill_rows(seed: int, stream: int, n_rows: int, row_len: int, scale: float, b
 
 def bf16_bits_to_f32(a: np.ndarray) -> np.ndarray:
     """Exact widening of bf16 bit patterns (uint16) to float32."""
-    return (a.astype(np.uint32) << 16).view(np.float32)
+    out = np.empty(a.shape, np.uint32)
+    np.left_shift(a, 16, out=out, dtype=np.uint32)
+    return out.view(np.float32)
 
 
 def as_f32(a: np.ndarray) -> np.ndarray:
