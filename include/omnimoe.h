@@ -292,6 +292,24 @@ omnimoe_status omnimoe_layer_forward(const omnimoe_layer_desc* desc, const void*
                                      const void* v, float* y, int32_t* idx_out, float* gates_out,
                                      void* workspace, size_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): omnimoe_layer_forward with its workspace taken from
+ * a scratch array of OMNIMOE_NOALLOC_SCRATCH_BYTES that the library holds in static device
+ * memory, one per GPU, until the process ends. The call allocates nothing (no hipMalloc,
+ * hipFree or allocating library routine); the caller still passes inputs and outputs, with the
+ * same meaning, layout and checks as omnimoe_layer_forward. It uses the scratch of the calling
+ * thread's current device, which must be the device of `stream`; the first call on a device
+ * looks the array's address up. A shape whose OMNIMOE_STAGE_LAYER workspace exceeds
+ * OMNIMOE_NOALLOC_SCRATCH_BYTES returns OMNIMOE_ERR_WORKSPACE before any launch (at the
+ * 1024 x 1024-expert, d = 2048, H = 8, K = 16 shape that is about 900 tokens). All calls on
+ * one GPU share its array: calls that overlap in time on one GPU (other streams, other
+ * threads) race and must be serialised by the caller. No state carries over between calls
+ * (nothing in the scratch needs to start at zero). */
+#define OMNIMOE_NOALLOC_SCRATCH_BYTES (64 * 1024 * 1024)
+omnimoe_status omnimoe_layer_forward_noalloc(const omnimoe_layer_desc* desc, const void* x,
+                                             const void* keys_row, const void* keys_col,
+                                             const void* u, const void* v, float* y,
+                                             int32_t* idx_out, float* gates_out, void* stream);
 
 /* The shared dense branch MLP(x) that the full layer adds to the routed output (Eq. 3, 7),
  * as a SwiGLU feed-forward block of width d_ff:

@@ -30,7 +30,7 @@ EXPORTED = (
     "omnimoe_expert_forward_scatter", "omnimoe_expert_forward_token_centric",
     "omnimoe_expert_backward",
     "omnimoe_route_backward",
-    "omnimoe_layer_forward", "omnimoe_timer_create",
+    "omnimoe_layer_forward", "omnimoe_layer_forward_noalloc", "omnimoe_timer_create",
     "omnimoe_timer_destroy", "omnimoe_timer_read", "omnimoe_layer_forward_timed",
     "omnimoe_status_string",
 )
@@ -78,6 +78,7 @@ def load_library():
         "omnimoe_expert_backward": [D, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_route_backward": [D, P, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_layer_forward": [D, P, P, P, P, P, P, P, P, P, SZ, P],
+        "omnimoe_layer_forward_noalloc": [D, P, P, P, P, P, P, P, P, P],
         "omnimoe_layer_forward_timed": [D, P, P, P, P, P, P, P, P, P, SZ, P, P],
         "omnimoe_timer_create": [I32, ctypes.POINTER(P)],
         "omnimoe_timer_destroy": [P],
@@ -247,6 +248,16 @@ def omnimoe_layer_forward(desc, x, keys_row, keys_col, u, v, y, idx_out=None, ga
     _check("omnimoe_layer_forward", load_library().omnimoe_layer_forward(
         ctypes.byref(desc), _ptr(x), _ptr(keys_row), _ptr(keys_col), _ptr(u), _ptr(v), _ptr(y),
         _ptr(idx_out), _ptr(gates_out), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024  # OMNIMOE_NOALLOC_SCRATCH_BYTES
+
+
+def omnimoe_layer_forward_noalloc(desc, x, keys_row, keys_col, u, v, y, idx_out=None,
+                                  gates_out=None, stream=None):
+    _check("omnimoe_layer_forward_noalloc", load_library().omnimoe_layer_forward_noalloc(
+        ctypes.byref(desc), _ptr(x), _ptr(keys_row), _ptr(keys_col), _ptr(u), _ptr(v), _ptr(y),
+        _ptr(idx_out), _ptr(gates_out), _stream(stream)))
 
 
 class Timer:

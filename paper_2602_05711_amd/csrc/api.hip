@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -11,6 +12,11 @@
 #include "internal.hpp"
 
 using omnimoe::Shape;
+
+// Workspace of omnimoe_layer_forward_noalloc: one copy on every GPU the library runs on, held
+// until the process ends. Host code never uses this name as an address: the device address is
+// looked up per device (noalloc_scratch below) and only that is passed to kernels.
+static __device__ __align__(256) unsigned char scratch[OMNIMOE_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -198,6 +204,26 @@ omnimoe_status layer_impl(const omnimoe_layer_desc* desc, const void* x, const v
   if ((e = routed_sum(s, v, idx, abuf, y, (char*)abuf + m_bytes(s), strm))) return hip_status(e);
   mark(5);
   if (timer) ++timer->used;
+  return OMNIMOE_OK;
+}
+
+// Device address of `scratch` on the calling thread's current device, looked up with that
+// device current on its first use and kept per device.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+omnimoe_status noalloc_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return OMNIMOE_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return OMNIMOE_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return OMNIMOE_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
   return OMNIMOE_OK;
 }
 
@@ -498,6 +524,24 @@ omnimoe_status omnimoe_layer_forward(const omnimoe_layer_desc* desc, const void*
                                      void* ws, size_t ws_bytes, void* stream) {
   return layer_impl(desc, x, keys_row, keys_col, u, v, y, idx_out, gates_out, ws, ws_bytes,
                     stream, nullptr);
+}
+
+omnimoe_status omnimoe_layer_forward_noalloc(const omnimoe_layer_desc* desc, const void* x,
+                                             const void* keys_row, const void* keys_col,
+                                             const void* u, const void* v, float* y,
+                                             int32_t* idx_out, float* gates_out, void* stream) {
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  if (s.T == 0) return OMNIMOE_OK;
+  if ((st = check_ptrs({x, keys_row, keys_col, u, v, y}))) return st;
+  if ((st = check_opt(idx_out)) || (st = check_opt(gates_out))) return st;
+  if (stage_bytes(s, OMNIMOE_STAGE_LAYER) > (size_t)OMNIMOE_NOALLOC_SCRATCH_BYTES)
+    return OMNIMOE_ERR_WORKSPACE;
+  void* ws = nullptr;
+  if ((st = noalloc_scratch(&ws))) return st;
+  return layer_impl(desc, x, keys_row, keys_col, u, v, y, idx_out, gates_out, ws,
+                    (size_t)OMNIMOE_NOALLOC_SCRATCH_BYTES, stream, nullptr);
 }
 
 omnimoe_status omnimoe_layer_forward_timed(const omnimoe_layer_desc* desc, const void* x,

@@ -24,7 +24,7 @@ def _declared_functions():
 def test_header_matches_exports():
     lib = P.load_library()
     names = _declared_functions()
-    assert len(names) == 20
+    assert len(names) == 21
     assert sorted(P.EXPORTED) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -167,6 +167,28 @@ def test_entry_points_check_pointers_before_launch():
     assert lib.omnimoe_layer_forward(D, a, a, a, a, a, a, bad, None, a, n(1 << 40), None) == ALIGN
     assert lib.omnimoe_layer_forward_timed(D, a, a, a, a, a, a, None, None, a, n(1 << 40), None,
                                            None) == INVALID
+    assert lib.omnimoe_layer_forward_noalloc(D, a, a, a, a, a, bad, None, None, None) == ALIGN
+    assert lib.omnimoe_layer_forward_noalloc(D, a, a, a, a, a, a, None, bad, None) == ALIGN
+    assert lib.omnimoe_layer_forward_noalloc(D, a, a, a, None, a, a, None, None, None) == INVALID
+
+
+def test_noalloc_rejects_shapes_beyond_its_scratch():
+    # The layer workspace of the shape must fit the library's static scratch; larger shapes
+    # are refused before any device call (this runs without a GPU).
+    with open(os.path.join(ROOT, "include", "omnimoe.h")) as f:
+        m = re.search(r"#define OMNIMOE_NOALLOC_SCRATCH_BYTES \(([\d\s*]+)\)", f.read())
+    assert m and eval(m.group(1)) == B.NOALLOC_SCRATCH_BYTES
+    lib = P.load_library()
+    a = ctypes.c_void_p(1 << 20)
+    w = synth.WORKLOADS["train_bf16"]
+    for T, fits in ((16384, False), (900, True), (1000, False)):
+        d = B.make_desc(w, T=T)
+        need = ctypes.c_size_t(0)
+        assert lib.omnimoe_workspace_size(ctypes.byref(d), B.STAGE_LAYER, ctypes.byref(need)) == OK
+        assert (need.value <= B.NOALLOC_SCRATCH_BYTES) == fits, (T, need.value)
+        if not fits:
+            assert lib.omnimoe_layer_forward_noalloc(ctypes.byref(d), a, a, a, a, a, a, None,
+                                                     None, None) == WORKSPACE
 
 
 def test_zero_tokens_is_a_noop():
@@ -183,6 +205,8 @@ def test_zero_tokens_is_a_noop():
                                               n(0), None) == OK
     assert lib.omnimoe_layer_forward(D, None, None, None, None, None, None, None, None, None,
                                      n(0), None) == OK
+    assert lib.omnimoe_layer_forward_noalloc(D, None, None, None, None, None, None, None, None,
+                                             None) == OK
 
 
 def test_status_strings():
