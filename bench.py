@@ -76,6 +76,21 @@ def load_traffic(kernel, workload):
     return t.get("bytes_per_launch")
 
 
+def load_mfma_busy(kernel, workload):
+    """MFMA-busy fraction of a matrix-core kernel from the committed rocprofv3 counter summary
+    (SQ_VALU_MFMA_BUSY_CYCLES over the SIMDs' cycles in the kernel), or None when absent or the
+    kernel's sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_mfma.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("sources_sha256_16") != kernel_sources_hash(KERNEL_FILES[kernel]):
+        return None
+    return {k: t[k] for k in ("mfma_busy", "simd_cycles", "mfma_busy_cycles", "normalisation")
+            if k in t}
+
+
 def routing_stats(idx, N):
     """Expert usage of one batch: active experts, usage, KL(z || uniform), top-10% share."""
     import numpy as np
@@ -135,6 +150,16 @@ def cpu_baseline(w, inp, sample_tokens, threads):
                       f"{w.n_rows}x{w.n_cols} sub-keys, Cartesian selection, schedule, "
                       f"expert-major forward), fp64, {dt:.1f} s on {threads} threads of "
                       f"{cpu_model()}"}
+
+
+def host_threads():
+    """Threads for the oracle leg: every core this process may run on, unless the job's CPU
+    share is set smaller (OMP_NUM_THREADS, as on a one-GPU job that is allotted 16 cores)."""
+    affinity = len(os.sched_getaffinity(0))
+    share = os.environ.get("OMP_NUM_THREADS", "")
+    threads = min(affinity, int(share)) if share.isdigit() and int(share) > 0 else affinity
+    return max(1, threads), {"nproc": os.cpu_count(), "affinity": affinity,
+                             "omp_num_threads": share or None, "cpu_model": cpu_model()}
 
 
 def cpu_model():
@@ -343,6 +368,8 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=16384,
                     help="tokens for the oracle leg (16384: about 10 s on 16 host threads)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle leg")
+    ap.add_argument("--single-thread-sample", type=int, default=256,
+                    help="tokens for the oracle leg on one host thread (0: skip)")
     ap.add_argument("--brute-sample", type=int, default=256,
                     help="tokens for the oracle's brute-force selection timing (0: skip)")
     ap.add_argument("--out", default=None, help="also write the JSON line here")
@@ -503,6 +530,10 @@ def main():
             # rocprofv3 bytes (L2 misses, MALL hits included) over the event-timed duration
             kd["counter_bytes"] = tb
             kd["counter_GBps"] = tb / (per[k] * 1e-3) / 1e9
+        if kd["bound"] == "mfma":
+            mb = load_mfma_busy(k, w.name)
+            if mb is not None:
+                kd["mfma_busy"] = mb
     dom = max(per, key=per.get)
     kd = kernels[dom]
     traffic = load_traffic(dom, w.name)
@@ -525,10 +556,14 @@ def main():
 
     cpu = None
     if not args.no_cpu:
-        threads = max(1, min(16, len(os.sched_getaffinity(0))))
-        log(f"oracle leg: {args.cpu_sample} tokens on {threads} host threads")
+        threads, hostinfo = host_threads()
+        log(f"oracle leg: {args.cpu_sample} tokens on {threads} host threads ({hostinfo})")
         cpu = cpu_baseline(w, inp, args.cpu_sample, threads)
+        cpu.update(hostinfo)
         log(f"oracle {cpu['value']:.1f} tokens/s")
+        if args.single_thread_sample > 0:
+            cpu["single_thread"] = cpu_baseline(w, inp, args.single_thread_sample, 1)
+            log(f"oracle on one thread {cpu['single_thread']['value']:.1f} tokens/s")
         if args.brute_sample > 0:
             cpu["bruteforce_select"] = cpu_bruteforce(w, inp, args.brute_sample, threads)
             log(f"oracle brute-force selection {cpu['bruteforce_select']['value']:.1f} tokens/s")

@@ -292,26 +292,37 @@ __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
     __syncthreads();
   }
 
+  // Epilogue. Each lane writes column n of rows m_lane + r, r = i * 32 + 8 (q / 4) + q % 4:
+  // one row pointer per column block and compile-time row offsets times the uniform stride.
+  // Only a tile that reaches past T checks rows, with one tile-wide branch; a per-element
+  // check costs a divergent branch per store, which made the epilogue as long as a quarter
+  // of the main loop.
+  const int64_t m_lane = m0 + wm * 128 + (lane >> 5) * 4;
+  float* const obase = SPLIT ? out : a.out;
+  auto store_all = [&](auto rows_ok) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int n = n0 + wn * 128 + j * 32 + (lane & 31);
-    if (n >= ncols) continue;
-    const int64_t oc = out_col(a, half, n);
+    for (int j = 0; j < 4; ++j) {
+      const int n = n0 + wn * 128 + j * 32 + (lane & 31);
+      if (n >= ncols) continue;
+      float* const orow = obase + m_lane * a.ldo + out_col(a, half, n);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < 4; ++i) {
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int64_t m = m0 + wm * 128 + i * 32 + (q >> 2) * 8 + (lane >> 5) * 4 + (q & 3);
-        if (m < a.T) {
-          if constexpr (SPLIT) out[m * a.ldo + oc] = acc[i][j][q];
-          else if constexpr (ACC) store_out<ACC>(a, m * a.ldo + oc, acc[i][j][q]);
+        for (int q = 0; q < 16; ++q) {
+          const int r = i * 32 + (q >> 2) * 8 + (q & 3);
+          if (!rows_ok(r)) continue;
+          float* const o = orow + (int64_t)r * a.ldo;
+          if constexpr (SPLIT) *o = acc[i][j][q];
+          else if constexpr (ACC) *o += acc[i][j][q];
           // non-temporal: the next kernel reads these once, and dirty lines left in L2 would
           // otherwise be written back while it streams them
-          else __builtin_nontemporal_store(acc[i][j][q], &a.out[m * a.ldo + oc]);
+          else __builtin_nontemporal_store(acc[i][j][q], o);
         }
       }
     }
-  }
+  };
+  if (m0 + LM <= a.T) store_all([](int) { return true; });
+  else store_all([&](int r) { return m_lane + r < a.T; });
 }
 
 // ---------------------------------------------------------------- skinny bf16 kernel
@@ -550,6 +561,33 @@ __global__ __launch_bounds__(256) void score_f32_kernel(ScoreArgs a) {
 
 }  // namespace
 
+// Reads the GEMM's operands once, in 16-byte chunks, so that they sit in the memory-side cache
+// (MALL, 256 MB) when the GEMM fetches them: the GEMM's two-stage pipeline covers the MALL's
+// latency but not HBM's, and its tiles fetch every operand line several times from beyond
+// L2. Three segments (x, row keys, column keys) in one grid-stride walk; nothing is written
+// (the sink store cannot happen: it needs a negative count).
+struct PrefetchArgs {
+  const uint4* p[3];
+  int64_t n[3];  // chunks per segment
+  uint32_t* sink;
+};
+
+__global__ __launch_bounds__(256) void prefetch_kernel(PrefetchArgs a) {
+  uint32_t acc = 0;
+  const int64_t stride = (int64_t)gridDim.x * 256;
+#pragma unroll
+  for (int seg = 0; seg < 3; ++seg) {
+    const uint4* __restrict__ p = a.p[seg];
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < a.n[seg]; i += stride) {
+      const uint4 v = p[i];
+      acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+  }
+  if (acc == 0x9E3779B9u && a.n[0] < 0) *a.sink = acc;
+}
+
+constexpr int64_t kPrefetchMaxBytes = 128ll << 20;  // half the MALL
+
 hipError_t launch_score(const Shape& s, const void* x, const void* keys_row,
                         const void* keys_col, float* half_scores, hipStream_t st,
                         bool accumulate) {
@@ -573,6 +611,21 @@ hipError_t launch_score(const Shape& s, const void* x, const void* keys_row,
   a.kchunk = 0;
   a.part_stride = 0;
   const int ncols = s.H * (s.nr > s.nc ? s.nr : s.nc);
+  // (not for the accumulating product: its operand was just written and is in the caches)
+  const bool large = s.bf16 && s.T > 64 && s.dk % 64 == 0;
+  if (large && !accumulate) {
+    // x rows are read whole (both query halves); the tables are [H, n, d_key] bf16
+    PrefetchArgs pa;
+    pa.p[0] = (const uint4*)x;
+    pa.p[1] = (const uint4*)keys_row;
+    pa.p[2] = (const uint4*)keys_col;
+    pa.n[0] = s.T * s.d * 2 / 16;
+    pa.n[1] = (int64_t)s.H * s.nr * s.dk * 2 / 16;
+    pa.n[2] = (int64_t)s.H * s.nc * s.dk * 2 / 16;
+    pa.sink = (uint32_t*)half_scores;
+    if ((pa.n[0] + pa.n[1] + pa.n[2]) * 16 <= kPrefetchMaxBytes)
+      hipLaunchKernelGGL(prefetch_kernel, dim3(4096), dim3(256), 0, st, pa);
+  }
   if (s.bf16 && s.T >= 8 && s.T <= 64 && s.dk % 256 == 0 && s.dk <= 1024) {
     dim3 grid((ncols + DC_KEYS - 1) / DC_KEYS, 2);
     const int rb = s.T > 32 ? 2 : 1;
