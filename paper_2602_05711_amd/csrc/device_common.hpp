@@ -120,6 +120,16 @@ __device__ __forceinline__ float wave_sum_uniform(float v) {
   return (r0 + r1) + (r2 + r3);
 }
 
+// Integer wave sum with the same DPP pattern; every lane gets the total.
+__device__ __forceinline__ int wave_sum_uniform_i32(int v) {
+  v += __builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false);   // quad [1,0,3,2]
+  v += __builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false);   // quad [2,3,0,1]
+  v += __builtin_amdgcn_update_dpp(v, v, 0x124, 0xF, 0xF, false);  // row_ror:4
+  v += __builtin_amdgcn_update_dpp(v, v, 0x128, 0xF, 0xF, false);  // row_ror:8
+  return (__builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 16)) +
+         (__builtin_amdgcn_readlane(v, 32) + __builtin_amdgcn_readlane(v, 48));
+}
+
 __device__ __forceinline__ int readlane_i32(int v, int lane) {
   return __builtin_amdgcn_readlane(v, lane);
 }

@@ -390,25 +390,27 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
 // ---------------------------------------------------------------- large K (65 .. 4096)
 // One workgroup per (token, head) row, for K beyond one wavefront (eight waves when the final
 // sort holds 2048 keys or more, four below, where more rows share a compute unit):
-//   1. each half is put in (logit desc, index asc) order. A half of at most 512 logits is
-//      ordered by counting, for each key, the larger keys of its half (keys are distinct, so
-//      that count is the key's rank); a longer half by a bitonic sort in LDS;
-//   2. the Cartesian candidates (a, b) with (a+1)(b+1) <= K form a flat list (row rank a
-//      holds min(Kc, floor(K / (a+1))) of them; the offsets depend only on (K, Kr, Kc) and are
-//      computed once per workgroup), and each thread walks a contiguous chunk of it. A
-//      candidate's key is (S as an order-preserving 64-bit integer, ~id);
-//   3. a radix select over the 96-bit keys, eight bits at a time from the top (twelve passes
-//      with an LDS histogram), finds the K-th largest key exactly. Passes walk every candidate
-//      until the keys that share the decided prefix fit in LDS; the next pass also copies
-//      those keys out, and the remaining passes read only the copy (one wave alone takes them
-//      when the copy is short, with no workgroup barriers);
-//   4. the K keys at or above the threshold are gathered and bitonic-sorted descending;
+//   1. each half is put in (logit desc, index asc) order: a half of at most 512 logits by a
+//      bitonic sort in one wave's registers (the two halves on two waves), a longer half by a
+//      bitonic sort in LDS;
+//   2. the K-th largest cell score s* of the grid of the top Kr rows and top Kc columns (the
+//      whole top K lies in it, see the file header). Row rank a holds the cells (a, b) in
+//      descending score as b grows, so the number of its cells scoring at least u is found by
+//      a binary search over the sorted columns. An interval [lo, hi) of ordered-double keys
+//      with count(>= lo) >= K > count(>= hi) is cut in four at every step (three counts per
+//      step, each row searching only between its counts at the two ends), until one of the
+//      counts is exactly K or the interval holds a single score;
+//   3. when several cells score exactly s*, the ones with the lowest ids are taken: within a
+//      row rank such cells have equal column logits, so their column indices ascend with b,
+//      and a second interval search over the id finds the smallest id bound that admits K;
+//   4. the selected cells of row rank a are then its first t_a columns: they are written out
+//      at the offsets of an exclusive scan of t_a and bitonic-sorted descending by (score,
+//      ~id);
 //   5. gates: softmax over the K scores, summed in a fixed order.
-// Integer comparisons throughout, so the result is exact and independent of thread timing.
+// Scores are compared as exact doubles (sums of two floats), integer keys elsewhere, so the
+// result is exact and independent of thread timing.
 
 constexpr int kLargeMaxWaves = 8;  // workgroups of 256 or 512 threads
-constexpr int kRankSortMax = 512;  // halves up to this padded length are ordered by counting
-constexpr int kWaveFinish = 1024;  // radix survivors up to this many are finished by one wave
 
 struct LargeArgs {
   const float* hs;
@@ -420,185 +422,64 @@ struct LargeArgs {
   int k2;   // power of two >= K
 };
 
-// LDS after the sorted halves: the selected keys (k2 of 12 bytes). Before the gather the
-// same bytes hold the radix survivors and, when counting orders the halves, the unsorted
-// half keys.
-size_t large_region_bytes(int n2, int k2) {
-  const size_t sel = (size_t)k2 * 12;
-  const size_t stage = n2 <= kRankSortMax ? (size_t)2 * n2 * 8 : 0;
-  return sel > stage ? sel : stage;
-}
-__device__ __forceinline__ int large_region_bytes_dev(int n2, int k2) {
-  const int sel = k2 * 12;
-  const int stage = n2 <= kRankSortMax ? 2 * n2 * 8 : 0;
-  return sel > stage ? sel : stage;
-}
+// LDS after the sorted halves: the selected keys (k2 of 12 bytes).
+size_t large_region_bytes(int, int k2) { return (size_t)k2 * 12; }
+__device__ __forceinline__ int large_region_bytes_dev(int, int k2) { return k2 * 12; }
 
-// Bytes of dynamic LDS the kernel needs.
+// Bytes of dynamic LDS the kernel needs: the sorted halves, the key region, and two arrays of
+// kr + 1 counts per row rank.
 size_t large_lds_bytes(int n2, int k2, int kr) {
-  return (size_t)2 * n2 * 8 + large_region_bytes(n2, k2) + (size_t)(kr + 1) * 4;
+  return (size_t)2 * n2 * 8 + large_region_bytes(n2, k2) + (size_t)2 * (kr + 1) * 4;
 }
 
 struct LargeShared {
-  uint32_t hist[256];
-  uint64_t ts, ms;   // decided high bits of the threshold key and their mask (score part)
-  uint32_t tn, mn;   // the same for the ~id part
-  int krem;          // keys still to select at and below the current digit
-  int mode;          // 0: walk every candidate; 1: walk and copy the prefix matches; 2: read the copy
-  int nsurv;         // keys copied
-  int count;         // gathered keys
+  int cnt[2][3][kLargeMaxWaves];  // per-wave partial counts, two buffers used in turn
   int wint[kLargeMaxWaves];
   float wsum[kLargeMaxWaves];
   uint64_t wmax[kLargeMaxWaves];
-  int pass0;         // first radix pass (the score bytes before it are shared, see step 3)
 };
 
-// Walks one thread's chunk of the flat candidate list, one candidate after the other. The
-// current row rank's logit (as a double) and id offset stay in registers; the next column key
-// and the next row rank's key and end offset are read one step ahead, so LDS latency overlaps
-// the work on the current candidate. Every row rank below kr holds at least one candidate,
-// so a step moves at most one row rank on.
-struct CandWalk {
-  const uint64_t* rk;
-  const uint64_t* ck;
-  const uint32_t* cum;
-  int kr, nc;
-  int ra, rb, rend;
-  double vr;
-  uint32_t rid;
-  uint64_t cv;     // column key of the current candidate
-  uint64_t rnext;  // key of row rank ra + 1
-  int rend_next;   // end offset of row rank ra + 1
-
-  __device__ __forceinline__ void set_row(uint64_t r) {
-    vr = (double)f32_from_ord((uint32_t)(r >> 32));
-    rid = (0xFFFFFFFFu - (uint32_t)r) * (uint32_t)nc;
+// Number of columns b in [lo, hi) of row value r (ascending b = descending column logit) whose
+// cell scores at least u (ordered-double key); the answer is known to lie in [lo, hi].
+__device__ __forceinline__ int cells_at_least(const uint64_t* ck, double r, uint64_t u, int lo,
+                                              int hi) {
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    const double s = r + (double)f32_from_ord((uint32_t)(ck[mid] >> 32));
+    if (ord_f64(s) >= u) lo = mid + 1; else hi = mid;
   }
-  __device__ __forceinline__ void prefetch_row() {
-    if (ra + 1 < kr) {
-      rnext = rk[ra + 1];
-      rend_next = (int)cum[ra + 2];
-    }
-  }
-  // Positions the walk at candidate c0 of row rank a_first (c0 < P).
-  __device__ __forceinline__ void start(int a_first, int c0) {
-    ra = a_first;
-    rb = c0 - (int)cum[ra];
-    rend = (int)cum[ra + 1];
-    set_row(rk[ra]);
-    cv = ck[rb];
-    prefetch_row();
-  }
-  // Key of candidate c, then a step to c + 1 (c < P; called for consecutive c).
-  __device__ __forceinline__ void next(int c, uint64_t* ks, uint32_t* kn) {
-    *ks = ord_f64(vr + (double)f32_from_ord((uint32_t)(cv >> 32)));
-    *kn = 0xFFFFFFFFu - (rid + (0xFFFFFFFFu - (uint32_t)cv));
-    if (c + 1 >= rend) {
-      if (ra + 1 < kr) {
-        ++ra;
-        rb = 0;
-        rend = rend_next;
-        set_row(rnext);
-        prefetch_row();
-      }
-    } else {
-      ++rb;
-    }
-    cv = ck[rb];  // in bounds also past the last candidate (rb stays below kc)
-  }
-};
-
-// Wave-aggregated append: lanes with take set store (ks, kn) at consecutive slots of
-// (dst_s, dst_n) reserved with one LDS atomic on *counter. Every lane of the wave calls it.
-__device__ __forceinline__ void wave_append(bool take, uint64_t ks, uint32_t kn, int* counter,
-                                            uint64_t* dst_s, uint32_t* dst_n, int cap) {
-  const uint64_t bal = __ballot(take);
-  if (bal == 0ull) return;
-  int base = 0;
-  if (lane_id() == 0) base = atomicAdd(counter, (int)__popcll(bal));
-  base = __builtin_amdgcn_readfirstlane(base);  // lane 0 is active: every lane calls this
-  if (take) {
-    const int pos = base + (int)__popcll(bal & lanemask_lt());
-    if (pos < cap) {
-      dst_s[pos] = ks;
-      dst_n[pos] = kn;
-    }
-  }
+  return lo;
 }
 
-// One radix step, run by all lanes of one wave once the histogram of the current digit is
-// complete: the largest digit whose count of keys at or above it reaches krem becomes part of
-// the threshold. Lane l reads bins 4l .. 4l + 3. Also advances the survivor-copy mode.
-__device__ __forceinline__ void pick_digit(LargeShared& sh, int pass, int mode, int k2) {
-  const int l = lane_id();
-  const int sh_s = 56 - 8 * pass;
-  const int sh_n = 24 - 8 * (pass - 8);
-  const int krem = sh.krem;
-  const uint32_t h0 = sh.hist[4 * l], h1 = sh.hist[4 * l + 1];
-  const uint32_t h2 = sh.hist[4 * l + 2], h3 = sh.hist[4 * l + 3];
-  const int mine = (int)(h0 + h1 + h2 + h3);
-  // suffix sum over lanes >= l
-  int suf = mine;
+// Number of columns b in [lo, hi) whose cell id i * nc + j (column index j = ~key low word)
+// is at most x; j ascends with b inside a run of equal column logits, which [lo, hi) is.
+__device__ __forceinline__ int ids_at_most(const uint64_t* ck, int64_t base, int64_t x, int lo,
+                                           int hi) {
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    const int64_t id = base + (int64_t)(0xFFFFFFFFu - (uint32_t)ck[mid]);
+    if (id <= x) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
+// Sum over the workgroup of three per-thread counts; every thread gets the totals. Buffer
+// `buf` alternates between calls, so one barrier per call suffices: a buffer is written again
+// only after the barrier of the next call, which every thread passes after reading it.
+template <int NW>
+__device__ __forceinline__ void block_sum3(LargeShared& sh, int (&v)[3], int w, int l, int buf) {
 #pragma unroll
-  for (int m = 1; m < kWave; m <<= 1) {
-    const int y = __shfl_down(suf, m, kWave);
-    if (l + m < kWave) suf += y;
+  for (int q = 0; q < 3; ++q) {
+    const int t = wave_sum_uniform_i32(v[q]);
+    if (l == 0) sh.cnt[buf][q][w] = t;
   }
-  const int above = suf - mine;  // keys in bins of higher lanes
-  const uint64_t hit = __ballot(suf >= krem && above < krem);
-  const int L = __ffsll((unsigned long long)hit) - 1;
-  if (l == L) {
-    // within the lane, from bin 4l + 3 down
-    int acc = above, dg;
-    uint32_t in_bin;
-    if (acc + (int)h3 >= krem) {
-      dg = 4 * l + 3;
-      in_bin = h3;
-    } else {
-      acc += (int)h3;
-      if (acc + (int)h2 >= krem) {
-        dg = 4 * l + 2;
-        in_bin = h2;
-      } else {
-        acc += (int)h2;
-        if (acc + (int)h1 >= krem) {
-          dg = 4 * l + 1;
-          in_bin = h1;
-        } else {
-          acc += (int)h1;
-          dg = 4 * l;
-          in_bin = h0;
-        }
-      }
-    }
-    sh.krem = krem - acc;
-    if (pass < 8) {
-      sh.ts |= (uint64_t)dg << sh_s;
-      sh.ms |= (uint64_t)0xFF << sh_s;
-    } else {
-      sh.tn |= (uint32_t)dg << sh_n;
-      sh.mn |= 0xFFu << sh_n;
-    }
-    // the copy is taken by the pass after the one whose chosen bin first fits
-    sh.mode = mode == 1 ? 2 : ((mode == 0 && (int)in_bin <= k2) ? 1 : mode);
-  }
-}
-
-// Histogram of the current digit over the survivor copy, threads tid, tid + stride, ...
-__device__ __forceinline__ void survivor_hist(LargeShared& sh, const uint64_t* sel_s,
-                                              const uint32_t* sel_n, int n, int pass, int tid,
-                                              int stride) {
-  const uint64_t ts = sh.ts, ms = sh.ms;
-  const uint32_t tn = sh.tn, mn = sh.mn;
-  const int sh_s = 56 - 8 * pass;
-  const int sh_n = 24 - 8 * (pass - 8);
-  for (int i = tid; i < n; i += stride) {
-    const uint64_t ks = sel_s[i];
-    const uint32_t kn = sel_n[i];
-    if ((ks & ms) == ts && (kn & mn) == tn) {
-      const uint32_t dg = pass < 8 ? (uint32_t)(ks >> sh_s) & 0xFFu : (kn >> sh_n) & 0xFFu;
-      atomicAdd(&sh.hist[dg], 1u);
-    }
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
+    int t = 0;
+#pragma unroll
+    for (int ww = 0; ww < NW; ++ww) t += sh.cnt[buf][q][ww];
+    v[q] = t;
   }
 }
 
@@ -644,38 +525,57 @@ __device__ __forceinline__ void sort_block8(uint64_t* ks, uint32_t* kn, int k2, 
   }
 }
 
-// Writes the keep largest of the n distinct keys src[0, n) to dst in descending order: the
-// rank of a key is the number of larger keys. src is padded with 0 to an even length and
-// 16-byte aligned; thread t of NT ranks keys t, t + NT, ...
-template <int NT>
-__device__ __forceinline__ void rank_half(const uint64_t* src, int n, int keep, int t,
-                                          uint64_t* dst) {
-  constexpr int kStride = NT;
-  constexpr int S = kRankSortMax / kStride;
-  uint64_t key[S];
-  int rank[S];
+// Descending bitonic sort of 512 keys held by one wave, eight consecutive keys per lane
+// (key i = 8 lane + q in x[q]): partner distances below 8 are exchanges between a lane's own
+// registers, larger ones swap with lane l ^ (distance / 8) through DPP and the lane-half swaps.
+template <int J>
+__device__ __forceinline__ void ce_lanes(uint64_t (&x)[8], int k) {
+  const int l = lane_id();
+  const bool lower = (l & J) == 0;
 #pragma unroll
-  for (int s = 0; s < S; ++s) {
-    const int j = t + kStride * s;
-    key[s] = j < n ? src[j] : ~0ull;
-    rank[s] = 0;
-  }
-  const int n_even = (n + 1) & ~1;
-#pragma unroll 4
-  for (int q = 0; q < n_even; q += 2) {
-    const ulonglong2 p = *reinterpret_cast<const ulonglong2*>(src + q);
-#pragma unroll
-    for (int s = 0; s < S; ++s) rank[s] += (p.x > key[s] ? 1 : 0) + (p.y > key[s] ? 1 : 0);
-  }
-#pragma unroll
-  for (int s = 0; s < S; ++s) {
-    const int j = t + kStride * s;
-    if (j < n && rank[s] < keep) dst[rank[s]] = key[s];
+  for (int q = 0; q < 8; ++q) {
+    const uint64_t o = xor_lane64<J>(x[q]);
+    const bool desc = ((8 * l + q) & k) == 0;
+    x[q] = (lower == desc) ? (x[q] > o ? x[q] : o) : (x[q] > o ? o : x[q]);
   }
 }
 
-template <int NT>
+__device__ __forceinline__ void wave_sort512_desc(uint64_t (&x)[8]) {
+  const int l = lane_id();
+#pragma unroll
+  for (int lk = 1; lk <= 9; ++lk) {
+    const int k = 1 << lk;
+#pragma unroll
+    for (int lj = lk - 1; lj >= 0; --lj) {
+      const int j = 1 << lj;
+      if (j >= 8) {
+        switch (j >> 3) {
+          case 1: ce_lanes<1>(x, k); break;
+          case 2: ce_lanes<2>(x, k); break;
+          case 4: ce_lanes<4>(x, k); break;
+          case 8: ce_lanes<8>(x, k); break;
+          case 16: ce_lanes<16>(x, k); break;
+          default: ce_lanes<32>(x, k); break;
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          if (q & j) continue;
+          const bool desc = ((8 * l + q) & k) == 0;
+          const uint64_t p0 = x[q], p1 = x[q + j];
+          const bool swap = desc ? (p0 < p1) : (p0 > p1);
+          x[q] = swap ? p1 : p0;
+          x[q + j] = swap ? p0 : p1;
+        }
+      }
+    }
+  }
+}
+
+// RPT: row ranks per thread in the searches (kr <= RPT * NT).
+template <int NT, int RPT>
 __global__ __launch_bounds__(NT, NT == 256 ? 5 : 4) void select_large_kernel(LargeArgs a) {
+  constexpr int kRowsPerThread = RPT;
   constexpr int kLargeThreads = NT;
   constexpr int kLargeWaves = NT / kWave;
   static_assert(kLargeWaves <= kLargeMaxWaves, "workgroup size");
@@ -687,60 +587,34 @@ __global__ __launch_bounds__(NT, NT == 256 ? 5 : 4) void select_large_kernel(Lar
   uint64_t* hk = (uint64_t*)smem;                 // [2][n2]: rows, then columns
   uint64_t* sel_s = hk + 2 * n2;                  // [k2]
   uint32_t* sel_n = (uint32_t*)(sel_s + k2);      // [k2]
-  uint32_t* cum = (uint32_t*)((unsigned char*)sel_s + large_region_bytes_dev(n2, k2));  // [kr + 1]
+  // per row rank: the search brackets (counts at the interval's two ends), later t_a and the
+  // exclusive scan of t_a
+  int* cnt_lo = (int*)((unsigned char*)sel_s + large_region_bytes_dev(n2, k2));  // [kr + 1]
+  int* cnt_hi = cnt_lo + (kr + 1);                                                 // [kr + 1]
   const int tid = threadIdx.x, l = lane_id(), w = tid >> 6;
-
-  // candidate offsets: cum[a] = sum over a' < a of min(kc, K / (a' + 1)), by a block scan
-  {
-    const int per = (kr + kLargeThreads - 1) / kLargeThreads;
-    const int a0 = tid * per;
-    int loc = 0;
-    for (int q = a0; q < a0 + per && q < kr; ++q) {
-      const int c = K / (q + 1);
-      loc += c < kc ? c : kc;
-    }
-    const int ex = wave_excl_scan_i32(loc);
-    if (l == kWave - 1) sh.wint[w] = ex + loc;
-    __syncthreads();
-    int off = 0;
-    for (int ww = 0; ww < w; ++ww) off += sh.wint[ww];
-    int run = off + ex;
-    for (int q = a0; q < a0 + per && q < kr; ++q) {
-      cum[q] = (uint32_t)run;
-      const int c = K / (q + 1);
-      run += c < kc ? c : kc;
-    }
-    if (a0 < kr && a0 + per >= kr) cum[kr] = (uint32_t)run;
-    __syncthreads();
-  }
-  const int P = (int)cum[kr];
-  const int chunk = (P + kLargeThreads - 1) / kLargeThreads;  // same on every thread
-  const int c0 = tid * chunk;
-  const int c1 = c0 + chunk < P ? c0 + chunk : P;
-  // first row rank of this thread's chunk (binary search in cum)
-  int a_first = 0;
-  if (c0 < P) {
-    int lo = 0, hi = kr - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if ((int)cum[mid] <= c0) lo = mid; else hi = mid - 1;
-    }
-    a_first = lo;
-  }
+  const uint64_t* ck = hk + n2;
 
   for (int64_t row = blockIdx.x; row < a.rows; row += gridDim.x) {
     const float* hr = a.hs + row * (int64_t)(a.nr + a.nc);
-    // 1. the top kr row keys and top kc column keys, descending
-    if (n2 <= kRankSortMax) {
-      uint64_t* stage = sel_s;  // [2][n2], unsorted, padded with 0 (below every finite logit)
-      for (int i = tid; i < 2 * n2; i += kLargeThreads) {
-        const int h = i >= n2, j = i - h * n2;
-        const int n = h ? a.nc : a.nr;
-        stage[i] = j < n ? logit_key(ord_f32(hr[h * a.nr + j]), j) : 0ull;
+    // 1. the top kr row keys and top kc column keys, descending. Halves of at most 512 logits:
+    // wave 0 sorts the rows and wave 1 the columns, each in its registers; longer halves: a
+    // bitonic sort in LDS by the whole workgroup. Keys are padded with 0 (below every finite
+    // logit).
+    if (n2 <= 512) {
+      if (w < 2) {
+        const int n = w == 0 ? a.nr : a.nc;
+        const float* src = hr + (w == 0 ? 0 : a.nr);
+        uint64_t x[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int j = 8 * l + q;
+          x[q] = j < n ? logit_key(ord_f32(src[j]), j) : 0ull;
+        }
+        wave_sort512_desc(x);
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          if (8 * l + q < n2) hk[w * n2 + 8 * l + q] = x[q];
       }
-      __syncthreads();
-      rank_half<NT>(stage, a.nr, kr, tid, hk);
-      rank_half<NT>(stage + n2, a.nc, kc, tid, hk + n2);
       __syncthreads();
     } else {
       // keys padded with 0 (below every finite logit), both halves sorted descending
@@ -767,25 +641,19 @@ __global__ __launch_bounds__(NT, NT == 256 ? 5 : 4) void select_large_kernel(Lar
         }
       }
     }
-    CandWalk walk;
-    walk.rk = hk;
-    walk.ck = hk + n2;
-    walk.cum = cum;
-    walk.kr = kr;
-    walk.nc = a.nc;
-    // 3. radix select of the K-th largest candidate key, eight bits at a time from the top.
-    // The leading score bytes that every key at or above the threshold shares are skipped: the
-    // largest score is row rank 0 plus column rank 0, and any A x B corner of the sorted grid
-    // with A B >= K holds K cells at or above its last cell, so r[A - 1] + c[B - 1] is at most
-    // the K-th largest score. All keys between the two share their common leading bytes, and no
-    // key lies above the largest, so the search starts below those bytes with krem = K.
+    // 2. the K-th largest score. Start: hi above the largest score (row rank 0 + column rank 0);
+    // lo the best corner bound, r[A - 1] + c[B - 1] over A x B blocks of the sorted grid with
+    // A B >= K (each such block holds K cells at or above its last one). Only the Cartesian
+    // candidates b < min(Kc, K / (a + 1)) are counted: every cell scoring above the K-th score
+    // is one, and a cell past the bound can at most tie with it, behind K cells (file header),
+    // so counting the candidates finds the same score and, below, the same tied cells.
+    uint64_t lo = 0ull, hi;
     {
       const int amin = (K + kc - 1) / kc;
-      uint64_t lo = 0ull;
       for (int A = amin + tid; A <= kr; A += kLargeThreads) {
         const int Bn = (K + A - 1) / A;  // <= kc
         const double v = (double)f32_from_ord((uint32_t)(hk[A - 1] >> 32)) +
-                         (double)f32_from_ord((uint32_t)(hk[n2 + Bn - 1] >> 32));
+                         (double)f32_from_ord((uint32_t)(ck[Bn - 1] >> 32));
         const uint64_t o = ord_f64(v);
         lo = o > lo ? o : lo;
       }
@@ -797,96 +665,170 @@ __global__ __launch_bounds__(NT, NT == 256 ? 5 : 4) void select_large_kernel(Lar
       lo = max_u64(lo, xor_lane64<1>(lo));
       if (l == 0) sh.wmax[w] = lo;
       __syncthreads();
-      if (tid == 0) {
-        for (int ww = 1; ww < kLargeWaves; ++ww) lo = sh.wmax[ww] > lo ? sh.wmax[ww] : lo;
-        const uint64_t hi = ord_f64((double)f32_from_ord((uint32_t)(hk[0] >> 32)) +
-                                    (double)f32_from_ord((uint32_t)(hk[n2] >> 32)));
-        const uint64_t diff = hi ^ lo;
-        const int same = diff == 0ull ? 8 : (int)(__clzll((long long)diff) >> 3);
-        const uint64_t mask = same == 0 ? 0ull : (same == 8 ? ~0ull : ~0ull << (64 - 8 * same));
-        sh.ts = hi & mask;
-        sh.ms = mask;
-        sh.pass0 = same;
-        sh.tn = 0u;
-        sh.mn = 0u;
-        sh.krem = K;
-        sh.mode = 0;
-        sh.nsurv = 0;
-        sh.count = 0;
-      }
-      __syncthreads();
+#pragma unroll
+      for (int ww = 0; ww < kLargeWaves; ++ww) lo = sh.wmax[ww] > lo ? sh.wmax[ww] : lo;
+      hi = ord_f64((double)f32_from_ord((uint32_t)(hk[0] >> 32)) +
+                   (double)f32_from_ord((uint32_t)(ck[0] >> 32))) + 1ull;
     }
-    int pass = sh.pass0;
-    for (; pass < 12; ++pass) {
-      for (int i = tid; i < 256; i += kLargeThreads) sh.hist[i] = 0u;
-      __syncthreads();
-      const uint64_t ts = sh.ts, ms = sh.ms;
-      const uint32_t tn = sh.tn, mn = sh.mn;
-      const int mode = sh.mode;
-      const int nsurv = sh.nsurv < k2 ? sh.nsurv : k2;
-      if (mode == 2 && nsurv <= kWaveFinish) break;  // the same on every thread
-      const int sh_s = 56 - 8 * pass;            // digit position in the score word (pass < 8)
-      const int sh_n = 24 - 8 * (pass - 8);      // digit position in the id word (pass >= 8)
-      if (mode == 2) {
-        survivor_hist(sh, sel_s, sel_n, nsurv, pass, tid, kLargeThreads);
-      } else {
-        // runs of equal digits along the chunk are counted before one LDS atomic, so bins that
-        // nearly every candidate hits are not serialised over all of them
-        uint32_t run_dg = 0u, run_n = 0u;
-        if (c0 < P) walk.start(a_first, c0);
-        for (int it = 0; it < chunk; ++it) {
-          const int c = c0 + it;
-          const bool live = c < c1;
-          uint64_t ks = 0ull;
-          uint32_t kn = 0u;
-          if (live) walk.next(c, &ks, &kn);
-          const bool match = live && (ks & ms) == ts && (kn & mn) == tn;
-          if (match) {
-            const uint32_t dg = pass < 8 ? (uint32_t)(ks >> sh_s) & 0xFFu : (kn >> sh_n) & 0xFFu;
-            if (run_n != 0u && dg != run_dg) {
-              atomicAdd(&sh.hist[run_dg], run_n);
-              run_n = 0u;
-            }
-            run_dg = dg;
-            ++run_n;
+    // this thread's row ranks r = tid + i NT: value, and the bracket [count at hi, count at lo]
+    double rv[kRowsPerThread];
+    int b_hi[kRowsPerThread], b_lo[kRowsPerThread];
+#pragma unroll
+    for (int i = 0; i < kRowsPerThread; ++i) {
+      const int r = tid + i * kLargeThreads;
+      rv[i] = r < kr ? (double)f32_from_ord((uint32_t)(hk[r] >> 32)) : 0.0;
+      b_hi[i] = 0;
+      const int cap = K / (r + 1);
+      b_lo[i] = r < kr ? (cap < kc ? cap : kc) : 0;
+    }
+    int buf = 0;
+    bool done = false;
+    while (hi - lo > 1ull) {  // lo and hi are the same on every thread
+      const uint64_t step = (hi - lo) >> 2;
+      uint64_t u[3];
+#pragma unroll
+      for (int q = 0; q < 3; ++q) {
+        const uint64_t o = step ? step * (uint64_t)(q + 1) : (uint64_t)(q + 1);
+        u[q] = lo + (o < hi - lo ? o : hi - lo - 1);
+      }
+      int cnt[kRowsPerThread][3];
+      int tot[3] = {0, 0, 0};
+#pragma unroll
+      for (int i = 0; i < kRowsPerThread; ++i) {
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+          cnt[i][q] = cells_at_least(ck, rv[i], u[q], b_hi[i], b_lo[i]);
+          tot[q] += cnt[i][q];
+        }
+      }
+      block_sum3<kLargeWaves>(sh, tot, w, l, buf);
+      buf ^= 1;
+      const int exact = tot[0] == K ? 0 : (tot[1] == K ? 1 : (tot[2] == K ? 2 : -1));
+      if (exact >= 0) {  // the selection is the cells scoring at least u[exact]
+#pragma unroll
+        for (int i = 0; i < kRowsPerThread; ++i) b_lo[i] = cnt[i][exact];
+        done = true;
+        break;
+      }
+      // the piece [u_j, u_j+1) holding the K-th score, u_0 = lo and u_4 = hi
+      int j = 0;
+#pragma unroll
+      for (int q = 0; q < 3; ++q) j += tot[q] >= K ? 1 : 0;
+#pragma unroll
+      for (int i = 0; i < kRowsPerThread; ++i) {
+        if (j > 0) b_lo[i] = cnt[i][j - 1];
+        if (j < 3) b_hi[i] = cnt[i][j];
+      }
+      if (j > 0) lo = u[j - 1];
+      if (j < 3) hi = u[j];
+    }
+    // 3. unless a count hit K, the interval holds the one score s* = lo. b_hi counts the
+    // candidates of a row above it and b_lo those at or above it (both ends were counted, or
+    // are the start's bounds; the rows confirm them here).
+    if (!done) {
+      int tot[3] = {0, 0, 0};
+#pragma unroll
+      for (int i = 0; i < kRowsPerThread; ++i) {
+        const int r = tid + i * kLargeThreads;
+        const int cap = K / (r + 1);
+        const int g = cells_at_least(ck, rv[i], hi, 0, r < kr ? (cap < kc ? cap : kc) : 0);
+        const int e = cells_at_least(ck, rv[i], lo, g, r < kr ? (cap < kc ? cap : kc) : 0);
+        b_hi[i] = g;
+        b_lo[i] = e;
+        tot[0] += g;
+        tot[1] += e;
+      }
+      block_sum3<kLargeWaves>(sh, tot, w, l, buf);
+      buf ^= 1;
+      const int krem = K - tot[0];  // cells to take among those scoring exactly s*
+      if (tot[1] - tot[0] > krem) {
+        // the smallest id bound x with krem tied cells of id <= x; invariant
+        // count(<= xlo) < krem <= count(<= xhi)
+        int64_t xlo = -1, xhi = (int64_t)a.nr * a.nc - 1;
+        // id of the row's first column: i a.nc, i the row index of rank r (read from LDS)
+        auto base = [&](int i) -> int64_t {
+          const int r = tid + i * kLargeThreads;
+          return r < kr ? (int64_t)(0xFFFFFFFFu - (uint32_t)hk[r]) * a.nc : 0;
+        };
+        while (xhi - xlo > 1) {
+          const int64_t step = (xhi - xlo) >> 2;
+          int64_t xs[3];
+#pragma unroll
+          for (int q = 0; q < 3; ++q) {
+            const int64_t o = step ? step * (q + 1) : (int64_t)(q + 1);
+            xs[q] = xlo + (o < xhi - xlo ? o : xhi - xlo - 1);
           }
-          if (mode == 1) wave_append(match, ks, kn, &sh.nsurv, sel_s, sel_n, k2);
+          int t3[3] = {0, 0, 0};
+#pragma unroll
+          for (int i = 0; i < kRowsPerThread; ++i)
+#pragma unroll
+            for (int q = 0; q < 3; ++q)
+              t3[q] += ids_at_most(ck, base(i), xs[q], b_hi[i], b_lo[i]) - b_hi[i];
+          block_sum3<kLargeWaves>(sh, t3, w, l, buf);
+          buf ^= 1;
+          int j = 0;  // thresholds that admit fewer than krem
+#pragma unroll
+          for (int q = 0; q < 3; ++q) j += t3[q] >= krem ? 0 : 1;
+          if (j > 0) xlo = xs[j - 1];
+          if (j < 3) xhi = xs[j];
         }
-        if (run_n != 0u) atomicAdd(&sh.hist[run_dg], run_n);
+#pragma unroll
+        for (int i = 0; i < kRowsPerThread; ++i)
+          b_lo[i] = ids_at_most(ck, base(i), xhi, b_hi[i], b_lo[i]);
       }
-      __syncthreads();
-      if (w == 0) pick_digit(sh, pass, mode, k2);
-      __syncthreads();
     }
-    if (pass < 12) {
-      // a short survivor copy: wave 0 alone takes the remaining digits, with no workgroup
-      // barriers between them
-      if (w == 0) {
-        const int nsurv = sh.nsurv < k2 ? sh.nsurv : k2;
-        for (; pass < 12; ++pass) {
-          for (int i = l; i < 256; i += kWave) sh.hist[i] = 0u;
-          wave_lds_sync();
-          survivor_hist(sh, sel_s, sel_n, nsurv, pass, l, kWave);
-          wave_lds_sync();
-          pick_digit(sh, pass, 2, k2);
-          wave_lds_sync();
-        }
-      }
-      __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kRowsPerThread; ++i) {
+      const int r = tid + i * kLargeThreads;
+      if (r < kr) cnt_lo[r] = b_lo[i];
     }
-    // 4. the threshold key is exact now; gather the K keys at or above it
+    __syncthreads();
+    // 4. t_a = cnt_lo[a] selected cells in row rank a: exclusive scan into cnt_hi, then the
+    // keys at their offsets. Threads scan contiguous chunks of row ranks.
     {
-      const uint64_t ts = sh.ts;
-      const uint32_t tn = sh.tn;
-      if (c0 < P) walk.start(a_first, c0);
-      for (int it = 0; it < chunk; ++it) {
-        const int c = c0 + it;
-        const bool live = c < c1;
-        uint64_t ks = 0ull;
-        uint32_t kn = 0u;
-        if (live) walk.next(c, &ks, &kn);
-        const bool take = live && (ks > ts || (ks == ts && kn >= tn));
-        wave_append(take, ks, kn, &sh.count, sel_s, sel_n, k2);
+      const int per = (kr + kLargeThreads - 1) / kLargeThreads;
+      const int a0 = tid * per;
+      int loc = 0;
+      for (int q = a0; q < a0 + per && q < kr; ++q) loc += cnt_lo[q];
+      const int ex = wave_excl_scan_i32(loc);
+      if (l == kWave - 1) sh.wint[w] = ex + loc;
+      __syncthreads();
+      int off = 0;
+      for (int ww = 0; ww < w; ++ww) off += sh.wint[ww];
+      int run = off + ex;
+      for (int q = a0; q < a0 + per && q < kr; ++q) {
+        cnt_hi[q] = run;
+        run += cnt_lo[q];
+      }
+      if (a0 < kr && a0 + per >= kr) cnt_hi[kr] = run;  // = K
+      __syncthreads();
+      // each thread writes a contiguous chunk of positions: one search for the row rank of its
+      // first position (the last rank whose offset is <= it), then a walk along the rows
+      const int chunk = (K + kLargeThreads - 1) / kLargeThreads;
+      const int q0 = tid * chunk;
+      const int q1 = q0 + chunk < K ? q0 + chunk : K;
+      if (q0 < q1) {
+        int ra = 0, hi = kr - 1;
+        while (ra < hi) {
+          const int mid = (ra + hi + 1) >> 1;
+          if (cnt_hi[mid] <= q0) ra = mid; else hi = mid - 1;
+        }
+        int next = cnt_hi[ra + 1];  // first position of the next row rank
+        uint64_t rk = hk[ra];
+        double rvv = (double)f32_from_ord((uint32_t)(rk >> 32));
+        uint32_t rid = (0xFFFFFFFFu - (uint32_t)rk) * (uint32_t)a.nc;
+        for (int q = q0; q < q1; ++q) {
+          while (q >= next) {  // row ranks with no selected cell are skipped
+            ++ra;
+            next = cnt_hi[ra + 1];
+            rk = hk[ra];
+            rvv = (double)f32_from_ord((uint32_t)(rk >> 32));
+            rid = (0xFFFFFFFFu - (uint32_t)rk) * (uint32_t)a.nc;
+          }
+          const uint64_t cq = ck[q - cnt_hi[ra]];
+          sel_s[q] = ord_f64(rvv + (double)f32_from_ord((uint32_t)(cq >> 32)));
+          sel_n[q] = 0xFFFFFFFFu - (rid + (0xFFFFFFFFu - (uint32_t)cq));
+        }
       }
       for (int i = K + tid; i < k2; i += kLargeThreads) {
         sel_s[i] = 0ull;
@@ -950,6 +892,7 @@ __global__ __launch_bounds__(NT, NT == 256 ? 5 : 4) void select_large_kernel(Lar
     __syncthreads();
   }
 }
+
 
 // ---------------------------------------------------------------- dense router (ablation)
 // Top K of all N logits of one (token, head) row by (logit desc, id asc), then softmax gates:
@@ -1061,11 +1004,24 @@ hipError_t launch_select(const Shape& s, const float* half_scores, int32_t* idx,
     const size_t lds = large_lds_bytes(n2, k2, kr);
     const dim3 grid((unsigned)(s.rows < 4096 ? s.rows : 4096));
     // eight waves per row once the final sort has 2048 keys or more; four below, where more
-    // rows share a compute unit
-    if (k2 >= 2048)
-      hipLaunchKernelGGL(select_large_kernel<512>, grid, dim3(512), lds, st, a);
-    else
-      hipLaunchKernelGGL(select_large_kernel<256>, grid, dim3(256), lds, st, a);
+    // rows share a compute unit. Each thread searches over ceil(kr / threads) row ranks,
+    // rounded up to a power of two (kr <= K <= 4096).
+    const int nt = k2 >= 2048 ? 512 : 256;
+    const int need = (kr + nt - 1) / nt;
+    const int rpt = need <= 1 ? 1 : (need <= 2 ? 2 : (need <= 4 ? 4 : 8));
+#define OMNIMOE_SELECT_LARGE(NT_, RPT_)                                                    \
+  hipLaunchKernelGGL((select_large_kernel<NT_, RPT_>), grid, dim3(NT_), lds, st, a)
+    if (nt == 512) {
+      if (rpt == 1) OMNIMOE_SELECT_LARGE(512, 1);
+      else if (rpt == 2) OMNIMOE_SELECT_LARGE(512, 2);
+      else if (rpt == 4) OMNIMOE_SELECT_LARGE(512, 4);
+      else OMNIMOE_SELECT_LARGE(512, 8);
+    } else {
+      if (rpt == 1) OMNIMOE_SELECT_LARGE(256, 1);
+      else if (rpt == 2) OMNIMOE_SELECT_LARGE(256, 2);
+      else OMNIMOE_SELECT_LARGE(256, 4);
+    }
+#undef OMNIMOE_SELECT_LARGE
     return hipGetLastError();
   }
   SelectArgs a;
