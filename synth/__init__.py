@@ -161,6 +161,23 @@ WORKLOADS: Dict[str, Workload] = {
                                 d_key=512, H=1, K=512),
     "paper_k4096_bf16": Workload("paper_k4096_bf16", T=4096, d=1024, n_rows=320, n_cols=320,
                                  d_key=512, H=1, K=4096),
+    # The paper's speed-benchmark sweeps (its benchmark table): the activated-expert budget
+    # K = 512 .. 4096 at 1k tokens, and 1k .. 16k tokens at K = 512 (4k tokens is
+    # paper_k512_bf16 above).
+    "paper_t1k_k512_bf16": Workload("paper_t1k_k512_bf16", T=1024, d=1024, n_rows=320,
+                                    n_cols=320, d_key=512, H=1, K=512),
+    "paper_t1k_k1024_bf16": Workload("paper_t1k_k1024_bf16", T=1024, d=1024, n_rows=320,
+                                     n_cols=320, d_key=512, H=1, K=1024),
+    "paper_t1k_k2048_bf16": Workload("paper_t1k_k2048_bf16", T=1024, d=1024, n_rows=320,
+                                     n_cols=320, d_key=512, H=1, K=2048),
+    "paper_t1k_k4096_bf16": Workload("paper_t1k_k4096_bf16", T=1024, d=1024, n_rows=320,
+                                     n_cols=320, d_key=512, H=1, K=4096),
+    "paper_t2k_k512_bf16": Workload("paper_t2k_k512_bf16", T=2048, d=1024, n_rows=320,
+                                    n_cols=320, d_key=512, H=1, K=512),
+    "paper_t8k_k512_bf16": Workload("paper_t8k_k512_bf16", T=8192, d=1024, n_rows=320,
+                                    n_cols=320, d_key=512, H=1, K=512),
+    "paper_t16k_k512_bf16": Workload("paper_t16k_k512_bf16", T=16384, d=1024, n_rows=320,
+                                     n_cols=320, d_key=512, H=1, K=512),
     # One decode step of a batch of 64, and a single token.
     "decode64_bf16": Workload("decode64_bf16", T=64, d=2048, n_rows=1024, n_cols=1024,
                               d_key=1024, H=8, K=16),
