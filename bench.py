@@ -313,6 +313,57 @@ def extras(args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1, 
             f"{perg['expert_dot']:.3f} ms vs per-task {per['expert_dot']:.3f} ms)")
         del wsg, yg
 
+    # The second product of Eq. 14 per group (partial rows per (group, token) slot, then a
+    # token-major sum over groups) against the grouped path's slot-order sum, for each B.
+    group_rows = None
+    if w.bf16 and w.d % 64 == 0 and args.group_rows_b:
+        group_rows = []
+        for gb in [int(b) for b in args.group_rows_b.split(",")]:
+            wg = w.with_(group_size=gb)
+            dg = P.make_desc(wg)
+            need = P.omnimoe_workspace_size(dg, 10)
+            if need > (8 << 30):
+                group_rows.append({"group_size": gb, "skipped": f"workspace {need / 2**30:.1f} GiB"})
+                continue
+            permg = torch.empty(w.M, dtype=torch.int32, device="cuda")
+            cap = min(w.M, w.N)
+            actg = torch.empty(cap, dtype=torch.int32, device="cuda")
+            offg = torch.empty(cap + 1, dtype=torch.int32, device="cuda")
+            nag = torch.empty(1, dtype=torch.int32, device="cuda")
+            P.omnimoe_schedule(dg, idx, permg, actg, offg, nag)
+            wsr = P.workspace(dg, 10)
+            wsq = P.workspace(dg, 8)
+            yr = torch.empty_like(y)
+            yq = torch.empty_like(y)
+            runs = {
+                "group_rows": lambda: P.omnimoe_expert_forward_group_rows(
+                    dg, d_in["x"], d_in["u"], d_in["v"], idx, g, permg, actg, nag, yr, ws=wsr,
+                    stream=stream),
+                "grouped_slot_order_sum": lambda: P.omnimoe_expert_forward_grouped(
+                    dg, d_in["x"], d_in["u"], d_in["v"], idx, g, permg, actg, nag, yq, ws=wsq,
+                    stream=stream),
+            }
+            rec = {"group_size": gb}
+            for name, fn in runs.items():
+                for _ in range(2):
+                    fn()
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for _ in range(args.steps):
+                    fn()
+                e1.record(stream)
+                torch.cuda.synchronize()
+                rec[name + "_ms"] = e0.elapsed_time(e1) / args.steps
+            rec["max_row_rel_diff"] = float(((yr - yq).abs().amax(dim=1) /
+                                             yq.abs().amax(dim=1).clamp_min(1e-30)).max())
+            rec["per_task_expert_stage_ms"] = per["expert_dot"] + per["accumulate"]
+            group_rows.append(rec)
+            log(f"group rows, B={gb}: {rec['group_rows_ms']:.3f} ms (grouped dot + slot-order sum "
+                f"{rec['grouped_slot_order_sum_ms']:.3f} ms; per-task stage "
+                f"{rec['per_task_expert_stage_ms']:.3f} ms)")
+            del wsr, wsq, yr, yq, permg, actg, offg, nag
+
     # Backward of the expert compute (training): token pass, per-expert pass over the
     # schedule's segments, softmax pass; dy is a seeded standard normal.
     perm, off, na, n_active = sched
@@ -356,7 +407,7 @@ def extras(args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1, 
                     "tokens_per_s": w.T / ((bw_ms + rb_ms) * 1e-3)}
         log(f"expert backward: {bw_ms:.3f} ms, router backward: {rb_ms:.3f} ms")
         del dy, dx, du, dv, wsb, dkr, dkc, wsr
-    return ablation, shared_mlp, no_cpr, backward, grouped, contrib
+    return ablation, shared_mlp, no_cpr, backward, grouped, contrib, group_rows
 
 
 def main():
@@ -386,6 +437,9 @@ def main():
     ap.add_argument("--grouped-b", type=int, default=64,
                     help="group size of the grouped-GEMM comparison timed beside the layer "
                          "(0: skip)")
+    ap.add_argument("--group-rows-b", default="",
+                    help="comma-separated group sizes at which the second product of Eq. 14 per "
+                         "group (partial rows) is timed against the slot-order sum")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="after timing, run a plain device copy of this many bytes twice "
                          "(a known-size reference for rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -505,9 +559,9 @@ def main():
     routing = routing_stats(idx.cpu().numpy(), w.N)
     assert routing["n_active"] == n_active
 
-    ablation = shared_mlp = no_cpr = backward = grouped = contrib = None
+    ablation = shared_mlp = no_cpr = backward = grouped = contrib = group_rows = None
     if not args.layer_only:
-        ablation, shared_mlp, no_cpr, backward, grouped, contrib = extras(
+        ablation, shared_mlp, no_cpr, backward, grouped, contrib, group_rows = extras(
             args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1,
             (perm, off, na, n_active))
 
@@ -585,6 +639,7 @@ def main():
         "ablation_no_schedule": ablation,
         "ablation_no_cartesian_router": no_cpr,
         "grouped_expert_gemm": grouped,
+        "group_rows_second_product": group_rows,
         "accumulate_contribution_rows": contrib,
         "n_active": n_active, "eta": w.M / max(1, n_active), "routing": routing,
         "schedule_share": per["schedule"] / sum(per.values()),

@@ -103,7 +103,8 @@ typedef enum {
   OMNIMOE_STAGE_EXPERT_BACKWARD = 6, /* omnimoe_expert_backward */
   OMNIMOE_STAGE_ROUTE_BACKWARD = 7,  /* omnimoe_route_backward */
   OMNIMOE_STAGE_EXPERT_GROUPED = 8,  /* omnimoe_expert_forward_grouped */
-  OMNIMOE_STAGE_EXPERT_SCATTER = 9   /* omnimoe_expert_forward_scatter */
+  OMNIMOE_STAGE_EXPERT_SCATTER = 9,  /* omnimoe_expert_forward_scatter */
+  OMNIMOE_STAGE_EXPERT_GROUP_ROWS = 10 /* omnimoe_expert_forward_group_rows */
 } omnimoe_stage;
 
 /* Bytes of workspace the given stage's entry point needs for this shape. */
@@ -203,6 +204,25 @@ omnimoe_status omnimoe_expert_forward_grouped(const omnimoe_layer_desc* desc, co
                                               const int32_t* active, const int32_t* n_active,
                                               float* y, void* workspace, size_t workspace_bytes,
                                               void* stream);
+
+/* Eq. 14 with both products group by group: the activations as in
+ * omnimoe_expert_forward_grouped, then the second product (.)V_q per group. For every slot s
+ * (a token t with tasks in group q, all of them adjacent in perm) a partial row
+ * O[s] = sum over those tasks, in perm order, of a_p v_e (fp32, d wide), and then
+ * y_t = sum of t's slot rows in group order. Arguments and layouts as
+ * omnimoe_expert_forward_grouped (perm in (group, task id) order for desc->group_size).
+ * The partial rows are written to and read back from the workspace: they move fewer bytes
+ * than gathering v per task only when a token has many tasks per group (large groups, many
+ * tasks per expert). bf16 and d % 64 == 0, else OMNIMOE_ERR_UNSUPPORTED. The result is the
+ * same on every run. Workspace: OMNIMOE_STAGE_EXPERT_GROUP_ROWS bytes (the partial rows are
+ * sized for min(M, ceil(min(M, N) / B) T) slots). */
+omnimoe_status omnimoe_expert_forward_group_rows(const omnimoe_layer_desc* desc, const void* x,
+                                                 const void* u, const void* v,
+                                                 const int32_t* idx, const float* gates,
+                                                 const int32_t* perm, const int32_t* active,
+                                                 const int32_t* n_active, float* y,
+                                                 void* workspace, size_t workspace_bytes,
+                                                 void* stream);
 
 /* Expert compute with the output stage in expert-major order, as the scatter-add of Eq. 14
  * orders it, made deterministic by a token-major reduction (the accumulate variant that reads

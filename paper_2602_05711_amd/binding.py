@@ -19,7 +19,7 @@ OMNIMOE_ACT_GELU, OMNIMOE_ACT_SILU = 0, 1
 OMNIMOE_QUERY_SPLIT, OMNIMOE_QUERY_SHARED = 0, 1
 (STAGE_ROUTE, STAGE_SELECT, STAGE_SCHEDULE, STAGE_EXPERT, STAGE_LAYER, STAGE_ROUTE_DENSE,
  STAGE_EXPERT_BACKWARD, STAGE_ROUTE_BACKWARD, STAGE_EXPERT_GROUPED,
- STAGE_EXPERT_SCATTER) = range(10)
+ STAGE_EXPERT_SCATTER, STAGE_EXPERT_GROUP_ROWS) = range(11)
 KERNEL_NAMES = ("score", "select", "schedule", "expert_dot", "accumulate")
 
 EXPORTED = (
@@ -28,6 +28,7 @@ EXPORTED = (
     "omnimoe_schedule",
     "omnimoe_expert_forward", "omnimoe_expert_forward_grouped",
     "omnimoe_expert_forward_scatter", "omnimoe_expert_forward_token_centric",
+    "omnimoe_expert_forward_group_rows",
     "omnimoe_expert_backward",
     "omnimoe_route_backward",
     "omnimoe_layer_forward", "omnimoe_layer_forward_noalloc", "omnimoe_timer_create",
@@ -74,6 +75,7 @@ def load_library():
         "omnimoe_expert_forward": [D, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_expert_forward_grouped": [D, P, P, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_expert_forward_scatter": [D, P, P, P, P, P, P, P, P, SZ, P],
+        "omnimoe_expert_forward_group_rows": [D, P, P, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_expert_forward_token_centric": [D, P, P, P, P, P, P, P],
         "omnimoe_expert_backward": [D, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_route_backward": [D, P, P, P, P, P, P, P, P, P, SZ, P],
@@ -203,6 +205,15 @@ def omnimoe_expert_forward_grouped(desc, x, u, v, idx, gates, perm, active, n_ac
     if ws is None:
         ws = workspace(desc, STAGE_EXPERT_GROUPED, x.device)
     _check("omnimoe_expert_forward_grouped", load_library().omnimoe_expert_forward_grouped(
+        ctypes.byref(desc), _ptr(x), _ptr(u), _ptr(v), _ptr(idx), _ptr(gates), _ptr(perm),
+        _ptr(active), _ptr(n_active), _ptr(y), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def omnimoe_expert_forward_group_rows(desc, x, u, v, idx, gates, perm, active, n_active, y,
+                                     ws=None, stream=None):
+    if ws is None:
+        ws = workspace(desc, STAGE_EXPERT_GROUP_ROWS, x.device)
+    _check("omnimoe_expert_forward_group_rows", load_library().omnimoe_expert_forward_group_rows(
         ctypes.byref(desc), _ptr(x), _ptr(u), _ptr(v), _ptr(idx), _ptr(gates), _ptr(perm),
         _ptr(active), _ptr(n_active), _ptr(y), _ptr(ws), ws.numel(), _stream(stream)))
 

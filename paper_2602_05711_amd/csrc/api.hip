@@ -104,6 +104,13 @@ hipError_t routed_sum(const Shape& s, const void* v, const int32_t* idx, const f
   return omnimoe::launch_accumulate(s, v, idx, abuf, y, st);
 }
 
+// Slots (group, token) of a schedule with groups of B: at most one per task, and at most one
+// per token in each of the ceil(min(M, N) / B) groups.
+int64_t group_rows_bound(const Shape& s) {
+  const int64_t groups = (std::min(s.M, s.N) + s.B - 1) / s.B;
+  return std::min(s.M, groups * s.T);
+}
+
 size_t sched_or_plan_bytes(const Shape& s) {
   const size_t sb = omnimoe::schedule_ws_bytes(s.M, s.N);
   return layer_grouped(s) ? sb + omnimoe::group_plan_ws_bytes(s) : sb;
@@ -119,6 +126,11 @@ size_t stage_bytes(const Shape& s, int stage) {
     case OMNIMOE_STAGE_EXPERT_BACKWARD: return omnimoe::backward_ws_bytes(s.M);
     case OMNIMOE_STAGE_ROUTE_BACKWARD: return omnimoe::route_backward_ws_bytes(s);
     case OMNIMOE_STAGE_EXPERT_SCATTER: return m_bytes(s) + align_up((size_t)s.M * s.d * 4);
+    case OMNIMOE_STAGE_EXPERT_GROUP_ROWS: {
+      const int64_t n = group_rows_bound(s);
+      return m_bytes(s) + omnimoe::group_plan_ws_bytes(s) + align_up((size_t)n * s.d * 4) +
+             omnimoe::slot_sort_ws_bytes(n, s.T);
+    }
     case OMNIMOE_STAGE_EXPERT_GROUPED:  // the plan is dead once the grouped dot has run
       return m_bytes(s) + std::max(omnimoe::group_plan_ws_bytes(s),
                                    omnimoe::dense_accumulate_ws_bytes(s));
@@ -246,7 +258,7 @@ const char* omnimoe_status_string(int32_t status) {
 omnimoe_status omnimoe_workspace_size(const omnimoe_layer_desc* desc, int32_t stage,
                                       size_t* bytes) {
   if (!bytes) return OMNIMOE_ERR_INVALID_ARG;
-  if (stage < OMNIMOE_STAGE_ROUTE || stage > OMNIMOE_STAGE_EXPERT_SCATTER)
+  if (stage < OMNIMOE_STAGE_ROUTE || stage > OMNIMOE_STAGE_EXPERT_GROUP_ROWS)
     return OMNIMOE_ERR_INVALID_ARG;
   Shape s;
   omnimoe_status st = check_desc(desc, &s);
@@ -447,6 +459,38 @@ omnimoe_status omnimoe_expert_forward_grouped(const omnimoe_layer_desc* desc, co
   if (e == hipSuccess)
     e = omnimoe::launch_grouped_dot(s, x, u, gates, perm, active, n_active, plan, abuf, strm);
   if (e == hipSuccess) e = routed_sum(s, v, idx, abuf, y, (char*)ws + m_bytes(s), strm);
+  return hip_status(e);
+}
+
+omnimoe_status omnimoe_expert_forward_group_rows(const omnimoe_layer_desc* desc, const void* x,
+                                                 const void* u, const void* v,
+                                                 const int32_t* idx, const float* gates,
+                                                 const int32_t* perm, const int32_t* active,
+                                                 const int32_t* n_active, float* y, void* ws,
+                                                 size_t ws_bytes, void* stream) {
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  if (s.T == 0) return OMNIMOE_OK;
+  if ((st = check_ptrs({x, u, v, idx, gates, perm, active, n_active, y, ws}))) return st;
+  if (!grouped_supported(s)) return OMNIMOE_ERR_UNSUPPORTED;
+  if (ws_bytes < stage_bytes(s, OMNIMOE_STAGE_EXPERT_GROUP_ROWS)) return OMNIMOE_ERR_WORKSPACE;
+  hipStream_t strm = (hipStream_t)stream;
+  const int64_t n = group_rows_bound(s);
+  char* w = (char*)ws;
+  float* abuf = (float*)w; w += m_bytes(s);
+  void* plan_ws = w; w += omnimoe::group_plan_ws_bytes(s);
+  float* rows = (float*)w; w += align_up((size_t)n * s.d * 4);
+  void* sort_ws = w;
+  omnimoe::GroupPlan plan;
+  omnimoe::SlotOrder order;
+  hipError_t e = omnimoe::launch_group_plan(s, perm, n_active, nullptr, idx, active, plan_ws,
+                                            &plan, strm);
+  if (e == hipSuccess)
+    e = omnimoe::launch_grouped_dot(s, x, u, gates, perm, active, n_active, plan, abuf, strm);
+  if (e == hipSuccess) e = omnimoe::launch_slot_sort(plan, n, s.T, sort_ws, &order, strm);
+  if (e == hipSuccess)
+    e = omnimoe::launch_group_rows(s, v, idx, perm, abuf, plan, order, rows, n, y, strm);
   return hip_status(e);
 }
 

@@ -285,6 +285,162 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_dot_kernel(GroupedDotArgs
   }
 }
 
+// ---------------------------------------------------------------- second product per group
+// O[s] = sum over the tasks of slot s (sorted positions slot_off[s] .. slot_off[s + 1], one
+// token's tasks in one group) of a_p v_e, in position order, fp32. One wave per slot; each
+// XCD takes a contiguous range of slots (workgroup b runs on XCD b % 8), i.e. whole groups one
+// after the other, so a group's v rows are fetched from HBM once and then found in that XCD's
+// L2. Columns go in chunks of 512 (eight per lane, one 16-byte load of bf16 per task).
+struct GroupRowsArgs {
+  const uint16_t* v;
+  const int32_t* idx;
+  const int32_t* perm;
+  const float* a;
+  const int32_t* slot_off;
+  const int32_t* counters;
+  float* rows;
+  int64_t M, N, n_max;
+  int d;
+};
+
+__device__ __forceinline__ void fma_bf16x8(float (&acc)[8], float w, uint4 q) {
+  acc[0] += w * bf16_lo(q.x); acc[1] += w * bf16_hi(q.x);
+  acc[2] += w * bf16_lo(q.y); acc[3] += w * bf16_hi(q.y);
+  acc[4] += w * bf16_lo(q.z); acc[5] += w * bf16_hi(q.z);
+  acc[6] += w * bf16_lo(q.w); acc[7] += w * bf16_hi(q.w);
+}
+
+// Columns in passes of 512 CH (CH 16-byte bf16 loads per lane and task, 8 CH fp32 sums per
+// lane); the tasks of a slot four at a time, their rows all requested before the sums.
+template <int CH>
+__device__ __forceinline__ void group_row_pass(const GroupRowsArgs& g, int64_t s, int p0, int p1,
+                                               int c0) {
+  typedef float f32x4_t __attribute__((ext_vector_type(4)));
+  const int l = lane_id();
+  float acc[CH][8];
+#pragma unroll
+  for (int h = 0; h < CH; ++h)
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[h][k] = 0.f;
+  bool on[CH];
+#pragma unroll
+  for (int h = 0; h < CH; ++h) on[h] = c0 + 512 * h + 8 * l < g.d;
+  for (int b0 = p0; b0 < p1; b0 += kWave) {
+    int e = 0;  // lane j: expert and activation of task b0 + j
+    float av = 0.f;
+    if (b0 + l < p1) {
+      int32_t p = g.perm[b0 + l];
+      p = p < 0 ? 0 : (p >= g.M ? (int32_t)(g.M - 1) : p);
+      const int32_t ee = g.idx[p];
+      e = ee < 0 ? 0 : (ee >= g.N ? (int)(g.N - 1) : ee);
+      av = g.a[p];
+    }
+    const int nb = p1 - b0 < kWave ? p1 - b0 : kWave;
+    for (int i = 0; i < nb; i += 4) {
+      uint4 q[4][CH];
+      float w4[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const bool live = i + u < nb;  // wave-uniform
+        const int ei = readlane_i32(e, live ? i + u : 0);
+        w4[u] = live ? readlane_f32(av, i + u) : 0.f;
+        const uint16_t* row = g.v + (int64_t)ei * g.d + c0 + 8 * l;
+#pragma unroll
+        for (int h = 0; h < CH; ++h)
+          q[u][h] = (live && on[h]) ? *(const uint4*)(row + 512 * h) : make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int h = 0; h < CH; ++h) fma_bf16x8(acc[h], w4[u], q[u][h]);
+    }
+  }
+#pragma unroll
+  for (int h = 0; h < CH; ++h) {
+    if (!on[h]) continue;
+    // non-temporal: the rows are read once, by the sum, and must not evict the v rows
+    float* o = g.rows + s * g.d + c0 + 512 * h + 8 * l;
+    __builtin_nontemporal_store(f32x4_t{acc[h][0], acc[h][1], acc[h][2], acc[h][3]}, (f32x4_t*)o);
+    __builtin_nontemporal_store(f32x4_t{acc[h][4], acc[h][5], acc[h][6], acc[h][7]},
+                                (f32x4_t*)(o + 4));
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void group_rows_kernel(GroupRowsArgs g) {
+  const int64_t n_slots = min((int64_t)g.counters[0], g.n_max);
+  const int64_t waves = (int64_t)gridDim.x * (kThreads / kWave);
+  const int64_t wv = xcd_contiguous(blockIdx.x, gridDim.x) * (kThreads / kWave) + (threadIdx.x >> 6);
+  const int64_t per = (n_slots + waves - 1) / waves;
+  const int64_t s_lo = wv * per;
+  const int64_t s_hi = min(s_lo + per, n_slots);
+  for (int64_t s = s_lo; s < s_hi; ++s) {
+    const int p0 = g.slot_off[s], p1 = g.slot_off[s + 1];
+    // the fp32 sums are the same whichever pass holds a column (each column is its own sum)
+    int c0 = 0;
+    for (; c0 + 2048 <= g.d; c0 += 2048) group_row_pass<4>(g, s, p0, p1, c0);
+    if (g.d - c0 > 512) group_row_pass<4>(g, s, p0, p1, c0);
+    else if (g.d > c0) group_row_pass<1>(g, s, p0, p1, c0);
+  }
+}
+
+// y_t = sum of token t's slot rows, in group order (its run in the slot order). One wave per
+// token.
+struct SumRowsArgs {
+  const float* rows;
+  const int32_t* slots;
+  const int32_t* tokens;
+  const int32_t* tok_start;
+  float* y;
+  int64_t T, n;
+  int d;
+};
+
+__global__ __launch_bounds__(kThreads) void sum_group_rows_kernel(SumRowsArgs g) {
+  const int l = lane_id();
+  const int64_t waves = (int64_t)gridDim.x * (kThreads / kWave);
+  typedef float f32x4_t __attribute__((ext_vector_type(4)));
+  for (int64_t t = (int64_t)blockIdx.x * (kThreads / kWave) + (threadIdx.x >> 6); t < g.T;
+       t += waves) {
+    const int i0 = g.tok_start[t];
+    for (int c0 = 0; c0 < g.d; c0 += 512) {
+      const int c = c0 + 8 * l;
+      const bool on = c < g.d;
+      float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      if (i0 >= 0) {
+        for (int64_t b0 = i0;; b0 += kWave) {
+          const int64_t i = b0 + l;
+          const bool mine = i < g.n && g.tokens[i] == (int32_t)t;
+          const int sl = mine ? g.slots[i] : 0;
+          const int nb = __popcll(__ballot(mine));  // a prefix of the lanes: the run is contiguous
+          for (int j = 0; j < nb; j += 4) {
+            f32x4_t lo[4], hi[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const bool live = j + u < nb;  // wave-uniform
+              const int sj = readlane_i32(sl, live ? j + u : 0);
+              const float* r = g.rows + (int64_t)sj * g.d + c;
+              lo[u] = (live && on) ? __builtin_nontemporal_load((const f32x4_t*)r) : f32x4_t{0.f, 0.f, 0.f, 0.f};
+              hi[u] = (live && on) ? __builtin_nontemporal_load((const f32x4_t*)(r + 4)) : f32x4_t{0.f, 0.f, 0.f, 0.f};
+            }
+            // added in slot order (u ascending), so the sum does not depend on the unrolling
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              acc[0] += lo[u].x; acc[1] += lo[u].y; acc[2] += lo[u].z; acc[3] += lo[u].w;
+              acc[4] += hi[u].x; acc[5] += hi[u].y; acc[6] += hi[u].z; acc[7] += hi[u].w;
+            }
+          }
+          if (nb < kWave) break;
+        }
+      }
+      if (on) {
+        float* o = g.y + t * g.d + c;
+        __builtin_nontemporal_store(f32x4_t{acc[0], acc[1], acc[2], acc[3]}, (f32x4_t*)o);
+        __builtin_nontemporal_store(f32x4_t{acc[4], acc[5], acc[6], acc[7]}, (f32x4_t*)(o + 4));
+      }
+    }
+  }
+}
+
 }  // namespace
 
 int grouped_tile_experts(int B) { return B <= 64 ? 64 : 160; }
@@ -322,6 +478,39 @@ hipError_t launch_grouped_dot(const Shape& s, const void* x, const void* u, cons
   else
     hipLaunchKernelGGL(grouped_dot_kernel<5>, dim3(256), dim3(kThreads),
                        2 * TileShape<5>::kStage, st, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_group_rows(const Shape& s, const void* v, const int32_t* idx,
+                             const int32_t* perm, const float* a, const GroupPlan& plan,
+                             const SlotOrder& order, float* rows, int64_t n_slots_max, float* y,
+                             hipStream_t st) {
+  if (s.M == 0) return hipSuccess;
+  GroupRowsArgs g;
+  g.v = (const uint16_t*)v;
+  g.idx = idx;
+  g.perm = perm;
+  g.a = a;
+  g.slot_off = plan.slot_off;
+  g.counters = plan.counters;
+  g.rows = rows;
+  g.M = s.M;
+  g.N = s.N;
+  g.n_max = n_slots_max;
+  g.d = s.d;
+  hipLaunchKernelGGL(group_rows_kernel, dim3(2048), dim3(kThreads), 0, st, g);
+  SumRowsArgs r;
+  r.rows = rows;
+  r.slots = order.slots;
+  r.tokens = order.tokens;
+  r.tok_start = order.tok_start;
+  r.y = y;
+  r.T = s.T;
+  r.n = n_slots_max;
+  r.d = s.d;
+  const int64_t wgs = (s.T + 3) / 4;
+  hipLaunchKernelGGL(sum_group_rows_kernel, dim3((unsigned)(wgs < 8192 ? wgs : 8192)),
+                     dim3(kThreads), 0, st, r);
   return hipGetLastError();
 }
 

@@ -133,6 +133,26 @@ hipError_t launch_group_plan(const Shape& s, const int32_t* perm, const int32_t*
                              const int32_t* sorted_group_keys, const int32_t* idx,
                              const int32_t* active, void* ws, GroupPlan* plan, hipStream_t st);
 
+// Slots of a group plan in token order (stable: each token's slots in group order). slots[i]
+// is a slot id, tokens[i] its token (T past the real slots), tok_start[t] the first place of
+// token t (-1 when it has none). n >= the number of slots (the bound min(M, G T)).
+struct SlotOrder {
+  int32_t* slots;
+  const int32_t* tokens;
+  int32_t* tok_start;
+};
+size_t slot_sort_ws_bytes(int64_t n, int64_t T);
+hipError_t launch_slot_sort(const GroupPlan& plan, int64_t n, int64_t T, void* ws,
+                            SlotOrder* out, hipStream_t st);
+
+// The second product of Eq. 14 group by group: O[s] = sum over the tasks of slot s, in
+// position order, of a_p v_e (fp32 rows of d, n_slots_max of them), then y_t = sum of the
+// token's slot rows in group order.
+hipError_t launch_group_rows(const Shape& s, const void* v, const int32_t* idx,
+                             const int32_t* perm, const float* a, const GroupPlan& plan,
+                             const SlotOrder& order, float* rows, int64_t n_slots_max, float* y,
+                             hipStream_t st);
+
 // a[p] = g_p * act(x_t . u_e) by groups: per work tile, the 256 x 64 block of
 // X_q U_q^T over the tile's slots (token rows) and experts on MFMA, then each task of the
 // tile's slots whose expert lies in the tile reads its entry. bf16, d % 64 == 0.

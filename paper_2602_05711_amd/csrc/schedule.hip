@@ -1219,4 +1219,76 @@ hipError_t launch_group_plan(const Shape& s, const int32_t* perm, const int32_t*
                      EmitTiles{plan->grp_tile, G + 1, plan->counters}, G + 1, partial, st);
 }
 
+// ---------------------------------------------------------------- slots by token
+// The second product of Eq. 14 per group leaves one partial row per (group, token) slot; the
+// token's output is the sum of its slots' rows in group order. The slots are listed group by
+// group (tokens ascending inside a group), so a stable sort of the slot ids by token gives every
+// token's slots as one run in group order. Slot ids n_slots <= s < n (unused entries) get the
+// key T and sort last.
+
+namespace {
+
+__global__ __launch_bounds__(kThreads) void slot_key_kernel(const int32_t* __restrict__ slot_token,
+                                                          const int32_t* __restrict__ counters,
+                                                          int32_t* __restrict__ key, int64_t n,
+                                                          int32_t T) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i < n) key[i] = i < counters[0] ? slot_token[i] : T;
+}
+
+// tok_start[t] = first place of token t in the sorted order (-1 when t has no slot).
+__global__ __launch_bounds__(kThreads) void token_start_kernel(const int32_t* __restrict__ sk,
+                                                             int32_t* __restrict__ tok_start,
+                                                             int64_t n, int32_t T) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i >= n) return;
+  const int32_t k = sk[i];
+  if (k < T && (i == 0 || sk[i - 1] != k)) tok_start[k] = (int32_t)i;
+}
+
+}  // namespace
+
+size_t slot_sort_ws_bytes(int64_t n, int64_t T) {
+  const int64_t tiles = (n + kTile - 1) / kTile;
+  const int64_t hist = (int64_t)kMaxRadix * (tiles > 0 ? tiles : 1);
+  size_t b = 0;
+  b += 6 * align_up((size_t)n * 4);             // keys, ping-pong keys/values, sorted ids
+  b += align_up((size_t)hist * 4);              // histogram
+  b += align_up((size_t)partial_count(n) * 4);  // scan partials
+  b += align_up((size_t)(T + 1) * 4);           // token starts
+  return b;
+}
+
+hipError_t launch_slot_sort(const GroupPlan& plan, int64_t n, int64_t T, void* ws,
+                            SlotOrder* out, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  char* w = (char*)ws;
+  int32_t* key = (int32_t*)w; w += align_up((size_t)n * 4);
+  SortBuffers b;
+  b.k0 = (int32_t*)w; w += align_up((size_t)n * 4);
+  b.v0 = (int32_t*)w; w += align_up((size_t)n * 4);
+  b.k1 = (int32_t*)w; w += align_up((size_t)n * 4);
+  b.v1 = (int32_t*)w; w += align_up((size_t)n * 4);
+  int32_t* ids = (int32_t*)w; w += align_up((size_t)n * 4);
+  const int64_t tiles = (n + kTile - 1) / kTile;
+  b.hist = (int32_t*)w; w += align_up((size_t)kMaxRadix * (tiles > 0 ? tiles : 1) * 4);
+  b.partial = (int32_t*)w; w += align_up((size_t)partial_count(n) * 4);
+  int32_t* tok_start = (int32_t*)w;
+  const unsigned grid = (unsigned)((n + kThreads - 1) / kThreads);
+  hipLaunchKernelGGL(slot_key_kernel, dim3(grid), dim3(kThreads), 0, st, plan.slot_token,
+                     plan.counters, key, n, (int32_t)T);
+  int bits = 1;
+  while ((1ll << bits) <= T) ++bits;  // keys 0 .. T
+  const int32_t* sk = nullptr;
+  hipError_t e = radix_sort_tasks(key, n, bits, ids, b, &sk, st);
+  if (e != hipSuccess) return e;
+  if ((e = launch_fill_i32(tok_start, T, -1, st)) != hipSuccess) return e;
+  hipLaunchKernelGGL(token_start_kernel, dim3(grid), dim3(kThreads), 0, st, sk, tok_start, n,
+                     (int32_t)T);
+  out->slots = ids;
+  out->tokens = sk;
+  out->tok_start = tok_start;
+  return hipGetLastError();
+}
+
 }  // namespace omnimoe

@@ -24,7 +24,7 @@ def _declared_functions():
 def test_header_matches_exports():
     lib = P.load_library()
     names = _declared_functions()
-    assert len(names) == 21
+    assert len(names) == 22
     assert sorted(P.EXPORTED) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -91,7 +91,12 @@ def test_workspace_sizes_cover_buffers():
     assert st == OK and route >= w.T * w.H * (w.n_rows + w.n_cols) * 4
     st, layer = _ws(d, B.STAGE_LAYER)
     assert st == OK and layer >= route + 3 * w.M * 4
-    assert _ws(d, 10)[0] == INVALID
+    assert _ws(d, 11)[0] == INVALID
+    # groups of B: partial rows for min(M, ceil(min(M, N) / B) T) slots of d floats
+    pg = synth.WORKLOADS["paper_t1k_k1024_bf16"].with_(group_size=320)
+    st, rows = _ws(B.make_desc(pg), B.STAGE_EXPERT_GROUP_ROWS)
+    bound = min(pg.M, -(-min(pg.M, pg.N) // 320) * pg.T)
+    assert st == OK and rows >= pg.M * 4 + bound * pg.d * 4 and bound == 320 * 1024
     st, scatter = _ws(d, B.STAGE_EXPERT_SCATTER)
     assert st == OK and scatter >= w.M * 4 + w.M * w.d * 4  # a[] and the contribution rows
     st, grouped = _ws(d, B.STAGE_EXPERT_GROUPED)

@@ -462,6 +462,79 @@ def test_dense_routed_sum(name):
     assert np.all(gap <= bound)
 
 
+GROUP_ROWS_CASES = [
+    # (shape, B): the second product of Eq. 14 per group (partial rows per (group, token)
+    # slot): small and large groups, one group holding every expert, B = 1, wide d (several
+    # 512-column chunks), K > 64 and the paper's grid, many slot tiles per group
+    ("small_bf16", 2), ("small_bf16", 64), ("k64_bf16", 33), ("all_experts_bf16", 1 << 20),
+    ("k64_bf16", 1), ("wide_bf16", 3), ("shared_bf16", 48), ("k256_bf16", 64),
+    ("paper_k512_bf16", 320), ("bucket_bf16", 100), ("dense_bf16", 8),
+]
+
+
+@pytest.mark.parametrize("case", GROUP_ROWS_CASES, ids=[f"{n}-B{b}" for n, b in GROUP_ROWS_CASES])
+def test_expert_forward_group_rows(case):
+    # Within tolerance of the oracle, the same bits on a second run, and element-wise within the
+    # reordering bound of the slot-order sum: both paths form the same a[p] (the grouped dot)
+    # and add the same H K terms a_p v_e per token in fp32, in two orders (each within
+    # gamma_{HK} sum |a v| of the exact sum).
+    name, Bg = case
+    w = SHAPES[name].with_(group_size=Bg)
+    say(f"[group rows] {name} B={Bg}")
+    inp, f = host_inputs(w)
+    dev = upload(inp)
+    dsc = oracle.desc(w)
+    sr, sc = oracle.half_scores(dsc, f["x"], f["keys_row"], f["keys_col"])
+    idx, _, g64, _ = oracle.select(dsc, sr, sc, oracle.CARTESIAN)
+    g32 = g64.astype(np.float32)
+    perm, active, _, _ = oracle.schedule(dsc, idx)
+    act_pad = np.zeros(min(w.M, w.N), dtype=np.int32)
+    act_pad[:len(active)] = active
+    gi, gg, gp, ga = to_dev(idx), to_dev(g32), to_dev(perm), to_dev(act_pad)
+    na = torch.tensor([len(active)], dtype=torch.int32, device="cuda")
+    d = B.make_desc(w)
+    ys = []
+    for _ in range(2):
+        y = torch.full((w.T, w.d), float("nan"), dtype=torch.float32, device="cuda")
+        P.omnimoe_expert_forward_group_rows(d, dev["x"], dev["u"], dev["v"], gi, gg, gp, ga, na, y)
+        ys.append(y)
+    y_ref_path = torch.empty((w.T, w.d), dtype=torch.float32, device="cuda")
+    P.omnimoe_expert_forward_grouped(d, dev["x"], dev["u"], dev["v"], gi, gg, gp, ga, na,
+                                     y_ref_path)
+    torch.cuda.synchronize()
+    y0, y1, yg = (t.cpu().numpy() for t in (ys[0], ys[1], y_ref_path))
+    assert np.array_equal(y0.view(np.uint8), y1.view(np.uint8))
+    y_ref = oracle.expert_forward(dsc, f["x"], f["u"], f["v"], idx, g32.astype(np.float64))
+    err = row_rel_err(y0, y_ref)
+    n = w.H * w.K
+    gam = 2.02 * (n + 1) * 2.0 ** -24 / (1 - (n + 1) * 2.0 ** -24)
+    # |a_p| <= g_p |x_t . u_e| (|act(z)| <= |z|), computed in fp64 from the inputs
+    flat = idx.reshape(w.T, -1)
+    xu = np.abs(np.einsum("td,tnd->tn", f["x"].astype(np.float64),
+                          f["u"][flat].astype(np.float64)))
+    amag = g32.reshape(w.T, -1).astype(np.float64) * xu * 1.01
+    mass = np.einsum("tn,tnd->td", amag, np.abs(f["v"][flat].astype(np.float64)))
+    gap = np.abs(y0.astype(np.float64) - yg)
+    say(f"  max row rel err {err.max():.3e}; max gap / bound {(gap / (gam * mass + 1e-30)).max():.3e}")
+    assert err.max() <= tol(w)
+    if not (w.H == 1 and w.K * 64 >= w.N):  # the grouped path's own sum is the slot-order one
+        assert np.all(gap <= gam * mass + 1e-30)
+
+
+def test_expert_forward_group_rows_rejects_fp32():
+    w = SHAPES["ragged_f32"].with_(group_size=4)
+    inp, _ = host_inputs(w)
+    dev = upload(inp)
+    z = torch.zeros(w.M, dtype=torch.int32, device="cuda")
+    y = torch.empty((w.T, w.d), dtype=torch.float32, device="cuda")
+    with pytest.raises(B.OmnimoeError) as ei:
+        P.omnimoe_expert_forward_group_rows(B.make_desc(w), dev["x"], dev["u"], dev["v"], z,
+                                            z.float(), z, z, z[:1], y,
+                                            ws=torch.empty(1 << 20, dtype=torch.uint8,
+                                                           device="cuda"))
+    assert "unsupported" in str(ei.value)
+
+
 @pytest.mark.parametrize("grouped", [False, True])
 def test_dense_routed_sum_repeated_ids(grouped):
     # Caller-supplied idx may name one expert in several slots of a token (the router never
