@@ -196,11 +196,16 @@ omnimoe_status layer_impl(const omnimoe_layer_desc* desc, const void* x, const v
   mark(2);
   const int32_t* sk = nullptr;
   const int32_t* gk = nullptr;
-  if ((e = omnimoe::launch_schedule(s, idx, perm, active, offsets, n_active, nullptr, sched_ws,
-                                    &sk, strm, &gk)))
+  // Few tasks (a decode step): almost every task has an expert of its own, so the layer takes
+  // the slot-order dot and forms no schedule.
+  const bool unscheduled = !layer_grouped(s) && omnimoe::slot_dot(s);
+  if (!unscheduled && (e = omnimoe::launch_schedule(s, idx, perm, active, offsets, n_active,
+                                                    nullptr, sched_ws, &sk, strm, &gk)))
     return hip_status(e);
   mark(3);
-  if (layer_grouped(s)) {
+  if (unscheduled) {
+    if ((e = omnimoe::launch_slot_dot(s, x, u, idx, gates, abuf, strm))) return hip_status(e);
+  } else if (layer_grouped(s)) {
     omnimoe::GroupPlan plan;
     void* plan_ws = (char*)sched_ws + omnimoe::schedule_ws_bytes(s.M, s.N);
     if ((e = omnimoe::launch_group_plan(s, perm, n_active, gk, idx, active, plan_ws, &plan,

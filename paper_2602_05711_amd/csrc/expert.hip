@@ -667,6 +667,63 @@ hipError_t dispatch_dot(int cpl, dim3 grid, hipStream_t st, const DotArgs& a) {
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- few tasks: slot order
+// For a small batch (M <= kSlotDotMaxTasks: one token up to a decode step) the dot runs in slot
+// order without a schedule: wave v takes slots 2v and 2v + 1, reads their experts and gates
+// and loads both u rows and token rows at once. With a handful of tasks per expert range there
+// is no u row to share between tasks (64 tokens pick ~8165 distinct experts of 2^20 in 8192
+// slots), so an expert-major order would cost a sort and save no reads. Each a[p] is summed
+// exactly as expert_dot_kernel sums it, so the two kernels give identical a.
+constexpr int kSlotDotMaxTasks = 8192;
+
+template <int CPL, bool BF16>
+__global__ __launch_bounds__(256) void slot_dot_kernel(DotArgs a) {
+  constexpr int G = CPL >= 8 ? 1 : 2;  // slots per wave, all in flight
+  const int l = lane_id();
+  const int64_t p0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * G;
+  const uint4* X = (const uint4*)a.x;
+  const uint4* U = (const uint4*)a.u;
+  bool cv[CPL];
+#pragma unroll
+  for (int q = 0; q < CPL; ++q) cv[q] = (l + kWave * q) < a.nchunks;
+  uint4 ur[G][CPL], xr[G][CPL];
+  float gj[G];
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
+    const int64_t p = p0 + i;
+    gj[i] = 0.0f;
+    if (p < a.M) {
+      const int e = clamp_i(a.idx[p], a.N);
+      gj[i] = a.gates[p];
+      load_row_nt<CPL>(ur[i], U + (int64_t)e * a.nchunks, cv);
+      load_row<CPL>(xr[i], X + (p / a.hk) * a.nchunks, cv);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
+    const int64_t p = p0 + i;
+    if (p < a.M) {
+      float acc = 0.0f;
+#pragma unroll
+      for (int q = 0; q < CPL; ++q) acc = chunk_dot<BF16>(ur[i][q], xr[i][q], acc);
+      const float hs = wave_sum_uniform(acc);
+      if (l == 0) a.a[p] = gj[i] * activation(a.act, hs);
+    }
+  }
+}
+
+template <bool BF16>
+hipError_t dispatch_slot_dot(int cpl, dim3 grid, hipStream_t st, const DotArgs& a) {
+  switch (cpl) {
+    case 1: hipLaunchKernelGGL((slot_dot_kernel<1, BF16>), grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((slot_dot_kernel<2, BF16>), grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((slot_dot_kernel<4, BF16>), grid, dim3(256), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((slot_dot_kernel<8, BF16>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((slot_dot_kernel<16, BF16>), grid, dim3(256), 0, st, a); break;
+  }
+  return hipGetLastError();
+}
+
 // Sixteen waves per workgroup when a wave holds at most two chunks of a row (registers for
 // eight rows in flight, at most 64 KiB of partial rows in LDS) and each wave still gets a few
 // slots; four otherwise.
@@ -761,6 +818,34 @@ hipError_t launch_expert_dot(const Shape& s, const void* x, const void* u, const
   dim3 grid((unsigned)((waves + 3) / 4));
   const int cpl = chunks_per_lane(a.nchunks);
   return s.bf16 ? dispatch_dot<true>(cpl, grid, st, a) : dispatch_dot<false>(cpl, grid, st, a);
+}
+
+bool slot_dot(const Shape& s) { return s.M > 0 && s.M <= kSlotDotMaxTasks; }
+
+hipError_t launch_slot_dot(const Shape& s, const void* x, const void* u, const int32_t* idx,
+                           const float* gates, float* abuf, hipStream_t st) {
+  if (s.M == 0) return hipSuccess;
+  DotArgs a;
+  a.x = x;
+  a.u = u;
+  a.idx = idx;
+  a.gates = gates;
+  a.perm = nullptr;
+  a.sk = nullptr;
+  a.a = abuf;
+  a.M = s.M;
+  a.N = s.N;
+  a.d = s.d;
+  a.hk = s.hk;
+  a.act = s.act;
+  a.nchunks = s.bf16 ? s.d / 8 : s.d / 4;
+  a.range = 1;
+  const int cpl = chunks_per_lane(a.nchunks);
+  const int64_t per_wave = cpl >= 8 ? 1 : 2;
+  const int64_t waves = (s.M + per_wave - 1) / per_wave;
+  const dim3 grid((unsigned)((waves + 3) / 4));
+  return s.bf16 ? dispatch_slot_dot<true>(cpl, grid, st, a)
+                : dispatch_slot_dot<false>(cpl, grid, st, a);
 }
 
 hipError_t launch_accumulate(const Shape& s, const void* v, const int32_t* idx, const float* abuf,

@@ -161,6 +161,12 @@ hipError_t launch_grouped_dot(const Shape& s, const void* x, const void* u, cons
                               const int32_t* n_active, const GroupPlan& plan, float* a,
                               hipStream_t st);
 
+// For M <= 8192 tasks: a[p] in slot order without a schedule (bf16 or fp32), identical to
+// launch_expert_dot's a.
+bool slot_dot(const Shape& s);
+hipError_t launch_slot_dot(const Shape& s, const void* x, const void* u, const int32_t* idx,
+                           const float* gates, float* abuf, hipStream_t st);
+
 // y[t] = sum over slots (h, k) in order of a[p] * v[idx[p]].
 hipError_t launch_accumulate(const Shape& s, const void* v, const int32_t* idx, const float* a,
                              float* y, hipStream_t st);

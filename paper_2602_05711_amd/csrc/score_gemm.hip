@@ -335,7 +335,9 @@ __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
 
 constexpr int SK_N = 32;
 
-template <bool ACC, int RB>
+// STEPS > 0: d_key = 64 STEPS, and all STEPS fragment pairs of the wave's quarter are requested
+// at once; STEPS = 0: any d_key % 256 == 0, four k steps in flight per iteration.
+template <bool ACC, int RB, int STEPS>
 __global__ __launch_bounds__(256) void score_bf16_skinny_kernel(ScoreArgs a) {
   const int half = blockIdx.y;
   const int ncols = a.H * a.nh[half];
@@ -363,20 +365,36 @@ __global__ __launch_bounds__(256) void score_bf16_skinny_kernel(ScoreArgs a) {
   for (int i = 0; i < RB; ++i)
 #pragma unroll
     for (int q = 0; q < 16; ++q) acc[i][q] = 0.f;
-  // four k steps of 16 in flight per iteration
-  for (int k = 0; k < kq; k += 64) {
-    bf16x8 fa[4][RB], fb[4];
+  if constexpr (STEPS > 0) {
+    bf16x8 fa[STEPS][RB], fb[STEPS];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
+    for (int s = 0; s < STEPS; ++s) {
 #pragma unroll
-      for (int i = 0; i < RB; ++i) fa[s][i] = *(const bf16x8*)(pa[i] + k + 16 * s);
-      fb[s] = *(const bf16x8*)(pb + k + 16 * s);
+      for (int i = 0; i < RB; ++i) fa[s][i] = *(const bf16x8*)(pa[i] + 16 * s);
+      fb[s] = *(const bf16x8*)(pb + 16 * s);
     }
+    __builtin_amdgcn_sched_barrier(0);  // keeps every load ahead of the first MFMA
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
+    for (int s = 0; s < STEPS; ++s)
 #pragma unroll
       for (int i = 0; i < RB; ++i)
         acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s], acc[i], 0, 0, 0);
+  } else {
+    // four k steps of 16 in flight per iteration
+    for (int k = 0; k < kq; k += 64) {
+      bf16x8 fa[4][RB], fb[4];
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+#pragma unroll
+        for (int i = 0; i < RB; ++i) fa[s][i] = *(const bf16x8*)(pa[i] + k + 16 * s);
+        fb[s] = *(const bf16x8*)(pb + k + 16 * s);
+      }
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int i = 0; i < RB; ++i)
+          acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s], acc[i], 0, 0, 0);
+    }
   }
   // tile element (row, col) of a 32 x 32 block: register q, lane l with
   // row = 8 (q / 4) + 4 (l / 32) + q % 4, col = l % 32
@@ -406,26 +424,33 @@ __global__ __launch_bounds__(256) void score_bf16_skinny_kernel(ScoreArgs a) {
 }
 
 // ---------------------------------------------------------------- decode bf16 kernel
-// For T <= 64 and d_key <= 1024 (decode): a workgroup owns 64 keys of one half and copies the
-// half's token rows (32·RB rows of d_key, RB = 1 when T <= 32, else 2) into LDS with coalesced
-// 16-byte loads straight to LDS. Wave w takes key block w % 2 (32 keys) over quarter w / 2 of
-// d_key: it requests all its key fragments from memory at once, before the token copy is
-// waited for, then runs v_mfma_f32_32x32x16_bf16 with the token fragments read from LDS. The
-// four quarters' partial tiles are added through LDS in quarter order, so the sum order is
-// fixed. LDS row r holds its 16-byte chunk c at c ^ (r % 16) within each group of sixteen, so
-// the sixteen rows read by a quarter-wave fall in distinct banks. Requires d_key % 256 == 0.
+// For T <= 64 and d_key <= 1024 (decode): a workgroup owns 64 keys of one half. Four copy
+// waves put the half's token rows (32·RB rows of d_key, RB = 1 when T <= 32, else 2) into LDS
+// with coalesced 16-byte loads, while eight compute waves request their key
+// fragments: wave w takes key block w % 2 (32 keys) over quarter w / 2 of d_key, STEPS
+// fragments, all in flight at once. After one barrier the compute waves run
+// v_mfma_f32_32x32x16_bf16 step by step as their fragments arrive, with the token fragments
+// read from LDS (the copy runs on other waves, so no compute wave waits for it through its own
+// load counter; it goes through registers, since an LDS read after a direct-to-LDS load makes
+// the compiler wait for every outstanding load, the fragments included). The four quarters' partial tiles go through LDS and every compute thread adds
+// four of them in quarter order (the sum order is fixed) and stores its share of the
+// 32·RB x 64 tile. LDS row r holds its 16-byte chunk c at c ^ (r % 16) within each group of
+// sixteen, so the sixteen rows read by a quarter-wave fall in distinct banks. Requires
+// d_key % 256 == 0.
 
 constexpr int DC_KEYS = 64;
-constexpr int DC_WAVES = 8;
+constexpr int DC_WAVES = 8;       // compute waves
+constexpr int DC_COPY_WAVES = 4;  // token-copy waves
 
 size_t decode_lds_bytes(int dk, int rb) {
   const size_t xb = (size_t)rb * 32 * dk * 2;                 // token rows
-  const size_t pb = (size_t)6 * rb * 32 * 32 * sizeof(float);  // partial tiles of quarters 1-3
+  const size_t pb = (size_t)8 * rb * 32 * 32 * sizeof(float);  // partial tiles of the quarters
   return xb > pb ? xb : pb;
 }
 
-template <bool ACC, int RB>
-__global__ __launch_bounds__(64 * DC_WAVES) void score_bf16_decode_kernel(ScoreArgs a) {
+template <bool ACC, int RB, int STEPS>
+__global__ __launch_bounds__(64 * (DC_WAVES + DC_COPY_WAVES)) void score_bf16_decode_kernel(
+    ScoreArgs a) {
   const int half = blockIdx.y;
   const int ncols = a.H * a.nh[half];
   const int n0 = blockIdx.x * DC_KEYS;
@@ -434,40 +459,57 @@ __global__ __launch_bounds__(64 * DC_WAVES) void score_bf16_decode_kernel(ScoreA
   const uint16_t* X = (const uint16_t*)a.x + a.col0[half];
   const uint16_t* Kt = (const uint16_t*)a.keys[half];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int kb = wid & 1, qi = wid >> 1;
-  const int kq = a.dk / 4;
-  const int steps = kq / 16;  // 4, 8, 12 or 16
+  const int kb = wid & 1, qi = (wid >> 1) & 3;
+  constexpr int kq = STEPS * 16;  // d_key / 4
+  constexpr int dk = 4 * kq;
+  constexpr int cpr = dk / 8;     // 16-byte chunks per token row
+  constexpr int npos = RB * 32 * cpr;
+  constexpr int per_wave = npos / (kWave * DC_COPY_WAVES);  // copy loads per copy wave
+  static_assert(npos % (kWave * DC_COPY_WAVES) == 0, "the copy divides evenly");
   const int frow = lane & 31;
-  // this wave's key fragments, all in flight
-  int n = n0 + kb * 32 + frow;
-  if (n >= ncols) n = ncols - 1;
-  const uint16_t* pb = Kt + (int64_t)n * a.dk + qi * kq + (lane >> 5) * 8;
-  bf16x8 fb[16];
-#pragma unroll
-  for (int s = 0; s < 16; ++s)
-    if (s < steps) fb[s] = *(const bf16x8*)(pb + 16 * s);
-  // token rows into LDS: 16-byte position p holds row p / cpr, chunk (p % cpr) ^ (row % 16)
-  const int cpr = a.dk / 8;
-  const int npos = RB * 32 * cpr;
-  for (int q = wid; q * kWave < npos; q += DC_WAVES) {
-    const int p = q * kWave + lane;
-    const int r = p / cpr;
-    const int c = (p - r * cpr) ^ (r & 15);
-    int64_t m = r < a.T ? r : a.T - 1;
-    __builtin_amdgcn_global_load_lds((const void*)(X + m * a.d + c * 8),
-                                     (lds_ptr_t)(smem + (size_t)q * kWave * 16), 16, 0, 0);
-  }
-  wait_vm0();
-  __syncthreads();
+  bf16x8 fb[STEPS];
+  // Both roles pass the same two barriers: the first once the copy's loads are issued (so the
+  // compute unit's memory pipeline takes them ahead of the key fragments), the second once the
+  // token rows are in LDS. The roles sit in separate branches up to the MFMAs, so the compute
+  // waves' LDS reads never follow a direct-to-LDS load in program order (the compiler would
+  // make them wait for every outstanding load, the key fragments included).
   f32x16 acc[RB];
 #pragma unroll
   for (int i = 0; i < RB; ++i)
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[i][e] = 0.f;
-  const int c0 = qi * kq / 8 + (lane >> 5);  // logical chunk of step 0
+  if (wid >= DC_WAVES) {
+    // token rows into LDS: 16-byte position p holds row p / cpr, chunk (p % cpr) ^ (row % 16)
+    const int cw = wid - DC_WAVES;
 #pragma unroll
-  for (int s = 0; s < 16; ++s) {
-    if (s < steps) {
+    for (int j = 0; j < per_wave; ++j) {
+      const int q = cw + DC_COPY_WAVES * j;
+      const int p = q * kWave + lane;
+      const int r = p / cpr;
+      const int c = (p - r * cpr) ^ (r & 15);
+      const int64_t m = r < a.T ? r : a.T - 1;
+      __builtin_amdgcn_global_load_lds((const void*)(X + m * a.d + c * 8),
+                                       (lds_ptr_t)(smem + (size_t)q * kWave * 16), 16, 0, 0);
+    }
+    __builtin_amdgcn_s_barrier();
+    wait_vm0();
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+  } else {
+    __builtin_amdgcn_s_barrier();
+    // this wave's key fragments, all in flight
+    bf16x8 fb[STEPS];
+    int n = n0 + kb * 32 + frow;
+    if (n >= ncols) n = ncols - 1;
+    const uint16_t* pb = Kt + (int64_t)n * dk + qi * kq + (lane >> 5) * 8;
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) fb[s] = *(const bf16x8*)(pb + 16 * s);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();  // the token rows are in LDS
+    asm volatile("" ::: "memory");
+    const int c0 = qi * kq / 8 + (lane >> 5);  // logical chunk of step 0
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) {
 #pragma unroll
       for (int i = 0; i < RB; ++i) {
         const int r = i * 32 + frow;
@@ -478,30 +520,67 @@ __global__ __launch_bounds__(64 * DC_WAVES) void score_bf16_decode_kernel(ScoreA
     }
   }
   __syncthreads();  // the token rows are no longer needed: the space takes the partial tiles
-  float* part = (float*)smem;  // [quarter - 1][key block][32 RB rows][32 keys]
-  const int c = lane & 31;
-  if (qi > 0) {
+  float* part = (float*)smem;  // [quarter][key block][32 RB rows][32 keys]
+  if (wid < DC_WAVES) {
 #pragma unroll
     for (int i = 0; i < RB; ++i)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int r = i * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
-        part[(((qi - 1) * 2 + kb) * RB * 32 + r) * 32 + c] = acc[i][e];
+        part[((qi * 2 + kb) * RB * 32 + r) * 32 + (lane & 31)] = acc[i][e];
       }
   }
   __syncthreads();
-  if (qi == 0 && n0 + kb * 32 + c < ncols) {
-    const int64_t oc = out_col(a, half, n0 + kb * 32 + c);
+  if (wid >= DC_WAVES) return;
+  // thread t: keys 4 k4 .. 4 k4 + 3 of the tile's 64 (k4 = t % 16) in rows t / 16 + 32 j
+  const int k4 = tid & 15;
+  const int b = k4 >> 3, cc = (k4 & 7) * 4;
+  const int nn0 = n0 + b * 32 + cc;
+  int64_t col[4];
+  {
+    int h = nn0 / a.nh[half], i = nn0 - h * a.nh[half];
 #pragma unroll
-    for (int i = 0; i < RB; ++i)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int r = i * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
-        float v = acc[i][e];
-#pragma unroll
-        for (int qq = 0; qq < 3; ++qq) v += part[((qq * 2 + kb) * RB * 32 + r) * 32 + c];
-        if (r < a.T) store_out<ACC>(a, (int64_t)r * a.ldo + oc, v);
+    for (int t = 0; t < 4; ++t) {
+      col[t] = (int64_t)h * a.per_head + a.out_off[half] + i;
+      if (++i == a.nh[half]) {
+        i = 0;
+        ++h;
       }
+    }
+  }
+  // one 16-byte store when the four columns are consecutive and aligned
+  const bool vec = nn0 + 3 < ncols && col[3] == col[0] + 3 && ((col[0] | a.ldo) & 3) == 0 &&
+                   ((uintptr_t)a.out & 15) == 0;
+#pragma unroll
+  for (int j = 0; j < RB; ++j) {
+    const int r = (j * 64 * DC_WAVES + tid) >> 4;
+    float4 v = *(const float4*)&part[((0 * 2 + b) * RB * 32 + r) * 32 + cc];
+#pragma unroll
+    for (int qq = 1; qq < 4; ++qq) {
+      const float4 w = *(const float4*)&part[((qq * 2 + b) * RB * 32 + r) * 32 + cc];
+      v.x += w.x;
+      v.y += w.y;
+      v.z += w.z;
+      v.w += w.w;
+    }
+    if (r >= a.T) continue;
+    float* o = a.out + (int64_t)r * a.ldo;
+    if (vec) {
+      float4* o4 = (float4*)(o + col[0]);
+      if constexpr (ACC) {
+        const float4 w = *o4;
+        v.x = w.x + v.x;
+        v.y = w.y + v.y;
+        v.z = w.z + v.z;
+        v.w = w.w + v.w;
+      }
+      *o4 = v;
+    } else {
+      const float vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        if (nn0 + t < ncols) store_out<ACC>(a, (int64_t)r * a.ldo + col[t], vv[t]);
+    }
   }
 }
 
@@ -630,25 +709,47 @@ hipError_t launch_score(const Shape& s, const void* x, const void* keys_row,
     dim3 grid((ncols + DC_KEYS - 1) / DC_KEYS, 2);
     const int rb = s.T > 32 ? 2 : 1;
     const size_t lds = decode_lds_bytes(s.dk, rb);
-    const dim3 block(64 * DC_WAVES);
-    if (accumulate && rb == 2)
-      hipLaunchKernelGGL((score_bf16_decode_kernel<true, 2>), grid, block, lds, st, a);
-    else if (accumulate)
-      hipLaunchKernelGGL((score_bf16_decode_kernel<true, 1>), grid, block, lds, st, a);
-    else if (rb == 2)
-      hipLaunchKernelGGL((score_bf16_decode_kernel<false, 2>), grid, block, lds, st, a);
-    else
-      hipLaunchKernelGGL((score_bf16_decode_kernel<false, 1>), grid, block, lds, st, a);
+    const dim3 block(64 * (DC_WAVES + DC_COPY_WAVES));
+#define OMNIMOE_DECODE(ACC_, RB_, ST_) \
+  hipLaunchKernelGGL((score_bf16_decode_kernel<ACC_, RB_, ST_>), grid, block, lds, st, a)
+#define OMNIMOE_DECODE_STEPS(ACC_, RB_)                  \
+  do {                                                   \
+    switch (s.dk / 64) {                                 \
+      case 4: OMNIMOE_DECODE(ACC_, RB_, 4); break;       \
+      case 8: OMNIMOE_DECODE(ACC_, RB_, 8); break;       \
+      case 12: OMNIMOE_DECODE(ACC_, RB_, 12); break;     \
+      default: OMNIMOE_DECODE(ACC_, RB_, 16); break;     \
+    }                                                    \
+  } while (0)
+    if (accumulate && rb == 2) OMNIMOE_DECODE_STEPS(true, 2);
+    else if (accumulate) OMNIMOE_DECODE_STEPS(true, 1);
+    else if (rb == 2) OMNIMOE_DECODE_STEPS(false, 2);
+    else OMNIMOE_DECODE_STEPS(false, 1);
+#undef OMNIMOE_DECODE_STEPS
+#undef OMNIMOE_DECODE
   } else if (s.bf16 && s.T <= 64 && s.dk % 256 == 0) {
     dim3 grid((ncols + SK_N - 1) / SK_N, 2);
-    if (accumulate && s.T > 32)
-      hipLaunchKernelGGL((score_bf16_skinny_kernel<true, 2>), grid, dim3(256), 0, st, a);
-    else if (accumulate)
-      hipLaunchKernelGGL((score_bf16_skinny_kernel<true, 1>), grid, dim3(256), 0, st, a);
-    else if (s.T > 32)
-      hipLaunchKernelGGL((score_bf16_skinny_kernel<false, 2>), grid, dim3(256), 0, st, a);
-    else
-      hipLaunchKernelGGL((score_bf16_skinny_kernel<false, 1>), grid, dim3(256), 0, st, a);
+    // every fragment in flight at once for d_key <= 1024 (below 8 tokens: one row block)
+    const int steps = s.dk <= 1024 ? s.dk / 64 : 0;
+#define OMNIMOE_SKINNY(ACC_, RB_, ST_) \
+  hipLaunchKernelGGL((score_bf16_skinny_kernel<ACC_, RB_, ST_>), grid, dim3(256), 0, st, a)
+#define OMNIMOE_SKINNY_STEPS(ACC_, RB_)                  \
+  do {                                                   \
+    switch (steps) {                                     \
+      case 4: OMNIMOE_SKINNY(ACC_, RB_, 4); break;       \
+      case 8: OMNIMOE_SKINNY(ACC_, RB_, 8); break;       \
+      case 12: OMNIMOE_SKINNY(ACC_, RB_, 12); break;     \
+      case 16: OMNIMOE_SKINNY(ACC_, RB_, 16); break;     \
+      default: OMNIMOE_SKINNY(ACC_, RB_, 0); break;      \
+    }                                                    \
+  } while (0)
+    if (accumulate && s.T > 32) OMNIMOE_SKINNY(true, 2, 0);
+    else if (accumulate) OMNIMOE_SKINNY(true, 1, 0);
+    else if (s.T > 32) OMNIMOE_SKINNY(false, 2, 0);
+    else if (s.T > 8) OMNIMOE_SKINNY(false, 1, 0);
+    else OMNIMOE_SKINNY_STEPS(false, 1);
+#undef OMNIMOE_SKINNY_STEPS
+#undef OMNIMOE_SKINNY
   } else if (s.bf16 && s.dk % LK == 0) {
     dim3 grid((ncols + LN - 1) / LN, (unsigned)((s.T + LM - 1) / LM), 2);
     if (accumulate)

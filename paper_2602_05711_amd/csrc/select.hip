@@ -294,15 +294,26 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
   __shared__ int n_cand;
   __shared__ uint64_t lists[4][2][kWave];  // per wave: sorted row keys, sorted column keys
   __shared__ uint64_t stage[4][kWave];     // per wave: survivors, rows at 0, columns at 32
+  __shared__ int rank_cells[kWave], rank_first[kWave];
   const int K = a.K;
   const int kr = K < a.nr ? K : a.nr;
   const int kc = K < a.nc ? K : a.nc;
-  if (threadIdx.x == 0) {
-    int c = 0;
-    for (int ra = 0; ra < kr; ++ra)
-      for (int rb = 0; rb < kc && (ra + 1) * (rb + 1) <= K; ++rb)
-        cand[c++] = (uint16_t)((ra << 8) | rb);
-    n_cand = c;
+  // The candidate cells: row rank ra < kr pairs with the column ranks rb < min(kc, K / (ra + 1)),
+  // i.e. (ra + 1)(rb + 1) <= K. Wave 0 counts them per row rank and scans the counts, then every
+  // thread writes its share of the (at most 64 x 64) box. Their order is immaterial: the cells
+  // are sorted by key below.
+  if (threadIdx.x < kWave) {
+    const int ra = (int)threadIdx.x;
+    const int cnt = ra < kr ? (kc < K / (ra + 1) ? kc : K / (ra + 1)) : 0;
+    const int first = wave_excl_scan_i32(cnt);
+    rank_cells[ra] = cnt;
+    rank_first[ra] = first;
+    if (ra == kWave - 1) n_cand = first + cnt;
+  }
+  __syncthreads();
+  for (int j = (int)threadIdx.x; j < kWave * kWave; j += (int)blockDim.x) {
+    const int ra = j / kWave, rb = j % kWave;
+    if (rb < rank_cells[ra]) cand[rank_first[ra] + rb] = (uint16_t)((ra << 8) | rb);
   }
   __syncthreads();
   const int P = n_cand;

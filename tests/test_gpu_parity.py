@@ -72,6 +72,12 @@ SHAPES = {
     # shared out to the XCDs by token range
     "bucket_bf16": synth.Workload("bucket_bf16", T=3000, d=128, n_rows=64, n_cols=64, d_key=64,
                                   H=2, K=128),
+    # at most 8192 tasks (the layer's slot-order dot, no schedule), every expert picked by every
+    # token: 400 and 2730 tasks per expert, and the largest such batch (8190 tasks, ragged)
+    "slots_crowded_bf16": synth.Workload("slots_crowded_bf16", T=200, d=256, n_rows=2, n_cols=4,
+                                         d_key=64, H=2, K=8),
+    "slots_crowded_f32": synth.Workload("slots_crowded_f32", T=1365, d=128, n_rows=1, n_cols=3,
+                                        d_key=32, H=2, K=3, dtype="f32"),
 }
 
 
