@@ -21,7 +21,30 @@
 namespace omnimoe {
 namespace {
 
-constexpr int kMaxCand = 320;  // cells with (a+1)(b+1) <= 64: 280
+// The candidate cells (a, b) with (a + 1)(b + 1) <= K for every K <= 64, row rank major, one
+// list per K (the lists for K = 1 .. 64 hold 8104 cells): a constant table, so that no
+// workgroup builds its list before the first row. With fewer than K rows (columns) in the grid,
+// the cells with a >= Kr (b >= Kc) are skipped where the list is read.
+constexpr int kCandK = 64;
+constexpr int kCandCells = 8104;
+struct CandTable {
+  uint16_t cell[kCandCells];  // (a << 8) | b
+  uint16_t first[kCandK + 2];  // list of K: cell[first[K] .. first[K + 1])
+};
+constexpr CandTable make_cand_table() {
+  CandTable t{};
+  int c = 0;
+  t.first[0] = 0;
+  for (int K = 1; K <= kCandK; ++K) {
+    t.first[K] = (uint16_t)c;
+    for (int a = 0; a < K; ++a)
+      for (int b = 0; (a + 1) * (b + 1) <= K; ++b) t.cell[c++] = (uint16_t)((a << 8) | b);
+  }
+  t.first[kCandK + 1] = (uint16_t)c;
+  return t;
+}
+static_assert(make_cand_table().first[kCandK + 1] == kCandCells, "candidate table size");
+__constant__ CandTable kCand = make_cand_table();
 
 struct SelectArgs {
   const float* hs;
@@ -290,33 +313,13 @@ __device__ __noinline__ uint64_t half_topk_batched(const float* __restrict__ p, 
 
 template <int R, bool VEC, bool FULL>
 __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
-  __shared__ uint16_t cand[kMaxCand];  // (a << 8) | b
-  __shared__ int n_cand;
   __shared__ uint64_t lists[4][2][kWave];  // per wave: sorted row keys, sorted column keys
   __shared__ uint64_t stage[4][kWave];     // per wave: survivors, rows at 0, columns at 32
-  __shared__ int rank_cells[kWave], rank_first[kWave];
   const int K = a.K;
   const int kr = K < a.nr ? K : a.nr;
   const int kc = K < a.nc ? K : a.nc;
-  // The candidate cells: row rank ra < kr pairs with the column ranks rb < min(kc, K / (ra + 1)),
-  // i.e. (ra + 1)(rb + 1) <= K. Wave 0 counts them per row rank and scans the counts, then every
-  // thread writes its share of the (at most 64 x 64) box. Their order is immaterial: the cells
-  // are sorted by key below.
-  if (threadIdx.x < kWave) {
-    const int ra = (int)threadIdx.x;
-    const int cnt = ra < kr ? (kc < K / (ra + 1) ? kc : K / (ra + 1)) : 0;
-    const int first = wave_excl_scan_i32(cnt);
-    rank_cells[ra] = cnt;
-    rank_first[ra] = first;
-    if (ra == kWave - 1) n_cand = first + cnt;
-  }
-  __syncthreads();
-  for (int j = (int)threadIdx.x; j < kWave * kWave; j += (int)blockDim.x) {
-    const int ra = j / kWave, rb = j % kWave;
-    if (rb < rank_cells[ra]) cand[rank_first[ra] + rb] = (uint16_t)((ra << 8) | rb);
-  }
-  __syncthreads();
-  const int P = n_cand;
+  const uint16_t* cand = kCand.cell + kCand.first[K];
+  const int P = kCand.first[K + 1] - kCand.first[K];
   const int l = lane_id();
   const int w = threadIdx.x >> 6;
   uint64_t* rowk = lists[w][0];
@@ -366,9 +369,10 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
     for (int base = 0; base < P; base += kWave) {
       const int c = base + l;
       CellKey key{0ull, 0u};
-      if (c < P) {
-        const uint64_t kr_c = rowk[cand[c] >> 8];
-        const uint64_t kc_c = colk[cand[c] & 0xFF];
+      const int cell = c < P ? cand[c] : 0;
+      if (c < P && (cell >> 8) < kr && (cell & 0xFF) < kc) {
+        const uint64_t kr_c = rowk[cell >> 8];
+        const uint64_t kc_c = colk[cell & 0xFF];
         const float vr = f32_from_ord((uint32_t)(kr_c >> 32));
         const float vc = f32_from_ord((uint32_t)(kc_c >> 32));
         const uint32_t i = 0xFFFFFFFFu - (uint32_t)kr_c;
