@@ -201,13 +201,21 @@ __global__ __launch_bounds__(256) void expert_dot_kernel(DotArgs a) {
         for (int q = 0; q < CPL; ++q) acc = chunk_dot<BF16>(ur[i][q], xr[i][q], acc);
         h[i] = acc;
       }
+      // lane i finishes task j0 + i: one activation for the group instead of one per task
+      float hv = 0.0f, gv = 0.0f;
+      int pv = 0;
 #pragma unroll
       for (int i = 0; i < G; ++i) {
         if (j0 + i < cnt) {
           const float hs = wave_sum_uniform(h[i]);
-          if (l == i) a.a[pj[i]] = gj[i] * activation(a.act, hs);
+          if (l == i) {
+            hv = hs;
+            gv = gj[i];
+            pv = pj[i];
+          }
         }
       }
+      if (l < G && j0 + l < cnt) a.a[pv] = gv * activation(a.act, hv);
       // The last filled slot's expert carries into the next group.
       const int last = (cnt - j0 < G ? cnt - j0 : G) - 1;
 #pragma unroll
@@ -699,17 +707,22 @@ __global__ __launch_bounds__(256) void slot_dot_kernel(DotArgs a) {
       load_row<CPL>(xr[i], X + (p / a.hk) * a.nchunks, cv);
     }
   }
+  // lane i finishes slot p0 + i: one activation for the wave's slots
+  float hv = 0.0f, gv = 0.0f;
 #pragma unroll
   for (int i = 0; i < G; ++i) {
-    const int64_t p = p0 + i;
-    if (p < a.M) {
+    if (p0 + i < a.M) {
       float acc = 0.0f;
 #pragma unroll
       for (int q = 0; q < CPL; ++q) acc = chunk_dot<BF16>(ur[i][q], xr[i][q], acc);
       const float hs = wave_sum_uniform(acc);
-      if (l == 0) a.a[p] = gj[i] * activation(a.act, hs);
+      if (l == i) {
+        hv = hs;
+        gv = gj[i];
+      }
     }
   }
+  if (l < G && p0 + l < a.M) a.a[p0 + l] = gv * activation(a.act, hv);
 }
 
 template <bool BF16>
