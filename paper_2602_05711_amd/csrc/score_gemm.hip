@@ -325,6 +325,70 @@ __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
   else store_all([&](int r) { return m_lane + r < a.T; });
 }
 
+// ---------------------------------------------------------------- few-token bf16 kernel
+// For T <= 4: reading the sub-keys once is the whole cost, and MFMA fragments (32 rows x 32
+// bytes per load instruction) make the loads address-bound. Here sixteen lanes share a key row
+// and read it in coalesced 256-byte pieces (lane c of the sixteen takes chunks c, c + 16, ...
+// of 8 bf16), each lane forming TT partial dot products with v_dot2_f32_bf16 against the token
+// rows held in registers; the sixteen partial sums of a (token, key) pair are added in a fixed
+// tree (DPP within each 16-lane row). A wave covers four keys, a workgroup of four waves
+// sixteen. Requires d_key = 128 CH with CH = 1, 2, 4, 8 or 16.
+constexpr int GV_KEYS = 16;
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// v_dot2_f32_bf16 on two words of bf16 pairs. The words are taken by value: a bit cast applied
+// straight to an element of a vector (v.y) has been seen to compile to the cast of element 0.
+__device__ __forceinline__ float dot2_words(uint32_t p, uint32_t q, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, p),
+                                         __builtin_bit_cast(bf16x2_t, q), acc, false);
+}
+
+template <bool ACC, int TT, int CH>
+__global__ __launch_bounds__(256) void score_bf16_gemv_kernel(ScoreArgs a) {
+  const int half = blockIdx.y;
+  const int ncols = a.H * a.nh[half];
+  const int lane = threadIdx.x & 63, c16 = lane & 15;
+  const int n = blockIdx.x * GV_KEYS + (threadIdx.x >> 4);  // this row of sixteen lanes' key
+  const int nn = n < ncols ? n : ncols - 1;
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4* kr = (const u32x4*)((const uint16_t*)a.keys[half] + (int64_t)nn * a.dk) + c16;
+  u32x4 kv[CH];
+#pragma unroll
+  for (int q = 0; q < CH; ++q) kv[q] = __builtin_nontemporal_load(kr + 16 * q);
+  __builtin_amdgcn_sched_barrier(0);  // every key load is issued before the first use
+  float acc[TT];
+#pragma unroll
+  for (int t = 0; t < TT; ++t) {
+    const u32x4* xr = (const u32x4*)((const uint16_t*)a.x + (int64_t)(t < a.T ? t : a.T - 1) * a.d +
+                                     a.col0[half]) + c16;
+    float s = 0.0f;
+#pragma unroll
+    for (int q = 0; q < CH; ++q) {
+      const u32x4 xv = xr[16 * q];
+      s = dot2_words(kv[q].x, xv.x, s);
+      s = dot2_words(kv[q].y, xv.y, s);
+      s = dot2_words(kv[q].z, xv.z, s);
+      s = dot2_words(kv[q].w, xv.w, s);
+    }
+    // sum over the sixteen lanes of the row (quad swaps, then rotations by 4 and 8)
+    int x = __float_as_int(s);
+    s += __int_as_float(__builtin_amdgcn_update_dpp(x, x, 0xB1, 0xF, 0xF, false));
+    x = __float_as_int(s);
+    s += __int_as_float(__builtin_amdgcn_update_dpp(x, x, 0x4E, 0xF, 0xF, false));
+    x = __float_as_int(s);
+    s += __int_as_float(__builtin_amdgcn_update_dpp(x, x, 0x124, 0xF, 0xF, false));
+    x = __float_as_int(s);
+    s += __int_as_float(__builtin_amdgcn_update_dpp(x, x, 0x128, 0xF, 0xF, false));
+    acc[t] = s;
+  }
+  if (n < ncols) {
+    const int64_t oc = out_col(a, half, n);
+#pragma unroll
+    for (int t = 0; t < TT; ++t)
+      if (c16 == t && t < a.T) store_out<ACC>(a, (int64_t)t * a.ldo + oc, acc[t]);
+  }
+}
+
 // ---------------------------------------------------------------- skinny bf16 kernel
 // For T <= 64 (decode): the work is reading the sub-keys once. A workgroup owns 32 keys of one
 // half for all (<= 64) tokens; its four waves split d_key in four quarters, load MFMA operand
@@ -727,6 +791,31 @@ hipError_t launch_score(const Shape& s, const void* x, const void* keys_row,
     else OMNIMOE_DECODE_STEPS(false, 1);
 #undef OMNIMOE_DECODE_STEPS
 #undef OMNIMOE_DECODE
+  } else if (s.bf16 && s.T <= 4 && s.dk % 128 == 0 && s.dk <= 2048 &&
+             ((s.dk / 128) & (s.dk / 128 - 1)) == 0) {
+    const dim3 grid((ncols + GV_KEYS - 1) / GV_KEYS, 2);
+#define OMNIMOE_GEMV(ACC_, TT_, CH_) \
+  hipLaunchKernelGGL((score_bf16_gemv_kernel<ACC_, TT_, CH_>), grid, dim3(256), 0, st, a)
+#define OMNIMOE_GEMV_CH(ACC_, TT_)                                           \
+  do {                                                                       \
+    const int ch = s.dk / 128;                                               \
+    if (ch == 1) OMNIMOE_GEMV(ACC_, TT_, 1);                                 \
+    else if (ch == 2) OMNIMOE_GEMV(ACC_, TT_, 2);                            \
+    else if (ch == 4) OMNIMOE_GEMV(ACC_, TT_, 4);                            \
+    else if (ch == 8) OMNIMOE_GEMV(ACC_, TT_, 8);                            \
+    else OMNIMOE_GEMV(ACC_, TT_, 16);                                        \
+  } while (0)
+    if (accumulate) {
+      if (s.T == 1) OMNIMOE_GEMV_CH(true, 1);
+      else if (s.T == 2) OMNIMOE_GEMV_CH(true, 2);
+      else OMNIMOE_GEMV_CH(true, 4);
+    } else {
+      if (s.T == 1) OMNIMOE_GEMV_CH(false, 1);
+      else if (s.T == 2) OMNIMOE_GEMV_CH(false, 2);
+      else OMNIMOE_GEMV_CH(false, 4);
+    }
+#undef OMNIMOE_GEMV_CH
+#undef OMNIMOE_GEMV
   } else if (s.bf16 && s.T <= 64 && s.dk % 256 == 0) {
     dim3 grid((ncols + SK_N - 1) / SK_N, 2);
     // every fragment in flight at once for d_key <= 1024 (below 8 tokens: one row block)

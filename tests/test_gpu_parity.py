@@ -53,6 +53,12 @@ SHAPES = {
                                   H=3, K=7),
     "skinny1_bf16": synth.Workload("skinny1_bf16", T=1, d=1024, n_rows=48, n_cols=80, d_key=512,
                                    H=2, K=12),
+    # T <= 4: the coalesced few-token logit kernel (d_key 256 and 128; key rows past a head's
+    # end and a key count that is not a multiple of the sixteen per workgroup)
+    "few3_bf16": synth.Workload("few3_bf16", T=3, d=512, n_rows=40, n_cols=23, d_key=256, H=2,
+                                K=7),
+    "few2_bf16": synth.Workload("few2_bf16", T=2, d=256, n_rows=9, n_cols=31, d_key=128, H=3,
+                                K=5),
     "decode8_bf16": synth.Workload("decode8_bf16", T=8, d=2048, n_rows=100, n_cols=36,
                                    d_key=1024, H=2, K=9),
     "decode_dk768_bf16": synth.Workload("decode_dk768_bf16", T=20, d=1536, n_rows=70, n_cols=64,
@@ -914,6 +920,8 @@ MLP_CASES = {
     "ragged_bf16": (RAGGED, 104),
     "small_bf16": (W["small_bf16"], 512),
     "skinny_bf16": (SHAPES["skinny_bf16"], 512),
+    "few_token_bf16": (SHAPES["skinny1_bf16"], 512),
+    "few3_bf16": (SHAPES["few3_bf16"], 384),
     "wide_f32": (SHAPES["wide_f32"], 1024),
 }
 
