@@ -59,6 +59,14 @@ SHAPES = {
                                 K=7),
     "few2_bf16": synth.Workload("few2_bf16", T=2, d=256, n_rows=9, n_cols=31, d_key=128, H=3,
                                 K=5),
+    # decode-sized layers (slot-order dot) with 96, 100 and 128 slots per token: the routed sum
+    # in sixteen partial rows per token, some of them empty; fp32
+    "slots96_bf16": synth.Workload("slots96_bf16", T=40, d=512, n_rows=64, n_cols=48,
+                                   d_key=128, H=4, K=24),
+    "slots100_bf16": synth.Workload("slots100_bf16", T=9, d=1024, n_rows=30, n_cols=50,
+                                    d_key=256, H=4, K=25),
+    "slots128_f32": synth.Workload("slots128_f32", T=5, d=256, n_rows=32, n_cols=32, d_key=64,
+                                   H=2, K=64, dtype="f32"),
     "decode8_bf16": synth.Workload("decode8_bf16", T=8, d=2048, n_rows=100, n_cols=36,
                                    d_key=1024, H=2, K=9),
     "decode_dk768_bf16": synth.Workload("decode_dk768_bf16", T=20, d=1536, n_rows=70, n_cols=64,
