@@ -304,9 +304,11 @@ omnimoe_status omnimoe_route_backward(const omnimoe_layer_desc* desc, const void
  *   x [T, d], keys_row [H, n_rows, d_key], keys_col [H, n_cols, d_key], u, v [N, d]   dtype
  *   y [T, d] fp32 out; idx_out and gates_out ([T, H, K], as omnimoe_route's) may be NULL.
  * The expert compute is omnimoe_expert_forward's, or omnimoe_expert_forward_grouped's when
- * group_size > 1, dtype is bf16 and d % 64 == 0. With at most 8192 tasks (T*H*K) and
- * group_size 1 (a decode step, where nearly every task has an expert of its own) no schedule
- * is formed: the same a_p are computed in slot order, with identical results. Workspace:
+ * group_size > 1, dtype is bf16 and d % 64 == 0. With group_size 1, where the expert-major
+ * order saves no memory traffic (at most 8192 tasks T*H*K, as in a decode step; at most one task
+ * per two experts; or a u table N*d of at most 128 MiB, which stays in the GPU's last-level
+ * cache), no schedule is formed: the same a_p are computed in slot order, with identical
+ * results. Workspace:
  * OMNIMOE_STAGE_LAYER bytes
  * (caller-owned device memory, contents need not be initialised; OMNIMOE_ERR_WORKSPACE when
  * short). */

@@ -196,8 +196,9 @@ omnimoe_status layer_impl(const omnimoe_layer_desc* desc, const void* x, const v
   mark(2);
   const int32_t* sk = nullptr;
   const int32_t* gk = nullptr;
-  // Few tasks (a decode step): almost every task has an expert of its own, so the layer takes
-  // the slot-order dot and forms no schedule.
+  // Where the expert-major order saves no memory traffic (a decode step; at most one task per
+  // two experts; or a u table that fits in the MALL) the layer takes the slot-order dot and
+  // forms no schedule.
   const bool unscheduled = !layer_grouped(s) && omnimoe::slot_dot(s);
   if (!unscheduled && (e = omnimoe::launch_schedule(s, idx, perm, active, offsets, n_active,
                                                     nullptr, sched_ws, &sk, strm, &gk)))

@@ -675,14 +675,21 @@ hipError_t dispatch_dot(int cpl, dim3 grid, hipStream_t st, const DotArgs& a) {
   return hipGetLastError();
 }
 
-// ---------------------------------------------------------------- few tasks: slot order
-// For a small batch (M <= kSlotDotMaxTasks: one token up to a decode step) the dot runs in slot
-// order without a schedule: wave v takes slots 2v and 2v + 1, reads their experts and gates
-// and loads both u rows and token rows at once. With a handful of tasks per expert range there
-// is no u row to share between tasks (64 tokens pick ~8165 distinct experts of 2^20 in 8192
-// slots), so an expert-major order would cost a sort and save no reads. Each a[p] is summed
-// exactly as expert_dot_kernel sums it, so the two kernels give identical a.
+// ---------------------------------------------------------------- slot order (no schedule)
+// Where the expert-major order saves no memory traffic, the layer runs the dot in slot order
+// without a schedule: wave v takes slots 2v and 2v + 1, reads their experts and gates and loads
+// both u rows and token rows at once. That is the case (measured: bench, layer per call)
+//   - for a decode step (M <= 8192): 64 tokens pick ~8165 distinct experts of 2^20 in 8192
+//     slots, so there is no u row to share;
+//   - when tasks are at most half the experts (M <= N / 2, about 1.1 tasks per active expert
+//     under uniform routing): 2048 tokens on the 2^20-expert tables, 0.611 -> 0.505 ms;
+//   - when the u table fits in half the 256 MB MALL, where a re-read costs no HBM traffic: 4096
+//     tokens on 2^16 experts of d = 512, 0.201 -> 0.148 ms.
+// With 2.3 tasks per active expert and 4 GiB tables (16384 tokens on 2^20 experts) the schedule
+// pays: 3.54 against 3.64 ms. Each a[p] is summed exactly as expert_dot_kernel sums it, so the
+// two kernels give identical a.
 constexpr int kSlotDotMaxTasks = 8192;
+constexpr int64_t kSlotDotMaxTableBytes = 128ll << 20;
 
 template <int CPL, bool BF16>
 __global__ __launch_bounds__(256) void slot_dot_kernel(DotArgs a) {
@@ -833,7 +840,11 @@ hipError_t launch_expert_dot(const Shape& s, const void* x, const void* u, const
   return s.bf16 ? dispatch_dot<true>(cpl, grid, st, a) : dispatch_dot<false>(cpl, grid, st, a);
 }
 
-bool slot_dot(const Shape& s) { return s.M > 0 && s.M <= kSlotDotMaxTasks; }
+bool slot_dot(const Shape& s) {
+  const int64_t table = s.N * (int64_t)s.d * (s.bf16 ? 2 : 4);
+  return s.M > 0 &&
+         (s.M <= kSlotDotMaxTasks || 2 * s.M <= s.N || table <= kSlotDotMaxTableBytes);
+}
 
 hipError_t launch_slot_dot(const Shape& s, const void* x, const void* u, const int32_t* idx,
                            const float* gates, float* abuf, hipStream_t st) {

@@ -161,7 +161,8 @@ hipError_t launch_grouped_dot(const Shape& s, const void* x, const void* u, cons
                               const int32_t* n_active, const GroupPlan& plan, float* a,
                               hipStream_t st);
 
-// For M <= 8192 tasks: a[p] in slot order without a schedule (bf16 or fp32), identical to
+// Where the expert-major order saves no memory traffic (M <= 8192, M <= N / 2, or a u table of
+// at most 128 MiB): a[p] in slot order without a schedule (bf16 or fp32), identical to
 // launch_expert_dot's a.
 bool slot_dot(const Shape& s);
 hipError_t launch_slot_dot(const Shape& s, const void* x, const void* u, const int32_t* idx,
