@@ -8,6 +8,9 @@
 // then for up to four of the run's tasks at a time loads the token rows, forms the dot
 // products in fp32, and writes a[p] = g_p * act(x_t . u_e) into the token-major slot p.
 //
+// slot_dot: the same a[p] in slot order, without a schedule, where the expert-major order saves
+// no memory traffic (a decode step, few tasks per expert, tables that stay in the MALL).
+//
 // accumulate: token-major, one wavefront per token. The token's H*K slots are read in
 // (head, k) order, their v rows are fetched eight at a time and y_t += a[p] * v_e is summed in
 // slot order in fp32. The order is fixed, so y is the same on every run; no atomics are used.

@@ -6,6 +6,8 @@
 //
 // bf16, d_key % 64 == 0: 256 x 256 tile, four waves of 128 x 128 on v_mfma_f32_32x32x16_bf16,
 //   operands copied global -> LDS without registers (two 64 KiB stages, XOR-swizzled rows);
+// bf16, one to four tokens, d_key = 128 * 2^k <= 2048: sixteen lanes per key row with coalesced
+//   loads and v_dot2_f32_bf16 (no MFMA);
 // bf16, at most 64 tokens, d_key % 256 == 0: a split-K decode kernel with the token rows in LDS
 //   (8 or more tokens, d_key <= 1024), else a split-K skinny kernel with operands straight from
 //   memory;
