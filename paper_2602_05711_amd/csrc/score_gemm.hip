@@ -4,7 +4,7 @@
 // straight from row-major memory. The same kernels serve the dense router of the ablation
 // (one half of N gating vectors) and the shared MLP's projections (accumulating into y).
 //
-// bf16, d_key % 64 == 0: 256 x 256 tile, four waves of 128 x 128 on v_mfma_f32_32x32x16_bf16,
+// bf16, d_key % 64 == 0: 256 x 256 tile, eight waves of 128 x 64 on v_mfma_f32_32x32x16_bf16,
 //   operands copied global -> LDS without registers (two 64 KiB stages, XOR-swizzled rows);
 // bf16, one to four tokens, d_key = 128 * 2^k <= 2048: sixteen lanes per key row with coalesced
 //   loads and v_dot2_f32_bf16 (no MFMA);
@@ -170,7 +170,9 @@ __global__ __launch_bounds__(256) void score_bf16_kernel(ScoreArgs a) {
 }
 
 // ---------------------------------------------------------------- large-tile bf16 kernel
-// 256 x 256 macro tile, four waves of 128 x 128 (8 x 8 MFMA tiles, accumulators in AGPRs),
+// 256 x 256 macro tile, eight waves of 128 x 64 (4 x 2 MFMA tiles each; two waves per SIMD, so
+// one wave's MFMAs run while the other waits for its LDS fragments or the barrier: 0.604 ->
+// 0.587 ms at the training shape against four waves of 128 x 128, for 1.5x the LDS reads),
 // k-step 64, two LDS stages filled straight from global memory (global_load_lds_dwordx4, no
 // register staging). LDS rows are 128 B (64 bf16); the 16-byte chunk j of row r is stored at
 // position j ^ ((r >> 1) & 7), so the 16 rows read by one MFMA operand load fall in distinct
@@ -188,7 +190,7 @@ __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 __device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
 template <bool ACC, bool SPLIT = false>
-__global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(512, 1) void score_bf16_large_kernel(ScoreArgs a) {
   const int half = SPLIT ? 0 : blockIdx.z;
   const int ncols = a.H * a.nh[half];
   const int n0 = blockIdx.x * LN;
@@ -204,15 +206,15 @@ __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wid = tid >> 6;
-  const int wm = wid >> 1, wn = wid & 1;
+  const int wm = wid >> 2, wn = wid & 3;
 
-  // Loader: instruction i (0..7) of wave w covers rows 8 (8 w + i) .. +8 of A and of B; lane l
+  // Loader: instruction i (0..3) of wave w covers rows 8 (4 w + i) .. +8 of A and of B; lane l
   // fills LDS position l % 8 of row l / 8, i.e. global chunk (l % 8) ^ swz(row).
-  const uint16_t* ga[8];
-  const uint16_t* gb[8];
+  const uint16_t* ga[4];
+  const uint16_t* gb[4];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int r = (wid * 8 + i) * 8 + (lane >> 3);
+  for (int i = 0; i < 4; ++i) {
+    const int r = (wid * 4 + i) * 8 + (lane >> 3);
     const int j = (lane & 7) ^ swz(r);
     int64_t gm = m0 + r;
     if (gm >= a.T) gm = a.T - 1;
@@ -224,9 +226,9 @@ __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
   auto issue = [&](int stage, int k0) {
     unsigned char* base = smem + stage * LSTAGE;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      unsigned char* la = base + (wid * 8 + i) * 8 * LROW;
-      unsigned char* lb = base + LM * LROW + (wid * 8 + i) * 8 * LROW;
+    for (int i = 0; i < 4; ++i) {
+      unsigned char* la = base + (wid * 4 + i) * 8 * LROW;
+      unsigned char* lb = base + LM * LROW + (wid * 4 + i) * 8 * LROW;
       __builtin_amdgcn_global_load_lds((const void*)(ga[i] + k0), (lds_ptr_t)la, 16, 0, 0);
       __builtin_amdgcn_global_load_lds((const void*)(gb[i] + k0), (lds_ptr_t)lb, 16, 0, 0);
     }
@@ -235,11 +237,11 @@ __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
   // v_mfma_f32_32x32x16_bf16: lane l holds row (l % 32) of the A operand (column of B) and k
   // values 8 (l / 32) .. +7 of a 16-wide k step; accumulator register q of a 32 x 32 tile is
   // row 8 (q / 4) + 4 (l / 32) + q % 4, column l % 32.
-  f32x16 acc[4][4];
+  f32x16 acc[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
 
@@ -254,7 +256,7 @@ __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     a_off[i] = (wm * 128 + i * 32 + frow) * LROW;
-    b_off[i] = LM * LROW + (wn * 128 + i * 32 + frow) * LROW;
+    b_off[i] = LM * LROW + (wn * 64 + (i & 1) * 32 + frow) * LROW;
   }
   const int sw = swz(frow);  // rows i * 32 + frow share (r >> 1) & 7 with frow
   auto frag = [&](const unsigned char* st, int off, int ks) -> bf16x8 {
@@ -264,21 +266,19 @@ __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
     const int cur = kt & 1;
     if (kt + 1 < KT) issue(cur ^ 1, (kt + 1) * LK);
     const unsigned char* st = smem + cur * LSTAGE;
-    bf16x8 fa[2][4], fb[2][4];
+    bf16x8 fa[2][4], fb[2][2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      fa[0][i] = frag(st, a_off[i], 0);
-      fb[0][i] = frag(st, b_off[i], 0);
-    }
+    for (int i = 0; i < 4; ++i) fa[0][i] = frag(st, a_off[i], 0);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) fb[0][i] = frag(st, b_off[i], 0);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const int c = ks & 1;
       if (ks + 1 < 4) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          fa[c ^ 1][i] = frag(st, a_off[i], ks + 1);
-          fb[c ^ 1][i] = frag(st, b_off[i], ks + 1);
-        }
+        for (int i = 0; i < 4; ++i) fa[c ^ 1][i] = frag(st, a_off[i], ks + 1);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) fb[c ^ 1][i] = frag(st, b_off[i], ks + 1);
       }
       // keep the double buffer: the next step's fragment reads are issued before this step's
       // MFMAs (left alone, the scheduler sinks each read next to its use)
@@ -286,7 +286,7 @@ __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 2; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[c][i], fb[c][j], acc[i][j], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -303,8 +303,8 @@ __global__ __launch_bounds__(256, 1) void score_bf16_large_kernel(ScoreArgs a) {
   float* const obase = SPLIT ? out : a.out;
   auto store_all = [&](auto rows_ok) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int n = n0 + wn * 128 + j * 32 + (lane & 31);
+    for (int j = 0; j < 2; ++j) {
+      const int n = n0 + wn * 64 + j * 32 + (lane & 31);
       if (n >= ncols) continue;
       float* const orow = obase + m_lane * a.ldo + out_col(a, half, n);
 #pragma unroll
@@ -844,9 +844,9 @@ hipError_t launch_score(const Shape& s, const void* x, const void* keys_row,
   } else if (s.bf16 && s.dk % LK == 0) {
     dim3 grid((ncols + LN - 1) / LN, (unsigned)((s.T + LM - 1) / LM), 2);
     if (accumulate)
-      hipLaunchKernelGGL(score_bf16_large_kernel<true>, grid, dim3(256), 2 * LSTAGE, st, a);
+      hipLaunchKernelGGL(score_bf16_large_kernel<true>, grid, dim3(512), 2 * LSTAGE, st, a);
     else
-      hipLaunchKernelGGL(score_bf16_large_kernel<false>, grid, dim3(256), 2 * LSTAGE, st, a);
+      hipLaunchKernelGGL(score_bf16_large_kernel<false>, grid, dim3(512), 2 * LSTAGE, st, a);
   } else if (s.bf16) {
     dim3 grid((ncols + BN - 1) / BN, (unsigned)((s.T + BM - 1) / BM), 2);
     if (accumulate)
@@ -886,7 +886,7 @@ hipError_t launch_gemm_splitk(int64_t M, int N, const void* A, int64_t lda, cons
   a.kchunk = kchunk;
   a.part_stride = M * (int64_t)N;
   dim3 grid((N + LN - 1) / LN, (unsigned)((M + LM - 1) / LM), splits);
-  hipLaunchKernelGGL((score_bf16_large_kernel<false, true>), grid, dim3(256), 2 * LSTAGE, st, a);
+  hipLaunchKernelGGL((score_bf16_large_kernel<false, true>), grid, dim3(512), 2 * LSTAGE, st, a);
   return hipGetLastError();
 }
 
