@@ -723,7 +723,7 @@ hipError_t dispatch_dot(int cpl, dim3 grid, hipStream_t st, const DotArgs& a) {
 constexpr int kSlotDotMaxTasks = 8192;
 constexpr int64_t kSlotDotMaxTableBytes = 128ll << 20;
 
-template <int CPL, bool BF16>
+template <int CPL, bool BF16, bool FULL>
 __global__ __launch_bounds__(256) void slot_dot_kernel(DotArgs a) {
   constexpr int G = CPL >= 8 ? 1 : 2;  // slots per wave, all in flight
   const int l = lane_id();
@@ -732,33 +732,38 @@ __global__ __launch_bounds__(256) void slot_dot_kernel(DotArgs a) {
   const uint4* U = (const uint4*)a.u;
   bool cv[CPL];
 #pragma unroll
-  for (int q = 0; q < CPL; ++q) cv[q] = (l + kWave * q) < a.nchunks;
+  for (int q = 0; q < CPL; ++q) cv[q] = FULL || (l + kWave * q) < a.nchunks;
   uint4 ur[G][CPL], xr[G][CPL];
   float gj[G];
+  int ej[G];
+  // Every slot's expert and gate first, then the token rows (they need no index), then the u
+  // rows: loads complete in order, so an index load issued behind rows would make the u row
+  // that needs it wait for those rows as well. The loads are unconditional (a slot past the
+  // end reads the last slot again and is not stored) so that the compiler can count them.
+  int64_t pj[G];
 #pragma unroll
   for (int i = 0; i < G; ++i) {
-    const int64_t p = p0 + i;
-    gj[i] = 0.0f;
-    if (p < a.M) {
-      const int e = clamp_i(a.idx[p], a.N);
-      gj[i] = a.gates[p];
-      load_row_nt<CPL>(ur[i], U + (int64_t)e * a.nchunks, cv);
-      load_row<CPL>(xr[i], X + (p / a.hk) * a.nchunks, cv);
-    }
+    pj[i] = p0 + i < a.M ? p0 + i : a.M - 1;
+    ej[i] = a.idx[pj[i]];
+    gj[i] = a.gates[pj[i]];
   }
-  // lane i finishes slot p0 + i: one activation for the wave's slots
+#pragma unroll
+  for (int i = 0; i < G; ++i) load_row<CPL>(xr[i], X + (pj[i] / a.hk) * a.nchunks, cv);
+#pragma unroll
+  for (int i = 0; i < G; ++i)
+    load_row_nt<CPL>(ur[i], U + (int64_t)clamp_i(ej[i], a.N) * a.nchunks, cv);
+  // lane i finishes slot p0 + i: one activation for the wave's slots (the sums are formed for
+  // every slot, so that no load is moved into a branch behind another slot's work)
   float hv = 0.0f, gv = 0.0f;
 #pragma unroll
   for (int i = 0; i < G; ++i) {
-    if (p0 + i < a.M) {
-      float acc = 0.0f;
+    float acc = 0.0f;
 #pragma unroll
-      for (int q = 0; q < CPL; ++q) acc = chunk_dot<BF16>(ur[i][q], xr[i][q], acc);
-      const float hs = wave_sum_uniform(acc);
-      if (l == i) {
-        hv = hs;
-        gv = gj[i];
-      }
+    for (int q = 0; q < CPL; ++q) acc = chunk_dot<BF16>(ur[i][q], xr[i][q], acc);
+    const float hs = wave_sum_uniform(acc);
+    if (l == i) {
+      hv = hs;
+      gv = gj[i];
     }
   }
   if (l < G && p0 + l < a.M) a.a[p0 + l] = gv * activation(a.act, hv);
@@ -766,13 +771,20 @@ __global__ __launch_bounds__(256) void slot_dot_kernel(DotArgs a) {
 
 template <bool BF16>
 hipError_t dispatch_slot_dot(int cpl, dim3 grid, hipStream_t st, const DotArgs& a) {
+  const bool full = a.nchunks == cpl * kWave;
+#define OMNIMOE_SLOT(C_)                                                                    \
+  do {                                                                                      \
+    if (full) hipLaunchKernelGGL((slot_dot_kernel<C_, BF16, true>), grid, dim3(256), 0, st, a); \
+    else hipLaunchKernelGGL((slot_dot_kernel<C_, BF16, false>), grid, dim3(256), 0, st, a);    \
+  } while (0)
   switch (cpl) {
-    case 1: hipLaunchKernelGGL((slot_dot_kernel<1, BF16>), grid, dim3(256), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((slot_dot_kernel<2, BF16>), grid, dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((slot_dot_kernel<4, BF16>), grid, dim3(256), 0, st, a); break;
-    case 8: hipLaunchKernelGGL((slot_dot_kernel<8, BF16>), grid, dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL((slot_dot_kernel<16, BF16>), grid, dim3(256), 0, st, a); break;
+    case 1: OMNIMOE_SLOT(1); break;
+    case 2: OMNIMOE_SLOT(2); break;
+    case 4: OMNIMOE_SLOT(4); break;
+    case 8: OMNIMOE_SLOT(8); break;
+    default: OMNIMOE_SLOT(16); break;
   }
+#undef OMNIMOE_SLOT
   return hipGetLastError();
 }
 
