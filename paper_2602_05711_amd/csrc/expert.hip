@@ -1,7 +1,7 @@
 // Per-expert vector compute (Eq. 4, 7, 14).
 //
-// expert_dot: expert-major. The schedule's sorted positions are cut into ranges of about 16 or
-// 64 tasks, each starting at an expert boundary (a range only starts inside an expert's run
+// expert_dot: expert-major. The schedule's sorted positions are cut into ranges of about 8, 16
+// or 64 tasks, each starting at an expert boundary (a range only starts inside an expert's run
 // when the run is longer than the range, so very hot experts are shared out); each XCD takes a
 // contiguous share of the ranges. One wavefront walks its range run by run: it loads the
 // expert's u row once (16-byte loads with the non-temporal hint, every lane a slice),
@@ -163,6 +163,11 @@ __global__ __launch_bounds__(256) void expert_dot_kernel(DotArgs a) {
 #pragma unroll
   for (int q = 0; q < CPL; ++q) cv[q] = FULL || (l + kWave * q) < a.nchunks;
 
+  // token of a task: p / (H K), a shift when H K is a power of two (a 32-bit division is some
+  // fifteen scalar instructions, issued for every task)
+  const int hk_shift = (a.hk & (a.hk - 1)) == 0 ? __builtin_ctz((unsigned)a.hk) : -1;
+  auto token_of = [&](int p) { return hk_shift >= 0 ? p >> hk_shift : p / a.hk; };
+
   int prev = -1;    // expert whose u row sits in ur[G - 1]
   uint4 ur[G][CPL];
   uint4 xr[G][CPL];
@@ -194,7 +199,7 @@ __global__ __launch_bounds__(256) void expert_dot_kernel(DotArgs a) {
       }
 #pragma unroll
       for (int i = 0; i < G; ++i)
-        if (j0 + i < cnt) load_row<CPL>(xr[i], X + (int64_t)(pj[i] / a.hk) * row_chunks, cv);
+        if (j0 + i < cnt) load_row<CPL>(xr[i], X + (int64_t)token_of(pj[i]) * row_chunks, cv);
 #pragma unroll
       for (int i = 0; i < G; ++i) {
         const int before = (i == 0) ? prev : ej[i - 1];
@@ -878,11 +883,11 @@ hipError_t launch_expert_dot(const Shape& s, const void* x, const void* u, const
   a.hk = s.hk;
   a.act = s.act;
   a.nchunks = s.bf16 ? s.d / 8 : s.d / 4;
-  // 16 tasks per wave when experts average fewer than 8 tasks (fewer tasks in flight per XCD
-  // keeps its stretch of token rows in L2), 64 otherwise (a range starts inside an expert's run
+  // 8 tasks per wave when experts average at most 4 tasks, 16 below 8 (fewer tasks in flight per
+  // XCD keeps its stretch of token rows in L2), 64 otherwise (a range starts inside an expert's run
   // only when the run is longer than the range, and each such start reads u again); fewer, down
   // to one, so that small batches still give at least 2048 waves.
-  a.range = s.M < 8 * s.N ? 16 : 64;
+  a.range = s.M <= 4 * s.N ? 8 : (s.M < 8 * s.N ? 16 : 64);
   while (a.range > 1 && s.M < (int64_t)a.range * 2048) a.range >>= 1;
   const int64_t waves = (s.M + a.range - 1) / a.range;
   dim3 grid((unsigned)((waves + 3) / 4));
