@@ -192,7 +192,25 @@ def extras(args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1, 
     ev1.record(stream)
     torch.cuda.synchronize()
     tc_ms = ev0.elapsed_time(ev1) / args.steps
-    ec_ms = per["schedule"] + per["expert_dot"] + per["accumulate"]
+    # The layer's dot: its own kernel group, or, where the selection kernel forms it, the
+    # selection group less the plain selection on the same logits.
+    dot_ms = per["expert_dot"]
+    if P.omnimoe_layer_path(desc) & P.binding.PATH_SELECT_DOT:
+        hs = torch.empty((w.T, w.H, w.n_rows + w.n_cols), dtype=torch.float32, device="cuda")
+        i2, g2 = torch.empty_like(idx), torch.empty_like(g)
+        P.omnimoe_route(desc, d_in["x"], d_in["keys_row"], d_in["keys_col"], i2, g2,
+                        half_scores=hs, stream=stream)
+        sel = lambda: P.omnimoe_select(desc, hs, i2, g2, stream=stream)  # noqa: E731
+        for _ in range(2):
+            sel()
+        ev0.record(stream)
+        for _ in range(args.steps):
+            sel()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        dot_ms = max(per["select"] - ev0.elapsed_time(ev1) / args.steps, 0.0)
+        del hs, i2, g2
+    ec_ms = per["schedule"] + dot_ms + per["accumulate"]
     ablation = {"token_centric_expert_ms": tc_ms, "expert_centric_expert_ms": ec_ms,
                 "token_over_expert_centric": tc_ms / ec_ms,
                 "same_y": bool(torch.equal(y_tc, y))}
@@ -218,7 +236,7 @@ def extras(args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1, 
         ev1.record(stream)
         torch.cuda.synchronize()
         sc_ms = ev0.elapsed_time(ev1) / args.steps
-        slot_ms = per["expert_dot"] + per["accumulate"]
+        slot_ms = dot_ms + per["accumulate"]
         den = y.abs().amax(dim=1).clamp_min(1e-30)
         rel = float(((y_sc - y).abs().amax(dim=1) / den).max())
         contrib = {"dot_scatter_reduce_ms": sc_ms, "dot_accumulate_ms": slot_ms,
@@ -306,11 +324,11 @@ def extras(args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1, 
         rel = float(((yg - y1).abs().amax(dim=1) / y1.abs().amax(dim=1).clamp_min(1e-30)).max())
         grouped = {"group_size": gb, "per_kernel_ms": perg, "layer_ms": sum(perg.values()),
                    "expert_stage_ms": perg["expert_dot"] + perg["accumulate"],
-                   "per_task_expert_stage_ms": per["expert_dot"] + per["accumulate"],
+                   "per_task_expert_stage_ms": dot_ms + per["accumulate"],
                    "max_row_rel_diff_vs_per_task": rel}
         del y1
         log(f"grouped GEMM, B={gb}: layer {grouped['layer_ms']:.3f} ms (dot "
-            f"{perg['expert_dot']:.3f} ms vs per-task {per['expert_dot']:.3f} ms)")
+            f"{perg['expert_dot']:.3f} ms vs per-task {dot_ms:.3f} ms)")
         del wsg, yg
 
     # The second product of Eq. 14 per group (partial rows per (group, token) slot, then a
@@ -357,7 +375,7 @@ def extras(args, w, desc, d_in, dev, idx, g, y, stream, per, ms_step, ev0, ev1, 
                 rec[name + "_ms"] = e0.elapsed_time(e1) / args.steps
             rec["max_row_rel_diff"] = float(((yr - yq).abs().amax(dim=1) /
                                              yq.abs().amax(dim=1).clamp_min(1e-30)).max())
-            rec["per_task_expert_stage_ms"] = per["expert_dot"] + per["accumulate"]
+            rec["per_task_expert_stage_ms"] = dot_ms + per["accumulate"]
             group_rows.append(rec)
             log(f"group rows, B={gb}: {rec['group_rows_ms']:.3f} ms (grouped dot + slot-order sum "
                 f"{rec['grouped_slot_order_sum_ms']:.3f} ms; per-task stage "
@@ -454,6 +472,7 @@ def main():
 
     import synth
     import paper_2602_05711_amd as P
+    from paper_2602_05711_amd import binding as B
 
     w = synth.WORKLOADS[args.workload]
     if args.group_size > 0:
@@ -566,8 +585,20 @@ def main():
             (perm, off, na, n_active))
 
     work = algorithmic_work(w, n_active)
+    path = P.omnimoe_layer_path(desc)
+    # Kernel groups the layer does not launch for this shape: no schedule (slot-order dot), or
+    # a dot formed by the selection kernel, whose time and bytes then count under "select".
+    absent = {}
+    if not path & B.PATH_SCHEDULE:
+        absent["schedule"] = "not formed (slot-order dot)"
+    if path & B.PATH_SELECT_DOT:
+        absent["expert_dot"] = "formed by the selection kernel"
+        work["select"] = ("hbm", work["select"][1] + work["expert_dot"][1])
     kernels = {}
     for k, (bound, amount) in work.items():
+        if k in absent:
+            kernels[k] = {"absent": absent[k], "ms": per[k]}
+            continue
         t_s = per[k] * 1e-3
         if bound == "hbm":
             ach = amount / t_s / 1e9
@@ -579,6 +610,8 @@ def main():
             kernels[k] = {"bound": bound, "ms": per[k], "achieved": ach, "unit": "TFLOP/s",
                           "frac": ach / peak, "flop": amount}
     for k, kd in kernels.items():
+        if "absent" in kd:
+            continue
         tb = load_traffic(k, w.name)
         if tb is not None:
             # rocprofv3 bytes (L2 misses, MALL hits included) over the event-timed duration
@@ -588,7 +621,7 @@ def main():
             mb = load_mfma_busy(k, w.name)
             if mb is not None:
                 kd["mfma_busy"] = mb
-    dom = max(per, key=per.get)
+    dom = max((k for k in per if k not in absent), key=per.get)
     kd = kernels[dom]
     traffic = load_traffic(dom, w.name)
     roofline = {"kernel": dom, "bound": kd["bound"], "achieved": kd["achieved"],
@@ -642,7 +675,11 @@ def main():
         "group_rows_second_product": group_rows,
         "accumulate_contribution_rows": contrib,
         "n_active": n_active, "eta": w.M / max(1, n_active), "routing": routing,
-        "schedule_share": per["schedule"] / sum(per.values()),
+        "schedule_share": per["schedule"] / sum(per.values()) if path & B.PATH_SCHEDULE else 0.0,
+        "layer_path": {"schedule": bool(path & B.PATH_SCHEDULE),
+                       "grouped": bool(path & B.PATH_GROUPED),
+                       "select_forms_dot": bool(path & B.PATH_SELECT_DOT),
+                       "dense_routed_sum": bool(path & B.PATH_DENSE_SUM)},
         "kernels": kernels,
     }
     s = json.dumps(line)

@@ -308,7 +308,8 @@ omnimoe_status omnimoe_route_backward(const omnimoe_layer_desc* desc, const void
  * order saves no memory traffic (at most 8192 tasks T*H*K, as in a decode step; at most one task
  * per two experts; or a u table N*d of at most 128 MiB, which stays in the GPU's last-level
  * cache), no schedule is formed: the same a_p are computed in slot order, with identical
- * results. Workspace:
+ * results (by the selection kernel itself when there are at least 256 (token, head) rows;
+ * omnimoe_layer_path tells which kernels run). Workspace:
  * OMNIMOE_STAGE_LAYER bytes
  * (caller-owned device memory, contents need not be initialised; OMNIMOE_ERR_WORKSPACE when
  * short). */
@@ -316,6 +317,20 @@ omnimoe_status omnimoe_layer_forward(const omnimoe_layer_desc* desc, const void*
                                      const void* keys_row, const void* keys_col, const void* u,
                                      const void* v, float* y, int32_t* idx_out, float* gates_out,
                                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* Which kernels omnimoe_layer_forward runs for a descriptor (no device work, no pointers):
+ * *path receives an OR of the flags below. OMNIMOE_ERR_INVALID_ARG for a bad descriptor or a
+ * NULL path. The result depends only on the descriptor, so it can be taken once per shape. */
+typedef enum {
+  OMNIMOE_PATH_SCHEDULE = 1,   /* the expert-major schedule is formed (Eq. 12-13); without it the
+                                  a_p are formed in slot order */
+  OMNIMOE_PATH_GROUPED = 2,    /* a_p from the grouped GEMM of Eq. 14 (group_size > 1) */
+  OMNIMOE_PATH_SELECT_DOT = 4, /* the selection kernel also forms the slot-order a_p (no separate
+                                  dot launch; the OMNIMOE_KERNEL_SELECT time includes it) */
+  OMNIMOE_PATH_DENSE_SUM = 8   /* the routed sum as one dense product over all experts (one head,
+                                  K >= N / 64) */
+} omnimoe_path_flag;
+omnimoe_status omnimoe_layer_path(const omnimoe_layer_desc* desc, int32_t* path);
 
 /* For callers that cannot allocate device memory (code under HIP graph capture, tight serving
  * loops, harnesses that forbid hipMalloc): omnimoe_layer_forward with its workspace taken from

@@ -31,7 +31,8 @@ EXPORTED = (
     "omnimoe_expert_forward_group_rows",
     "omnimoe_expert_backward",
     "omnimoe_route_backward",
-    "omnimoe_layer_forward", "omnimoe_layer_forward_noalloc", "omnimoe_timer_create",
+    "omnimoe_layer_forward", "omnimoe_layer_forward_noalloc", "omnimoe_layer_path",
+    "omnimoe_timer_create",
     "omnimoe_timer_destroy", "omnimoe_timer_read", "omnimoe_layer_forward_timed",
     "omnimoe_status_string",
 )
@@ -81,6 +82,7 @@ def load_library():
         "omnimoe_route_backward": [D, P, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_layer_forward": [D, P, P, P, P, P, P, P, P, P, SZ, P],
         "omnimoe_layer_forward_noalloc": [D, P, P, P, P, P, P, P, P, P],
+        "omnimoe_layer_path": [D, ctypes.POINTER(I32)],
         "omnimoe_layer_forward_timed": [D, P, P, P, P, P, P, P, P, P, SZ, P, P],
         "omnimoe_timer_create": [I32, ctypes.POINTER(P)],
         "omnimoe_timer_destroy": [P],
@@ -262,6 +264,17 @@ def omnimoe_layer_forward(desc, x, keys_row, keys_col, u, v, y, idx_out=None, ga
 
 
 NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024  # OMNIMOE_NOALLOC_SCRATCH_BYTES
+
+# omnimoe_path_flag
+PATH_SCHEDULE, PATH_GROUPED, PATH_SELECT_DOT, PATH_DENSE_SUM = 1, 2, 4, 8
+
+
+def omnimoe_layer_path(desc):
+    """The omnimoe_path_flag bits of the kernels omnimoe_layer_forward runs for desc."""
+    out = ctypes.c_int32(0)
+    _check("omnimoe_layer_path", load_library().omnimoe_layer_path(ctypes.byref(desc),
+                                                                    ctypes.byref(out)))
+    return out.value
 
 
 def omnimoe_layer_forward_noalloc(desc, x, keys_row, keys_col, u, v, y, idx_out=None,

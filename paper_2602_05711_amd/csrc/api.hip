@@ -93,6 +93,25 @@ size_t active_bytes(const Shape& s) { return align_up((size_t)(std::min(s.M, s.N
 bool grouped_supported(const Shape& s) { return s.bf16 && s.d % 64 == 0; }
 bool layer_grouped(const Shape& s) { return s.B > 1 && grouped_supported(s); }
 
+// Which kernels the layer runs for a shape (omnimoe_layer_path reports the same flags).
+// Where the expert-major order saves no memory traffic (a decode step; at most one task per two
+// experts; or a u table that fits in the MALL) the layer takes the slot-order dot and forms no
+// schedule. With at least kSelectDotMinRows (token, head) rows the selection kernel forms that
+// dot itself; with fewer, a wave per row would fetch its K u rows four at a time, while the
+// separate dot kernel fetches all of them at once (one decoded token: 19.1 against 22.1 us).
+constexpr int64_t kSelectDotMinRows = 256;
+int32_t layer_path(const Shape& s) {
+  const bool grouped = layer_grouped(s);
+  const bool unscheduled = !grouped && omnimoe::slot_dot(s);
+  int32_t f = 0;
+  if (!unscheduled) f |= OMNIMOE_PATH_SCHEDULE;
+  if (grouped) f |= OMNIMOE_PATH_GROUPED;
+  if (unscheduled && s.rows >= kSelectDotMinRows && omnimoe::select_dot_fusable(s))
+    f |= OMNIMOE_PATH_SELECT_DOT;
+  if (omnimoe::dense_accumulate(s)) f |= OMNIMOE_PATH_DENSE_SUM;
+  return f;
+}
+
 // Schedule workspace, followed by the grouped plan's (which reads the schedule's sorted keys).
 // The routed sum y_t = sum of a_p v_e over t's tasks: one dense GEMM over all experts when
 // the pairs are dense enough (Eq. 14 with a single group), else the token-major slot-order
@@ -140,6 +159,10 @@ size_t stage_bytes(const Shape& s, int stage) {
       // buffers.
       size_t fixed = 3 * m_bytes(s) + 2 * active_bytes(s) + 256;
       size_t late = sched_or_plan_bytes(s) + m_bytes(s) + omnimoe::dense_accumulate_ws_bytes(s);
+      // A selection kernel that forms a[] writes it while other rows' logits are still being
+      // read: a[] and the dense sum's buffers then follow the logits instead of sharing them.
+      if (layer_path(s) & OMNIMOE_PATH_SELECT_DOT)
+        late = hs_bytes(s) + m_bytes(s) + omnimoe::dense_accumulate_ws_bytes(s);
       return fixed + std::max(hs_bytes(s), late);
     }
   }
@@ -180,7 +203,10 @@ omnimoe_status layer_impl(const omnimoe_layer_desc* desc, const void* x, const v
   char* late = w;
   float* hs = (float*)late;
   void* sched_ws = late;
-  float* abuf = (float*)(late + sched_or_plan_bytes(s));
+  const int32_t path = layer_path(s);
+  // (after the logits when the selection kernel writes a[]: see stage_bytes)
+  float* abuf = (float*)(late + ((path & OMNIMOE_PATH_SELECT_DOT) ? hs_bytes(s)
+                                                                  : sched_or_plan_bytes(s)));
   if (idx_out) idx = idx_out;
   if (gates_out) gates = gates_out;
 
@@ -192,21 +218,25 @@ omnimoe_status layer_impl(const omnimoe_layer_desc* desc, const void* x, const v
   mark(0);
   if ((e = omnimoe::launch_score(s, x, keys_row, keys_col, hs, strm))) return hip_status(e);
   mark(1);
-  if ((e = omnimoe::launch_select(s, hs, idx, gates, strm))) return hip_status(e);
+  const bool unscheduled = !(path & OMNIMOE_PATH_SCHEDULE);
+  const bool fused = (path & OMNIMOE_PATH_SELECT_DOT) != 0;
+  if (fused) {
+    if ((e = omnimoe::launch_select_dot(s, hs, idx, gates, x, u, abuf, strm)))
+      return hip_status(e);
+  } else if ((e = omnimoe::launch_select(s, hs, idx, gates, strm))) {
+    return hip_status(e);
+  }
   mark(2);
   const int32_t* sk = nullptr;
   const int32_t* gk = nullptr;
-  // Where the expert-major order saves no memory traffic (a decode step; at most one task per
-  // two experts; or a u table that fits in the MALL) the layer takes the slot-order dot and
-  // forms no schedule.
-  const bool unscheduled = !layer_grouped(s) && omnimoe::slot_dot(s);
   if (!unscheduled && (e = omnimoe::launch_schedule(s, idx, perm, active, offsets, n_active,
                                                     nullptr, sched_ws, &sk, strm, &gk)))
     return hip_status(e);
   mark(3);
   if (unscheduled) {
-    if ((e = omnimoe::launch_slot_dot(s, x, u, idx, gates, abuf, strm))) return hip_status(e);
-  } else if (layer_grouped(s)) {
+    if (!fused && (e = omnimoe::launch_slot_dot(s, x, u, idx, gates, abuf, strm)))
+      return hip_status(e);
+  } else if (path & OMNIMOE_PATH_GROUPED) {
     omnimoe::GroupPlan plan;
     void* plan_ws = (char*)sched_ws + omnimoe::schedule_ws_bytes(s.M, s.N);
     if ((e = omnimoe::launch_group_plan(s, perm, n_active, gk, idx, active, plan_ws, &plan,
@@ -574,6 +604,15 @@ omnimoe_status omnimoe_layer_forward(const omnimoe_layer_desc* desc, const void*
                                      void* ws, size_t ws_bytes, void* stream) {
   return layer_impl(desc, x, keys_row, keys_col, u, v, y, idx_out, gates_out, ws, ws_bytes,
                     stream, nullptr);
+}
+
+omnimoe_status omnimoe_layer_path(const omnimoe_layer_desc* desc, int32_t* path) {
+  Shape s;
+  omnimoe_status st = check_desc(desc, &s);
+  if (st) return st;
+  if (!path) return OMNIMOE_ERR_INVALID_ARG;
+  *path = layer_path(s);
+  return OMNIMOE_OK;
 }
 
 omnimoe_status omnimoe_layer_forward_noalloc(const omnimoe_layer_desc* desc, const void* x,

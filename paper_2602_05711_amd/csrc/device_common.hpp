@@ -101,6 +101,32 @@ __device__ __forceinline__ int wave_excl_scan_i32(int v) {
   return x - v;
 }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float dot2_bf16(uint32_t p, uint32_t q, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p),
+                                         __builtin_bit_cast(bf16x2, q), acc, false);
+}
+
+// fp32 dot of one 16-byte chunk pair (bf16 pairs through v_dot2_f32_bf16), the products
+// added in a fixed order; the expert dot kernels and the fused selection share it, so that
+// every path forms the same a[p].
+template <bool BF16>
+__device__ __forceinline__ float chunk_dot(const uint4& p, const uint4& q, float acc) {
+  if constexpr (BF16) {
+    acc = dot2_bf16(p.x, q.x, acc);
+    acc = dot2_bf16(p.y, q.y, acc);
+    acc = dot2_bf16(p.z, q.z, acc);
+    acc = dot2_bf16(p.w, q.w, acc);
+  } else {
+    acc = fmaf(__uint_as_float(p.x), __uint_as_float(q.x), acc);
+    acc = fmaf(__uint_as_float(p.y), __uint_as_float(q.y), acc);
+    acc = fmaf(__uint_as_float(p.z), __uint_as_float(q.z), acc);
+    acc = fmaf(__uint_as_float(p.w), __uint_as_float(q.w), acc);
+  }
+  return acc;
+}
+
 // Wave-uniform sum: DPP adds within each 16-lane row (quad swaps, then rotations by 4 and 8),
 // then the four row sums read out in a fixed order. Every lane gets the same value.
 __device__ __forceinline__ float wave_sum_uniform(float v) {

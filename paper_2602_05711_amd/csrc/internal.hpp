@@ -55,6 +55,13 @@ hipError_t launch_dense_accumulate(const Shape& s, const void* v, const int32_t*
 hipError_t launch_select(const Shape& s, const float* half_scores, int32_t* idx, float* gates,
                          hipStream_t st);
 
+// launch_select followed by the slot-order dot of launch_slot_dot, in one kernel (the same idx,
+// gates and a): bf16, K <= 64, nr == nc in {256, 512, 1024}, d / 8 in {64, 128, 256, 512}.
+bool select_dot_fusable(const Shape& s);
+hipError_t launch_select_dot(const Shape& s, const float* half_scores, int32_t* idx,
+                             float* gates, const void* x, const void* u, float* abuf,
+                             hipStream_t st);
+
 // Dense-router selection (the router ablation): top K of each row of logits [rows, n] by
 // (logit desc, id asc) and softmax gates.
 hipError_t launch_select_dense(int64_t rows, int64_t n, int K, const float* logits, int32_t* idx,

@@ -349,6 +349,9 @@ template <bool ACC, int TT, int CH>
 __global__ __launch_bounds__(256) void score_bf16_gemv_kernel(ScoreArgs a) {
   const int half = blockIdx.y;
   const int ncols = a.H * a.nh[half];
+  // a workgroup past the half's keys (all of them for an empty half, as the shared MLP's and the
+  // dense router's single-half products have) reads nothing: the clamp below needs a key
+  if ((int)blockIdx.x * GV_KEYS >= ncols) return;
   const int lane = threadIdx.x & 63, c16 = lane & 15;
   const int n = blockIdx.x * GV_KEYS + (threadIdx.x >> 4);  // this row of sixteen lanes' key
   const int nn = n < ncols ? n : ncols - 1;

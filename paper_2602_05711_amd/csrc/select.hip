@@ -52,6 +52,13 @@ struct SelectArgs {
   float* gates;
   int64_t rows;
   int nr, nc, K;
+  // fused slot-order dot (select_kernel with DCPL > 0): a[row K + k] = g * act(x_t . u_e) for
+  // each pick, bf16 rows of exactly DCPL * 64 16-byte chunks
+  const void* x;
+  const void* u;
+  float* abuf;
+  int64_t N;
+  int H, act;
 };
 
 // ---------------------------------------------------------------- cross-lane exchange
@@ -311,7 +318,11 @@ __device__ __noinline__ uint64_t half_topk_batched(const float* __restrict__ p, 
   return best;
 }
 
-template <int R, bool VEC, bool FULL>
+// DCPL > 0: after a row's picks and gates, the same wave forms their a[p] in slot order (the
+// layer's dot where it forms no schedule): the token row once, then the u rows four at a time,
+// each product summed exactly as slot_dot_kernel sums it, so a[p] is the same on both paths.
+// This saves the dot's launch and its reads of idx and gates at a decode step.
+template <int R, bool VEC, bool FULL, int DCPL = 0>
 __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
   __shared__ uint64_t lists[4][2][kWave];  // per wave: sorted row keys, sorted column keys
   __shared__ uint64_t stage[4][kWave];     // per wave: survivors, rows at 0, columns at 32
@@ -393,6 +404,39 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
     if (l < K) {
       a.idx[row * K + l] = (int32_t)(0xFFFFFFFFu - best.nn);
       a.gates[row * K + l] = e / z;
+    }
+    if constexpr (DCPL > 0) {
+      typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+      const uint4* X = (const uint4*)a.x + (row / a.H) * (int64_t)(DCPL * kWave);
+      const uint4* U = (const uint4*)a.u;
+      const int eid = (int)(0xFFFFFFFFu - best.nn);  // lane k < K: the k-th pick
+      uint4 xr[DCPL];
+#pragma unroll
+      for (int q = 0; q < DCPL; ++q) xr[q] = X[l + kWave * q];
+      float hv = 0.0f;
+      for (int j0 = 0; j0 < K; j0 += 4) {
+        uint4 ur[4][DCPL];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          int ei = readlane_i32(eid, j0 + i < K ? j0 + i : K - 1);
+          ei = ei < 0 ? 0 : (ei >= a.N ? (int)(a.N - 1) : ei);
+          const u32x4_t* ub = (const u32x4_t*)(U + (int64_t)ei * (DCPL * kWave));
+#pragma unroll
+          for (int q = 0; q < DCPL; ++q) {
+            const u32x4_t v = __builtin_nontemporal_load(ub + l + kWave * q);
+            ur[i][q] = make_uint4(v.x, v.y, v.z, v.w);
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float acc = 0.0f;
+#pragma unroll
+          for (int q = 0; q < DCPL; ++q) acc = chunk_dot<true>(ur[i][q], xr[q], acc);
+          const float hs = wave_sum_uniform(acc);
+          if (l == j0 + i) hv = hs;
+        }
+      }
+      if (l < K) a.abuf[row * K + l] = (e / z) * activation(a.act, hv);
     }
 #pragma unroll
     for (int k = 0; k < R; ++k) {
@@ -1069,6 +1113,50 @@ hipError_t launch_select(const Shape& s, const float* half_scores, int32_t* idx,
   else if (nmax <= 2048) OMNIMOE_SELECT(32);
   else OMNIMOE_SELECT(64);
 #undef OMNIMOE_SELECT
+  return hipGetLastError();
+}
+
+bool select_dot_fusable(const Shape& s) {
+  const int nchunks = s.d / 8;
+  const bool rows_ok = s.nr == s.nc && (s.nr == 256 || s.nr == 512 || s.nr == 1024);
+  const bool dot_ok = nchunks == 64 || nchunks == 128 || nchunks == 256 || nchunks == 512;
+  return s.bf16 && s.K <= kWave && s.d % 8 == 0 && rows_ok && dot_ok;
+}
+
+hipError_t launch_select_dot(const Shape& s, const float* half_scores, int32_t* idx,
+                             float* gates, const void* x, const void* u, float* abuf,
+                             hipStream_t st) {
+  if (s.rows == 0) return hipSuccess;
+  if (!select_dot_fusable(s)) return hipErrorNotSupported;
+  SelectArgs a;
+  a.hs = half_scores;
+  a.idx = idx;
+  a.gates = gates;
+  a.rows = s.rows;
+  a.nr = s.nr;
+  a.nc = s.nc;
+  a.K = s.K;
+  a.x = x;
+  a.u = u;
+  a.abuf = abuf;
+  a.N = s.N;
+  a.H = s.H;
+  a.act = s.act;
+  int64_t blocks = (s.rows + 3) / 4;
+  if (blocks > 8192) blocks = 8192;
+  const dim3 grid((unsigned)blocks), block(256);
+  const int cpl = s.d / 8 / kWave;
+#define OMNIMOE_SELECT_DOT(R_)                                                                 \
+  do {                                                                                         \
+    if (cpl == 1) hipLaunchKernelGGL((select_kernel<R_, true, true, 1>), grid, block, 0, st, a);      \
+    else if (cpl == 2) hipLaunchKernelGGL((select_kernel<R_, true, true, 2>), grid, block, 0, st, a); \
+    else if (cpl == 4) hipLaunchKernelGGL((select_kernel<R_, true, true, 4>), grid, block, 0, st, a); \
+    else hipLaunchKernelGGL((select_kernel<R_, true, true, 8>), grid, block, 0, st, a);               \
+  } while (0)
+  if (s.nr == 256) OMNIMOE_SELECT_DOT(4);
+  else if (s.nr == 512) OMNIMOE_SELECT_DOT(8);
+  else OMNIMOE_SELECT_DOT(16);
+#undef OMNIMOE_SELECT_DOT
   return hipGetLastError();
 }
 

@@ -24,7 +24,7 @@ def _declared_functions():
 def test_header_matches_exports():
     lib = P.load_library()
     names = _declared_functions()
-    assert len(names) == 22
+    assert len(names) == 23
     assert sorted(P.EXPORTED) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -226,3 +226,26 @@ def test_binding_raises_on_error():
     d.K = 5000
     with pytest.raises(B.OmnimoeError):
         B.omnimoe_workspace_size(d, B.STAGE_LAYER)
+
+
+def test_layer_path_flags():
+    # Host-side only: which kernels the layer runs for a descriptor.
+    f = {w: P.omnimoe_layer_path(B.make_desc(synth.WORKLOADS[w]))
+         for w in ("train_bf16", "skew_bf16", "decode1_bf16", "decode64_bf16", "dp8share_bf16",
+                   "small_bf16", "tiny_f32", "paper_k512_bf16", "paper_k4096_bf16")}
+    assert f["train_bf16"] == B.PATH_SCHEDULE and f["skew_bf16"] == B.PATH_SCHEDULE
+    # a decode step forms no schedule; with 512 (token, head) rows the selection forms the dot,
+    # with 8 a separate kernel does
+    assert f["decode1_bf16"] == 0
+    assert f["decode64_bf16"] == B.PATH_SELECT_DOT
+    assert f["dp8share_bf16"] == B.PATH_SELECT_DOT and f["small_bf16"] == B.PATH_SELECT_DOT
+    assert f["tiny_f32"] == 0  # fp32: no fused selection
+    assert f["paper_k512_bf16"] == B.PATH_SCHEDULE
+    assert f["paper_k4096_bf16"] == B.PATH_SCHEDULE | B.PATH_DENSE_SUM
+    grouped = B.make_desc(synth.WORKLOADS["paper_k4096_bf16"].with_(group_size=64))
+    assert P.omnimoe_layer_path(grouped) & B.PATH_GROUPED
+    bad = B.make_desc(synth.WORKLOADS["small_bf16"])
+    bad.K = 0
+    with pytest.raises(P.OmnimoeError):
+        P.omnimoe_layer_path(bad)
+    assert P.load_library().omnimoe_layer_path(ctypes.byref(bad), None) == INVALID

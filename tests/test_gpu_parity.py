@@ -855,6 +855,8 @@ DENSE_SHAPES = {
                                      d_key=64, H=1, K=16),
     # 64 tokens: the skinny logit kernel, 65536-wide rows
     "small64_bf16": W["small_bf16"].with_(name="small64_bf16", T=64),
+    # one token: the few-token logit kernel on a single (N-wide) half, the other half empty
+    "one_token_bf16": W["small_bf16"].with_(name="one_token_bf16", T=1),
 }
 
 
@@ -929,6 +931,9 @@ MLP_CASES = {
     "small_bf16": (W["small_bf16"], 512),
     "skinny_bf16": (SHAPES["skinny_bf16"], 512),
     "few_token_bf16": (SHAPES["skinny1_bf16"], 512),
+    # a decode step's width: both projections on the few-token kernel with 2048-wide rows and
+    # an empty second half
+    "decode1_bf16": (W["decode1_bf16"], 2048),
     "few3_bf16": (SHAPES["few3_bf16"], 384),
     "wide_f32": (SHAPES["wide_f32"], 1024),
 }
