@@ -67,18 +67,74 @@ __device__ __forceinline__ float chunk_elem(const uint4& c, int k) {
   }
 }
 
-template <int CPL, bool BF16>
+// Slots s0 .. s0 + GG - 1 of token t (expert e and gate g of slot s0 + i on lane i of ev/gv, an
+// offset of the slot batch sb): their u and v rows are loaded together, then h, da, a, dh and
+// dgates are formed and dx += dh u_e summed in slot order.
+template <int GG, int CPL, bool BF16>
+__device__ __forceinline__ void token_slots(const BwdArgs& a, int64_t t, int s0, int sb, int ev,
+                                            float gv, const uint4 (&xr)[CPL],
+                                            const float (&dyr)[CPL][BF16 ? 8 : 4],
+                                            const bool (&cv)[CPL],
+                                            float (&acc)[CPL][BF16 ? 8 : 4]) {
+  constexpr int EPC = BF16 ? 8 : 4;
+  const int l = lane_id();
+  const uint4* U = (const uint4*)a.u;
+  const uint4* V = (const uint4*)a.v;
+  const int64_t rc = a.nchunks;
+  uint4 ur[GG][CPL], vr[GG][CPL];
+#pragma unroll
+  for (int i = 0; i < GG; ++i) {
+    const int e = clamp_id(readlane_i32(ev, s0 + i - sb), a.N);
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      ur[i][q] = cv[q] ? U[(int64_t)e * rc + l + kWave * q] : make_uint4(0, 0, 0, 0);
+      vr[i][q] = cv[q] ? V[(int64_t)e * rc + l + kWave * q] : make_uint4(0, 0, 0, 0);
+    }
+  }
+  // every row of the group is requested before the first product
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int i = 0; i < GG; ++i) {
+    const int64_t p = t * a.hk + s0 + i;
+    const float g = readlane_f32(gv, s0 + i - sb);
+    float hs = 0.0f, ds = 0.0f;
+#pragma unroll
+    for (int q = 0; q < CPL; ++q)
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) {
+        hs = fmaf(chunk_elem<BF16>(xr[q], k), chunk_elem<BF16>(ur[i][q], k), hs);
+        ds = fmaf(dyr[q][k], chunk_elem<BF16>(vr[i][q], k), ds);
+      }
+    const float h = wave_sum_uniform(hs);
+    const float da = wave_sum_uniform(ds);
+    const float act = activation(a.act, h);
+    const float dh = da * g * activation_grad(a.act, h);
+    if (l == 0) {
+      a.a[p] = g * act;
+      a.dh[p] = dh;
+      a.dgates[p] = da * act;
+    }
+#pragma unroll
+    for (int q = 0; q < CPL; ++q)
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) acc[q][k] = fmaf(dh, chunk_elem<BF16>(ur[i][q], k), acc[q][k]);
+  }
+}
+
+// Token pass: one wave per token. The token's experts and gates are read 64 slots at a time
+// (one load per lane), and the slots then go through G at a time with all of their u and v
+// rows in flight, whole groups first and the rest singly, so that no row load waits behind the
+// previous slot's work. FULL: the row is exactly CPL * 64 chunks (no load carries a guard).
+template <int CPL, bool BF16, bool FULL>
 __global__ __launch_bounds__(256) void bwd_token_kernel(BwdArgs a) {
   constexpr int EPC = BF16 ? 8 : 4;
   constexpr int G = CPL >= 8 ? 1 : (CPL >= 4 ? 2 : 4);
   const int l = lane_id();
   const uint4* X = (const uint4*)a.x;
-  const uint4* U = (const uint4*)a.u;
-  const uint4* V = (const uint4*)a.v;
   const int64_t rc = a.nchunks;
   bool cv[CPL];
 #pragma unroll
-  for (int q = 0; q < CPL; ++q) cv[q] = (l + kWave * q) < a.nchunks;
+  for (int q = 0; q < CPL; ++q) cv[q] = FULL || (l + kWave * q) < a.nchunks;
   const int64_t stride = (int64_t)gridDim.x * 4;
   for (int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < a.T; t += stride) {
     uint4 xr[CPL];
@@ -88,55 +144,27 @@ __global__ __launch_bounds__(256) void bwd_token_kernel(BwdArgs a) {
     for (int q = 0; q < CPL; ++q) {
       const int c = l + kWave * q;
       xr[q] = cv[q] ? X[t * rc + c] : make_uint4(0, 0, 0, 0);
+      const float4* dyc = (const float4*)(a.dy + t * a.d + (int64_t)c * EPC);
 #pragma unroll
-      for (int k = 0; k < EPC; ++k) {
-        dyr[q][k] = cv[q] ? a.dy[t * a.d + (int64_t)c * EPC + k] : 0.0f;
-        acc[q][k] = 0.0f;
+      for (int k = 0; k < EPC; k += 4) {
+        const float4 y4 = cv[q] ? dyc[k / 4] : make_float4(0.f, 0.f, 0.f, 0.f);
+        dyr[q][k] = y4.x;
+        dyr[q][k + 1] = y4.y;
+        dyr[q][k + 2] = y4.z;
+        dyr[q][k + 3] = y4.w;
       }
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) acc[q][k] = 0.0f;
     }
-    // G slots at a time: their u and v rows are all in flight before the first reduction
-    for (int s0 = 0; s0 < a.hk; s0 += G) {
-      uint4 ur[G][CPL], vr[G][CPL];
-      float gj[G];
-      int64_t pj[G];
-#pragma unroll
-      for (int i = 0; i < G; ++i) {
-        const int s = s0 + i < a.hk ? s0 + i : a.hk - 1;
-        pj[i] = t * a.hk + s;
-        const int e = clamp_id(a.idx[pj[i]], a.N);
-        gj[i] = a.gates[pj[i]];
-#pragma unroll
-        for (int q = 0; q < CPL; ++q) {
-          ur[i][q] = cv[q] ? U[(int64_t)e * rc + l + kWave * q] : make_uint4(0, 0, 0, 0);
-          vr[i][q] = cv[q] ? V[(int64_t)e * rc + l + kWave * q] : make_uint4(0, 0, 0, 0);
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < G; ++i) {
-        if (s0 + i >= a.hk) break;
-        float hs = 0.0f, ds = 0.0f;
-#pragma unroll
-        for (int q = 0; q < CPL; ++q)
-#pragma unroll
-          for (int k = 0; k < EPC; ++k) {
-            hs = fmaf(chunk_elem<BF16>(xr[q], k), chunk_elem<BF16>(ur[i][q], k), hs);
-            ds = fmaf(dyr[q][k], chunk_elem<BF16>(vr[i][q], k), ds);
-          }
-        const float h = wave_sum_uniform(hs);
-        const float da = wave_sum_uniform(ds);
-        const float act = activation(a.act, h);
-        const float dh = da * gj[i] * activation_grad(a.act, h);
-        if (l == 0) {
-          a.a[pj[i]] = gj[i] * act;
-          a.dh[pj[i]] = dh;
-          a.dgates[pj[i]] = da * act;
-        }
-#pragma unroll
-        for (int q = 0; q < CPL; ++q)
-#pragma unroll
-          for (int k = 0; k < EPC; ++k)
-            acc[q][k] = fmaf(dh, chunk_elem<BF16>(ur[i][q], k), acc[q][k]);
-      }
+    for (int sb = 0; sb < a.hk; sb += kWave) {
+      const int n = a.hk - sb < kWave ? a.hk - sb : kWave;
+      const int64_t pl = t * a.hk + sb + (l < n ? l : n - 1);
+      const int ev = a.idx[pl];
+      const float gv = a.gates[pl];
+      int s0 = sb;
+      for (; s0 + G <= sb + n; s0 += G)
+        token_slots<G, CPL, BF16>(a, t, s0, sb, ev, gv, xr, dyr, cv, acc);
+      for (; s0 < sb + n; ++s0) token_slots<1, CPL, BF16>(a, t, s0, sb, ev, gv, xr, dyr, cv, acc);
     }
 #pragma unroll
     for (int q = 0; q < CPL; ++q) {
@@ -149,15 +177,66 @@ __global__ __launch_bounds__(256) void bwd_token_kernel(BwdArgs a) {
   }
 }
 
-template <int CPL, bool BF16>
+// Tasks j0 .. j0 + GG - 1 of the lanes' batch (slot pl, a_p apl, dh_p dhl on lane j): all their
+// token and dy rows are loaded, then du += dh_p x_t and dv += a_p dy_t in task order.
+template <int GG, int CPL, bool BF16>
+__device__ __forceinline__ void task_group(const BwdArgs& a, const uint4* X, int64_t rc,
+                                           const bool (&cv)[CPL], int pl, float apl, float dhl,
+                                           int j0, float (&du)[CPL][BF16 ? 8 : 4],
+                                           float (&dv)[CPL][BF16 ? 8 : 4]) {
+  constexpr int EPC = BF16 ? 8 : 4;
+  const int l = lane_id();
+  uint4 xr[GG][CPL];
+  float4 yr[GG][CPL][EPC / 4];
+#pragma unroll
+  for (int i = 0; i < GG; ++i) {
+    const int64_t t = readlane_i32(pl, j0 + i) / a.hk;
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      const int c = l + kWave * q;
+      xr[i][q] = cv[q] ? X[t * rc + c] : make_uint4(0, 0, 0, 0);
+      const float4* dyc = (const float4*)(a.dy + t * a.d + (int64_t)c * EPC);
+#pragma unroll
+      for (int k = 0; k < EPC / 4; ++k) yr[i][q][k] = cv[q] ? dyc[k] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  }
+  // every load above is issued before the first product (left alone, the scheduler interleaves
+  // them with the products and waits for each row in turn)
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int i = 0; i < GG; ++i) {
+    const float ap = readlane_f32(apl, j0 + i), dhp = readlane_f32(dhl, j0 + i);
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+#pragma unroll
+      for (int k = 0; k < EPC; k += 4) {
+        const float4 yv = yr[i][q][k / 4];
+        dv[q][k] = fmaf(ap, yv.x, dv[q][k]);
+        dv[q][k + 1] = fmaf(ap, yv.y, dv[q][k + 1]);
+        dv[q][k + 2] = fmaf(ap, yv.z, dv[q][k + 2]);
+        dv[q][k + 3] = fmaf(ap, yv.w, dv[q][k + 3]);
+      }
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) du[q][k] = fmaf(dhp, chunk_elem<BF16>(xr[i][q], k), du[q][k]);
+    }
+  }
+}
+
+// Expert pass. The segment's tasks are taken 64 at a time: lane j loads the j-th one's slot,
+// a and dh (one round trip for all of them), and the tasks then go through in order, G at a time
+// with all of their token and dy rows in flight before the first product (the sums keep task
+// order, so du and dv are the same as with one task at a time). FULL: the row is exactly CPL * 64
+// chunks and no load carries a guard (guarded loads made the compiler wait for each chunk).
+template <int CPL, bool BF16, bool FULL>
 __global__ __launch_bounds__(256) void bwd_expert_kernel(BwdArgs a) {
   constexpr int EPC = BF16 ? 8 : 4;
+  constexpr int G = CPL >= 8 ? 1 : 2;
   const int l = lane_id();
   const uint4* X = (const uint4*)a.x;
   const int64_t rc = a.nchunks;
   bool cv[CPL];
 #pragma unroll
-  for (int q = 0; q < CPL; ++q) cv[q] = (l + kWave * q) < a.nchunks;
+  for (int q = 0; q < CPL; ++q) cv[q] = FULL || (l + kWave * q) < a.nchunks;
   const int64_t na = *a.n_active < a.cap ? *a.n_active : a.cap;
   const int64_t stride = (int64_t)gridDim.x * 4;
   for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < na; r += stride) {
@@ -169,27 +248,15 @@ __global__ __launch_bounds__(256) void bwd_expert_kernel(BwdArgs a) {
     int64_t b = a.offsets[r], e = a.offsets[r + 1];
     b = b < 0 ? 0 : (b > a.M ? a.M : b);
     e = e < b ? b : (e > a.M ? a.M : e);
-    for (int64_t tau = b; tau < e; ++tau) {
-      const int p = clamp_id(a.perm[tau], a.M);
-      const int64_t t = p / a.hk;
-      const float ap = a.a[p], dhp = a.dh[p];
-#pragma unroll
-      for (int q = 0; q < CPL; ++q) {
-        if (!cv[q]) continue;
-        const int c = l + kWave * q;
-        const uint4 xc = X[t * rc + c];
-        const float4* dyc = (const float4*)(a.dy + t * a.d + (int64_t)c * EPC);
-#pragma unroll
-        for (int k = 0; k < EPC; k += 4) {
-          const float4 yv = dyc[k / 4];
-          dv[q][k] = fmaf(ap, yv.x, dv[q][k]);
-          dv[q][k + 1] = fmaf(ap, yv.y, dv[q][k + 1]);
-          dv[q][k + 2] = fmaf(ap, yv.z, dv[q][k + 2]);
-          dv[q][k + 3] = fmaf(ap, yv.w, dv[q][k + 3]);
-        }
-#pragma unroll
-        for (int k = 0; k < EPC; ++k) du[q][k] = fmaf(dhp, chunk_elem<BF16>(xc, k), du[q][k]);
-      }
+    for (int64_t base = b; base < e; base += kWave) {
+      const int n = (int)(e - base < kWave ? e - base : kWave);
+      const int pl = clamp_id(a.perm[base + (l < n ? l : n - 1)], a.M);
+      const float apl = a.a[pl], dhl = a.dh[pl];
+      // whole groups of G tasks, then the remaining ones singly: every product of a group is
+      // unconditional, so the compiler cannot move a task's loads behind the previous task's work
+      int j0 = 0;
+      for (; j0 + G <= n; j0 += G) task_group<G, CPL, BF16>(a, X, rc, cv, pl, apl, dhl, j0, du, dv);
+      for (; j0 < n; ++j0) task_group<1, CPL, BF16>(a, X, rc, cv, pl, apl, dhl, j0, du, dv);
     }
 #pragma unroll
     for (int q = 0; q < CPL; ++q) {
@@ -407,10 +474,18 @@ hipError_t dispatch_bwd(int cpl, int64_t t_blocks, int64_t e_blocks, hipStream_t
                         const BwdArgs& a) {
 #define OMNIMOE_BWD(C)                                                                    \
   case C:                                                                                 \
-    hipLaunchKernelGGL((bwd_token_kernel<C, BF16>), dim3((unsigned)t_blocks), dim3(256), 0,  \
-                       st, a);                                                            \
-    hipLaunchKernelGGL((bwd_expert_kernel<C, BF16>), dim3((unsigned)e_blocks), dim3(256), 0, \
-                       st, a);                                                            \
+    if (a.nchunks == C * kWave)                                                           \
+      hipLaunchKernelGGL((bwd_token_kernel<C, BF16, true>), dim3((unsigned)t_blocks),       \
+                         dim3(256), 0, st, a);                                            \
+    else                                                                                  \
+      hipLaunchKernelGGL((bwd_token_kernel<C, BF16, false>), dim3((unsigned)t_blocks),      \
+                         dim3(256), 0, st, a);                                            \
+    if (a.nchunks == C * kWave)                                                           \
+      hipLaunchKernelGGL((bwd_expert_kernel<C, BF16, true>), dim3((unsigned)e_blocks),      \
+                         dim3(256), 0, st, a);                                            \
+    else                                                                                  \
+      hipLaunchKernelGGL((bwd_expert_kernel<C, BF16, false>), dim3((unsigned)e_blocks),     \
+                         dim3(256), 0, st, a);                                            \
     break;
   switch (cpl) {
     OMNIMOE_BWD(1)
