@@ -69,6 +69,15 @@ SHAPES = {
                                    H=2, K=64, dtype="f32"),
     "decode8_bf16": synth.Workload("decode8_bf16", T=8, d=2048, n_rows=100, n_cols=36,
                                    d_key=1024, H=2, K=9),
+    # the selection kernel forming the slot-order dot (256 or more (token, head) rows, a square
+    # grid of 256 or 512): one pick per row; three (a partial group of four); 64 (the wave's
+    # width) with d = 1024
+    "fused_k1_bf16": synth.Workload("fused_k1_bf16", T=64, d=512, n_rows=256, n_cols=256,
+                                    d_key=256, H=4, K=1),
+    "fused_k3_bf16": synth.Workload("fused_k3_bf16", T=100, d=512, n_rows=256, n_cols=256,
+                                    d_key=128, H=3, K=3, act="silu"),
+    "fused_k64_bf16": synth.Workload("fused_k64_bf16", T=32, d=1024, n_rows=512, n_cols=512,
+                                     d_key=512, H=8, K=64),
     "decode_dk768_bf16": synth.Workload("decode_dk768_bf16", T=20, d=1536, n_rows=70, n_cols=64,
                                         d_key=768, H=2, K=5),
     # K > 64 (workgroup-per-row selection), incl. the paper's benchmark grid 320 x 320, K = 512
@@ -659,6 +668,27 @@ def test_layer_forward(name):
     same = np.all(idx == idx_orc, axis=(1, 2))
     assert same.mean() > 0.5
     assert row_rel_err(y, y_orc)[same].max() <= tol(w)
+
+
+@pytest.mark.parametrize("name", ["fused_k1_bf16", "fused_k3_bf16", "fused_k64_bf16",
+                                  "small_bf16"])
+def test_fused_selection_dot_matches_expert_stage(name):
+    # Where the selection kernel forms the slot-order a_p (omnimoe_layer_path), the layer's y must
+    # equal, bit for bit, the expert stage launched on its own (omnimoe_expert_forward, the
+    # expert-major dot) on the layer's own routing: both form every a_p the same way.
+    w = SHAPES[name]
+    d = B.make_desc(w)
+    assert P.omnimoe_layer_path(d) & B.PATH_SELECT_DOT
+    say(f"[fused selection + dot] {name}")
+    inp, _ = host_inputs(w)
+    dev = upload(inp)
+    y, idx, g = gpu_layer(w, dev)
+    perm, _, _, _ = oracle.schedule(oracle.desc(w), idx)
+    y2 = torch.empty((w.T, w.d), dtype=torch.float32, device="cuda")
+    P.omnimoe_expert_forward(d, dev["x"], dev["u"], dev["v"], to_dev(idx), to_dev(g),
+                             to_dev(perm), y2)
+    torch.cuda.synchronize()
+    assert np.array_equal(y.view(np.uint8), y2.cpu().numpy().view(np.uint8))
 
 
 def test_layer_is_deterministic():
