@@ -316,17 +316,48 @@ struct KeySumArgs {
   int nchunks;       // 16-byte chunks of a d_key slice
 };
 
+// Tasks j0 .. j0 + GG - 1 of a keysum batch (slot pl, weight wl on lane j): their x slices are
+// loaded together, then acc += ds_p x_t in task order.
+template <int GG, int CPL, bool BF16>
+__device__ __forceinline__ void keysum_group(const KeySumArgs& a, const uint4* X, int64_t xrc,
+                                             int64_t c0, const bool (&cv)[CPL], int pl, float wl,
+                                             int j0, float (&acc)[CPL][BF16 ? 8 : 4]) {
+  constexpr int EPC = BF16 ? 8 : 4;
+  const int l = lane_id();
+  uint4 xr[GG][CPL];
+#pragma unroll
+  for (int i = 0; i < GG; ++i) {
+    const int64_t t = readlane_i32(pl, j0 + i) / a.hk;
+#pragma unroll
+    for (int q = 0; q < CPL; ++q)
+      xr[i][q] = cv[q] ? X[t * xrc + c0 + l + kWave * q] : make_uint4(0, 0, 0, 0);
+  }
+  __builtin_amdgcn_sched_barrier(0);  // all of the group's loads before its first product
+#pragma unroll
+  for (int i = 0; i < GG; ++i) {
+    const float w = readlane_f32(wl, j0 + i);
+#pragma unroll
+    for (int q = 0; q < CPL; ++q)
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) acc[q][k] = fmaf(w, chunk_elem<BF16>(xr[i][q], k), acc[q][k]);
+  }
+}
+
 // One wavefront per selected sub-key: dk[key] = sum over its tasks (task order) of ds_p x_t.
-template <int CPL, bool BF16>
+// The segment's tasks are taken 64 at a time (slot and ds with one load per lane), then eight
+// (or, with wide rows, fewer) at a time with their x slices in flight together; whole groups
+// first and the rest singly, so that every product of a group is unconditional.
+template <int CPL, bool BF16, bool FULL>
 __global__ __launch_bounds__(256) void keysum_kernel(KeySumArgs a) {
   constexpr int EPC = BF16 ? 8 : 4;
+  constexpr int G = CPL >= 8 ? 2 : (CPL >= 4 ? 4 : 8);
   const int l = lane_id();
   const int64_t xrc = a.d / EPC;   // chunks per x row
   const int64_t c0 = a.c0 / EPC;
   const uint4* X = (const uint4*)a.x;
   bool cv[CPL];
 #pragma unroll
-  for (int q = 0; q < CPL; ++q) cv[q] = (l + kWave * q) < a.nchunks;
+  for (int q = 0; q < CPL; ++q) cv[q] = FULL || (l + kWave * q) < a.nchunks;
   const int64_t na = *a.n_active < a.cap ? *a.n_active : a.cap;
   const int64_t stride = (int64_t)gridDim.x * 4;
   for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < na; r += stride) {
@@ -338,17 +369,13 @@ __global__ __launch_bounds__(256) void keysum_kernel(KeySumArgs a) {
     int64_t b = a.offsets[r], e = a.offsets[r + 1];
     b = b < 0 ? 0 : (b > a.M ? a.M : b);
     e = e < b ? b : (e > a.M ? a.M : e);
-    for (int64_t tau = b; tau < e; ++tau) {
-      const int p = clamp_id(a.perm[tau], a.M);
-      const int64_t t = p / a.hk;
-      const float w = a.ds[p];
-#pragma unroll
-      for (int q = 0; q < CPL; ++q) {
-        if (!cv[q]) continue;
-        const uint4 xc = X[t * xrc + c0 + l + kWave * q];
-#pragma unroll
-        for (int k = 0; k < EPC; ++k) acc[q][k] = fmaf(w, chunk_elem<BF16>(xc, k), acc[q][k]);
-      }
+    for (int64_t base = b; base < e; base += kWave) {
+      const int n = (int)(e - base < kWave ? e - base : kWave);
+      const int pl = clamp_id(a.perm[base + (l < n ? l : n - 1)], a.M);
+      const float wl = a.ds[pl];
+      int j0 = 0;
+      for (; j0 + G <= n; j0 += G) keysum_group<G, CPL, BF16>(a, X, xrc, c0, cv, pl, wl, j0, acc);
+      for (; j0 < n; ++j0) keysum_group<1, CPL, BF16>(a, X, xrc, c0, cv, pl, wl, j0, acc);
     }
     const int key = clamp_id(a.active[r], a.n_keys);
 #pragma unroll
@@ -378,18 +405,58 @@ struct RouteDxArgs {
   int nchunks;   // 16-byte chunks of a d_key row
 };
 
-// dx_t[0 : d_key] += sum of ds_p keys_row[h, i_p]; dx_t[c0 : c0 + d_key] += sum of ds_p
-// keys_col[h, j_p]; one wavefront per token, slots in order.
-template <int CPL, bool BF16>
-__global__ __launch_bounds__(256) void route_dx_kernel(RouteDxArgs a) {
+// Slots s0 .. s0 + GG - 1 of token t (expert on lane s - sb of ev, weight of wv): both sub-key
+// rows of each are loaded together, then ar += ds_p keys_row[h, i_p] and ac += ds_p
+// keys_col[h, j_p] in slot order.
+template <int GG, int CPL, bool BF16>
+__device__ __forceinline__ void route_dx_group(const RouteDxArgs& a, const bool (&cv)[CPL], int s0,
+                                               int sb, int ev, float wv,
+                                               float (&ar)[CPL][BF16 ? 8 : 4],
+                                               float (&ac)[CPL][BF16 ? 8 : 4]) {
   constexpr int EPC = BF16 ? 8 : 4;
   const int l = lane_id();
   const uint4* KR = (const uint4*)a.kr;
   const uint4* KC = (const uint4*)a.kc;
   const int64_t rc = a.nchunks;
+  uint4 rr[GG][CPL], cr[GG][CPL];
+#pragma unroll
+  for (int i = 0; i < GG; ++i) {
+    const int s = s0 + i;
+    const int e = clamp_id(readlane_i32(ev, s - sb), a.N);
+    const int h = s / a.K;
+    const int64_t ri = (int64_t)h * a.nr + e / a.nc;
+    const int64_t cj = (int64_t)h * a.nc + e % a.nc;
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) {
+      rr[i][q] = cv[q] ? KR[ri * rc + l + kWave * q] : make_uint4(0, 0, 0, 0);
+      cr[i][q] = cv[q] ? KC[cj * rc + l + kWave * q] : make_uint4(0, 0, 0, 0);
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);  // all of the group's loads before its first product
+#pragma unroll
+  for (int i = 0; i < GG; ++i) {
+    const float w = readlane_f32(wv, s0 + i - sb);
+#pragma unroll
+    for (int q = 0; q < CPL; ++q)
+#pragma unroll
+      for (int k = 0; k < EPC; ++k) {
+        ar[q][k] = fmaf(w, chunk_elem<BF16>(rr[i][q], k), ar[q][k]);
+        ac[q][k] = fmaf(w, chunk_elem<BF16>(cr[i][q], k), ac[q][k]);
+      }
+  }
+}
+
+// dx_t[0 : d_key] += sum of ds_p keys_row[h, i_p]; dx_t[c0 : c0 + d_key] += sum of ds_p
+// keys_col[h, j_p]; one wavefront per token, slots in order: experts and weights read 64 slots
+// at a time, then groups of slots with all of their sub-key rows in flight.
+template <int CPL, bool BF16, bool FULL>
+__global__ __launch_bounds__(256) void route_dx_kernel(RouteDxArgs a) {
+  constexpr int EPC = BF16 ? 8 : 4;
+  constexpr int G = CPL >= 8 ? 1 : (CPL >= 4 ? 2 : 4);
+  const int l = lane_id();
   bool cv[CPL];
 #pragma unroll
-  for (int q = 0; q < CPL; ++q) cv[q] = (l + kWave * q) < a.nchunks;
+  for (int q = 0; q < CPL; ++q) cv[q] = FULL || (l + kWave * q) < a.nchunks;
   const int64_t stride = (int64_t)gridDim.x * 4;
   for (int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < a.T; t += stride) {
     float ar[CPL][EPC], ac[CPL][EPC];
@@ -397,24 +464,14 @@ __global__ __launch_bounds__(256) void route_dx_kernel(RouteDxArgs a) {
     for (int q = 0; q < CPL; ++q)
 #pragma unroll
       for (int k = 0; k < EPC; ++k) ar[q][k] = ac[q][k] = 0.0f;
-    for (int s = 0; s < a.hk; ++s) {
-      const int64_t p = t * a.hk + s;
-      const int e = clamp_id(a.idx[p], a.N);
-      const int h = s / a.K;
-      const float w = a.ds[p];
-      const int64_t ri = (int64_t)h * a.nr + e / a.nc;
-      const int64_t cj = (int64_t)h * a.nc + e % a.nc;
-#pragma unroll
-      for (int q = 0; q < CPL; ++q) {
-        if (!cv[q]) continue;
-        const uint4 r = KR[ri * rc + l + kWave * q];
-        const uint4 c = KC[cj * rc + l + kWave * q];
-#pragma unroll
-        for (int k = 0; k < EPC; ++k) {
-          ar[q][k] = fmaf(w, chunk_elem<BF16>(r, k), ar[q][k]);
-          ac[q][k] = fmaf(w, chunk_elem<BF16>(c, k), ac[q][k]);
-        }
-      }
+    for (int sb = 0; sb < a.hk; sb += kWave) {
+      const int n = a.hk - sb < kWave ? a.hk - sb : kWave;
+      const int64_t pl = t * a.hk + sb + (l < n ? l : n - 1);
+      const int ev = a.idx[pl];
+      const float wv = a.ds[pl];
+      int s0 = sb;
+      for (; s0 + G <= sb + n; s0 += G) route_dx_group<G, CPL, BF16>(a, cv, s0, sb, ev, wv, ar, ac);
+      for (; s0 < sb + n; ++s0) route_dx_group<1, CPL, BF16>(a, cv, s0, sb, ev, wv, ar, ac);
     }
 #pragma unroll
     for (int q = 0; q < CPL; ++q) {
@@ -442,11 +499,21 @@ void launch_router_bwd_kernels(const KeySumArgs& kr, const KeySumArgs& kc, const
     const KeySumArgs& a = pass == 0 ? kr : kc;
     int64_t blocks = (a.cap + 3) / 4;
     if (blocks > 65536) blocks = 65536;
-    hipLaunchKernelGGL((keysum_kernel<CPL, BF16>), dim3((unsigned)blocks), dim3(256), 0, st, a);
+    if (a.nchunks == CPL * kWave)
+      hipLaunchKernelGGL((keysum_kernel<CPL, BF16, true>), dim3((unsigned)blocks), dim3(256), 0,
+                         st, a);
+    else
+      hipLaunchKernelGGL((keysum_kernel<CPL, BF16, false>), dim3((unsigned)blocks), dim3(256), 0,
+                         st, a);
   } else {
     int64_t blocks = (rd.T + 3) / 4;
     if (blocks > 16384) blocks = 16384;
-    hipLaunchKernelGGL((route_dx_kernel<CPL, BF16>), dim3((unsigned)blocks), dim3(256), 0, st, rd);
+    if (rd.nchunks == CPL * kWave)
+      hipLaunchKernelGGL((route_dx_kernel<CPL, BF16, true>), dim3((unsigned)blocks), dim3(256), 0,
+                         st, rd);
+    else
+      hipLaunchKernelGGL((route_dx_kernel<CPL, BF16, false>), dim3((unsigned)blocks), dim3(256),
+                         0, st, rd);
   }
 }
 
