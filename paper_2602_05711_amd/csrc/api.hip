@@ -100,6 +100,9 @@ bool layer_grouped(const Shape& s) { return s.B > 1 && grouped_supported(s); }
 // dot itself; with fewer, a wave per row would fetch its K u rows four at a time, while the
 // separate dot kernel fetches all of them at once (one decoded token: 19.1 against 22.1 us).
 constexpr int64_t kSelectDotMinRows = 256;
+// Up to this many tasks the sort by expert is one launch, as cheap as the flag pass and scan
+// that replace it above (launch_group_schedule).
+constexpr int64_t kSortFreeMinTasks = 8192;
 int32_t layer_path(const Shape& s) {
   const bool grouped = layer_grouped(s);
   const bool unscheduled = !grouped && omnimoe::slot_dot(s);
@@ -229,9 +232,17 @@ omnimoe_status layer_impl(const omnimoe_layer_desc* desc, const void* x, const v
   mark(2);
   const int32_t* sk = nullptr;
   const int32_t* gk = nullptr;
-  if (!unscheduled && (e = omnimoe::launch_schedule(s, idx, perm, active, offsets, n_active,
-                                                    nullptr, sched_ws, &sk, strm, &gk)))
-    return hip_status(e);
+  if (!unscheduled) {
+    // The grouped product needs the active list and the (group, task id) order but no
+    // per-expert offsets, so past the single-launch sizes it skips the sort by expert.
+    if ((path & OMNIMOE_PATH_GROUPED) && s.M > kSortFreeMinTasks &&
+        omnimoe::group_schedule_fits(s))
+      e = omnimoe::launch_group_schedule(s, idx, perm, active, n_active, sched_ws, &gk, strm);
+    else
+      e = omnimoe::launch_schedule(s, idx, perm, active, offsets, n_active, nullptr, sched_ws,
+                                   &sk, strm, &gk);
+    if (e) return hip_status(e);
+  }
   mark(3);
   if (unscheduled) {
     if (!fused && (e = omnimoe::launch_slot_dot(s, x, u, idx, gates, abuf, strm)))

@@ -78,6 +78,13 @@ hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, in
                            int32_t* active_offsets, int32_t* n_active, int32_t* dense_offsets,
                            void* ws, const int32_t** sorted_keys, hipStream_t st,
                            const int32_t** group_keys = nullptr);
+// For the layer with groups of B > 1 experts: perm in (group, task id) order, active and
+// n_active as launch_schedule gives them, *group_keys the sorted packed keys; no per-expert
+// offsets. Same workspace as launch_schedule. Needs group_schedule_fits(s) (N <= 262144).
+bool group_schedule_fits(const Shape& s);
+hipError_t launch_group_schedule(const Shape& s, const int32_t* idx, int32_t* perm,
+                                 int32_t* active, int32_t* n_active, void* ws,
+                                 const int32_t** group_keys, hipStream_t st);
 
 // a[p] = g_p * act(x_t . u_e) over the expert-major order given by perm (sorted_keys may be
 // NULL: the kernel then reads idx[perm[pos]]).

@@ -151,12 +151,27 @@ struct EmitSegments {
 // Second step of the scan: each block first adds up the chunk totals of the blocks before it
 // (at most a few hundred values), so no separate pass over the totals is needed. The last
 // block hands the grand total to emit.finish.
+// This thread's share of partial[0 .. nb): four loads in flight per round (clamped addresses,
+// masked values) rather than one load and wait per value.
+__device__ __forceinline__ int partial_prefix(const int32_t* partial, int nb) {
+  int pre = 0;
+  for (int i0 = 0; i0 < nb; i0 += 4 * kThreads) {
+    int a[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * kThreads + (int)threadIdx.x;
+      a[u] = partial[i < nb ? i : nb - 1];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) pre += i0 + u * kThreads + (int)threadIdx.x < nb ? a[u] : 0;
+  }
+  return pre;
+}
+
 template <class F, class E>
 __global__ __launch_bounds__(kThreads) void scan_down_kernel(F f, E emit, const int32_t* partial) {
-  int pre = 0;
-  for (int i = threadIdx.x; i < (int)blockIdx.x; i += kThreads) pre += partial[i];
   int before;
-  block_excl_scan(pre, &before);
+  block_excl_scan(partial_prefix(partial, (int)blockIdx.x), &before);
   const int64_t base = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kItems;
   int v[kItems];
   eval_items(f, base, v);
@@ -362,37 +377,6 @@ __global__ __launch_bounds__(kThreads) void rank_fill_kernel(const int32_t* acti
   if (e >= 0 && e < n_experts) rank[e] = (int32_t)a;
 }
 
-// Group key of every task, with the expert's place inside its group packed above it:
-// key[p] = (r % B) << gb | r / B for r = rank[idx[p]]. The sort reads only the low gb bits,
-// so the place rides along to the sorted order.
-__global__ __launch_bounds__(kThreads) void group_key_kernel(const int32_t* idx,
-                                                            const int32_t* rank, int32_t* key,
-                                                            int64_t m, int64_t n_experts, int b,
-                                                            int gb) {
-  const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (p >= m) return;
-  int32_t e = idx[p];
-  e = e < 0 ? 0 : (e >= n_experts ? (int32_t)(n_experts - 1) : e);
-  const int32_t r = rank[e];
-  key[p] = ((r % b) << gb) | (r / b);
-}
-
-// The same key for each sorted position of a caller's schedule: key[i] of task perm[i].
-__global__ __launch_bounds__(kThreads) void position_key_kernel(const int32_t* perm,
-                                                               const int32_t* idx,
-                                                               const int32_t* rank, int32_t* key,
-                                                               int64_t m, int64_t n_experts,
-                                                               int b, int gb) {
-  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (i >= m) return;
-  int32_t p = perm[i];
-  p = p < 0 ? 0 : (p >= m ? (int32_t)(m - 1) : p);
-  int32_t e = idx[p];
-  e = e < 0 ? 0 : (e >= n_experts ? (int32_t)(n_experts - 1) : e);
-  const int32_t r = rank[e];
-  key[i] = ((r % b) << gb) | (r / b);
-}
-
 // ------------------------------------------------------------------ grouped-GEMM plan
 // For a schedule with groups of B > 1 experts (tasks in (group, task id) order), a slot is a
 // (group, token) pair: the tasks of one token inside one group, contiguous in perm since a
@@ -417,6 +401,207 @@ DivMagic div_magic(uint32_t d) {
 }
 __device__ __forceinline__ uint32_t div_by(uint32_t n, DivMagic g) {
   return (__umulhi(g.m, n) + n) >> g.l;
+}
+
+// Group key of a task of expert e: the expert's rank r in the active list split as
+// (r % B) << gb | r / B. The sort reads only the low gb bits, so the expert's place inside its
+// group rides along to the sorted order.
+__device__ __forceinline__ int32_t group_key_of(int32_t e, const int32_t* rank, int64_t n_experts,
+                                                int b, DivMagic bm, int gb) {
+  e = e < 0 ? 0 : (e >= n_experts ? (int32_t)(n_experts - 1) : e);
+  const uint32_t r = (uint32_t)rank[e];
+  const uint32_t q = div_by(r, bm);
+  return (int32_t)(((r - q * (uint32_t)b) << gb) | q);
+}
+
+constexpr int kKeyItems = 8;  // tasks per thread of the key kernels
+unsigned key_blocks(int64_t m) {
+  const int64_t per = (int64_t)kThreads * kKeyItems;
+  return (unsigned)((m + per - 1) / per);
+}
+
+// key[p] = group_key_of(idx[p]) for every task, kKeyItems consecutive tasks per thread: the ids
+// with 16-byte loads, then all their rank reads in flight at once (one task per thread would
+// leave each wave waiting on one HBM load and one dependent L2 load at a time). idx and key are
+// 16-byte aligned.
+__global__ __launch_bounds__(kThreads) void group_key_kernel(const int32_t* __restrict__ idx,
+                                                            const int32_t* __restrict__ rank,
+                                                            int32_t* __restrict__ key, int64_t m,
+                                                            int64_t n_experts, int b, DivMagic bm,
+                                                            int gb) {
+  const int64_t p0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * kKeyItems;
+  if (p0 >= m) return;
+  if (p0 + kKeyItems <= m) {
+    const int4 a = *(const int4*)(idx + p0);
+    const int4 c = *(const int4*)(idx + p0 + 4);
+    int4 ka, kc;
+    ka.x = group_key_of(a.x, rank, n_experts, b, bm, gb);
+    ka.y = group_key_of(a.y, rank, n_experts, b, bm, gb);
+    ka.z = group_key_of(a.z, rank, n_experts, b, bm, gb);
+    ka.w = group_key_of(a.w, rank, n_experts, b, bm, gb);
+    kc.x = group_key_of(c.x, rank, n_experts, b, bm, gb);
+    kc.y = group_key_of(c.y, rank, n_experts, b, bm, gb);
+    kc.z = group_key_of(c.z, rank, n_experts, b, bm, gb);
+    kc.w = group_key_of(c.w, rank, n_experts, b, bm, gb);
+    *(int4*)(key + p0) = ka;
+    *(int4*)(key + p0 + 4) = kc;
+    return;
+  }
+  for (int64_t p = p0; p < m; ++p) key[p] = group_key_of(idx[p], rank, n_experts, b, bm, gb);
+}
+
+// The same key for each sorted position of a caller's schedule: key[i] of task perm[i],
+// kKeyItems positions per thread (perm with 16-byte loads, the idx and rank reads batched).
+__global__ __launch_bounds__(kThreads) void position_key_kernel(const int32_t* __restrict__ perm,
+                                                               const int32_t* __restrict__ idx,
+                                                               const int32_t* __restrict__ rank,
+                                                               int32_t* __restrict__ key,
+                                                               int64_t m, int64_t n_experts,
+                                                               int b, DivMagic bm, int gb) {
+  const int64_t i0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * kKeyItems;
+  if (i0 >= m) return;
+  if (i0 + kKeyItems <= m) {
+    const int4 pa = *(const int4*)(perm + i0);
+    const int4 pc = *(const int4*)(perm + i0 + 4);
+    const int32_t pp[kKeyItems] = {pa.x, pa.y, pa.z, pa.w, pc.x, pc.y, pc.z, pc.w};
+    int32_t e[kKeyItems];
+#pragma unroll
+    for (int j = 0; j < kKeyItems; ++j) e[j] = idx[clamp_task(pp[j], m)];
+    int4 ka, kc;
+    ka.x = group_key_of(e[0], rank, n_experts, b, bm, gb);
+    ka.y = group_key_of(e[1], rank, n_experts, b, bm, gb);
+    ka.z = group_key_of(e[2], rank, n_experts, b, bm, gb);
+    ka.w = group_key_of(e[3], rank, n_experts, b, bm, gb);
+    kc.x = group_key_of(e[4], rank, n_experts, b, bm, gb);
+    kc.y = group_key_of(e[5], rank, n_experts, b, bm, gb);
+    kc.z = group_key_of(e[6], rank, n_experts, b, bm, gb);
+    kc.w = group_key_of(e[7], rank, n_experts, b, bm, gb);
+    *(int4*)(key + i0) = ka;
+    *(int4*)(key + i0 + 4) = kc;
+    return;
+  }
+  for (int64_t i = i0; i < m; ++i)
+    key[i] = group_key_of(idx[clamp_task(perm[i], m)], rank, n_experts, b, bm, gb);
+}
+
+// ------------------------------------------------------------------ active experts by bitmap
+// For the grouped layer the active list and each expert's rank in it come from a bitmap of the
+// experts that have tasks, bit e of word e / 32, instead of a sort by expert. With the bitmap
+// and its per-word prefix popcounts in LDS a task's group key needs no global gather:
+// rank(e) = prefix[e / 32] + popcount(bits[e / 32] below bit e % 32).
+
+constexpr int kMapWords = 8192;     // largest bitmap kept in LDS with its prefix: 262144 experts
+constexpr int kMapThreads = 1024;
+constexpr int kMapChunk = kMapThreads * 16;  // tasks per workgroup round, 16 per thread
+
+__device__ __forceinline__ uint32_t clamp_expert(int32_t e, int64_t n_experts) {
+  return (uint32_t)(e < 0 ? 0 : (e >= n_experts ? (int32_t)(n_experts - 1) : e));
+}
+
+// Sets the bit of the expert of every task (ids clamped into [0, n_experts), as the key kernels
+// clamp them). Each workgroup sets the bits of its rounds of tasks in an LDS copy, then ORs the
+// copy's nonzero words into bits: one global atomic per word and workgroup instead of a
+// scattered store per task. bits holds `words` zeroed words.
+__global__ __launch_bounds__(kMapThreads) void mark_experts_kernel(const int32_t* __restrict__ idx,
+                                                                  uint32_t* bits, int64_t m,
+                                                                  int64_t n_experts, int words) {
+  extern __shared__ uint32_t sb[];
+  for (int w = threadIdx.x; w < words; w += kMapThreads) sb[w] = 0;
+  __syncthreads();
+  auto set = [&](int32_t e) {
+    const uint32_t c = clamp_expert(e, n_experts);
+    atomicOr(&sb[c >> 5], 1u << (c & 31u));
+  };
+  for (int64_t c0 = (int64_t)blockIdx.x * kMapChunk; c0 < m; c0 += (int64_t)gridDim.x * kMapChunk) {
+    if (c0 + kMapChunk <= m) {
+      int4 a[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        a[q] = *(const int4*)(idx + c0 + q * (kMapThreads * 4) + threadIdx.x * 4);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        set(a[q].x); set(a[q].y); set(a[q].z); set(a[q].w);
+      }
+    } else {
+      for (int64_t p = c0 + threadIdx.x; p < m; p += kMapThreads) set(idx[p]);
+    }
+  }
+  __syncthreads();
+  for (int w = threadIdx.x; w < words; w += kMapThreads)
+    if (sb[w]) atomicOr(&bits[w], sb[w]);
+}
+
+struct PopWord {  // number of active experts in bitmap word i
+  const uint32_t* bits;
+  int64_t n;
+  __device__ int operator()(int64_t i) const { return i < n ? __popc(bits[i]) : 0; }
+};
+
+// Stores each word's exclusive prefix popcount; closes the active list with n_active.
+struct EmitPrefix {
+  int32_t* prefix;
+  int32_t* n_active;
+  int64_t n;
+  int32_t cap;
+  __device__ void operator()(int64_t i, int val, int pos) const {
+    (void)val;
+    if (i < n) prefix[i] = pos;
+  }
+  __device__ void finish(int total) const { *n_active = total < cap ? total : cap; }
+};
+
+// active[rank(e)] = e for every marked expert e, one thread per expert.
+__global__ __launch_bounds__(kThreads) void list_active_kernel(const uint32_t* __restrict__ bits,
+                                                              const int32_t* __restrict__ prefix,
+                                                              int32_t* __restrict__ active,
+                                                              int64_t n_experts, int32_t cap) {
+  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (e >= n_experts) return;
+  const uint32_t word = bits[e >> 5];
+  const uint32_t bit = (uint32_t)e & 31u;
+  if (!((word >> bit) & 1u)) return;
+  const int32_t r = prefix[e >> 5] + __popc(word & ((1u << bit) - 1u));
+  if (r < cap) active[r] = (int32_t)e;
+}
+
+// group_key_of for every task with the rank taken from the LDS bitmap and prefix (dynamic LDS of
+// 2 * words words); kMapChunk tasks per workgroup round, idx and key 16-byte aligned.
+__global__ __launch_bounds__(kMapThreads) void group_key_map_kernel(
+    const int32_t* __restrict__ idx, const uint32_t* __restrict__ bits,
+    const int32_t* __restrict__ prefix, int32_t* __restrict__ key, int64_t m, int64_t n_experts,
+    int words, int b, DivMagic bm, int gb) {
+  extern __shared__ uint32_t sm[];
+  uint32_t* sb = sm;
+  int32_t* sp = (int32_t*)(sm + words);
+  for (int w = threadIdx.x; w < words; w += kMapThreads) {
+    sb[w] = bits[w];
+    sp[w] = prefix[w];
+  }
+  __syncthreads();
+  auto key_of = [&](int32_t e) {
+    const uint32_t c = clamp_expert(e, n_experts);
+    const uint32_t w = c >> 5;
+    const uint32_t r =
+        (uint32_t)sp[w] + (uint32_t)__popc(sb[w] & ((1u << (c & 31u)) - 1u));
+    const uint32_t q = div_by(r, bm);
+    return (int32_t)(((r - q * (uint32_t)b) << gb) | q);
+  };
+  for (int64_t c0 = (int64_t)blockIdx.x * kMapChunk; c0 < m; c0 += (int64_t)gridDim.x * kMapChunk) {
+    if (c0 + kMapChunk <= m) {
+      int4 a[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        a[q] = *(const int4*)(idx + c0 + q * (kMapThreads * 4) + threadIdx.x * 4);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        int4 k;
+        k.x = key_of(a[q].x); k.y = key_of(a[q].y); k.z = key_of(a[q].z); k.w = key_of(a[q].w);
+        *(int4*)(key + c0 + q * (kMapThreads * 4) + threadIdx.x * 4) = k;
+      }
+    } else {
+      for (int64_t p = c0 + threadIdx.x; p < m; p += kMapThreads) key[p] = key_of(idx[p]);
+    }
+  }
 }
 
 struct SlotHead {  // 1 where sorted position i starts a new (group, token) slot
@@ -462,6 +647,8 @@ __device__ __forceinline__ void eval_items(const SlotHead& h, int64_t base, int 
     v[j] = ((((uint32_t)k[j + 1] ^ (uint32_t)k[j]) & h.gmask) != 0u || t[j + 1] != t[j]) ? 1 : 0;
 }
 
+// Outputs of the slot-head scan (slot_heads_down_kernel): every slot's token and first sorted
+// position, every group's first slot, the slot count.
 struct EmitSlots {
   SlotHead h;
   const int32_t* n_active;
@@ -471,15 +658,6 @@ struct EmitSlots {
   int32_t* slot_off;
   int32_t* grp_slot;
   int32_t* counters;
-  __device__ void operator()(int64_t i, int val, int pos) const {
-    if (!val) return;
-    slot_token[pos] = (int32_t)div_by((uint32_t)clamp_task(h.perm[i], h.m), h.hk);
-    slot_off[pos] = (int32_t)i;
-    const uint32_t g = (uint32_t)h.key[i] & h.gmask;
-    if ((i == 0 || ((((uint32_t)h.key[i - 1]) ^ (uint32_t)h.key[i]) & h.gmask) != 0u) &&
-        g < (uint64_t)groups)
-      grp_slot[g] = pos;
-  }
   __device__ void finish(int total) const {
     slot_off[total] = (int32_t)h.m;
     counters[0] = total;
@@ -487,6 +665,73 @@ struct EmitSlots {
     grp_slot[ng < groups ? ng : groups] = total;
   }
 };
+
+// The slot-head scan's second step with the compaction staged in LDS: each thread keeps the
+// token and group key of its items from the flag evaluation, puts its heads' (token, position)
+// pairs at their rank inside the tile, and the workgroup writes both lists out as contiguous
+// runs (emitting from the items would re-read perm and key for every head and store one
+// scattered word per head). Group heads, a few per tile, are written directly.
+__global__ __launch_bounds__(kThreads) void slot_heads_down_kernel(EmitSlots e,
+                                                                  const int32_t* partial) {
+  __shared__ int32_t s_tok[kTile];
+  __shared__ int32_t s_off[kTile];
+  const SlotHead& h = e.h;
+  int before;
+  block_excl_scan(partial_prefix(partial, (int)blockIdx.x), &before);
+  const int64_t base = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kItems;
+  // perm and key at positions base - 1 .. base + kItems - 1 (clamped into [0, m) at the ends)
+  int32_t p[kItems + 1], k[kItems + 1];
+  if (base > 0 && base + kItems <= h.m) {
+    p[0] = h.perm[base - 1];
+    k[0] = h.key[base - 1];
+#pragma unroll
+    for (int q = 0; q < kItems / 4; ++q) {
+      const int4 pp = *(const int4*)(h.perm + base + 4 * q);
+      const int4 kk = *(const int4*)(h.key + base + 4 * q);
+      p[1 + 4 * q] = pp.x; p[2 + 4 * q] = pp.y; p[3 + 4 * q] = pp.z; p[4 + 4 * q] = pp.w;
+      k[1 + 4 * q] = kk.x; k[2 + 4 * q] = kk.y; k[3 + 4 * q] = kk.z; k[4 + 4 * q] = kk.w;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j <= kItems; ++j) {
+      int64_t i = base - 1 + j;
+      i = i < 0 ? 0 : (i >= h.m ? h.m - 1 : i);
+      p[j] = h.perm[i];
+      k[j] = h.key[i];
+    }
+  }
+  uint32_t t[kItems + 1];
+#pragma unroll
+  for (int j = 0; j <= kItems; ++j) t[j] = div_by((uint32_t)clamp_task(p[j], h.m), h.hk);
+  int v[kItems], cnt = 0;
+  uint32_t gnew = 0;
+#pragma unroll
+  for (int j = 0; j < kItems; ++j) {
+    const int64_t i = base + j;
+    const bool gs = i == 0 || ((((uint32_t)k[j + 1] ^ (uint32_t)k[j]) & h.gmask) != 0u);
+    v[j] = (i < h.m && (gs || t[j + 1] != t[j])) ? 1 : 0;
+    gnew |= (i < h.m && gs) ? 1u << j : 0u;
+    cnt += v[j];
+  }
+  int total;
+  int lp = block_excl_scan(cnt, &total);
+#pragma unroll
+  for (int j = 0; j < kItems; ++j) {
+    if (v[j]) {
+      s_tok[lp] = (int32_t)t[j + 1];
+      s_off[lp] = (int32_t)(base + j);
+      const uint32_t g = (uint32_t)k[j + 1] & h.gmask;
+      if (((gnew >> j) & 1u) && g < (uint64_t)e.groups) e.grp_slot[g] = before + lp;
+    }
+    lp += v[j];
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < total; i += kThreads) {
+    e.slot_token[before + i] = s_tok[i];
+    e.slot_off[before + i] = s_off[i];
+  }
+  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) e.finish(before + total);
+}
 
 struct GroupTiles {  // work tiles of group q: ceil(slots / 256) * ceil(experts / te)
   const int32_t* grp_slot;
@@ -1005,6 +1250,11 @@ int64_t partial_count(int64_t M) {
   return (std::max<int64_t>(hist, M) + kTile - 1) / kTile + 1;
 }
 
+// Scan partials of a schedule: the sort's scans over M tasks, and a scan over the N experts.
+int64_t sched_partial_count(int64_t M, int64_t N) {
+  return std::max<int64_t>(partial_count(M), (N + kTile - 1) / kTile + 1);
+}
+
 struct SortBuffers {
   int32_t *k0, *v0, *k1, *v1, *hist, *partial;
 };
@@ -1054,7 +1304,7 @@ size_t schedule_ws_bytes(int64_t M, int64_t N) {
   size_t b = 0;
   b += 4 * align_up((size_t)M * 4);               // keys/values ping-pong
   b += align_up((size_t)hist * 4);                // histogram
-  b += align_up((size_t)partial_count(M) * 4);    // scan partials
+  b += align_up((size_t)sched_partial_count(M, N) * 4);  // scan partials
   b += align_up((size_t)N * 4);                   // expert -> rank in the active list (B > 1)
   b += align_up((size_t)M * 4);                   // group key of every task (B > 1)
   return b;
@@ -1079,7 +1329,7 @@ hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, in
   b.k1 = (int32_t*)w; w += align_up((size_t)M * 4);
   b.v1 = (int32_t*)w; w += align_up((size_t)M * 4);
   b.hist = (int32_t*)w; w += align_up((size_t)kMaxRadix * (tiles > 0 ? tiles : 1) * 4);
-  b.partial = (int32_t*)w; w += align_up((size_t)partial_count(M) * 4);
+  b.partial = (int32_t*)w; w += align_up((size_t)sched_partial_count(M, s.N) * 4);
   int32_t* rank = (int32_t*)w; w += align_up((size_t)s.N * 4);
   int32_t* gkey = (int32_t*)w;
   const int64_t cap64 = std::min<int64_t>(M, s.N);
@@ -1150,8 +1400,8 @@ hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, in
                        dim3(kThreads), 0, st, (const int32_t*)active, (const int32_t*)n_active,
                        rank, cap64, s.N);
     const int gb = group_key_bits(s);
-    hipLaunchKernelGGL(group_key_kernel, dim3((unsigned)((M + kThreads - 1) / kThreads)),
-                       dim3(kThreads), 0, st, idx, (const int32_t*)rank, gkey, M, s.N, s.B, gb);
+    hipLaunchKernelGGL(group_key_kernel, dim3(key_blocks(M)), dim3(kThreads), 0, st, idx,
+                       (const int32_t*)rank, gkey, M, s.N, s.B, div_magic((uint32_t)s.B), gb);
     const int32_t* gk = nullptr;
     hipError_t e = radix_sort_tasks(gkey, M, gb, perm, b, &gk, st);
     if (e != hipSuccess) return e;
@@ -1161,6 +1411,53 @@ hipError_t launch_schedule(const Shape& s, const int32_t* idx, int32_t* perm, in
   return hipGetLastError();
 }
 
+
+// The grouped layer's schedule without the sort by expert: the active list only needs to know
+// which experts have tasks, so a bitmap of them (mark_experts_kernel) and one scan over its words
+// give the ascending active list and every expert's rank; the group keys and the stable sort by
+// group key then run as in launch_schedule. Same workspace: the bitmap and its prefix take the
+// rank array's place.
+bool group_schedule_fits(const Shape& s) { return (s.N + 31) / 32 <= kMapWords; }
+
+hipError_t launch_group_schedule(const Shape& s, const int32_t* idx, int32_t* perm,
+                                 int32_t* active, int32_t* n_active, void* ws,
+                                 const int32_t** group_keys, hipStream_t st) {
+  if (!group_schedule_fits(s)) return hipErrorInvalidValue;
+  const int64_t M = s.M;
+  const int64_t tiles = (M + kTile - 1) / kTile;
+  char* w = (char*)ws;
+  SortBuffers b;
+  b.k0 = (int32_t*)w; w += align_up((size_t)M * 4);
+  b.v0 = (int32_t*)w; w += align_up((size_t)M * 4);
+  b.k1 = (int32_t*)w; w += align_up((size_t)M * 4);
+  b.v1 = (int32_t*)w; w += align_up((size_t)M * 4);
+  b.hist = (int32_t*)w; w += align_up((size_t)kMaxRadix * (tiles > 0 ? tiles : 1) * 4);
+  b.partial = (int32_t*)w; w += align_up((size_t)sched_partial_count(M, s.N) * 4);
+  // 2 * words <= max(64, N) ints: inside the rank array
+  const int words = (int)((s.N + 31) / 32);
+  uint32_t* bits = (uint32_t*)w;
+  int32_t* prefix = (int32_t*)w + words;
+  w += align_up((size_t)s.N * 4);
+  int32_t* gkey = (int32_t*)w;
+  const int32_t cap = (int32_t)std::min<int64_t>(M, s.N);
+  const int64_t rounds = (M + kMapChunk - 1) / kMapChunk;
+  const unsigned grid = (unsigned)std::min<int64_t>(rounds, 512);
+  hipLaunchKernelGGL(fill_i32_kernel, dim3((unsigned)((words + kThreads - 1) / kThreads)),
+                     dim3(kThreads), 0, st, (int32_t*)bits, (int64_t)words, 0);
+  hipLaunchKernelGGL(mark_experts_kernel, dim3(grid), dim3(kMapThreads), (size_t)words * 4, st,
+                     idx, bits, M, s.N, words);
+  hipError_t e = device_scan(PopWord{bits, words}, EmitPrefix{prefix, n_active, words, cap},
+                             words, b.partial, st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(list_active_kernel, dim3((unsigned)((s.N + kThreads - 1) / kThreads)),
+                     dim3(kThreads), 0, st, (const uint32_t*)bits, (const int32_t*)prefix, active,
+                     s.N, cap);
+  const int gb = group_key_bits(s);
+  hipLaunchKernelGGL(group_key_map_kernel, dim3(grid), dim3(kMapThreads), (size_t)words * 8, st,
+                     idx, (const uint32_t*)bits, (const int32_t*)prefix, gkey, M, s.N, words,
+                     s.B, div_magic((uint32_t)s.B), gb);
+  return radix_sort_tasks(gkey, M, gb, perm, b, group_keys, st);
+}
 
 int64_t group_count_bound(const Shape& s) {
   const int64_t cap = std::min<int64_t>(s.M, s.N);
@@ -1203,17 +1500,21 @@ hipError_t launch_group_plan(const Shape& s, const int32_t* perm, const int32_t*
   } else {
     hipLaunchKernelGGL(rank_fill_kernel, dim3((unsigned)((cap + kThreads - 1) / kThreads)),
                        dim3(kThreads), 0, st, active, n_active, rank, cap, s.N);
-    hipLaunchKernelGGL(position_key_kernel, dim3((unsigned)((M + kThreads - 1) / kThreads)),
-                       dim3(kThreads), 0, st, perm, idx, (const int32_t*)rank, keys, M, s.N, s.B,
+    hipLaunchKernelGGL(position_key_kernel, dim3(key_blocks(M)), dim3(kThreads), 0, st, perm,
+                       idx, (const int32_t*)rank, keys, M, s.N, s.B, div_magic((uint32_t)s.B),
                        plan->gbits);
     plan->key = keys;
   }
   const SlotHead head{perm, plan->key, M, (1u << plan->gbits) - 1u,
                       div_magic((uint32_t)s.hk)};
-  hipError_t e = device_scan(head,
-                             EmitSlots{head, n_active, G, s.B, plan->slot_token, plan->slot_off,
-                                       plan->grp_slot, plan->counters},
-                             M, partial, st);
+  const int nb = (int)((M + kTile - 1) / kTile);
+  hipLaunchKernelGGL(scan_reduce_kernel<SlotHead>, dim3(nb), dim3(kThreads), 0, st, head, M,
+                     partial);
+  hipLaunchKernelGGL(slot_heads_down_kernel, dim3(nb), dim3(kThreads), 0, st,
+                     EmitSlots{head, n_active, G, s.B, plan->slot_token, plan->slot_off,
+                               plan->grp_slot, plan->counters},
+                     (const int32_t*)partial);
+  hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return device_scan(GroupTiles{plan->grp_slot, n_active, G, s.B, grouped_tile_experts(s.B)},
                      EmitTiles{plan->grp_tile, G + 1, plan->counters}, G + 1, partial, st);
