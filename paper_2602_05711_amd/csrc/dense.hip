@@ -34,11 +34,20 @@ __global__ __launch_bounds__(256) void densify_kernel(const int32_t* __restrict_
   const int tid = threadIdx.x;
   int e[kDenseSlots];
   uint16_t v[kDenseSlots];
+  float av[kDenseSlots];
+  // All 2 * kDenseSlots loads in flight at once: unconditional, a slot past hk reading the last
+  // slot and masked afterwards (guarded loads would each wait for the previous one).
 #pragma unroll
   for (int q = 0; q < kDenseSlots; ++q) {
-    const int j = q * 256 + tid;
-    e[q] = j < hk ? idx[t * hk + j] : -1;
-    v[q] = j < hk ? bf16_rne(a[t * hk + j]) : (uint16_t)0;
+    const int j = q * 256 + tid < hk ? q * 256 + tid : hk - 1;
+    e[q] = idx[t * hk + j];
+    av[q] = a[t * hk + j];
+  }
+#pragma unroll
+  for (int q = 0; q < kDenseSlots; ++q) {
+    const bool ok = q * 256 + tid < hk;
+    e[q] = ok ? e[q] : -1;
+    v[q] = ok ? bf16_rne(av[q]) : (uint16_t)0;
   }
   uint4* dst_row = (uint4*)(A + t * kpad);
   for (int64_t c0 = 0; c0 < kpad; c0 += kDenseChunk) {

@@ -448,7 +448,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
 
 // ---------------------------------------------------------------- large K (65 .. 4096)
 // One workgroup per (token, head) row, for K beyond one wavefront (eight waves when the final
-// sort holds 2048 keys or more, four below, where more rows share a compute unit):
+// order holds 2048 keys or more, four below, where more rows share a compute unit):
 //   1. each half is put in (logit desc, index asc) order: a half of at most 512 logits by a
 //      bitonic sort in one wave's registers (the two halves on two waves), a longer half by a
 //      bitonic sort in LDS;
@@ -463,13 +463,16 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
 //      row rank such cells have equal column logits, so their column indices ascend with b,
 //      and a second interval search over the id finds the smallest id bound that admits K;
 //   4. the selected cells of row rank a are then its first t_a columns: they are written out
-//      at the offsets of an exclusive scan of t_a and bitonic-sorted descending by (score,
-//      ~id);
-//   5. gates: softmax over the K scores, summed in a fixed order.
+//      at the offsets of an exclusive scan of t_a, one run per row rank, each run already in
+//      the final order (score descending, id ascending);
+//   5. from 1024 keys on the runs are merged pairwise, level by level (merge path, in place);
+//      up to 512 keys a bitonic sort over LDS is faster;
+//   6. gates: softmax over the K scores, summed in a fixed order.
 // Scores are compared as exact doubles (sums of two floats), integer keys elsewhere, so the
 // result is exact and independent of thread timing.
 
 constexpr int kLargeMaxWaves = 8;  // workgroups of 256 or 512 threads
+constexpr int kMergeMinKeys = 1024;  // final order by merging the runs from k2 = 1024 keys on
 
 struct LargeArgs {
   const float* hs;
@@ -542,48 +545,6 @@ __device__ __forceinline__ void block_sum3(LargeShared& sh, int (&v)[3], int w, 
   }
 }
 
-// Bitonic merges k = k_lo, 2 k_lo, ..., k_hi (k_hi <= 8) restricted to partner distances below
-// 8, on blocks of eight consecutive keys (block b of k2 / 8 held by one thread in registers):
-// for each merge, distances min(k / 2, 4), ..., 1; keys are ordered descending by (s, n) where
-// (i & k) == 0, ascending elsewhere, as in the LDS levels.
-__device__ __forceinline__ void sort_block8(uint64_t* ks, uint32_t* kn, int k2, int k_lo,
-                                            int k_hi, int tid, int nthreads) {
-  for (int b = tid; b < (k2 >> 3); b += nthreads) {
-    uint64_t s[8];
-    uint32_t n[8];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      s[q] = ks[8 * b + q];
-      n[q] = kn[8 * b + q];
-    }
-    for (int k = k_lo; k <= k_hi; k <<= 1) {
-#pragma unroll
-      for (int j = 4; j >= 1; j >>= 1) {
-        if (j >= k) continue;
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          if (q & j) continue;
-          const bool up = ((8 * b + q) & k) == 0;
-          const bool lt = s[q] < s[q + j] || (s[q] == s[q + j] && n[q] < n[q + j]);
-          if (lt == up) {
-            const uint64_t ts = s[q];
-            s[q] = s[q + j];
-            s[q + j] = ts;
-            const uint32_t tn = n[q];
-            n[q] = n[q + j];
-            n[q + j] = tn;
-          }
-        }
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      ks[8 * b + q] = s[q];
-      kn[8 * b + q] = n[q];
-    }
-  }
-}
-
 // Descending bitonic sort of 512 keys held by one wave, eight consecutive keys per lane
 // (key i = 8 lane + q in x[q]): partner distances below 8 are exchanges between a lane's own
 // registers, larger ones swap with lane l ^ (distance / 8) through DPP and the lane-half swaps.
@@ -631,8 +592,9 @@ __device__ __forceinline__ void wave_sort512_desc(uint64_t (&x)[8]) {
   }
 }
 
-// RPT: row ranks per thread in the searches (kr <= RPT * NT).
-template <int NT, int RPT>
+// RPT: row ranks per thread in the searches (kr <= RPT * NT). MERGE: the final order by merging
+// the runs (k2 >= 1024), else by a bitonic sort (k2 <= 512, four waves).
+template <int NT, int RPT, bool MERGE>
 __global__ __launch_bounds__(NT, NT == 256 ? 5 : 4) void select_large_kernel(LargeArgs a) {
   constexpr int kRowsPerThread = RPT;
   constexpr int kLargeThreads = NT;
@@ -889,48 +851,143 @@ __global__ __launch_bounds__(NT, NT == 256 ? 5 : 4) void select_large_kernel(Lar
           sel_n[q] = 0xFFFFFFFFu - (rid + (0xFFFFFFFFu - (uint32_t)cq));
         }
       }
+    }
+    __syncthreads();
+    // 5. the final order. Row rank a's selected cells are already in it (descending score,
+    // ascending id: its columns are in descending logit order, equal logits by ascending
+    // index), so the K keys are kr sorted runs at the offsets cnt_hi. They are merged pairwise,
+    // level by level: at level L the runs of row ranks [2m 2^L, (2m + 1) 2^L) and
+    // [(2m + 1) 2^L, (2m + 2) 2^L) become one. Each thread produces kOut consecutive outputs:
+    // the split of its first output between the two inputs comes from a binary search along
+    // the merge path, the rest from a sequential merge with the two heads in registers (moving
+    // on to the next run where one ends); after a barrier the outputs are written in place.
+    // Keys are unique (distinct ids), so the order is fully determined.
+    if constexpr (!MERGE) {
+      // short lists (k2 <= 512): a bitonic sort over LDS (keys past K padded with 0, below
+      // every key) takes fewer cycles than the merge levels (at K = 512: 25k against 31k)
       for (int i = K + tid; i < k2; i += kLargeThreads) {
         sel_s[i] = 0ull;
         sel_n[i] = 0u;
       }
-    }
-    __syncthreads();
-    // bitonic sort of the K selected keys, descending by (score, ~id). With eight waves (2048 keys
-    // or more) the levels with partner distance 8 or more run over LDS, one compare-exchange
-    // per pair, and the last three levels of each merge (distances 4, 2, 1), and the whole of
-    // the first three merges, run on eight consecutive keys held in one thread's registers: one
-    // LDS pass instead of three. With four waves every level runs over LDS (registers are kept
-    // for occupancy there).
-    constexpr int kRegFrom = NT == 512 ? 4 : 1;  // first merge whose low levels use registers
-    if constexpr (NT == 512) {
-      sort_block8(sel_s, sel_n, k2, 2, 8, tid, kLargeThreads);
       __syncthreads();
-    }
-    for (int lk = kRegFrom; (1 << lk) <= k2; ++lk) {
-      const int k = 1 << lk;
-      for (int lj = lk - 1; lj >= (NT == 512 ? 3 : 0); --lj) {
-        const int j = 1 << lj;
-        for (int t = tid; t < (k2 >> 1); t += kLargeThreads) {
-          const int i = ((t >> lj) << (lj + 1)) | (t & (j - 1));
-          const uint64_t xs = sel_s[i], ys = sel_s[i + j];
-          const uint32_t xn = sel_n[i], yn = sel_n[i + j];
-          const bool up = (i & k) == 0;
-          const bool lt = xs < ys || (xs == ys && xn < yn);
-          if (lt == up) {
-            sel_s[i] = ys;
-            sel_s[i + j] = xs;
-            sel_n[i] = yn;
-            sel_n[i + j] = xn;
+      for (int lk = 1; (1 << lk) <= k2; ++lk) {
+        const int k = 1 << lk;
+        for (int lj = lk - 1; lj >= 0; --lj) {
+          const int j = 1 << lj;
+          for (int t = tid; t < (k2 >> 1); t += kLargeThreads) {
+            const int i = ((t >> lj) << (lj + 1)) | (t & (j - 1));
+            const uint64_t xs = sel_s[i], ys = sel_s[i + j];
+            const uint32_t xn = sel_n[i], yn = sel_n[i + j];
+            const bool up = (i & k) == 0;
+            const bool lt = xs < ys || (xs == ys && xn < yn);
+            if (lt == up) {
+              sel_s[i] = ys;
+              sel_s[i + j] = xs;
+              sel_n[i] = yn;
+              sel_n[i + j] = xn;
+            }
+          }
+          __syncthreads();
+        }
+      }
+    } else {
+      constexpr int kOut = NT == 512 ? 8 : 4;  // NT kOut >= k2 >= K
+      const int o0 = tid * kOut;
+      const int nout = o0 < K ? (K - o0 < kOut ? K - o0 : kOut) : 0;
+      int a0 = 0;  // row rank holding position o0: the last a with cnt_hi[a] <= o0
+      if (nout > 0) {
+        int ahi = kr - 1;
+        while (a0 < ahi) {
+          const int mid = (a0 + ahi + 1) >> 1;
+          if (cnt_hi[mid] <= o0) a0 = mid; else ahi = mid - 1;
+        }
+      }
+      auto before = [](uint64_t s0, uint32_t n0, uint64_t s1, uint32_t n1) {
+        return s0 > s1 || (s0 == s1 && n0 > n1);
+      };
+      for (int L = 0; (1 << L) < kr; ++L) {
+        uint64_t os[kOut];
+        uint32_t on[kOut];
+        if (nout > 0) {
+          // the merged run holding o0 (it holds row rank a0) and its inputs A = [as, ae),
+          // B = [ae, be)
+          int m = a0 >> (L + 1);
+          const int as = cnt_hi[m << (L + 1)];
+          int ae = cnt_hi[min((m << (L + 1)) + (1 << L), kr)];
+          int be = cnt_hi[min((m + 1) << (L + 1), kr)];
+          // merge path: the run's first d = o0 - as outputs are i keys of A and d - i of B
+          const int d = o0 - as;
+          int lo2 = d - (be - ae) > 0 ? d - (be - ae) : 0;
+          int hi2 = d < ae - as ? d : ae - as;
+          while (lo2 < hi2) {
+            const int mid = (lo2 + hi2) >> 1;
+            const int bj = ae + d - mid - 1;
+            const uint64_t sa = sel_s[as + mid], sb = sel_s[bj];
+            bool bf = sa > sb;
+            if (sa == sb) bf = sel_n[as + mid] > sel_n[bj];  // ids only on equal scores
+            if (bf) lo2 = mid + 1;
+            else hi2 = mid;
+          }
+          int ia = as + lo2, ib = ae + d - lo2;
+          // heads (key 0 past an input's end: below every key)
+          uint64_t ha = ia < ae ? sel_s[ia] : 0ull, hb = ib < be ? sel_s[ib] : 0ull;
+          uint32_t na = ia < ae ? sel_n[ia] : 0u, nb = ib < be ? sel_n[ib] : 0u;
+#pragma unroll
+          for (int q = 0; q < kOut; ++q) {
+            if (q < nout) {
+              const int o = o0 + q;
+              if (o == be) {  // this run is done: the next nonempty one starts at o
+                do {
+                  ++m;
+                  ae = cnt_hi[min((m << (L + 1)) + (1 << L), kr)];
+                  be = cnt_hi[min((m + 1) << (L + 1), kr)];
+                } while (be <= o);
+                ia = o;
+                ib = ae;
+                ha = ia < ae ? sel_s[ia] : 0ull;
+                na = ia < ae ? sel_n[ia] : 0u;
+                hb = ib < be ? sel_s[ib] : 0ull;
+                nb = ib < be ? sel_n[ib] : 0u;
+              }
+              const bool ta = before(ha, na, hb, nb);
+              os[q] = ta ? ha : hb;
+              on[q] = ta ? na : nb;
+              // one read for the new head of the input just taken from (index clamped, the
+              // key replaced by 0 past that input's end)
+              if (ta) ++ia; else ++ib;
+              const int nx = ta ? ia : ib;
+              const bool live = nx < (ta ? ae : be);
+              const int rx = nx < K ? nx : K - 1;
+              const uint64_t ks = live ? sel_s[rx] : 0ull;
+              const uint32_t kn = live ? sel_n[rx] : 0u;
+              ha = ta ? ks : ha;
+              na = ta ? kn : na;
+              hb = ta ? hb : ks;
+              nb = ta ? nb : kn;
+            }
+          }
+        }
+        __syncthreads();
+        if (nout == kOut) {  // 16-byte stores (o0 is a multiple of kOut)
+#pragma unroll
+          for (int q = 0; q < kOut; q += 2)
+            *(ulonglong2*)(sel_s + o0 + q) = make_ulonglong2(os[q], os[q + 1]);
+#pragma unroll
+          for (int q = 0; q < kOut; q += 4)
+            *(uint4*)(sel_n + o0 + q) = make_uint4(on[q], on[q + 1], on[q + 2], on[q + 3]);
+        } else {
+#pragma unroll
+          for (int q = 0; q < kOut; ++q) {
+            if (q < nout) {
+              sel_s[o0 + q] = os[q];
+              sel_n[o0 + q] = on[q];
+            }
           }
         }
         __syncthreads();
       }
-      if constexpr (NT == 512) {
-        sort_block8(sel_s, sel_n, k2, k, k, tid, kLargeThreads);
-        __syncthreads();
-      }
     }
-    // 5. gates: e_k = exp(S_k - S_0), summed per thread over a contiguous range, then across
+    // 6. gates: e_k = exp(S_k - S_0), summed per thread over a contiguous range, then across
     // lanes and waves in a fixed order
     const double s0 = f64_from_ord(sel_s[0]);
     const int per = (K + kLargeThreads - 1) / kLargeThreads;
@@ -1062,23 +1119,29 @@ hipError_t launch_select(const Shape& s, const float* half_scores, int32_t* idx,
     const int kr = s.K < s.nr ? s.K : s.nr;
     const size_t lds = large_lds_bytes(n2, k2, kr);
     const dim3 grid((unsigned)(s.rows < 4096 ? s.rows : 4096));
-    // eight waves per row once the final sort has 2048 keys or more; four below, where more
-    // rows share a compute unit. Each thread searches over ceil(kr / threads) row ranks,
-    // rounded up to a power of two (kr <= K <= 4096).
+    // eight waves per row once the final order holds 2048 keys or more; four below, where
+    // more rows share a compute unit. The final order comes from merging the runs from 1024
+    // keys on, from a bitonic sort below. Each thread searches over ceil(kr / threads) row
+    // ranks, rounded up to a power of two (kr <= K <= 4096).
     const int nt = k2 >= 2048 ? 512 : 256;
+    const bool merge = k2 >= kMergeMinKeys;
     const int need = (kr + nt - 1) / nt;
     const int rpt = need <= 1 ? 1 : (need <= 2 ? 2 : (need <= 4 ? 4 : 8));
-#define OMNIMOE_SELECT_LARGE(NT_, RPT_)                                                    \
-  hipLaunchKernelGGL((select_large_kernel<NT_, RPT_>), grid, dim3(NT_), lds, st, a)
+#define OMNIMOE_SELECT_LARGE(NT_, RPT_, M_)                                                \
+  hipLaunchKernelGGL((select_large_kernel<NT_, RPT_, M_>), grid, dim3(NT_), lds, st, a)
     if (nt == 512) {
-      if (rpt == 1) OMNIMOE_SELECT_LARGE(512, 1);
-      else if (rpt == 2) OMNIMOE_SELECT_LARGE(512, 2);
-      else if (rpt == 4) OMNIMOE_SELECT_LARGE(512, 4);
-      else OMNIMOE_SELECT_LARGE(512, 8);
+      if (rpt == 1) OMNIMOE_SELECT_LARGE(512, 1, true);
+      else if (rpt == 2) OMNIMOE_SELECT_LARGE(512, 2, true);
+      else if (rpt == 4) OMNIMOE_SELECT_LARGE(512, 4, true);
+      else OMNIMOE_SELECT_LARGE(512, 8, true);
+    } else if (merge) {
+      if (rpt == 1) OMNIMOE_SELECT_LARGE(256, 1, true);
+      else if (rpt == 2) OMNIMOE_SELECT_LARGE(256, 2, true);
+      else OMNIMOE_SELECT_LARGE(256, 4, true);
     } else {
-      if (rpt == 1) OMNIMOE_SELECT_LARGE(256, 1);
-      else if (rpt == 2) OMNIMOE_SELECT_LARGE(256, 2);
-      else OMNIMOE_SELECT_LARGE(256, 4);
+      if (rpt == 1) OMNIMOE_SELECT_LARGE(256, 1, false);
+      else if (rpt == 2) OMNIMOE_SELECT_LARGE(256, 2, false);
+      else OMNIMOE_SELECT_LARGE(256, 4, false);
     }
 #undef OMNIMOE_SELECT_LARGE
     return hipGetLastError();
