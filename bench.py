@@ -589,11 +589,20 @@ def main():
     # Kernel groups the layer does not launch for this shape: no schedule (slot-order dot), or
     # a dot formed by the selection kernel, whose time and bytes then count under "select".
     absent = {}
-    if not path & B.PATH_SCHEDULE:
+    if not path & (B.PATH_SCHEDULE | B.PATH_DENSE_DOT):
         absent["schedule"] = "not formed (slot-order dot)"
     if path & B.PATH_SELECT_DOT:
         absent["expert_dot"] = "formed by the selection kernel"
         work["select"] = ("hbm", work["select"][1] + work["expert_dot"][1])
+    # Products dense over all experts (Eq. 14 with a single group) are MFMA GEMMs: priced by the
+    # FLOP they perform, 2 T N d each (the expert dimension padded to the split width).
+    dense_flop = 2.0 * w.T * w.N * w.d
+    if path & B.PATH_DENSE_SUM:
+        work["accumulate"] = ("mfma", dense_flop)
+    if path & B.PATH_DENSE_DOT:
+        work["expert_dot"] = ("mfma", dense_flop)
+        # the selection-mask pass: idx and gates in; mask, prefix counts and sorted gates out
+        work["schedule"] = ("hbm", 8.0 * w.M + 8.0 * w.T * ((w.N + 31) // 32) + 4.0 * w.M)
     kernels = {}
     for k, (bound, amount) in work.items():
         if k in absent:
@@ -679,7 +688,8 @@ def main():
         "layer_path": {"schedule": bool(path & B.PATH_SCHEDULE),
                        "grouped": bool(path & B.PATH_GROUPED),
                        "select_forms_dot": bool(path & B.PATH_SELECT_DOT),
-                       "dense_routed_sum": bool(path & B.PATH_DENSE_SUM)},
+                       "dense_routed_sum": bool(path & B.PATH_DENSE_SUM),
+                       "dense_expert_dot": bool(path & B.PATH_DENSE_DOT)},
         "kernels": kernels,
     }
     s = json.dumps(line)

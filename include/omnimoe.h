@@ -327,8 +327,13 @@ typedef enum {
   OMNIMOE_PATH_GROUPED = 2,    /* a_p from the grouped GEMM of Eq. 14 (group_size > 1) */
   OMNIMOE_PATH_SELECT_DOT = 4, /* the selection kernel also forms the slot-order a_p (no separate
                                   dot launch; the OMNIMOE_KERNEL_SELECT time includes it) */
-  OMNIMOE_PATH_DENSE_SUM = 8   /* the routed sum as one dense product over all experts (one head,
+  OMNIMOE_PATH_DENSE_SUM = 8,  /* the routed sum as one dense product over all experts (one head,
                                   K >= N / 64) */
+  OMNIMOE_PATH_DENSE_DOT = 16  /* with groups of one expert, the a_p as well: x . u for every
+                                  (token, expert) pair on the MFMA kernel, gate and activation
+                                  kept at the selected pairs only (Eq. 14 with a single group;
+                                  no schedule; OMNIMOE_KERNEL_SCHEDULE times the selection-mask
+                                  pass, OMNIMOE_KERNEL_EXPERT_DOT this product) */
 } omnimoe_path_flag;
 omnimoe_status omnimoe_layer_path(const omnimoe_layer_desc* desc, int32_t* path);
 

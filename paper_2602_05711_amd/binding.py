@@ -266,7 +266,7 @@ def omnimoe_layer_forward(desc, x, keys_row, keys_col, u, v, y, idx_out=None, ga
 NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024  # OMNIMOE_NOALLOC_SCRATCH_BYTES
 
 # omnimoe_path_flag
-PATH_SCHEDULE, PATH_GROUPED, PATH_SELECT_DOT, PATH_DENSE_SUM = 1, 2, 4, 8
+PATH_SCHEDULE, PATH_GROUPED, PATH_SELECT_DOT, PATH_DENSE_SUM, PATH_DENSE_DOT = 1, 2, 4, 8, 16
 
 
 def omnimoe_layer_path(desc):

@@ -112,6 +112,8 @@ int32_t layer_path(const Shape& s) {
   if (unscheduled && s.rows >= kSelectDotMinRows && omnimoe::select_dot_fusable(s))
     f |= OMNIMOE_PATH_SELECT_DOT;
   if (omnimoe::dense_accumulate(s)) f |= OMNIMOE_PATH_DENSE_SUM;
+  // Both products dense over all experts: no schedule and no per-task dot.
+  if (omnimoe::dense_dot(s)) f = OMNIMOE_PATH_DENSE_SUM | OMNIMOE_PATH_DENSE_DOT;
   return f;
 }
 
@@ -166,6 +168,8 @@ size_t stage_bytes(const Shape& s, int stage) {
       // read: a[] and the dense sum's buffers then follow the logits instead of sharing them.
       if (layer_path(s) & OMNIMOE_PATH_SELECT_DOT)
         late = hs_bytes(s) + m_bytes(s) + omnimoe::dense_accumulate_ws_bytes(s);
+      // Both products dense: only their buffers, after the logits are dead.
+      if (layer_path(s) & OMNIMOE_PATH_DENSE_DOT) late = omnimoe::dense_dot_ws_bytes(s);
       return fixed + std::max(hs_bytes(s), late);
     }
   }
@@ -230,6 +234,16 @@ omnimoe_status layer_impl(const omnimoe_layer_desc* desc, const void* x, const v
     return hip_status(e);
   }
   mark(2);
+  if (path & OMNIMOE_PATH_DENSE_DOT) {
+    if ((e = omnimoe::launch_select_mask(s, idx, gates, late, strm))) return hip_status(e);
+    mark(3);
+    if ((e = omnimoe::launch_dense_dot(s, x, u, late, strm))) return hip_status(e);
+    mark(4);
+    if ((e = omnimoe::launch_dense_routed_sum(s, v, y, late, strm))) return hip_status(e);
+    mark(5);
+    if (timer) ++timer->used;
+    return OMNIMOE_OK;
+  }
   const int32_t* sk = nullptr;
   const int32_t* gk = nullptr;
   if (!unscheduled) {

@@ -4,6 +4,10 @@
 // single group. A is built in bf16 (a_p rounded to nearest even), V is transposed once so that
 // the expert dimension is contiguous, the product runs on the MFMA logit kernel split over the
 // expert dimension, and the split partials are added in split order, so y is deterministic.
+// In the layer (one head, routing from the selection kernel) the first product runs dense as
+// well: h = X U^T over all experts on the same MFMA kernel, whose epilogue keeps only the
+// selected cells, A[t, e] = g * act(h[t, e]) in bf16, from a per-token selection mask; the
+// schedule, the per-task dot and the densify pass are then not needed.
 // A token's slots normally name distinct experts (the router picks K distinct cells), so each
 // A[t, e] is a single a_p; when a caller's idx repeats an expert within a token, that entry is
 // the sum of the repeated slots' a_p in slot order, so the result stays deterministic.
@@ -152,6 +156,77 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restr
   }
 }
 
+// Selection of one token as a bitmask over expert ids (bit e % 32 of word e / 32), the number
+// of selected experts in the words before each word, and the gates in expert-id order:
+// gsorted[t, r] = gate of the selected expert of rank r. One workgroup per token; the mask and
+// the prefix counts are built in LDS (bits set with LDS atomic ORs, which commute). The layer's
+// ids come from the selection kernel and are distinct within a token.
+constexpr int kMaskWordsMax = 9216;  // a token's words held in LDS (N up to 294912 experts)
+
+__global__ __launch_bounds__(256) void select_mask_kernel(const int32_t* __restrict__ idx,
+                                                          const float* __restrict__ gates,
+                                                          uint32_t* __restrict__ mask,
+                                                          int32_t* __restrict__ pre,
+                                                          float* __restrict__ gsorted, int hk,
+                                                          int64_t N, int words) {
+  __shared__ uint32_t lm[kMaskWordsMax];
+  __shared__ int32_t lpre[kMaskWordsMax];
+  __shared__ int32_t part[256];
+  const int64_t t = blockIdx.x;
+  const int tid = threadIdx.x;
+  // the token's slots, kDenseSlots per thread, all loads in flight at once (a slot past hk reads
+  // the last slot and is dropped)
+  int e[kDenseSlots];
+  float gv[kDenseSlots];
+#pragma unroll
+  for (int q = 0; q < kDenseSlots; ++q) {
+    const int j = q * 256 + tid < hk ? q * 256 + tid : hk - 1;
+    e[q] = idx[t * hk + j];
+    gv[q] = gates[t * hk + j];
+  }
+  for (int w = tid; w < words; w += 256) lm[w] = 0u;
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < kDenseSlots; ++q) {
+    if (q * 256 + tid >= hk || e[q] < 0 || e[q] >= N) e[q] = -1;
+    if (e[q] >= 0) atomicOr(&lm[e[q] >> 5], 1u << (e[q] & 31));
+  }
+  __syncthreads();
+  // exclusive prefix of the words' popcounts: thread tid sums a contiguous run of words, the
+  // 256 run sums are scanned in LDS, then each run is walked again
+  const int per = (words + 255) / 256;
+  const int w_lo = tid * per < words ? tid * per : words;
+  const int w_hi = w_lo + per < words ? w_lo + per : words;
+  int run = 0;
+  for (int w = w_lo; w < w_hi; ++w) run += __popc(lm[w]);
+  part[tid] = run;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    const int v = tid >= off ? part[tid - off] : 0;
+    __syncthreads();
+    part[tid] += v;
+    __syncthreads();
+  }
+  int c = part[tid] - run;
+  for (int w = w_lo; w < w_hi; ++w) {
+    lpre[w] = c;
+    c += __popc(lm[w]);
+  }
+  __syncthreads();
+  for (int w = tid; w < words; w += 256) {
+    mask[t * words + w] = lm[w];
+    pre[t * words + w] = lpre[w];
+  }
+#pragma unroll
+  for (int q = 0; q < kDenseSlots; ++q) {
+    if (e[q] >= 0) {
+      const int w = e[q] >> 5;
+      const int r = lpre[w] + __popc(lm[w] & ((1u << (e[q] & 31)) - 1u));
+      gsorted[t * hk + r] = gv[q];
+    }
+  }
+}
+
 struct DensePlan {
   int splits;
   int kchunk;
@@ -189,9 +264,12 @@ size_t dense_accumulate_ws_bytes(const Shape& s) {
   return b;
 }
 
-hipError_t launch_dense_accumulate(const Shape& s, const void* v, const int32_t* idx,
-                                   const float* abuf, float* y, void* ws, hipStream_t st) {
-  if (s.T == 0) return hipSuccess;
+namespace {
+
+// y = A V from A [T, kpad] bf16 at the start of ws (V transposed, split-K product, partials
+// added in split order).
+hipError_t launch_dense_product(const Shape& s, const void* v, float* y, void* ws,
+                                hipStream_t st) {
   const DensePlan p = dense_plan(s);
   char* w = (char*)ws;
   uint16_t* A = (uint16_t*)w;
@@ -199,8 +277,6 @@ hipError_t launch_dense_accumulate(const Shape& s, const void* v, const int32_t*
   uint16_t* Vt = (uint16_t*)w;
   w += align256((size_t)s.d * p.kpad * 2);
   float* part = p.splits > 1 ? (float*)w : y;
-  hipLaunchKernelGGL(densify_kernel, dim3((unsigned)s.T), dim3(256), 0, st, idx, abuf, A, s.hk,
-                     s.N, p.kpad);
   hipLaunchKernelGGL(transpose_bf16_kernel, dim3((unsigned)(p.kpad / 64), (unsigned)(s.d / 64)),
                      dim3(256), 0, st, (const uint16_t*)v, Vt, s.N, s.d, p.kpad);
   hipError_t e = launch_gemm_splitk(s.T, s.d, A, p.kpad, Vt, p.kpad, p.kchunk, p.splits, part, st);
@@ -213,6 +289,74 @@ hipError_t launch_dense_accumulate(const Shape& s, const void* v, const int32_t*
                        (const float*)part, y, n4, p.splits, n4);
   }
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_dense_accumulate(const Shape& s, const void* v, const int32_t* idx,
+                                   const float* abuf, float* y, void* ws, hipStream_t st) {
+  if (s.T == 0) return hipSuccess;
+  const DensePlan p = dense_plan(s);
+  hipLaunchKernelGGL(densify_kernel, dim3((unsigned)s.T), dim3(256), 0, st, idx, abuf,
+                     (uint16_t*)ws, s.hk, s.N, p.kpad);
+  return launch_dense_product(s, v, y, ws, st);
+}
+
+bool dense_dot(const Shape& s) {
+  return dense_accumulate(s) && s.B == 1 && dense_plan(s).kpad / 32 <= kMaskWordsMax;
+}
+
+size_t dense_dot_ws_bytes(const Shape& s) {
+  if (!dense_dot(s)) return 0;
+  const int64_t words = dense_plan(s).kpad / 32;
+  return dense_accumulate_ws_bytes(s) + 2 * align256((size_t)s.T * words * 4) +
+         align256((size_t)s.T * s.hk * 4);
+}
+
+namespace {
+
+struct MaskBufs {
+  uint32_t* mask;
+  int32_t* pre;
+  float* gsorted;
+  int64_t words;
+};
+
+MaskBufs mask_bufs(const Shape& s, void* ws) {
+  MaskBufs b;
+  b.words = dense_plan(s).kpad / 32;
+  char* w = (char*)ws + dense_accumulate_ws_bytes(s);
+  b.mask = (uint32_t*)w;
+  w += align256((size_t)s.T * b.words * 4);
+  b.pre = (int32_t*)w;
+  w += align256((size_t)s.T * b.words * 4);
+  b.gsorted = (float*)w;
+  return b;
+}
+
+}  // namespace
+
+hipError_t launch_select_mask(const Shape& s, const int32_t* idx, const float* gates, void* ws,
+                              hipStream_t st) {
+  if (s.T == 0) return hipSuccess;
+  const MaskBufs b = mask_bufs(s, ws);
+  hipLaunchKernelGGL(select_mask_kernel, dim3((unsigned)s.T), dim3(256), 0, st, idx, gates,
+                     b.mask, b.pre, b.gsorted, s.hk, s.N, (int)b.words);
+  return hipGetLastError();
+}
+
+hipError_t launch_dense_dot(const Shape& s, const void* x, const void* u, void* ws,
+                            hipStream_t st) {
+  if (s.T == 0) return hipSuccess;
+  const MaskBufs b = mask_bufs(s, ws);
+  return launch_gemm_act_mask(s.T, (int)s.N, (int)dense_plan(s).kpad, x, s.d, u, b.mask, b.pre,
+                              b.words, b.gsorted, s.hk, s.act, (uint16_t*)ws, st);
+}
+
+hipError_t launch_dense_routed_sum(const Shape& s, const void* v, float* y, void* ws,
+                                   hipStream_t st) {
+  if (s.T == 0) return hipSuccess;
+  return launch_dense_product(s, v, y, ws, st);
 }
 
 }  // namespace omnimoe

@@ -51,6 +51,29 @@ size_t dense_accumulate_ws_bytes(const Shape& s);  // 0 when not taken
 hipError_t launch_dense_accumulate(const Shape& s, const void* v, const int32_t* idx,
                                    const float* abuf, float* y, void* ws, hipStream_t st);
 
+// The layer's first product over all experts as well (Eq. 14 with a single group), taken when
+// dense_dot(s): dense_accumulate(s) with groups of one expert. launch_select_mask builds each
+// token's selection mask and gates in expert-id order; launch_dense_dot runs h = X U^T with the
+// masked-activation epilogue, leaving A at the start of ws; launch_dense_routed_sum then forms
+// y = A V. ws holds dense_dot_ws_bytes(s) bytes for all three.
+bool dense_dot(const Shape& s);
+size_t dense_dot_ws_bytes(const Shape& s);  // 0 when not taken
+hipError_t launch_select_mask(const Shape& s, const int32_t* idx, const float* gates, void* ws,
+                              hipStream_t st);
+hipError_t launch_dense_dot(const Shape& s, const void* x, const void* u, void* ws,
+                            hipStream_t st);
+hipError_t launch_dense_routed_sum(const Shape& s, const void* v, float* y, void* ws,
+                                   hipStream_t st);
+
+// bf16 product with the masked-activation epilogue: for t < T and n < ncols_out (a multiple of
+// 64), aout[t, n] = bf16(g * act(x_t . u_n)) where bit n of sel_mask[t] is set (g =
+// sel_gates[t, sel_pre[t, n / 32] + selected bits of that word below n]) and 0 elsewhere;
+// x [T, d] and u [N, d] row-major, d % 64 == 0, no bit set at n >= N.
+hipError_t launch_gemm_act_mask(int64_t T, int N, int ncols_out, const void* x, int d,
+                                const void* u, const uint32_t* sel_mask, const int32_t* sel_pre,
+                                int64_t words, const float* sel_gates, int hk, int act,
+                                uint16_t* aout, hipStream_t st);
+
 // Per-half top-K, Cartesian merge and gates from fp32 half-scores.
 hipError_t launch_select(const Shape& s, const float* half_scores, int32_t* idx, float* gates,
                          hipStream_t st);

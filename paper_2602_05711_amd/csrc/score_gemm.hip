@@ -42,6 +42,17 @@ struct ScoreArgs {
   // kchunk) of half 0 and writes its partial product at out + z part_stride
   int kchunk;
   int64_t part_stride;
+  // masked-activation epilogue (large kernel with ADOT): for token t and expert column n <
+  // ncols_out, aout[t, n] = bf16(g * act(C[t, n])) when bit n of sel_mask[t] is set, where g is
+  // the gate of that expert (sel_gates[t, rank], rank = selected experts of t below n), else 0
+  const uint32_t* sel_mask;  // [T, words] bit n % 32 of word n / 32
+  const int32_t* sel_pre;    // [T, words] selected experts of t in the words before
+  const float* sel_gates;    // [T, hk] gates of t's selected experts in expert-id order
+  uint16_t* aout;            // [T, ncols_out] bf16
+  int64_t words;
+  int ncols_out;
+  int hk;
+  int act;
 };
 
 // One output element (ACC: added to what is there). Each element is written by exactly one
@@ -189,13 +200,147 @@ __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 
 __device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
-template <bool ACC, bool SPLIT = false>
+// Epilogue of the masked-activation product (the first product of Eq. 14 over all experts).
+// Only the selected cells of a tile (a few percent in the layers that take this product) need
+// the activation. The wave's 128 x 64 region of A is first cleared with 16-byte stores; then,
+// a quarter (32 rows) at a time, the wave's accumulators are staged in LDS, each lane takes one
+// selection word of the quarter (a row's 32 columns) and the wave queues the words' set bits,
+// the k-th set bit of every lane in step k (a ballot places them), and the queued cells are
+// evaluated on packed lanes, two per lane at a time so that their gate loads are in flight
+// together, and stored over the cleared region (after a wait for the clearing stores). The work
+// is then proportional to the words and the selected cells, not to the 8192 cells of the region.
+// LDS (the operand stages are free by now): selection words and prefix counts of the tile's 256
+// rows x 8 words (16 KiB); per wave a quarter of accumulators, [32 rows][65] fp32 (an odd row
+// stride, so that the 4-byte staging stores of a half-wave hit distinct banks), and a queue of
+// up to 2048 positions (4 KiB).
+constexpr int kQRow = 65;
+
+// The tile's selection words and prefix counts, four of each per thread (entry tid + 512 i is
+// row (tid + 512 i) / 8, word (tid + 512 i) % 8 of the tile), loaded before the main loop so
+// that their latency is hidden behind it.
+struct TileSel {
+  uint32_t w[4];
+  int32_t p[4];
+};
+
+__device__ __forceinline__ TileSel load_tile_sel(const ScoreArgs& a, int64_t m0, int n0,
+                                                 int tid) {
+  TileSel ts;
+  const int64_t w0 = n0 >> 5;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int e = tid + 512 * i;
+    const int64_t t = m0 + (e >> 3), w = w0 + (e & 7);
+    const bool ok = t < a.T && w < a.words;
+    ts.w[i] = ok ? a.sel_mask[t * a.words + w] : 0u;
+    ts.p[i] = ok ? a.sel_pre[t * a.words + w] : 0;
+  }
+  return ts;
+}
+
+__device__ __forceinline__ void act_mask_epilogue(const ScoreArgs& a, const f32x16 (&acc)[4][2],
+                                                  const TileSel& ts, unsigned char* smem,
+                                                  int64_t m0, int n0, int wm, int wn, int wid,
+                                                  int lane, int tid) {
+  uint32_t* lw = (uint32_t*)smem;                                   // [256][8]
+  int32_t* lp = (int32_t*)(smem + 8192);                            // [256][8]
+  float* R = (float*)(smem + 16384 + wid * (32 * kQRow * 4));       // [32][kQRow]
+  uint16_t* qe = (uint16_t*)(smem + 16384 + 8 * (32 * kQRow * 4) + wid * 4096);  // [2048]
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    lw[tid + 512 * i] = ts.w[i];
+    lp[tid + 512 * i] = ts.p[i];
+  }
+  __syncthreads();
+  const int nw = n0 + wn * 64;  // first column of this wave's region (ncols_out % 64 == 0)
+  if (nw >= a.ncols_out) return;
+  // wave-uniform bases of the region's rows in A and in the gate table; offsets from them fit
+  // in 32 bits (128 rows of at most 2^20 columns, or of hk <= 4096 gates)
+  const int64_t t0 = m0 + wm * 128;
+  uint16_t* const abase = a.aout + t0 * a.ncols_out + nw;
+  const float* const gbase = a.sel_gates + t0 * a.hk;
+  const int ldo = a.ncols_out, hk = a.hk;
+  {
+    const int nrows = a.T - t0 < 128 ? (int)(a.T - t0) : 128;
+    const uint4 z = make_uint4(0, 0, 0, 0);
+#pragma unroll 4
+    for (int rr = lane >> 3; rr < nrows; rr += 8) *(uint4*)(abase + rr * ldo + (lane & 7) * 8) = z;
+  }
+  bool cleared = false;  // the clearing stores have completed
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    // stage: lane (c, h) holds column j 32 + c, row 8 (q / 4) + 4 h + q % 4 in acc[i][j][q]
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int r = (q >> 2) * 8 + (lane >> 5) * 4 + (q & 3);
+        R[r * kQRow + j * 32 + (lane & 31)] = acc[i][j][q];
+      }
+    // this lane's word: row lane / 2 of the quarter, columns (lane % 2) 32 .. + 31
+    uint32_t w = lw[(wm * 128 + i * 32 + (lane >> 1)) * 8 + wn * 2 + (lane & 1)];
+    int total = 0;
+    for (uint64_t b = __ballot(w != 0u); b; b = __ballot(w != 0u)) {
+      if (w) {
+        const int pos = total + __builtin_amdgcn_mbcnt_hi((uint32_t)(b >> 32),
+                                                          __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0));
+        const int bit = __builtin_ctz(w);
+        w &= w - 1u;
+        qe[pos] = (uint16_t)(((lane >> 1) << 6) | ((lane & 1) * 32 + bit));
+      }
+      total += __popcll(b);
+    }
+    wave_lds_sync();
+    if (total > 0 && !cleared) {
+      wait_vm0();
+      cleared = true;
+    }
+    // Two entries per lane at a time; entries past total read the last entry again (unguarded
+    // loads stay in flight together) and store nothing.
+    for (int base = 0; base < total; base += 2 * kWave) {
+      float h[2], gt[2];
+      int o[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int k = base + u * kWave + lane < total ? base + u * kWave + lane : total - 1;
+        const int e = qe[k];
+        const int rq = e >> 6, cc = e & 63;
+        h[u] = R[rq * kQRow + cc];
+        const int rw = i * 32 + rq;  // row within the wave's region
+        const int wi = (wm * 128 + rw) * 8 + wn * 2 + (cc >> 5);
+        const int rank = lp[wi] + __popc(lw[wi] & ((1u << (cc & 31)) - 1u));
+        gt[u] = gbase[rw * hk + rank];
+        o[u] = rw * ldo + cc;
+      }
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+        if (base + u * kWave + lane < total)
+          abase[o[u]] = bf16_rne(gt[u] * activation(a.act, h[u]));
+    }
+    wave_lds_sync();
+  }
+}
+
+template <bool ACC, bool SPLIT = false, bool ADOT = false>
 __global__ __launch_bounds__(512, 1) void score_bf16_large_kernel(ScoreArgs a) {
   const int half = SPLIT ? 0 : blockIdx.z;
   const int ncols = a.H * a.nh[half];
-  const int n0 = blockIdx.x * LN;
-  if (n0 >= ncols) return;
-  const int64_t m0 = (int64_t)blockIdx.y * LM;
+  int tile_n = blockIdx.x, tile_m = blockIdx.y;
+  if constexpr (ADOT) {
+    // One-dimensional grid. Workgroup b runs on XCD b % 8; each XCD takes a contiguous range of
+    // tiles in column-major order, so the token-row tiles that share an expert tile run together
+    // on one XCD and that tile of U is fetched into its L2 once.
+    const int ntm = (int)((a.T + LM - 1) / LM);
+    const int total = ((a.ncols_out + LN - 1) / LN) * ntm;
+    const int per = (total + 7) / 8;
+    const int k = (int)(blockIdx.x % 8) * per + (int)(blockIdx.x / 8);
+    if (k >= total || (int)(blockIdx.x / 8) >= per) return;
+    tile_n = k / ntm;
+    tile_m = k - tile_n * ntm;
+  }
+  const int n0 = tile_n * LN;
+  if (n0 >= (ADOT ? a.ncols_out : ncols)) return;
+  const int64_t m0 = (int64_t)tile_m * LM;
   const int64_t kbase = SPLIT ? (int64_t)blockIdx.z * a.kchunk : 0;
   const uint16_t* X = (const uint16_t*)a.x + kbase;
   const uint16_t* Kt = (const uint16_t*)a.keys[half] + kbase;
@@ -246,6 +391,8 @@ __global__ __launch_bounds__(512, 1) void score_bf16_large_kernel(ScoreArgs a) {
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
 
   const int KT = (SPLIT ? a.kchunk : a.dk) / LK;
+  [[maybe_unused]] TileSel sel;
+  if constexpr (ADOT) sel = load_tile_sel(a, m0, n0, tid);
   issue(0, 0);
   wait_vm0();
   __syncthreads();
@@ -299,6 +446,10 @@ __global__ __launch_bounds__(512, 1) void score_bf16_large_kernel(ScoreArgs a) {
   // Only a tile that reaches past T checks rows, with one tile-wide branch; a per-element
   // check costs a divergent branch per store, which made the epilogue as long as a quarter
   // of the main loop.
+  if constexpr (ADOT) {
+    act_mask_epilogue(a, acc, sel, smem, m0, n0, wm, wn, wid, lane, tid);
+    return;
+  }
   const int64_t m_lane = m0 + wm * 128 + (lane >> 5) * 4;
   float* const obase = SPLIT ? out : a.out;
   auto store_all = [&](auto rows_ok) {
@@ -890,6 +1041,38 @@ hipError_t launch_gemm_splitk(int64_t M, int N, const void* A, int64_t lda, cons
   a.part_stride = M * (int64_t)N;
   dim3 grid((N + LN - 1) / LN, (unsigned)((M + LM - 1) / LM), splits);
   hipLaunchKernelGGL((score_bf16_large_kernel<false, true>), grid, dim3(512), 2 * LSTAGE, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_act_mask(int64_t T, int N, int ncols_out, const void* x, int d,
+                                const void* u, const uint32_t* sel_mask, const int32_t* sel_pre,
+                                int64_t words, const float* sel_gates, int hk, int act,
+                                uint16_t* aout, hipStream_t st) {
+  if (T == 0 || ncols_out == 0) return hipSuccess;
+  ScoreArgs a = {};
+  a.x = x;
+  a.keys[0] = u;
+  a.keys[1] = u;
+  a.out = nullptr;
+  a.T = T;
+  a.d = d;
+  a.dk = d;
+  a.H = 1;
+  a.nh[0] = N;
+  a.per_head = N;
+  a.ldo = N;
+  a.sel_mask = sel_mask;
+  a.sel_pre = sel_pre;
+  a.sel_gates = sel_gates;
+  a.aout = aout;
+  a.words = words;
+  a.ncols_out = ncols_out;
+  a.hk = hk;
+  a.act = act;
+  const int64_t total = (int64_t)((ncols_out + LN - 1) / LN) * ((T + LM - 1) / LM);
+  const int64_t grid = ((total + 7) / 8) * 8;
+  hipLaunchKernelGGL((score_bf16_large_kernel<false, false, true>), dim3((unsigned)grid),
+                     dim3(512), 2 * LSTAGE, st, a);
   return hipGetLastError();
 }
 

@@ -110,7 +110,9 @@ def test_workspace_sizes_cover_buffers():
     st, ex = _ws(dp, B.STAGE_EXPERT)
     assert st == OK and ex >= p.M * 4 + p.T * p.N * 2 + p.d * p.N * 2
     st, lay = _ws(dp, B.STAGE_LAYER)
-    assert st == OK and lay >= ex
+    # the layer's dense first product adds each token's selection mask and prefix counts
+    # ([T, N / 32] each) and its gates in expert-id order
+    assert st == OK and lay >= ex + 2 * p.T * (p.N // 32) * 4 + p.M * 4
     dp.K = 1024  # below N / 64: the slot-order sum, no dense buffers
     st, ex2 = _ws(dp, B.STAGE_EXPERT)
     assert st == OK and ex2 < p.T * p.N * 2
@@ -241,9 +243,10 @@ def test_layer_path_flags():
     assert f["dp8share_bf16"] == B.PATH_SELECT_DOT and f["small_bf16"] == B.PATH_SELECT_DOT
     assert f["tiny_f32"] == 0  # fp32: no fused selection
     assert f["paper_k512_bf16"] == B.PATH_SCHEDULE
-    assert f["paper_k4096_bf16"] == B.PATH_SCHEDULE | B.PATH_DENSE_SUM
+    # one head with K >= N / 64 and groups of one expert: both products dense over all experts
+    assert f["paper_k4096_bf16"] == B.PATH_DENSE_SUM | B.PATH_DENSE_DOT
     grouped = B.make_desc(synth.WORKLOADS["paper_k4096_bf16"].with_(group_size=64))
-    assert P.omnimoe_layer_path(grouped) & B.PATH_GROUPED
+    assert P.omnimoe_layer_path(grouped) == B.PATH_SCHEDULE | B.PATH_GROUPED | B.PATH_DENSE_SUM
     bad = B.make_desc(synth.WORKLOADS["small_bf16"])
     bad.K = 0
     with pytest.raises(P.OmnimoeError):

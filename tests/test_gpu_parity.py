@@ -91,6 +91,10 @@ SHAPES = {
                                  K=64),
     "dense_k100_bf16": synth.Workload("dense_k100_bf16", T=77, d=192, n_rows=40, n_cols=50,
                                       d_key=64, H=1, K=100),
+    # several row and column tiles of the dense first product (42 tiles over 8 XCDs), N and d
+    # not multiples of 256, the expert dimension padded to the split width (3584 > 3360)
+    "dense_wide_bf16": synth.Workload("dense_wide_bf16", T=700, d=320, n_rows=56, n_cols=60,
+                                      d_key=64, H=1, K=64),
     # groups of 64 experts with about twelve slot tiles each: the grouped GEMM's tiles are
     # shared out to the XCDs by token range
     "bucket_bf16": synth.Workload("bucket_bf16", T=3000, d=128, n_rows=64, n_cols=64, d_key=64,
@@ -564,6 +568,46 @@ def test_expert_forward_group_rows_rejects_fp32():
     assert "unsupported" in str(ei.value)
 
 
+@pytest.mark.parametrize("name", ["dense_bf16", "dense_k100_bf16", "dense_wide_bf16"])
+def test_dense_expert_dot_layer(name):
+    # One head with K >= N / 64 and groups of one expert: the layer forms the a_p inside one dense
+    # product x U^T over all experts (gate and activation kept at the selected cells only) and
+    # sums y = A V densely, with no schedule. The same bits on a second run, and on the layer's
+    # own routing within an element-wise bound of the token-centric stage (a in fp32, slot-order
+    # sums): A holds each a_p rounded to bf16 once (2^-9 |a|); the x . u sums run in another
+    # order (at most 2 d 2^-24 ||x|| ||u|| apart, times |act'| <= 1.13); the two y sums (H K
+    # terms, plus the split partials) each within gamma_n of the exact one.
+    w = SHAPES[name]
+    d = B.make_desc(w)
+    assert P.omnimoe_layer_path(d) == B.PATH_DENSE_SUM | B.PATH_DENSE_DOT
+    assert not P.omnimoe_layer_path(B.make_desc(w.with_(group_size=4))) & B.PATH_DENSE_DOT
+    say(f"[dense expert dot, layer] {name}")
+    inp, f = host_inputs(w)
+    dev = upload(inp)
+    y, idx, g = gpu_layer(w, dev)
+    y2, idx2, g2 = gpu_layer(w, dev)
+    assert np.array_equal(y.view(np.uint8), y2.view(np.uint8)) and np.array_equal(idx, idx2)
+    y_tc = torch.empty((w.T, w.d), dtype=torch.float32, device="cuda")
+    P.omnimoe_expert_forward_token_centric(d, dev["x"], dev["u"], dev["v"], to_dev(idx),
+                                           to_dev(g), y_tc)
+    torch.cuda.synchronize()
+    y_tc = y_tc.cpu().numpy().astype(np.float64)
+    xn = np.linalg.norm(f["x"].astype(np.float64), axis=1)
+    un = np.linalg.norm(f["u"].astype(np.float64), axis=1)
+    va = np.abs(f["v"].astype(np.float64))
+    flat = idx.reshape(w.T, -1)
+    a = g.reshape(w.T, -1).astype(np.float64) * xn[:, None] * un[flat]
+    mass = np.zeros((w.T, w.d))
+    for j in range(flat.shape[1]):
+        mass += a[:, j:j + 1] * va[flat[:, j]]
+    n = flat.shape[1] + 520
+    bound = mass * (2.0 ** -8 + (2.3 * w.d + 2 * n) * 2.0 ** -24) + 1e-30
+    gap = np.abs(y.astype(np.float64) - y_tc)
+    say(f"  max gap / bound {(gap / bound).max():.3e}; max row rel err "
+        f"{row_rel_err(y, y_tc).max():.3e}")
+    assert np.all(gap <= bound)
+
+
 @pytest.mark.parametrize("grouped", [False, True])
 def test_dense_routed_sum_repeated_ids(grouped):
     # Caller-supplied idx may name one expert in several slots of a token (the router never
@@ -702,7 +746,7 @@ def test_layer_is_deterministic():
 
 
 @pytest.mark.parametrize("name", ["small_bf16", "decode64_like_bf16", "grouped_b64_bf16",
-                                  "grouped_k256_b100_bf16"])
+                                  "grouped_k256_b100_bf16", "dense_wide_bf16"])
 def test_layer_graph_replays_match_eager(name):
     # The layer call allocates nothing and clears with kernels only, so it can be captured in a
     # HIP graph; every replay (with other eager work and synchronisations in between) must
@@ -711,7 +755,9 @@ def test_layer_graph_replays_match_eager(name):
          "decode64_like_bf16": SHAPES["skinny_bf16"].with_(T=64),
          # groups of B > 1: the grouped GEMM, its plan and the group sort inside the graph
          "grouped_b64_bf16": W["small_bf16"].with_(group_size=64),
-         "grouped_k256_b100_bf16": SHAPES["k256_bf16"].with_(group_size=100)}[name]
+         "grouped_k256_b100_bf16": SHAPES["k256_bf16"].with_(group_size=100),
+         # both products dense over all experts (selection mask, masked-activation GEMM)
+         "dense_wide_bf16": SHAPES["dense_wide_bf16"]}[name]
     inp, _ = host_inputs(w)
     dev = upload(inp)
     y_ref, idx_ref, g_ref = gpu_layer(w, dev)
