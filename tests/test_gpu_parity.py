@@ -95,6 +95,12 @@ SHAPES = {
     # not multiples of 256, the expert dimension padded to the split width (3584 > 3360)
     "dense_wide_bf16": synth.Workload("dense_wide_bf16", T=700, d=320, n_rows=56, n_cols=60,
                                       d_key=64, H=1, K=64),
+    # every expert selected by every token (K = N): the epilogue's queues hold all 2048 cells of
+    # each quarter; SiLU in the masked-activation epilogue, shared query
+    "dense_all_bf16": synth.Workload("dense_all_bf16", T=300, d=128, n_rows=8, n_cols=8, d_key=64,
+                                     H=1, K=64),
+    "dense_silu_bf16": synth.Workload("dense_silu_bf16", T=260, d=192, n_rows=24, n_cols=40,
+                                      d_key=64, H=1, K=40, act="silu", query_mode="shared"),
     # groups of 64 experts with about twelve slot tiles each: the grouped GEMM's tiles are
     # shared out to the XCDs by token range
     "bucket_bf16": synth.Workload("bucket_bf16", T=3000, d=128, n_rows=64, n_cols=64, d_key=64,
@@ -568,7 +574,8 @@ def test_expert_forward_group_rows_rejects_fp32():
     assert "unsupported" in str(ei.value)
 
 
-@pytest.mark.parametrize("name", ["dense_bf16", "dense_k100_bf16", "dense_wide_bf16"])
+@pytest.mark.parametrize("name", ["dense_bf16", "dense_k100_bf16", "dense_wide_bf16",
+                                  "dense_all_bf16", "dense_silu_bf16"])
 def test_dense_expert_dot_layer(name):
     # One head with K >= N / 64 and groups of one expert: the layer forms the a_p inside one dense
     # product x U^T over all experts (gate and activation kept at the selected cells only) and
