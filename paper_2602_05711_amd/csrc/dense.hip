@@ -159,9 +159,12 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restr
 // Selection of one token as a bitmask over expert ids (bit e % 32 of word e / 32), the number
 // of selected experts in the words before each word, and the gates in expert-id order:
 // gsorted[t, r] = gate of the selected expert of rank r. One workgroup per token; the mask and
-// the prefix counts are built in LDS (bits set with LDS atomic ORs, which commute). The layer's
-// ids come from the selection kernel and are distinct within a token.
-constexpr int kMaskWordsMax = 9216;  // a token's words held in LDS (N up to 294912 experts)
+// the prefix counts are built in LDS (bits set with LDS atomic ORs, which commute), sized per
+// launch (words x 6 bytes: the counts fit in 16 bits, hk <= 4096) so that several tokens share a
+// compute unit. The layer's ids come from the selection kernel and are distinct within a token.
+constexpr int kMaskWordsMax = 9216;  // words of one token (N up to 294912 experts)
+
+size_t select_mask_lds_bytes(int words) { return (size_t)words * 6 + 16; }
 
 __global__ __launch_bounds__(256) void select_mask_kernel(const int32_t* __restrict__ idx,
                                                           const float* __restrict__ gates,
@@ -169,11 +172,12 @@ __global__ __launch_bounds__(256) void select_mask_kernel(const int32_t* __restr
                                                           int32_t* __restrict__ pre,
                                                           float* __restrict__ gsorted, int hk,
                                                           int64_t N, int words) {
-  __shared__ uint32_t lm[kMaskWordsMax];
-  __shared__ int32_t lpre[kMaskWordsMax];
-  __shared__ int32_t part[256];
+  extern __shared__ __attribute__((aligned(16))) unsigned char sm[];
+  uint32_t* lm = (uint32_t*)sm;                 // [words]
+  uint16_t* lpre = (uint16_t*)(sm + words * 4);  // [words]
+  __shared__ int wtot[4];
   const int64_t t = blockIdx.x;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   // the token's slots, kDenseSlots per thread, all loads in flight at once (a slot past hk reads
   // the last slot and is dropped)
   int e[kDenseSlots];
@@ -192,24 +196,20 @@ __global__ __launch_bounds__(256) void select_mask_kernel(const int32_t* __restr
     if (e[q] >= 0) atomicOr(&lm[e[q] >> 5], 1u << (e[q] & 31));
   }
   __syncthreads();
-  // exclusive prefix of the words' popcounts: thread tid sums a contiguous run of words, the
-  // 256 run sums are scanned in LDS, then each run is walked again
+  // exclusive prefix of the words' popcounts: thread tid sums a contiguous run of words, the run
+  // sums are scanned within each wave and then across the four waves, and each run is walked again
   const int per = (words + 255) / 256;
   const int w_lo = tid * per < words ? tid * per : words;
   const int w_hi = w_lo + per < words ? w_lo + per : words;
   int run = 0;
   for (int w = w_lo; w < w_hi; ++w) run += __popc(lm[w]);
-  part[tid] = run;
+  const int excl = wave_excl_scan_i32(run);
+  if (lane == kWave - 1) wtot[wv] = excl + run;
   __syncthreads();
-  for (int off = 1; off < 256; off <<= 1) {
-    const int v = tid >= off ? part[tid - off] : 0;
-    __syncthreads();
-    part[tid] += v;
-    __syncthreads();
-  }
-  int c = part[tid] - run;
+  int c = excl;
+  for (int v = 0; v < wv; ++v) c += wtot[v];
   for (int w = w_lo; w < w_hi; ++w) {
-    lpre[w] = c;
+    lpre[w] = (uint16_t)c;
     c += __popc(lm[w]);
   }
   __syncthreads();
@@ -340,8 +340,9 @@ hipError_t launch_select_mask(const Shape& s, const int32_t* idx, const float* g
                               hipStream_t st) {
   if (s.T == 0) return hipSuccess;
   const MaskBufs b = mask_bufs(s, ws);
-  hipLaunchKernelGGL(select_mask_kernel, dim3((unsigned)s.T), dim3(256), 0, st, idx, gates,
-                     b.mask, b.pre, b.gsorted, s.hk, s.N, (int)b.words);
+  hipLaunchKernelGGL(select_mask_kernel, dim3((unsigned)s.T), dim3(256),
+                     select_mask_lds_bytes((int)b.words), st, idx, gates, b.mask, b.pre, b.gsorted,
+                     s.hk, s.N, (int)b.words);
   return hipGetLastError();
 }
 
