@@ -2,7 +2,9 @@
 // token's query slice x[:, c0:c0+d_key] and Keys stacks the H heads' sub-key tables
 // ([H * n_half, d_key]). Both operands are contiguous along d_key, so MFMA fragments load
 // straight from row-major memory. The same kernels serve the dense router of the ablation
-// (one half of N gating vectors) and the shared MLP's projections (accumulating into y).
+// (one half of N gating vectors), the shared MLP's projections (accumulating into y), the split-K
+// second product of Eq. 14 over all experts and, with a masked-activation epilogue, its first
+// product (x . u for every (token, expert) pair, g * act kept at the selected pairs only).
 //
 // bf16, d_key % 64 == 0: 256 x 256 tile, eight waves of 128 x 64 on v_mfma_f32_32x32x16_bf16,
 //   operands copied global -> LDS without registers (two 64 KiB stages, XOR-swizzled rows);
