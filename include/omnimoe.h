@@ -309,7 +309,10 @@ omnimoe_status omnimoe_route_backward(const omnimoe_layer_desc* desc, const void
  * per two experts; or a u table N*d of at most 128 MiB, which stays in the GPU's last-level
  * cache), no schedule is formed: the same a_p are computed in slot order, with identical
  * results (by the selection kernel itself when there are at least 256 (token, head) rows;
- * omnimoe_layer_path tells which kernels run). Workspace:
+ * omnimoe_layer_path tells which kernels run). With one head, K >= N / 64 and group_size 1,
+ * both products run dense over all experts (Eq. 14 with a single group): x . u for every
+ * (token, expert) pair, gate and activation kept at the selected pairs (a_p rounded to bf16),
+ * then y = A V; no schedule is formed. Workspace:
  * OMNIMOE_STAGE_LAYER bytes
  * (caller-owned device memory, contents need not be initialised; OMNIMOE_ERR_WORKSPACE when
  * short). */
